@@ -1,0 +1,138 @@
+"""Pure-Python brute force for tiny inputs.  TEST INFRASTRUCTURE ONLY.
+
+An independent second route to the same definitions as ``lookme_oracle``:
+plain loops over Python numbers, repeated maximum extraction instead of
+sorting, exact rational arithmetic (``fractions.Fraction``) for sums, and an
+exact rational round-to-nearest-even to bfloat16 / binary32.  It pins the
+oracle; it is far too slow for anything but a few dozen tokens.
+
+Paper: arXiv 2607.16305, Sec. 3.2 (Eq. 4-7) and Sec. 3.3 (Eq. 9-10).
+"""
+
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+
+def round_fraction(v: Fraction, mant_bits: int, emin: int = -126) -> Fraction:
+    """Exact round-to-nearest-even of a rational to a binary format with
+    ``mant_bits`` significand bits (hidden bit included) and minimum normal
+    exponent ``emin``.  Overflow is not handled (inputs here are small)."""
+    if v == 0:
+        return Fraction(0)
+    sign = -1 if v < 0 else 1
+    a = abs(v)
+    # find e with 2^e <= a < 2^(e+1)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    e = max(e, emin)
+    quantum = Fraction(2) ** (e - (mant_bits - 1))
+    m = a / quantum
+    fl = m.numerator // m.denominator
+    rem = m - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    return sign * fl * quantum
+
+
+def round_bf16(v: Fraction) -> Fraction:
+    return round_fraction(v, 8)
+
+
+def round_f32(v: Fraction) -> Fraction:
+    return round_fraction(v, 24)
+
+
+def dot(a, b) -> Fraction:
+    s = Fraction(0)
+    for x, y in zip(a, b):
+        s += Fraction(x) * Fraction(y)
+    return s
+
+
+def matvec_rows(x_rows, w_rows):
+    """[(x . w_j) for each output row j] for every token row."""
+    return [[dot(xr, wr) for wr in w_rows] for xr in x_rows]
+
+
+def argmax_lowest(vals) -> int:
+    best = 0
+    for i in range(1, len(vals)):
+        if vals[i] > vals[best]:
+            best = i
+    return best
+
+
+def topk_by_extraction(vals, k):
+    """k largest by repeated extraction of the maximum (lowest index wins an
+    exact tie), in extraction order."""
+    taken = []
+    used = [False] * len(vals)
+    for _ in range(k):
+        best = -1
+        for i, v in enumerate(vals):
+            if used[i]:
+                continue
+            if best < 0 or v > vals[best]:
+                best = i
+        used[best] = True
+        taken.append(best)
+    return taken
+
+
+def project(x_rows, w_t_rows, rounder):
+    """q = round(x W) with W given output-row-major (w_t_rows[j] = column j)."""
+    return [[rounder(v) for v in row] for row in matvec_rows(x_rows, w_t_rows)]
+
+
+def route(q_rows, scene_keys, bias=None):
+    out = []
+    for q in q_rows:
+        s = [dot(q, key) + (Fraction(bias[j]) if bias is not None else 0)
+             for j, key in enumerate(scene_keys)]
+        out.append(argmax_lowest(s))
+    return out
+
+
+def lookup_flat_sim(q_rows, scenes, flat_keys, P, k):
+    """Two-level result via a one-level similarity search restricted to the
+    chosen scene's rows [s*P, (s+1)*P) of the flat key table (the 1-L(sim)
+    baseline of the paper restricted to one scene).  Returns (prim, scores)
+    with prim relative to the scene."""
+    prim, top = [], []
+    for q, s in zip(q_rows, scenes):
+        scores = [dot(q, flat_keys[s * P + p]) for p in range(P)]
+        idx = topk_by_extraction(scores, k)
+        prim.append(idx)
+        top.append([scores[i] for i in idx])
+    return prim, top
+
+
+def softmax(vals):
+    m = max(vals)
+    e = [math.exp(float(v - m)) for v in vals]
+    s = math.fsum(e)
+    return [x / s for x in e]
+
+
+def select(norm_sq, n_keep):
+    """Top n_keep by criticality via repeated extraction (ties lowest index),
+    reported ascending.  Comparing squared norms orders exactly like norms."""
+    return sorted(topk_by_extraction(norm_sq, n_keep))
+
+
+def inject(hidden_rows, value_rows, P, scenes, prim, w, kept, rounder):
+    """Exact rational sum of the weighted rows plus H, rounded once."""
+    out = [list(map(Fraction, r)) for r in hidden_rows]
+    d_v = len(value_rows[0])
+    for t in kept:
+        for j in range(d_v):
+            acc = Fraction(hidden_rows[t][j])
+            for i, p in enumerate(prim[t]):
+                acc += Fraction(w[t][i]) * Fraction(value_rows[scenes[t] * P + p][j])
+            out[t][j] = rounder(acc)
+    return out

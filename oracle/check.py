@@ -1,0 +1,291 @@
+"""Tie- and rounding-aware comparison of library outputs with the oracle.
+TEST INFRASTRUCTURE ONLY (used by the tests, the smoke check and the
+benchmark's CPU leg; never by the library).
+
+Every comparison recomputes the oracle's view with ``lookme_oracle`` on the
+inputs the library saw for that stage (stage-wise checking): the scene is
+checked on the library's q, the primitives under the library's scene, the
+injected rows with the library's (kept, scene, prim).  Index results must be
+identical except where the oracle's own float64 scores of the competing
+choices tie within
+
+    |a - b| <= 1e-5 * max(|a|, |b|) + 1e-7 * ||q_t||_2
+
+(the relative part is the stated acceptance rule; the small absolute floor is
+the size of a float32 summation error for scores near zero).  Each such
+exemption is counted; more than 1% of decisions of one kind exempted fails the
+check, so a systematic error cannot hide inside the tolerance.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+
+from . import lookme_oracle as O
+
+REL_TIE = 1e-5
+ABS_TIE_PER_QNORM = 1e-7
+MAX_EXEMPT_FRACTION = 0.01
+
+
+@dataclasses.dataclass
+class Report:
+    decisions: dict = dataclasses.field(default_factory=dict)
+    exemptions: dict = dataclasses.field(default_factory=dict)
+    failures: list = dataclasses.field(default_factory=list)
+
+    def count(self, kind: str, n: int = 1):
+        self.decisions[kind] = self.decisions.get(kind, 0) + n
+
+    def exempt(self, kind: str, n: int = 1):
+        self.exemptions[kind] = self.exemptions.get(kind, 0) + n
+
+    def fail(self, msg: str):
+        if len(self.failures) < 50:
+            self.failures.append(msg)
+
+    def finish(self) -> "Report":
+        for kind, n in self.decisions.items():
+            e = self.exemptions.get(kind, 0)
+            if n > 0 and e > max(1, MAX_EXEMPT_FRACTION * n):
+                self.fail(f"{kind}: {e} tie exemptions out of {n} decisions (> 1%)")
+        return self
+
+    @property
+    def ok(self) -> bool:
+        return not self.failures
+
+    def __str__(self):
+        return (f"decisions={self.decisions} exemptions={self.exemptions} "
+                f"failures={self.failures[:10]}")
+
+
+def tie(a: float, b: float, qnorm: float = 0.0) -> bool:
+    return abs(a - b) <= REL_TIE * max(abs(a), abs(b)) + ABS_TIE_PER_QNORM * qnorm
+
+
+# ---------------------------------------------------------------------------
+# Rounding distance in units in the last place
+# ---------------------------------------------------------------------------
+
+def _mono_bf16(bits: np.ndarray) -> np.ndarray:
+    b = np.asarray(bits).astype(np.int64) & 0xFFFF
+    mag = b & 0x7FFF
+    return np.where(b >> 15 == 1, -mag, mag)
+
+
+def _mono_f32(x: np.ndarray) -> np.ndarray:
+    b = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.int64)
+    mag = b & 0x7FFFFFFF
+    return np.where(b >> 31 == 1, -mag, mag)
+
+
+def ulp_distance(a: np.ndarray, b: np.ndarray, dtype: str) -> np.ndarray:
+    """Distance in representable steps between stored values (bf16 bit
+    patterns or float32 arrays)."""
+    if dtype == "bf16":
+        return np.abs(_mono_bf16(a) - _mono_bf16(b))
+    return np.abs(_mono_f32(a) - _mono_f32(b))
+
+
+# ---------------------------------------------------------------------------
+# Stage checks
+# ---------------------------------------------------------------------------
+
+def check_q(q_lib, q_orc, dtype: str, rep: Report, max_ulp: int = 1):
+    """C1: every element of the library's q within ``max_ulp`` of the
+    oracle's correctly rounded q."""
+    d = ulp_distance(q_lib, q_orc, dtype)
+    rep.count("q", d.size)
+    bad = int(np.sum(d > max_ulp))
+    if bad:
+        i = np.unravel_index(int(np.argmax(d)), d.shape)
+        rep.fail(f"q: {bad} elements beyond {max_ulp} ulp (worst {int(d[i])} at {i})")
+    return d
+
+
+def check_scene(q: np.ndarray, scene_keys: np.ndarray, bias, score: str,
+                scene_lib: np.ndarray, rep: Report, tokens=None):
+    """C2: the library's scene is the oracle's arg max, or ties with it."""
+    tokens = np.arange(q.shape[0]) if tokens is None else np.asarray(tokens)
+    s1 = O.scene_scores(q[tokens], scene_keys, bias, score)
+    best = np.argmax(s1, axis=1)
+    for r, t in enumerate(tokens):
+        g = int(scene_lib[t])
+        rep.count("scene")
+        if g < 0 or g >= scene_keys.shape[0]:
+            rep.fail(f"scene[{t}]={g} out of range")
+            continue
+        b = int(best[r])
+        if g == b:
+            continue
+        qn = float(np.linalg.norm(q[t]))
+        if tie(s1[r, g], s1[r, b], qn):
+            rep.exempt("scene")
+        else:
+            rep.fail(f"scene[{t}]: library {g} score {s1[r, g]!r}, oracle {b} score {s1[r, b]!r}")
+
+
+def check_prim(q: np.ndarray, scene: np.ndarray, scene_prim_keys, k: int, score: str,
+               prim_lib: np.ndarray, w_lib: np.ndarray, rep: Report, tokens=None,
+               w_tol: float = 1e-5):
+    """C3 + C4: the library's k primitives under the library's scene.
+
+    ``scene_prim_keys(s)`` returns the float64 [P, d_e] keys of scene s.
+    The set must equal the oracle's top-k except for swaps among scores tied
+    with the k-th; the listed order must be score-descending (exact ties by
+    ascending p); the weights must equal the softmax of the oracle's scores of
+    the library's set within ``w_tol``.  Returns the oracle weights of the
+    library's set, [len(tokens), k].
+    """
+    tokens = np.arange(q.shape[0]) if tokens is None else np.asarray(tokens)
+    w_orc = np.zeros((len(tokens), k))
+    cache = {}
+    for r, t in enumerate(tokens):
+        s = int(scene[t])
+        if s not in cache:
+            if len(cache) > 64:
+                cache.clear()
+            cache[s] = scene_prim_keys(s)
+        keys = cache[s]
+        P = keys.shape[0]
+        s2 = O.primitive_scores(q[t], keys, score)
+        qn = float(np.linalg.norm(q[t]))
+        g = np.asarray(prim_lib[t], dtype=np.int64)
+        rep.count("prim")
+        if np.any(g < 0) or np.any(g >= P) or len(set(g.tolist())) != k:
+            rep.fail(f"prim[{t}]={g.tolist()} invalid (P={P})")
+            continue
+        ref = O.topk_order(s2, k)
+        kth = s2[ref[-1]]
+        gs = s2[g]
+        exempt = False
+        # every listed element must reach the k-th score (up to a tie)
+        for p, v in zip(g, gs):
+            if v < kth and not tie(v, kth, qn):
+                rep.fail(f"prim[{t}]: p={p} score {v!r} below k-th {kth!r}")
+                exempt = None
+                break
+            if v < kth:
+                exempt = True
+        if exempt is None:
+            continue
+        # every element strictly above the k-th score must be listed
+        gset = set(g.tolist())
+        for p in ref:
+            if int(p) not in gset:
+                if not tie(s2[p], kth, qn):
+                    rep.fail(f"prim[{t}]: missing p={p} score {s2[p]!r} (k-th {kth!r})")
+                    exempt = None
+                    break
+                exempt = True
+        if exempt is None:
+            continue
+        # order: descending score, exact ties ascending p
+        for i in range(k - 1):
+            a, b = gs[i], gs[i + 1]
+            if a < b and not tie(a, b, qn):
+                rep.fail(f"prim[{t}]: order {g.tolist()} not descending")
+                break
+            if a == b and g[i] > g[i + 1]:
+                rep.fail(f"prim[{t}]: equal scores not in ascending p order")
+                break
+        if exempt:
+            rep.exempt("prim")
+        wo = O.softmax_weights(gs)
+        w_orc[r] = wo
+        rep.count("w", k)
+        dw = np.max(np.abs(np.asarray(w_lib[t], dtype=np.float64) - wo))
+        if not dw <= w_tol:
+            rep.fail(f"w[{t}]: max |dw| = {dw:.3g} > {w_tol}")
+    return w_orc
+
+
+def check_kept(c: np.ndarray, n_keep: int, kept_lib: np.ndarray, rep: Report):
+    """C5: the kept set equals the oracle's except for swaps among
+    criticalities tied with the n_keep-th; ascending, unique, in range."""
+    n = c.shape[0]
+    kept_lib = np.asarray(kept_lib, dtype=np.int64)
+    rep.count("kept", max(1, n_keep))
+    if kept_lib.shape[0] != n_keep:
+        rep.fail(f"kept: {kept_lib.shape[0]} entries, expected {n_keep}")
+        return
+    if n_keep == 0:
+        return
+    if np.any(kept_lib < 0) or np.any(kept_lib >= n):
+        rep.fail("kept: token index out of range")
+        return
+    if np.any(np.diff(kept_lib) <= 0):
+        rep.fail("kept: not strictly ascending")
+        return
+    ref = O.select(c, n_keep)
+    if np.array_equal(ref, kept_lib):
+        return
+    cut = np.sort(c)[::-1][n_keep - 1]
+    swaps = 0
+    for t in np.setdiff1d(kept_lib, ref):
+        if not tie(c[t], cut):
+            rep.fail(f"kept: token {t} (c={c[t]!r}) kept below the cut {cut!r}")
+            return
+        swaps += 1
+    for t in np.setdiff1d(ref, kept_lib):
+        if not tie(c[t], cut):
+            rep.fail(f"kept: token {t} (c={c[t]!r}) above the cut {cut!r} missing")
+            return
+    rep.exempt("kept", swaps)
+
+
+def check_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: int,
+                 scene: np.ndarray, prim: np.ndarray, w_orc_of, kept: np.ndarray,
+                 rep: Report, tokens=None, contract_abs: float = 2e-2):
+    """C6: recompute the injection with the library's (kept, scene, prim) and
+    the oracle's weights.  Untouched elements must be bit-identical; touched
+    bf16 elements within ``contract_abs`` and 1 ulp of the correctly rounded
+    oracle value; float32 within 1e-5 * (|H| + sum w |V|).
+
+    h_in, h_out_lib : stored arrays [n, d_h] (bf16 bits or float32), or the
+                      rows for ``tokens`` when given.
+    values_rows(rows) -> float64 [len(rows), d_v]
+    w_orc_of(t) -> float64 [k] oracle weights of the library's set for t.
+    """
+    n = h_in.shape[0]
+    tokens = np.arange(n) if tokens is None else np.asarray(tokens)
+    kept_set = set(np.asarray(kept).tolist())
+    h_in_f = O.to_f64(h_in, dtype)
+    h_lib_f = O.to_f64(h_out_lib, dtype)
+    worst = 0.0
+    for r, t in enumerate(tokens):
+        rep.count("hidden_row")
+        if int(t) not in kept_set:
+            same = (np.array_equal(np.asarray(h_in[r]).view(np.uint8),
+                                   np.asarray(h_out_lib[r]).view(np.uint8)))
+            if not same:
+                rep.fail(f"hidden: untouched row {t} modified")
+            continue
+        rows = int(scene[t]) * P + np.asarray(prim[t], dtype=np.int64)
+        V = values_rows(rows)
+        d_v = V.shape[1]
+        w = w_orc_of(int(t))
+        exact = h_in_f[r, :d_v] + np.sum(w[:, None] * V, axis=0)
+        ref = O.round_to_dtype(exact, dtype)
+        got = h_lib_f[r, :d_v]
+        if not np.array_equal(np.asarray(h_in[r, d_v:]).view(np.uint8),
+                              np.asarray(h_out_lib[r, d_v:]).view(np.uint8)):
+            rep.fail(f"hidden: row {t} columns >= d_v modified")
+        if dtype == "bf16":
+            err = float(np.max(np.abs(got - ref)))
+            worst = max(worst, err)
+            ulp = ulp_distance(O.from_f64(got, "bf16"), O.from_f64(ref, "bf16"), "bf16")
+            if err > contract_abs:
+                rep.fail(f"hidden[{t}]: max-abs {err:.3g} > {contract_abs}")
+            elif np.any(ulp > 1):
+                rep.fail(f"hidden[{t}]: {int(np.sum(ulp > 1))} elements beyond 1 ulp")
+        else:
+            bound = 1e-5 * (np.abs(h_in_f[r, :d_v]) + np.sum(np.abs(w[:, None] * V), axis=0))
+            err = np.abs(got - exact)
+            worst = max(worst, float(np.max(err)))
+            if np.any(err > bound + 1e-30):
+                rep.fail(f"hidden[{t}]: float32 error beyond 1e-5 relative")
+    return worst

@@ -1,0 +1,287 @@
+"""Plain fp64 CPU oracle for the LookME image-pathway hot path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import this
+module: only the tests, the smoke check and the benchmark's CPU-baseline leg
+use it.  It shares no code with the HIP library (no kernels, no headers, no
+helpers); it receives the same input bytes and recomputes every result from
+the paper's definitions, slowly and obviously.
+
+Paper: "LookME: Lookup-Based Multimodal Embeddings for Layer Injection in
+Vision-Language Models" (arXiv 2607.16305).
+
+What is computed, step by step (each function cites its passage):
+
+  project     Sec. 3.2 "Level-1: scene retrieval": v_e = v W_{v->e}
+  route       Sec. 3.2 Level-1, Eq. 5: scene = argmax(score(v_e, e_img) + b)
+  lookup      Sec. 3.2 Level-2, Eq. 6-7 in the configured form: top-k
+              primitives of the chosen scene by dot score against per-row
+              primitive keys, softmax weights over the k selected scores
+  criticality Sec. 3.3 "Intra-Layer Sparse Activation", Eq. 9: the gate is
+              driven by the size of Delta_i, the attention update
+  select      Eq. 10: the pathway runs only at the gated positions; the
+              configured gate keeps the n_keep positions of largest
+              ||Delta_i||_2
+  inject      Eq. 10 and Eq. 2: H_out = H + S(R_img) at the kept positions,
+              S(R)[i] = sum_p w_p * E[scene_i, p, :]
+  run         all of the above for L layers that share one table (Sec. 3.3,
+              "Inter-Layer Sparse Activation": neighbouring layers retrieve
+              similar primitives, so one table serves several layers)
+
+Readings of the paper taken here (the paper is silent or differs from the
+configured workloads; each is listed in the design notes of the repository):
+  * Scores are dot products (the configured workloads); ``score="cos"``
+    gives the cosine of Eq. 5 / Eq. 7 (both vectors normalised).
+  * Level-2 candidates are scored against primitive keys K2[s, p, :], one key
+    per table row; table rows V[s*P + p, :] are the values that are summed.
+  * Softmax over the k selected scores, temperature 1, max subtracted.
+  * Exact ties go to the lowest index (scene, primitive, token).
+  * q is quantised once to the storage dtype (bf16 or fp32) with
+    round-to-nearest-even from the exact product; later stages use that q.
+  * The injected increment is added into the first d_v columns of H; the
+    result is rounded once to the storage dtype.
+
+Inputs are numpy arrays.  bf16 tensors are passed as their raw uint16 bit
+patterns (numpy has no bf16) together with ``dtype="bf16"``; fp32 tensors as
+float32 arrays with ``dtype="f32"``.  All arithmetic is float64.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+# ---------------------------------------------------------------------------
+# Number formats (IEEE-754 binary32 and bfloat16: 1 sign, 8 exponent bits,
+# 7 stored fraction bits).  These are written out here from the format
+# definitions; the oracle does not use any GPU-side conversion routine.
+# ---------------------------------------------------------------------------
+
+_BF16_MANT_BITS = 8          # significand precision including the hidden bit
+_BF16_EMIN = -126            # smallest normal exponent (same as binary32)
+_BF16_EMAX = 127
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact value of bfloat16 numbers given as uint16 bit patterns."""
+    b = np.asarray(bits).astype(np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bfloat16 (ties to even), directly
+    from the exact float64 value (no intermediate binary32 rounding).
+
+    Returns float64 values that are exactly representable in bfloat16.
+    Values beyond the largest finite bfloat16 after rounding become +-inf.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros_like(x)
+    nz = (x != 0) & np.isfinite(x)
+    ax = np.abs(x[nz])
+    # exponent e with 2^e <= |x| < 2^(e+1)
+    _, e2 = np.frexp(ax)            # ax = m * 2^e2, 0.5 <= m < 1
+    e = e2 - 1
+    e = np.maximum(e, _BF16_EMIN)   # subnormal range keeps the fixed quantum
+    quantum_exp = e - (_BF16_MANT_BITS - 1)
+    scaled = np.ldexp(ax, -quantum_exp)          # exact (power-of-two scale)
+    r = np.ldexp(np.rint(scaled), quantum_exp)  # rint: half to even
+    max_finite = np.ldexp(np.float64(2 ** _BF16_MANT_BITS - 1),
+                          _BF16_EMAX - (_BF16_MANT_BITS - 1))
+    r = np.where(r > max_finite, np.inf, r)
+    out[nz] = np.sign(x[nz]) * r
+    out[~np.isfinite(x)] = x[~np.isfinite(x)]
+    return out
+
+
+def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Bit patterns of float64 values that are already bfloat16 values."""
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    return (f.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def round_to_dtype(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round float64 values once to the storage dtype; returns float64."""
+    if dtype == "bf16":
+        return round_to_bf16(x)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def to_f64(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact float64 value of a stored tensor (bf16 bits or float32)."""
+    if dtype == "bf16":
+        return bf16_bits_to_f64(a)
+    if dtype == "f32":
+        return np.asarray(a, dtype=np.float32).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def from_f64(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Storage representation of float64 values already in the dtype."""
+    if dtype == "bf16":
+        return f64_to_bf16_bits(x)
+    return np.asarray(x, dtype=np.float64).astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# The method
+# ---------------------------------------------------------------------------
+
+def project(x: np.ndarray, w_t: np.ndarray | None, dtype: str) -> np.ndarray:
+    """Query projection v_e = v W_{v->e} (Sec. 3.2, Level-1 paragraph).
+
+    x    : [n, d_in] float64 values of the stored tokens.
+    w_t  : [d_e, d_in] float64 values of W stored output-row-major (the
+           transpose of the paper's d_in x d_e matrix), or None when the
+           tokens are already queries (d_in == d_e, no projection).
+    Returns q: [n, d_e] float64 values rounded once to ``dtype``.
+    """
+    if w_t is None:
+        return np.array(x, dtype=np.float64, copy=True)
+    q_exact = x @ w_t.T           # (v W)[t, j] = sum_i v[t, i] W[i, j]
+    return round_to_dtype(q_exact, dtype)
+
+
+def _unit_rows(a: np.ndarray) -> np.ndarray:
+    n = np.sqrt(np.sum(a * a, axis=-1, keepdims=True))
+    with np.errstate(invalid="ignore", divide="ignore"):
+        return np.where(n > 0, a / np.where(n > 0, n, 1.0), 0.0)
+
+
+def scene_scores(q: np.ndarray, scene_keys: np.ndarray,
+                 bias: np.ndarray | None = None, score: str = "dot") -> np.ndarray:
+    """Level-1 scores (Eq. 5): score(v_e, e_img[s]) + b[s] for every scene.
+
+    q [n, d_e], scene_keys [S, d_e], bias [S] or None.  Returns [n, S].
+    """
+    if score == "cos":
+        s = _unit_rows(q) @ _unit_rows(scene_keys).T
+    elif score == "dot":
+        s = q @ scene_keys.T
+    else:
+        raise ValueError(score)
+    if bias is not None:
+        s = s + np.asarray(bias, dtype=np.float64)[None, :]
+    return s
+
+
+def route(q: np.ndarray, scene_keys: np.ndarray, bias: np.ndarray | None = None,
+          score: str = "dot") -> np.ndarray:
+    """Level-1 scene retrieval (Eq. 5): the arg max over scenes, lowest scene
+    index on exact ties.  Returns scene [n] int32."""
+    s = scene_scores(q, scene_keys, bias, score)
+    if s.shape[1] == 0:
+        raise ValueError("no scenes")
+    return np.argmax(s, axis=1).astype(np.int32)   # first maximum = lowest s
+
+
+def primitive_scores(q_t: np.ndarray, prim_keys_s: np.ndarray,
+                     score: str = "dot") -> np.ndarray:
+    """Level-2 scores of one token against every primitive key of its scene
+    (Eq. 6-7, configured form).  q_t [d_e], prim_keys_s [P, d_e] -> [P]."""
+    if score == "cos":
+        return _unit_rows(prim_keys_s) @ _unit_rows(q_t[None, :])[0]
+    return prim_keys_s @ q_t
+
+
+def softmax_weights(top_scores: np.ndarray) -> np.ndarray:
+    """phi in Eq. 7: softmax over the k selected scores (temperature 1),
+    evaluated with the largest score subtracted."""
+    z = top_scores - np.max(top_scores)
+    e = np.exp(z)
+    return e / np.sum(e)
+
+
+def topk_order(scores: np.ndarray, k: int) -> np.ndarray:
+    """Indices of the k largest scores, ordered by (score descending,
+    index ascending): a stable sort of the negated scores."""
+    order = np.argsort(-scores, kind="stable")
+    return order[:k]
+
+
+def lookup(q: np.ndarray, scene: np.ndarray, prim_keys: np.ndarray, k: int,
+           score: str = "dot"):
+    """Level-2 scene-primitive retrieval (Eq. 6-7, configured form).
+
+    q [n, d_e], scene [n], prim_keys [S, P, d_e] (float64 values).
+    Returns (prim [n, k] int32 in [0, P), descending score; w [n, k] float64;
+    top_scores [n, k] float64).
+    """
+    n = q.shape[0]
+    P = prim_keys.shape[1]
+    if not (1 <= k <= P):
+        raise ValueError("k must be in [1, P]")
+    prim = np.zeros((n, k), dtype=np.int32)
+    w = np.zeros((n, k), dtype=np.float64)
+    top = np.zeros((n, k), dtype=np.float64)
+    for t in range(n):
+        s2 = primitive_scores(q[t], prim_keys[scene[t]], score)
+        idx = topk_order(s2, k)
+        prim[t] = idx
+        top[t] = s2[idx]
+        w[t] = softmax_weights(s2[idx])
+    return prim, w, top
+
+
+def criticality(delta: np.ndarray) -> np.ndarray:
+    """Size of the attention update that drives the SKA gate (Eq. 9):
+    c_t = ||Delta_t||_2.  delta [n, d_c] -> [n]."""
+    return np.sqrt(np.sum(delta * delta, axis=1))
+
+
+def select(c: np.ndarray, n_keep: int) -> np.ndarray:
+    """Sparse activation (Eq. 10) with the configured gate: keep the n_keep
+    tokens of largest criticality, ties to the lowest token index; returned in
+    ascending token order."""
+    n = c.shape[0]
+    if not (0 <= n_keep <= n):
+        raise ValueError("n_keep must be in [0, n]")
+    order = np.argsort(-c, kind="stable")
+    return np.sort(order[:n_keep]).astype(np.int32)
+
+
+def retrieved(values: np.ndarray, P: int, scene_t: int, prim_t: np.ndarray,
+              w_t: np.ndarray) -> np.ndarray:
+    """R_img for one token (Eq. 7): sum_i w_i * E[scene, prim_i, :], where
+    table row (s, p) is stored at V[s*P + p, :]."""
+    rows = values[scene_t * P + np.asarray(prim_t, dtype=np.int64)]
+    return np.sum(np.asarray(w_t, dtype=np.float64)[:, None] * rows, axis=0)
+
+
+def inject(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarray,
+           prim: np.ndarray, w: np.ndarray, kept: np.ndarray, dtype: str) -> np.ndarray:
+    """Residual injection (Eq. 2 and Eq. 10): for kept tokens,
+    H[t, :d_v] <- round(H[t, :d_v] + R_img[t]); everything else unchanged.
+
+    hidden [n, d_h] and values [S*P, d_v] are float64 values; returns the new
+    hidden as float64 values of ``dtype``.
+    """
+    out = np.array(hidden, dtype=np.float64, copy=True)
+    d_v = values.shape[1]
+    for t in np.asarray(kept, dtype=np.int64):
+        r = retrieved(values, P, int(scene[t]), prim[t], w[t])
+        out[t, :d_v] = round_to_dtype(hidden[t, :d_v] + r, dtype)
+    return out
+
+
+def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
+        k: int, n_keep: int, dtype: str, score: str = "dot"):
+    """Whole path for L layers sharing one table (Sec. 3.3 inter-layer reuse).
+
+    x [n, d_in]; w_t [L, d_e, d_in] or None; delta [L, n, d_c];
+    hidden [L, n, d_h]; all float64 values.  Returns a dict of per-layer
+    results: q [L,n,d_e], scene [L,n], prim [L,n,k], w [L,n,k],
+    kept [L,n_keep], hidden [L,n,d_h].
+    """
+    L = hidden.shape[0]
+    P = prim_keys.shape[1]
+    res = {k_: [] for k_ in ("q", "scene", "prim", "w", "kept", "hidden")}
+    for l in range(L):
+        q = project(x, None if w_t is None else w_t[l], dtype)
+        sc = route(q, scene_keys, bias, score)
+        pr, ww, _ = lookup(q, sc, prim_keys, k, score)
+        kept = select(criticality(delta[l]), n_keep)
+        h = inject(hidden[l], values, P, sc, pr, ww, kept, dtype)
+        for name, v in zip(res, (q, sc, pr, ww, kept, h)):
+            res[name].append(v)
+    return {name: np.stack(v) for name, v in res.items()}

@@ -1,0 +1,8 @@
+"""Seeded synthetic workloads for the LookME hot path (inputs only).
+
+This package holds no part of the method's arithmetic: it draws random
+tensors with the shapes and distributions of the paper's workloads and is the
+one piece shared by the tests, the benchmark and the CPU oracle's callers.
+"""
+
+from .gen import Workload, WORKLOADS, make_inputs, n_keep_for  # noqa: F401

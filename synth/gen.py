@@ -1,0 +1,194 @@
+"""Seeded, chunked generation of synthetic LookME workloads.
+
+The paper's own inputs (vision-encoder tokens of Qwen2.5-VL on its fifteen
+evaluation benchmarks, and its trained tables) are not available; these
+synthetic tensors stand in for them with the shapes of the paper's
+configuration (Sec. 4.1: d_e = 512, top-8 primitives, LookME at several LLM
+layers) scaled to the sizes of the benchmark workloads.  No benchmark item is
+reproduced.
+
+Recipe (all normal draws are std, not variance):
+  tokens x          iid N(0, 1), or clustered: x_t = c_{label_t} + N(0, 0.3^2)
+                    with centroids c_s ~ N(0, I) and labels uniform or Zipf
+  projection W_l    N(0, 1/d_in), stored as W_l^T  [d_e, d_in]
+  scene keys K1     unit-norm Gaussian rows, or for clustered tokens
+                    normalize(c_s W_0) so that layer-0 routing recovers labels
+  primitive keys K2 unit-norm Gaussian rows  [S, P, d_e]
+  table values V    N(0, value_std)          [S*P, d_v]
+  criticality Delta Delta_t = a_t z_t, a_t ~ LogNormal(0, 1), z_t ~ N(0, I/d_c)
+  hidden H          iid N(0, 1)              [L, N, d_h]
+
+Seeds: sub-seed = 1000 * seed + tensor id (x=1, K1=2, K2=3, V=4, labels=5,
+centroids=6, zipf permutation=7, W_l=10+l, Delta_l=20+l, H_l=30+l); large
+tensors are drawn in chunks of 2^26 elements, chunk c seeded from
+(sub-seed, c), so the bytes depend only on (workload, seed, device type).
+Tensors are drawn in float32 and rounded to the storage dtype (bf16 by
+round-to-nearest-even in torch); keys are normalised in float32 first.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import torch
+
+CHUNK = 1 << 26
+
+TID_X, TID_K1, TID_K2, TID_V, TID_LABELS, TID_CENT, TID_PERM = 1, 2, 3, 4, 5, 6, 7
+TID_W, TID_DELTA, TID_H = 10, 20, 30
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str            # "bf16" | "f32"
+    n_tokens: int
+    layers: int
+    d_in: int
+    d_e: int
+    scenes: int
+    prims: int
+    d_v: int
+    d_h: int
+    top_k: int
+    keep_pct: int         # percent of tokens kept per layer
+    usage: str = "iid"    # "iid" | "uniform" | "zipf"
+    zipf_s: float = 1.1
+    project: bool = True  # False: tokens are used directly as queries
+    value_std: float = 0.02
+    noise_std: float = 0.3
+    d_c: int = 0          # criticality width; 0 means d_h
+
+    @property
+    def crit_dim(self) -> int:
+        return self.d_c or self.d_h
+
+    @property
+    def n_keep(self) -> int:
+        return n_keep_for(self.keep_pct, self.n_tokens)
+
+    def scaled(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+def n_keep_for(pct: int, n: int) -> int:
+    """Kept-token count: pct percent of n rounded half up, in integers."""
+    return (pct * n + 50) // 100
+
+
+# The five benchmark workloads (sizes as stated for the benchmark suite).
+WORKLOADS = {
+    0: Workload("tiny_f32_n256_s16_p64", "f32", 256, 1, 256, 256, 16, 64, 256, 256,
+                4, 25, usage="iid", project=False),
+    1: Workload("image_n1024_s256_p1024_dv2048", "bf16", 1024, 1, 2048, 512, 256, 1024,
+                2048, 2048, 8, 20, usage="iid"),
+    2: Workload("multiscale_n23040_s1024_p1024_dv1536", "bf16", 23040, 1, 2048, 512, 1024,
+                1024, 1536, 2048, 8, 15, usage="uniform"),
+    3: Workload("reuse4_n23040_s1024_p1024_dv2048", "bf16", 23040, 4, 2048, 512, 1024, 1024,
+                2048, 2048, 8, 10, usage="uniform"),
+    4: Workload("zipf_n32768_s4096_p4096_dv1024", "bf16", 32768, 1, 4096, 512, 4096, 4096,
+                1024, 4096, 16, 20, usage="zipf"),
+}
+
+TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def _gen(seed: int, chunk: int, device) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed((seed * 1_000_003 + chunk * 7919 + 12345) & 0x7FFF_FFFF_FFFF)
+    return g
+
+
+def _randn_rows(rows: int, cols: int, sub_seed: int, device, std: float,
+                dtype, normalize: bool = False) -> torch.Tensor:
+    """[rows, cols] N(0, std) drawn in row-aligned chunks, optionally with
+    every row scaled to unit L2 norm, then rounded to ``dtype``."""
+    out = torch.empty((rows, cols), dtype=dtype, device=device)
+    rows_per = max(1, CHUNK // max(cols, 1))
+    for c, r0 in enumerate(range(0, rows, rows_per)):
+        r1 = min(rows, r0 + rows_per)
+        t = torch.randn((r1 - r0, cols), generator=_gen(sub_seed, c, device),
+                        device=device, dtype=torch.float32)
+        if normalize:
+            t = t / t.norm(dim=1, keepdim=True).clamp_min(1e-30)
+        else:
+            t.mul_(std)
+        out[r0:r1] = t.to(dtype)
+    return out
+
+
+def _labels(wl: Workload, base: int, device) -> torch.Tensor:
+    n, S = wl.n_tokens, wl.scenes
+    g = _gen(base + TID_LABELS, 0, device)
+    if wl.usage == "uniform":
+        return torch.randint(0, S, (n,), generator=g, device=device, dtype=torch.int64)
+    if wl.usage == "zipf":
+        ranks = torch.arange(1, S + 1, device=device, dtype=torch.float64)
+        p = ranks.pow(-wl.zipf_s)
+        p = (p / p.sum()).to(torch.float32)
+        r = torch.multinomial(p, n, replacement=True, generator=g)
+        perm = torch.randperm(S, generator=_gen(base + TID_PERM, 0, device), device=device)
+        return perm[r]
+    raise ValueError(wl.usage)
+
+
+def make_inputs(wl: Workload, seed: int, device="cpu") -> dict:
+    """Draw every input of one workload.
+
+    Returns a dict of torch tensors on ``device``:
+      x [N, d_in]; wt [L, d_e, d_in] (None when tokens are queries);
+      scene_keys [S, d_e]; prim_keys [S, P, d_e]; values [S*P, d_v];
+      bias None; delta [L, N, d_c]; hidden [L, N, d_h]; labels [N] or None;
+    plus the workload and the integer parameters k and n_keep.
+    """
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[wl.dtype]
+    base = 1000 * seed
+    N, L = wl.n_tokens, wl.layers
+    if not wl.project and wl.d_in != wl.d_e:
+        raise ValueError("unprojected workloads need d_in == d_e")
+
+    labels = None
+    centroids = None
+    if wl.usage == "iid":
+        x = _randn_rows(N, wl.d_in, base + TID_X, dev, 1.0, dt)
+    else:
+        labels = _labels(wl, base, dev)
+        centroids = _randn_rows(wl.scenes, wl.d_in, base + TID_CENT, dev, 1.0, torch.float32)
+        noise = _randn_rows(N, wl.d_in, base + TID_X, dev, wl.noise_std, torch.float32)
+        x = (centroids[labels] + noise).to(dt)
+        del noise
+
+    wt = None
+    if wl.project:
+        wt = torch.empty((L, wl.d_e, wl.d_in), dtype=dt, device=dev)
+        for l in range(L):
+            wt[l] = _randn_rows(wl.d_e, wl.d_in, base + TID_W + l, dev,
+                                1.0 / math.sqrt(wl.d_in), dt)
+
+    if centroids is not None and wt is not None:
+        k1 = centroids @ wt[0].to(torch.float32).T
+        k1 = k1 / k1.norm(dim=1, keepdim=True).clamp_min(1e-30)
+        scene_keys = k1.to(dt)
+    else:
+        scene_keys = _randn_rows(wl.scenes, wl.d_e, base + TID_K1, dev, 1.0, dt,
+                                 normalize=True)
+    prim_keys = _randn_rows(wl.scenes * wl.prims, wl.d_e, base + TID_K2, dev, 1.0, dt,
+                            normalize=True).view(wl.scenes, wl.prims, wl.d_e)
+    values = _randn_rows(wl.scenes * wl.prims, wl.d_v, base + TID_V, dev, wl.value_std, dt)
+
+    delta = torch.empty((L, N, wl.crit_dim), dtype=dt, device=dev)
+    hidden = torch.empty((L, N, wl.d_h), dtype=dt, device=dev)
+    for l in range(L):
+        g = _gen(base + TID_DELTA + l, 0, dev)
+        a = torch.exp(torch.randn((N, 1), generator=g, device=dev, dtype=torch.float32))
+        z = _randn_rows(N, wl.crit_dim, base + TID_DELTA + l + 500, dev,
+                        1.0 / math.sqrt(wl.crit_dim), torch.float32)
+        delta[l] = (a * z).to(dt)
+        del z
+        hidden[l] = _randn_rows(N, wl.d_h, base + TID_H + l, dev, 1.0, dt)
+
+    return dict(workload=wl, x=x, wt=wt, scene_keys=scene_keys, prim_keys=prim_keys,
+                values=values, bias=None, delta=delta, hidden=hidden, labels=labels,
+                k=wl.top_k, n_keep=wl.n_keep)

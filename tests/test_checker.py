@@ -1,0 +1,116 @@
+"""The checker must accept the oracle's own results, accept genuine ties, and
+reject planted mistakes (all on the CPU, no library involved)."""
+
+import numpy as np
+
+from oracle import check as C
+from oracle import lookme_oracle as O
+
+
+def _setup(seed=0, n=40, S=6, P=30, d=16, k=4, d_v=8, d_h=10):
+    rng = np.random.default_rng(seed)
+    q = O.round_to_bf16(rng.standard_normal((n, d)))
+    K1 = O.round_to_bf16(rng.standard_normal((S, d)) / np.sqrt(d))
+    K2 = O.round_to_bf16(rng.standard_normal((S, P, d)) / np.sqrt(d))
+    V = O.round_to_bf16(rng.standard_normal((S * P, d_v)) * 0.02)
+    H = O.round_to_bf16(rng.standard_normal((n, d_h)))
+    D = rng.standard_normal((n, d_h)) * rng.lognormal(size=(n, 1))
+    return q, K1, K2, V, H, D, k
+
+
+def test_checker_accepts_oracle_results():
+    q, K1, K2, V, H, D, k = _setup()
+    rep = C.Report()
+    scene = O.route(q, K1)
+    C.check_scene(q, K1, None, "dot", scene, rep)
+    prim, w, _ = O.lookup(q, scene, K2, k)
+    w_orc = C.check_prim(q, scene, lambda s: K2[s], k, "dot", prim, w.astype(np.float32), rep)
+    c = O.criticality(D)
+    kept = O.select(c, 13)
+    C.check_kept(c, 13, kept, rep)
+    out = O.inject(H, V, K2.shape[1], scene, prim, w, kept, "bf16")
+    C.check_hidden(O.from_f64(H, "bf16"), O.from_f64(out, "bf16"), "bf16", lambda r: V[r],
+                   K2.shape[1], scene, prim, lambda t: w_orc[t], kept, rep)
+    assert rep.finish().ok, str(rep)
+    assert not rep.exemptions
+
+
+def test_checker_rejects_planted_mistakes():
+    q, K1, K2, V, H, D, k = _setup(1)
+    scene = O.route(q, K1)
+    # a wrong scene
+    bad = scene.copy()
+    bad[3] = (bad[3] + 1) % K1.shape[0]
+    rep = C.Report()
+    C.check_scene(q, K1, None, "dot", bad, rep)
+    assert not rep.ok
+    # a primitive set missing its best element
+    prim, w, _ = O.lookup(q, scene, K2, k)
+    bp = prim.copy()
+    bp[5, 0] = [p for p in range(K2.shape[1]) if p not in prim[5]][0]
+    rep = C.Report()
+    C.check_prim(q, scene, lambda s: K2[s], k, "dot", bp, w, rep)
+    assert not rep.ok
+    # ascending instead of descending order
+    rep = C.Report()
+    C.check_prim(q, scene, lambda s: K2[s], k, "dot", prim[:, ::-1], w[:, ::-1], rep)
+    assert not rep.ok
+    # weights off by 1e-4
+    rep = C.Report()
+    C.check_prim(q, scene, lambda s: K2[s], k, "dot", prim, w + 1e-4, rep)
+    assert not rep.ok
+    # kept set with the smallest instead of the largest
+    c = O.criticality(D)
+    rep = C.Report()
+    C.check_kept(c, 5, np.sort(np.argsort(c)[:5]), rep)
+    assert not rep.ok
+    rep = C.Report()
+    C.check_kept(c, 5, O.select(c, 5)[::-1], rep)
+    assert not rep.ok
+    # an untouched row modified, and a touched row off by one bf16 step x2
+    kept = O.select(c, 10)
+    out = O.inject(H, V, K2.shape[1], scene, prim, w, kept, "bf16")
+    bits = O.from_f64(out, "bf16")
+    untouched = [t for t in range(q.shape[0]) if t not in kept][0]
+    b2 = bits.copy()
+    b2[untouched, 0] ^= 1
+    rep = C.Report()
+    C.check_hidden(O.from_f64(H, "bf16"), b2, "bf16", lambda r: V[r], K2.shape[1], scene, prim,
+                   lambda t: w[t], kept, rep)
+    assert not rep.ok
+    b3 = bits.copy()
+    b3[kept[0], 1] = (b3[kept[0], 1].astype(np.int32) + 2).astype(np.uint16)
+    rep = C.Report()
+    C.check_hidden(O.from_f64(H, "bf16"), b3, "bf16", lambda r: V[r], K2.shape[1], scene, prim,
+                   lambda t: w[t], kept, rep)
+    assert not rep.ok
+
+
+def test_checker_exempts_true_ties_only():
+    # two scenes whose scores for the token differ by 1e-7 relative
+    q = np.array([[1.0, 0.0]])
+    K1 = np.array([[1.0, 0.0], [1.0 - 1e-7, 0.0]])
+    rep = C.Report()
+    C.check_scene(q, K1, None, "dot", np.array([1]), rep)
+    assert rep.ok and rep.exemptions == {"scene": 1}
+    K1b = np.array([[1.0, 0.0], [0.999, 0.0]])
+    rep = C.Report()
+    C.check_scene(q, K1b, None, "dot", np.array([1]), rep)
+    assert not rep.ok
+
+
+def test_checker_fails_when_exemptions_exceed_one_percent():
+    rep = C.Report()
+    rep.count("prim", 1000)
+    rep.exempt("prim", 11)
+    assert not rep.finish().ok
+    rep = C.Report()
+    rep.count("prim", 1000)
+    rep.exempt("prim", 9)
+    assert rep.finish().ok
+
+
+def test_ulp_distance():
+    a = O.from_f64(np.array([1.0, -1.0, 0.0]), "bf16")
+    b = O.from_f64(np.array([1 + 2 ** -7, -1.0 - 2 ** -6, -0.0]), "bf16")
+    assert C.ulp_distance(a, b, "bf16").tolist() == [1, 2, 0]

@@ -1,0 +1,466 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle
+itself: a hand-derived worked example, closed forms, library routines,
+exact rational brute force and invariants (arXiv 2607.16305, Sec. 3.2-3.3).
+
+Each test names the mistake it is there to catch.
+"""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import brute as B
+from oracle import lookme_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bf16_values(rng, shape, scale=1.0):
+    """Random float64 values that are exactly bfloat16 numbers."""
+    return O.round_to_bf16(rng.standard_normal(shape) * scale)
+
+
+def _unit(rng, shape):
+    a = rng.standard_normal(shape)
+    return a / np.linalg.norm(a, axis=-1, keepdims=True)
+
+
+# --------------------------------------------------------------------------
+# Number formats
+# --------------------------------------------------------------------------
+
+def test_round_bf16_matches_torch_on_float32_inputs():
+    """Catches a wrong rounding rule: for values that are exact binary32
+    numbers, direct rounding to bf16 must equal torch's fp32->bf16 (RNE)."""
+    rng = np.random.default_rng(1)
+    x = np.concatenate([
+        rng.standard_normal(20000),
+        rng.standard_normal(2000) * 1e-38,     # binary32 subnormal range
+        rng.standard_normal(2000) * 1e30,
+        np.array([0.0, -0.0, 1.0, -1.0]),
+    ]).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = O.round_to_bf16(x.astype(np.float64))
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_round_bf16_ties_to_even_and_no_double_rounding():
+    """Catches round-half-up, truncation and rounding through binary32."""
+    e = 2.0 ** -8
+    assert O.round_to_bf16(np.array([1 + e]))[0] == 1.0               # tie -> even
+    assert O.round_to_bf16(np.array([1 + 3 * e]))[0] == 1 + 2 ** -6    # tie -> even
+    assert O.round_to_bf16(np.array([-(1 + 3 * e)]))[0] == -(1 + 2 ** -6)
+    # just above the midpoint: binary32 would round to the midpoint first and
+    # then tie to 1.0; the correct result is the upper neighbour.
+    v = 1 + e + 2.0 ** -30
+    assert np.float32(v) == np.float32(1 + e)
+    assert O.round_to_bf16(np.array([v]))[0] == 1 + 2 ** -7
+
+
+def test_round_bf16_matches_exact_rational_rounding():
+    """Two independent roundings (float64 scaling vs exact Fractions)."""
+    rng = np.random.default_rng(2)
+    x = np.concatenate([rng.standard_normal(3000) * 10.0 ** rng.integers(-40, 38, 3000)])
+    got = O.round_to_bf16(x)
+    for a, g in zip(x, got):
+        assert Fraction(float(g)) == B.round_bf16(Fraction(float(a)))
+
+
+def test_round_f32_matches_exact_rational_rounding():
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal(3000) * 10.0 ** rng.integers(-30, 30, 3000)
+    got = O.round_to_dtype(x, "f32")
+    for a, g in zip(x, got):
+        assert Fraction(float(g)) == B.round_f32(Fraction(float(a)))
+
+
+def test_bf16_bits_roundtrip():
+    rng = np.random.default_rng(4)
+    bits = rng.integers(0, 1 << 16, 5000).astype(np.uint16)
+    vals = O.bf16_bits_to_f64(bits)
+    fin = np.isfinite(vals)
+    back = O.f64_to_bf16_bits(vals[fin])
+    np.testing.assert_array_equal(back, bits[fin])
+    # against torch's own reinterpretation of the same bits
+    t = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(vals[fin], t[fin])
+
+
+# --------------------------------------------------------------------------
+# Worked example (hand-derived, tests/golden)
+# --------------------------------------------------------------------------
+
+def _softmax_closed(scores):
+    ex = [math.exp(s - max(scores)) for s in scores]
+    return [e / sum(ex) for e in ex]
+
+
+def test_worked_example():
+    """Catches wrong tie-breaks (scene, primitive and token), a wrong table
+    row index s*P + p, and a wrong weight formula."""
+    with open(os.path.join(GOLDEN, "worked_example_s2_p3.json")) as f:
+        g = json.load(f)
+    q = np.array(g["queries"], dtype=np.float64)
+    K1 = np.array(g["scene_keys"], dtype=np.float64)
+    K2 = np.array(g["prim_keys"], dtype=np.float64)
+    V = np.array(g["values"], dtype=np.float64)
+    H = np.array(g["hidden"], dtype=np.float64)
+    D = np.array(g["delta"], dtype=np.float64)
+    k, n_keep = g["k"], g["n_keep"]
+    exp = g["expected"]
+
+    scene = O.route(q, K1)
+    assert scene.tolist() == exp["scene"]
+    prim, w, top = O.lookup(q, scene, K2, k)
+    assert prim.tolist() == exp["prim"]
+    np.testing.assert_array_equal(top, np.array(exp["top_scores"], dtype=np.float64))
+    for t in range(4):
+        np.testing.assert_allclose(w[t], _softmax_closed(exp["top_scores"][t]), rtol=1e-15)
+    kept = O.select(O.criticality(D), n_keep)
+    assert kept.tolist() == exp["kept"]
+    out = O.inject(H, V, K2.shape[1], scene, prim, w, kept, "f32")
+    for t in range(4):
+        if t in exp["kept"]:
+            ws = _softmax_closed(exp["top_scores"][t])
+            r = [sum(ws[i] * V[exp["rows"][t][i]][j] for i in range(k)) for j in range(2)]
+            np.testing.assert_array_equal(out[t], np.float32(r).astype(np.float64))
+        else:
+            np.testing.assert_array_equal(out[t], H[t])
+    # t1 lives in scene 1: its rows are V[3*1 + 1] and V[3*1 + 0]
+    np.testing.assert_allclose(out[1], [4 - w[1, 1], 40 - 10 * w[1, 1]], rtol=1e-6)
+
+
+# --------------------------------------------------------------------------
+# Projection
+# --------------------------------------------------------------------------
+
+def test_project_matches_exact_rational_brute_force():
+    """Catches a transposed W (d_in != d_e), a missing rounding and a wrong
+    rounding point."""
+    rng = np.random.default_rng(10)
+    n, d_in, d_e = 5, 7, 3
+    x = _bf16_values(rng, (n, d_in))
+    wt = _bf16_values(rng, (d_e, d_in), 0.3)
+    q = O.project(x, wt, "bf16")
+    ref = B.project(x.tolist(), wt.tolist(), B.round_bf16)
+    assert q.shape == (n, d_e)
+    for t in range(n):
+        for j in range(d_e):
+            assert Fraction(float(q[t, j])) == ref[t][j]
+
+
+def test_project_one_hot_tokens_pick_columns():
+    """Closed form: token e_i projects to column i of W (row i of W^T...)."""
+    rng = np.random.default_rng(11)
+    d_in, d_e = 6, 4
+    wt = _bf16_values(rng, (d_e, d_in))
+    x = np.eye(d_in)
+    q = O.project(x, wt, "bf16")
+    np.testing.assert_array_equal(q, wt.T)
+
+
+def test_project_without_weights_is_identity():
+    x = np.arange(12, dtype=np.float64).reshape(3, 4)
+    np.testing.assert_array_equal(O.project(x, None, "f32"), x)
+
+
+# --------------------------------------------------------------------------
+# Level-1 routing (Eq. 5)
+# --------------------------------------------------------------------------
+
+def test_route_matches_brute_force():
+    rng = np.random.default_rng(20)
+    n, S, d = 40, 9, 8
+    q = _bf16_values(rng, (n, d))
+    K1 = O.round_to_bf16(_unit(rng, (S, d)))
+    b = rng.standard_normal(S) * 0.1
+    assert O.route(q, K1, b).tolist() == B.route(q.tolist(), K1.tolist(), b.tolist())
+    assert O.route(q, K1).tolist() == B.route(q.tolist(), K1.tolist())
+
+
+def test_route_exact_integer_ties_go_to_lowest_scene():
+    """Catches highest-index or arbitrary tie-breaks."""
+    K1 = np.array([[1, 0, 0], [0, 1, 0], [1, 0, 0], [0, 1, 0]], dtype=np.float64)
+    q = np.array([[2, 2, 0], [0, 3, 1], [5, 1, 9]], dtype=np.float64)
+    assert O.route(q, K1).tolist() == [0, 1, 0]
+
+
+def test_route_bias_sign():
+    """Catches a subtracted (rather than added) bias."""
+    K1 = np.eye(2)
+    q = np.array([[1.0, 2.0]])
+    assert O.route(q, K1).tolist() == [1]
+    assert O.route(q, K1, np.array([1.5, 0.0])).tolist() == [0]
+    assert O.route(q, K1, np.array([0.0, -1.5])).tolist() == [0]
+
+
+def test_route_planted_clusters_and_single_scene():
+    rng = np.random.default_rng(21)
+    S, d = 12, 32
+    K1 = _unit(rng, (S, d))
+    labels = rng.integers(0, S, 200)
+    q = 5.0 * K1[labels] + 0.05 * rng.standard_normal((200, d))
+    assert np.array_equal(O.route(q, K1), labels)
+    assert O.route(q, K1[:1]).tolist() == [0] * 200
+
+
+def test_route_cos_equals_dot_for_unit_keys_without_bias():
+    """A positive per-token scale preserves the arg max."""
+    rng = np.random.default_rng(22)
+    K1 = _unit(rng, (30, 16))
+    q = rng.standard_normal((50, 16)) * rng.uniform(0.1, 10, (50, 1))
+    assert np.array_equal(O.route(q, K1, score="cos"), O.route(q, K1, score="dot"))
+
+
+# --------------------------------------------------------------------------
+# Level-2 lookup (Eq. 6-7, configured form)
+# --------------------------------------------------------------------------
+
+def test_lookup_equals_exhaustive_search_within_scene():
+    """spec brute force: the two-level result equals an exhaustive top-k
+    over the rows [s*P, (s+1)*P) of the chosen scene in the flat table.
+    Catches a wrong scene offset and a transposed key operand (S != P != d)."""
+    rng = np.random.default_rng(30)
+    n, S, P, d, k = 25, 5, 11, 6, 4
+    q = _bf16_values(rng, (n, d))
+    K2 = O.round_to_bf16(_unit(rng, (S, P, d)))
+    scene = rng.integers(0, S, n).astype(np.int32)
+    prim, w, top = O.lookup(q, scene, K2, k)
+    bp, btop = B.lookup_flat_sim(q.tolist(), scene.tolist(), K2.reshape(S * P, d).tolist(), P, k)
+    assert prim.tolist() == bp
+    for t in range(n):
+        assert [Fraction(float(v)) for v in top[t]] == btop[t]
+        np.testing.assert_allclose(w[t], B.softmax(btop[t]), rtol=1e-14)
+
+
+def test_lookup_planted_ranking():
+    """Keys at known angles to q: the top-k and the weights are known."""
+    rng = np.random.default_rng(31)
+    d, P, k = 64, 20, 5
+    q = rng.standard_normal(d)
+    qh = q / np.linalg.norm(q)
+    betas = rng.permutation(np.linspace(-0.9, 0.95, P))
+    keys = np.zeros((P, d))
+    for p in range(P):
+        u = rng.standard_normal(d)
+        u -= (u @ qh) * qh
+        u /= np.linalg.norm(u)
+        keys[p] = betas[p] * qh + math.sqrt(1 - betas[p] ** 2) * u
+    prim, w, top = O.lookup(q[None], np.array([0]), keys[None], k)
+    expect = np.argsort(-betas)[:k]
+    assert prim[0].tolist() == expect.tolist()
+    s = betas[expect] * np.linalg.norm(q)
+    np.testing.assert_allclose(top[0], s, rtol=1e-12)
+    np.testing.assert_allclose(w[0], np.exp(s - s.max()) / np.exp(s - s.max()).sum(), rtol=1e-12)
+
+
+def test_lookup_k_equals_p_and_integer_ties():
+    """k = P lists every primitive; exact ties list the lower p first."""
+    K2 = np.array([[[1, 0], [0, 1], [1, 0], [2, 0], [0, 1]]], dtype=np.float64)
+    q = np.array([[1.0, 1.0]])
+    prim, w, top = O.lookup(q, np.array([0]), K2, 5)
+    # scores 1, 1, 1, 2, 1 -> 3 first, then 0, 1, 2, 4 in index order
+    assert prim[0].tolist() == [3, 0, 1, 2, 4]
+    prim, _, _ = O.lookup(q, np.array([0]), K2, 2)
+    assert prim[0].tolist() == [3, 0]
+
+
+def test_lookup_many_exact_ties_against_brute_force():
+    """Integer keys with few distinct scores over P = 300: an unstable sort
+    (e.g. an introsort on long arrays) would list tied primitives out of
+    index order."""
+    rng = np.random.default_rng(32)
+    P, d, k = 300, 4, 40
+    K2 = rng.integers(-1, 2, (1, P, d)).astype(np.float64)
+    q = rng.integers(-2, 3, (3, d)).astype(np.float64)
+    prim, _, top = O.lookup(q, np.zeros(3, dtype=np.int32), K2, k)
+    bp, btop = B.lookup_flat_sim(q.tolist(), [0, 0, 0], K2[0].tolist(), P, k)
+    assert prim.tolist() == bp
+
+
+def test_softmax_closed_forms():
+    """k = 1 gives exactly 1; equal scores give exactly 1/k; ln3 vs 0 gives
+    3/4 and 1/4; huge scores do not overflow (max subtracted)."""
+    assert O.softmax_weights(np.array([7.25])).tolist() == [1.0]
+    assert O.softmax_weights(np.array([2.0] * 4)).tolist() == [0.25] * 4
+    np.testing.assert_allclose(O.softmax_weights(np.array([math.log(3), 0.0])), [0.75, 0.25],
+                               rtol=1e-15)
+    w = O.softmax_weights(np.array([1000.0, 999.0]))
+    np.testing.assert_allclose(w, [1 / (1 + math.exp(-1)), math.exp(-1) / (1 + math.exp(-1))])
+    assert abs(O.softmax_weights(np.random.default_rng(0).standard_normal(16)).sum() - 1) < 1e-15
+
+
+# --------------------------------------------------------------------------
+# Criticality select (Eq. 9-10, configured gate)
+# --------------------------------------------------------------------------
+
+def test_select_matches_brute_force_and_is_ascending():
+    rng = np.random.default_rng(40)
+    D = rng.standard_normal((60, 9)) * rng.lognormal(size=(60, 1))
+    c = O.criticality(D)
+    nsq = [sum(Fraction(float(v)) ** 2 for v in row) for row in D]
+    for n_keep in (0, 1, 7, 30, 60):
+        assert O.select(c, n_keep).tolist() == B.select(nsq, n_keep)
+
+
+def test_select_planted_and_ties():
+    """Planted norms gamma_t e_1; equal norms keep the lowest indices.
+    Catches keeping the smallest instead of the largest."""
+    gam = np.array([3.0, 9.0, 1.0, 7.0, 5.0])
+    D = np.zeros((5, 4))
+    D[:, 0] = gam
+    assert O.select(O.criticality(D), 2).tolist() == [1, 3]
+    assert O.select(O.criticality(-D), 3).tolist() == [1, 3, 4]
+    E = np.ones((6, 3))
+    assert O.select(O.criticality(E), 4).tolist() == [0, 1, 2, 3]
+    # long arrays with few distinct norms: ties must still keep low indices
+    rng = np.random.default_rng(41)
+    F = rng.integers(0, 3, (500, 2)).astype(np.float64)
+    nsq = [int(a * a + b * b) for a, b in F]
+    for n_keep in (37, 250, 499):
+        assert O.select(O.criticality(F), n_keep).tolist() == B.select(nsq, n_keep)
+    assert O.select(O.criticality(E), 6).tolist() == list(range(6))
+    assert O.select(O.criticality(E), 0).tolist() == []
+
+
+# --------------------------------------------------------------------------
+# Injection (Eq. 2, Eq. 10)
+# --------------------------------------------------------------------------
+
+def test_inject_matches_exact_rational_brute_force_bf16():
+    """Catches a double rounding, a missing H term and a wrong row index."""
+    rng = np.random.default_rng(50)
+    n, S, P, d_v, d_h, k = 6, 3, 4, 5, 7, 3
+    H = _bf16_values(rng, (n, d_h))
+    V = _bf16_values(rng, (S * P, d_v), 0.5)
+    scene = rng.integers(0, S, n)
+    prim = np.array([rng.permutation(P)[:k] for _ in range(n)])
+    w = np.array([O.softmax_weights(rng.standard_normal(k)) for _ in range(n)])
+    kept = np.array([0, 2, 3, 5])
+    out = O.inject(H, V, P, scene, prim, w, kept, "bf16")
+    ref = B.inject(H.tolist(), V.tolist(), P, scene.tolist(), prim.tolist(), w.tolist(),
+                   kept.tolist(), B.round_bf16)
+    for t in range(n):
+        for j in range(d_h):
+            assert Fraction(float(out[t, j])) == ref[t][j], (t, j)
+
+
+def test_inject_k1_float32_is_one_correctly_rounded_add():
+    """k = 1 in float32: out = fl(H + V_row) bit for bit."""
+    rng = np.random.default_rng(51)
+    n, S, P, d = 8, 2, 3, 16
+    H32 = rng.standard_normal((n, d)).astype(np.float32)
+    V32 = (rng.standard_normal((S * P, d)) * 1e-3).astype(np.float32)
+    scene = rng.integers(0, S, n)
+    prim = rng.integers(0, P, (n, 1))
+    w = np.ones((n, 1))
+    kept = np.arange(n)
+    out = O.inject(H32.astype(np.float64), V32.astype(np.float64), P, scene, prim, w, kept, "f32")
+    ref = H32 + V32[scene * P + prim[:, 0]]
+    np.testing.assert_array_equal(out.astype(np.float32), ref)
+
+
+def test_inject_zero_hidden_gives_retrieved_rows_and_leaves_rest():
+    """Rows that encode their own index reveal which rows were gathered;
+    untouched rows and columns >= d_v keep their bits."""
+    S, P, d_v, d_h = 3, 4, 2, 3
+    V = np.array([[r, -r] for r in range(S * P)], dtype=np.float64)
+    H = np.zeros((4, d_h))
+    H[:, 2] = 9.0
+    scene = np.array([2, 0, 1, 1])
+    prim = np.array([[3], [1], [0], [2]])
+    w = np.ones((4, 1))
+    out = O.inject(H, V, P, scene, prim, w, np.array([0, 2]), "f32")
+    assert out[0].tolist() == [11.0, -11.0, 9.0]      # row 2*4 + 3
+    assert out[2].tolist() == [4.0, -4.0, 9.0]        # row 1*4 + 0
+    assert out[1].tolist() == [0.0, 0.0, 9.0]
+    assert out[3].tolist() == [0.0, 0.0, 9.0]
+
+
+def test_retrieved_is_in_convex_hull_of_rows():
+    rng = np.random.default_rng(52)
+    V = rng.standard_normal((12, 5))
+    w = O.softmax_weights(rng.standard_normal(4))
+    r = O.retrieved(V, 4, 2, np.array([0, 3, 1, 2]), w)
+    rows = V[8:12][[0, 3, 1, 2]]
+    assert np.all(r <= rows.max(axis=0) + 1e-15) and np.all(r >= rows.min(axis=0) - 1e-15)
+
+
+# --------------------------------------------------------------------------
+# Whole path
+# --------------------------------------------------------------------------
+
+def _tiny_inputs(seed, L=2, n=24, d_in=12, d_e=8, S=4, P=6, d_v=5, d_h=7, k=3):
+    rng = np.random.default_rng(seed)
+    return dict(
+        x=_bf16_values(rng, (n, d_in)),
+        w_t=_bf16_values(rng, (L, d_e, d_in), 0.3),
+        scene_keys=O.round_to_bf16(_unit(rng, (S, d_e))),
+        prim_keys=O.round_to_bf16(_unit(rng, (S, P, d_e))),
+        values=_bf16_values(rng, (S * P, d_v), 0.02),
+        bias=None,
+        delta=_bf16_values(rng, (L, n, d_h)),
+        hidden=_bf16_values(rng, (L, n, d_h)),
+    ), k
+
+
+def test_run_layers_equal_independent_single_layer_runs():
+    """Table reuse across layers must not change any layer's result."""
+    inp, k = _tiny_inputs(60)
+    full = O.run(**inp, k=k, n_keep=7, dtype="bf16")
+    for l in range(2):
+        one = dict(inp)
+        one["w_t"] = inp["w_t"][l:l + 1]
+        one["delta"] = inp["delta"][l:l + 1]
+        one["hidden"] = inp["hidden"][l:l + 1]
+        r = O.run(**one, k=k, n_keep=7, dtype="bf16")
+        for name in full:
+            np.testing.assert_array_equal(full[name][l], r[name][0])
+
+
+def test_run_token_permutation_equivariance():
+    inp, k = _tiny_inputs(61, L=1)
+    perm = np.random.default_rng(5).permutation(inp["x"].shape[0])
+    a = O.run(**inp, k=k, n_keep=24, dtype="bf16")    # keep all: no cut ties
+    pinp = dict(inp)
+    pinp["x"] = inp["x"][perm]
+    pinp["delta"] = inp["delta"][:, perm]
+    pinp["hidden"] = inp["hidden"][:, perm]
+    b = O.run(**pinp, k=k, n_keep=24, dtype="bf16")
+    for name in ("q", "scene", "prim", "w", "hidden"):
+        np.testing.assert_array_equal(a[name][0][perm], b[name][0])
+
+
+def test_run_matches_brute_force_end_to_end():
+    """Every stage of the whole path against the rational brute force."""
+    inp, k = _tiny_inputs(62, L=1, n=10)
+    n_keep = 4
+    res = O.run(**inp, k=k, n_keep=n_keep, dtype="bf16")
+    q = B.project(inp["x"].tolist(), inp["w_t"][0].tolist(), B.round_bf16)
+    assert [[Fraction(float(v)) for v in row] for row in res["q"][0]] == q
+    scenes = B.route(q, inp["scene_keys"].tolist())
+    assert res["scene"][0].tolist() == scenes
+    S, P, d_e = inp["prim_keys"].shape
+    prim, top = B.lookup_flat_sim(q, scenes, inp["prim_keys"].reshape(S * P, d_e).tolist(), P, k)
+    assert res["prim"][0].tolist() == prim
+    nsq = [sum(Fraction(float(v)) ** 2 for v in row) for row in inp["delta"][0]]
+    kept = B.select(nsq, n_keep)
+    assert res["kept"][0].tolist() == kept
+    w = [B.softmax(tp) for tp in top]
+    np.testing.assert_allclose(res["w"][0], w, rtol=1e-13)
+    hid = B.inject(inp["hidden"][0].tolist(), inp["values"].tolist(), P, scenes, prim,
+                   res["w"][0].tolist(), kept, B.round_bf16)
+    for t in range(10):
+        assert [Fraction(float(v)) for v in res["hidden"][0][t]] == hid[t]
+
+
+def test_oracle_rejects_bad_sizes():
+    with pytest.raises(ValueError):
+        O.select(np.ones(3), 4)
+    with pytest.raises(ValueError):
+        O.lookup(np.ones((1, 2)), np.array([0]), np.ones((1, 3, 2)), 4)
