@@ -1,0 +1,158 @@
+/*
+ * lookme.h -- C ABI of the LookME image-pathway hot path on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * Paper: "LookME: Lookup-Based Multimodal Embeddings for Layer Injection in
+ * Vision-Language Models", arXiv 2607.16305.
+ *
+ * For every continuous multimodal token the library
+ *   1. projects it into the table's key space      (Sec. 3.2, Level-1: v_e = v W_{v->e})
+ *   2. routes it to one scene                        (Sec. 3.2, Eq. 5)
+ *   3. picks the top-k primitives of that scene and  (Sec. 3.2, Eq. 6-7, dot-score form
+ *      softmax-weights them                           against per-row primitive keys)
+ *   4. selects the critical tokens                   (Sec. 3.3, Eq. 9-10: keep the n_keep
+ *                                                     tokens of largest ||Delta_t||_2)
+ *   5. adds the weighted table rows into their       (Eq. 2 and Eq. 10)
+ *      hidden states,
+ * for one or several layers that share the table (Sec. 3.3, inter-layer reuse).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  * Tensors are DEVICE pointers, row-major and contiguous, owned by the
+ *    caller.  Every pointer must be 16-byte aligned.  Element type is the
+ *    table dtype (LOOKME_F32 or LOOKME_BF16) unless stated (int32 indices,
+ *    float32 weights and bias).
+ *  * Calls are asynchronous on `stream` (a hipStream_t; NULL = default
+ *    stream).  The library itself never allocates device memory: scratch
+ *    space comes from the caller's workspace (lookme_set_workspace).
+ *  * Every argument is validated before anything is launched; on any error
+ *    nothing is written and the status says why (lookme_last_error() gives
+ *    the message).  No C++ exception crosses this boundary.
+ *  * n == 0 is a valid no-op.  A handle is not thread-safe (it owns one
+ *    workspace); calls on one handle must be ordered on one stream.
+ *  * Exact score ties resolve to the lowest index (scene, primitive, token).
+ */
+#ifndef LOOKME_H_
+#define LOOKME_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lookme_s* lookme_t;           /* opaque; borrows the table */
+
+typedef enum {
+  LOOKME_OK = 0,
+  LOOKME_ERR_INVALID = 1,       /* bad argument (null, size, alignment, range) */
+  LOOKME_ERR_UNSUPPORTED = 2,   /* valid but outside what this build implements */
+  LOOKME_ERR_WORKSPACE = 3,     /* no workspace set, or too small for the call */
+  LOOKME_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed */
+} lookme_status_t;
+
+typedef enum { LOOKME_F32 = 0, LOOKME_BF16 = 1 } lookme_dtype_t;
+typedef enum { LOOKME_SCORE_DOT = 0, LOOKME_SCORE_COS = 1 } lookme_score_t;
+
+/* Largest supported top-k (T~ in Eq. 6). */
+#define LOOKME_KMAX 32
+
+typedef struct {
+  int32_t num_scenes;       /* N_s  (Sec. 3.2 "Two-level embedding table")            */
+  int32_t prims_per_scene;  /* N_p                                                   */
+  int32_t key_dim;          /* d_e: width of scene keys, primitive keys and queries;
+                               key_dim * elem_size must be a multiple of 64 bytes
+                               and at most 2048 bytes                               */
+  int32_t value_dim;        /* d_v: width of a table row that is added into H;
+                               value_dim * elem_size must be a multiple of 16 bytes  */
+  int32_t top_k;            /* T~ (Eq. 6): 1 <= top_k <= min(N_p, LOOKME_KMAX)       */
+  int32_t dtype;            /* lookme_dtype_t of keys, values, queries, hidden       */
+  int32_t score;            /* lookme_score_t; this build implements DOT (the dot
+                               score of the configured workloads); COS (the cosine
+                               of Eq. 5 and Eq. 7) returns LOOKME_ERR_UNSUPPORTED    */
+} lookme_desc_t;
+
+/*
+ * lookme_create -- describe an HBM-resident table (Sec. 3.2).
+ *   scene_keys [N_s, d_e]        e_img of Eq. 4-5: one routing key per scene
+ *   prim_keys  [N_s, N_p, d_e]   one key per table row, scored in Level-2
+ *   values     [N_s * N_p, d_v]  table rows; row (s, p) is values[s*N_p + p]
+ *   scene_bias [N_s] float32 or NULL (b of Eq. 5; NULL means 0)
+ * The handle BORROWS the four pointers: they must stay valid and unmodified
+ * until lookme_destroy.  Nothing is copied (a table may be tens of GiB).
+ * No HIP call is made.
+ */
+lookme_status_t lookme_create(const lookme_desc_t* desc, const void* scene_keys,
+                              const void* prim_keys, const void* values,
+                              const float* scene_bias, lookme_t* out);
+
+/* Bytes of device workspace needed by route/lookup/inject for `layers`
+ * layers of `n_tokens` tokens each.  No HIP call is made. */
+lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_tokens,
+                                      size_t* bytes);
+
+/* Attach caller-owned device workspace (256-byte aligned).  The library
+ * zero-fills a small counter region of it once here (hipMemset on the current
+ * device); it must not be modified by the caller while the handle uses it. */
+lookme_status_t lookme_set_workspace(lookme_t h, void* dev_ptr, size_t bytes);
+
+/*
+ * lookme_route -- query projection and Level-1 scene routing (Eq. 5).
+ *   x         [n, d_in]            tokens v (vision-encoder outputs), shared by all layers
+ *   w_proj    [layers, d_e, d_in]  W_{v->e} of each layer stored output-row-major
+ *                                  (row j holds column j of the paper's d_in x d_e
+ *                                  matrix), or NULL when the tokens already are
+ *                                  the queries of every layer (then d_in must
+ *                                  equal d_e; q_out may alias x for one layer)
+ *   q_out     [layers, n, d_e]     q = round_to_dtype(x W), float32 accumulation
+ *   scene_out [layers, n] int32    argmax_s <q, scene_keys[s]> + bias[s]
+ * d_in * elem_size must be a multiple of 16 bytes.
+ */
+lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in,
+                             const void* x, const void* w_proj, void* q_out,
+                             int32_t* scene_out, void* stream);
+
+/*
+ * lookme_lookup -- Level-2 scene-primitive retrieval (Eq. 6-7, dot form).
+ *   q        [layers, n, d_e]       queries (q_out of lookme_route)
+ *   scene    [layers, n] int32      scenes in [0, N_s)
+ *   prim_out [layers, n, k] int32   the k primitives p in [0, N_p) of largest
+ *                                   <q, prim_keys[scene, p]>, score-descending
+ *   w_out    [layers, n, k] float32 softmax of those k scores (temperature 1)
+ * Needs a workspace of at least lookme_workspace_size(layers, n).
+ */
+lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void* q,
+                              const int32_t* scene, int32_t* prim_out, float* w_out,
+                              void* stream);
+
+/*
+ * lookme_inject -- sparse injection (Eq. 9-10) and residual add (Eq. 2).
+ *   crit     [layers, n, d_c]   Delta of each layer (the attention update);
+ *                               criticality c_t = ||crit_t||_2
+ *   scene, prim, w              outputs of route and lookup
+ *   hidden   [layers, n, d_h]   H, updated IN PLACE: for the n_keep tokens of
+ *                               largest c_t (ties: lowest t) and j < d_v,
+ *                               H[t,j] <- round(H[t,j] + sum_i w[t,i] *
+ *                               values[scene[t]*N_p + prim[t,i], j]);
+ *                               every other element keeps its bits
+ *   kept_out [layers, n_keep] int32, ascending kept token ids, or NULL
+ * Requires 0 <= n_keep <= n, d_v <= d_h, d_c * elem_size and d_h * elem_size
+ * multiples of 16 bytes.  Needs the workspace of lookme_workspace_size.
+ */
+lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                              const void* crit, int32_t d_c, const int32_t* scene,
+                              const int32_t* prim, const float* w, void* hidden,
+                              int32_t d_h, int32_t* kept_out, void* stream);
+
+/* Release the handle (not the borrowed table or the workspace). NULL is OK. */
+lookme_status_t lookme_destroy(lookme_t h);
+
+/* Message of the last non-OK status returned on this thread ("" if none). */
+const char* lookme_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOOKME_H_ */

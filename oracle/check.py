@@ -35,6 +35,7 @@ class Report:
     decisions: dict = dataclasses.field(default_factory=dict)
     exemptions: dict = dataclasses.field(default_factory=dict)
     failures: list = dataclasses.field(default_factory=list)
+    notes: dict = dataclasses.field(default_factory=dict)
 
     def count(self, kind: str, n: int = 1):
         self.decisions[kind] = self.decisions.get(kind, 0) + n
@@ -59,7 +60,7 @@ class Report:
 
     def __str__(self):
         return (f"decisions={self.decisions} exemptions={self.exemptions} "
-                f"failures={self.failures[:10]}")
+                f"notes={self.notes} failures={self.failures[:10]}")
 
 
 def tie(a: float, b: float, qnorm: float = 0.0) -> bool:
@@ -95,8 +96,7 @@ def ulp_distance(a: np.ndarray, b: np.ndarray, dtype: str) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 def check_q(q_lib, q_orc, dtype: str, rep: Report, max_ulp: int = 1):
-    """C1: every element of the library's q within ``max_ulp`` of the
-    oracle's correctly rounded q."""
+    """C1 (exact copies): every element within ``max_ulp`` of the oracle's."""
     d = ulp_distance(q_lib, q_orc, dtype)
     rep.count("q", d.size)
     bad = int(np.sum(d > max_ulp))
@@ -104,6 +104,29 @@ def check_q(q_lib, q_orc, dtype: str, rep: Report, max_ulp: int = 1):
         i = np.unravel_index(int(np.argmax(d)), d.shape)
         rep.fail(f"q: {bad} elements beyond {max_ulp} ulp (worst {int(d[i])} at {i})")
     return d
+
+
+def check_projection(q_lib, x: np.ndarray, w_t: np.ndarray, dtype: str, rep: Report):
+    """C1 (projection): the library accumulates x . w in float32 and rounds
+    once to ``dtype``.  A float32 sum of d_in exact products differs from the
+    exact sum by at most d_in * 2^-24 * sum_i |x_i w_i| (the standard
+    recursive-summation bound), so the library's value must lie between the
+    roundings of (exact - E) and (exact + E).  Most elements land on the
+    correctly rounded value; the count of those that do not is reported."""
+    exact = x @ w_t.T
+    E = x.shape[1] * 2.0 ** -24 * (np.abs(x) @ np.abs(w_t).T)
+    lo = O.round_to_dtype(exact - E, dtype)
+    hi = O.round_to_dtype(exact + E, dtype)
+    got = O.to_f64(q_lib, dtype)
+    rep.count("q", got.size)
+    bad = (got < lo) | (got > hi)
+    if np.any(bad):
+        i = np.unravel_index(int(np.argmax(bad)), bad.shape)
+        rep.fail(f"q: {int(bad.sum())} elements outside the float32 accumulation bound "
+                 f"(first at {i}: got {got[i]!r}, exact {exact[i]!r}, bound {E[i]!r})")
+    off = int(np.sum(got != O.round_to_dtype(exact, dtype)))
+    rep.notes["q_not_correctly_rounded"] = rep.notes.get("q_not_correctly_rounded", 0) + off
+    return off
 
 
 def check_scene(q: np.ndarray, scene_keys: np.ndarray, bias, score: str,
@@ -239,16 +262,24 @@ def check_kept(c: np.ndarray, n_keep: int, kept_lib: np.ndarray, rep: Report):
 
 def check_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: int,
                  scene: np.ndarray, prim: np.ndarray, w_orc_of, kept: np.ndarray,
-                 rep: Report, tokens=None, contract_abs: float = 2e-2):
-    """C6: recompute the injection with the library's (kept, scene, prim) and
-    the oracle's weights.  Untouched elements must be bit-identical; touched
-    bf16 elements within ``contract_abs`` and 1 ulp of the correctly rounded
-    oracle value; float32 within 1e-5 * (|H| + sum w |V|).
+                 rep: Report, tokens=None, contract_abs: float = 2e-2, w_lib_of=None):
+    """C6: recompute the injection with the library's (kept, scene, prim).
+
+    * Untouched elements (tokens not kept, columns >= d_v) must keep their bits.
+    * Contract, against the oracle's weights: bf16 within ``contract_abs``
+      max-abs; float32 within 1e-5 * (|H| + sum_i w_i |V_i|).
+    * Evaluation bound (bf16), when the library's weights are given: with
+      e = H + sum_i w_lib_i V_i in exact arithmetic, a float32 evaluation
+      (k fused multiply-adds, one add of H) errs by at most
+      E = (k + 1) * 2^-24 * (|H| + sum_i |w_lib_i V_i|), so the stored value
+      must lie between the roundings of e - E and e + E.  (A flat one-ulp rule
+      is wrong where H + R cancels towards zero.)
 
     h_in, h_out_lib : stored arrays [n, d_h] (bf16 bits or float32), or the
                       rows for ``tokens`` when given.
     values_rows(rows) -> float64 [len(rows), d_v]
     w_orc_of(t) -> float64 [k] oracle weights of the library's set for t.
+    w_lib_of(t) -> float32 [k] library weights for t (optional).
     """
     n = h_in.shape[0]
     tokens = np.arange(n) if tokens is None else np.asarray(tokens)
@@ -268,22 +299,33 @@ def check_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: int,
         V = values_rows(rows)
         d_v = V.shape[1]
         w = w_orc_of(int(t))
-        exact = h_in_f[r, :d_v] + np.sum(w[:, None] * V, axis=0)
-        ref = O.round_to_dtype(exact, dtype)
+        H = h_in_f[r, :d_v]
+        exact = H + np.sum(w[:, None] * V, axis=0)
         got = h_lib_f[r, :d_v]
         if not np.array_equal(np.asarray(h_in[r, d_v:]).view(np.uint8),
                               np.asarray(h_out_lib[r, d_v:]).view(np.uint8)):
             rep.fail(f"hidden: row {t} columns >= d_v modified")
         if dtype == "bf16":
-            err = float(np.max(np.abs(got - ref)))
+            err = float(np.max(np.abs(got - O.round_to_dtype(exact, dtype))))
             worst = max(worst, err)
-            ulp = ulp_distance(O.from_f64(got, "bf16"), O.from_f64(ref, "bf16"), "bf16")
             if err > contract_abs:
                 rep.fail(f"hidden[{t}]: max-abs {err:.3g} > {contract_abs}")
-            elif np.any(ulp > 1):
-                rep.fail(f"hidden[{t}]: {int(np.sum(ulp > 1))} elements beyond 1 ulp")
+            if w_lib_of is not None:
+                wl = np.asarray(w_lib_of(int(t)), dtype=np.float64)
+                e = H + np.sum(wl[:, None] * V, axis=0)
+                E = (len(wl) + 1) * 2.0 ** -24 * (np.abs(H) + np.sum(np.abs(wl[:, None] * V),
+                                                                     axis=0))
+                lo = O.round_to_dtype(e - E, dtype)
+                hi = O.round_to_dtype(e + E, dtype)
+                bad = (got < lo) | (got > hi)
+                if np.any(bad):
+                    rep.fail(f"hidden[{t}]: {int(bad.sum())} elements outside the float32 "
+                             f"evaluation bound")
+                off = int(np.sum(got != O.round_to_dtype(e, dtype)))
+                rep.notes["hidden_not_correctly_rounded"] = (
+                    rep.notes.get("hidden_not_correctly_rounded", 0) + off)
         else:
-            bound = 1e-5 * (np.abs(h_in_f[r, :d_v]) + np.sum(np.abs(w[:, None] * V), axis=0))
+            bound = 1e-5 * (np.abs(H) + np.sum(np.abs(w[:, None] * V), axis=0))
             err = np.abs(got - exact)
             worst = max(worst, float(np.max(err)))
             if np.any(err > bound + 1e-30):

@@ -1,0 +1,255 @@
+// Sparse injection (arXiv 2607.16305, Sec. 3.3, Eq. 9-10) and the residual
+// add of Eq. 2: the criticality of token t is ||Delta_t||_2 (the size of the
+// attention update that drives the SKA gate); the n_keep most critical tokens
+// of every layer receive H[t, :d_v] += sum_i w_i * V[scene_t * P + p_i, :].
+//
+//   crit_norm   one wave per row streams Delta once (HBM-bound) and stores
+//               the fp32 sum of squares as its bit pattern (non-negative
+//               floats order like their bits, and the square root keeps the
+//               order, so selecting on it selects on the norm);
+//   crit_select one workgroup per layer: 4-pass MSB-first radix select of
+//               the n_keep-th largest key, then an order-preserving
+//               compaction (ballot prefix sums) of the kept token ids;
+//   inject      one workgroup per kept token: 16-byte coalesced loads of its
+//               k table rows (all in flight together), fp32 weighted sum in
+//               a fixed order, one rounding of H + sum, in-place store.
+#include "common.h"
+#include "kernels.h"
+
+namespace lookme {
+
+constexpr int NORM_WAVES = 4;
+constexpr int SEL_THREADS = 1024;
+constexpr int SEL_WAVES = SEL_THREADS / WAVE;
+constexpr int INJ_THREADS = 256;
+
+template <int DT>
+__global__ __launch_bounds__(NORM_WAVES * WAVE) void crit_norm_kernel(
+    const char* __restrict__ crit, int64_t rows, int64_t row_bytes,
+    uint32_t* __restrict__ key) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * NORM_WAVES + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const char* p = crit + r * row_bytes;
+  const int chunks = (int)(row_bytes / 16);
+  float acc0 = 0.f, acc1 = 0.f;
+  for (int c = lane; c < chunks; c += WAVE) {
+    const u32x4_t v = ld16_nt(p + (int64_t)c * 16);
+    if constexpr (DT == DT_BF16) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = bf16lo(v[e]), hi = bf16hi(v[e]);
+        acc0 = fmaf(lo, lo, acc0);
+        acc1 = fmaf(hi, hi, acc1);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float f = as_f32(v[e]);
+        if (e & 1) acc1 = fmaf(f, f, acc1);
+        else acc0 = fmaf(f, f, acc0);
+      }
+    }
+  }
+  float acc = acc0 + acc1;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d, 64);
+  if (lane == 0) key[r] = as_u32(acc);
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
+    const uint32_t* __restrict__ key_all, int64_t n, int64_t n_keep,
+    int32_t* __restrict__ kept_all) {
+  __shared__ int hist[256];
+  __shared__ uint32_t s_prefix;
+  __shared__ int64_t s_need;
+  __shared__ int wsel[SEL_WAVES], weq[SEL_WAVES];
+  const int layer = blockIdx.x;
+  const uint32_t* key = key_all + (int64_t)layer * n;
+  int32_t* kept = kept_all + (int64_t)layer * n_keep;
+  if (n_keep == 0) return;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+
+  // ---- radix select: the n_keep-th largest key value T -----------------
+  uint32_t prefix = 0, mask = 0;
+  int64_t need = n_keep;   // rank (from the top) still to be located
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < n; i += SEL_THREADS) {
+      const uint32_t k = key[i];
+      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int64_t cum = 0;
+      int d = 255;
+      for (; d > 0; --d) {
+        if (cum + hist[d] >= need) break;
+        cum += hist[d];
+      }
+      s_need = need - cum;
+      s_prefix = prefix | ((uint32_t)d << shift);
+    }
+    __syncthreads();
+    need = s_need;
+    prefix = s_prefix;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  const uint32_t T = prefix;       // keys > T are kept, plus `need` keys == T
+  const int64_t take_eq = need;    // lowest-index ones first
+
+  // ---- order-preserving compaction ------------------------------------------
+  int64_t base_sel = 0, base_eq = 0;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int64_t c0 = 0; c0 < n; c0 += SEL_THREADS) {
+    const int64_t i = c0 + threadIdx.x;
+    const uint32_t k = i < n ? key[i] : 0u;
+    const bool eq = i < n && k == T;
+    const uint64_t meq = __ballot(eq);
+    if (lane == 0) weq[wv] = __popcll(meq);
+    __syncthreads();
+    int64_t eq_before = base_eq + __popcll(meq & below);
+    int64_t tot_eq = 0;
+    for (int w = 0; w < SEL_WAVES; ++w) {
+      if (w < wv) eq_before += weq[w];
+      tot_eq += weq[w];
+    }
+    const bool sel = i < n && (k > T || (eq && eq_before < take_eq));
+    const uint64_t msel = __ballot(sel);
+    if (lane == 0) wsel[wv] = __popcll(msel);
+    __syncthreads();
+    int64_t pos = base_sel + __popcll(msel & below);
+    int64_t tot_sel = 0;
+    for (int w = 0; w < SEL_WAVES; ++w) {
+      if (w < wv) pos += wsel[w];
+      tot_sel += wsel[w];
+    }
+    if (sel && pos < n_keep) kept[pos] = (int32_t)i;   // the count is n_keep by construction
+    base_sel += tot_sel;
+    base_eq += tot_eq;
+    __syncthreads();
+  }
+}
+
+template <int DT, int K>
+__global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
+    int64_t n, int64_t n_keep, const int32_t* __restrict__ kept_all,
+    const int32_t* __restrict__ scene_all, const int32_t* __restrict__ prim_all,
+    const float* __restrict__ w_all, const char* __restrict__ values, int S, int P, int k,
+    int64_t v_bytes, char* __restrict__ hidden, int64_t h_bytes) {
+  const int64_t j = blockIdx.x;
+  const int64_t layer = j / n_keep;
+  int64_t t = kept_all[j];   // [layers, n_keep], row-major
+  t = t < 0 ? 0 : (t >= n ? n - 1 : t);
+  const int64_t row = layer * n + t;
+  int s = scene_all[row];
+  s = s < 0 ? 0 : (s >= S ? S - 1 : s);
+  int64_t vrow[K];
+  float wt[K];
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    if (i < k) {
+      int p = prim_all[row * k + i];
+      p = p < 0 ? 0 : (p >= P ? P - 1 : p);
+      vrow[i] = (int64_t)s * P + p;
+      wt[i] = w_all[row * k + i];
+    } else {
+      vrow[i] = 0;
+      wt[i] = 0.f;
+    }
+  }
+  char* h = hidden + row * h_bytes;
+  const int chunks = (int)(v_bytes / 16);
+  for (int c = threadIdx.x; c < chunks; c += INJ_THREADS) {
+    u32x4_t vv[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+      if (i < k) vv[i] = ld16_nt(values + vrow[i] * v_bytes + (int64_t)c * 16);
+    const u32x4_t hv = ld16(h + (int64_t)c * 16);
+    u32x4_t out;
+    if constexpr (DT == DT_BF16) {
+      float acc[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+#pragma unroll
+      for (int i = 0; i < K; ++i) {
+        if (i < k) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[2 * e] = fmaf(wt[i], bf16lo(vv[i][e]), acc[2 * e]);
+            acc[2 * e + 1] = fmaf(wt[i], bf16hi(vv[i][e]), acc[2 * e + 1]);
+          }
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        out[e] = pack_bf16x2(bf16lo(hv[e]) + acc[2 * e], bf16hi(hv[e]) + acc[2 * e + 1]);
+    } else {
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < K; ++i) {
+        if (i < k) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc[e] = fmaf(wt[i], as_f32(vv[i][e]), acc[e]);
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        out[e] = as_u32(as_f32(hv[e]) + acc[e]);
+    }
+    st16(h + (int64_t)c * 16, out);
+  }
+}
+
+template <int DT>
+static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_t n_keep,
+                            const int32_t* kept, const int32_t* scene, const int32_t* prim,
+                            const float* w, const char* values, int S, int P, int64_t vb,
+                            char* hidden, int64_t hb) {
+#define LOOKME_INJ(K_)                                                                         \
+  hipLaunchKernelGGL((inject_kernel<DT, K_>), grid, dim3(INJ_THREADS), 0, st, n, n_keep, kept, \
+                     scene, prim, w, values, S, P, kk, vb, hidden, hb)
+  if (kk <= 4) LOOKME_INJ(4);
+  else if (kk <= 8) LOOKME_INJ(8);
+  else if (kk <= 16) LOOKME_INJ(16);
+  else LOOKME_INJ(32);
+#undef LOOKME_INJ
+}
+
+hipError_t launch_inject(int dt, int layers, int64_t n, int64_t n_keep, const void* crit,
+                         int d_c, const int32_t* scene, const int32_t* prim, const float* w,
+                         const void* values, int S, int P, int d_v, int k, void* hidden, int d_h,
+                         int32_t* kept_out, const InjectWs& ws, hipStream_t st) {
+  if (n == 0 || layers == 0) return hipSuccess;
+  const int es = dt == DT_BF16 ? 2 : 4;
+  const int64_t rows = (int64_t)layers * n;
+  const int64_t grid_norm = (rows + NORM_WAVES - 1) / NORM_WAVES;
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(crit_norm_kernel<DT_BF16>, dim3((unsigned)grid_norm),
+                       dim3(NORM_WAVES * WAVE), 0, st, static_cast<const char*>(crit), rows,
+                       (int64_t)d_c * es, ws.crit_key);
+  else
+    hipLaunchKernelGGL(crit_norm_kernel<DT_F32>, dim3((unsigned)grid_norm),
+                       dim3(NORM_WAVES * WAVE), 0, st, static_cast<const char*>(crit), rows,
+                       (int64_t)d_c * es, ws.crit_key);
+  if (n_keep == 0) return hipGetLastError();
+  int32_t* kept = kept_out ? kept_out : ws.kept;
+  hipLaunchKernelGGL(crit_select_kernel, dim3(layers), dim3(SEL_THREADS), 0, st, ws.crit_key, n,
+                     n_keep, kept);
+  const dim3 grid((unsigned)(layers * n_keep));
+  if (dt == DT_BF16)
+    launch_inject_k<DT_BF16>(k, grid, st, n, n_keep, kept, scene, prim, w,
+                             static_cast<const char*>(values), S, P, (int64_t)d_v * es,
+                             static_cast<char*>(hidden), (int64_t)d_h * es);
+  else
+    launch_inject_k<DT_F32>(k, grid, st, n, n_keep, kept, scene, prim, w,
+                            static_cast<const char*>(values), S, P, (int64_t)d_v * es,
+                            static_cast<char*>(hidden), (int64_t)d_h * es);
+  return hipGetLastError();
+}
+
+}  // namespace lookme

@@ -1,0 +1,51 @@
+// Host-side launchers of the gfx950 kernels.  Each returns the HIP status of
+// its launches; shapes are validated by the caller (lookme_abi.cpp) before
+// any launcher runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lookme {
+
+// ---- projection: q[l, t, :] = round(x[t, :] . Wt[l]^T) --------------------
+hipError_t launch_project(int dt, const void* x, const void* wt, void* q, int64_t n, int d_in,
+                          int d_e, int layers, hipStream_t st);
+
+// ---- routing: scene[r] = argmax_s <q_r, K1[s]> + bias[s] over rows r -------
+hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
+                        int32_t* scene, int64_t rows, int d_e, int S, hipStream_t st);
+
+// ---- bucketing of rows by scene -----------------------------------------
+struct BucketWs {
+  int32_t* chunk_hist;   // [chunks, S]
+  int32_t* local_rank;   // [rows]
+  int32_t* offsets;      // [S + 1]
+  int32_t* perm;         // [rows]
+  int32_t* unit_scene;   // [max_units]
+  int32_t* unit_begin;   // [max_units]
+  int32_t* unit_count;   // [1]
+  int64_t chunks;
+  int64_t max_units;
+};
+int64_t bucket_chunks(int64_t rows);
+int64_t bucket_max_units(int64_t rows, int S);
+hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, const BucketWs& ws,
+                         hipStream_t st);
+
+// ---- Level-2 scoring of bucketed rows, fused top-k + softmax --------------
+hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
+                         int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st);
+
+// ---- criticality, select and injection ------------------------------------
+struct InjectWs {
+  uint32_t* crit_key;    // [layers, n] squared norm bits
+  int32_t* kept;         // [layers, n] (first n_keep used)
+};
+hipError_t launch_inject(int dt, int layers, int64_t n, int64_t n_keep, const void* crit,
+                         int d_c, const int32_t* scene, const int32_t* prim, const float* w,
+                         const void* values, int S, int P, int d_v, int k, void* hidden, int d_h,
+                         int32_t* kept_out, const InjectWs& ws, hipStream_t st);
+
+}  // namespace lookme

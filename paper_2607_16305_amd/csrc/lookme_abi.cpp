@@ -1,0 +1,309 @@
+// C ABI of the LookME hot path: argument validation, workspace layout and
+// launch sequencing.  All arithmetic happens in the gfx950 kernels; this file
+// only checks arguments (before anything is launched) and enqueues kernels.
+#include "../../include/lookme.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "kernels.h"
+
+struct lookme_s {
+  lookme_desc_t d;
+  const void* scene_keys;
+  const void* prim_keys;
+  const void* values;
+  const float* bias;
+  void* ws;
+  size_t ws_bytes;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+lookme_status_t fail(lookme_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+lookme_status_t fail(lookme_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+lookme_status_t hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return LOOKME_OK;
+  return fail(LOOKME_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline int elem_size(int32_t dt) { return dt == LOOKME_BF16 ? 2 : 4; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
+
+constexpr int32_t MAX_SCENES = 16384;   // bucketing keeps one histogram per chunk in LDS
+
+// Workspace layout for `layers` x `n` rows.
+struct Layout {
+  size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, crit_key,
+      kept, total;
+};
+
+Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n) {
+  const int64_t rows = (int64_t)layers * n;
+  const int64_t chunks = lookme::bucket_chunks(rows);
+  const int64_t units = lookme::bucket_max_units(rows, d.num_scenes);
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += up256(bytes);
+    return at;
+  };
+  L.unit_count = take(256);   // counters first: the region zeroed at set-up
+  L.chunk_hist = take((size_t)chunks * d.num_scenes * 4);
+  L.local_rank = take((size_t)rows * 4);
+  L.offsets = take(((size_t)d.num_scenes + 1) * 4);
+  L.perm = take((size_t)rows * 4);
+  L.unit_scene = take((size_t)units * 4);
+  L.unit_begin = take((size_t)units * 4);
+  L.crit_key = take((size_t)rows * 4);
+  L.kept = take((size_t)rows * 4);
+  L.total = off;
+  return L;
+}
+
+lookme_status_t check_handle(lookme_t h) {
+  if (h == nullptr) return fail(LOOKME_ERR_INVALID, "null handle");
+  return LOOKME_OK;
+}
+
+lookme_status_t check_ptr(const void* p, const char* name) {
+  if (p == nullptr) return fail(LOOKME_ERR_INVALID, "%s is NULL", name);
+  if (!aligned16(p)) return fail(LOOKME_ERR_INVALID, "%s is not 16-byte aligned", name);
+  return LOOKME_OK;
+}
+
+lookme_status_t check_layers_n(int32_t layers, int64_t n) {
+  if (layers < 1) return fail(LOOKME_ERR_INVALID, "layers must be >= 1 (got %d)", layers);
+  if (n < 0) return fail(LOOKME_ERR_INVALID, "n must be >= 0 (got %lld)", (long long)n);
+  if ((int64_t)layers * n > (int64_t)INT32_MAX / 2)
+    return fail(LOOKME_ERR_UNSUPPORTED, "layers * n = %lld exceeds 2^30 rows",
+                (long long)((int64_t)layers * n));
+  return LOOKME_OK;
+}
+
+lookme_status_t check_workspace(lookme_t h, int32_t layers, int64_t n, Layout* L) {
+  *L = layout(h->d, layers, n);
+  if (h->ws == nullptr) return fail(LOOKME_ERR_WORKSPACE, "no workspace set");
+  if (h->ws_bytes < L->total)
+    return fail(LOOKME_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed for %d x %lld rows",
+                h->ws_bytes, L->total, layers, (long long)n);
+  return LOOKME_OK;
+}
+
+#define LOOKME_TRY(expr)                    \
+  do {                                      \
+    lookme_status_t st_ = (expr);           \
+    if (st_ != LOOKME_OK) return st_;       \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* lookme_last_error(void) { return g_err.c_str(); }
+
+lookme_status_t lookme_create(const lookme_desc_t* desc, const void* scene_keys,
+                              const void* prim_keys, const void* values, const float* scene_bias,
+                              lookme_t* out) {
+  if (out == nullptr) return fail(LOOKME_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (desc == nullptr) return fail(LOOKME_ERR_INVALID, "desc is NULL");
+  const lookme_desc_t d = *desc;
+  if (d.dtype != LOOKME_F32 && d.dtype != LOOKME_BF16)
+    return fail(LOOKME_ERR_INVALID, "unknown dtype %d", d.dtype);
+  if (d.score != LOOKME_SCORE_DOT && d.score != LOOKME_SCORE_COS)
+    return fail(LOOKME_ERR_INVALID, "unknown score %d", d.score);
+  if (d.num_scenes < 1 || d.prims_per_scene < 1 || d.key_dim < 1 || d.value_dim < 1)
+    return fail(LOOKME_ERR_INVALID, "table sizes must be positive");
+  if (d.top_k < 1 || d.top_k > d.prims_per_scene)
+    return fail(LOOKME_ERR_INVALID, "top_k %d outside [1, prims_per_scene=%d]", d.top_k,
+                d.prims_per_scene);
+  if (d.top_k > LOOKME_KMAX)
+    return fail(LOOKME_ERR_UNSUPPORTED, "top_k %d above LOOKME_KMAX=%d", d.top_k, LOOKME_KMAX);
+  const int es = elem_size(d.dtype);
+  const int64_t kb = (int64_t)d.key_dim * es;
+  if (kb % 64 != 0 || kb > 2048)
+    return fail(LOOKME_ERR_UNSUPPORTED,
+                "key_dim * elem_size = %lld bytes; must be a multiple of 64 and <= 2048",
+                (long long)kb);
+  if (((int64_t)d.value_dim * es) % 16 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "value_dim * elem_size must be a multiple of 16 bytes");
+  if (d.num_scenes > MAX_SCENES)
+    return fail(LOOKME_ERR_UNSUPPORTED, "num_scenes %d above %d", d.num_scenes, MAX_SCENES);
+  if ((int64_t)d.num_scenes * d.prims_per_scene > (int64_t)INT32_MAX)
+    return fail(LOOKME_ERR_UNSUPPORTED, "num_scenes * prims_per_scene exceeds 2^31 - 1 rows");
+  if (d.score == LOOKME_SCORE_COS)
+    return fail(LOOKME_ERR_UNSUPPORTED, "cosine scoring is not implemented in this build");
+  LOOKME_TRY(check_ptr(scene_keys, "scene_keys"));
+  LOOKME_TRY(check_ptr(prim_keys, "prim_keys"));
+  LOOKME_TRY(check_ptr(values, "values"));
+  if (scene_bias != nullptr && (reinterpret_cast<uintptr_t>(scene_bias) & 3u))
+    return fail(LOOKME_ERR_INVALID, "scene_bias is not 4-byte aligned");
+  lookme_s* h = new (std::nothrow) lookme_s{};
+  if (h == nullptr) return fail(LOOKME_ERR_INVALID, "out of host memory");
+  h->d = d;
+  h->scene_keys = scene_keys;
+  h->prim_keys = prim_keys;
+  h->values = values;
+  h->bias = scene_bias;
+  *out = h;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_destroy(lookme_t h) {
+  delete h;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_tokens,
+                                      size_t* bytes) {
+  LOOKME_TRY(check_handle(h));
+  if (bytes == nullptr) return fail(LOOKME_ERR_INVALID, "bytes is NULL");
+  LOOKME_TRY(check_layers_n(layers, n_tokens));
+  *bytes = layout(h->d, layers, n_tokens).total;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_set_workspace(lookme_t h, void* dev_ptr, size_t bytes) {
+  LOOKME_TRY(check_handle(h));
+  if (dev_ptr == nullptr) return fail(LOOKME_ERR_INVALID, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(dev_ptr) & 255u)
+    return fail(LOOKME_ERR_INVALID, "workspace is not 256-byte aligned");
+  if (bytes < 256) return fail(LOOKME_ERR_WORKSPACE, "workspace below 256 bytes");
+  LOOKME_TRY(hip_status(hipMemset(dev_ptr, 0, 256), "hipMemset(workspace counters)"));
+  h->ws = dev_ptr;
+  h->ws_bytes = bytes;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in, const void* x,
+                             const void* w_proj, void* q_out, int32_t* scene_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  const lookme_desc_t& d = h->d;
+  const int es = elem_size(d.dtype);
+  if (d_in < 1) return fail(LOOKME_ERR_INVALID, "d_in must be positive");
+  if (((int64_t)d_in * es) % 16 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "d_in * elem_size must be a multiple of 16 bytes");
+  if (w_proj == nullptr && d_in != d.key_dim)
+    return fail(LOOKME_ERR_INVALID, "w_proj is NULL but d_in (%d) != key_dim (%d)", d_in,
+                d.key_dim);
+  if (w_proj == nullptr && layers > 1 && q_out == x)
+    return fail(LOOKME_ERR_INVALID, "q_out may alias x only for one layer");
+  if ((int64_t)layers * d.key_dim > (int64_t)INT32_MAX / 2)
+    return fail(LOOKME_ERR_UNSUPPORTED, "layers * key_dim too large");
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(x, "x"));
+  if (w_proj) LOOKME_TRY(check_ptr(w_proj, "w_proj"));
+  LOOKME_TRY(check_ptr(q_out, "q_out"));
+  LOOKME_TRY(check_ptr(scene_out, "scene_out"));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t rows = (int64_t)layers * n;
+  if (w_proj) {
+    LOOKME_TRY(hip_status(
+        lookme::launch_project(d.dtype, x, w_proj, q_out, n, d_in, d.key_dim, layers, st),
+        "projection launch"));
+  } else {
+    // the tokens are the queries of every layer
+    const size_t bytes = (size_t)n * d.key_dim * es;
+    for (int32_t l = 0; l < layers; ++l) {
+      char* dst = static_cast<char*>(q_out) + (size_t)l * bytes;
+      if (dst == x) continue;
+      LOOKME_TRY(hip_status(hipMemcpyAsync(dst, x, bytes, hipMemcpyDeviceToDevice, st),
+                            "copy of queries"));
+    }
+  }
+  return hip_status(lookme::launch_route(d.dtype, q_out, h->scene_keys, h->bias, scene_out, rows,
+                                         d.key_dim, d.num_scenes, st),
+                    "routing launch");
+}
+
+lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void* q,
+                              const int32_t* scene, int32_t* prim_out, float* w_out,
+                              void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(q, "q"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(prim_out, "prim_out"));
+  LOOKME_TRY(check_ptr(w_out, "w_out"));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  const lookme_desc_t& d = h->d;
+  const int64_t rows = (int64_t)layers * n;
+  char* ws = static_cast<char*>(h->ws);
+  lookme::BucketWs b{};
+  b.chunk_hist = reinterpret_cast<int32_t*>(ws + L.chunk_hist);
+  b.local_rank = reinterpret_cast<int32_t*>(ws + L.local_rank);
+  b.offsets = reinterpret_cast<int32_t*>(ws + L.offsets);
+  b.perm = reinterpret_cast<int32_t*>(ws + L.perm);
+  b.unit_scene = reinterpret_cast<int32_t*>(ws + L.unit_scene);
+  b.unit_begin = reinterpret_cast<int32_t*>(ws + L.unit_begin);
+  b.unit_count = reinterpret_cast<int32_t*>(ws + L.unit_count);
+  b.chunks = lookme::bucket_chunks(rows);
+  b.max_units = lookme::bucket_max_units(rows, d.num_scenes);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, b, st),
+                        "bucketing launch"));
+  return hip_status(lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
+                                          d.prims_per_scene, d.top_k, prim_out, w_out, st),
+                    "lookup launch");
+}
+
+lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                              const void* crit, int32_t d_c, const int32_t* scene,
+                              const int32_t* prim, const float* w, void* hidden, int32_t d_h,
+                              int32_t* kept_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  const lookme_desc_t& d = h->d;
+  const int es = elem_size(d.dtype);
+  if (n_keep < 0 || n_keep > n)
+    return fail(LOOKME_ERR_INVALID, "n_keep %lld outside [0, n=%lld]", (long long)n_keep,
+                (long long)n);
+  if (d_c < 1 || d_h < 1) return fail(LOOKME_ERR_INVALID, "d_c and d_h must be positive");
+  if (d.value_dim > d_h)
+    return fail(LOOKME_ERR_INVALID, "value_dim %d exceeds d_h %d", d.value_dim, d_h);
+  if (((int64_t)d_c * es) % 16 != 0 || ((int64_t)d_h * es) % 16 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "d_c and d_h times elem_size must be multiples of 16");
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(crit, "crit"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(prim, "prim"));
+  LOOKME_TRY(check_ptr(w, "w"));
+  LOOKME_TRY(check_ptr(hidden, "hidden"));
+  if (kept_out) LOOKME_TRY(check_ptr(kept_out, "kept_out"));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  char* ws = static_cast<char*>(h->ws);
+  lookme::InjectWs iw{};
+  iw.crit_key = reinterpret_cast<uint32_t*>(ws + L.crit_key);
+  iw.kept = reinterpret_cast<int32_t*>(ws + L.kept);
+  return hip_status(
+      lookme::launch_inject(d.dtype, layers, n, n_keep, crit, d_c, scene, prim, w, h->values,
+                            d.num_scenes, d.prims_per_scene, d.value_dim, d.top_k, hidden, d_h,
+                            kept_out, iw, static_cast<hipStream_t>(stream)),
+      "inject launch");
+}
+
+}  // extern "C"

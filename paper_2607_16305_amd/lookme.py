@@ -1,0 +1,192 @@
+"""Thin ctypes binding of liblookme.so (the C ABI in include/lookme.h).
+
+Argument marshalling only: every step of the path runs in the library's
+gfx950 kernels.  If the library has not been built this module raises on
+first use; there is no other implementation to fall back to.
+
+The functions keep the C names and order of arguments; tensors are torch
+tensors (device memory), converted to raw pointers here.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblookme.so")
+
+LOOKME_OK, LOOKME_ERR_INVALID, LOOKME_ERR_UNSUPPORTED, LOOKME_ERR_WORKSPACE, LOOKME_ERR_HIP = range(5)
+LOOKME_F32, LOOKME_BF16 = 0, 1
+LOOKME_SCORE_DOT, LOOKME_SCORE_COS = 0, 1
+LOOKME_KMAX = 32
+
+STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "HIP"}
+
+EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "lookme_route",
+            "lookme_lookup", "lookme_inject", "lookme_destroy", "lookme_last_error")
+
+
+class LookmeError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"LOOKME_ERR_{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class lookme_desc_t(ctypes.Structure):
+    _fields_ = [("num_scenes", ctypes.c_int32), ("prims_per_scene", ctypes.c_int32),
+                ("key_dim", ctypes.c_int32), ("value_dim", ctypes.c_int32),
+                ("top_k", ctypes.c_int32), ("dtype", ctypes.c_int32), ("score", ctypes.c_int32)]
+
+
+_lib = None
+_vp = ctypes.c_void_p
+
+
+def load():
+    """Load liblookme.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2607_16305_amd.build` (no fallback path exists)")
+    lib = ctypes.CDLL(LIB_PATH)
+    st = ctypes.c_int
+    sig = {
+        "lookme_create": [ctypes.POINTER(lookme_desc_t), _vp, _vp, _vp, _vp, ctypes.POINTER(_vp)],
+        "lookme_workspace_size": [_vp, ctypes.c_int32, ctypes.c_int64,
+                                  ctypes.POINTER(ctypes.c_size_t)],
+        "lookme_set_workspace": [_vp, _vp, ctypes.c_size_t],
+        "lookme_route": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _vp, _vp, _vp, _vp,
+                         _vp],
+        "lookme_lookup": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp],
+        "lookme_inject": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
+                          ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp],
+        "lookme_destroy": [_vp],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = st
+    lib.lookme_last_error.argtypes = []
+    lib.lookme_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != LOOKME_OK:
+        raise LookmeError(status, load().lookme_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+DTYPE_CODE = {torch.float32: LOOKME_F32, torch.bfloat16: LOOKME_BF16}
+
+
+def lookme_create(desc: lookme_desc_t, scene_keys, prim_keys, values, scene_bias=None):
+    """Returns an opaque handle (int).  The table tensors are borrowed."""
+    h = _vp()
+    _check(load().lookme_create(ctypes.byref(desc), _ptr(scene_keys), _ptr(prim_keys),
+                                _ptr(values), _ptr(scene_bias), ctypes.byref(h)))
+    return h.value
+
+
+def lookme_workspace_size(h, layers: int, n_tokens: int) -> int:
+    out = ctypes.c_size_t()
+    _check(load().lookme_workspace_size(h, layers, n_tokens, ctypes.byref(out)))
+    return out.value
+
+
+def lookme_set_workspace(h, ws, nbytes: int):
+    _check(load().lookme_set_workspace(h, _ptr(ws), nbytes))
+
+
+def lookme_route(h, layers, n, d_in, x, w_proj, q_out, scene_out, stream=None):
+    _check(load().lookme_route(h, layers, n, d_in, _ptr(x), _ptr(w_proj), _ptr(q_out),
+                               _ptr(scene_out), _stream(stream)))
+
+
+def lookme_lookup(h, layers, n, q, scene, prim_out, w_out, stream=None):
+    _check(load().lookme_lookup(h, layers, n, _ptr(q), _ptr(scene), _ptr(prim_out),
+                                _ptr(w_out), _stream(stream)))
+
+
+def lookme_inject(h, layers, n, n_keep, crit, d_c, scene, prim, w, hidden, d_h, kept_out=None,
+                  stream=None):
+    _check(load().lookme_inject(h, layers, n, n_keep, _ptr(crit), d_c, _ptr(scene), _ptr(prim),
+                                _ptr(w), _ptr(hidden), d_h, _ptr(kept_out), _stream(stream)))
+
+
+def lookme_destroy(h):
+    if h:
+        _check(load().lookme_destroy(h))
+
+
+def lookme_last_error() -> str:
+    return load().lookme_last_error().decode()
+
+
+class Table:
+    """Convenience owner of a handle plus its workspace (torch device memory)."""
+
+    def __init__(self, scene_keys, prim_keys, values, top_k, scene_bias=None,
+                 score=LOOKME_SCORE_DOT):
+        S, P, d_e = prim_keys.shape
+        self.desc = lookme_desc_t(S, P, d_e, values.shape[1], top_k,
+                                  DTYPE_CODE[prim_keys.dtype], score)
+        self.tensors = (scene_keys, prim_keys, values, scene_bias)   # keep alive
+        self.handle = lookme_create(self.desc, scene_keys, prim_keys, values, scene_bias)
+        self.ws = None
+        self.ws_rows = (0, 0)
+        self.device = prim_keys.device
+
+    def reserve(self, layers: int, n: int):
+        need = lookme_workspace_size(self.handle, layers, n)
+        if self.ws is None or self.ws.numel() < need:
+            self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+            lookme_set_workspace(self.handle, self.ws, self.ws.numel())
+        return need
+
+    def route(self, x, w_proj, q_out, scene_out, layers=1, stream=None):
+        n, d_in = x.shape
+        lookme_route(self.handle, layers, n, d_in, x, w_proj, q_out, scene_out, stream)
+
+    def lookup(self, q, scene, prim_out, w_out, layers=1, stream=None):
+        n = scene.numel() // layers
+        self.reserve(layers, n)
+        lookme_lookup(self.handle, layers, n, q, scene, prim_out, w_out, stream)
+
+    def inject(self, crit, scene, prim, w, hidden, n_keep, kept_out=None, layers=1, stream=None):
+        n = scene.numel() // layers
+        self.reserve(layers, n)
+        lookme_inject(self.handle, layers, n, n_keep, crit, crit.shape[-1], scene, prim, w,
+                      hidden, hidden.shape[-1], kept_out, stream)
+
+    def close(self):
+        if self.handle:
+            lookme_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -192,3 +192,26 @@ def make_inputs(wl: Workload, seed: int, device="cpu") -> dict:
     return dict(workload=wl, x=x, wt=wt, scene_keys=scene_keys, prim_keys=prim_keys,
                 values=values, bias=None, delta=delta, hidden=hidden, labels=labels,
                 k=wl.top_k, n_keep=wl.n_keep)
+
+
+def make_integer_inputs(n: int, S: int, P: int, d_e: int, d_v: int, d_h: int, k: int,
+                        n_keep: int, seed: int, dtype: str = "bf16", device="cpu",
+                        layers: int = 1) -> dict:
+    """Inputs whose scores are small exact integers (entries in {-2..2}), so
+    that many scores tie exactly; queries are used directly (no projection).
+    Exact in fp32 and bf16 arithmetic for d_e <= 256: every tie-break is
+    decided by index alone."""
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[dtype]
+    g = _gen(1000 * seed + 90, 0, dev)
+    ri = lambda shape, lo, hi: torch.randint(lo, hi + 1, shape, generator=g, device=dev,
+                                             dtype=torch.int64).to(dt)
+    x = ri((n, d_e), -2, 2)
+    scene_keys = ri((S, d_e), -1, 1)
+    prim_keys = ri((S, P, d_e), -1, 1)
+    values = ri((S * P, d_v), -3, 3)
+    delta = ri((layers, n, d_h), -1, 1)       # few distinct norms: ties at the cut
+    hidden = ri((layers, n, d_h), -4, 4)
+    return dict(workload=None, x=x, wt=None, scene_keys=scene_keys, prim_keys=prim_keys,
+                values=values, bias=None, delta=delta, hidden=hidden, labels=None, k=k,
+                n_keep=n_keep)

@@ -1,0 +1,125 @@
+"""Test-side driver: runs the library through its C ABI on one workload and
+checks every stage against the oracle (stage-wise, see oracle/check.py).
+
+Used by the GPU tests, the smoke check and the benchmark's parity sample.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import check as C
+from oracle import lookme_oracle as O
+from paper_2607_16305_amd import lookme as lk
+
+
+def to_np(t: torch.Tensor) -> np.ndarray:
+    """Stored representation: bf16 -> uint16 bits, fp32 -> float32, ints as is."""
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def dtype_name(t: torch.Tensor) -> str:
+    return "bf16" if t.dtype == torch.bfloat16 else "f32"
+
+
+def f64(t: torch.Tensor) -> np.ndarray:
+    return O.to_f64(to_np(t), dtype_name(t))
+
+
+class Run:
+    """Outputs of one pass of the path (device tensors) plus the inputs."""
+
+    def __init__(self, inp: dict, n_keep: int | None = None, k: int | None = None,
+                 table: lk.Table | None = None, with_kept=True, stream=None):
+        self.inp = inp
+        x, wt = inp["x"], inp["wt"]
+        self.dev = x.device
+        self.L = inp["hidden"].shape[0]
+        self.n = x.shape[0]
+        self.k = k if k is not None else inp["k"]
+        self.n_keep = n_keep if n_keep is not None else inp["n_keep"]
+        S, P, d_e = inp["prim_keys"].shape
+        self.S, self.P, self.d_e = S, P, d_e
+        self.table = table or lk.Table(inp["scene_keys"], inp["prim_keys"], inp["values"],
+                                       self.k, inp.get("bias"))
+        self.table.reserve(self.L, self.n)
+        L, n = self.L, self.n
+        dt = x.dtype
+        self.q = torch.empty((L, n, d_e), dtype=dt, device=self.dev)
+        self.scene = torch.full((L, n), -7, dtype=torch.int32, device=self.dev)
+        self.prim = torch.full((L, n, self.k), -7, dtype=torch.int32, device=self.dev)
+        self.w = torch.full((L, n, self.k), -7.0, dtype=torch.float32, device=self.dev)
+        self.kept = (torch.full((L, max(self.n_keep, 1)), -7, dtype=torch.int32,
+                                device=self.dev) if with_kept else None)
+        self.h_in = inp["hidden"].clone()
+        self.hidden = inp["hidden"].clone()
+        self.stream = stream
+
+    def run(self):
+        inp, L = self.inp, self.L
+        self.table.route(inp["x"], inp["wt"], self.q, self.scene, layers=L, stream=self.stream)
+        self.table.lookup(self.q, self.scene, self.prim, self.w, layers=L, stream=self.stream)
+        self.table.inject(inp["delta"], self.scene, self.prim, self.w, self.hidden, self.n_keep,
+                          kept_out=self.kept, layers=L, stream=self.stream)
+        return self
+
+
+def check_run(r: Run, tokens=None, layers=None) -> C.Report:
+    """Stage-wise comparison of a finished run against the oracle.
+
+    ``tokens``: None for every token, else an array of token indices that are
+    checked for route/lookup/inject (the kept set is always checked in full,
+    since it is a global selection)."""
+    torch.cuda.synchronize()
+    inp = r.inp
+    dt = dtype_name(inp["x"])
+    rep = C.Report()
+    L = r.L
+    layers = range(L) if layers is None else layers
+    toks = np.arange(r.n) if tokens is None else np.asarray(tokens)
+    K1 = f64(inp["scene_keys"])
+    bias = None if inp.get("bias") is None else inp["bias"].detach().cpu().numpy().astype(np.float64)
+    prim_keys = inp["prim_keys"]
+    values = inp["values"]
+    x64 = f64(inp["x"][torch.as_tensor(toks, device=inp["x"].device)])
+
+    def scene_keys_of(s):
+        return f64(prim_keys[s])
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    for l in layers:
+        # C1: projection of the sampled tokens
+        q_lib_bits = to_np(r.q[l])[toks]
+        if inp["wt"] is not None:
+            C.check_projection(q_lib_bits, x64, f64(inp["wt"][l]), dt, rep)
+        else:
+            C.check_q(q_lib_bits, O.from_f64(x64, dt), dt, rep, max_ulp=0)
+        q_lib = O.to_f64(q_lib_bits, dt)
+        # C2: scene on the library's q
+        scene = to_np(r.scene[l]).astype(np.int64)
+        C.check_scene(q_lib, K1, bias, "dot", scene[toks], rep)
+        # C3/C4: primitives under the library's scene
+        prim = to_np(r.prim[l])
+        w = to_np(r.w[l])
+        w_orc = C.check_prim(q_lib, scene[toks], scene_keys_of, r.k, "dot", prim[toks], w[toks],
+                             rep)
+        w_of = {int(t): w_orc[i] for i, t in enumerate(toks)}
+        # C5: kept set (global)
+        c = O.criticality(f64(inp["delta"][l]))
+        kept_lib = to_np(r.kept[l])[: r.n_keep] if r.kept is not None else None
+        if kept_lib is not None:
+            C.check_kept(c, r.n_keep, kept_lib, rep)
+        kept = kept_lib if kept_lib is not None else O.select(c, r.n_keep)
+        # C6: hidden rows of the sampled tokens
+        tsel = torch.as_tensor(toks, device=r.h_in.device)
+        C.check_hidden(to_np(r.h_in[l][tsel]), to_np(r.hidden[l][tsel]), dt, values_rows, r.P,
+                       scene, prim, lambda t: w_of[t], kept, rep, tokens=toks,
+                       w_lib_of=lambda t: w[t])
+    return rep.finish()

@@ -1,0 +1,135 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry
+point declared in include/lookme.h, and rejects bad arguments before
+anything is launched (fake, aligned device addresses are never touched)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_16305_amd import lookme as lk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lookme.h")
+FAKE = 0x7F0000100000          # 256-byte aligned stand-in address, never dereferenced
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(lookme_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(lk.LIB_PATH):
+        pytest.fail("liblookme.so is not built (run __graft_entry__.build())")
+    return lk.load()
+
+
+def test_exports_every_declared_entry_point(lib):
+    names = _declared()
+    assert set(lk.EXPORTED) == set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def _desc(**kw):
+    d = dict(num_scenes=16, prims_per_scene=64, key_dim=256, value_dim=256, top_k=4,
+             dtype=lk.LOOKME_F32, score=lk.LOOKME_SCORE_DOT)
+    d.update(kw)
+    return lk.lookme_desc_t(**d)
+
+
+def _status(fn):
+    try:
+        fn()
+    except lk.LookmeError as e:
+        return e.status, str(e)
+    return lk.LOOKME_OK, ""
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(top_k=0), lk.LOOKME_ERR_INVALID),
+    (dict(top_k=65), lk.LOOKME_ERR_INVALID),                  # k > P
+    (dict(prims_per_scene=64, top_k=33), lk.LOOKME_ERR_UNSUPPORTED),   # k > KMAX
+    (dict(num_scenes=0), lk.LOOKME_ERR_INVALID),
+    (dict(dtype=7), lk.LOOKME_ERR_INVALID),
+    (dict(key_dim=250), lk.LOOKME_ERR_UNSUPPORTED),           # 1000 B, not a multiple of 64
+    (dict(key_dim=1024), lk.LOOKME_ERR_UNSUPPORTED),          # 4096 B > 2048 B (fp32)
+    (dict(value_dim=3), lk.LOOKME_ERR_UNSUPPORTED),
+    (dict(num_scenes=20000), lk.LOOKME_ERR_UNSUPPORTED),
+    (dict(score=lk.LOOKME_SCORE_COS), lk.LOOKME_ERR_UNSUPPORTED),
+])
+def test_create_rejects(lib, kw, status):
+    st, msg = _status(lambda: lk.lookme_create(_desc(**kw), FAKE, FAKE, FAKE))
+    assert st == status, msg
+    assert msg
+
+
+def test_create_rejects_null_and_misaligned(lib):
+    assert _status(lambda: lk.lookme_create(_desc(), None, FAKE, FAKE))[0] == lk.LOOKME_ERR_INVALID
+    assert _status(lambda: lk.lookme_create(_desc(), FAKE, FAKE + 8, FAKE))[0] == \
+        lk.LOOKME_ERR_INVALID
+
+
+def test_create_destroy_and_workspace_size(lib):
+    h = lk.lookme_create(_desc(), FAKE, FAKE, FAKE)
+    try:
+        a = lk.lookme_workspace_size(h, 1, 256)
+        b = lk.lookme_workspace_size(h, 4, 256)
+        assert 0 < a < b
+        assert lk.lookme_workspace_size(h, 1, 0) >= 256
+        assert _status(lambda: lk.lookme_workspace_size(h, 0, 5))[0] == lk.LOOKME_ERR_INVALID
+        assert _status(lambda: lk.lookme_workspace_size(h, 1, -1))[0] == lk.LOOKME_ERR_INVALID
+    finally:
+        lk.lookme_destroy(h)
+
+
+def test_calls_validate_before_launch(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        # n == 0 is a no-op, even with null pointers
+        assert S(lambda: lk.lookme_route(h, 1, 0, 2048, None, FAKE, None, None, 0)) == lk.LOOKME_OK
+        assert S(lambda: lk.lookme_lookup(h, 1, 0, None, None, None, None, 0)) == lk.LOOKME_OK
+        # null and misaligned pointers
+        assert S(lambda: lk.lookme_route(h, 1, 8, 2048, None, FAKE, FAKE, FAKE, 0)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_route(h, 1, 8, 2048, FAKE + 4, FAKE, FAKE, FAKE, 0)) == \
+            lk.LOOKME_ERR_INVALID
+        # no projection needs d_in == d_e
+        assert S(lambda: lk.lookme_route(h, 1, 8, 2048, FAKE, None, FAKE, FAKE, 0)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_route(h, 1, 8, 100, FAKE, FAKE, FAKE, FAKE, 0)) == \
+            lk.LOOKME_ERR_UNSUPPORTED
+        assert S(lambda: lk.lookme_route(h, 0, 8, 2048, FAKE, FAKE, FAKE, FAKE, 0)) == \
+            lk.LOOKME_ERR_INVALID
+        # lookup and inject need a workspace
+        assert S(lambda: lk.lookme_lookup(h, 1, 8, FAKE, FAKE, FAKE, FAKE, 0)) == \
+            lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: lk.lookme_inject(h, 1, 8, 2, FAKE, 2048, FAKE, FAKE, FAKE, FAKE, 2048,
+                                          None, 0)) == lk.LOOKME_ERR_WORKSPACE
+        # inject argument ranges
+        assert S(lambda: lk.lookme_inject(h, 1, 8, 9, FAKE, 2048, FAKE, FAKE, FAKE, FAKE, 2048,
+                                          None, 0)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_inject(h, 1, 8, -1, FAKE, 2048, FAKE, FAKE, FAKE, FAKE, 2048,
+                                          None, 0)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_inject(h, 1, 8, 2, FAKE, 2048, FAKE, FAKE, FAKE, FAKE, 1024,
+                                          None, 0)) == lk.LOOKME_ERR_INVALID     # d_v > d_h
+        assert S(lambda: lk.lookme_inject(h, 1, 8, 2, FAKE, 2047, FAKE, FAKE, FAKE, FAKE, 2048,
+                                          None, 0)) == lk.LOOKME_ERR_UNSUPPORTED
+        msg = _status(lambda: lk.lookme_inject(h, 1, 8, 9, FAKE, 2048, FAKE, FAKE, FAKE, FAKE,
+                                               2048, None, 0))[1]
+        assert "n_keep" in msg and "n_keep" in lk.lookme_last_error()
+    finally:
+        lk.lookme_destroy(h)
+
+
+def test_null_handle(lib):
+    assert _status(lambda: lk.lookme_workspace_size(None, 1, 1))[0] == lk.LOOKME_ERR_INVALID
+    assert _status(lambda: lk.lookme_route(None, 1, 1, 1, FAKE, FAKE, FAKE, FAKE, 0))[0] == \
+        lk.LOOKME_ERR_INVALID
+    lk.lookme_destroy(None)

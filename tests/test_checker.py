@@ -82,8 +82,13 @@ def test_checker_rejects_planted_mistakes():
     b3[kept[0], 1] = (b3[kept[0], 1].astype(np.int32) + 2).astype(np.uint16)
     rep = C.Report()
     C.check_hidden(O.from_f64(H, "bf16"), b3, "bf16", lambda r: V[r], K2.shape[1], scene, prim,
-                   lambda t: w[t], kept, rep)
+                   lambda t: w[t], kept, rep, w_lib_of=lambda t: w[t].astype(np.float32))
     assert not rep.ok
+    # the untouched result with the library weights passes the evaluation bound
+    rep = C.Report()
+    C.check_hidden(O.from_f64(H, "bf16"), bits, "bf16", lambda r: V[r], K2.shape[1], scene, prim,
+                   lambda t: w[t], kept, rep, w_lib_of=lambda t: w[t])
+    assert rep.ok, str(rep)
 
 
 def test_checker_exempts_true_ties_only():
@@ -114,3 +119,28 @@ def test_ulp_distance():
     a = O.from_f64(np.array([1.0, -1.0, 0.0]), "bf16")
     b = O.from_f64(np.array([1 + 2 ** -7, -1.0 - 2 ** -6, -0.0]), "bf16")
     assert C.ulp_distance(a, b, "bf16").tolist() == [1, 2, 0]
+
+
+def test_projection_bound_accepts_float32_accumulation_and_rejects_errors():
+    """A float32 left-to-right accumulation (what any float32 kernel may do)
+    lies inside the bound even under heavy cancellation; a value one bf16
+    step beyond the bound's rounding is rejected."""
+    rng = np.random.default_rng(7)
+    n, d_in, d_e = 50, 768, 40
+    x = O.round_to_bf16(rng.standard_normal((n, d_in)))
+    w = O.round_to_bf16(rng.standard_normal((d_e, d_in)) / np.sqrt(d_in))
+    acc = np.zeros((n, d_e), dtype=np.float32)
+    for i in range(d_in):
+        acc = (acc + (x[:, i:i + 1] * w[:, i][None, :]).astype(np.float32)).astype(np.float32)
+    lib = O.from_f64(O.round_to_bf16(acc.astype(np.float64)), "bf16")
+    rep = C.Report()
+    C.check_projection(lib, x, w, "bf16", rep)
+    assert rep.ok, str(rep)
+    exact = x @ w.T
+    E = d_in * 2.0 ** -24 * (np.abs(x) @ np.abs(w).T)
+    bad = O.round_to_bf16(exact + E)
+    bad_bits = O.from_f64(bad, "bf16").astype(np.int32)
+    bad_bits[3, 5] += 1 if bad[3, 5] >= 0 else -1       # one step beyond the upper rounding
+    rep = C.Report()
+    C.check_projection(bad_bits.astype(np.uint16), x, w, "bf16", rep)
+    assert not rep.ok

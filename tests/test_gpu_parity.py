@@ -1,0 +1,175 @@
+"""GPU parity: the library (through its C ABI) against the CPU oracle on the
+same seeded inputs, stage by stage (q, scene, primitives, weights, kept set,
+injected hidden states), with the tie rules of oracle/check.py.
+
+Sizes: small shapes that span several 16-row tiles, several 16-key blocks
+per wave and ragged tails, checked on every token; the benchmark workloads
+at full size, checked on sampled tokens (and the full kept set).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import lookme_oracle as O
+from synth import WORKLOADS, Workload, make_inputs, make_integer_inputs
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _announce(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    from paper_2607_16305_amd import lookme as lk
+    lk.load()          # fails loudly if the library was not built
+    yield
+    torch.cuda.synchronize()
+
+
+def _run_check(inp, tokens=None, **kw):
+    from tests.harness import Run, check_run
+    r = Run(inp, **kw).run()
+    rep = check_run(r, tokens=tokens)
+    assert rep.ok, str(rep)
+    return r, rep
+
+
+SMALL = {
+    "bf16_ragged_l2": Workload("bf16_ragged_l2", "bf16", 300, 2, 768, 512, 20, 200, 392, 520,
+                               8, 33, usage="uniform"),
+    "f32_proj_l3": Workload("f32_proj_l3", "f32", 77, 3, 96, 256, 5, 37, 36, 40, 3, 40,
+                            usage="iid"),
+    "bf16_narrow_keys": Workload("bf16_narrow_keys", "bf16", 130, 1, 160, 96, 7, 50, 64, 64,
+                                 5, 50, usage="iid"),
+    "bf16_wide_keys": Workload("bf16_wide_keys", "bf16", 90, 1, 256, 1024, 6, 70, 128, 128, 8,
+                               30, usage="iid"),
+    "bf16_zipf_tiles": Workload("bf16_zipf_tiles", "bf16", 2000, 1, 512, 512, 50, 64, 256, 256,
+                                16, 20, usage="zipf"),
+    "f32_k1": Workload("f32_k1", "f32", 64, 1, 64, 64, 3, 16, 64, 64, 1, 100, usage="iid",
+                       project=False, value_std=1.0),
+    "bf16_k_eq_p": Workload("bf16_k_eq_p", "bf16", 40, 1, 128, 128, 2, 16, 64, 64, 16, 50),
+    "bf16_k32": Workload("bf16_k32", "bf16", 40, 1, 128, 128, 2, 40, 64, 64, 32, 50),
+    "bf16_one_scene": Workload("bf16_one_scene", "bf16", 33, 1, 128, 256, 1, 19, 32, 32, 4, 50),
+    "bf16_one_prim": Workload("bf16_one_prim", "bf16", 21, 1, 64, 64, 9, 1, 16, 16, 1, 50),
+    "bf16_one_token": Workload("bf16_one_token", "bf16", 1, 1, 64, 64, 9, 24, 16, 16, 4, 100),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_workloads_every_token(name):
+    wl = SMALL[name]
+    _announce(f"{name}: {wl}")
+    inp = make_inputs(wl, seed=3, device=DEV)
+    r, rep = _run_check(inp)
+    if wl.usage != "iid" and wl.project:
+        # planted clusters: layer-0 routing recovers the cluster label
+        lab = inp["labels"].cpu().numpy()
+        got = r.scene[0].cpu().numpy()
+        assert np.mean(got == lab) > 0.99
+
+
+def test_tiny_f32_workload_every_token():
+    wl = WORKLOADS[0]
+    _announce(f"config 0: {wl}")
+    _run_check(make_inputs(wl, seed=0, device=DEV))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_integer_scores_tie_break_exactly(dtype):
+    """Exact integer scores: every tie (scene, primitive, kept token) must go
+    to the lowest index, with no tolerance and no exemption."""
+    _announce(f"integer ties {dtype}")
+    inp = make_integer_inputs(n=211, S=7, P=45, d_e=128, d_v=32, d_h=48, k=6, n_keep=70,
+                              seed=5, dtype=dtype, device=DEV, layers=2)
+    _, rep = _run_check(inp)
+    assert not rep.exemptions, rep.exemptions
+
+
+def test_f32_k1_inject_is_one_rounded_add():
+    wl = SMALL["f32_k1"]
+    inp = make_inputs(wl, seed=9, device=DEV)
+    from tests.harness import Run
+    r = Run(inp).run()
+    torch.cuda.synchronize()
+    assert torch.all(r.w == 1.0)
+    s = r.scene[0].long()
+    p = r.prim[0, :, 0].long()
+    rows = inp["values"][s * wl.prims + p]
+    ref = r.h_in[0].clone()
+    ref[:, : wl.d_v] = r.h_in[0][:, : wl.d_v] + rows
+    assert torch.equal(r.hidden[0], ref)
+
+
+def test_edge_counts():
+    from tests.harness import Run
+    wl = SMALL["bf16_ragged_l2"].scaled(layers=1)
+    inp = make_inputs(wl, seed=4, device=DEV)
+    # n_keep = 0 leaves H untouched; n_keep = n touches every row
+    r = Run(inp, n_keep=0).run()
+    torch.cuda.synchronize()
+    assert torch.equal(r.hidden, r.h_in)
+    _run_check(inp, n_keep=wl.n_tokens)
+    # n = 0 is a no-op
+    from paper_2607_16305_amd import lookme as lk
+    t = lk.Table(inp["scene_keys"], inp["prim_keys"], inp["values"], wl.top_k)
+    e = torch.empty(0, device=DEV)
+    t.reserve(1, 0)
+    lk.lookme_route(t.handle, 1, 0, wl.d_e, e, None, e, e)
+    lk.lookme_lookup(t.handle, 1, 0, e, e, e, e)
+    lk.lookme_inject(t.handle, 1, 0, 0, e, wl.d_h, e, e, e, e, wl.d_h)
+    torch.cuda.synchronize()
+
+
+def test_deterministic_reruns():
+    from tests.harness import Run
+    wl = SMALL["bf16_zipf_tiles"]
+    inp = make_inputs(wl, seed=11, device=DEV)
+    a = Run(inp).run()
+    b = Run(inp, table=a.table).run()
+    torch.cuda.synchronize()
+    for name in ("q", "scene", "prim", "w", "kept", "hidden"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+
+
+def test_layers_batched_equal_sequential():
+    from tests.harness import Run
+    wl = SMALL["bf16_ragged_l2"].scaled(layers=3)
+    inp = make_inputs(wl, seed=12, device=DEV)
+    full = Run(inp).run()
+    for l in range(3):
+        one = dict(inp)
+        one["wt"] = inp["wt"][l:l + 1]
+        one["delta"] = inp["delta"][l:l + 1]
+        one["hidden"] = inp["hidden"][l:l + 1]
+        r = Run(one, table=full.table).run()
+        torch.cuda.synchronize()
+        for name in ("q", "scene", "prim", "w", "kept", "hidden"):
+            assert torch.equal(getattr(full, name)[l], getattr(r, name)[0]), (l, name)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_benchmark_workloads_sampled(cfg):
+    """Full-size workloads in the benchmark's launch configuration; sampled
+    tokens are checked stage-wise, the kept set in full."""
+    from tests.harness import Run, check_run
+    wl = WORKLOADS[cfg]
+    _announce(f"config {cfg}: {wl}")
+    inp = make_inputs(wl, seed=cfg, device=DEV)
+    r = Run(inp).run()
+    rng = np.random.default_rng(cfg)
+    kept0 = r.kept[0].cpu().numpy()[: min(48, wl.n_keep)]
+    toks = np.unique(np.concatenate([rng.choice(wl.n_tokens, 80, replace=False), kept0]))
+    rep = check_run(r, tokens=toks)
+    assert rep.ok, str(rep)
+    if wl.usage != "iid":
+        lab = inp["labels"].cpu().numpy()
+        assert np.mean(r.scene[0].cpu().numpy() == lab) > 0.99
+    del inp, r
+    torch.cuda.empty_cache()
