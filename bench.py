@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Throughput of the LookME hot path on one MI355X.
+
+One step = lookme_route + lookme_lookup + lookme_inject over one batch of
+synthetic tokens (projection, Level-1 routing, bucketing, Level-2 top-k
+scoring with softmax, criticality select, row gather and residual add), with
+every input resident in HBM before the timed region starts.  The metric is
+tokens looked up and injected per second, counting tokens x layers.
+
+The default workload is a single image on one layer (1024 tokens, 256 scenes
+x 1024 primitives, 1 GiB table, bf16).  To keep one step from finding the
+previous step's keys in the 256 MiB Infinity Cache, the table is held in
+several copies and consecutive steps use different copies.
+
+Printed: one JSON line with the throughput, the roofline of the dominant
+kernel (Level-2 scoring: its key stream is HBM-bound) measured with HIP
+events inside the library on the launch stream, and the CPU oracle's
+throughput on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload 1] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "multimodal tokens looked up+injected/sec at 1 MI355X; % HBM BW / % MFMA peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=1, help="index into synth.WORKLOADS")
+    ap.add_argument("--copies", type=int, default=0, help="table copies (0: automatic)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=0, help="oracle sample size (0: auto)")
+    return ap.parse_args()
+
+
+class Bench:
+    def __init__(self, wl, seed, copies):
+        import torch
+        from paper_2607_16305_amd import lookme as lk
+        from synth import make_inputs
+        self.torch, self.lk, self.wl = torch, lk, wl
+        self.inp = make_inputs(wl, seed=seed, device="cuda")
+        inp = self.inp
+        table_bytes = sum(inp[k].numel() * inp[k].element_size()
+                          for k in ("scene_keys", "prim_keys", "values"))
+        if copies <= 0:
+            copies = max(1, min(4, (24 << 30) // max(table_bytes, 1)))
+        self.copies = copies
+        self.tables = []
+        for c in range(copies):
+            if c == 0:
+                sk, pk, v = inp["scene_keys"], inp["prim_keys"], inp["values"]
+            else:
+                sk, pk, v = (inp["scene_keys"].clone(), inp["prim_keys"].clone(),
+                             inp["values"].clone())
+            t = lk.Table(sk, pk, v, wl.top_k)
+            t.reserve(wl.layers, wl.n_tokens)
+            self.tables.append(t)
+        L, n, k = wl.layers, wl.n_tokens, wl.top_k
+        dt = inp["x"].dtype
+        dev = inp["x"].device
+        self.q = torch.empty((L, n, wl.d_e), dtype=dt, device=dev)
+        self.scene = torch.empty((L, n), dtype=torch.int32, device=dev)
+        self.prim = torch.empty((L, n, k), dtype=torch.int32, device=dev)
+        self.w = torch.empty((L, n, k), dtype=torch.float32, device=dev)
+        self.kept = torch.empty((L, max(wl.n_keep, 1)), dtype=torch.int32, device=dev)
+        self.hidden = inp["hidden"].clone()
+        self.stream = torch.cuda.current_stream().cuda_stream
+        torch.cuda.synchronize()
+
+    def step(self, i):
+        lk, wl, inp = self.lk, self.wl, self.inp
+        h = self.tables[i % self.copies].handle
+        L, n = wl.layers, wl.n_tokens
+        lk.lookme_route(h, L, n, wl.d_in, inp["x"], inp["wt"], self.q, self.scene, self.stream)
+        lk.lookme_lookup(h, L, n, self.q, self.scene, self.prim, self.w, self.stream)
+        lk.lookme_inject(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.scene, self.prim,
+                         self.w, self.hidden, wl.d_h, self.kept, self.stream)
+
+    def timed(self, steps):
+        torch = self.torch
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            self.step(i)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    def profiled(self, steps):
+        """Per-kernel-group times from the library's HIP events (launch stream)."""
+        lk = self.lk
+        for t in self.tables:
+            lk.lookme_profile_read(t.handle, 0, reset=True)
+            lk.lookme_profile_enable(t.handle, True)
+        self.timed(steps)
+        out = {}
+        for g, name in enumerate(lk.GROUPS):
+            cnt, ms = 0, 0.0
+            for t in self.tables:
+                c, m = lk.lookme_profile_read(t.handle, g)
+                cnt += c
+                ms += m
+            if cnt:
+                out[name] = ms / cnt
+        for t in self.tables:
+            lk.lookme_profile_enable(t.handle, False)
+            lk.lookme_profile_read(t.handle, 0, reset=True)
+        return out   # average milliseconds per launch
+
+    def algorithmic_bytes(self):
+        """Bytes each kernel group must move per launch."""
+        torch, wl = self.torch, self.wl
+        es = self.inp["x"].element_size()
+        L, n, k = wl.layers, wl.n_tokens, wl.top_k
+        rows = L * n
+        nonempty = int(torch.unique(self.scene).numel())
+        keep = L * wl.n_keep
+        b = {}
+        b["project"] = (n * wl.d_in + L * wl.d_e * wl.d_in + rows * wl.d_e) * es
+        b["route"] = (rows * wl.d_e + wl.scenes * wl.d_e) * es + rows * 4
+        b["score"] = (nonempty * wl.prims * wl.d_e * es      # key stream of each used scene
+                      + rows * wl.d_e * es                    # queries
+                      + rows * 4                              # bucketed row ids
+                      + rows * k * 8)                         # prim + weights written
+        b["norm"] = rows * wl.crit_dim * es + rows * 4
+        b["inject"] = keep * (k * wl.d_v * es + 2 * wl.d_v * es + k * 8 + 8)
+        flops = {"project": 2 * n * wl.d_in * L * wl.d_e, "route": 2 * rows * wl.d_e * wl.scenes,
+                 "score": 2 * rows * wl.d_e * wl.prims}
+        return b, flops, nonempty
+
+
+def cpu_baseline(b: "Bench", m: int):
+    """The oracle, unchanged, on the first m tokens of the same workload
+    (single thread); returns tokens/s and details."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import lookme_oracle as O
+    from tests.harness import to_np
+
+    wl, inp = b.wl, b.inp
+    dt = wl.dtype
+    n_keep = (wl.keep_pct * m + 50) // 100
+    x = to_np(inp["x"][:m])
+    wt = None if inp["wt"] is None else to_np(inp["wt"])
+    K1 = to_np(inp["scene_keys"])
+    K2 = to_np(inp["prim_keys"])
+    V = to_np(inp["values"])
+    D = to_np(inp["delta"][:, :m])
+    H = to_np(inp["hidden"][:, :m])
+
+    class Rows:
+        """Table slices converted to float64 on access (the oracle indexes
+        prim_keys[scene] and values[rows] only)."""
+        def __init__(self, a):
+            self.a, self.shape = a, a.shape
+
+        def __getitem__(self, i):
+            return O.to_f64(self.a[i], dt)
+
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        res = O.run(O.to_f64(x, dt), None if wt is None else O.to_f64(wt, dt), O.to_f64(K1, dt),
+                    Rows(K2), Rows(V), None, O.to_f64(D, dt), O.to_f64(H, dt),
+                    k=wl.top_k, n_keep=n_keep, dtype=dt)
+        el = time.perf_counter() - t0
+    assert res["hidden"].shape == (wl.layers, m, wl.d_h)
+    return {"value": wl.layers * m / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {m} of {wl.n_tokens} tokens x {wl.layers} layer(s), whole path "
+                      f"(projection..injection, n_keep={n_keep}), float64 NumPy, 1 thread, "
+                      f"{el:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    from synth import WORKLOADS
+    wl = WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    b = Bench(wl, args.workload, args.copies)
+
+    for i in range(args.warmup):
+        b.step(i)
+    el = b.timed(args.steps)
+    ms_step = el * 1000.0 / args.steps
+    value = wl.layers * wl.n_tokens / (el / args.steps)
+
+    prof = b.profiled(args.steps)
+    bytes_, flops, nonempty = b.algorithmic_bytes()
+    kern = {}
+    for name, ms in prof.items():
+        e = {"avg_us": round(ms * 1000.0, 3)}
+        if name in bytes_:
+            gbs = bytes_[name] / (ms * 1e-3) / 1e9
+            e["gbps"] = round(gbs, 1)
+            e["hbm_frac"] = round(gbs / HBM_PEAK_GBS, 4)
+        if name in flops:
+            e["tflops"] = round(flops[name] / (ms * 1e-3) / 1e12, 2)
+        kern[name] = e
+    score_ms = prof.get("score")
+    achieved = bytes_["score"] / (score_ms * 1e-3) / 1e9 if score_ms else None
+    roofline = {"bound": "hbm", "kernel": "score_kernel (Level-2 scoring + top-k + softmax)",
+                "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
+                "traffic": None, "algorithmic_bytes_per_launch": bytes_["score"],
+                "nonempty_scenes": nonempty}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        m = args.cpu_tokens or min(wl.n_tokens, 1024)
+        cpu = cpu_baseline(b, m)
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "tokens": wl.n_tokens, "layers": wl.layers,
+                   "d_in": wl.d_in, "d_e": wl.d_e, "scenes": wl.scenes, "prims": wl.prims,
+                   "d_v": wl.d_v, "d_h": wl.d_h, "top_k": wl.top_k, "n_keep": wl.n_keep,
+                   "usage": wl.usage, "table_copies": b.copies},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kern,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

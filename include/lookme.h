@@ -145,6 +145,31 @@ lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_k
                               const int32_t* prim, const float* w, void* hidden,
                               int32_t d_h, int32_t* kept_out, void* stream);
 
+/*
+ * Measurement support (not part of the method).  When enabled, each kernel
+ * group that route/lookup/inject launches is bracketed by a pair of HIP timing
+ * events recorded on the call's stream.  lookme_profile_read waits for the
+ * recorded events, adds their durations to per-group totals and returns the
+ * totals since the last reset.  Groups (lookme_group_t):
+ *   PROJECT  query projection GEMM          ROUTE   Level-1 scoring + arg max
+ *   BUCKET   scene bucketing (3 kernels)    SCORE   Level-2 scoring + top-k + softmax
+ *   NORM     criticality norms              SELECT  top-n_keep select + compaction
+ *   INJECT   row gather + residual add
+ * Timing events cost a few microseconds of launch overhead per group; leave
+ * profiling off when measuring end-to-end throughput.
+ */
+typedef enum {
+  LOOKME_GROUP_PROJECT = 0, LOOKME_GROUP_ROUTE = 1, LOOKME_GROUP_BUCKET = 2,
+  LOOKME_GROUP_SCORE = 3, LOOKME_GROUP_NORM = 4, LOOKME_GROUP_SELECT = 5,
+  LOOKME_GROUP_INJECT = 6, LOOKME_GROUP_COUNT = 7
+} lookme_group_t;
+
+lookme_status_t lookme_profile_enable(lookme_t h, int32_t enabled);
+/* count: number of timed launches of `group`; total_ms: their summed time.
+ * reset != 0 clears the totals after reading. */
+lookme_status_t lookme_profile_read(lookme_t h, int32_t group, int64_t* count,
+                                    double* total_ms, int32_t reset);
+
 /* Release the handle (not the borrowed table or the workspace). NULL is OK. */
 lookme_status_t lookme_destroy(lookme_t h);
 

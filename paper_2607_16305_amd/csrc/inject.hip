@@ -220,26 +220,34 @@ static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_
 #undef LOOKME_INJ
 }
 
-hipError_t launch_inject(int dt, int layers, int64_t n, int64_t n_keep, const void* crit,
-                         int d_c, const int32_t* scene, const int32_t* prim, const float* w,
-                         const void* values, int S, int P, int d_v, int k, void* hidden, int d_h,
-                         int32_t* kept_out, const InjectWs& ws, hipStream_t st) {
-  if (n == 0 || layers == 0) return hipSuccess;
+hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uint32_t* key,
+                            hipStream_t st) {
+  if (rows == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
-  const int64_t rows = (int64_t)layers * n;
-  const int64_t grid_norm = (rows + NORM_WAVES - 1) / NORM_WAVES;
+  const dim3 grid((unsigned)((rows + NORM_WAVES - 1) / NORM_WAVES));
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(crit_norm_kernel<DT_BF16>, dim3((unsigned)grid_norm),
-                       dim3(NORM_WAVES * WAVE), 0, st, static_cast<const char*>(crit), rows,
-                       (int64_t)d_c * es, ws.crit_key);
+    hipLaunchKernelGGL(crit_norm_kernel<DT_BF16>, grid, dim3(NORM_WAVES * WAVE), 0, st,
+                       static_cast<const char*>(crit), rows, (int64_t)d_c * es, key);
   else
-    hipLaunchKernelGGL(crit_norm_kernel<DT_F32>, dim3((unsigned)grid_norm),
-                       dim3(NORM_WAVES * WAVE), 0, st, static_cast<const char*>(crit), rows,
-                       (int64_t)d_c * es, ws.crit_key);
-  if (n_keep == 0) return hipGetLastError();
-  int32_t* kept = kept_out ? kept_out : ws.kept;
-  hipLaunchKernelGGL(crit_select_kernel, dim3(layers), dim3(SEL_THREADS), 0, st, ws.crit_key, n,
-                     n_keep, kept);
+    hipLaunchKernelGGL(crit_norm_kernel<DT_F32>, grid, dim3(NORM_WAVES * WAVE), 0, st,
+                       static_cast<const char*>(crit), rows, (int64_t)d_c * es, key);
+  return hipGetLastError();
+}
+
+hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint32_t* key,
+                              int32_t* kept, hipStream_t st) {
+  if (n == 0 || n_keep == 0) return hipSuccess;
+  hipLaunchKernelGGL(crit_select_kernel, dim3(layers), dim3(SEL_THREADS), 0, st, key, n, n_keep,
+                     kept);
+  return hipGetLastError();
+}
+
+hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
+                              const int32_t* scene, const int32_t* prim, const float* w,
+                              const void* values, int S, int P, int d_v, int k, void* hidden,
+                              int d_h, hipStream_t st) {
+  if (n == 0 || n_keep == 0) return hipSuccess;
+  const int es = dt == DT_BF16 ? 2 : 4;
   const dim3 grid((unsigned)(layers * n_keep));
   if (dt == DT_BF16)
     launch_inject_k<DT_BF16>(k, grid, st, n, n_keep, kept, scene, prim, w,

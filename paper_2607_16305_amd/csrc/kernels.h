@@ -39,13 +39,13 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st);
 
 // ---- criticality, select and injection ------------------------------------
-struct InjectWs {
-  uint32_t* crit_key;    // [layers, n] squared norm bits
-  int32_t* kept;         // [layers, n] (first n_keep used)
-};
-hipError_t launch_inject(int dt, int layers, int64_t n, int64_t n_keep, const void* crit,
-                         int d_c, const int32_t* scene, const int32_t* prim, const float* w,
-                         const void* values, int S, int P, int d_v, int k, void* hidden, int d_h,
-                         int32_t* kept_out, const InjectWs& ws, hipStream_t st);
+hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uint32_t* key,
+                            hipStream_t st);
+hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint32_t* key,
+                              int32_t* kept, hipStream_t st);
+hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
+                              const int32_t* scene, const int32_t* prim, const float* w,
+                              const void* values, int S, int P, int d_v, int k, void* hidden,
+                              int d_h, hipStream_t st);
 
 }  // namespace lookme

@@ -11,8 +11,15 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "kernels.h"
+
+// Timing events of one kernel group launch (measurement support only).
+struct TimedLaunch {
+  int group;
+  hipEvent_t start, stop;
+};
 
 struct lookme_s {
   lookme_desc_t d;
@@ -22,6 +29,11 @@ struct lookme_s {
   const float* bias;
   void* ws;
   size_t ws_bytes;
+  bool profiling;
+  std::vector<TimedLaunch> pending;        // recorded, not yet read
+  std::vector<hipEvent_t> spare;           // event pool
+  int64_t prof_count[LOOKME_GROUP_COUNT];
+  double prof_ms[LOOKME_GROUP_COUNT];
 };
 
 namespace {
@@ -109,6 +121,36 @@ lookme_status_t check_workspace(lookme_t h, int32_t layers, int64_t n, Layout* L
   return LOOKME_OK;
 }
 
+hipError_t take_event(lookme_t h, hipEvent_t* ev) {
+  if (!h->spare.empty()) {
+    *ev = h->spare.back();
+    h->spare.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(ev);
+}
+
+// Brackets one kernel group with timing events when profiling is on.
+class Timed {
+ public:
+  Timed(lookme_t h, int group, hipStream_t st) : h_(h), st_(st) {
+    if (!h->profiling) return;
+    t_.group = group;
+    if (take_event(h, &t_.start) != hipSuccess || take_event(h, &t_.stop) != hipSuccess) return;
+    armed_ = hipEventRecord(t_.start, st) == hipSuccess;
+  }
+  ~Timed() {
+    if (!armed_) return;
+    if (hipEventRecord(t_.stop, st_) == hipSuccess) h_->pending.push_back(t_);
+  }
+
+ private:
+  lookme_t h_;
+  hipStream_t st_;
+  TimedLaunch t_{};
+  bool armed_ = false;
+};
+
 #define LOOKME_TRY(expr)                    \
   do {                                      \
     lookme_status_t st_ = (expr);           \
@@ -170,7 +212,46 @@ lookme_status_t lookme_create(const lookme_desc_t* desc, const void* scene_keys,
 }
 
 lookme_status_t lookme_destroy(lookme_t h) {
+  if (h == nullptr) return LOOKME_OK;
+  for (auto& t : h->pending) {
+    (void)hipEventSynchronize(t.stop);
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  for (auto e : h->spare) (void)hipEventDestroy(e);
   delete h;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_profile_enable(lookme_t h, int32_t enabled) {
+  LOOKME_TRY(check_handle(h));
+  h->profiling = enabled != 0;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_profile_read(lookme_t h, int32_t group, int64_t* count, double* total_ms,
+                                    int32_t reset) {
+  LOOKME_TRY(check_handle(h));
+  if (group < 0 || group >= LOOKME_GROUP_COUNT)
+    return fail(LOOKME_ERR_INVALID, "unknown kernel group %d", group);
+  for (auto& t : h->pending) {
+    float ms = 0.f;
+    LOOKME_TRY(hip_status(hipEventSynchronize(t.stop), "hipEventSynchronize"));
+    LOOKME_TRY(hip_status(hipEventElapsedTime(&ms, t.start, t.stop), "hipEventElapsedTime"));
+    h->prof_count[t.group] += 1;
+    h->prof_ms[t.group] += ms;
+    h->spare.push_back(t.start);
+    h->spare.push_back(t.stop);
+  }
+  h->pending.clear();
+  if (count) *count = h->prof_count[group];
+  if (total_ms) *total_ms = h->prof_ms[group];
+  if (reset) {
+    for (int g = 0; g < LOOKME_GROUP_COUNT; ++g) {
+      h->prof_count[g] = 0;
+      h->prof_ms[g] = 0.0;
+    }
+  }
   return LOOKME_OK;
 }
 
@@ -219,6 +300,7 @@ lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t rows = (int64_t)layers * n;
   if (w_proj) {
+    Timed tm(h, LOOKME_GROUP_PROJECT, st);
     LOOKME_TRY(hip_status(
         lookme::launch_project(d.dtype, x, w_proj, q_out, n, d_in, d.key_dim, layers, st),
         "projection launch"));
@@ -232,6 +314,7 @@ lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in
                             "copy of queries"));
     }
   }
+  Timed tm(h, LOOKME_GROUP_ROUTE, st);
   return hip_status(lookme::launch_route(d.dtype, q_out, h->scene_keys, h->bias, scene_out, rows,
                                          d.key_dim, d.num_scenes, st),
                     "routing launch");
@@ -263,8 +346,12 @@ lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void*
   b.chunks = lookme::bucket_chunks(rows);
   b.max_units = lookme::bucket_max_units(rows, d.num_scenes);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, b, st),
-                        "bucketing launch"));
+  {
+    Timed tm(h, LOOKME_GROUP_BUCKET, st);
+    LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, b, st),
+                          "bucketing launch"));
+  }
+  Timed tm(h, LOOKME_GROUP_SCORE, st);
   return hip_status(lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
                                           d.prims_per_scene, d.top_k, prim_out, w_out, st),
                     "lookup launch");
@@ -296,14 +383,26 @@ lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_k
   Layout L;
   LOOKME_TRY(check_workspace(h, layers, n, &L));
   char* ws = static_cast<char*>(h->ws);
-  lookme::InjectWs iw{};
-  iw.crit_key = reinterpret_cast<uint32_t*>(ws + L.crit_key);
-  iw.kept = reinterpret_cast<int32_t*>(ws + L.kept);
-  return hip_status(
-      lookme::launch_inject(d.dtype, layers, n, n_keep, crit, d_c, scene, prim, w, h->values,
-                            d.num_scenes, d.prims_per_scene, d.value_dim, d.top_k, hidden, d_h,
-                            kept_out, iw, static_cast<hipStream_t>(stream)),
-      "inject launch");
+  uint32_t* key = reinterpret_cast<uint32_t*>(ws + L.crit_key);
+  int32_t* kept = kept_out ? kept_out : reinterpret_cast<int32_t*>(ws + L.kept);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  {
+    Timed tm(h, LOOKME_GROUP_NORM, st);
+    LOOKME_TRY(hip_status(lookme::launch_crit_norm(d.dtype, (int64_t)layers * n, crit, d_c, key,
+                                                   st),
+                          "criticality launch"));
+  }
+  if (n_keep == 0) return LOOKME_OK;
+  {
+    Timed tm(h, LOOKME_GROUP_SELECT, st);
+    LOOKME_TRY(hip_status(lookme::launch_crit_select(layers, n, n_keep, key, kept, st),
+                          "select launch"));
+  }
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  return hip_status(lookme::launch_inject_rows(d.dtype, layers, n, n_keep, kept, scene, prim, w,
+                                               h->values, d.num_scenes, d.prims_per_scene,
+                                               d.value_dim, d.top_k, hidden, d_h, st),
+                    "inject launch");
 }
 
 }  // extern "C"

@@ -26,7 +26,10 @@ LOOKME_KMAX = 32
 STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "HIP"}
 
 EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "lookme_route",
-            "lookme_lookup", "lookme_inject", "lookme_destroy", "lookme_last_error")
+            "lookme_lookup", "lookme_inject", "lookme_destroy", "lookme_last_error",
+            "lookme_profile_enable", "lookme_profile_read")
+
+GROUPS = ("project", "route", "bucket", "score", "norm", "select", "inject")
 
 
 class LookmeError(RuntimeError):
@@ -66,6 +69,9 @@ def load():
         "lookme_inject": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
                           ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp],
         "lookme_destroy": [_vp],
+        "lookme_profile_enable": [_vp, ctypes.c_int32],
+        "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+                                ctypes.POINTER(ctypes.c_double), ctypes.c_int32],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -138,6 +144,19 @@ def lookme_inject(h, layers, n, n_keep, crit, d_c, scene, prim, w, hidden, d_h, 
 def lookme_destroy(h):
     if h:
         _check(load().lookme_destroy(h))
+
+
+def lookme_profile_enable(h, enabled: bool):
+    _check(load().lookme_profile_enable(h, 1 if enabled else 0))
+
+
+def lookme_profile_read(h, group: int, reset: bool = False):
+    """(number of timed launches, total milliseconds) of one kernel group."""
+    c = ctypes.c_int64()
+    ms = ctypes.c_double()
+    _check(load().lookme_profile_read(h, group, ctypes.byref(c), ctypes.byref(ms),
+                                      1 if reset else 0))
+    return c.value, ms.value
 
 
 def lookme_last_error() -> str:
