@@ -156,12 +156,78 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_scatter_kernel(
   perm[pos] = (int32_t)t;
 }
 
+// All three passes in one workgroup, for batches of at most one chunk
+// (saves two launches where launch latency dominates).
+__global__ __launch_bounds__(BK_THREADS) void bucket_small_kernel(
+    const int32_t* __restrict__ scene, int64_t rows, int S, int sbits,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ unit_scene,
+    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count) {
+  extern __shared__ int hist[];
+  for (int i = threadIdx.x; i < S; i += BK_THREADS) hist[i] = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int t = threadIdx.x;
+  const bool valid = t < rows;
+  const int s = valid ? clamp_scene(scene[t], S) : 0;
+  uint64_t match = __ballot(valid);
+  for (int b = 0; b < sbits; ++b) {
+    const uint64_t ones = __ballot(valid && ((s >> b) & 1));
+    match &= ((s >> b) & 1) ? ones : ~ones;
+  }
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int rank_in_wave = __popcll(match & below);
+  const int cnt = __popcll(match);
+  int base = 0;
+  for (int w = 0; w < BK_WAVES; ++w) {
+    if (wv == w && valid) {
+      base = hist[s];
+      if (rank_in_wave == 0) hist[s] = base + cnt;
+    }
+    __syncthreads();
+  }
+  const int rank = base + rank_in_wave;
+  // bucket offsets and the tile work list (hist[] becomes the offsets)
+  const int ipt = (S + BK_THREADS - 1) / BK_THREADS;
+  const int s0 = min(S, (int)threadIdx.x * ipt), s1 = min(S, s0 + ipt);
+  int sum_rows = 0, sum_tiles = 0;
+  for (int x = s0; x < s1; ++x) {
+    sum_rows += hist[x];
+    sum_tiles += (hist[x] + TILE_ROWS - 1) / TILE_ROWS;
+  }
+  int pre_rows = sum_rows, pre_tiles = sum_tiles, tot_rows, tot_tiles;
+  block_excl_scan2(pre_rows, pre_tiles, tot_rows, tot_tiles);
+  for (int x = s0; x < s1; ++x) {
+    const int size = hist[x];
+    const int tiles = (size + TILE_ROWS - 1) / TILE_ROWS;
+    hist[x] = pre_rows;
+    offsets[x] = pre_rows;
+    for (int u = 0; u < tiles; ++u) {
+      unit_scene[pre_tiles + u] = x;
+      unit_begin[pre_tiles + u] = pre_rows + u * TILE_ROWS;
+    }
+    pre_rows += size;
+    pre_tiles += tiles;
+  }
+  if (threadIdx.x == 0) {
+    offsets[S] = tot_rows;
+    *unit_count = tot_tiles;
+  }
+  __syncthreads();
+  if (valid) perm[hist[s] + rank] = t;
+}
+
 hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, const BucketWs& ws,
                          hipStream_t st) {
   if (rows == 0) return hipSuccess;
   int sbits = 0;
   while ((1 << sbits) < S) ++sbits;
   const int64_t chunks = bucket_chunks(rows);
+  if (chunks == 1) {
+    hipLaunchKernelGGL(bucket_small_kernel, dim3(1), dim3(BK_THREADS), (size_t)S * sizeof(int),
+                       st, scene, rows, S, sbits, ws.offsets, ws.perm, ws.unit_scene,
+                       ws.unit_begin, ws.unit_count);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(bucket_hist_kernel, dim3((unsigned)chunks), dim3(BK_THREADS),
                      (size_t)S * sizeof(int), st, scene, rows, S, sbits, ws.chunk_hist,
                      ws.local_rank);

@@ -57,80 +57,98 @@ __global__ __launch_bounds__(NORM_WAVES * WAVE) void crit_norm_kernel(
   if (lane == 0) key[r] = as_u32(acc);
 }
 
+// Inclusive prefix sum over the threads of one wave.
+__device__ __forceinline__ int wave_scan_incl(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int o = __shfl_up(v, d, 64);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Inclusive prefix sum over the first `waves` waves of the block (all
+// threads of the block must call it; threads beyond them pass 0).
+template <int MAXW>
+__device__ __forceinline__ int block_scan_incl(int v, int* wsum) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int incl = wave_scan_incl(v);
+  if (lane == 63 && wv < MAXW) wsum[wv] = incl;
+  __syncthreads();
+  int off = 0;
+  for (int w = 0; w < wv && w < MAXW; ++w) off += wsum[w];
+  __syncthreads();
+  return incl + off;
+}
+
 __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
     const uint32_t* __restrict__ key_all, int64_t n, int64_t n_keep,
     int32_t* __restrict__ kept_all) {
   __shared__ int hist[256];
+  __shared__ int wsum[SEL_WAVES];
   __shared__ uint32_t s_prefix;
-  __shared__ int64_t s_need;
-  __shared__ int wsel[SEL_WAVES], weq[SEL_WAVES];
+  __shared__ int s_need;
   const int layer = blockIdx.x;
   const uint32_t* key = key_all + (int64_t)layer * n;
   int32_t* kept = kept_all + (int64_t)layer * n_keep;
   if (n_keep == 0) return;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  // every thread owns a contiguous range of tokens
+  const int64_t per = (n + SEL_THREADS - 1) / SEL_THREADS;
+  const int64_t i0 = min<int64_t>(n, tid * per), i1 = min<int64_t>(n, i0 + per);
 
-  // ---- radix select: the n_keep-th largest key value T -----------------
+  // ---- radix select (MSB first, 8 bits a pass): the n_keep-th largest T ----
   uint32_t prefix = 0, mask = 0;
-  int64_t need = n_keep;   // rank (from the top) still to be located
+  int need = (int)n_keep;   // rank from the top still to be located
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+    if (tid < 256) hist[tid] = 0;
     __syncthreads();
-    for (int64_t i = threadIdx.x; i < n; i += SEL_THREADS) {
+    for (int64_t i = i0; i < i1; ++i) {
       const uint32_t k = key[i];
       if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      int64_t cum = 0;
-      int d = 255;
-      for (; d > 0; --d) {
-        if (cum + hist[d] >= need) break;
-        cum += hist[d];
-      }
-      s_need = need - cum;
-      s_prefix = prefix | ((uint32_t)d << shift);
+    // thread t looks at bin 255 - t: cum = keys in bins >= that bin
+    const int b = 255 - tid;
+    const int h = tid < 256 ? hist[b] : 0;
+    const int cum = block_scan_incl<4>(h, wsum);
+    if (tid < 256 && cum - h < need && need <= cum) {
+      s_prefix = prefix | ((uint32_t)b << shift);
+      s_need = need - (cum - h);
     }
     __syncthreads();
-    need = s_need;
     prefix = s_prefix;
+    need = s_need;
     mask |= 255u << shift;
-    __syncthreads();
   }
-  const uint32_t T = prefix;       // keys > T are kept, plus `need` keys == T
-  const int64_t take_eq = need;    // lowest-index ones first
+  const uint32_t T = prefix;   // kept: keys > T, plus the first `need` keys == T
+  const int take_eq = need;
 
-  // ---- order-preserving compaction ------------------------------------------
-  int64_t base_sel = 0, base_eq = 0;
-  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int64_t c0 = 0; c0 < n; c0 += SEL_THREADS) {
-    const int64_t i = c0 + threadIdx.x;
-    const uint32_t k = i < n ? key[i] : 0u;
-    const bool eq = i < n && k == T;
-    const uint64_t meq = __ballot(eq);
-    if (lane == 0) weq[wv] = __popcll(meq);
-    __syncthreads();
-    int64_t eq_before = base_eq + __popcll(meq & below);
-    int64_t tot_eq = 0;
-    for (int w = 0; w < SEL_WAVES; ++w) {
-      if (w < wv) eq_before += weq[w];
-      tot_eq += weq[w];
+  // ---- order-preserving compaction: one block scan of per-thread counts ----
+  int n_gt = 0, n_eq = 0;
+  for (int64_t i = i0; i < i1; ++i) {
+    const uint32_t k = key[i];
+    n_gt += k > T;
+    n_eq += k == T;
+  }
+  const int gt_before = block_scan_incl<SEL_WAVES>(n_gt, wsum) - n_gt;
+  const int eq_before = block_scan_incl<SEL_WAVES>(n_eq, wsum) - n_eq;
+  int g = gt_before, e = eq_before;
+  for (int64_t i = i0; i < i1; ++i) {
+    const uint32_t k = key[i];
+    if (k > T) {
+      const int pos = g + min(e, take_eq);
+      if (pos < n_keep) kept[pos] = (int32_t)i;
+      ++g;
+    } else if (k == T) {
+      if (e < take_eq) {
+        const int pos = g + e;
+        if (pos < n_keep) kept[pos] = (int32_t)i;
+      }
+      ++e;
     }
-    const bool sel = i < n && (k > T || (eq && eq_before < take_eq));
-    const uint64_t msel = __ballot(sel);
-    if (lane == 0) wsel[wv] = __popcll(msel);
-    __syncthreads();
-    int64_t pos = base_sel + __popcll(msel & below);
-    int64_t tot_sel = 0;
-    for (int w = 0; w < SEL_WAVES; ++w) {
-      if (w < wv) pos += wsel[w];
-      tot_sel += wsel[w];
-    }
-    if (sel && pos < n_keep) kept[pos] = (int32_t)i;   // the count is n_keep by construction
-    base_sel += tot_sel;
-    base_eq += tot_eq;
-    __syncthreads();
   }
 }
 

@@ -1,7 +1,7 @@
 // C ABI of the LookME hot path: argument validation, workspace layout and
 // launch sequencing.  All arithmetic happens in the gfx950 kernels; this file
 // only checks arguments (before anything is launched) and enqueues kernels.
-#include "../../include/lookme.h"
+#include "lookme.h"
 
 #include <hip/hip_runtime.h>
 

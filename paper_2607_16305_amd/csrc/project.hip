@@ -4,8 +4,9 @@
 //
 // C[M, N] = A[M, K] . B[N, K]^T with A = x [n, d_in], B = W^T stacked
 // [layers * d_e, d_in]; C is rounded once to the storage dtype and scattered
-// to q[layer, token, :].  Tiled on LDS for the matrix cores: 128 x 128 output
-// tile per workgroup of 4 waves (each wave 64 x 64 = 4 x 4 MFMA tiles),
+// to q[layer, token, :].  Tiled on LDS for the matrix cores: a BM x BN output
+// tile per workgroup of 4 waves in a 2 x 2 grid (128 x 128, each wave 4 x 4
+// MFMA tiles, when that gives enough tiles to fill the chip; 64 x 64 else),
 // 128-byte K stages double-buffered in LDS (rows padded by 16 bytes so the
 // 16-byte fragment reads of 8 consecutive rows hit distinct banks), the next
 // stage's global loads in flight while the current one is multiplied.
@@ -14,64 +15,68 @@
 
 namespace lookme {
 
-constexpr int PJ_BM = 128, PJ_BN = 128;
 constexpr int PJ_STAGE = 128;                // bytes of K per stage and row
 constexpr int PJ_LD = PJ_STAGE + 16;         // padded LDS row pitch
 constexpr int PJ_THREADS = 256;
 constexpr int PJ_CPR = PJ_STAGE / 16;        // 16-byte chunks per row per stage
-constexpr int PJ_LOADS = PJ_BM * PJ_CPR / PJ_THREADS;  // chunks per thread per operand
 
-template <int DT>
+template <int DT, int BM, int BN>
 __global__ __launch_bounds__(PJ_THREADS) void project_kernel(
     const char* __restrict__ A, const char* __restrict__ B, char* __restrict__ Q, int64_t M,
     int N, int64_t k_bytes, int d_e) {
-  __shared__ __attribute__((aligned(16))) char lds[2][2][PJ_BM * PJ_LD];  // [stage][A|B]
+  constexpr int MI = BM / 32, NJ = BN / 32;  // 16 x 16 MFMA tiles per wave
+  constexpr int LA = BM * PJ_CPR / PJ_THREADS, LB = BN * PJ_CPR / PJ_THREADS;
+  __shared__ __attribute__((aligned(16))) char lds_a[2][BM * PJ_LD];
+  __shared__ __attribute__((aligned(16))) char lds_b[2][BN * PJ_LD];
   constexpr int ES = DT == DT_BF16 ? 2 : 4;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wv = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
-  const int wm = (wv >> 1) * 64, wn = (wv & 1) * 64;
+  const int wm = (wv >> 1) * (BM / 2), wn = (wv & 1) * (BN / 2);
 
-  const int64_t tiles_n = (N + PJ_BN - 1) / PJ_BN;
-  const int64_t m0 = (int64_t)(blockIdx.x / tiles_n) * PJ_BM;
-  const int n0 = (int)(blockIdx.x % tiles_n) * PJ_BN;
+  const int64_t tiles_n = (N + BN - 1) / BN;
+  const int64_t m0 = (int64_t)(blockIdx.x / tiles_n) * BM;
+  const int n0 = (int)(blockIdx.x % tiles_n) * BN;
   const int kchunks = (int)(k_bytes / 16);
   const int nstages = (int)((k_bytes + PJ_STAGE - 1) / PJ_STAGE);
 
-  // global chunk indices owned by this thread (same for A and B)
-  int lrow[PJ_LOADS], lcol[PJ_LOADS];
-#pragma unroll
-  for (int r = 0; r < PJ_LOADS; ++r) {
-    const int ci = tid + r * PJ_THREADS;
-    lrow[r] = ci / PJ_CPR;
-    lcol[r] = ci % PJ_CPR;
-  }
-  u32x4_t ra[PJ_LOADS], rb[PJ_LOADS];
+  u32x4_t ra[LA], rb[LB];
   auto gload = [&](int stage) {
 #pragma unroll
-    for (int r = 0; r < PJ_LOADS; ++r) {
-      const int kc = stage * PJ_CPR + lcol[r];
-      const int64_t am = m0 + lrow[r];
-      const int bn = n0 + lrow[r];
+    for (int r = 0; r < LA; ++r) {
+      const int ci = tid + r * PJ_THREADS;
+      const int kc = stage * PJ_CPR + ci % PJ_CPR;
+      const int64_t am = m0 + ci / PJ_CPR;
       ra[r] = (am < M && kc < kchunks) ? ld16(A + am * k_bytes + (int64_t)kc * 16)
                                        : u32x4_t{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int r = 0; r < LB; ++r) {
+      const int ci = tid + r * PJ_THREADS;
+      const int kc = stage * PJ_CPR + ci % PJ_CPR;
+      const int bn = n0 + ci / PJ_CPR;
       rb[r] = (bn < N && kc < kchunks) ? ld16(B + (int64_t)bn * k_bytes + (int64_t)kc * 16)
                                        : u32x4_t{0, 0, 0, 0};
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int r = 0; r < PJ_LOADS; ++r) {
-      st16(&lds[buf][0][lrow[r] * PJ_LD + lcol[r] * 16], ra[r]);
-      st16(&lds[buf][1][lrow[r] * PJ_LD + lcol[r] * 16], rb[r]);
+    for (int r = 0; r < LA; ++r) {
+      const int ci = tid + r * PJ_THREADS;
+      st16(&lds_a[buf][(ci / PJ_CPR) * PJ_LD + (ci % PJ_CPR) * 16], ra[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < LB; ++r) {
+      const int ci = tid + r * PJ_THREADS;
+      st16(&lds_b[buf][(ci / PJ_CPR) * PJ_LD + (ci % PJ_CPR) * 16], rb[r]);
     }
   };
 
-  f32x4_t acc[4][4];
+  f32x4_t acc[MI][NJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   gload(0);
   lstore(0);
@@ -81,18 +86,19 @@ __global__ __launch_bounds__(PJ_THREADS) void project_kernel(
     if (st + 1 < nstages) gload(st + 1);
 #pragma unroll
     for (int s = 0; s < PJ_STAGE / 64; ++s) {
-      u32x4_t fa[4], fb[4];
+      u32x4_t fa[MI], fb[NJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < MI; ++i)
         fa[i] = *reinterpret_cast<const u32x4_t*>(
-            &lds[buf][0][(wm + 16 * i + n16) * PJ_LD + (4 * s + g) * 16]);
-        fb[i] = *reinterpret_cast<const u32x4_t*>(
-            &lds[buf][1][(wn + 16 * i + n16) * PJ_LD + (4 * s + g) * 16]);
-      }
+            &lds_a[buf][(wm + 16 * i + n16) * PJ_LD + (4 * s + g) * 16]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < NJ; ++j)
+        fb[j] = *reinterpret_cast<const u32x4_t*>(
+            &lds_b[buf][(wn + 16 * j + n16) * PJ_LD + (4 * s + g) * 16]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_chunk<DT>(fa[i], fb[j], acc[i][j]);
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_chunk<DT>(fa[i], fb[j], acc[i][j]);
     }
     if (st + 1 < nstages) {
       // the other buffer was last read in the previous stage, which every
@@ -105,13 +111,13 @@ __global__ __launch_bounds__(PJ_THREADS) void project_kernel(
   // lane holds C[m0 + wm + 16i + 4g + r][n0 + wn + 16j + n16]
   const int64_t layer_stride = M * d_e;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     const int col = n0 + wn + 16 * j + n16;
     if (col >= N) continue;
     const int layer = col / d_e, jj = col % d_e;
     char* qcol = Q + ((int64_t)layer * layer_stride + jj) * ES;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MI; ++i) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t row = m0 + wm + 16 * i + 4 * g + r;
@@ -127,21 +133,30 @@ __global__ __launch_bounds__(PJ_THREADS) void project_kernel(
   }
 }
 
+template <int DT, int BM, int BN>
+static void launch_tiles(const void* x, const void* wt, void* q, int64_t n, int N, int64_t kb,
+                         int d_e, hipStream_t st) {
+  const int64_t tiles = ((n + BM - 1) / BM) * ((N + BN - 1) / BN);
+  hipLaunchKernelGGL((project_kernel<DT, BM, BN>), dim3((unsigned)tiles), dim3(PJ_THREADS), 0,
+                     st, static_cast<const char*>(x), static_cast<const char*>(wt),
+                     static_cast<char*>(q), n, N, kb, d_e);
+}
+
 hipError_t launch_project(int dt, const void* x, const void* wt, void* q, int64_t n, int d_in,
                           int d_e, int layers, hipStream_t st) {
   if (n == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const int N = layers * d_e;
-  const int64_t tiles = ((n + PJ_BM - 1) / PJ_BM) * ((N + PJ_BN - 1) / PJ_BN);
   const int64_t kb = (int64_t)d_in * es;
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL(project_kernel<DT_BF16>, dim3((unsigned)tiles), dim3(PJ_THREADS), 0, st,
-                       static_cast<const char*>(x), static_cast<const char*>(wt),
-                       static_cast<char*>(q), n, N, kb, d_e);
-  else
-    hipLaunchKernelGGL(project_kernel<DT_F32>, dim3((unsigned)tiles), dim3(PJ_THREADS), 0, st,
-                       static_cast<const char*>(x), static_cast<const char*>(wt),
-                       static_cast<char*>(q), n, N, kb, d_e);
+  // 128 x 128 tiles when there are enough of them to occupy every CU twice
+  const bool big = ((n + 127) / 128) * ((N + 127) / 128) >= 512;
+  if (dt == DT_BF16) {
+    if (big) launch_tiles<DT_BF16, 128, 128>(x, wt, q, n, N, kb, d_e, st);
+    else launch_tiles<DT_BF16, 64, 64>(x, wt, q, n, N, kb, d_e, st);
+  } else {
+    if (big) launch_tiles<DT_F32, 128, 128>(x, wt, q, n, N, kb, d_e, st);
+    else launch_tiles<DT_F32, 64, 64>(x, wt, q, n, N, kb, d_e, st);
+  }
   return hipGetLastError();
 }
 
