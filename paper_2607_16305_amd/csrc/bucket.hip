@@ -6,8 +6,9 @@
 //      rank among equal-scene rows earlier in the chunk (wave match masks
 //      built from ballots over the scene bits, then the 16 waves in order);
 //   2. one workgroup: per-scene prefix over chunks, exclusive scan over
-//      scenes (wavefront prefix sums) giving bucket offsets, and the work
-//      list of 16-row tiles of every non-empty bucket;
+//      scenes (wavefront prefix sums) giving bucket offsets, and the Level-2
+//      work list (a bucket of <= 16 rows is one streaming unit, a larger one
+//      is cut into shared units of <= 128 rows);
 //   3. per chunk: perm[offset + chunk prefix + rank] = row.
 // Within a bucket rows keep ascending order.  Scene values outside [0, S)
 // are clamped (results for such rows are undefined; memory stays in bounds).
@@ -20,7 +21,32 @@ namespace lookme {
 
 constexpr int BK_THREADS = 1024;
 constexpr int BK_WAVES = BK_THREADS / WAVE;
-constexpr int TILE_ROWS = 16;
+constexpr int TILE_ROWS = UNIT_STREAM_ROWS;
+
+// Shared and streaming work units of a bucket of `size` rows.
+__device__ __forceinline__ int shared_units(int size, int shared_rows) {
+  return size > UNIT_STREAM_ROWS ? (size + shared_rows - 1) / shared_rows : 0;
+}
+__device__ __forceinline__ int stream_units(int size) {
+  return (size > 0 && size <= UNIT_STREAM_ROWS) ? 1 : 0;
+}
+
+// Writes the units of scene s: shared ones at index sh, a streaming one at st.
+__device__ __forceinline__ void write_units(int s, int offset, int size, int sh, int st,
+                                            int shared_rows, int32_t* unit_scene,
+                                            int32_t* unit_begin) {
+  if (size == 0) return;
+  if (size <= UNIT_STREAM_ROWS) {
+    unit_scene[st] = s;
+    unit_begin[st] = offset;
+    return;
+  }
+  const int units = shared_units(size, shared_rows);
+  for (int u = 0; u < units; ++u) {
+    unit_scene[sh + u] = s | UNIT_SHARED;
+    unit_begin[sh + u] = offset + u * shared_rows;
+  }
+}
 
 int64_t bucket_chunks(int64_t rows) { return (rows + BK_THREADS - 1) / BK_THREADS; }
 
@@ -76,29 +102,67 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-// Exclusive block prefix of (a, b) pairs over the block's threads; returns
-// the totals through the references.
-__device__ __forceinline__ void block_excl_scan2(int& a, int& b, int& tot_a, int& tot_b) {
-  __shared__ int wa[BK_WAVES], wb[BK_WAVES];
+// Exclusive block prefix of three counters over the block's threads; returns
+// the totals through `tot`.
+__device__ __forceinline__ void block_excl_scan3(int (&v)[3], int (&tot)[3]) {
+  __shared__ int ws[3][BK_WAVES];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int ia = wave_incl_scan(a), ib = wave_incl_scan(b);
-  if (lane == 63) { wa[wv] = ia; wb[wv] = ib; }
-  __syncthreads();
-  int pa = 0, pb = 0;
-  tot_a = 0;
-  tot_b = 0;
-  for (int w = 0; w < BK_WAVES; ++w) {
-    if (w < wv) { pa += wa[w]; pb += wb[w]; }
-    tot_a += wa[w];
-    tot_b += wb[w];
+  int inc[3];
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    inc[c] = wave_incl_scan(v[c]);
+    if (lane == 63) ws[c][wv] = inc[c];
   }
-  a = pa + ia - a;
-  b = pb + ib - b;
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    int pre = 0;
+    tot[c] = 0;
+    for (int w = 0; w < BK_WAVES; ++w) {
+      if (w < wv) pre += ws[c][w];
+      tot[c] += ws[c][w];
+    }
+    v[c] = pre + inc[c] - v[c];
+  }
   __syncthreads();
 }
 
+// Offsets of the buckets [s0, s1) given their sizes in size_of(s), and the
+// work list: returns the unit count through *unit_count (thread 0).
+template <typename SizeOf, typename SetOffset>
+__device__ __forceinline__ void offsets_and_units(int S, int shared_rows, SizeOf size_of,
+                                                  SetOffset set_offset, int32_t* offsets,
+                                                  int32_t* unit_scene, int32_t* unit_begin,
+                                                  int32_t* unit_count) {
+  const int ipt = (S + BK_THREADS - 1) / BK_THREADS;
+  const int s0 = min(S, (int)threadIdx.x * ipt), s1 = min(S, s0 + ipt);
+  int v[3] = {0, 0, 0};   // rows, shared units, streaming units
+  for (int s = s0; s < s1; ++s) {
+    const int size = size_of(s);
+    v[0] += size;
+    v[1] += shared_units(size, shared_rows);
+    v[2] += stream_units(size);
+  }
+  int tot[3];
+  block_excl_scan3(v, tot);
+  int row = v[0], sh = v[1], st = tot[1] + v[2];
+  for (int s = s0; s < s1; ++s) {
+    const int size = size_of(s);
+    set_offset(s, row);
+    write_units(s, row, size, sh, st, shared_rows, unit_scene, unit_begin);
+    row += size;
+    sh += shared_units(size, shared_rows);
+    st += stream_units(size);
+  }
+  if (threadIdx.x == 0) {
+    offsets[S] = tot[0];
+    *unit_count = tot[1] + tot[2];
+  }
+}
+
 __global__ __launch_bounds__(BK_THREADS) void bucket_scan_kernel(
-    int32_t* __restrict__ chunk_hist, int64_t chunks, int S, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ chunk_hist, int64_t chunks, int S, int shared_rows,
+    int32_t* __restrict__ offsets,
     int32_t* __restrict__ unit_scene, int32_t* __restrict__ unit_begin,
     int32_t* __restrict__ unit_count) {
   // 1. per-scene prefix over chunks; bucket sizes go to offsets[] for now
@@ -118,31 +182,10 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_scan_kernel(
     offsets[s] = run;
   }
   __syncthreads();
-  // 2. exclusive scan of sizes and of tile counts over scenes
-  const int ipt = (S + BK_THREADS - 1) / BK_THREADS;
-  const int s0 = min(S, (int)threadIdx.x * ipt), s1 = min(S, s0 + ipt);
-  int sum_rows = 0, sum_tiles = 0;
-  for (int s = s0; s < s1; ++s) {
-    sum_rows += offsets[s];
-    sum_tiles += (offsets[s] + TILE_ROWS - 1) / TILE_ROWS;
-  }
-  int pre_rows = sum_rows, pre_tiles = sum_tiles, tot_rows, tot_tiles;
-  block_excl_scan2(pre_rows, pre_tiles, tot_rows, tot_tiles);
-  for (int s = s0; s < s1; ++s) {
-    const int size = offsets[s];
-    const int tiles = (size + TILE_ROWS - 1) / TILE_ROWS;
-    offsets[s] = pre_rows;
-    for (int t = 0; t < tiles; ++t) {
-      unit_scene[pre_tiles + t] = s;
-      unit_begin[pre_tiles + t] = pre_rows + t * TILE_ROWS;
-    }
-    pre_rows += size;
-    pre_tiles += tiles;
-  }
-  if (threadIdx.x == 0) {
-    offsets[S] = tot_rows;
-    *unit_count = tot_tiles;
-  }
+  // 2. exclusive scan of the sizes over scenes: offsets and the work list
+  offsets_and_units(
+      S, shared_rows, [&](int s) { return offsets[s]; },
+      [&](int s, int off) { offsets[s] = off; }, offsets, unit_scene, unit_begin, unit_count);
 }
 
 __global__ __launch_bounds__(BK_THREADS) void bucket_scatter_kernel(
@@ -159,7 +202,7 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_scatter_kernel(
 // All three passes in one workgroup, for batches of at most one chunk
 // (saves two launches where launch latency dominates).
 __global__ __launch_bounds__(BK_THREADS) void bucket_small_kernel(
-    const int32_t* __restrict__ scene, int64_t rows, int S, int sbits,
+    const int32_t* __restrict__ scene, int64_t rows, int S, int sbits, int shared_rows,
     int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ unit_scene,
     int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count) {
   extern __shared__ int hist[];
@@ -186,45 +229,27 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_small_kernel(
     __syncthreads();
   }
   const int rank = base + rank_in_wave;
-  // bucket offsets and the tile work list (hist[] becomes the offsets)
-  const int ipt = (S + BK_THREADS - 1) / BK_THREADS;
-  const int s0 = min(S, (int)threadIdx.x * ipt), s1 = min(S, s0 + ipt);
-  int sum_rows = 0, sum_tiles = 0;
-  for (int x = s0; x < s1; ++x) {
-    sum_rows += hist[x];
-    sum_tiles += (hist[x] + TILE_ROWS - 1) / TILE_ROWS;
-  }
-  int pre_rows = sum_rows, pre_tiles = sum_tiles, tot_rows, tot_tiles;
-  block_excl_scan2(pre_rows, pre_tiles, tot_rows, tot_tiles);
-  for (int x = s0; x < s1; ++x) {
-    const int size = hist[x];
-    const int tiles = (size + TILE_ROWS - 1) / TILE_ROWS;
-    hist[x] = pre_rows;
-    offsets[x] = pre_rows;
-    for (int u = 0; u < tiles; ++u) {
-      unit_scene[pre_tiles + u] = x;
-      unit_begin[pre_tiles + u] = pre_rows + u * TILE_ROWS;
-    }
-    pre_rows += size;
-    pre_tiles += tiles;
-  }
-  if (threadIdx.x == 0) {
-    offsets[S] = tot_rows;
-    *unit_count = tot_tiles;
-  }
+  // bucket offsets and the work list (hist[] becomes the offsets)
+  offsets_and_units(
+      S, shared_rows, [&](int x) { return hist[x]; },
+      [&](int x, int off) {
+        hist[x] = off;
+        offsets[x] = off;
+      },
+      offsets, unit_scene, unit_begin, unit_count);
   __syncthreads();
   if (valid) perm[hist[s] + rank] = t;
 }
 
-hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, const BucketWs& ws,
-                         hipStream_t st) {
+hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, int shared_rows,
+                         const BucketWs& ws, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   int sbits = 0;
   while ((1 << sbits) < S) ++sbits;
   const int64_t chunks = bucket_chunks(rows);
   if (chunks == 1) {
     hipLaunchKernelGGL(bucket_small_kernel, dim3(1), dim3(BK_THREADS), (size_t)S * sizeof(int),
-                       st, scene, rows, S, sbits, ws.offsets, ws.perm, ws.unit_scene,
+                       st, scene, rows, S, sbits, shared_rows, ws.offsets, ws.perm, ws.unit_scene,
                        ws.unit_begin, ws.unit_count);
     return hipGetLastError();
   }
@@ -232,7 +257,7 @@ hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, const Bucket
                      (size_t)S * sizeof(int), st, scene, rows, S, sbits, ws.chunk_hist,
                      ws.local_rank);
   hipLaunchKernelGGL(bucket_scan_kernel, dim3(1), dim3(BK_THREADS), 0, st, ws.chunk_hist, chunks,
-                     S, ws.offsets, ws.unit_scene, ws.unit_begin, ws.unit_count);
+                     S, shared_rows, ws.offsets, ws.unit_scene, ws.unit_begin, ws.unit_count);
   hipLaunchKernelGGL(bucket_scatter_kernel, dim3((unsigned)chunks), dim3(BK_THREADS), 0, st,
                      scene, rows, S, ws.chunk_hist, ws.local_rank, ws.offsets, ws.perm);
   return hipGetLastError();

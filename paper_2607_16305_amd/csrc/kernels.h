@@ -18,6 +18,21 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
                         int32_t* scene, int64_t rows, int d_e, int S, hipStream_t st);
 
 // ---- bucketing of rows by scene -----------------------------------------
+// Level-2 work units: a bucket of at most UNIT_STREAM_ROWS rows is one
+// streaming unit; a larger bucket is cut into shared units of at most
+// shared_unit_rows() rows, tagged with UNIT_SHARED in unit_scene.  The work
+// list holds every shared unit first (they are the long ones), then the
+// streaming units, each part in scene order.
+constexpr int UNIT_STREAM_ROWS = 16;
+constexpr int32_t UNIT_SHARED = 1 << 30;
+// Rows of a shared unit: each of its 4 waves keeps two 16-row query tiles in
+// registers when a key row is at most 1 KiB and k <= 8, one tile otherwise
+// (two 32-step tiles would need 64 fragment loads in flight, more than the
+// 6-bit vector-memory counter of a wave can track; with k = 16 the two tiles'
+// candidate lists would halve the waves a SIMD can hold).
+inline int shared_unit_rows(int64_t row_bytes, int k) {
+  return (row_bytes <= 1024 && k <= 8) ? 128 : 64;
+}
 struct BucketWs {
   int32_t* chunk_hist;   // [chunks, S]
   int32_t* local_rank;   // [rows]
@@ -31,8 +46,8 @@ struct BucketWs {
 };
 int64_t bucket_chunks(int64_t rows);
 int64_t bucket_max_units(int64_t rows, int S);
-hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, const BucketWs& ws,
-                         hipStream_t st);
+hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, int shared_rows,
+                         const BucketWs& ws, hipStream_t st);
 
 // ---- Level-2 scoring of bucketed rows, fused top-k + softmax --------------
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,

@@ -348,7 +348,9 @@ lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void*
   hipStream_t st = static_cast<hipStream_t>(stream);
   {
     Timed tm(h, LOOKME_GROUP_BUCKET, st);
-    LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, b, st),
+    const int shared_rows =
+        lookme::shared_unit_rows((int64_t)d.key_dim * elem_size(d.dtype), d.top_k);
+    LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, shared_rows, b, st),
                           "bucketing launch"));
   }
   Timed tm(h, LOOKME_GROUP_SCORE, st);

@@ -1,24 +1,34 @@
-// Streaming key-scoring kernels: Level-1 routing (Eq. 5, fused arg max) and
-// Level-2 primitive scoring over scene buckets (Eq. 6-7 in the dot form,
-// fused top-k and softmax).  arXiv 2607.16305, Sec. 3.2.
+// Key-scoring kernels: Level-1 routing (Eq. 5, fused arg max) and Level-2
+// primitive scoring over scene buckets (Eq. 6-7 in the dot form, fused
+// top-k and softmax).  arXiv 2607.16305, Sec. 3.2.
 //
-// Work unit = up to 16 query rows that share one key set (all rows for
-// routing; one scene's bucket tile for Level-2).  The unit's key set is
-// split over the NW waves of the workgroup; each wave streams 16-key blocks
-// straight from HBM into registers (the next block's chunk is requested as
-// soon as the current one has been consumed by the MFMA), computes a
-// 16 keys x 16 rows score tile on the matrix cores with the keys as operand A
-// and the queries as operand B, and keeps per-lane running results: lane
-// (g, n) of the wave sees keys 4g..4g+3 of every block for query row n.
-// At the end the 4*NW per-lane candidate lists of every query row are merged
-// in parallel: one thread per list, k rounds of a butterfly arg max over the
-// row's threads, the winning list advancing its head.  Score matrices are
-// never written to memory.
+// Every product is a 16 keys x 16 query rows tile on the matrix cores, the
+// keys as MFMA operand A and the queries as operand B, so that lane (g, n)
+// of a wave holds the scores of keys 4g..4g+3 of a block for query row n and
+// keeps its own running arg max / sorted top-k list (keys reach a lane in
+// increasing index, so a strict '>' keeps the lower index on exact ties).
+// Score matrices are never written to memory.  A work unit is a set of query
+// rows that share one key set (all rows for routing, one scene's bucket for
+// Level-2); units come in two modes:
+//
+//  * streaming (up to 16 rows): the unit's key blocks are split over the 4
+//    waves; each wave streams its 16-key blocks straight from HBM into
+//    registers, two blocks in flight.  At the end the 16 per-lane lists of
+//    every row are merged in parallel (one thread per list, k rounds of a
+//    butterfly arg max).  Suits the many small buckets: all 4 waves compute.
+//  * shared (up to 128 rows): every 16-key block is loaded once by the whole
+//    workgroup into an LDS tile (double-buffered, two blocks in flight in
+//    registers) and read by every wave, each holding one or two 16-row query
+//    tiles; the key stream is paid once for up to 8 tiles.  Lists are merged
+//    inside the wave (4 lanes per row).  Suits large buckets and routing of
+//    many rows.
 #include "common.h"
 #include "kernels.h"
 
 namespace lookme {
 
+constexpr int SC_WAVES = 4;
+constexpr int SC_THREADS = SC_WAVES * WAVE;
 
 struct ScoreParams {
   const char* q;            // [rows, d_e]
@@ -34,203 +44,104 @@ struct ScoreParams {
   int ks;                   // chunk steps per row = row_bytes / 64
   int nkeys;                // routing: S; lookup: P
   int k;                    // lookup: top-k
+  int route_rows;           // routing: rows per unit (16: streaming, else shared)
+  int shared_rows;          // lookup: rows of a shared unit (at most)
   int32_t* out_idx;         // routing: scene[rows]; lookup: prim[rows, k]
   float* out_w;             // lookup: w[rows, k]
 };
 
-// KS: compile-time number of chunk steps; with MASKED, steps >= ks are
-// skipped (row widths that are not a power-of-two multiple of 64 bytes).
-// KL: per-lane candidate list length (>= k) for lookup; 1 for routing.
-// NW: waves per workgroup (they split the unit's key blocks).
-template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, int NW>
-__global__ __launch_bounds__(NW * WAVE) void score_kernel(ScoreParams a) {
-  constexpr int NL = NW * 4;                 // candidate lists per query row
-  __shared__ float cand_s[NL][16][KL];
-  __shared__ int cand_i[NL][16][KL];
+template <int KS, bool MASKED>
+__device__ __forceinline__ void load_row_frags(u32x4_t (&f)[KS], const char* row_ptr, int g,
+                                               int ks) {
+  const char* p = row_ptr + g * 16;
+#pragma unroll
+  for (int j = 0; j < KS; ++j) f[j] = (!MASKED || j < ks) ? ld16(p + j * 64) : u32x4_t{0, 0, 0, 0};
+}
 
-  const int lane = threadIdx.x & 63;
-  // wave index as a scalar, so that the key range (and every branch on it)
-  // is known to be uniform across the wave
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n = lane & 15;     // A: key row in block; B: query row in tile
-  const int g = lane >> 4;     // 16-lane group: chunk 4*j + g of each step
-
-  // ---- the unit: rows [begin, begin + nr) and its key set -----------------
-  int64_t begin;
-  int nr;
-  const char* keys;
-  if constexpr (LOOKUP) {
-    const int u = xcd_remap(blockIdx.x, *a.unit_count);
-    if (u < 0) return;
-    const int s = a.unit_scene[u];
-    begin = a.unit_begin[u];
-    nr = min(16, a.offsets[s + 1] - (int)begin);
-    keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
+// Scores of 4 keys (blk*16 + 4g + r) for one query row folded into the
+// lane's running result: arg max (routing, with the scene bias) or a sorted
+// list of the KL best (Level-2).
+template <bool LOOKUP, int KL>
+__device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int kend, const float* bias,
+                                            float (&ls)[KL], int (&li)[KL]) {
+  float v[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) v[r] = blk * 16 + 4 * g + r < kend ? acc[r] : -__builtin_inff();
+  if constexpr (!LOOKUP) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int p = blk * 16 + 4 * g + r;
+      float x = v[r];
+      if (bias != nullptr && p < kend) x += bias[p];
+      if (x > ls[0]) { ls[0] = x; li[0] = p; }
+    }
   } else {
-    const int64_t tiles = (a.rows + 15) >> 4;
-    const int u = xcd_remap(blockIdx.x, (int)tiles);
-    if (u < 0) return;
-    begin = (int64_t)u * 16;
-    nr = (int)min<int64_t>(16, a.rows - begin);
-    keys = a.keys;
-  }
-  const int nkeys = a.nkeys;
-
-  // ---- query fragments (operand B), kept in registers for the whole unit --
-  const int my_row_slot = n < nr ? n : nr - 1;
-  int64_t my_row;
-  if constexpr (LOOKUP) my_row = a.perm[begin + my_row_slot];
-  else my_row = begin + my_row_slot;
-  u32x4_t qb[KS];
-  {
-    const char* qp = a.q + my_row * a.row_bytes + g * 16;
-#pragma unroll
-    for (int j = 0; j < KS; ++j)
-      qb[j] = (!MASKED || j < a.ks) ? ld16(qp + j * 64) : u32x4_t{0, 0, 0, 0};
-  }
-
-  // ---- this wave's share of the key blocks --------------------------------
-  const int nblk = (nkeys + 15) >> 4;
-  const int bpw = (nblk + NW - 1) / NW;
-  const int kb0 = wv * bpw;
-  const int kb1 = min(nblk, kb0 + bpw);
-  const int kend = min(nkeys, kb1 * 16);
-
-  float ls[KL];
-  int li[KL];
-#pragma unroll
-  for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
-
-  // loads of one 16-key block: lane (n, g) takes chunk 4j + g of key row n
-  auto load_block = [&](u32x4_t (&buf)[KS], int blk) {
-    const int row = min(blk * 16 + n, kend - 1);
-    const char* kp = keys + (int64_t)row * a.row_bytes + g * 16;
-#pragma unroll
-    for (int j = 0; j < KS; ++j)
-      buf[j] = (!MASKED || j < a.ks) ? ld16(kp + j * 64) : u32x4_t{0, 0, 0, 0};
-  };
-  // scores of one block; the buffer is refilled with block `next` right
-  // after the matrix cores have read it.  The refill is unconditional (past
-  // the wave's range it re-reads the last block, an L2 hit): a conditional
-  // load would make the compiler wait for every load before each block.
-  auto score_block = [&](u32x4_t (&buf)[KS], int next) {
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < KS; ++j)
-      if (!MASKED || j < a.ks) acc = mfma_chunk<DT>(buf[j], qb[j], acc);
-    load_block(buf, min(next, kb1 - 1));
-    return acc;
-  };
-  // lane holds scores of keys blk*16 + 4g + r (r = 0..3) for query row n
-  auto update = [&](f32x4_t acc, int blk) {
-    float v[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) v[r] = blk * 16 + 4 * g + r < kend ? acc[r] : -__builtin_inff();
-    if constexpr (!LOOKUP) {
+    const float best = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+    if (best > ls[KL - 1]) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int p = blk * 16 + 4 * g + r;
-        float x = v[r];
-        if (a.bias != nullptr && p < kend) x += a.bias[p];
-        if (x > ls[0]) { ls[0] = x; li[0] = p; }
-      }
-    } else {
-      const float best = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-      if (best > ls[KL - 1]) {
-        // keys reach a lane in increasing p: strict '>' keeps the lower p
-        // ahead on exact ties
+        const float x = v[r];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int p = blk * 16 + 4 * g + r;
-          const float x = v[r];
-#pragma unroll
-          for (int e = KL - 1; e >= 1; --e) {
-            const bool above_prev = x > ls[e - 1];
-            const bool above_cur = x > ls[e];
-            const float s_keep = above_cur ? x : ls[e];
-            const int i_keep = above_cur ? p : li[e];
-            ls[e] = above_prev ? ls[e - 1] : s_keep;
-            li[e] = above_prev ? li[e - 1] : i_keep;
-          }
-          const bool top = x > ls[0];
-          ls[0] = top ? x : ls[0];
-          li[0] = top ? p : li[0];
+        for (int e = KL - 1; e >= 1; --e) {
+          const bool above_prev = x > ls[e - 1];
+          const bool above_cur = x > ls[e];
+          const float s_keep = above_cur ? x : ls[e];
+          const int i_keep = above_cur ? p : li[e];
+          ls[e] = above_prev ? ls[e - 1] : s_keep;
+          li[e] = above_prev ? li[e - 1] : i_keep;
         }
+        const bool top = x > ls[0];
+        ls[0] = top ? x : ls[0];
+        li[0] = top ? p : li[0];
       }
     }
-  };
-
-  // The query fragments must have landed before the key stream starts, so
-  // that at the loop head only key loads are outstanding, oldest first, on
-  // every path into it (otherwise the per-block waits become conservative).
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  if (kb0 < kb1) {
-    // two register buffers: while one block is multiplied, the next two are
-    // in flight (the single-buffer form keeps 64 more VGPRs free for very
-    // wide keys)
-    u32x4_t ka[KS];
-    load_block(ka, kb0);
-    if constexpr (KS <= 16) {
-      u32x4_t kbuf[KS];
-      asm volatile("" ::: "memory");   // keep the first block's loads the oldest
-      load_block(kbuf, min(kb0 + 1, kb1 - 1));
-      // full pairs only inside the loop: every path into the loop head then
-      // has the same loads outstanding (an early exit in the middle would
-      // make the compiler's wait counts conservative)
-      int blk = kb0;
-      for (; blk + 1 < kb1; blk += 2) {
-        update(score_block(ka, blk + 2), blk);
-        update(score_block(kbuf, blk + 3), blk + 1);
-      }
-      if (blk < kb1) update(score_block(ka, blk + 2), blk);
-    } else {
-      for (int blk = kb0; blk < kb1; ++blk) update(score_block(ka, blk + 1), blk);
-    }
   }
+}
 
-  // ---- merge: thread (t, L) owns list L of query row t ---------------------
-  const int list = wv * 4 + g;
-#pragma unroll
-  for (int e = 0; e < KL; ++e) {
-    cand_s[list][n][e] = ls[e];
-    cand_i[list][n][e] = li[e];
-  }
-  __syncthreads();
-  const int t = threadIdx.x / NL;          // query row of this thread
-  const int L = threadIdx.x % NL;          // its list
+// k rounds of a butterfly arg max over the 2^STEPS lanes that hold the
+// candidate lists of one row (lane distance `stride`, doubling each step).
+// Each lane passes its own sorted list; every lane receives the k winners.
+template <int KL, int STEPS>
+__device__ __forceinline__ void merge_lists(const float (&ls)[KL], const int (&li)[KL], int k,
+                                            int stride, float (&top_s)[KL], int (&top_i)[KL]) {
   int head = 0;
-  float hs = cand_s[L][t][0];
-  int hi = cand_i[L][t][0];
-  const int k = LOOKUP ? a.k : 1;
-  float top_s[KL];
-  int top_i[KL];
+  float hs = ls[0];
+  int hi = li[0];
 #pragma unroll
   for (int e = 0; e < KL; ++e) {
     if (e < k) {
       float bs = hs;
       int bi = hi;
 #pragma unroll
-      for (int d = NL / 2; d >= 1; d >>= 1) {
-        const float os = __shfl_xor(bs, d, NL);
-        const int oi = __shfl_xor(bi, d, NL);
+      for (int d = 0; d < STEPS; ++d) {
+        const float os = __shfl_xor(bs, stride << d, 64);
+        const int oi = __shfl_xor(bi, stride << d, 64);
         if (beats(os, oi, bs, bi)) { bs = os; bi = oi; }
       }
       top_s[e] = bs;
       top_i[e] = bi;
-      if (hi == bi && hs == bs) {      // this list supplied the winner
+      if (hi == bi && hs == bs) {   // this list supplied the winner
         ++head;
-        hs = head < KL ? cand_s[L][t][head] : -__builtin_inff();
-        hi = head < KL ? cand_i[L][t][head] : -1;
+        float ns = -__builtin_inff();
+        int ni = -1;
+#pragma unroll
+        for (int x = 1; x < KL; ++x)
+          if (x == head) { ns = ls[x]; ni = li[x]; }
+        hs = ns;
+        hi = ni;
       }
     }
   }
-  if (L != 0 || t >= nr) return;
-  int64_t out_row;
-  if constexpr (LOOKUP) out_row = a.perm[begin + t];
-  else out_row = begin + t;
+}
+
+template <bool LOOKUP, int KL>
+__device__ __forceinline__ void write_row(const ScoreParams& a, int64_t out_row,
+                                          const float (&top_s)[KL], const int (&top_i)[KL]) {
   if constexpr (!LOOKUP) {
     a.out_idx[out_row] = top_i[0];
   } else {
+    const int k = a.k;
     float sum = 0.f;
 #pragma unroll
     for (int e = 0; e < KL; ++e)
@@ -248,15 +159,264 @@ __global__ __launch_bounds__(NW * WAVE) void score_kernel(ScoreParams a) {
   }
 }
 
+template <bool LOOKUP>
+__device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, int slot) {
+  if constexpr (LOOKUP) return a.perm[begin + slot];
+  else return begin + slot;
+}
+
+// ---------------------------------------------------------------------------
+// Streaming mode: <= 16 rows, key blocks split over the waves
+// ---------------------------------------------------------------------------
+template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
+__device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, int64_t begin,
+                                            int nr, const char* keys) {
+  constexpr int NL = SC_WAVES * 4;   // candidate lists per query row
+  float (*cand_s)[16][KL] = reinterpret_cast<float (*)[16][KL]>(smem);
+  int (*cand_i)[16][KL] = reinterpret_cast<int (*)[16][KL]>(smem + NL * 16 * KL * 4);
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = lane & 15, g = lane >> 4;
+  const int nkeys = a.nkeys;
+
+  u32x4_t qb[KS];
+  load_row_frags<KS, MASKED>(qb, a.q + row_id<LOOKUP>(a, begin, n < nr ? n : nr - 1) * a.row_bytes,
+                             g, a.ks);
+
+  const int nblk = (nkeys + 15) >> 4;
+  const int bpw = (nblk + SC_WAVES - 1) / SC_WAVES;
+  const int kb0 = wv * bpw;
+  const int kb1 = min(nblk, kb0 + bpw);
+  const int kend = min(nkeys, kb1 * 16);
+
+  float ls[KL];
+  int li[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
+
+  auto load_block = [&](u32x4_t (&buf)[KS], int blk) {
+    const int row = min(blk * 16 + n, kend - 1);
+    load_row_frags<KS, MASKED>(buf, keys + (int64_t)row * a.row_bytes, g, a.ks);
+  };
+  // The buffer is refilled with block `next` right after the matrix cores
+  // have read it.  The refill is unconditional (past the wave's range it
+  // re-reads the last block, an L2 hit): a conditional load would make the
+  // compiler wait for every load before each block.
+  auto score_block = [&](u32x4_t (&buf)[KS], int next) {
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KS; ++j)
+      if (!MASKED || j < a.ks) acc = mfma_chunk<DT>(buf[j], qb[j], acc);
+    load_block(buf, min(next, kb1 - 1));
+    return acc;
+  };
+
+  // The query fragments must have landed before the key stream starts, so
+  // that at the loop head only key loads are outstanding, oldest first, on
+  // every path into it (otherwise the per-block waits become conservative).
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (kb0 < kb1) {
+    u32x4_t ka[KS];
+    load_block(ka, kb0);
+    if constexpr (KS <= 16) {
+      u32x4_t kbuf[KS];
+      asm volatile("" ::: "memory");   // keep the first block's loads the oldest
+      load_block(kbuf, min(kb0 + 1, kb1 - 1));
+      // full pairs only inside the loop: every path into the loop head then
+      // has the same loads outstanding
+      int blk = kb0;
+      for (; blk + 1 < kb1; blk += 2) {
+        fold_scores<LOOKUP, KL>(score_block(ka, blk + 2), blk, g, kend, a.bias, ls, li);
+        fold_scores<LOOKUP, KL>(score_block(kbuf, blk + 3), blk + 1, g, kend, a.bias, ls, li);
+      }
+      if (blk < kb1) fold_scores<LOOKUP, KL>(score_block(ka, blk + 2), blk, g, kend, a.bias, ls, li);
+    } else {
+      for (int blk = kb0; blk < kb1; ++blk)
+        fold_scores<LOOKUP, KL>(score_block(ka, blk + 1), blk, g, kend, a.bias, ls, li);
+    }
+  }
+
+  // merge: thread (t, L) owns list L of query row t
+  const int list = wv * 4 + g;
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    cand_s[list][n][e] = ls[e];
+    cand_i[list][n][e] = li[e];
+  }
+  __syncthreads();
+  const int t = threadIdx.x / NL;
+  const int L = threadIdx.x % NL;
+  float ms[KL];
+  int mi[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) { ms[e] = cand_s[L][t][e]; mi[e] = cand_i[L][t][e]; }
+  float top_s[KL];
+  int top_i[KL];
+  merge_lists<KL, 4>(ms, mi, LOOKUP ? a.k : 1, 1, top_s, top_i);
+  if (L == 0 && t < nr) write_row<LOOKUP, KL>(a, row_id<LOOKUP>(a, begin, t), top_s, top_i);
+}
+
+// ---------------------------------------------------------------------------
+// Shared mode: up to 128 rows, every key block staged once in LDS
+// ---------------------------------------------------------------------------
+template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
+__device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, int64_t begin,
+                                            int nr, const char* keys) {
+  constexpr int CPT = KS / 4;          // 16-byte chunks per thread per key block
+  constexpr int BLOCK_BYTES = KS * 1024;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, g = lane >> 4;
+  const int nkeys = a.nkeys;
+  // a wave keeps two 16-row query tiles (rows 16 w.. and 16 (w+4)..) when a
+  // key row is at most 1 KiB and k <= 8, one otherwise (see shared_unit_rows)
+  constexpr bool TWO_TILES = KS <= 16 && KL <= 8;
+  const int tiles = (nr + 15) >> 4;
+  const bool has0 = wv < tiles, has1 = TWO_TILES && wv + SC_WAVES < tiles;
+
+  u32x4_t q0[KS], q1[KS];
+  {
+    const int s0 = min(16 * wv + n, nr - 1);
+    load_row_frags<KS, MASKED>(q0, a.q + row_id<LOOKUP>(a, begin, s0) * a.row_bytes, g, a.ks);
+    if constexpr (TWO_TILES) {
+      const int s1 = min(16 * (wv + SC_WAVES) + n, nr - 1);
+      load_row_frags<KS, MASKED>(q1, a.q + row_id<LOOKUP>(a, begin, s1) * a.row_bytes, g, a.ks);
+    }
+  }
+  float ls0[KL], ls1[KL];
+  int li0[KL], li1[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    ls0[e] = ls1[e] = -__builtin_inff();
+    li0[e] = li1[e] = -1;
+  }
+
+  const int nblk = (nkeys + 15) >> 4;
+  // LDS image of a block: segment j (1 KiB) holds, at lane slot L, chunk
+  // 4j + (L >> 4) of key row (L & 15): exactly the operand-A fragment of
+  // lane L at step j, so each wave reads it with one conflict-free 16-byte
+  // load per lane.  Thread tid fills slots c = tid + 256 i.
+  auto gload = [&](u32x4_t (&r)[CPT], int blk) {
+    blk = min(blk, nblk - 1);          // unconditional: past the end, an L2 hit
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + SC_THREADS * i;
+      const int j = c >> 6, L = c & 63;
+      const int row = min(blk * 16 + (L & 15), nkeys - 1);
+      r[i] = (!MASKED || j < a.ks)
+                 ? ld16(keys + (int64_t)row * a.row_bytes + (4 * j + (L >> 4)) * 16)
+                 : u32x4_t{0, 0, 0, 0};
+    }
+  };
+  auto lstore = [&](int buf, const u32x4_t (&r)[CPT]) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) st16(smem + buf * BLOCK_BYTES + (tid + SC_THREADS * i) * 16, r[i]);
+  };
+  auto compute = [&](int buf, int blk) {
+    if (!has0) return;                 // a wave without rows only helps to load
+    f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    const char* base = smem + buf * BLOCK_BYTES + lane * 16;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      if (!MASKED || j < a.ks) {
+        const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(base + j * 1024);
+        acc0 = mfma_chunk<DT>(kf, q0[j], acc0);
+        if constexpr (TWO_TILES)
+          if (has1) acc1 = mfma_chunk<DT>(kf, q1[j], acc1);
+      }
+    }
+    fold_scores<LOOKUP, KL>(acc0, blk, g, nkeys, a.bias, ls0, li0);
+    if (has1) fold_scores<LOOKUP, KL>(acc1, blk, g, nkeys, a.bias, ls1, li1);
+  };
+
+  // Pipeline: at the top of step b the LDS buffer b%2 holds block b, the
+  // register set for block b+1 and the one for block b+2 are in flight.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
+  u32x4_t r0[CPT], r1[CPT];
+  gload(r0, 0);
+  asm volatile("" ::: "memory");
+  gload(r1, 1);
+  lstore(0, r0);
+  __syncthreads();
+  gload(r0, 2);
+  int blk = 0;
+  for (; blk + 1 < nblk; blk += 2) {
+    compute(0, blk);
+    lstore(1, r1);          // block blk+1 (buffer 1 was last read two steps ago)
+    __syncthreads();
+    gload(r1, blk + 3);
+    compute(1, blk + 1);
+    lstore(0, r0);          // block blk+2
+    __syncthreads();
+    gload(r0, blk + 4);
+  }
+  if (blk < nblk) compute(0, blk);
+
+  // merge inside the wave: the 4 lists of row n sit in lanes n + 16 g
+  const int k = LOOKUP ? a.k : 1;
+  float top_s[KL];
+  int top_i[KL];
+  if (has0) {
+    merge_lists<KL, 2>(ls0, li0, k, 16, top_s, top_i);
+    const int slot = 16 * wv + n;
+    if (g == 0 && slot < nr) write_row<LOOKUP, KL>(a, row_id<LOOKUP>(a, begin, slot), top_s, top_i);
+  }
+  if (has1) {
+    merge_lists<KL, 2>(ls1, li1, k, 16, top_s, top_i);
+    const int slot = 16 * (wv + SC_WAVES) + n;
+    if (g == 0 && slot < nr) write_row<LOOKUP, KL>(a, row_id<LOOKUP>(a, begin, slot), top_s, top_i);
+  }
+}
+
+// KS: compile-time number of chunk steps; with MASKED, steps >= ks are
+// skipped (row widths that are not a power-of-two multiple of 64 bytes).
+// KL: per-lane candidate list length (>= k) for lookup; 1 for routing.
+template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
+__global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
+  constexpr int MERGE_BYTES = SC_WAVES * 4 * 16 * KL * 8;
+  constexpr int STAGE_BYTES = 2 * KS * 1024;
+  constexpr int SMEM = MERGE_BYTES > STAGE_BYTES ? MERGE_BYTES : STAGE_BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+
+  int64_t begin;
+  int nr;
+  bool shared;
+  const char* keys;
+  if constexpr (LOOKUP) {
+    // units in list order (the long shared units first, spread over the
+    // XCDs by the round-robin dispatch)
+    const int u = blockIdx.x;
+    if (u >= *a.unit_count) return;
+    const int tag = a.unit_scene[u];
+    const int s = tag & ~UNIT_SHARED;
+    shared = (tag & UNIT_SHARED) != 0;
+    begin = a.unit_begin[u];
+    nr = min(shared ? a.shared_rows : UNIT_STREAM_ROWS, a.offsets[s + 1] - (int)begin);
+    keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
+  } else {
+    const int R = a.route_rows;
+    const int64_t units = (a.rows + R - 1) / R;
+    const int u = xcd_remap(blockIdx.x, (int)units);
+    if (u < 0) return;
+    begin = (int64_t)u * R;
+    nr = (int)min<int64_t>(R, a.rows - begin);
+    shared = R > 16;
+    keys = a.keys;
+  }
+  if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL>(a, smem, begin, nr, keys);
+  else stream_unit<DT, KS, MASKED, LOOKUP, KL>(a, smem, begin, nr, keys);
+}
+
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 
-template <int DT, bool LOOKUP, int KL, int NW>
+template <int DT, bool LOOKUP, int KL>
 static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t st) {
-#define LOOKME_SCORE_LAUNCH(KS_, M_)                                                     \
-  hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL, NW>), dim3(grid), dim3(NW * WAVE), \
-                     0, st, p)
+#define LOOKME_SCORE_LAUNCH(KS_, M_)                                                          \
+  hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL>), dim3(grid), dim3(SC_THREADS), 0, \
+                     st, p)
   switch (ks) {
     case 4: LOOKME_SCORE_LAUNCH(4, false); break;
     case 8: LOOKME_SCORE_LAUNCH(8, false); break;
@@ -268,13 +428,21 @@ static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t 
   return hipGetLastError();
 }
 
-template <bool LOOKUP, int KL, int NW>
+template <bool LOOKUP, int KL>
 static hipError_t launch_dt(int dt, int ks, int grid, const ScoreParams& p, hipStream_t st) {
-  return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL, NW>(ks, grid, p, st)
-                       : launch_ks<DT_F32, LOOKUP, KL, NW>(ks, grid, p, st);
+  return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL>(ks, grid, p, st)
+                       : launch_ks<DT_F32, LOOKUP, KL>(ks, grid, p, st);
 }
 
 static inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
+
+static int route_unit_rows(int64_t rows, int shared_rows) {
+  // shared mode when there are enough rows to keep the chip busy with
+  // 64- or 128-row units; small batches stream 16-row tiles
+  if (shared_rows >= 128 && rows >= (int64_t)128 * 512) return 128;
+  if (rows >= (int64_t)64 * 256) return 64;
+  return UNIT_STREAM_ROWS;
+}
 
 hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
                         int32_t* scene, int64_t rows, int d_e, int S, hipStream_t st) {
@@ -288,9 +456,10 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
   p.ks = (int)(p.row_bytes / 64);
   p.nkeys = S;
   p.k = 1;
+  p.route_rows = route_unit_rows(rows, shared_unit_rows(p.row_bytes, 1));
   p.out_idx = scene;
-  const int64_t tiles = (rows + 15) / 16;
-  return launch_dt<false, 1, 4>(dt, p.ks, (int)round8(tiles), p, st);
+  const int64_t units = (rows + p.route_rows - 1) / p.route_rows;
+  return launch_dt<false, 1>(dt, p.ks, (int)round8(units), p, st);
 }
 
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
@@ -305,15 +474,16 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
   p.unit_count = ws.unit_count;
   p.row_bytes = (int64_t)d_e * (dt == DT_BF16 ? 2 : 4);
   p.ks = (int)(p.row_bytes / 64);
+  p.shared_rows = shared_unit_rows(p.row_bytes, k);
   p.nkeys = P;
   p.k = k;
   p.out_idx = prim;
   p.out_w = w;
-  const int grid = (int)round8(ws.max_units);
-  if (k <= 4) return launch_dt<true, 4, 4>(dt, p.ks, grid, p, st);
-  if (k <= 8) return launch_dt<true, 8, 4>(dt, p.ks, grid, p, st);
-  if (k <= 16) return launch_dt<true, 16, 4>(dt, p.ks, grid, p, st);
-  return launch_dt<true, 32, 4>(dt, p.ks, grid, p, st);
+  const int grid = (int)ws.max_units;
+  if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st);
+  if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st);
+  if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st);
+  return launch_dt<true, 32>(dt, p.ks, grid, p, st);
 }
 
 }  // namespace lookme
