@@ -45,7 +45,120 @@ def parse():
     ap.add_argument("--copies", type=int, default=0, help="table copies (0: automatic)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=0, help="oracle sample size (0: auto)")
+    ap.add_argument("--pmc-calibrate", action="store_true",
+                    help="first run a plain 256 MiB read+write kernel (counter calibration)")
+    ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
+                         "script into profiles/, with the algorithmic bytes of a bench line "
+                         "of the same workload, and exit (no GPU needed)")
     return ap.parse_args()
+
+
+# --------------------------------------------------------------------------
+# HBM traffic of the dominant kernel from PMC counters
+# --------------------------------------------------------------------------
+
+CALIB_BYTES = 256 << 20
+SCORE_KERNEL = "score_kernel"
+KERNEL_SOURCES = ("paper_2607_16305_amd/csrc/score.hip", "paper_2607_16305_amd/csrc/common.h",
+                  "paper_2607_16305_amd/csrc/kernels.h")
+
+
+def kernel_source_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(workload_name: str) -> str:
+    return os.path.join(ROOT, "profiles", f"traffic_score_kernel_{workload_name}.json")
+
+
+def calibration_copy():
+    """A plain elementwise kernel of known traffic: reads and writes 256 MiB."""
+    import torch
+    src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+
+
+def _counter_rows(d: str):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    return rows
+
+
+def _per_dispatch(rows, counter, match):
+    vals = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter or match not in r.get("Kernel_Name", ""):
+            continue
+        key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
+    return list(vals.values())
+
+
+def summarise_traffic(fetch_dir: str, write_dir: str, wl, algorithmic: int):
+    """Scale FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the scoring kernel by
+    what the same counters read for the 256 MiB calibration kernel."""
+    fr, wr = _counter_rows(fetch_dir), _counter_rows(write_dir)
+    cal_f = _per_dispatch(fr, "FETCH_SIZE", "neg_kernel") or _per_dispatch(fr, "FETCH_SIZE", "elementwise")
+    cal_w = _per_dispatch(wr, "WRITE_SIZE", "neg_kernel") or _per_dispatch(wr, "WRITE_SIZE", "elementwise")
+    sc_f = _per_dispatch(fr, "FETCH_SIZE", SCORE_KERNEL)
+    sc_w = _per_dispatch(wr, "WRITE_SIZE", SCORE_KERNEL)
+    # the routing launch of the scoring kernel is the smaller one; keep the
+    # Level-2 launches (every other dispatch, the larger reading)
+    sc_f = sorted(sc_f)[len(sc_f) // 2:]
+    sc_w = sorted(sc_w)[len(sc_w) // 2:]
+    mean = lambda v: sum(v) / len(v)
+    f_read = max(cal_f) * 1024 / CALIB_BYTES
+    f_write = max(cal_w) * 1024 / CALIB_BYTES
+    fetch_b = mean(sc_f) * 1024 / f_read
+    write_b = mean(sc_w) * 1024 / f_write
+    out = {
+        "kernel": SCORE_KERNEL + " (Level-2 launch)", "workload": wl.name,
+        "kernel_source_sha": kernel_source_sha(),
+        "fetch_kib_per_launch_raw": mean(sc_f), "write_kib_per_launch_raw": mean(sc_w),
+        "calibration": {"bytes_read": CALIB_BYTES, "bytes_written": CALIB_BYTES,
+                        "fetch_kib": max(cal_f), "write_kib": max(cal_w),
+                        "read_factor": f_read, "write_factor": f_write},
+        "traffic_bytes_per_launch": fetch_b + write_b,
+        "algorithmic_bytes_per_launch": algorithmic,
+        "traffic_over_algorithmic": (fetch_b + write_b) / algorithmic,
+        "commands": [
+            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <FETCH_DIR> -o run -- "
+            "python3 bench.py --steps 20 --warmup 2 --no-cpu-baseline --pmc-calibrate",
+            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <WRITE_DIR> -o run -- "
+            "python3 bench.py --steps 20 --warmup 2 --no-cpu-baseline --pmc-calibrate",
+            "python3 bench.py --traffic-from <FETCH_DIR> <WRITE_DIR> <BENCH_JSON>"],
+    }
+    with open(traffic_path(wl.name), "w") as fh:
+        json.dump(out, fh, indent=1)
+    return out
+
+
+def stored_traffic(wl):
+    """Measured traffic per launch, if taken on the current kernel source."""
+    try:
+        with open(traffic_path(wl.name)) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha") != kernel_source_sha():
+        return None
+    return t.get("traffic_bytes_per_launch")
 
 
 class Bench:
@@ -191,10 +304,21 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
-    import torch
     from synth import WORKLOADS
     wl = WORKLOADS[args.workload]
+    if args.traffic_from:
+        with open(args.traffic_from[2]) as fh:
+            line = json.load(fh)
+        if line["config"]["workload"] != wl.name:
+            raise SystemExit("the bench line is for another workload")
+        out = summarise_traffic(args.traffic_from[0], args.traffic_from[1], wl,
+                                line["roofline"]["algorithmic_bytes_per_launch"])
+        print(json.dumps(out))
+        return
+    import torch
     torch.cuda.set_device(0)
+    if args.pmc_calibrate:
+        calibration_copy()
     b = Bench(wl, args.workload, args.copies)
 
     for i in range(args.warmup):
@@ -220,7 +344,7 @@ def main():
     roofline = {"bound": "hbm", "kernel": "score_kernel (Level-2 scoring + top-k + softmax)",
                 "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
-                "traffic": None, "algorithmic_bytes_per_launch": bytes_["score"],
+                "traffic": stored_traffic(wl), "algorithmic_bytes_per_launch": bytes_["score"],
                 "nonempty_scenes": nonempty}
 
     cpu = None
