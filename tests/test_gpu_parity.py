@@ -59,6 +59,15 @@ SMALL = {
     "bf16_one_scene": Workload("bf16_one_scene", "bf16", 33, 1, 128, 256, 1, 19, 32, 32, 4, 50),
     "bf16_one_prim": Workload("bf16_one_prim", "bf16", 21, 1, 64, 64, 9, 1, 16, 16, 1, 50),
     "bf16_one_token": Workload("bf16_one_token", "bf16", 1, 1, 64, 64, 9, 24, 16, 16, 4, 100),
+    # projections large enough for the direct-to-LDS kernel (>= 256 tiles of
+    # 128 x 128), with ragged row and K edges
+    "bf16_dtl_proj_l4": Workload("bf16_dtl_proj_l4", "bf16", 1999, 4, 320, 512, 12, 40, 64, 64,
+                                 4, 20, usage="uniform"),
+    "f32_dtl_proj_l4": Workload("f32_dtl_proj_l4", "f32", 2100, 4, 96, 512, 5, 24, 32, 32, 3,
+                                30, usage="iid"),
+    # same size, K not in whole 128-byte steps: the register-staged kernel
+    "f32_ragged_k_proj_l4": Workload("f32_ragged_k_proj_l4", "f32", 2100, 4, 48, 512, 5, 24, 32,
+                                     32, 3, 30, usage="iid"),
 }
 
 
