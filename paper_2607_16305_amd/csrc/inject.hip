@@ -8,8 +8,9 @@
 //               floats order like their bits, and the square root keeps the
 //               order, so selecting on it selects on the norm);
 //   crit_select one workgroup per layer: 4-pass MSB-first radix select of
-//               the n_keep-th largest key, then an order-preserving
-//               compaction (ballot prefix sums) of the kept token ids;
+//               the n_keep-th largest key (keys cached in LDS when they
+//               fit), then an order-preserving compaction (block prefix
+//               sums) of the kept token ids;
 //   inject      one workgroup per kept token: 16-byte coalesced loads of its
 //               k table rows (all in flight together), fp32 weighted sum in
 //               a fixed order, one rounding of H + sum, in-place store.
@@ -82,6 +83,13 @@ __device__ __forceinline__ int block_scan_incl(int v, int* wsum) {
   return incl + off;
 }
 
+// CACHED: a layer's keys are first copied to LDS (n <= SEL_CACHE_N), so that
+// the four passes and the compaction read them there instead of from L2
+// (one global round trip instead of five).  Element i sits at i + i / 32:
+// the padding keeps threads that walk ranges of 32 keys on distinct banks.
+constexpr int SEL_CACHE_N = 32768;
+
+template <bool CACHED>
 __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
     const uint32_t* __restrict__ key_all, int64_t n, int64_t n_keep,
     int32_t* __restrict__ kept_all) {
@@ -89,11 +97,20 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
   __shared__ int wsum[SEL_WAVES];
   __shared__ uint32_t s_prefix;
   __shared__ int s_need;
+  __shared__ uint32_t cache[CACHED ? SEL_CACHE_N + SEL_CACHE_N / 32 : 1];
   const int layer = blockIdx.x;
-  const uint32_t* key = key_all + (int64_t)layer * n;
+  const uint32_t* gkey = key_all + (int64_t)layer * n;
   int32_t* kept = kept_all + (int64_t)layer * n_keep;
   if (n_keep == 0) return;
   const int tid = threadIdx.x;
+  if constexpr (CACHED) {
+    for (int i = tid; i < n; i += SEL_THREADS) cache[i + (i >> 5)] = gkey[i];
+    __syncthreads();
+  }
+  auto key = [&](int64_t i) -> uint32_t {
+    if constexpr (CACHED) return cache[i + (i >> 5)];
+    else return gkey[i];
+  };
   // every thread owns a contiguous range of tokens
   const int64_t per = (n + SEL_THREADS - 1) / SEL_THREADS;
   const int64_t i0 = min<int64_t>(n, tid * per), i1 = min<int64_t>(n, i0 + per);
@@ -106,7 +123,7 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
     for (int64_t i = i0; i < i1; ++i) {
-      const uint32_t k = key[i];
+      const uint32_t k = key(i);
       if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1);
     }
     __syncthreads();
@@ -129,7 +146,7 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
   // ---- order-preserving compaction: one block scan of per-thread counts ----
   int n_gt = 0, n_eq = 0;
   for (int64_t i = i0; i < i1; ++i) {
-    const uint32_t k = key[i];
+    const uint32_t k = key(i);
     n_gt += k > T;
     n_eq += k == T;
   }
@@ -137,7 +154,7 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
   const int eq_before = block_scan_incl<SEL_WAVES>(n_eq, wsum) - n_eq;
   int g = gt_before, e = eq_before;
   for (int64_t i = i0; i < i1; ++i) {
-    const uint32_t k = key[i];
+    const uint32_t k = key(i);
     if (k > T) {
       const int pos = g + min(e, take_eq);
       if (pos < n_keep) kept[pos] = (int32_t)i;
@@ -255,8 +272,12 @@ hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uin
 hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint32_t* key,
                               int32_t* kept, hipStream_t st) {
   if (n == 0 || n_keep == 0) return hipSuccess;
-  hipLaunchKernelGGL(crit_select_kernel, dim3(layers), dim3(SEL_THREADS), 0, st, key, n, n_keep,
-                     kept);
+  if (n <= SEL_CACHE_N)
+    hipLaunchKernelGGL(crit_select_kernel<true>, dim3(layers), dim3(SEL_THREADS), 0, st, key, n,
+                       n_keep, kept);
+  else
+    hipLaunchKernelGGL(crit_select_kernel<false>, dim3(layers), dim3(SEL_THREADS), 0, st, key, n,
+                       n_keep, kept);
   return hipGetLastError();
 }
 

@@ -25,13 +25,22 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
 // streaming units, each part in scene order.
 constexpr int UNIT_STREAM_ROWS = 16;
 constexpr int32_t UNIT_SHARED = 1 << 30;
+// Chunk steps (64 bytes of a key row each) the scoring kernel is compiled
+// for, given the row width: 4, 8, 16 or 32 exactly; narrower rows run the
+// 4-step kernel and other widths the 32-step kernel, with the steps past the
+// row masked off.
+inline int score_ks(int64_t row_bytes) {
+  const int64_t ks = row_bytes / 64;
+  if (ks == 4 || ks == 8 || ks == 16 || ks == 32) return (int)ks;
+  return ks < 4 ? 4 : 32;
+}
 // Rows of a shared unit: each of its 4 waves keeps two 16-row query tiles in
-// registers when a key row is at most 1 KiB and k <= 8, one tile otherwise
-// (two 32-step tiles would need 64 fragment loads in flight, more than the
-// 6-bit vector-memory counter of a wave can track; with k = 16 the two tiles'
-// candidate lists would halve the waves a SIMD can hold).
+// registers when the kernel runs at most 16 chunk steps and k <= 8, one tile
+// otherwise (two 32-step tiles would need 64 fragment loads in flight, more
+// than the 6-bit vector-memory counter of a wave can track; with k = 16 the
+// two tiles' candidate lists would halve the waves a SIMD can hold).
 inline int shared_unit_rows(int64_t row_bytes, int k) {
-  return (row_bytes <= 1024 && k <= 8) ? 128 : 64;
+  return (score_ks(row_bytes) <= 16 && k <= 8) ? 128 : 64;
 }
 struct BucketWs {
   int32_t* chunk_hist;   // [chunks, S]

@@ -417,12 +417,15 @@ static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t 
 #define LOOKME_SCORE_LAUNCH(KS_, M_)                                                          \
   hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL>), dim3(grid), dim3(SC_THREADS), 0, \
                      st, p)
+  // the compiled step count follows score_ks(), which also sizes the units
   switch (ks) {
     case 4: LOOKME_SCORE_LAUNCH(4, false); break;
     case 8: LOOKME_SCORE_LAUNCH(8, false); break;
     case 16: LOOKME_SCORE_LAUNCH(16, false); break;
     case 32: LOOKME_SCORE_LAUNCH(32, false); break;
-    default: LOOKME_SCORE_LAUNCH(32, true);
+    default:
+      if (ks < 4) LOOKME_SCORE_LAUNCH(4, true);
+      else LOOKME_SCORE_LAUNCH(32, true);
   }
 #undef LOOKME_SCORE_LAUNCH
   return hipGetLastError();

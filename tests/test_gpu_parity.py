@@ -65,6 +65,9 @@ SMALL = {
                                  4, 20, usage="uniform"),
     "f32_dtl_proj_l4": Workload("f32_dtl_proj_l4", "f32", 2100, 4, 96, 512, 5, 24, 32, 32, 3,
                                 30, usage="iid"),
+    # more tokens per layer than the select kernel caches in LDS
+    "bf16_many_tokens": Workload("bf16_many_tokens", "bf16", 40000, 1, 64, 64, 8, 16, 16, 16, 2,
+                                 10, usage="iid"),
     # same size, K not in whole 128-byte steps: the register-staged kernel
     "f32_ragged_k_proj_l4": Workload("f32_ragged_k_proj_l4", "f32", 2100, 4, 48, 512, 5, 24, 32,
                                      32, 3, 30, usage="iid"),
