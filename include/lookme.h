@@ -92,9 +92,11 @@ lookme_status_t lookme_create(const lookme_desc_t* desc, const void* scene_keys,
 lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_tokens,
                                       size_t* bytes);
 
-/* Attach caller-owned device workspace (256-byte aligned).  The library
+/* Attach caller-owned device workspace (256-byte aligned, at least 1280
+ * bytes; lookme_workspace_size gives what a call needs).  The library
  * zero-fills a small counter region of it once here (hipMemset on the current
- * device); it must not be modified by the caller while the handle uses it. */
+ * device); every call leaves those counters at zero again.  The workspace
+ * must not be modified by the caller while the handle uses it. */
 lookme_status_t lookme_set_workspace(lookme_t h, void* dev_ptr, size_t bytes);
 
 /*
@@ -107,7 +109,9 @@ lookme_status_t lookme_set_workspace(lookme_t h, void* dev_ptr, size_t bytes);
  *                                  equal d_e; q_out may alias x for one layer)
  *   q_out     [layers, n, d_e]     q = round_to_dtype(x W), float32 accumulation
  *   scene_out [layers, n] int32    argmax_s <q, scene_keys[s]> + bias[s]
- * d_in * elem_size must be a multiple of 16 bytes.
+ * d_in * elem_size must be a multiple of 16 bytes.  Needs a workspace of at
+ * least lookme_workspace_size(layers, n) (small batches pass partial arg
+ * maxima between workgroups through it).
  */
 lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in,
                              const void* x, const void* w_proj, void* q_out,

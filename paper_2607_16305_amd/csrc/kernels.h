@@ -14,8 +14,16 @@ hipError_t launch_project(int dt, const void* x, const void* wt, void* q, int64_
                           int d_e, int layers, hipStream_t st);
 
 // ---- routing: scene[r] = argmax_s <q_r, K1[s]> + bias[s] over rows r -------
+// Small batches split the scene keys of a 16-row tile over several
+// workgroups; `part` ([ROUTE_PART_ENTRIES] of (scene, score) pairs) and
+// `count` ([ROUTE_MAX_TILES], zero before the first call, left zero by each
+// call) carry the partial results.
+constexpr int ROUTE_MAX_TILES = 256;
+constexpr int ROUTE_PART_ENTRIES = (512 + ROUTE_MAX_TILES) * 16;
+void route_split(int64_t rows, int S, int* splits, int* kps);
 hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
-                        int32_t* scene, int64_t rows, int d_e, int S, hipStream_t st);
+                        int32_t* scene, int64_t rows, int d_e, int S, uint64_t* part,
+                        int32_t* count, hipStream_t st);
 
 // ---- bucketing of rows by scene -----------------------------------------
 // Level-2 work units: a bucket of at most UNIT_STREAM_ROWS rows is one

@@ -64,9 +64,14 @@ constexpr int32_t MAX_SCENES = 16384;   // bucketing keeps one histogram per chu
 
 // Workspace layout for `layers` x `n` rows.
 struct Layout {
-  size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, crit_key,
-      kept, total;
+  size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, route_count,
+      route_part, crit_key, kept, total;
 };
+
+// The leading bytes of the workspace hold counters that start at zero; they
+// are zero-filled once when the workspace is attached and every call leaves
+// them at zero.
+constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_MAX_TILES * 4;
 
 Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n) {
   const int64_t rows = (int64_t)layers * n;
@@ -80,6 +85,8 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n) {
     return at;
   };
   L.unit_count = take(256);   // counters first: the region zeroed at set-up
+  L.route_count = take((size_t)lookme::ROUTE_MAX_TILES * 4);
+  L.route_part = take((size_t)lookme::ROUTE_PART_ENTRIES * 8);
   L.chunk_hist = take((size_t)chunks * d.num_scenes * 4);
   L.local_rank = take((size_t)rows * 4);
   L.offsets = take(((size_t)d.num_scenes + 1) * 4);
@@ -269,8 +276,9 @@ lookme_status_t lookme_set_workspace(lookme_t h, void* dev_ptr, size_t bytes) {
   if (dev_ptr == nullptr) return fail(LOOKME_ERR_INVALID, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(dev_ptr) & 255u)
     return fail(LOOKME_ERR_INVALID, "workspace is not 256-byte aligned");
-  if (bytes < 256) return fail(LOOKME_ERR_WORKSPACE, "workspace below 256 bytes");
-  LOOKME_TRY(hip_status(hipMemset(dev_ptr, 0, 256), "hipMemset(workspace counters)"));
+  if (bytes < ZEROED_BYTES)
+    return fail(LOOKME_ERR_WORKSPACE, "workspace below %zu bytes", ZEROED_BYTES);
+  LOOKME_TRY(hip_status(hipMemset(dev_ptr, 0, ZEROED_BYTES), "hipMemset(workspace counters)"));
   h->ws = dev_ptr;
   h->ws_bytes = bytes;
   return LOOKME_OK;
@@ -297,8 +305,11 @@ lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in
   if (w_proj) LOOKME_TRY(check_ptr(w_proj, "w_proj"));
   LOOKME_TRY(check_ptr(q_out, "q_out"));
   LOOKME_TRY(check_ptr(scene_out, "scene_out"));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t rows = (int64_t)layers * n;
+  char* ws = static_cast<char*>(h->ws);
   if (w_proj) {
     Timed tm(h, LOOKME_GROUP_PROJECT, st);
     LOOKME_TRY(hip_status(
@@ -315,9 +326,11 @@ lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in
     }
   }
   Timed tm(h, LOOKME_GROUP_ROUTE, st);
-  return hip_status(lookme::launch_route(d.dtype, q_out, h->scene_keys, h->bias, scene_out, rows,
-                                         d.key_dim, d.num_scenes, st),
-                    "routing launch");
+  return hip_status(
+      lookme::launch_route(d.dtype, q_out, h->scene_keys, h->bias, scene_out, rows, d.key_dim,
+                           d.num_scenes, reinterpret_cast<uint64_t*>(ws + L.route_part),
+                           reinterpret_cast<int32_t*>(ws + L.route_count), st),
+      "routing launch");
 }
 
 lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void* q,

@@ -45,6 +45,10 @@ struct ScoreParams {
   int nkeys;                // routing: S; lookup: P
   int k;                    // lookup: top-k
   int route_rows;           // routing: rows per unit (16: streaming, else shared)
+  int route_splits;         // routing, streaming: key ranges per 16-row tile
+  int route_kps;            // routing, streaming: keys per range (multiple of 64)
+  uint64_t* route_part;     // routing, splits > 1: [tiles, splits, 16] (idx, score)
+  int32_t* route_count;     // routing, splits > 1: [tiles] arrivals, left at zero
   int shared_rows;          // lookup: rows of a shared unit (at most)
   int32_t* out_idx;         // routing: scene[rows]; lookup: prim[rows, k]
   float* out_w;             // lookup: w[rows, k]
@@ -168,16 +172,54 @@ __device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, i
 // ---------------------------------------------------------------------------
 // Streaming mode: <= 16 rows, key blocks split over the waves
 // ---------------------------------------------------------------------------
+// Routing with the keys split over several workgroups: the workgroup's best
+// (score, scene) of each row goes to the partial table; the last of a tile's
+// workgroups to arrive (device-scope counter) reduces the tile's partials in
+// key-range order with the lowest-index tie rule, writes the scenes and
+// resets the counter for the next call.
+__device__ __forceinline__ void route_partial(const ScoreParams& a, int64_t tile, int split,
+                                              int t, int nr, float best_s, int best_i,
+                                              int* s_last) {
+  const int splits = a.route_splits;
+  uint64_t* part = a.route_part + (tile * splits) * 16;
+  if (t < nr)
+    part[split * 16 + t] = ((uint64_t)(uint32_t)best_i << 32) | __float_as_uint(best_s);
+  // the barrier orders every thread's store before thread 0's release; the
+  // acquire half makes the other workgroups' partials visible to the last
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *s_last = __hip_atomic_fetch_add(&a.route_count[tile], 1, __ATOMIC_ACQ_REL,
+                                     __HIP_MEMORY_SCOPE_AGENT) == splits - 1;
+  __syncthreads();
+  if (!*s_last) return;
+  if (t < nr) {
+    float bs = -__builtin_inff();
+    int bi = -1;
+    for (int sp = 0; sp < splits; ++sp) {
+      const uint64_t v = __hip_atomic_load(&part[sp * 16 + t], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+      const float vs = __uint_as_float((uint32_t)v);
+      const int vi = (int)(v >> 32);
+      if (beats(vs, vi, bs, bi)) { bs = vs; bi = vi; }
+    }
+    a.out_idx[tile * 16 + t] = bi;
+  }
+  if (threadIdx.x == 0) a.route_count[tile] = 0;
+}
+
+// key0, nkeys: the unit's key range (routing may split the keys; Level-2
+// units take all P keys of their scene, key0 = 0).
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
 __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, int64_t begin,
-                                            int nr, const char* keys) {
+                                            int nr, const char* keys, int key0, int nkeys,
+                                            int split) {
   constexpr int NL = SC_WAVES * 4;   // candidate lists per query row
   float (*cand_s)[16][KL] = reinterpret_cast<float (*)[16][KL]>(smem);
   int (*cand_i)[16][KL] = reinterpret_cast<int (*)[16][KL]>(smem + NL * 16 * KL * 4);
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n = lane & 15, g = lane >> 4;
-  const int nkeys = a.nkeys;
+  const float* bias = a.bias != nullptr ? a.bias + key0 : nullptr;
 
   u32x4_t qb[KS];
   load_row_frags<KS, MASKED>(qb, a.q + row_id<LOOKUP>(a, begin, n < nr ? n : nr - 1) * a.row_bytes,
@@ -226,13 +268,13 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
       // has the same loads outstanding
       int blk = kb0;
       for (; blk + 1 < kb1; blk += 2) {
-        fold_scores<LOOKUP, KL>(score_block(ka, blk + 2), blk, g, kend, a.bias, ls, li);
-        fold_scores<LOOKUP, KL>(score_block(kbuf, blk + 3), blk + 1, g, kend, a.bias, ls, li);
+        fold_scores<LOOKUP, KL>(score_block(ka, blk + 2), blk, g, kend, bias, ls, li);
+        fold_scores<LOOKUP, KL>(score_block(kbuf, blk + 3), blk + 1, g, kend, bias, ls, li);
       }
-      if (blk < kb1) fold_scores<LOOKUP, KL>(score_block(ka, blk + 2), blk, g, kend, a.bias, ls, li);
+      if (blk < kb1) fold_scores<LOOKUP, KL>(score_block(ka, blk + 2), blk, g, kend, bias, ls, li);
     } else {
       for (int blk = kb0; blk < kb1; ++blk)
-        fold_scores<LOOKUP, KL>(score_block(ka, blk + 1), blk, g, kend, a.bias, ls, li);
+        fold_scores<LOOKUP, KL>(score_block(ka, blk + 1), blk, g, kend, bias, ls, li);
     }
   }
 
@@ -253,6 +295,14 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
   float top_s[KL];
   int top_i[KL];
   merge_lists<KL, 4>(ms, mi, LOOKUP ? a.k : 1, 1, top_s, top_i);
+  if constexpr (!LOOKUP) {
+    top_i[0] += key0;
+    if (a.route_splits > 1) {
+      __shared__ int s_last;
+      route_partial(a, begin / 16, split, L == 0 ? t : 16, nr, top_s[0], top_i[0], &s_last);
+      return;
+    }
+  }
   if (L == 0 && t < nr) write_row<LOOKUP, KL>(a, row_id<LOOKUP>(a, begin, t), top_s, top_i);
 }
 
@@ -383,6 +433,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   int nr;
   bool shared;
   const char* keys;
+  int key0 = 0, nk = a.nkeys, split = 0;
   if constexpr (LOOKUP) {
     // units in list order (the long shared units first, spread over the
     // XCDs by the round-robin dispatch)
@@ -396,16 +447,20 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
   } else {
     const int R = a.route_rows;
-    const int64_t units = (a.rows + R - 1) / R;
+    const int splits = R > 16 ? 1 : a.route_splits;
+    const int64_t units = (a.rows + R - 1) / R * splits;
     const int u = xcd_remap(blockIdx.x, (int)units);
     if (u < 0) return;
-    begin = (int64_t)u * R;
+    begin = (int64_t)(u / splits) * R;
     nr = (int)min<int64_t>(R, a.rows - begin);
     shared = R > 16;
-    keys = a.keys;
+    split = u % splits;
+    key0 = split * a.route_kps;
+    nk = min(a.route_kps, a.nkeys - key0);
+    keys = a.keys + (int64_t)key0 * a.row_bytes;
   }
   if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL>(a, smem, begin, nr, keys);
-  else stream_unit<DT, KS, MASKED, LOOKUP, KL>(a, smem, begin, nr, keys);
+  else stream_unit<DT, KS, MASKED, LOOKUP, KL>(a, smem, begin, nr, keys, key0, nk, split);
 }
 
 // ---------------------------------------------------------------------------
@@ -447,8 +502,26 @@ static int route_unit_rows(int64_t rows, int shared_rows) {
   return UNIT_STREAM_ROWS;
 }
 
+// Streaming routing of a small batch splits the keys of every 16-row tile
+// over several workgroups (at least 64 keys each) until about 512
+// workgroups run; batches of more than ROUTE_MAX_TILES tiles do not split.
+void route_split(int64_t rows, int S, int* splits, int* kps) {
+  const int64_t tiles = (rows + 15) / 16;
+  int sp = 1;
+  if (tiles <= ROUTE_MAX_TILES) {
+    const int want = (int)((512 + tiles - 1) / tiles);
+    const int most = (S + 63) / 64;
+    sp = want < most ? want : most;
+    if (sp < 1) sp = 1;
+  }
+  const int per = (S + sp - 1) / sp;
+  *kps = (per + 63) / 64 * 64;
+  *splits = (S + *kps - 1) / *kps;
+}
+
 hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
-                        int32_t* scene, int64_t rows, int d_e, int S, hipStream_t st) {
+                        int32_t* scene, int64_t rows, int d_e, int S, uint64_t* part,
+                        int32_t* count, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   ScoreParams p{};
   p.q = static_cast<const char*>(q);
@@ -461,7 +534,12 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
   p.k = 1;
   p.route_rows = route_unit_rows(rows, shared_unit_rows(p.row_bytes, 1));
   p.out_idx = scene;
-  const int64_t units = (rows + p.route_rows - 1) / p.route_rows;
+  p.route_splits = 1;
+  p.route_kps = S;
+  if (p.route_rows == UNIT_STREAM_ROWS) route_split(rows, S, &p.route_splits, &p.route_kps);
+  p.route_part = part;
+  p.route_count = count;
+  const int64_t units = (rows + p.route_rows - 1) / p.route_rows * p.route_splits;
   return launch_dt<false, 1>(dt, p.ks, (int)round8(units), p, st);
 }
 

@@ -180,12 +180,13 @@ class Table:
     def reserve(self, layers: int, n: int):
         need = lookme_workspace_size(self.handle, layers, n)
         if self.ws is None or self.ws.numel() < need:
-            self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+            self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
             lookme_set_workspace(self.handle, self.ws, self.ws.numel())
         return need
 
     def route(self, x, w_proj, q_out, scene_out, layers=1, stream=None):
         n, d_in = x.shape
+        self.reserve(layers, n)
         lookme_route(self.handle, layers, n, d_in, x, w_proj, q_out, scene_out, stream)
 
     def lookup(self, q, scene, prim_out, w_out, layers=1, stream=None):

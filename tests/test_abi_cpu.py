@@ -107,7 +107,9 @@ def test_calls_validate_before_launch(lib):
             lk.LOOKME_ERR_UNSUPPORTED
         assert S(lambda: lk.lookme_route(h, 0, 8, 2048, FAKE, FAKE, FAKE, FAKE, 0)) == \
             lk.LOOKME_ERR_INVALID
-        # lookup and inject need a workspace
+        # route, lookup and inject need a workspace
+        assert S(lambda: lk.lookme_route(h, 1, 8, 2048, FAKE, FAKE, FAKE, FAKE, 0)) == \
+            lk.LOOKME_ERR_WORKSPACE
         assert S(lambda: lk.lookme_lookup(h, 1, 8, FAKE, FAKE, FAKE, FAKE, 0)) == \
             lk.LOOKME_ERR_WORKSPACE
         assert S(lambda: lk.lookme_inject(h, 1, 8, 2, FAKE, 2048, FAKE, FAKE, FAKE, FAKE, 2048,

@@ -104,6 +104,24 @@ def test_integer_scores_tie_break_exactly(dtype):
     assert not rep.exemptions, rep.exemptions
 
 
+@pytest.mark.parametrize("layers,with_bias", [(1, True), (2, False)])
+def test_routing_with_split_keys(layers, with_bias):
+    """Small batches split the scene keys of a 16-row tile over several
+    workgroups (here 5 ranges of 64, 64, 64, 64 and 44 keys; 13 or 25 tiles,
+    the last one ragged); the scene is the arg max over all of them, bias
+    included, and repeated calls reuse the arrival counters."""
+    wl = Workload("bf16_split_route", "bf16", 200, layers, 256, 256, 300, 16, 32, 32, 4, 25,
+                  usage="uniform")
+    _announce(f"split routing: {wl}, bias={with_bias}")
+    inp = make_inputs(wl, seed=12, device=DEV)
+    if with_bias:
+        g = torch.Generator(device="cpu").manual_seed(77)
+        inp["bias"] = (torch.randn(wl.scenes, generator=g) * 0.5).to(DEV)
+    r1, _ = _run_check(inp)
+    r2, _ = _run_check(inp, table=r1.table)   # same workspace: counters were reset
+    assert torch.equal(r1.scene, r2.scene)
+
+
 def test_f32_k1_inject_is_one_rounded_add():
     wl = SMALL["f32_k1"]
     inp = make_inputs(wl, seed=9, device=DEV)
