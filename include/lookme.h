@@ -92,7 +92,7 @@ lookme_status_t lookme_create(const lookme_desc_t* desc, const void* scene_keys,
 lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_tokens,
                                       size_t* bytes);
 
-/* Attach caller-owned device workspace (256-byte aligned, at least 1280
+/* Attach caller-owned device workspace (256-byte aligned, at least 16640
  * bytes; lookme_workspace_size gives what a call needs).  The library
  * zero-fills a small counter region of it once here (hipMemset on the current
  * device); every call leaves those counters at zero again.  The workspace

@@ -14,16 +14,36 @@ hipError_t launch_project(int dt, const void* x, const void* wt, void* q, int64_
                           int d_e, int layers, hipStream_t st);
 
 // ---- routing: scene[r] = argmax_s <q_r, K1[s]> + bias[s] over rows r -------
-// Small batches split the scene keys of a 16-row tile over several
-// workgroups; `part` ([ROUTE_PART_ENTRIES] of (scene, score) pairs) and
-// `count` ([ROUTE_MAX_TILES], zero before the first call, left zero by each
-// call) carry the partial results.
-constexpr int ROUTE_MAX_TILES = 256;
-constexpr int ROUTE_PART_ENTRIES = (512 + ROUTE_MAX_TILES) * 16;
-void route_split(int64_t rows, int S, int* splits, int* kps);
+// Three kernels, by batch size (route_plan):
+//  * ROUTE_DTL: batches of ROUTE_DTL_MIN_ROWS to 128 * ROUTE_DTL_MAX_BLOCKS rows
+//    whose key rows are whole 128-byte steps (larger batches run faster in
+//    the shared mode): 128-row blocks x 256-key tiles on the matrix cores
+//    (route.hip), the key tiles of a block split over up to `splits`
+//    workgroups of `per_split` tiles when there are few blocks;
+//  * ROUTE_STREAM: small batches, 16-row tiles in the scoring kernel's
+//    streaming mode, the keys split over `splits` workgroups of `per_split`
+//    keys;
+//  * ROUTE_SHARED: the scoring kernel's shared mode (64- or 128-row units).
+// Split work meets in route_partial: `part` holds part_entries (scene, score)
+// pairs, `count` ROUTE_COUNTERS arrival counters that are zero before the
+// first call and left at zero by every call.
+constexpr int ROUTE_STREAM = 0, ROUTE_SHARED = 1, ROUTE_DTL = 2;
+constexpr int ROUTE_DTL_ROWS = 128, ROUTE_DTL_KEYS = 256, ROUTE_DTL_MAX_TPS = 16;
+constexpr int64_t ROUTE_DTL_MIN_ROWS = 4096, ROUTE_DTL_MAX_BLOCKS = 512;
+constexpr int ROUTE_COUNTERS = 4096;
+struct RoutePlan {
+  int mode;
+  int splits;
+  int per_split;          // DTL: 256-key tiles; STREAM: keys (a multiple of 64)
+  int64_t part_entries;
+};
+RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes);
 hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
                         int32_t* scene, int64_t rows, int d_e, int S, uint64_t* part,
                         int32_t* count, hipStream_t st);
+hipError_t launch_route_dtl(int dt, const void* q, const void* scene_keys, const float* bias,
+                            int32_t* scene, int64_t rows, int d_e, int S, const RoutePlan& plan,
+                            uint64_t* part, int32_t* count, hipStream_t st);
 
 // ---- bucketing of rows by scene -----------------------------------------
 // Level-2 work units: a bucket of at most UNIT_STREAM_ROWS rows is one

@@ -71,7 +71,7 @@ struct Layout {
 // The leading bytes of the workspace hold counters that start at zero; they
 // are zero-filled once when the workspace is attached and every call leaves
 // them at zero.
-constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_MAX_TILES * 4;
+constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_COUNTERS * 4;
 
 Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n) {
   const int64_t rows = (int64_t)layers * n;
@@ -85,8 +85,10 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n) {
     return at;
   };
   L.unit_count = take(256);   // counters first: the region zeroed at set-up
-  L.route_count = take((size_t)lookme::ROUTE_MAX_TILES * 4);
-  L.route_part = take((size_t)lookme::ROUTE_PART_ENTRIES * 8);
+  L.route_count = take((size_t)lookme::ROUTE_COUNTERS * 4);
+  const lookme::RoutePlan plan =
+      lookme::route_plan(rows, d.num_scenes, (int64_t)d.key_dim * elem_size(d.dtype));
+  L.route_part = take((size_t)plan.part_entries * 8);
   L.chunk_hist = take((size_t)chunks * d.num_scenes * 4);
   L.local_rank = take((size_t)rows * 4);
   L.offsets = take(((size_t)d.num_scenes + 1) * 4);

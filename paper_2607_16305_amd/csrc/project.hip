@@ -13,6 +13,7 @@
 #include <type_traits>
 
 #include "common.h"
+#include "dtl.h"
 #include "kernels.h"
 
 namespace lookme {
@@ -217,34 +218,6 @@ __global__ __launch_bounds__(PJ_THREADS * KG) void project_kernel(
 // With NS >= 3 the fragments of stage s + 1 are read while the matrix cores
 // work on stage s; with NS = 2 the loads of stage s + 1 fly during stage s.
 // Needs K in whole KB-byte steps.
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
-// One direct global-to-LDS load of 16 bytes per lane: lane i's bytes land at
-// lds_dst + 16 i (lds_dst is the same for the whole wave).  A plain function,
-// so that the builtin is never looked at in a dependent context.
-__device__ __forceinline__ void load_lds16(const void* src, char* lds_dst) {
-  __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)lds_dst, 16, 0, 0);
-}
-
-// chunk c of row r of a block sits in slot c ^ blk_swz(r): rows that share a
-// 128-byte or 256-byte bank window get distinct slots for one chunk index
-template <int KB>
-__device__ __forceinline__ int blk_swz(int r) {
-  if constexpr (KB == 64) return ((r >> 1) & 3) ^ ((r >> 3) & 1);
-  else return (r & 7) ^ ((r >> 3) & 1);
-}
-
-template <int WM, int WN, int MI, int NJ, int KB>
-struct DtlShape {
-  static_assert(KB == 64 || KB == 128, "stage width");
-  static constexpr int BM = 16 * MI * WM, BN = 16 * NJ * WN;
-  static constexpr int STAGE = (BM + BN) * KB;               // bytes per stage
-  static constexpr int INSTR = STAGE / 1024;                 // load instructions per stage
-  static constexpr int PER_WAVE = INSTR / (WM * WN);
-  static_assert(PER_WAVE * WM * WN == INSTR, "loads split evenly over the waves");
-  static constexpr int LPR = KB / 16, RPI = 64 / LPR;        // lanes per row, rows per load
-};
-
 template <int DT, int WM, int WN, int MI, int NJ, int KB, int NS>
 __global__ __launch_bounds__(64 * WM * WN) void project_dtl_kernel(
     const char* __restrict__ A, const char* __restrict__ B, char* __restrict__ Q, int64_t M,

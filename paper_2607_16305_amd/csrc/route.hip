@@ -1,0 +1,236 @@
+// Level-1 scene routing of large batches (arXiv 2607.16305, Sec. 3.2, Eq. 5)
+// as a tiled product on the matrix cores with a fused arg max: scene[r] =
+// argmax_s <q_r, K1[s]> + b[s], lowest s on exact ties; the scores are never
+// written to memory.
+//
+// A workgroup owns 128 query rows and a range of 256-key tiles; 8 waves in a
+// 2 x 4 grid each compute a 64 x 64 block of every tile.  The queries and the
+// keys of a tile stream through LDS in 128-byte K stages by direct global-to-
+// LDS loads (dtl.h), one stream of stages across all of the workgroup's key
+// tiles, the next stage in flight while one is multiplied.  After a tile's
+// last stage every lane folds its scores (plus the bias, staged in LDS) into
+// a running best per row; at the end the 16 lanes and then the 4 waves that
+// share a row are merged in key order.  When a batch has few row blocks the
+// key tiles are split over several workgroups and the partial arg maxima
+// meet in route_partial (route_merge.h).
+#include "common.h"
+#include "dtl.h"
+#include "kernels.h"
+#include "route_merge.h"
+
+namespace lookme {
+
+// WM x WN waves, each MI x NJ MFMA tiles; K stages of KB bytes, NS buffers
+constexpr int RT_WM = 2, RT_WN = 4, RT_MI = 4, RT_NJ = 4, RT_KB = 128, RT_NS = 2;
+using RtShape = DtlShape<RT_WM, RT_WN, RT_MI, RT_NJ, RT_KB>;
+static_assert(RtShape::BM == ROUTE_DTL_ROWS && RtShape::BN == ROUTE_DTL_KEYS, "tile shape");
+
+struct RouteDtlParams {
+  const char* q;         // [rows, d_e]
+  const char* keys;      // [S, d_e]
+  const float* bias;     // [S] or null
+  int64_t rows;
+  int64_t k_bytes;       // d_e * elem size, a multiple of 128
+  int S;
+  int splits;            // key ranges per row block
+  int tps;               // 256-key tiles per range
+  int units;             // row blocks * splits
+  int32_t* scene;
+  uint64_t* part;
+  int32_t* count;
+};
+
+template <int DT>
+__global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlParams a) {
+  using S = RtShape;
+  constexpr int MI = RT_MI, NJ = RT_NJ, KB = RT_KB, KSL = KB / 64, NS = RT_NS;
+  constexpr int THREADS = 64 * RT_WM * RT_WN;
+  __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
+  __shared__ float s_bias[ROUTE_DTL_MAX_TPS * S::BN];
+  __shared__ float m_s[RT_WN][S::BM];
+  __shared__ int m_i[RT_WN][S::BM];
+  static_assert(NS >= 2, "a stage in flight while one is multiplied");
+  __shared__ int s_last;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n16 = lane & 15, g = lane >> 4;
+  const int wni = wv % RT_WN;
+  const int wm = (wv / RT_WN) * 16 * MI, wn = wni * 16 * NJ;
+
+  const int u = xcd_remap(blockIdx.x, a.units);
+  if (u < 0) return;
+  const int64_t rb = u / a.splits;
+  const int split = u % a.splits;
+  const int64_t m0 = rb * S::BM;
+  const int ntiles = (a.S + S::BN - 1) / S::BN;
+  const int kt0 = split * a.tps, kt1 = min(ntiles, kt0 + a.tps);
+  const int nst = (int)(a.k_bytes / KB);
+  const int total = (kt1 - kt0) * nst;   // K stages of this unit, tile by tile
+
+  // the bias of the unit's keys (0 past the last scene: those keys are
+  // masked by index anyway)
+  for (int i = tid; i < (kt1 - kt0) * S::BN; i += THREADS) {
+    const int key = kt0 * S::BN + i;
+    s_bias[i] = (a.bias != nullptr && key < a.S) ? a.bias[key] : 0.f;
+  }
+
+  // load b of a stage covers tile rows [trow - lane / LPR, + RPI): the query
+  // rows come first, then the 256 key rows of the stage's tile; rows past
+  // either operand are clamped into it (they feed no stored result)
+  int trow[S::PER_WAVE], chunk[S::PER_WAVE];
+#pragma unroll
+  for (int b = 0; b < S::PER_WAVE; ++b) {
+    trow[b] = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
+    chunk[b] = (lane % S::LPR) ^ blk_swz<KB>(trow[b] & 15);
+  }
+  auto issue = [&](int sigma) {
+    const int sg = sigma < total ? sigma : total - 1;   // past the end: a harmless reload
+    const int tile = kt0 + sg / nst, s = sg % nst;
+    char* dst = lds[sigma % NS];
+#pragma unroll
+    for (int b = 0; b < S::PER_WAVE; ++b) {
+      const char* src;
+      if (trow[b] < S::BM) {
+        int64_t r = m0 + trow[b];
+        r = r < a.rows ? r : a.rows - 1;
+        src = a.q + r * a.k_bytes;
+      } else {
+        int r = tile * S::BN + trow[b] - S::BM;
+        r = r < a.S ? r : a.S - 1;
+        src = a.keys + (int64_t)r * a.k_bytes;
+      }
+      load_lds16(src + (int64_t)s * KB + chunk[b] * 16, dst + (wv * S::PER_WAVE + b) * 1024);
+    }
+  };
+
+  f32x4_t acc[MI][NJ];
+  float bs[MI][4];
+  int bi[MI][4];
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      bs[i][r] = -__builtin_inff();
+      bi[i][r] = -1;
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i) issue(i);
+  for (int sigma = 0; sigma < total; ++sigma) {
+    // this wave's loads of stage sigma have landed once at most those of the
+    // NS - 2 younger stages are outstanding; the barrier makes every wave's
+    // visible (and the bias table, the first time) and ends every read of
+    // stage sigma - 1, whose buffer the next loads fill (a plain s_barrier:
+    // the fence of __syncthreads would wait for every load in flight; the
+    // empty asm statements keep LDS accesses on their side)
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NS - 2) * S::PER_WAVE) : "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(sigma + NS - 1);
+    const char* buf = lds[sigma % NS];
+#pragma unroll
+    for (int ks = 0; ks < KSL; ++ks) {
+      u32x4_t fa[MI], fb[NJ];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) fa[i] = read_frag<KB>(buf, wm + 16 * i, ks, n16, g);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_chunk<DT>(fa[i], fb[j], acc[i][j]);
+    }
+    if (sigma % nst == nst - 1) {
+      // the tile is complete: the lane holds rows wm + 16 i + 4 g + r and
+      // keys tile * 256 + wn + 16 j + n16 (increasing in j: '>' keeps the first)
+      const int tl = sigma / nst;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int kin = tl * S::BN + wn + 16 * j + n16;   // index within the unit's keys
+        const int key = kt0 * S::BN + kin;
+        const float b = s_bias[kin];
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v = key < a.S ? acc[i][j][r] + b : -__builtin_inff();
+            if (v > bs[i][r]) {
+              bs[i][r] = v;
+              bi[i][r] = key;
+            }
+            acc[i][j][r] = 0.f;
+          }
+      }
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
+
+  // merge the 16 lanes of a row group (keys n16 + 16 j of every tile), then
+  // the 4 waves that share rows, in key order
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+#pragma unroll
+      for (int d = 1; d < 16; d <<= 1) {
+        const float os = __shfl_xor(bs[i][r], d, 64);
+        const int oi = __shfl_xor(bi[i][r], d, 64);
+        if (beats(os, oi, bs[i][r], bi[i][r])) {
+          bs[i][r] = os;
+          bi[i][r] = oi;
+        }
+      }
+      if (n16 == 0) {
+        m_s[wni][wm + 16 * i + 4 * g + r] = bs[i][r];
+        m_i[wni][wm + 16 * i + 4 * g + r] = bi[i][r];
+      }
+    }
+  __syncthreads();
+  const int nr = (int)min<int64_t>(S::BM, a.rows - m0);
+  float best_s = -__builtin_inff();
+  int best_i = -1;
+  if (tid < S::BM) {
+#pragma unroll
+    for (int w = 0; w < RT_WN; ++w)
+      if (beats(m_s[w][tid], m_i[w][tid], best_s, best_i)) {
+        best_s = m_s[w][tid];
+        best_i = m_i[w][tid];
+      }
+  }
+  if (a.splits == 1) {
+    if (tid < nr) a.scene[m0 + tid] = best_i;
+    return;
+  }
+  route_partial<S::BM>(a.part, a.count, a.splits, a.scene, rb, split, tid < S::BM ? tid : S::BM,
+                       nr, best_s, best_i, &s_last);
+}
+
+hipError_t launch_route_dtl(int dt, const void* q, const void* scene_keys, const float* bias,
+                            int32_t* scene, int64_t rows, int d_e, int S, const RoutePlan& plan,
+                            uint64_t* part, int32_t* count, hipStream_t st) {
+  RouteDtlParams p{};
+  p.q = static_cast<const char*>(q);
+  p.keys = static_cast<const char*>(scene_keys);
+  p.bias = bias;
+  p.rows = rows;
+  p.k_bytes = (int64_t)d_e * (dt == DT_BF16 ? 2 : 4);
+  p.S = S;
+  p.splits = plan.splits;
+  p.tps = plan.per_split;
+  p.units = (int)(((rows + RtShape::BM - 1) / RtShape::BM) * plan.splits);
+  p.scene = scene;
+  p.part = part;
+  p.count = count;
+  const unsigned grid = (unsigned)((p.units + 7) / 8 * 8);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(route_dtl_kernel<DT_BF16>, dim3(grid), dim3(64 * RT_WM * RT_WN), 0, st, p);
+  else
+    hipLaunchKernelGGL(route_dtl_kernel<DT_F32>, dim3(grid), dim3(64 * RT_WM * RT_WN), 0, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace lookme

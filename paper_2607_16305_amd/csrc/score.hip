@@ -24,6 +24,7 @@
 //    many rows.
 #include "common.h"
 #include "kernels.h"
+#include "route_merge.h"
 
 namespace lookme {
 
@@ -172,41 +173,6 @@ __device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, i
 // ---------------------------------------------------------------------------
 // Streaming mode: <= 16 rows, key blocks split over the waves
 // ---------------------------------------------------------------------------
-// Routing with the keys split over several workgroups: the workgroup's best
-// (score, scene) of each row goes to the partial table; the last of a tile's
-// workgroups to arrive (device-scope counter) reduces the tile's partials in
-// key-range order with the lowest-index tie rule, writes the scenes and
-// resets the counter for the next call.
-__device__ __forceinline__ void route_partial(const ScoreParams& a, int64_t tile, int split,
-                                              int t, int nr, float best_s, int best_i,
-                                              int* s_last) {
-  const int splits = a.route_splits;
-  uint64_t* part = a.route_part + (tile * splits) * 16;
-  if (t < nr)
-    part[split * 16 + t] = ((uint64_t)(uint32_t)best_i << 32) | __float_as_uint(best_s);
-  // the barrier orders every thread's store before thread 0's release; the
-  // acquire half makes the other workgroups' partials visible to the last
-  __syncthreads();
-  if (threadIdx.x == 0)
-    *s_last = __hip_atomic_fetch_add(&a.route_count[tile], 1, __ATOMIC_ACQ_REL,
-                                     __HIP_MEMORY_SCOPE_AGENT) == splits - 1;
-  __syncthreads();
-  if (!*s_last) return;
-  if (t < nr) {
-    float bs = -__builtin_inff();
-    int bi = -1;
-    for (int sp = 0; sp < splits; ++sp) {
-      const uint64_t v = __hip_atomic_load(&part[sp * 16 + t], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-      const float vs = __uint_as_float((uint32_t)v);
-      const int vi = (int)(v >> 32);
-      if (beats(vs, vi, bs, bi)) { bs = vs; bi = vi; }
-    }
-    a.out_idx[tile * 16 + t] = bi;
-  }
-  if (threadIdx.x == 0) a.route_count[tile] = 0;
-}
-
 // key0, nkeys: the unit's key range (routing may split the keys; Level-2
 // units take all P keys of their scene, key0 = 0).
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
@@ -299,7 +265,9 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
     top_i[0] += key0;
     if (a.route_splits > 1) {
       __shared__ int s_last;
-      route_partial(a, begin / 16, split, L == 0 ? t : 16, nr, top_s[0], top_i[0], &s_last);
+      route_partial<UNIT_STREAM_ROWS>(a.route_part, a.route_count, a.route_splits, a.out_idx,
+                                      begin / 16, split, L == 0 ? t : 16, nr, top_s[0], top_i[0],
+                                      &s_last);
       return;
     }
   }
@@ -502,21 +470,49 @@ static int route_unit_rows(int64_t rows, int shared_rows) {
   return UNIT_STREAM_ROWS;
 }
 
-// Streaming routing of a small batch splits the keys of every 16-row tile
-// over several workgroups (at least 64 keys each) until about 512
-// workgroups run; batches of more than ROUTE_MAX_TILES tiles do not split.
-void route_split(int64_t rows, int S, int* splits, int* kps) {
-  const int64_t tiles = (rows + 15) / 16;
-  int sp = 1;
-  if (tiles <= ROUTE_MAX_TILES) {
-    const int want = (int)((512 + tiles - 1) / tiles);
-    const int most = (S + 63) / 64;
-    sp = want < most ? want : most;
-    if (sp < 1) sp = 1;
+static int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes) {
+  RoutePlan p{ROUTE_SHARED, 1, S, 0};
+  if (rows <= 0 || S <= 0) return p;
+  const int64_t blocks = (rows + ROUTE_DTL_ROWS - 1) / ROUTE_DTL_ROWS;
+  if (rows >= ROUTE_DTL_MIN_ROWS && blocks < ROUTE_DTL_MAX_BLOCKS && row_bytes % 128 == 0) {
+    // enough 128-row blocks for the matrix-core kernel but too few to fill
+    // the chip with the shared-mode units; split the key tiles until about
+    // 512 workgroups run (and at most ROUTE_DTL_MAX_TPS tiles stay with one
+    // workgroup, whose bias table lives in LDS)
+    const int tiles = cdiv(S, ROUTE_DTL_KEYS);
+    int sp = blocks < 512 ? cdiv(512, blocks) : 1;
+    sp = sp < tiles ? sp : tiles;
+    const int least = cdiv(tiles, ROUTE_DTL_MAX_TPS);
+    sp = sp > least ? sp : least;
+    const int tps = cdiv(tiles, sp);
+    sp = cdiv(tiles, tps);
+    if (sp == 1 || blocks <= ROUTE_COUNTERS) {
+      p.mode = ROUTE_DTL;
+      p.splits = sp;
+      p.per_split = tps;
+      p.part_entries = sp > 1 ? blocks * sp * ROUTE_DTL_ROWS : 0;
+      return p;
+    }
   }
-  const int per = (S + sp - 1) / sp;
-  *kps = (per + 63) / 64 * 64;
-  *splits = (S + *kps - 1) / *kps;
+  if (route_unit_rows(rows, shared_unit_rows(row_bytes, 1)) == UNIT_STREAM_ROWS) {
+    // small batch: split the keys of every 16-row tile (at least 64 keys a
+    // workgroup) until about 512 workgroups run
+    const int64_t tiles = (rows + 15) / 16;
+    int sp = 1;
+    if (tiles <= ROUTE_COUNTERS) {
+      sp = tiles < 512 ? cdiv(512, tiles) : 1;
+      const int most = cdiv(S, 64);
+      sp = sp < most ? sp : most;
+    }
+    const int kps = cdiv(cdiv(S, sp), 64) * 64;
+    p.mode = ROUTE_STREAM;
+    p.splits = cdiv(S, kps);
+    p.per_split = kps;
+    p.part_entries = p.splits > 1 ? tiles * p.splits * UNIT_STREAM_ROWS : 0;
+  }
+  return p;
 }
 
 hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
@@ -534,9 +530,12 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
   p.k = 1;
   p.route_rows = route_unit_rows(rows, shared_unit_rows(p.row_bytes, 1));
   p.out_idx = scene;
-  p.route_splits = 1;
-  p.route_kps = S;
-  if (p.route_rows == UNIT_STREAM_ROWS) route_split(rows, S, &p.route_splits, &p.route_kps);
+  const RoutePlan plan = route_plan(rows, S, p.row_bytes);
+  if (plan.mode == ROUTE_DTL)
+    return launch_route_dtl(dt, q, scene_keys, bias, scene, rows, d_e, S, plan, part, count, st);
+  p.route_rows = plan.mode == ROUTE_STREAM ? UNIT_STREAM_ROWS : p.route_rows;
+  p.route_splits = plan.mode == ROUTE_STREAM ? plan.splits : 1;
+  p.route_kps = plan.mode == ROUTE_STREAM ? plan.per_split : S;
   p.route_part = part;
   p.route_count = count;
   const int64_t units = (rows + p.route_rows - 1) / p.route_rows * p.route_splits;

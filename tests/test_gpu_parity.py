@@ -104,14 +104,28 @@ def test_integer_scores_tie_break_exactly(dtype):
     assert not rep.exemptions, rep.exemptions
 
 
-@pytest.mark.parametrize("layers,with_bias", [(1, True), (2, False)])
-def test_routing_with_split_keys(layers, with_bias):
-    """Small batches split the scene keys of a 16-row tile over several
-    workgroups (here 5 ranges of 64, 64, 64, 64 and 44 keys; 13 or 25 tiles,
-    the last one ragged); the scene is the arg max over all of them, bias
-    included, and repeated calls reuse the arrival counters."""
-    wl = Workload("bf16_split_route", "bf16", 200, layers, 256, 256, 300, 16, 32, 32, 4, 25,
-                  usage="uniform")
+SPLIT_ROUTE = {
+    # 16-row tiles, keys in 5 ranges of 64, 64, 64, 64 and 44 (13 / 25 tiles)
+    "stream_l1_bias": (Workload("bf16_split_route", "bf16", 200, 1, 256, 256, 300, 16, 32, 32,
+                                4, 25, usage="uniform"), True),
+    "stream_l2": (Workload("bf16_split_route", "bf16", 200, 2, 256, 256, 300, 16, 32, 32, 4,
+                           25, usage="uniform"), False),
+    # matrix-core kernel: 33 blocks of 128 rows (the last ragged) x 3 key
+    # tiles of 256, 256 and 188 keys, one tile per workgroup
+    "tiles_bias": (Workload("bf16_tile_route", "bf16", 4100, 1, 256, 256, 700, 16, 32, 32, 4,
+                            20, usage="uniform"), True),
+    # fp32, 2 key tiles (256 + 44) over 2 workgroups
+    "tiles_f32": (Workload("f32_tile_route", "f32", 4200, 1, 128, 128, 300, 16, 32, 32, 4, 20,
+                           usage="iid"), False),
+}
+
+
+@pytest.mark.parametrize("case", list(SPLIT_ROUTE))
+def test_routing_with_split_keys(case):
+    """Routing splits the scene keys of a row tile over several workgroups;
+    the scene is the arg max over all of them, bias included, and repeated
+    calls reuse the arrival counters."""
+    wl, with_bias = SPLIT_ROUTE[case]
     _announce(f"split routing: {wl}, bias={with_bias}")
     inp = make_inputs(wl, seed=12, device=DEV)
     if with_bias:
