@@ -62,13 +62,15 @@ inline int score_ks(int64_t row_bytes) {
   if (ks == 4 || ks == 8 || ks == 16 || ks == 32) return (int)ks;
   return ks < 4 ? 4 : 32;
 }
-// Rows of a shared unit: each of its 4 waves keeps two 16-row query tiles in
-// registers when the kernel runs at most 16 chunk steps and k <= 8, one tile
-// otherwise (two 32-step tiles would need 64 fragment loads in flight, more
-// than the 6-bit vector-memory counter of a wave can track; with k = 16 the
-// two tiles' candidate lists would halve the waves a SIMD can hold).
+// Rows of a shared unit.  Level-2 (k > 0): 64, one 16-row query tile per
+// wave (the per-lane top-k upkeep of a second tile would double each wave's
+// serial vector work and its registers, one workgroup per CU instead of two).
+// Routing (k = 0): two tiles per wave, 128 rows, when the kernel runs at most
+// 16 chunk steps (two 32-step tiles would need 64 fragment loads in flight,
+// more than the 6-bit vector-memory counter of a wave can track).
 inline int shared_unit_rows(int64_t row_bytes, int k) {
-  return (score_ks(row_bytes) <= 16 && k <= 8) ? 128 : 64;
+  if (k > 0) return 64;
+  return score_ks(row_bytes) <= 16 ? 128 : 64;
 }
 struct BucketWs {
   int32_t* chunk_hist;   // [chunks, S]

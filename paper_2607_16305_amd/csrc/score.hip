@@ -16,12 +16,12 @@
 //    registers, two blocks in flight.  At the end the 16 per-lane lists of
 //    every row are merged in parallel (one thread per list, k rounds of a
 //    butterfly arg max).  Suits the many small buckets: all 4 waves compute.
-//  * shared (up to 128 rows): every 16-key block is loaded once by the whole
-//    workgroup into an LDS tile (double-buffered, two blocks in flight in
-//    registers) and read by every wave, each holding one or two 16-row query
-//    tiles; the key stream is paid once for up to 8 tiles.  Lists are merged
-//    inside the wave (4 lanes per row).  Suits large buckets and routing of
-//    many rows.
+//  * shared (64 rows for Level-2, 128 for routing): every 16-key block is
+//    loaded once by the whole workgroup into an LDS tile (double-buffered,
+//    two blocks in flight in registers) and read by every wave, each holding
+//    one 16-row query tile (two for routing); the key stream is paid once for
+//    up to 4 (8) tiles.  Lists are merged inside the wave (4 lanes per row).
+//    Suits large buckets and routing of many rows.
 #include "common.h"
 #include "kernels.h"
 #include "route_merge.h"
@@ -287,9 +287,9 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, g = lane >> 4;
   const int nkeys = a.nkeys;
-  // a wave keeps two 16-row query tiles (rows 16 w.. and 16 (w+4)..) when a
-  // key row is at most 1 KiB and k <= 8, one otherwise (see shared_unit_rows)
-  constexpr bool TWO_TILES = KS <= 16 && KL <= 8;
+  // routing: a wave keeps two 16-row query tiles (rows 16 w.. and 16 (w+4)..)
+  // when a key row is at most 1 KiB; Level-2: one (see shared_unit_rows)
+  constexpr bool TWO_TILES = !LOOKUP && KS <= 16;
   const int tiles = (nr + 15) >> 4;
   const bool has0 = wv < tiles, has1 = TWO_TILES && wv + SC_WAVES < tiles;
 
@@ -496,7 +496,7 @@ RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes) {
       return p;
     }
   }
-  if (route_unit_rows(rows, shared_unit_rows(row_bytes, 1)) == UNIT_STREAM_ROWS) {
+  if (route_unit_rows(rows, shared_unit_rows(row_bytes, 0)) == UNIT_STREAM_ROWS) {
     // small batch: split the keys of every 16-row tile (at least 64 keys a
     // workgroup) until about 512 workgroups run
     const int64_t tiles = (rows + 15) / 16;
@@ -528,7 +528,7 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
   p.ks = (int)(p.row_bytes / 64);
   p.nkeys = S;
   p.k = 1;
-  p.route_rows = route_unit_rows(rows, shared_unit_rows(p.row_bytes, 1));
+  p.route_rows = route_unit_rows(rows, shared_unit_rows(p.row_bytes, 0));
   p.out_idx = scene;
   const RoutePlan plan = route_plan(rows, S, p.row_bytes);
   if (plan.mode == ROUTE_DTL)
