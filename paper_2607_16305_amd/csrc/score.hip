@@ -81,25 +81,36 @@ __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int ken
       if (x > ls[0]) { ls[0] = x; li[0] = p; }
     }
   } else {
-    const float best = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-    if (best > ls[KL - 1]) {
+    // The 4 values go in largest first (the first of equal values, i.e. the
+    // lowest key), one insertion round per value that still beats some
+    // lane's list: the rounds are wave-wide (branch-free sorted insertion),
+    // and after the first blocks a round is rarely needed by any lane, so
+    // most blocks cost one vote instead of four insertions.
+    const int p0 = blk * 16 + 4 * g;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int p = blk * 16 + 4 * g + r;
-        const float x = v[r];
+    for (int round = 0; round < 4; ++round) {
+      float x = v[0];
+      int w = 0;
 #pragma unroll
-        for (int e = KL - 1; e >= 1; --e) {
-          const bool above_prev = x > ls[e - 1];
-          const bool above_cur = x > ls[e];
-          const float s_keep = above_cur ? x : ls[e];
-          const int i_keep = above_cur ? p : li[e];
-          ls[e] = above_prev ? ls[e - 1] : s_keep;
-          li[e] = above_prev ? li[e - 1] : i_keep;
-        }
-        const bool top = x > ls[0];
-        ls[0] = top ? x : ls[0];
-        li[0] = top ? p : li[0];
+      for (int r = 1; r < 4; ++r)
+        if (v[r] > x) { x = v[r]; w = r; }
+      if (!__any(x > ls[KL - 1])) break;
+      const int p = p0 + w;
+#pragma unroll
+      for (int e = KL - 1; e >= 1; --e) {
+        const bool above_prev = x > ls[e - 1];
+        const bool above_cur = x > ls[e];
+        const float s_keep = above_cur ? x : ls[e];
+        const int i_keep = above_cur ? p : li[e];
+        ls[e] = above_prev ? ls[e - 1] : s_keep;
+        li[e] = above_prev ? li[e - 1] : i_keep;
       }
+      const bool top = x > ls[0];
+      ls[0] = top ? x : ls[0];
+      li[0] = top ? p : li[0];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (r == w) v[r] = -__builtin_inff();
     }
   }
 }
