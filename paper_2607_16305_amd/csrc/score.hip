@@ -414,9 +414,11 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   const char* keys;
   int key0 = 0, nk = a.nkeys, split = 0;
   if constexpr (LOOKUP) {
-    // units in list order (the long shared units first, spread over the
-    // XCDs by the round-robin dispatch)
-    const int u = blockIdx.x;
+    // units in list order (the long shared units first), dealt to the XCDs
+    // in pairs: a scene whose bucket spans two units reads its keys into one
+    // XCD's L2 once, while a scene with many units is still spread over all
+    const int b = blockIdx.x, slot = b >> 3;
+    const int u = (slot >> 1) * 16 + (b & 7) * 2 + (slot & 1);
     if (u >= *a.unit_count) return;
     const int tag = a.unit_scene[u];
     const int s = tag & ~UNIT_SHARED;
@@ -570,7 +572,7 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
   p.k = k;
   p.out_idx = prim;
   p.out_w = w;
-  const int grid = (int)ws.max_units;
+  const int grid = (int)((ws.max_units + 15) / 16 * 16);   // whole pairs on every XCD
   if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st);
   if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st);
   if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st);
