@@ -57,6 +57,12 @@ SMALL = {
     "bf16_k_eq_p": Workload("bf16_k_eq_p", "bf16", 40, 1, 128, 128, 2, 16, 64, 64, 16, 50),
     "bf16_k32": Workload("bf16_k32", "bf16", 40, 1, 128, 128, 2, 40, 64, 64, 32, 50),
     "bf16_one_scene": Workload("bf16_one_scene", "bf16", 33, 1, 128, 256, 1, 19, 32, 32, 4, 50),
+    # buckets of about 150 rows: shared units (64 rows, the last ragged) with
+    # the widest lists, and fp32 with k = 16
+    "bf16_k32_shared": Workload("bf16_k32_shared", "bf16", 300, 1, 128, 128, 2, 70, 32, 32, 32,
+                                30, usage="uniform"),
+    "f32_k16_shared": Workload("f32_k16_shared", "f32", 450, 1, 64, 128, 3, 90, 16, 16, 16, 30,
+                               usage="uniform"),
     "bf16_one_prim": Workload("bf16_one_prim", "bf16", 21, 1, 64, 64, 9, 1, 16, 16, 1, 50),
     "bf16_one_token": Workload("bf16_one_token", "bf16", 1, 1, 64, 64, 9, 24, 16, 16, 4, 100),
     # projections large enough for the direct-to-LDS kernel (>= 256 tiles of
