@@ -23,12 +23,14 @@
 //    up to 4 (8) tiles.  Lists are merged inside the wave (4 lanes per row).
 //    Suits large buckets and routing of many rows.
 #include "common.h"
+#include "dtl.h"
 #include "kernels.h"
 #include "route_merge.h"
 
 namespace lookme {
 
 constexpr int SC_WAVES = 4;
+constexpr int SH_LDS_BYTES = 48 * 1024;   // LDS for a shared unit's key block images
 constexpr int SC_THREADS = SC_WAVES * WAVE;
 
 struct ScoreParams {
@@ -288,11 +290,19 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
 // ---------------------------------------------------------------------------
 // Shared mode: up to 128 rows, every key block staged once in LDS
 // ---------------------------------------------------------------------------
+// Key block images kept in LDS by a shared unit: as many as SH_LDS_BYTES
+// hold, at least 2 and at most 8.
+constexpr int shared_nbuf(int ks) {
+  return SH_LDS_BYTES / (ks * 1024) < 2 ? 2
+         : SH_LDS_BYTES / (ks * 1024) > 8 ? 8
+                                          : SH_LDS_BYTES / (ks * 1024);
+}
+
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
 __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, int64_t begin,
                                             int nr, const char* keys) {
-  constexpr int CPT = KS / 4;          // 16-byte chunks per thread per key block
   constexpr int BLOCK_BYTES = KS * 1024;
+  constexpr int CPT = KS / 4;          // routing: 16-byte chunks per thread per key block
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -322,26 +332,6 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
   }
 
   const int nblk = (nkeys + 15) >> 4;
-  // LDS image of a block: segment j (1 KiB) holds, at lane slot L, chunk
-  // 4j + (L >> 4) of key row (L & 15): exactly the operand-A fragment of
-  // lane L at step j, so each wave reads it with one conflict-free 16-byte
-  // load per lane.  Thread tid fills slots c = tid + 256 i.
-  auto gload = [&](u32x4_t (&r)[CPT], int blk) {
-    blk = min(blk, nblk - 1);          // unconditional: past the end, an L2 hit
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + SC_THREADS * i;
-      const int j = c >> 6, L = c & 63;
-      const int row = min(blk * 16 + (L & 15), nkeys - 1);
-      r[i] = (!MASKED || j < a.ks)
-                 ? ld16(keys + (int64_t)row * a.row_bytes + (4 * j + (L >> 4)) * 16)
-                 : u32x4_t{0, 0, 0, 0};
-    }
-  };
-  auto lstore = [&](int buf, const u32x4_t (&r)[CPT]) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) st16(smem + buf * BLOCK_BYTES + (tid + SC_THREADS * i) * 16, r[i]);
-  };
   auto compute = [&](int buf, int blk) {
     if (!has0) return;                 // a wave without rows only helps to load
     f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
@@ -359,28 +349,87 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
     if (has1) fold_scores<LOOKUP, KL>(acc1, blk, g, nkeys, a.bias, ls1, li1);
   };
 
-  // Pipeline: at the top of step b the LDS buffer b%2 holds block b, the
-  // register set for block b+1 and the one for block b+2 are in flight.
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
-  u32x4_t r0[CPT], r1[CPT];
-  gload(r0, 0);
-  asm volatile("" ::: "memory");
-  gload(r1, 1);
-  lstore(0, r0);
-  __syncthreads();
-  gload(r0, 2);
-  int blk = 0;
-  for (; blk + 1 < nblk; blk += 2) {
-    compute(0, blk);
-    lstore(1, r1);          // block blk+1 (buffer 1 was last read two steps ago)
+  if constexpr (LOOKUP) {
+    // LDS image of a block: segment j (1 KiB) holds, at lane slot L, chunk
+    // 4j + (L >> 4) of key row (L & 15): exactly the operand-A fragment of
+    // lane L at step j, so each wave reads it with one conflict-free 16-byte
+    // load per lane.  The segments go straight from global memory to LDS
+    // (global_load_lds: lane L's 16 bytes land at slot L), segment j by wave
+    // j % 4, into a ring of NBUF block images: NBUF - 1 blocks are in flight
+    // while one is multiplied, and no register holds them on the way.
+    constexpr int NBUF = shared_nbuf(KS);
+    constexpr int PW = KS / SC_WAVES;    // load instructions per wave and block
+    auto issue = [&](int blk) {
+      char* dst = smem + (blk % NBUF) * BLOCK_BYTES;
+      blk = min(blk, nblk - 1);          // past the end: a harmless reload
+      const char* src = keys + (int64_t)min(blk * 16 + n, nkeys - 1) * a.row_bytes + g * 16;
+#pragma unroll
+      for (int i = 0; i < PW; ++i) {
+        const int j = wv + SC_WAVES * i;
+        // masked steps reload the last real one (never multiplied)
+        const int jj = MASKED ? min(j, a.ks - 1) : j;
+        load_lds16(src + jj * 64, dst + j * 1024);
+      }
+    };
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
+#pragma unroll
+    for (int b = 0; b < NBUF - 1; ++b) issue(b);
+    for (int blk = 0; blk < nblk; ++blk) {
+      // this wave's segments of block blk have landed once at most those of
+      // the NBUF - 2 younger blocks are outstanding; the barrier makes every
+      // wave's visible and ends every read of block blk - 1, whose image the
+      // next loads overwrite (a plain s_barrier: the fence of __syncthreads
+      // would wait for every load in flight)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 2) * PW) : "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      issue(blk + NBUF - 1);
+      compute(blk % NBUF, blk);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
+  } else {
+    // routing: the same block images, staged through registers (two blocks
+    // in flight; measured faster for routing than the direct-to-LDS ring).
+    // Thread tid fills slots c = tid + 256 i.
+    auto gload = [&](u32x4_t (&r)[CPT], int blk) {
+      blk = min(blk, nblk - 1);          // unconditional: past the end, an L2 hit
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int c = tid + SC_THREADS * i;
+        const int j = c >> 6, L = c & 63;
+        const int row = min(blk * 16 + (L & 15), nkeys - 1);
+        r[i] = (!MASKED || j < a.ks)
+                   ? ld16(keys + (int64_t)row * a.row_bytes + (4 * j + (L >> 4)) * 16)
+                   : u32x4_t{0, 0, 0, 0};
+      }
+    };
+    auto lstore = [&](int buf, const u32x4_t (&r)[CPT]) {
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) st16(smem + buf * BLOCK_BYTES + (tid + SC_THREADS * i) * 16, r[i]);
+    };
+    // Pipeline: at the top of step b the LDS buffer b%2 holds block b, the
+    // register set for block b+1 and the one for block b+2 are in flight.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
+    u32x4_t r0[CPT], r1[CPT];
+    gload(r0, 0);
+    asm volatile("" ::: "memory");
+    gload(r1, 1);
+    lstore(0, r0);
     __syncthreads();
-    gload(r1, blk + 3);
-    compute(1, blk + 1);
-    lstore(0, r0);          // block blk+2
-    __syncthreads();
-    gload(r0, blk + 4);
+    gload(r0, 2);
+    int blk = 0;
+    for (; blk + 1 < nblk; blk += 2) {
+      compute(0, blk);
+      lstore(1, r1);          // block blk+1 (buffer 1 was last read two steps ago)
+      __syncthreads();
+      gload(r1, blk + 3);
+      compute(1, blk + 1);
+      lstore(0, r0);          // block blk+2
+      __syncthreads();
+      gload(r0, blk + 4);
+    }
+    if (blk < nblk) compute(0, blk);
   }
-  if (blk < nblk) compute(0, blk);
 
   // merge inside the wave: the 4 lists of row n sit in lanes n + 16 g
   const int k = LOOKUP ? a.k : 1;
@@ -404,9 +453,9 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
 __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   constexpr int MERGE_BYTES = SC_WAVES * 4 * 16 * KL * 8;
-  constexpr int STAGE_BYTES = 2 * KS * 1024;
+  constexpr int STAGE_BYTES = (LOOKUP ? shared_nbuf(KS) : 2) * KS * 1024;
   constexpr int SMEM = MERGE_BYTES > STAGE_BYTES ? MERGE_BYTES : STAGE_BYTES;
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   int64_t begin;
   int nr;
