@@ -1,11 +1,13 @@
 #!/usr/bin/env python3
 """Throughput of the LookME hot path on one MI355X.
 
-One step = lookme_route + lookme_lookup + lookme_inject over one batch of
-synthetic tokens (projection, Level-1 routing, bucketing, Level-2 top-k
-scoring with softmax, criticality select, row gather and residual add), with
-every input resident in HBM before the timed region starts.  The metric is
-tokens looked up and injected per second, counting tokens x layers.
+One step = one pass of the hot path over one batch of synthetic tokens
+(projection, Level-1 routing, bucketing, Level-2 top-k scoring with softmax,
+criticality select, row gather and residual add), with every input resident
+in HBM before the timed region starts: lookme_select runs on a second stream
+while lookme_route runs on the first (the kept set depends on neither routing
+nor lookup), then lookme_inject_kept adds the rows.  The metric is tokens
+looked up and injected per second, counting tokens x layers.
 
 The default workload is a single image on one layer (1024 tokens, 256 scenes
 x 1024 primitives, 1 GiB table, bf16).  To keep one step from finding the
@@ -193,17 +195,35 @@ class Bench:
         self.w = torch.empty((L, n, k), dtype=torch.float32, device=dev)
         self.kept = torch.empty((L, max(wl.n_keep, 1)), dtype=torch.int32, device=dev)
         self.hidden = inp["hidden"].clone()
-        self.stream = torch.cuda.current_stream().cuda_stream
+        # the kept set is selected on a second stream (default priority, as
+        # the first) while routing and lookup run; two reusable events order
+        # the streams within a step
+        self.main = torch.cuda.current_stream()
+        self.side = torch.cuda.Stream()
+        self.stream = self.main.cuda_stream
+        self.side_handle = self.side.cuda_stream
+        self.ev_start = torch.cuda.Event()
+        self.ev_kept = torch.cuda.Event()
         torch.cuda.synchronize()
 
     def step(self, i):
         lk, wl, inp = self.lk, self.wl, self.inp
         h = self.tables[i % self.copies].handle
         L, n = wl.layers, wl.n_tokens
+        # the select starts after the previous step's inject (which reads the
+        # kept buffer it overwrites) and runs beside the projection and
+        # routing; measured faster than beside the Level-2 lookup, whose
+        # workgroups it would slow
+        self.ev_start.record(self.main)
+        self.side.wait_event(self.ev_start)
+        lk.lookme_select(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.kept,
+                         self.side_handle)
+        self.ev_kept.record(self.side)
         lk.lookme_route(h, L, n, wl.d_in, inp["x"], inp["wt"], self.q, self.scene, self.stream)
         lk.lookme_lookup(h, L, n, self.q, self.scene, self.prim, self.w, self.stream)
-        lk.lookme_inject(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.scene, self.prim,
-                         self.w, self.hidden, wl.d_h, self.kept, self.stream)
+        self.main.wait_event(self.ev_kept)
+        lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
+                              self.hidden, wl.d_h, self.stream)
 
     def timed(self, steps):
         torch = self.torch

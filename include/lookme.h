@@ -150,6 +150,36 @@ lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_k
                               int32_t d_h, int32_t* kept_out, void* stream);
 
 /*
+ * lookme_select -- the sparse injection set alone (Eq. 9): c_t = ||crit_t||_2
+ * for every token, then per layer the n_keep tokens of largest c_t (ties:
+ * lowest t) written to
+ *   kept_out [layers, n_keep] int32, ascending token ids
+ * -- the set that lookme_inject selects.  It reads no routing or lookup
+ * result and its part of the workspace is disjoint from theirs, so it may run
+ * on another stream, concurrently with lookme_route / lookme_lookup of the
+ * same batch; lookme_inject_kept then adds the rows.  Requires
+ * 0 <= n_keep <= n, d_c * elem_size a multiple of 16 bytes, kept_out non-NULL
+ * when n_keep > 0 (n_keep = 0 does nothing).  Needs the workspace of
+ * lookme_workspace_size.
+ */
+lookme_status_t lookme_select(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                              const void* crit, int32_t d_c, int32_t* kept_out, void* stream);
+
+/*
+ * lookme_inject_kept -- the gather and residual add of lookme_inject (Eq. 10,
+ * Eq. 2) for a kept set computed beforehand:
+ *   kept [layers, n_keep] int32   token ids of each layer (kept_out of
+ *                                 lookme_select); ids outside [0, n) are
+ *                                 clamped into it, and an id listed twice in
+ *                                 a layer races on its row of hidden
+ * The other arguments as for lookme_inject; the result is the same when kept
+ * is the set lookme_select writes.  Needs no workspace.
+ */
+lookme_status_t lookme_inject_kept(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                                   const int32_t* kept, const int32_t* scene, const int32_t* prim,
+                                   const float* w, void* hidden, int32_t d_h, void* stream);
+
+/*
  * Measurement support (not part of the method).  When enabled, each kernel
  * group that route/lookup/inject launches is bracketed by a pair of HIP timing
  * events recorded on the call's stream.  lookme_profile_read waits for the

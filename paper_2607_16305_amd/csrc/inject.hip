@@ -83,21 +83,24 @@ __device__ __forceinline__ int block_scan_incl(int v, int* wsum) {
   return incl + off;
 }
 
-// CACHED: a layer's keys are first copied to LDS (n <= SEL_CACHE_N), so that
-// the four passes and the compaction read them there instead of from L2
-// (one global round trip instead of five).  Element i sits at i + i / 32:
-// the padding keeps threads that walk ranges of 32 keys on distinct banks.
-constexpr int SEL_CACHE_N = 32768;
+// CN > 0: a layer's keys (n <= CN) are first copied to LDS, so that the four
+// passes and the compaction read them there instead of from L2 (one global
+// round trip instead of five).  Element i sits at i + i / 32: the padding
+// keeps threads that walk ranges of 32 keys on distinct banks.  The launcher
+// takes the smallest cache that holds n: the small one leaves room on the CU
+// for the workgroups of a kernel that runs beside the select.
+constexpr int SEL_CACHE_SMALL = 4096, SEL_CACHE_N = 32768;
 
-template <bool CACHED>
+template <int CN>
 __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
     const uint32_t* __restrict__ key_all, int64_t n, int64_t n_keep,
     int32_t* __restrict__ kept_all) {
+  constexpr bool CACHED = CN > 0;
   __shared__ int hist[256];
   __shared__ int wsum[SEL_WAVES];
   __shared__ uint32_t s_prefix;
   __shared__ int s_need;
-  __shared__ uint32_t cache[CACHED ? SEL_CACHE_N + SEL_CACHE_N / 32 : 1];
+  __shared__ uint32_t cache[CACHED ? CN + CN / 32 : 1];
   const int layer = blockIdx.x;
   const uint32_t* gkey = key_all + (int64_t)layer * n;
   int32_t* kept = kept_all + (int64_t)layer * n_keep;
@@ -272,11 +275,14 @@ hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uin
 hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint32_t* key,
                               int32_t* kept, hipStream_t st) {
   if (n == 0 || n_keep == 0) return hipSuccess;
-  if (n <= SEL_CACHE_N)
-    hipLaunchKernelGGL(crit_select_kernel<true>, dim3(layers), dim3(SEL_THREADS), 0, st, key, n,
-                       n_keep, kept);
+  if (n <= SEL_CACHE_SMALL)
+    hipLaunchKernelGGL(crit_select_kernel<SEL_CACHE_SMALL>, dim3(layers), dim3(SEL_THREADS), 0, st,
+                       key, n, n_keep, kept);
+  else if (n <= SEL_CACHE_N)
+    hipLaunchKernelGGL(crit_select_kernel<SEL_CACHE_N>, dim3(layers), dim3(SEL_THREADS), 0, st,
+                       key, n, n_keep, kept);
   else
-    hipLaunchKernelGGL(crit_select_kernel<false>, dim3(layers), dim3(SEL_THREADS), 0, st, key, n,
+    hipLaunchKernelGGL(crit_select_kernel<0>, dim3(layers), dim3(SEL_THREADS), 0, st, key, n,
                        n_keep, kept);
   return hipGetLastError();
 }

@@ -130,6 +130,29 @@ lookme_status_t check_workspace(lookme_t h, int32_t layers, int64_t n, Layout* L
   return LOOKME_OK;
 }
 
+lookme_status_t check_keep(int64_t n, int64_t n_keep) {
+  if (n_keep < 0 || n_keep > n)
+    return fail(LOOKME_ERR_INVALID, "n_keep %lld outside [0, n=%lld]", (long long)n_keep,
+                (long long)n);
+  return LOOKME_OK;
+}
+
+lookme_status_t check_crit_dim(const lookme_desc_t& d, int32_t d_c) {
+  if (d_c < 1) return fail(LOOKME_ERR_INVALID, "d_c must be positive");
+  if (((int64_t)d_c * elem_size(d.dtype)) % 16 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "d_c times elem_size must be a multiple of 16");
+  return LOOKME_OK;
+}
+
+lookme_status_t check_hidden_dim(const lookme_desc_t& d, int32_t d_h) {
+  if (d_h < 1) return fail(LOOKME_ERR_INVALID, "d_h must be positive");
+  if (d.value_dim > d_h)
+    return fail(LOOKME_ERR_INVALID, "value_dim %d exceeds d_h %d", d.value_dim, d_h);
+  if (((int64_t)d_h * elem_size(d.dtype)) % 16 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "d_h times elem_size must be a multiple of 16");
+  return LOOKME_OK;
+}
+
 hipError_t take_event(lookme_t h, hipEvent_t* ev) {
   if (!h->spare.empty()) {
     *ev = h->spare.back();
@@ -165,6 +188,35 @@ class Timed {
     lookme_status_t st_ = (expr);           \
     if (st_ != LOOKME_OK) return st_;       \
   } while (0)
+
+// criticality norms and, when n_keep > 0, the top-n_keep select (Eq. 9)
+lookme_status_t run_select(lookme_t h, const Layout& L, int32_t layers, int64_t n,
+                           int64_t n_keep, const void* crit, int32_t d_c, int32_t* kept,
+                           hipStream_t st) {
+  uint32_t* key = reinterpret_cast<uint32_t*>(static_cast<char*>(h->ws) + L.crit_key);
+  {
+    Timed tm(h, LOOKME_GROUP_NORM, st);
+    LOOKME_TRY(hip_status(lookme::launch_crit_norm(h->d.dtype, (int64_t)layers * n, crit, d_c,
+                                                   key, st),
+                          "criticality launch"));
+  }
+  if (n_keep == 0) return LOOKME_OK;
+  Timed tm(h, LOOKME_GROUP_SELECT, st);
+  return hip_status(lookme::launch_crit_select(layers, n, n_keep, key, kept, st),
+                    "select launch");
+}
+
+// row gather + residual add of the kept tokens (Eq. 10, Eq. 2)
+lookme_status_t run_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                           const int32_t* kept, const int32_t* scene, const int32_t* prim,
+                           const float* w, void* hidden, int32_t d_h, hipStream_t st) {
+  const lookme_desc_t& d = h->d;
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  return hip_status(lookme::launch_inject_rows(d.dtype, layers, n, n_keep, kept, scene, prim, w,
+                                               h->values, d.num_scenes, d.prims_per_scene,
+                                               d.value_dim, d.top_k, hidden, d_h, st),
+                    "inject launch");
+}
 
 }  // namespace
 
@@ -380,16 +432,9 @@ lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_k
                               int32_t* kept_out, void* stream) {
   LOOKME_TRY(check_handle(h));
   LOOKME_TRY(check_layers_n(layers, n));
-  const lookme_desc_t& d = h->d;
-  const int es = elem_size(d.dtype);
-  if (n_keep < 0 || n_keep > n)
-    return fail(LOOKME_ERR_INVALID, "n_keep %lld outside [0, n=%lld]", (long long)n_keep,
-                (long long)n);
-  if (d_c < 1 || d_h < 1) return fail(LOOKME_ERR_INVALID, "d_c and d_h must be positive");
-  if (d.value_dim > d_h)
-    return fail(LOOKME_ERR_INVALID, "value_dim %d exceeds d_h %d", d.value_dim, d_h);
-  if (((int64_t)d_c * es) % 16 != 0 || ((int64_t)d_h * es) % 16 != 0)
-    return fail(LOOKME_ERR_UNSUPPORTED, "d_c and d_h times elem_size must be multiples of 16");
+  LOOKME_TRY(check_keep(n, n_keep));
+  LOOKME_TRY(check_crit_dim(h->d, d_c));
+  LOOKME_TRY(check_hidden_dim(h->d, d_h));
   if (n == 0) return LOOKME_OK;
   LOOKME_TRY(check_ptr(crit, "crit"));
   LOOKME_TRY(check_ptr(scene, "scene"));
@@ -399,27 +444,42 @@ lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_k
   if (kept_out) LOOKME_TRY(check_ptr(kept_out, "kept_out"));
   Layout L;
   LOOKME_TRY(check_workspace(h, layers, n, &L));
-  char* ws = static_cast<char*>(h->ws);
-  uint32_t* key = reinterpret_cast<uint32_t*>(ws + L.crit_key);
-  int32_t* kept = kept_out ? kept_out : reinterpret_cast<int32_t*>(ws + L.kept);
+  int32_t* kept = kept_out ? kept_out : reinterpret_cast<int32_t*>(static_cast<char*>(h->ws) + L.kept);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  {
-    Timed tm(h, LOOKME_GROUP_NORM, st);
-    LOOKME_TRY(hip_status(lookme::launch_crit_norm(d.dtype, (int64_t)layers * n, crit, d_c, key,
-                                                   st),
-                          "criticality launch"));
-  }
+  LOOKME_TRY(run_select(h, L, layers, n, n_keep, crit, d_c, kept, st));
   if (n_keep == 0) return LOOKME_OK;
-  {
-    Timed tm(h, LOOKME_GROUP_SELECT, st);
-    LOOKME_TRY(hip_status(lookme::launch_crit_select(layers, n, n_keep, key, kept, st),
-                          "select launch"));
-  }
-  Timed tm(h, LOOKME_GROUP_INJECT, st);
-  return hip_status(lookme::launch_inject_rows(d.dtype, layers, n, n_keep, kept, scene, prim, w,
-                                               h->values, d.num_scenes, d.prims_per_scene,
-                                               d.value_dim, d.top_k, hidden, d_h, st),
-                    "inject launch");
+  return run_inject(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h, st);
+}
+
+lookme_status_t lookme_select(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                              const void* crit, int32_t d_c, int32_t* kept_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_keep(n, n_keep));
+  LOOKME_TRY(check_crit_dim(h->d, d_c));
+  if (n == 0 || n_keep == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(crit, "crit"));
+  LOOKME_TRY(check_ptr(kept_out, "kept_out"));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  return run_select(h, L, layers, n, n_keep, crit, d_c, kept_out, static_cast<hipStream_t>(stream));
+}
+
+lookme_status_t lookme_inject_kept(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                                   const int32_t* kept, const int32_t* scene, const int32_t* prim,
+                                   const float* w, void* hidden, int32_t d_h, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_keep(n, n_keep));
+  LOOKME_TRY(check_hidden_dim(h->d, d_h));
+  if (n == 0 || n_keep == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(kept, "kept"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(prim, "prim"));
+  LOOKME_TRY(check_ptr(w, "w"));
+  LOOKME_TRY(check_ptr(hidden, "hidden"));
+  return run_inject(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h,
+                    static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

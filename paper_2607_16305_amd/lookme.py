@@ -26,7 +26,8 @@ LOOKME_KMAX = 32
 STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "HIP"}
 
 EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "lookme_route",
-            "lookme_lookup", "lookme_inject", "lookme_destroy", "lookme_last_error",
+            "lookme_lookup", "lookme_inject", "lookme_select", "lookme_inject_kept",
+            "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
 GROUPS = ("project", "route", "bucket", "score", "norm", "select", "inject")
@@ -68,6 +69,10 @@ def load():
         "lookme_lookup": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp],
         "lookme_inject": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
                           ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp],
+        "lookme_select": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
+                          ctypes.c_int32, _vp, _vp],
+        "lookme_inject_kept": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp, _vp, _vp,
+                               _vp, _vp, ctypes.c_int32, _vp],
         "lookme_destroy": [_vp],
         "lookme_profile_enable": [_vp, ctypes.c_int32],
         "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
@@ -141,6 +146,16 @@ def lookme_inject(h, layers, n, n_keep, crit, d_c, scene, prim, w, hidden, d_h, 
                                 _ptr(w), _ptr(hidden), d_h, _ptr(kept_out), _stream(stream)))
 
 
+def lookme_select(h, layers, n, n_keep, crit, d_c, kept_out, stream=None):
+    _check(load().lookme_select(h, layers, n, n_keep, _ptr(crit), d_c, _ptr(kept_out),
+                                _stream(stream)))
+
+
+def lookme_inject_kept(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h, stream=None):
+    _check(load().lookme_inject_kept(h, layers, n, n_keep, _ptr(kept), _ptr(scene), _ptr(prim),
+                                     _ptr(w), _ptr(hidden), d_h, _stream(stream)))
+
+
 def lookme_destroy(h):
     if h:
         _check(load().lookme_destroy(h))
@@ -199,6 +214,16 @@ class Table:
         self.reserve(layers, n)
         lookme_inject(self.handle, layers, n, n_keep, crit, crit.shape[-1], scene, prim, w,
                       hidden, hidden.shape[-1], kept_out, stream)
+
+    def select(self, crit, kept_out, n_keep, layers=1, stream=None):
+        n = crit.numel() // (layers * crit.shape[-1])
+        self.reserve(layers, n)
+        lookme_select(self.handle, layers, n, n_keep, crit, crit.shape[-1], kept_out, stream)
+
+    def inject_kept(self, kept, scene, prim, w, hidden, n_keep, layers=1, stream=None):
+        n = scene.numel() // layers
+        lookme_inject_kept(self.handle, layers, n, n_keep, kept, scene, prim, w, hidden,
+                           hidden.shape[-1], stream)
 
     def close(self):
         if self.handle:

@@ -67,6 +67,23 @@ class Run:
                           kept_out=self.kept, layers=L, stream=self.stream)
         return self
 
+    def run_split(self):
+        """The same pass with the kept set selected on a second stream while
+        routing and lookup run, then the rows added for that set."""
+        inp, L = self.inp, self.L
+        main = torch.cuda.current_stream()
+        side = torch.cuda.Stream()
+        self.table.reserve(L, self.n)
+        side.wait_stream(main)
+        with torch.cuda.stream(side):
+            self.table.select(inp["delta"], self.kept, self.n_keep, layers=L, stream=side)
+        self.table.route(inp["x"], inp["wt"], self.q, self.scene, layers=L, stream=main)
+        self.table.lookup(self.q, self.scene, self.prim, self.w, layers=L, stream=main)
+        main.wait_stream(side)
+        self.table.inject_kept(self.kept, self.scene, self.prim, self.w, self.hidden, self.n_keep,
+                               layers=L, stream=main)
+        return self
+
 
 def check_run(r: Run, tokens=None, layers=None) -> C.Report:
     """Stage-wise comparison of a finished run against the oracle.

@@ -126,6 +126,25 @@ def test_calls_validate_before_launch(lib):
         msg = _status(lambda: lk.lookme_inject(h, 1, 8, 9, FAKE, 2048, FAKE, FAKE, FAKE, FAKE,
                                                2048, None, 0))[1]
         assert "n_keep" in msg and "n_keep" in lk.lookme_last_error()
+        # select alone: ranges, the kept output, the workspace; n_keep = 0 does nothing
+        assert S(lambda: lk.lookme_select(h, 1, 8, 9, FAKE, 2048, FAKE, 0)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_select(h, 1, 8, 2, FAKE, 2047, FAKE, 0)) == \
+            lk.LOOKME_ERR_UNSUPPORTED
+        assert S(lambda: lk.lookme_select(h, 1, 8, 2, FAKE, 2048, None, 0)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_select(h, 1, 8, 2, FAKE, 2048, FAKE, 0)) == \
+            lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: lk.lookme_select(h, 1, 8, 0, None, 2048, None, 0)) == lk.LOOKME_OK
+        # inject of a given kept set: ranges and pointers (it needs no workspace)
+        assert S(lambda: lk.lookme_inject_kept(h, 1, 8, 9, FAKE, FAKE, FAKE, FAKE, FAKE, 2048,
+                                               0)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_inject_kept(h, 1, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 1024,
+                                               0)) == lk.LOOKME_ERR_INVALID     # d_v > d_h
+        assert S(lambda: lk.lookme_inject_kept(h, 1, 8, 2, None, FAKE, FAKE, FAKE, FAKE, 2048,
+                                               0)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_inject_kept(h, 1, 8, 0, None, None, None, None, None, 2048,
+                                               0)) == lk.LOOKME_OK
     finally:
         lk.lookme_destroy(h)
 

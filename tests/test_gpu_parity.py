@@ -188,6 +188,23 @@ def test_deterministic_reruns():
         assert torch.equal(getattr(a, name), getattr(b, name)), name
 
 
+@pytest.mark.parametrize("name", ["bf16_ragged_l2", "f32_proj_l3", "bf16_many_tokens",
+                                  "bf16_one_token"])
+def test_select_on_second_stream_then_inject_kept(name):
+    """lookme_select on its own stream, concurrent with route and lookup, then
+    lookme_inject_kept: the oracle's results, and the same bits as
+    lookme_inject on one stream."""
+    from tests.harness import Run, check_run
+    wl = SMALL[name]
+    inp = make_inputs(wl, seed=31, device=DEV)
+    ref = Run(inp).run()
+    r = Run(inp, table=ref.table).run_split()
+    rep = check_run(r)
+    assert rep.ok, str(rep)
+    for key in ("q", "scene", "prim", "w", "kept", "hidden"):
+        assert torch.equal(getattr(ref, key), getattr(r, key)), key
+
+
 def test_layers_batched_equal_sequential():
     from tests.harness import Run
     wl = SMALL["bf16_ragged_l2"].scaled(layers=3)
