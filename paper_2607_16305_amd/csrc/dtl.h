@@ -20,11 +20,14 @@ __device__ __forceinline__ void load_lds16(const void* src, char* lds_dst) {
 }
 
 // chunk c of row r of a block sits in slot c ^ blk_swz(r): rows that share a
-// 128-byte or 256-byte bank window get distinct slots for one chunk index
+// bank window get distinct slots for one chunk index.  For 128-byte rows,
+// r & 7 lets a fragment read (16 rows, one chunk index) run at ~210 bytes
+// per clock per CU on gfx950; adding (r >> 3) & 1, as a 128-byte bank
+// window would suggest, halves that (measured with a read-only probe)
 template <int KB>
 __device__ __forceinline__ int blk_swz(int r) {
   if constexpr (KB == 64) return ((r >> 1) & 3) ^ ((r >> 3) & 1);
-  else return (r & 7) ^ ((r >> 3) & 1);
+  else return r & 7;
 }
 
 template <int WM, int WN, int MI, int NJ, int KB>

@@ -11,9 +11,10 @@
 //               the n_keep-th largest key (keys cached in LDS when they
 //               fit), then an order-preserving compaction (block prefix
 //               sums) of the kept token ids;
-//   inject      one workgroup per kept token: 16-byte coalesced loads of its
-//               k table rows (all in flight together), fp32 weighted sum in
-//               a fixed order, one rounding of H + sum, in-place store.
+//   inject      one workgroup per kept token (one thread per 16-byte chunk of
+//               a row, up to 256): coalesced loads of its k table rows (all
+//               in flight together), fp32 weighted sum in a fixed order, one
+//               rounding of H + sum, in-place store.
 #include "common.h"
 #include "kernels.h"
 
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
   }
   char* h = hidden + row * h_bytes;
   const int chunks = (int)(v_bytes / 16);
-  for (int c = threadIdx.x; c < chunks; c += INJ_THREADS) {
+  for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
     u32x4_t vv[K];
 #pragma unroll
     for (int i = 0; i < K; ++i)
@@ -248,8 +249,12 @@ static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_
                             const int32_t* kept, const int32_t* scene, const int32_t* prim,
                             const float* w, const char* values, int S, int P, int64_t vb,
                             char* hidden, int64_t hb) {
-#define LOOKME_INJ(K_)                                                                         \
-  hipLaunchKernelGGL((inject_kernel<DT, K_>), grid, dim3(INJ_THREADS), 0, st, n, n_keep, kept, \
+  // as many whole waves as the row has 16-byte chunks (up to 256 threads):
+  // narrow rows leave no thread idle, and the CU holds more workgroups
+  const int ch = (int)(vb / 16);
+  const int bs = ch >= INJ_THREADS ? INJ_THREADS : (ch + 63) / 64 * 64;
+#define LOOKME_INJ(K_)                                                                \
+  hipLaunchKernelGGL((inject_kernel<DT, K_>), grid, dim3(bs), 0, st, n, n_keep, kept, \
                      scene, prim, w, values, S, P, kk, vb, hidden, hb)
   if (kk <= 4) LOOKME_INJ(4);
   else if (kk <= 8) LOOKME_INJ(8);
