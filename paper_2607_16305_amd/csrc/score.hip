@@ -87,8 +87,14 @@ __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int ken
     // lowest key), one insertion round per value that still beats some
     // lane's list: the rounds are wave-wide (branch-free sorted insertion),
     // and after the first blocks a round is rarely needed by any lane, so
-    // most blocks cost one vote instead of four insertions.
+    // most blocks cost one vote instead of four insertions.  A value below
+    // T, the largest k-th entry of the row's 4 lists in this wave, cannot
+    // reach the row's top k (that list holds k keys at least as large), so
+    // it is dropped; values equal to T stay, for the lower-index rule.
     const int p0 = blk * 16 + 4 * g;
+    float T = ls[KL - 1];
+    T = fmaxf(T, __shfl_xor(T, 16, 64));
+    T = fmaxf(T, __shfl_xor(T, 32, 64));
 #pragma unroll
     for (int round = 0; round < 4; ++round) {
       float x = v[0];
@@ -96,6 +102,7 @@ __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int ken
 #pragma unroll
       for (int r = 1; r < 4; ++r)
         if (v[r] > x) { x = v[r]; w = r; }
+      if (!(x >= T)) x = -__builtin_inff();
       if (!__any(x > ls[KL - 1])) break;
       const int p = p0 + w;
 #pragma unroll
