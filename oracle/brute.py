@@ -136,3 +136,43 @@ def inject(hidden_rows, value_rows, P, scenes, prim, w, kept, rounder):
                 acc += Fraction(w[t][i]) * Fraction(value_rows[scenes[t] * P + p][j])
             out[t][j] = rounder(acc)
     return out
+
+
+def relevance(q_rows, scene, scene_key_rows, w1_rows, b1, w2_rows, b2, prim_key_rows, P, k,
+              mant_bits):
+    """Level-2 in the paper's form (Eq. 6-7) by plain loops: exact rational
+    MLP layers (ReLU, one rounding of the hidden activations), repeated
+    maximum extraction for the top k (lowest p among equal logits), then
+    cos + tanh and a softmax in floating point.  Returns (a, prim, w)."""
+    a_rows, prims, ws = [], [], []
+    for t, qt in enumerate(q_rows):
+        inp = list(qt) + list(scene_key_rows[scene[t]])
+        a = []
+        for j, wr in enumerate(w1_rows):
+            z = dot(inp, wr) + Fraction(b1[j])
+            a.append(round_fraction(z, mant_bits) if z > 0 else Fraction(0))
+        a_rows.append(a)
+        r = [dot(a, w2_rows[p]) + Fraction(b2[p]) for p in range(P)]
+        left = list(range(P))
+        chosen = []
+        for _ in range(k):
+            best = left[0]
+            for p in left[1:]:
+                if r[p] > r[best]:
+                    best = p
+            chosen.append(best)
+            left.remove(best)
+        z = []
+        for p in chosen:
+            e = prim_key_rows[scene[t] * P + p]
+            num = float(dot(qt, e))
+            nq = math.sqrt(float(dot(qt, qt)))
+            ne = math.sqrt(float(dot(e, e)))
+            c = 0.0 if nq == 0 or ne == 0 else num / (nq * ne)
+            z.append(c + math.tanh(float(r[p])))
+        m = max(z)
+        ex = [math.exp(v - m) for v in z]
+        tot = sum(ex)
+        prims.append(chosen)
+        ws.append([v / tot for v in ex])
+    return a_rows, prims, ws

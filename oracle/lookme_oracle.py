@@ -26,6 +26,10 @@ What is computed, step by step (each function cites its passage):
   run         all of the above for L layers that share one table (Sec. 3.3,
               "Inter-Layer Sparse Activation": neighbouring layers retrieve
               similar primitives, so one table serves several layers)
+  relevance_* Level-2 in the paper's own form (Eq. 6-7): a scene-shared
+              two-layer MLP over [v_e, e_img[j]] gives relevance logits r_j;
+              the top-k primitives by r are weighted by the softmax of
+              cos(v_e, e_{j,p}) + tanh(r_j[p])
 
 Readings of the paper taken here (the paper is silent or differs from the
 configured workloads; each is listed in the design notes of the repository):
@@ -39,6 +43,11 @@ configured workloads; each is listed in the design notes of the repository):
     round-to-nearest-even from the exact product; later stages use that q.
   * The injected increment is added into the first d_v columns of H; the
     result is rounded once to the storage dtype.
+  * Relevance MLP (Eq. 6): r = W2 act(W1 [v_e ; e_img[j]] + b1) + b2 with
+    act = ReLU and a given hidden width; the hidden activations are rounded
+    once to the storage dtype (the second layer runs on them as stored);
+    e_img are the scene keys; the primitive rows whose cosine Eq. 7 takes are
+    the primitive keys K2[j, p, :] (a zero vector has cosine 0).
 
 Inputs are numpy arrays.  bf16 tensors are passed as their raw uint16 bit
 patterns (numpy has no bf16) together with ``dtype="bf16"``; fp32 tensors as
@@ -285,3 +294,65 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
         for name, v in zip(res, (q, sc, pr, ww, kept, h)):
             res[name].append(v)
     return {name: np.stack(v) for name, v in res.items()}
+
+
+# ---------------------------------------------------------------------------
+# Level-2 in the paper's form: relevance MLP (Eq. 6) and cosine + tanh
+# weights (Eq. 7)
+# ---------------------------------------------------------------------------
+
+def relevance_hidden(q: np.ndarray, scene: np.ndarray, scene_keys: np.ndarray,
+                     w1: np.ndarray, b1: np.ndarray, dtype: str) -> np.ndarray:
+    """First layer of the scene-shared relevance MLP (Sec. 3.2, Level-2,
+    Eq. 6) on the concatenation [v_e, e_img[j]] of a token's query and its
+    scene's key: a = ReLU(W1 [v_e ; e_img[j]] + b1), rounded once to dtype.
+
+    q [n, d_e], scene [n], scene_keys [S, d_e], w1 [h, 2 d_e] (columns
+    0..d_e-1 act on v_e, the rest on e_img[j]), b1 [h].  Returns [n, h].
+    """
+    inp = np.concatenate([q, scene_keys[np.asarray(scene, dtype=np.int64)]], axis=1)
+    z = inp @ w1.T + np.asarray(b1, dtype=np.float64)[None, :]
+    return round_to_dtype(np.maximum(z, 0.0), dtype)
+
+
+def relevance_logits(a: np.ndarray, w2: np.ndarray, b2: np.ndarray) -> np.ndarray:
+    """Second layer of the MLP (Eq. 6): r_j = W2 a + b2, one logit per
+    primitive.  a [n, h], w2 [P, h], b2 [P] -> [n, P]."""
+    return a @ w2.T + np.asarray(b2, dtype=np.float64)[None, :]
+
+
+def cosine(u: np.ndarray, v: np.ndarray) -> float:
+    """cos(u, v) = <u, v> / (|u| |v|); 0 when either vector is zero."""
+    nu = np.sqrt(np.dot(u, u))
+    nv = np.sqrt(np.dot(v, v))
+    if nu == 0 or nv == 0:
+        return 0.0
+    return float(np.dot(u, v) / (nu * nv))
+
+
+def relevance_lookup(q: np.ndarray, scene: np.ndarray, a: np.ndarray, w2: np.ndarray,
+                     b2: np.ndarray, prim_keys: np.ndarray, k: int):
+    """Level-2 retrieval in the paper's form (Eq. 6-7): the top-k primitives
+    of the token's scene by relevance logit (ties to the lowest p), weighted
+    by the softmax over those k of cos(v_e, e_{j,p}) + tanh(r_j[p]).
+
+    q [n, d_e], scene [n], a [n, h] (relevance_hidden), w2 [P, h], b2 [P],
+    prim_keys [S, P, d_e].  Returns (prim [n, k] int32, w [n, k] float64,
+    r_top [n, k] float64: the logits of the chosen primitives).
+    """
+    n = q.shape[0]
+    P = prim_keys.shape[1]
+    if not (1 <= k <= P):
+        raise ValueError("k must be in [1, P]")
+    r = relevance_logits(a, w2, b2)
+    prim = np.zeros((n, k), dtype=np.int32)
+    w = np.zeros((n, k), dtype=np.float64)
+    r_top = np.zeros((n, k), dtype=np.float64)
+    for t in range(n):
+        idx = topk_order(r[t], k)
+        rows = prim_keys[int(scene[t])][idx]
+        z = np.array([cosine(q[t], rows[i]) for i in range(k)]) + np.tanh(r[t, idx])
+        prim[t] = idx
+        r_top[t] = r[t, idx]
+        w[t] = softmax_weights(z)
+    return prim, w, r_top

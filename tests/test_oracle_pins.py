@@ -464,3 +464,122 @@ def test_oracle_rejects_bad_sizes():
         O.select(np.ones(3), 4)
     with pytest.raises(ValueError):
         O.lookup(np.ones((1, 2)), np.array([0]), np.ones((1, 3, 2)), 4)
+
+
+# --------------------------------------------------------------------------
+# Level-2 in the paper's form: relevance MLP (Eq. 6), cos + tanh weights
+# (Eq. 7)
+# --------------------------------------------------------------------------
+
+def _relevance_tiny(seed, n=6, d_e=4, S=3, P=7, h=5, dtype="bf16"):
+    rng = np.random.default_rng(seed)
+    rnd = _bf16_values if dtype == "bf16" else (lambda r, sh, sc=1.0: r.standard_normal(sh) * sc)
+    q = rnd(rng, (n, d_e))
+    keys = rnd(rng, (S, d_e))
+    w1 = rnd(rng, (h, 2 * d_e), 0.5)
+    b1 = rng.standard_normal(h) * 0.25
+    w2 = rnd(rng, (P, h), 0.5)
+    b2 = rng.standard_normal(P) * 0.25
+    K2 = rnd(rng, (S, P, d_e))
+    scene = rng.integers(0, S, n)
+    return q, scene, keys, w1, b1, w2, b2, K2
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_relevance_matches_exact_rational_brute_force(dtype):
+    """Catches swapped halves of W1 (query vs scene key), a transposed W2, a
+    missing bias, the activation applied after the rounding or not at all,
+    and a top-k over the wrong axis."""
+    q, scene, keys, w1, b1, w2, b2, K2 = _relevance_tiny(40, dtype=dtype)
+    k = 3
+    a = O.relevance_hidden(q, scene, keys, w1, b1, dtype)
+    prim, w, r_top = O.relevance_lookup(q, scene, a, w2, b2, K2, k)
+    mant = 8 if dtype == "bf16" else 24
+    P = K2.shape[1]
+    ba, bp, bw = B.relevance(q.tolist(), scene.tolist(), keys.tolist(), w1.tolist(), b1.tolist(),
+                             w2.tolist(), b2.tolist(), K2.reshape(-1, K2.shape[2]).tolist(), P, k,
+                             mant)
+    for t in range(q.shape[0]):
+        assert [Fraction(float(v)) for v in a[t]] == ba[t]
+    assert prim.tolist() == bp
+    np.testing.assert_allclose(w, np.array(bw), rtol=1e-12, atol=1e-15)
+
+
+def test_relevance_constant_hidden_gives_planted_ranking():
+    """W1 = 0 and b1 > 0 make the hidden layer a constant; with one hidden
+    unit of value 1 the logits are the rows of W2 plus b2, so the top k is
+    known by construction (and independent of the token and its scene)."""
+    d_e, S, P, k = 4, 2, 9, 4
+    planted = np.array([0.5, -1.0, 2.0, 0.25, 2.0, -3.0, 1.5, 0.75, 1.0])   # two equal maxima
+    w1 = np.zeros((1, 2 * d_e))
+    b1 = np.array([1.0])
+    w2 = planted[:, None] - 0.125
+    b2 = np.full(P, 0.125)
+    rng = np.random.default_rng(41)
+    q = rng.standard_normal((3, d_e))
+    keys = rng.standard_normal((S, d_e))
+    K2 = rng.standard_normal((S, P, d_e))
+    a = O.relevance_hidden(q, np.array([0, 1, 1]), keys, w1, b1, "f32")
+    assert np.all(a == 1.0)
+    prim, _, r_top = O.relevance_lookup(q, np.array([0, 1, 1]), a, w2, b2, K2, k)
+    for t in range(3):
+        assert prim[t].tolist() == [2, 4, 6, 8]      # 2.0 (p=2 before p=4), 1.5, 1.0
+        assert r_top[t].tolist() == [2.0, 2.0, 1.5, 1.0]
+
+
+def test_relevance_relu_zeroes_negative_preactivations():
+    """Pre-activations all below zero leave a = 0, so the logits are b2:
+    catches a missing or sign-flipped activation."""
+    d_e, P, h = 3, 6, 4
+    q = np.array([[1.0, 2.0, 0.5]])
+    keys = np.array([[0.25, 0.5, 1.0]])
+    w1 = np.full((h, 2 * d_e), 1.0)
+    b1 = np.full(h, -100.0)
+    b2 = np.array([0.3, -0.2, 0.9, 0.1, 0.9, -1.0])
+    w2 = np.ones((P, h))
+    a = O.relevance_hidden(q, np.array([0]), keys, w1, b1, "f32")
+    assert np.all(a == 0.0)
+    prim, _, r_top = O.relevance_lookup(q, np.array([0]), a, w2, b2, np.ones((1, P, d_e)), 3)
+    assert prim[0].tolist() == [2, 4, 0]
+    assert r_top[0].tolist() == [0.9, 0.9, 0.3]
+
+
+def test_relevance_weights_closed_forms():
+    """Eq. 7 in closed form: rows parallel to v_e have cosine 1 and rows
+    opposite to it -1, so the weights are a softmax of 1 + tanh(r) or
+    -1 + tanh(r); k = 1 gives exactly 1."""
+    d_e, P = 4, 3
+    q = np.array([[1.0, -2.0, 0.5, 3.0]])
+    K2 = np.stack([2.0 * q[0], 0.5 * q[0], -3.0 * q[0]])[None]        # cos = 1, 1, -1
+    r = np.array([0.0, math.atanh(0.5), math.atanh(-0.25)])
+    # one hidden unit equal to 1 carries the logits
+    w1 = np.zeros((1, 2 * d_e))
+    b1 = np.array([1.0])
+    a = O.relevance_hidden(q, np.array([0]), np.zeros((1, d_e)), w1, b1, "f32")
+    prim, w, _ = O.relevance_lookup(q, np.array([0]), a, r[:, None], np.zeros(P), K2, 3)
+    assert prim[0].tolist() == [1, 0, 2]
+    z = np.array([1 + 0.5, 1 + 0.0, -1 - 0.25])
+    np.testing.assert_allclose(w[0], np.exp(z) / np.exp(z).sum(), rtol=1e-14)
+    _, w1k, _ = O.relevance_lookup(q, np.array([0]), a, r[:, None], np.zeros(P), K2, 1)
+    assert w1k[0].tolist() == [1.0]
+
+
+def test_relevance_invariants():
+    """Relabelling the hidden units (rows of W1 and b1, columns of W2 alike)
+    leaves the logits unchanged; scaling primitive rows by positive factors
+    leaves the cosines, hence the weights, unchanged.  Catches W1/W2 index
+    mix-ups and a dot product used in place of the cosine."""
+    q, scene, keys, w1, b1, w2, b2, K2 = _relevance_tiny(42, n=8, d_e=6, S=2, P=11, h=7,
+                                                         dtype="f32")
+    k = 4
+    a = O.relevance_hidden(q, scene, keys, w1, b1, "f32")
+    prim, w, r_top = O.relevance_lookup(q, scene, a, w2, b2, K2, k)
+    perm = np.random.default_rng(43).permutation(w1.shape[0])
+    a2 = O.relevance_hidden(q, scene, keys, w1[perm], b1[perm], "f32")
+    prim2, w2_, r2 = O.relevance_lookup(q, scene, a2, w2[:, perm], b2, K2, k)
+    assert prim2.tolist() == prim.tolist()
+    np.testing.assert_allclose(r2, r_top, rtol=1e-12)
+    scale = np.random.default_rng(44).uniform(0.1, 10.0, K2.shape[:2])[..., None]
+    prim3, w3, _ = O.relevance_lookup(q, scene, a, w2, b2, K2 * scale, k)
+    assert prim3.tolist() == prim.tolist()
+    np.testing.assert_allclose(w3, w, rtol=1e-12)
