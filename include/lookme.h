@@ -180,6 +180,39 @@ lookme_status_t lookme_inject_kept(lookme_t h, int32_t layers, int64_t n, int64_
                                    const float* w, void* hidden, int32_t d_h, void* stream);
 
 /*
+ * lookme_set_relevance -- registers the scene-shared relevance MLP that
+ * Level-2 uses in the paper's own form (Sec. 3.2, Eq. 6).  The tensors are
+ * borrowed like the table (they must stay alive and unmodified while used):
+ *   hidden  width h of the hidden layer; h * elem_size a multiple of 64 bytes
+ *   w1      [h, 2 * key_dim] dtype; columns [0, key_dim) act on the query,
+ *           [key_dim, 2 key_dim) on the scene key e_img[j]
+ *   b1      [h] float32, or NULL for zero
+ *   w2      [prims_per_scene, h] dtype
+ *   b2      [prims_per_scene] float32, or NULL for zero
+ * Needs key_dim * elem_size a multiple of 128 bytes.  Replaces an earlier
+ * registration.
+ */
+lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
+                                     const float* b1, const void* w2, const float* b2);
+
+/*
+ * lookme_lookup_relevance -- Level-2 in the paper's form (Eq. 6-7), with
+ * the MLP of lookme_set_relevance:
+ *   q, scene   as for lookme_lookup (q [layers, n, d_e], scene [layers, n])
+ *   act_out    [layers, n, h] dtype: a = round(ReLU(W1 [q ; scene_keys[scene]]
+ *              + b1)), float32 accumulation, one rounding to dtype
+ *   prim_out   [layers, n, k] int32: the k primitives p of largest logit
+ *              r_p = <W2[p], a> + b2[p] (ties: lowest p), logit-descending
+ *   w_out      [layers, n, k] float32: softmax over the k of
+ *              cos(q, prim_keys[scene, p]) + tanh(r_p) (cosine 0 for a zero
+ *              vector)
+ * Needs no workspace.
+ */
+lookme_status_t lookme_lookup_relevance(lookme_t h, int32_t layers, int64_t n, const void* q,
+                                        const int32_t* scene, void* act_out, int32_t* prim_out,
+                                        float* w_out, void* stream);
+
+/*
  * Measurement support (not part of the method).  When enabled, each kernel
  * group that route/lookup/inject launches is bracketed by a pair of HIP timing
  * events recorded on the call's stream.  lookme_profile_read waits for the

@@ -151,6 +151,49 @@ def check_scene(q: np.ndarray, scene_keys: np.ndarray, bias, score: str,
             rep.fail(f"scene[{t}]: library {g} score {s1[r, g]!r}, oracle {b} score {s1[r, b]!r}")
 
 
+def _check_topk_set(t, s2: np.ndarray, qn: float, g: np.ndarray, k: int, rep: Report):
+    """C3 for one row: the listed k indices ``g`` against the exact scores
+    ``s2``: the set equals the top k except for swaps among scores tied with
+    the k-th, listed score-descending (exact ties by ascending index).
+    Returns the scores of the listed set, or None after a failure."""
+    P = s2.shape[0]
+    rep.count("prim")
+    if np.any(g < 0) or np.any(g >= P) or len(set(g.tolist())) != k:
+        rep.fail(f"prim[{t}]={g.tolist()} invalid (P={P})")
+        return None
+    ref = O.topk_order(s2, k)
+    kth = s2[ref[-1]]
+    gs = s2[g]
+    exempt = False
+    # every listed element must reach the k-th score (up to a tie)
+    for p, v in zip(g, gs):
+        if v < kth and not tie(v, kth, qn):
+            rep.fail(f"prim[{t}]: p={p} score {v!r} below k-th {kth!r}")
+            return None
+        if v < kth:
+            exempt = True
+    # every element strictly above the k-th score must be listed
+    gset = set(g.tolist())
+    for p in ref:
+        if int(p) not in gset:
+            if not tie(s2[p], kth, qn):
+                rep.fail(f"prim[{t}]: missing p={p} score {s2[p]!r} (k-th {kth!r})")
+                return None
+            exempt = True
+    # order: descending score, exact ties ascending index
+    for i in range(k - 1):
+        a, b = gs[i], gs[i + 1]
+        if a < b and not tie(a, b, qn):
+            rep.fail(f"prim[{t}]: order {g.tolist()} not descending")
+            break
+        if a == b and g[i] > g[i + 1]:
+            rep.fail(f"prim[{t}]: equal scores not in ascending p order")
+            break
+    if exempt:
+        rep.exempt("prim")
+    return gs
+
+
 def check_prim(q: np.ndarray, scene: np.ndarray, scene_prim_keys, k: int, score: str,
                prim_lib: np.ndarray, w_lib: np.ndarray, rep: Report, tokens=None,
                w_tol: float = 1e-5):
@@ -177,48 +220,62 @@ def check_prim(q: np.ndarray, scene: np.ndarray, scene_prim_keys, k: int, score:
         s2 = O.primitive_scores(q[t], keys, score)
         qn = float(np.linalg.norm(q[t]))
         g = np.asarray(prim_lib[t], dtype=np.int64)
-        rep.count("prim")
-        if np.any(g < 0) or np.any(g >= P) or len(set(g.tolist())) != k:
-            rep.fail(f"prim[{t}]={g.tolist()} invalid (P={P})")
+        gs = _check_topk_set(t, s2, qn, g, k, rep)
+        if gs is None:
             continue
-        ref = O.topk_order(s2, k)
-        kth = s2[ref[-1]]
-        gs = s2[g]
-        exempt = False
-        # every listed element must reach the k-th score (up to a tie)
-        for p, v in zip(g, gs):
-            if v < kth and not tie(v, kth, qn):
-                rep.fail(f"prim[{t}]: p={p} score {v!r} below k-th {kth!r}")
-                exempt = None
-                break
-            if v < kth:
-                exempt = True
-        if exempt is None:
-            continue
-        # every element strictly above the k-th score must be listed
-        gset = set(g.tolist())
-        for p in ref:
-            if int(p) not in gset:
-                if not tie(s2[p], kth, qn):
-                    rep.fail(f"prim[{t}]: missing p={p} score {s2[p]!r} (k-th {kth!r})")
-                    exempt = None
-                    break
-                exempt = True
-        if exempt is None:
-            continue
-        # order: descending score, exact ties ascending p
-        for i in range(k - 1):
-            a, b = gs[i], gs[i + 1]
-            if a < b and not tie(a, b, qn):
-                rep.fail(f"prim[{t}]: order {g.tolist()} not descending")
-                break
-            if a == b and g[i] > g[i + 1]:
-                rep.fail(f"prim[{t}]: equal scores not in ascending p order")
-                break
-        if exempt:
-            rep.exempt("prim")
         wo = O.softmax_weights(gs)
         w_orc[r] = wo
+        rep.count("w", k)
+        dw = np.max(np.abs(np.asarray(w_lib[t], dtype=np.float64) - wo))
+        if not dw <= w_tol:
+            rep.fail(f"w[{t}]: max |dw| = {dw:.3g} > {w_tol}")
+    return w_orc
+
+
+def check_relevance_hidden(act_lib, q: np.ndarray, scene: np.ndarray, scene_keys: np.ndarray,
+                           w1: np.ndarray, b1: np.ndarray, dtype: str, rep: Report):
+    """C1 for the relevance MLP's hidden layer (Eq. 6): the library sums the
+    2 d_e products of [q, e_img[scene]] and W1 plus b1 in float32 and applies
+    ReLU and one rounding; with E the recursive-summation bound, its value
+    must lie between the roundings of ReLU(exact - E) and ReLU(exact + E)."""
+    inp = np.concatenate([q, scene_keys[np.asarray(scene, dtype=np.int64)]], axis=1)
+    b = np.asarray(b1, dtype=np.float64)[None, :]
+    exact = inp @ w1.T + b
+    E = (inp.shape[1] + 1) * 2.0 ** -24 * (np.abs(inp) @ np.abs(w1).T + np.abs(b))
+    lo = O.round_to_dtype(np.maximum(exact - E, 0.0), dtype)
+    hi = O.round_to_dtype(np.maximum(exact + E, 0.0), dtype)
+    got = O.to_f64(act_lib, dtype)
+    rep.count("act", got.size)
+    bad = (got < lo) | (got > hi)
+    if np.any(bad):
+        i = np.unravel_index(int(np.argmax(bad)), bad.shape)
+        rep.fail(f"act: {int(bad.sum())} elements outside the float32 accumulation bound "
+                 f"(first at {i}: got {got[i]!r}, exact {exact[i]!r}, bound {E[i]!r})")
+    off = int(np.sum(got != O.round_to_dtype(np.maximum(exact, 0.0), dtype)))
+    rep.notes["act_not_correctly_rounded"] = rep.notes.get("act_not_correctly_rounded", 0) + off
+
+
+def check_relevance_prim(act: np.ndarray, w2: np.ndarray, b2: np.ndarray, q: np.ndarray,
+                         scene: np.ndarray, scene_prim_keys, k: int, prim_lib: np.ndarray,
+                         w_lib: np.ndarray, rep: Report, w_tol: float = 1e-5):
+    """C3 + C4 for Level-2 in the paper's form (Eq. 6-7), on the library's
+    hidden activations: the k primitives must be the top k of the logits
+    W2 a + b2 (ties as in C3), and the weights the softmax over that set of
+    cos(q, e_{j,p}) + tanh(r_p) within ``w_tol``.  Rows are those of the
+    arguments (already sampled).  Returns the oracle weights of the library's
+    sets, [rows, k]."""
+    r_all = O.relevance_logits(act, w2, b2)
+    w_orc = np.zeros((act.shape[0], k))
+    for t in range(act.shape[0]):
+        rn = float(np.linalg.norm(act[t]) * np.max(np.linalg.norm(w2, axis=1)))
+        g = np.asarray(prim_lib[t], dtype=np.int64)
+        gs = _check_topk_set(t, r_all[t], rn, g, k, rep)
+        if gs is None:
+            continue
+        keys = scene_prim_keys(int(scene[t]))
+        z = np.array([O.cosine(q[t], keys[p]) for p in g]) + np.tanh(gs)
+        wo = O.softmax_weights(z)
+        w_orc[t] = wo
         rep.count("w", k)
         dw = np.max(np.abs(np.asarray(w_lib[t], dtype=np.float64) - wo))
         if not dw <= w_tol:

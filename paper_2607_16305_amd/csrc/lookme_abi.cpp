@@ -34,6 +34,7 @@ struct lookme_s {
   std::vector<hipEvent_t> spare;           // event pool
   int64_t prof_count[LOOKME_GROUP_COUNT];
   double prof_ms[LOOKME_GROUP_COUNT];
+  lookme::RelevanceMlp rel;                // hidden == 0: none registered
 };
 
 namespace {
@@ -480,6 +481,47 @@ lookme_status_t lookme_inject_kept(lookme_t h, int32_t layers, int64_t n, int64_
   LOOKME_TRY(check_ptr(hidden, "hidden"));
   return run_inject(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h,
                     static_cast<hipStream_t>(stream));
+}
+
+lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
+                                     const float* b1, const void* w2, const float* b2) {
+  LOOKME_TRY(check_handle(h));
+  const int es = elem_size(h->d.dtype);
+  if (hidden < 1) return fail(LOOKME_ERR_INVALID, "hidden must be positive (got %d)", hidden);
+  if (((int64_t)hidden * es) % 64 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "hidden * elem_size must be a multiple of 64 bytes");
+  if (((int64_t)h->d.key_dim * es) % 128 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "key_dim * elem_size must be a multiple of 128 bytes");
+  LOOKME_TRY(check_ptr(w1, "w1"));
+  LOOKME_TRY(check_ptr(w2, "w2"));
+  if ((b1 != nullptr && (reinterpret_cast<uintptr_t>(b1) & 3u)) ||
+      (b2 != nullptr && (reinterpret_cast<uintptr_t>(b2) & 3u)))
+    return fail(LOOKME_ERR_INVALID, "b1 and b2 must be 4-byte aligned");
+  h->rel = lookme::RelevanceMlp{hidden, w1, b1, w2, b2};
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_lookup_relevance(lookme_t h, int32_t layers, int64_t n, const void* q,
+                                        const int32_t* scene, void* act_out, int32_t* prim_out,
+                                        float* w_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  if (h->rel.hidden < 1)
+    return fail(LOOKME_ERR_INVALID, "no relevance MLP registered (lookme_set_relevance)");
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(q, "q"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(act_out, "act_out"));
+  LOOKME_TRY(check_ptr(prim_out, "prim_out"));
+  LOOKME_TRY(check_ptr(w_out, "w_out"));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Timed tm(h, LOOKME_GROUP_SCORE, st);
+  return hip_status(lookme::launch_relevance(d.dtype, q, scene, h->scene_keys, h->prim_keys,
+                                             h->rel, (int64_t)layers * n, d.key_dim,
+                                             d.num_scenes, d.prims_per_scene, d.top_k, act_out,
+                                             prim_out, w_out, st),
+                    "relevance lookup launch");
 }
 
 }  // extern "C"

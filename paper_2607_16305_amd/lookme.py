@@ -27,6 +27,7 @@ STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "HIP
 
 EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "lookme_route",
             "lookme_lookup", "lookme_inject", "lookme_select", "lookme_inject_kept",
+            "lookme_set_relevance", "lookme_lookup_relevance",
             "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
@@ -73,6 +74,9 @@ def load():
                           ctypes.c_int32, _vp, _vp],
         "lookme_inject_kept": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp, _vp, _vp,
                                _vp, _vp, ctypes.c_int32, _vp],
+        "lookme_set_relevance": [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp],
+        "lookme_lookup_relevance": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
+                                    _vp],
         "lookme_destroy": [_vp],
         "lookme_profile_enable": [_vp, ctypes.c_int32],
         "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
@@ -156,6 +160,15 @@ def lookme_inject_kept(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h, 
                                      _ptr(w), _ptr(hidden), d_h, _stream(stream)))
 
 
+def lookme_set_relevance(h, hidden, w1, b1, w2, b2):
+    _check(load().lookme_set_relevance(h, hidden, _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2)))
+
+
+def lookme_lookup_relevance(h, layers, n, q, scene, act_out, prim_out, w_out, stream=None):
+    _check(load().lookme_lookup_relevance(h, layers, n, _ptr(q), _ptr(scene), _ptr(act_out),
+                                          _ptr(prim_out), _ptr(w_out), _stream(stream)))
+
+
 def lookme_destroy(h):
     if h:
         _check(load().lookme_destroy(h))
@@ -224,6 +237,15 @@ class Table:
         n = scene.numel() // layers
         lookme_inject_kept(self.handle, layers, n, n_keep, kept, scene, prim, w, hidden,
                            hidden.shape[-1], stream)
+
+    def set_relevance(self, w1, b1, w2, b2):
+        self.relevance = (w1, b1, w2, b2)      # keep alive
+        lookme_set_relevance(self.handle, w1.shape[0], w1, b1, w2, b2)
+
+    def lookup_relevance(self, q, scene, act_out, prim_out, w_out, layers=1, stream=None):
+        n = scene.numel() // layers
+        lookme_lookup_relevance(self.handle, layers, n, q, scene, act_out, prim_out, w_out,
+                                stream)
 
     def close(self):
         if self.handle:

@@ -5,4 +5,5 @@ tensors with the shapes and distributions of the paper's workloads and is the
 one piece shared by the tests, the benchmark and the CPU oracle's callers.
 """
 
-from .gen import Workload, WORKLOADS, make_inputs, make_integer_inputs, n_keep_for  # noqa: F401
+from .gen import (Workload, WORKLOADS, make_inputs, make_integer_inputs,  # noqa: F401
+                  make_relevance, n_keep_for)

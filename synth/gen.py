@@ -37,6 +37,7 @@ CHUNK = 1 << 26
 
 TID_X, TID_K1, TID_K2, TID_V, TID_LABELS, TID_CENT, TID_PERM = 1, 2, 3, 4, 5, 6, 7
 TID_W, TID_DELTA, TID_H = 10, 20, 30
+TID_MLP_W1, TID_MLP_B1, TID_MLP_W2, TID_MLP_B2 = 40, 41, 42, 43
 
 
 @dataclasses.dataclass(frozen=True)
@@ -215,3 +216,20 @@ def make_integer_inputs(n: int, S: int, P: int, d_e: int, d_v: int, d_h: int, k:
     return dict(workload=None, x=x, wt=None, scene_keys=scene_keys, prim_keys=prim_keys,
                 values=values, bias=None, delta=delta, hidden=hidden, labels=None, k=k,
                 n_keep=n_keep)
+
+
+def make_relevance(wl: Workload, seed: int, hidden: int, device="cpu") -> dict:
+    """Seeded weights of a scene-shared relevance MLP (the paper trains them;
+    none are available here): W1 [hidden, 2 d_e] ~ N(0, 1/(2 d_e)) and
+    W2 [P, hidden] ~ N(0, 2/hidden), so that activations and logits stay of
+    order one, in the workload's dtype; biases b1 [hidden], b2 [P] ~ N(0, 0.1)
+    in float32."""
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[wl.dtype]
+    base = 1000 * seed
+    w1 = _randn_rows(hidden, 2 * wl.d_e, base + TID_MLP_W1, dev,
+                     1.0 / math.sqrt(2 * wl.d_e), dt)
+    b1 = _randn_rows(1, hidden, base + TID_MLP_B1, dev, 0.1, torch.float32)[0]
+    w2 = _randn_rows(wl.prims, hidden, base + TID_MLP_W2, dev, math.sqrt(2.0 / hidden), dt)
+    b2 = _randn_rows(1, wl.prims, base + TID_MLP_B2, dev, 0.1, torch.float32)[0]
+    return dict(w1=w1, b1=b1.contiguous(), w2=w2, b2=b2.contiguous(), hidden=hidden)

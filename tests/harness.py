@@ -85,6 +85,74 @@ class Run:
         return self
 
 
+class RelevanceRun(Run):
+    """A pass with Level-2 in the paper's form (Eq. 6-7): routing, the
+    relevance lookup (hidden activations, primitives, weights), then the kept
+    set and the injection as in the configured path."""
+
+    def __init__(self, inp: dict, mlp: dict, **kw):
+        super().__init__(inp, **kw)
+        self.mlp = mlp
+        self.act = torch.full((self.L, self.n, mlp["hidden"]), 7, dtype=inp["x"].dtype,
+                              device=self.dev)
+        self.table.set_relevance(mlp["w1"], mlp["b1"], mlp["w2"], mlp["b2"])
+
+    def run(self):
+        inp, L = self.inp, self.L
+        self.table.route(inp["x"], inp["wt"], self.q, self.scene, layers=L, stream=self.stream)
+        self.table.lookup_relevance(self.q, self.scene, self.act, self.prim, self.w, layers=L,
+                                    stream=self.stream)
+        self.table.inject(inp["delta"], self.scene, self.prim, self.w, self.hidden, self.n_keep,
+                          kept_out=self.kept, layers=L, stream=self.stream)
+        return self
+
+
+def check_relevance_run(r: RelevanceRun, tokens=None) -> C.Report:
+    """Stage-wise check of a relevance pass on the sampled tokens: q and the
+    scene as in check_run, the hidden activations (C1 bound), the primitives
+    and weights on the library's activations (C3/C4), the injected rows."""
+    torch.cuda.synchronize()
+    inp, mlp = r.inp, r.mlp
+    dt = dtype_name(inp["x"])
+    rep = C.Report()
+    toks = np.arange(r.n) if tokens is None else np.asarray(tokens)
+    tsel = torch.as_tensor(toks, device=r.dev)
+    K1 = f64(inp["scene_keys"])
+    w1, w2 = f64(mlp["w1"]), f64(mlp["w2"])
+    b1 = mlp["b1"].cpu().numpy().astype(np.float64)
+    b2 = mlp["b2"].cpu().numpy().astype(np.float64)
+    prim_keys = inp["prim_keys"]
+    values = inp["values"]
+    x64 = f64(inp["x"][tsel])
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    for l in range(r.L):
+        q_bits = to_np(r.q[l])[toks]
+        if inp["wt"] is not None:
+            C.check_projection(q_bits, x64, f64(inp["wt"][l]), dt, rep)
+        q_lib = O.to_f64(q_bits, dt)
+        scene = to_np(r.scene[l]).astype(np.int64)
+        C.check_scene(q_lib, K1, None, "dot", scene[toks], rep)
+        act_bits = to_np(r.act[l])[toks]
+        C.check_relevance_hidden(act_bits, q_lib, scene[toks], K1, w1, b1, dt, rep)
+        prim = to_np(r.prim[l])
+        w = to_np(r.w[l])
+        w_orc = C.check_relevance_prim(O.to_f64(act_bits, dt), w2, b2, q_lib, scene[toks],
+                                       lambda s: f64(prim_keys[s]), r.k, prim[toks], w[toks],
+                                       rep)
+        w_of = {int(t): w_orc[i] for i, t in enumerate(toks)}
+        c = O.criticality(f64(inp["delta"][l]))
+        kept = to_np(r.kept[l])[: r.n_keep]
+        C.check_kept(c, r.n_keep, kept, rep)
+        C.check_hidden(to_np(r.h_in[l][tsel]), to_np(r.hidden[l][tsel]), dt, values_rows, r.P,
+                       scene, prim, lambda t: w_of[t], kept, rep, tokens=toks,
+                       w_lib_of=lambda t: w[t])
+    return rep.finish()
+
+
 def check_run(r: Run, tokens=None, layers=None) -> C.Report:
     """Stage-wise comparison of a finished run against the oracle.
 

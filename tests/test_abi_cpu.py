@@ -149,6 +149,39 @@ def test_calls_validate_before_launch(lib):
         lk.lookme_destroy(h)
 
 
+def test_relevance_entry_points_validate(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        # lookup before any MLP is registered
+        assert S(lambda: lk.lookme_lookup_relevance(h, 1, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 0)) \
+            == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_relevance(h, 0, FAKE, None, FAKE, None)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_relevance(h, 24, FAKE, None, FAKE, None)) == \
+            lk.LOOKME_ERR_UNSUPPORTED        # 48 bytes: not whole 64-byte steps
+        assert S(lambda: lk.lookme_set_relevance(h, 512, None, None, FAKE, None)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_relevance(h, 512, FAKE, FAKE + 2, FAKE, None)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_relevance(h, 512, FAKE, None, FAKE, None)) == lk.LOOKME_OK
+        assert S(lambda: lk.lookme_lookup_relevance(h, 1, 0, None, None, None, None, None, 0)) \
+            == lk.LOOKME_OK
+        assert S(lambda: lk.lookme_lookup_relevance(h, 1, 8, FAKE, None, FAKE, FAKE, FAKE, 0)) \
+            == lk.LOOKME_ERR_INVALID
+    finally:
+        lk.lookme_destroy(h)
+    # the first layer needs key rows in whole 128-byte stages
+    h = lk.lookme_create(_desc(dtype=lk.LOOKME_BF16, key_dim=32), FAKE, FAKE, FAKE)
+    try:
+        assert _status(lambda: lk.lookme_set_relevance(h, 64, FAKE, None, FAKE, None))[0] == \
+            lk.LOOKME_ERR_UNSUPPORTED
+    finally:
+        lk.lookme_destroy(h)
+
+
 def test_null_handle(lib):
     assert _status(lambda: lk.lookme_workspace_size(None, 1, 1))[0] == lk.LOOKME_ERR_INVALID
     assert _status(lambda: lk.lookme_route(None, 1, 1, 1, FAKE, FAKE, FAKE, FAKE, 0))[0] == \

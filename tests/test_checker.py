@@ -144,3 +144,40 @@ def test_projection_bound_accepts_float32_accumulation_and_rejects_errors():
     rep = C.Report()
     C.check_projection(bad_bits.astype(np.uint16), x, w, "bf16", rep)
     assert not rep.ok
+
+
+def test_relevance_checks_accept_the_oracle_and_reject_planted_errors():
+    """The relevance-mode checks pass the oracle's own answer and fail a
+    swapped primitive, a wrong weight and an activation off by a lot."""
+    rng = np.random.default_rng(7)
+    n, d_e, S, P, h, k = 5, 8, 3, 20, 6, 4
+    q = rng.standard_normal((n, d_e))
+    keys = rng.standard_normal((S, d_e))
+    w1 = rng.standard_normal((h, 2 * d_e)) * 0.3
+    b1 = rng.standard_normal(h) * 0.1
+    w2 = rng.standard_normal((P, h))
+    b2 = rng.standard_normal(P) * 0.1
+    K2 = rng.standard_normal((S, P, d_e))
+    scene = rng.integers(0, S, n)
+    a = O.relevance_hidden(q, scene, keys, w1, b1, "f32")
+    prim, w, _ = O.relevance_lookup(q, scene, a, w2, b2, K2, k)
+    rep = C.Report()
+    C.check_relevance_hidden(a.astype(np.float32), q, scene, keys, w1, b1, "f32", rep)
+    C.check_relevance_prim(a, w2, b2, q, scene, lambda s: K2[s], k, prim, w, rep)
+    assert rep.finish().ok, str(rep)
+    bad = prim.copy()
+    r = O.relevance_logits(a, w2, b2)
+    bad[0, -1] = int(np.argsort(r[0])[0])          # the worst primitive instead
+    rep = C.Report()
+    C.check_relevance_prim(a, w2, b2, q, scene, lambda s: K2[s], k, bad, w, rep)
+    assert not rep.ok
+    w_bad = w.copy()
+    w_bad[1, 0] += 1e-3
+    rep = C.Report()
+    C.check_relevance_prim(a, w2, b2, q, scene, lambda s: K2[s], k, prim, w_bad, rep)
+    assert not rep.ok
+    a_bad = a.astype(np.float32).copy()
+    a_bad[2, 1] += 0.5
+    rep = C.Report()
+    C.check_relevance_hidden(a_bad, q, scene, keys, w1, b1, "f32", rep)
+    assert not rep.ok

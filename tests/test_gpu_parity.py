@@ -12,7 +12,7 @@ import pytest
 import torch
 
 from oracle import lookme_oracle as O
-from synth import WORKLOADS, Workload, make_inputs, make_integer_inputs
+from synth import WORKLOADS, Workload, make_inputs, make_integer_inputs, make_relevance
 
 pytestmark = pytest.mark.gpu
 
@@ -219,6 +219,44 @@ def test_layers_batched_equal_sequential():
         torch.cuda.synchronize()
         for name in ("q", "scene", "prim", "w", "kept", "hidden"):
             assert torch.equal(getattr(full, name)[l], getattr(r, name)[0]), (l, name)
+
+
+# Level-2 in the paper's form (Eq. 6-7): (workload, hidden width, sampled
+# tokens or None for all).  Hidden widths of 96 and 48 give a ragged 64-wide
+# tile in the first layer and 192-byte rows in the second (three 64-byte
+# steps: the masked 4-step kernel); the image case has the benchmark's
+# shapes.
+RELEVANCE = {
+    "bf16_rel_l2": (Workload("bf16_rel_l2", "bf16", 300, 2, 256, 128, 20, 200, 64, 64, 8, 30,
+                             usage="uniform"), 96, None),
+    "f32_rel": (Workload("f32_rel", "f32", 77, 1, 96, 64, 5, 37, 40, 40, 3, 40, usage="iid"),
+                48, None),
+    "bf16_rel_k32": (Workload("bf16_rel_k32", "bf16", 130, 1, 128, 64, 7, 300, 32, 32, 32, 30,
+                              usage="uniform"), 64, None),
+    "bf16_rel_image": (WORKLOADS[1], 512, 80),
+}
+
+
+@pytest.mark.parametrize("name", list(RELEVANCE))
+def test_relevance_lookup(name):
+    """Routing, the relevance MLP, top-k by logit, cos + tanh weights and the
+    injection, stage by stage against the oracle."""
+    from tests.harness import RelevanceRun, check_relevance_run
+    wl, hidden, sample = RELEVANCE[name]
+    _announce(f"relevance {name}: {wl} hidden {hidden}")
+    inp = make_inputs(wl, seed=5, device=DEV)
+    mlp = make_relevance(wl, 5, hidden, device=DEV)
+    r = RelevanceRun(inp, mlp).run()
+    toks = None
+    if sample:
+        toks = np.random.default_rng(5).choice(wl.n_tokens, sample, replace=False)
+    rep = check_relevance_run(r, tokens=toks)
+    assert rep.ok, str(rep)
+    assert min(rep.decisions.get(kind, 0) for kind in ("act", "prim", "w", "hidden_row")) > 0
+    r2 = RelevanceRun(inp, mlp, table=r.table).run()
+    torch.cuda.synchronize()
+    for key in ("act", "prim", "w"):
+        assert torch.equal(getattr(r, key), getattr(r2, key)), key
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
