@@ -35,6 +35,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}     # dense, MI355X
 METRIC = "multimodal tokens looked up+injected/sec at 1 MI355X; % HBM BW / % MFMA peak"
 
 
@@ -47,6 +48,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=0, help="table copies (0: automatic)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=0, help="oracle sample size (0: auto)")
+    ap.add_argument("--relevance", type=int, default=0, metavar="HIDDEN",
+                    help="Level-2 in the paper's form (relevance MLP of this hidden width, "
+                         "seeded weights) instead of the key-scored Level-2")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -164,7 +168,7 @@ def stored_traffic(wl):
 
 
 class Bench:
-    def __init__(self, wl, seed, copies):
+    def __init__(self, wl, seed, copies, relevance=0):
         import torch
         from paper_2607_16305_amd import lookme as lk
         from synth import make_inputs
@@ -195,6 +199,15 @@ class Bench:
         self.w = torch.empty((L, n, k), dtype=torch.float32, device=dev)
         self.kept = torch.empty((L, max(wl.n_keep, 1)), dtype=torch.int32, device=dev)
         self.hidden = inp["hidden"].clone()
+        self.mlp = None
+        if relevance:
+            from synth import make_relevance
+            self.mlp = make_relevance(wl, seed, relevance, device="cuda")
+            m = self.mlp
+            for t in self.tables:
+                t.set_relevance(m["w1"], m["b1"], m["w2"], m["b2"])
+                t.reserve(L, n)          # the relevance logits need a larger workspace
+            self.act = torch.empty((L, n, relevance), dtype=dt, device=dev)
         # the kept set is selected on a second stream (default priority, as
         # the first) while routing and lookup run; two reusable events order
         # the streams within a step
@@ -220,7 +233,11 @@ class Bench:
                          self.side_handle)
         self.ev_kept.record(self.side)
         lk.lookme_route(h, L, n, wl.d_in, inp["x"], inp["wt"], self.q, self.scene, self.stream)
-        lk.lookme_lookup(h, L, n, self.q, self.scene, self.prim, self.w, self.stream)
+        if self.mlp is None:
+            lk.lookme_lookup(h, L, n, self.q, self.scene, self.prim, self.w, self.stream)
+        else:
+            lk.lookme_lookup_relevance(h, L, n, self.q, self.scene, self.act, self.prim, self.w,
+                                       self.stream)
         self.main.wait_event(self.ev_kept)
         lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
                               self.hidden, wl.d_h, self.stream)
@@ -274,6 +291,11 @@ class Bench:
         b["inject"] = keep * (k * wl.d_v * es + 2 * wl.d_v * es + k * 8 + 8)
         flops = {"project": 2 * n * wl.d_in * L * wl.d_e, "route": 2 * rows * wl.d_e * wl.scenes,
                  "score": 2 * rows * wl.d_e * wl.prims}
+        if self.mlp is not None:
+            hid = self.mlp["hidden"]
+            # the two MLP layers (the cosines are 2 k d_e per row, negligible)
+            flops["score"] = 2 * rows * 2 * wl.d_e * hid + 2 * rows * hid * wl.prims
+            b["score"] = None
         return b, flops, nonempty
 
 
@@ -306,6 +328,12 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
         def __getitem__(self, i):
             return O.to_f64(self.a[i], dt)
 
+    mlp = None
+    if b.mlp is not None:
+        f = lambda t: t.detach().cpu().numpy().astype(np.float64)
+        mlp = (O.to_f64(to_np(b.mlp["w1"]), dt), f(b.mlp["b1"]), O.to_f64(to_np(b.mlp["w2"]), dt),
+               f(b.mlp["b2"]))
+
     # the sample is repeated until about min_seconds of CPU work have been
     # timed (the same inputs each time), so that the rate is not a single
     # short measurement
@@ -315,14 +343,15 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
             t0 = time.perf_counter()
             res = O.run(O.to_f64(x, dt), None if wt is None else O.to_f64(wt, dt),
                         O.to_f64(K1, dt), Rows(K2), Rows(V), None, O.to_f64(D, dt),
-                        O.to_f64(H, dt), k=wl.top_k, n_keep=n_keep, dtype=dt)
+                        O.to_f64(H, dt), k=wl.top_k, n_keep=n_keep, dtype=dt, mlp=mlp)
             el += time.perf_counter() - t0
             reps += 1
             assert res["hidden"].shape == (wl.layers, m, wl.d_h)
     return {"value": reps * wl.layers * m / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {m} of {wl.n_tokens} tokens x {wl.layers} layer(s), whole path "
-                      f"(projection..injection, n_keep={n_keep}), float64 NumPy, 1 thread, "
-                      f"{reps} repetitions, {el:.1f} s"}
+                      f"(projection..injection, n_keep={n_keep}"
+                      f"{', relevance Level-2' if mlp is not None else ''}), float64 NumPy, "
+                      f"1 thread, {reps} repetitions, {el:.1f} s"}
 
 
 def main():
@@ -345,7 +374,7 @@ def main():
     torch.cuda.set_device(0)
     if args.pmc_calibrate:
         calibration_copy()
-    b = Bench(wl, args.workload, args.copies)
+    b = Bench(wl, args.workload, args.copies, args.relevance)
 
     for i in range(args.warmup):
         b.step(i)
@@ -358,7 +387,7 @@ def main():
     kern = {}
     for name, ms in prof.items():
         e = {"avg_us": round(ms * 1000.0, 3)}
-        if name in bytes_:
+        if bytes_.get(name):
             gbs = bytes_[name] / (ms * 1e-3) / 1e9
             e["gbps"] = round(gbs, 1)
             e["hbm_frac"] = round(gbs / HBM_PEAK_GBS, 4)
@@ -366,12 +395,24 @@ def main():
             e["tflops"] = round(flops[name] / (ms * 1e-3) / 1e12, 2)
         kern[name] = e
     score_ms = prof.get("score")
-    achieved = bytes_["score"] / (score_ms * 1e-3) / 1e9 if score_ms else None
-    roofline = {"bound": "hbm", "kernel": "score_kernel (Level-2 scoring + top-k + softmax)",
-                "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
-                "traffic": stored_traffic(wl), "algorithmic_bytes_per_launch": bytes_["score"],
-                "nonempty_scenes": nonempty}
+    if b.mlp is None:
+        achieved = bytes_["score"] / (score_ms * 1e-3) / 1e9 if score_ms else None
+        roofline = {"bound": "hbm", "kernel": "score_kernel (Level-2 scoring + top-k + softmax)",
+                    "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
+                    "traffic": stored_traffic(wl),
+                    "algorithmic_bytes_per_launch": bytes_["score"], "nonempty_scenes": nonempty}
+    else:
+        # the relevance lookup is a pair of dense products: judged on the
+        # matrix cores, whole launch group (both MLP layers and the weights)
+        peak = MFMA_PEAK_TFLOPS[wl.dtype]
+        achieved = flops["score"] / (score_ms * 1e-3) / 1e12 if score_ms else None
+        roofline = {"bound": "mfma",
+                    "kernel": "relevance lookup (MLP layers, top-k, cos + tanh weights)",
+                    "achieved": round(achieved, 2) if achieved else None, "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(achieved / peak, 4) if achieved else None,
+                    "traffic": None, "algorithmic_flops_per_launch": flops["score"]}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -386,7 +427,9 @@ def main():
         "config": {"workload": wl.name, "tokens": wl.n_tokens, "layers": wl.layers,
                    "d_in": wl.d_in, "d_e": wl.d_e, "scenes": wl.scenes, "prims": wl.prims,
                    "d_v": wl.d_v, "d_h": wl.d_h, "top_k": wl.top_k, "n_keep": wl.n_keep,
-                   "usage": wl.usage, "table_copies": b.copies},
+                   "usage": wl.usage, "table_copies": b.copies,
+                   "level2": (f"relevance MLP, hidden {args.relevance}" if args.relevance
+                              else "primitive keys")},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kern,

@@ -183,14 +183,15 @@ lookme_status_t lookme_inject_kept(lookme_t h, int32_t layers, int64_t n, int64_
  * lookme_set_relevance -- registers the scene-shared relevance MLP that
  * Level-2 uses in the paper's own form (Sec. 3.2, Eq. 6).  The tensors are
  * borrowed like the table (they must stay alive and unmodified while used):
- *   hidden  width h of the hidden layer; h * elem_size a multiple of 64 bytes
+ *   hidden  width h of the hidden layer; h * elem_size a multiple of 128 bytes
  *   w1      [h, 2 * key_dim] dtype; columns [0, key_dim) act on the query,
  *           [key_dim, 2 key_dim) on the scene key e_img[j]
  *   b1      [h] float32, or NULL for zero
  *   w2      [prims_per_scene, h] dtype
  *   b2      [prims_per_scene] float32, or NULL for zero
  * Needs key_dim * elem_size a multiple of 128 bytes.  Replaces an earlier
- * registration.
+ * registration.  From then on lookme_workspace_size includes the lookup's
+ * logits, layers * n * prims_per_scene float32.
  */
 lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
                                      const float* b1, const void* w2, const float* b2);
@@ -206,7 +207,8 @@ lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
  *   w_out      [layers, n, k] float32: softmax over the k of
  *              cos(q, prim_keys[scene, p]) + tanh(r_p) (cosine 0 for a zero
  *              vector)
- * Needs no workspace.
+ * Needs the workspace of lookme_workspace_size (queried after
+ * lookme_set_relevance): the logits of every row go through it.
  */
 lookme_status_t lookme_lookup_relevance(lookme_t h, int32_t layers, int64_t n, const void* q,
                                         const int32_t* scene, void* act_out, int32_t* prim_out,

@@ -274,13 +274,15 @@ def inject(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarray,
 
 
 def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
-        k: int, n_keep: int, dtype: str, score: str = "dot"):
+        k: int, n_keep: int, dtype: str, score: str = "dot", mlp=None):
     """Whole path for L layers sharing one table (Sec. 3.3 inter-layer reuse).
 
     x [n, d_in]; w_t [L, d_e, d_in] or None; delta [L, n, d_c];
-    hidden [L, n, d_h]; all float64 values.  Returns a dict of per-layer
-    results: q [L,n,d_e], scene [L,n], prim [L,n,k], w [L,n,k],
-    kept [L,n_keep], hidden [L,n,d_h].
+    hidden [L, n, d_h]; all float64 values.  ``mlp`` = (w1, b1, w2, b2)
+    selects Level-2 in the paper's form (relevance_hidden/relevance_lookup)
+    instead of the key-scored one.  Returns a dict of per-layer results:
+    q [L,n,d_e], scene [L,n], prim [L,n,k], w [L,n,k], kept [L,n_keep],
+    hidden [L,n,d_h].
     """
     L = hidden.shape[0]
     P = prim_keys.shape[1]
@@ -288,7 +290,12 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
     for l in range(L):
         q = project(x, None if w_t is None else w_t[l], dtype)
         sc = route(q, scene_keys, bias, score)
-        pr, ww, _ = lookup(q, sc, prim_keys, k, score)
+        if mlp is None:
+            pr, ww, _ = lookup(q, sc, prim_keys, k, score)
+        else:
+            w1, b1, w2, b2 = mlp
+            a = relevance_hidden(q, sc, scene_keys, w1, b1, dtype)
+            pr, ww, _ = relevance_lookup(q, sc, a, w2, b2, prim_keys, k)
         kept = select(criticality(delta[l]), n_keep)
         h = inject(hidden[l], values, P, sc, pr, ww, kept, dtype)
         for name, v in zip(res, (q, sc, pr, ww, kept, h)):

@@ -92,7 +92,7 @@ hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, int shared_r
 // The MLP's tensors are borrowed from the caller: w1 [hidden, 2 d_e] and
 // w2 [P, hidden] in the table's dtype, b1 [hidden] and b2 [P] float32 (or
 // null).  launch_relevance writes act [rows, hidden], prim [rows, k] and
-// w [rows, k]; launch_relevance_topk writes the top-k logits into w.
+// w [rows, k], with logits [rows, P] float32 as scratch (workspace).
 struct RelevanceMlp {
   int hidden;
   const void* w1;
@@ -103,10 +103,7 @@ struct RelevanceMlp {
 hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const void* scene_keys,
                             const void* prim_keys, const RelevanceMlp& mlp, int64_t rows, int d_e,
                             int S, int P, int k, void* act, int32_t* prim, float* w,
-                            hipStream_t st);
-hipError_t launch_relevance_topk(int dt, const void* act, const void* w2, const float* b2,
-                                 int64_t rows, int hidden, int P, int k, int32_t* prim,
-                                 float* logits, hipStream_t st);
+                            float* logits, hipStream_t st);
 
 // ---- Level-2 scoring of bucketed rows, fused top-k + softmax --------------
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,

@@ -66,7 +66,7 @@ constexpr int32_t MAX_SCENES = 16384;   // bucketing keeps one histogram per chu
 // Workspace layout for `layers` x `n` rows.
 struct Layout {
   size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, route_count,
-      route_part, crit_key, kept, total;
+      route_part, crit_key, kept, rel_logits, total;
 };
 
 // The leading bytes of the workspace hold counters that start at zero; they
@@ -74,7 +74,7 @@ struct Layout {
 // them at zero.
 constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_COUNTERS * 4;
 
-Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n) {
+Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance) {
   const int64_t rows = (int64_t)layers * n;
   const int64_t chunks = lookme::bucket_chunks(rows);
   const int64_t units = lookme::bucket_max_units(rows, d.num_scenes);
@@ -98,6 +98,8 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n) {
   L.unit_begin = take((size_t)units * 4);
   L.crit_key = take((size_t)rows * 4);
   L.kept = take((size_t)rows * 4);
+  // relevance logits [rows, P] float32, when an MLP is registered
+  L.rel_logits = take(relevance ? (size_t)rows * d.prims_per_scene * 4 : 0);
   L.total = off;
   return L;
 }
@@ -123,7 +125,7 @@ lookme_status_t check_layers_n(int32_t layers, int64_t n) {
 }
 
 lookme_status_t check_workspace(lookme_t h, int32_t layers, int64_t n, Layout* L) {
-  *L = layout(h->d, layers, n);
+  *L = layout(h->d, layers, n, h->rel.hidden > 0);
   if (h->ws == nullptr) return fail(LOOKME_ERR_WORKSPACE, "no workspace set");
   if (h->ws_bytes < L->total)
     return fail(LOOKME_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed for %d x %lld rows",
@@ -322,7 +324,7 @@ lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_toke
   LOOKME_TRY(check_handle(h));
   if (bytes == nullptr) return fail(LOOKME_ERR_INVALID, "bytes is NULL");
   LOOKME_TRY(check_layers_n(layers, n_tokens));
-  *bytes = layout(h->d, layers, n_tokens).total;
+  *bytes = layout(h->d, layers, n_tokens, h->rel.hidden > 0).total;
   return LOOKME_OK;
 }
 
@@ -488,8 +490,8 @@ lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
   LOOKME_TRY(check_handle(h));
   const int es = elem_size(h->d.dtype);
   if (hidden < 1) return fail(LOOKME_ERR_INVALID, "hidden must be positive (got %d)", hidden);
-  if (((int64_t)hidden * es) % 64 != 0)
-    return fail(LOOKME_ERR_UNSUPPORTED, "hidden * elem_size must be a multiple of 64 bytes");
+  if (((int64_t)hidden * es) % 128 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "hidden * elem_size must be a multiple of 128 bytes");
   if (((int64_t)h->d.key_dim * es) % 128 != 0)
     return fail(LOOKME_ERR_UNSUPPORTED, "key_dim * elem_size must be a multiple of 128 bytes");
   LOOKME_TRY(check_ptr(w1, "w1"));
@@ -514,14 +516,18 @@ lookme_status_t lookme_lookup_relevance(lookme_t h, int32_t layers, int64_t n, c
   LOOKME_TRY(check_ptr(act_out, "act_out"));
   LOOKME_TRY(check_ptr(prim_out, "prim_out"));
   LOOKME_TRY(check_ptr(w_out, "w_out"));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
   const lookme_desc_t& d = h->d;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Timed tm(h, LOOKME_GROUP_SCORE, st);
-  return hip_status(lookme::launch_relevance(d.dtype, q, scene, h->scene_keys, h->prim_keys,
-                                             h->rel, (int64_t)layers * n, d.key_dim,
-                                             d.num_scenes, d.prims_per_scene, d.top_k, act_out,
-                                             prim_out, w_out, st),
-                    "relevance lookup launch");
+  return hip_status(
+      lookme::launch_relevance(d.dtype, q, scene, h->scene_keys, h->prim_keys, h->rel,
+                               (int64_t)layers * n, d.key_dim, d.num_scenes, d.prims_per_scene,
+                               d.top_k, act_out, prim_out, w_out,
+                               reinterpret_cast<float*>(static_cast<char*>(h->ws) + L.rel_logits),
+                               st),
+      "relevance lookup launch");
 }
 
 }  // extern "C"

@@ -1,20 +1,20 @@
 // Level-2 in the paper's own form (arXiv 2607.16305, Sec. 3.2, Eq. 6-7):
 // a scene-shared two-layer MLP on [v_e, e_img[j]] gives one relevance logit
 // per primitive, the top k primitives by logit are kept, and their weights
-// are the softmax of cos(v_e, e_{j,p}) + tanh(r_j[p]).  Three launches:
+// are the softmax of cos(v_e, e_{j,p}) + tanh(r_j[p]).  Four launches:
 //
-//   relevance_hidden_kernel   a = round(ReLU([q_t, K1[scene_t]] W1^T + b1)):
+//   rel_gemm_kernel (hidden)  a = round(ReLU([q_t, K1[scene_t]] W1^T + b1)):
 //                             64 x 64 output tiles on the matrix cores, the
 //                             operand-A row of token t being its query
 //                             followed by its scene's key (gathered per row,
 //                             K stages of 128 bytes straight into LDS);
-//   score_kernel (dense)      r = a W2^T + b2 with a fused top-k over the N_p
-//                             logits (the Level-2 scoring kernel's shared
-//                             units, every row against the one key set W2);
-//                             writes the k logits, not weights;
+//   rel_gemm_kernel (logits)  r = a W2^T + b2 in float32, to the workspace;
+//   relevance_topk_kernel     one wave per row: the k largest logits (lowest
+//                             p on ties), each lane keeping a sorted list of
+//                             its strided share, merged across the wave;
 //   relevance_weights_kernel  one wave per row: the k cosines against the
 //                             chosen primitive keys, + tanh of the logits,
-//                             softmax over the k (in place of the logits).
+//                             softmax over the k.
 #include "common.h"
 #include "dtl.h"
 #include "kernels.h"
@@ -26,20 +26,23 @@ namespace lookme {
 using RhShape = DtlShape<2, 2, 2, 2, 128>;
 constexpr int RH_KB = 128;
 
-struct RelHiddenParams {
-  const char* q;            // [rows, d_e]
-  const int32_t* scene;     // [rows]
-  const char* keys;         // [S, d_e] scene keys
-  const char* w1;           // [h, 2 d_e]
-  const float* b1;          // [h] or null
-  char* act;                // [rows, h]
+struct RelGemmParams {
+  const char* a0;           // operand-A rows: stages [0, ksplit) from a0 + row * a_bytes
+  const char* a1;           // stages [ksplit, nst) from a1 + sel(row) * a_bytes, or null
+  const int32_t* sel;       // [rows] row of a1 for each A row (clamped to [0, sel_rows))
+  const char* b;            // [cols, K] operand-B rows
+  const float* bias;        // [cols] or null
+  char* out;                // [rows, cols]: dtype (EPI_ACT) or float32 (EPI_LOGIT)
   int64_t rows;
-  int64_t q_bytes;          // d_e * elem size, a multiple of 128
-  int S, h, tiles;
+  int64_t a_bytes;          // bytes of an A row half (a0 and a1 rows)
+  int64_t k_bytes;          // K in bytes, a multiple of 128
+  int sel_rows, cols, ksplit, tiles;
 };
 
-template <int DT>
-__global__ __launch_bounds__(256) void relevance_hidden_kernel(RelHiddenParams a) {
+enum : int { EPI_ACT = 0, EPI_LOGIT = 1 };
+
+template <int DT, int EPI>
+__global__ __launch_bounds__(256) void rel_gemm_kernel(RelGemmParams a) {
   using S = RhShape;
   constexpr int MI = 2, NJ = 2, KB = RH_KB, KSL = KB / 64, WN = 2;
   constexpr int ES = DT == DT_BF16 ? 2 : 4;
@@ -50,20 +53,20 @@ __global__ __launch_bounds__(256) void relevance_hidden_kernel(RelHiddenParams a
   const int n16 = lane & 15, g = lane >> 4;
   const int wm = (wv / WN) * 16 * MI, wn = (wv % WN) * 16 * NJ;
 
-  const int tiles_n = (a.h + S::BN - 1) / S::BN;
+  const int tiles_n = (a.cols + S::BN - 1) / S::BN;
   const int tile = xcd_remap(blockIdx.x, a.tiles);
   if (tile < 0) return;
   const int64_t m0 = (int64_t)(tile / tiles_n) * S::BM;
   const int n0 = (tile % tiles_n) * S::BN;
-  const int nq = (int)(a.q_bytes / KB);   // stages of the query half of K
-  const int nst = 2 * nq;
+  const int nst = (int)(a.k_bytes / KB);
 
-  // load b covers tile row trow (A rows first, then B rows); p0 serves the
-  // stages of the first half of K, p1 those of the second: for an A row the
-  // token's query and its scene's key, for a B row the two halves of the
-  // W1 row.  Rows past the edge are clamped (their outputs are not stored).
+  // load b covers tile row trow (A rows first, then B rows); an A row takes
+  // its first ksplit stages from p0 and the rest from p1 (the hidden layer:
+  // the token's query, then its scene's key); a B row is contiguous.  Rows
+  // past the edge are clamped (their outputs are not stored).
   const char* p0[S::PER_WAVE];
   const char* p1[S::PER_WAVE];
+  int split[S::PER_WAVE];
 #pragma unroll
   for (int b = 0; b < S::PER_WAVE; ++b) {
     const int trow = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
@@ -71,15 +74,21 @@ __global__ __launch_bounds__(256) void relevance_hidden_kernel(RelHiddenParams a
     if (trow < S::BM) {
       int64_t r = m0 + trow;
       r = r < a.rows ? r : a.rows - 1;
-      int s = a.scene[r];
-      s = s < 0 ? 0 : (s >= a.S ? a.S - 1 : s);
-      p0[b] = a.q + r * a.q_bytes + chunk * 16;
-      p1[b] = a.keys + (int64_t)s * a.q_bytes + chunk * 16;
+      p0[b] = a.a0 + r * a.a_bytes + chunk * 16;
+      if (a.a1 != nullptr) {
+        int s = a.sel[r];
+        s = s < 0 ? 0 : (s >= a.sel_rows ? a.sel_rows - 1 : s);
+        p1[b] = a.a1 + (int64_t)s * a.a_bytes + chunk * 16;
+      } else {
+        p1[b] = p0[b] + (int64_t)a.ksplit * KB;
+      }
+      split[b] = a.ksplit;
     } else {
       int r = n0 + trow - S::BM;
-      r = r < a.h ? r : a.h - 1;
-      p0[b] = a.w1 + (int64_t)r * 2 * a.q_bytes + chunk * 16;
-      p1[b] = p0[b] + a.q_bytes;
+      r = r < a.cols ? r : a.cols - 1;
+      p0[b] = a.b + (int64_t)r * a.k_bytes + chunk * 16;
+      p1[b] = p0[b];
+      split[b] = nst;
     }
   }
   auto issue = [&](int stage) {
@@ -87,7 +96,8 @@ __global__ __launch_bounds__(256) void relevance_hidden_kernel(RelHiddenParams a
     char* dst = lds[stage & 1];
 #pragma unroll
     for (int b = 0; b < S::PER_WAVE; ++b) {
-      const char* src = s < nq ? p0[b] + (int64_t)s * KB : p1[b] + (int64_t)(s - nq) * KB;
+      const char* src =
+          s < split[b] ? p0[b] + (int64_t)s * KB : p1[b] + (int64_t)(s - split[b]) * KB;
       load_lds16(src, dst + (wv * S::PER_WAVE + b) * 1024);
     }
   };
@@ -123,26 +133,95 @@ __global__ __launch_bounds__(256) void relevance_hidden_kernel(RelHiddenParams a
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
 
-  // the lane holds rows m0 + wm + 16 i + 4 g + r and hidden unit
-  // n0 + wn + 16 j + n16: + b1, ReLU, one rounding to the storage dtype
+  // the lane holds rows m0 + wm + 16 i + 4 g + r and column n0 + wn + 16 j +
+  // n16: + bias, then ReLU and one rounding to dtype (hidden layer) or a
+  // float32 store (logits)
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const int col = n0 + wn + 16 * j + n16;
-    if (col >= a.h) continue;
-    const float bias = a.b1 != nullptr ? a.b1[col] : 0.f;
+    if (col >= a.cols) continue;
+    const float bias = a.bias != nullptr ? a.bias[col] : 0.f;
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t row = m0 + wm + 16 * i + 4 * g + r;
         if (row >= a.rows) continue;
-        const float z = fmaxf(acc[i][j][r] + bias, 0.f);
-        char* dst = a.act + (row * a.h + col) * ES;
-        if constexpr (DT == DT_BF16)
-          *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16_rne(z);
-        else
-          *reinterpret_cast<float*>(dst) = z;
+        const float z = acc[i][j][r] + bias;
+        if constexpr (EPI == EPI_LOGIT) {
+          reinterpret_cast<float*>(a.out)[row * a.cols + col] = z;
+        } else {
+          char* dst = a.out + (row * a.cols + col) * ES;
+          if constexpr (DT == DT_BF16)
+            *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16_rne(fmaxf(z, 0.f));
+          else
+            *reinterpret_cast<float*>(dst) = fmaxf(z, 0.f);
+        }
       }
+  }
+}
+
+// One wave per row of logits [rows, P]: lane l keeps a sorted list of the
+// KL largest of logits l, l + 64, ... (visited in increasing p, so a strict
+// '>' keeps the lower p first among equal values), then k rounds of a
+// butterfly arg max over the 64 lists give the row's top k in order.
+template <int KL>
+__global__ __launch_bounds__(256) void relevance_topk_kernel(const float* __restrict__ logits,
+                                                             int64_t rows, int P, int k,
+                                                             int32_t* __restrict__ prim,
+                                                             float* __restrict__ top) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= rows) return;
+  const float* r = logits + t * P;
+  float ls[KL];
+  int li[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
+  for (int p = lane; p < P; p += WAVE) {
+    const float x = r[p];
+    if (x > ls[KL - 1]) {
+#pragma unroll
+      for (int e = KL - 1; e >= 1; --e) {
+        const bool above_prev = x > ls[e - 1];
+        const bool above_cur = x > ls[e];
+        const float s_keep = above_cur ? x : ls[e];
+        const int i_keep = above_cur ? p : li[e];
+        ls[e] = above_prev ? ls[e - 1] : s_keep;
+        li[e] = above_prev ? li[e - 1] : i_keep;
+      }
+      if (x > ls[0]) { ls[0] = x; li[0] = p; }
+    }
+  }
+  int head = 0;
+  float hs = ls[0];
+  int hi = li[0];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    if (e < k) {
+      float bs = hs;
+      int bi = hi;
+#pragma unroll
+      for (int d = 1; d < WAVE; d <<= 1) {
+        const float os = __shfl_xor(bs, d, 64);
+        const int oi = __shfl_xor(bi, d, 64);
+        if (beats(os, oi, bs, bi)) { bs = os; bi = oi; }
+      }
+      if (lane == 0) {
+        prim[t * k + e] = bi;
+        top[t * k + e] = bs;
+      }
+      if (hi == bi && hs == bs) {   // this lane's list supplied the winner
+        ++head;
+        float ns = -__builtin_inff();
+        int ni = -1;
+#pragma unroll
+        for (int x = 1; x < KL; ++x)
+          if (x == head) { ns = ls[x]; ni = li[x]; }
+        hs = ns;
+        hi = ni;
+      }
+    }
   }
 }
 
@@ -226,32 +305,67 @@ __global__ __launch_bounds__(256) void relevance_weights_kernel(
 hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const void* scene_keys,
                             const void* prim_keys, const RelevanceMlp& mlp, int64_t rows, int d_e,
                             int S, int P, int k, void* act, int32_t* prim, float* w,
-                            hipStream_t st) {
+                            float* logits, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
-  RelHiddenParams hp{};
-  hp.q = static_cast<const char*>(q);
-  hp.scene = scene;
-  hp.keys = static_cast<const char*>(scene_keys);
-  hp.w1 = static_cast<const char*>(mlp.w1);
-  hp.b1 = mlp.b1;
-  hp.act = static_cast<char*>(act);
-  hp.rows = rows;
-  hp.q_bytes = (int64_t)d_e * es;
-  hp.S = S;
-  hp.h = mlp.hidden;
-  hp.tiles = (int)(((rows + RhShape::BM - 1) / RhShape::BM) *
-                   ((mlp.hidden + RhShape::BN - 1) / RhShape::BN));
-  const unsigned grid = (unsigned)((hp.tiles + 7) / 8 * 8);
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL(relevance_hidden_kernel<DT_BF16>, dim3(grid), dim3(256), 0, st, hp);
-  else
-    hipLaunchKernelGGL(relevance_hidden_kernel<DT_F32>, dim3(grid), dim3(256), 0, st, hp);
-  hipError_t e = hipGetLastError();
+  auto gemm = [&](const RelGemmParams& gp, int epi) {
+    const unsigned grid = (unsigned)((gp.tiles + 7) / 8 * 8);
+    if (dt == DT_BF16) {
+      if (epi == EPI_ACT)
+        hipLaunchKernelGGL((rel_gemm_kernel<DT_BF16, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
+      else
+        hipLaunchKernelGGL((rel_gemm_kernel<DT_BF16, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
+    } else {
+      if (epi == EPI_ACT)
+        hipLaunchKernelGGL((rel_gemm_kernel<DT_F32, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
+      else
+        hipLaunchKernelGGL((rel_gemm_kernel<DT_F32, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
+    }
+    return hipGetLastError();
+  };
+  const int64_t rt = (rows + RhShape::BM - 1) / RhShape::BM;
+  // hidden layer: K = [query ; scene key]
+  RelGemmParams g1{};
+  g1.a0 = static_cast<const char*>(q);
+  g1.a1 = static_cast<const char*>(scene_keys);
+  g1.sel = scene;
+  g1.b = static_cast<const char*>(mlp.w1);
+  g1.bias = mlp.b1;
+  g1.out = static_cast<char*>(act);
+  g1.rows = rows;
+  g1.a_bytes = (int64_t)d_e * es;
+  g1.k_bytes = 2 * g1.a_bytes;
+  g1.sel_rows = S;
+  g1.cols = mlp.hidden;
+  g1.ksplit = (int)(g1.a_bytes / RH_KB);
+  g1.tiles = (int)(rt * ((mlp.hidden + RhShape::BN - 1) / RhShape::BN));
+  hipError_t e = gemm(g1, EPI_ACT);
   if (e != hipSuccess) return e;
-  e = launch_relevance_topk(dt, act, mlp.w2, mlp.b2, rows, mlp.hidden, P, k, prim, w, st);
+  // logits: r = a W2^T + b2, float32
+  RelGemmParams g2{};
+  g2.a0 = static_cast<const char*>(act);
+  g2.b = static_cast<const char*>(mlp.w2);
+  g2.bias = mlp.b2;
+  g2.out = reinterpret_cast<char*>(logits);
+  g2.rows = rows;
+  g2.a_bytes = (int64_t)mlp.hidden * es;
+  g2.k_bytes = g2.a_bytes;
+  g2.cols = P;
+  g2.ksplit = (int)(g2.k_bytes / RH_KB);
+  g2.tiles = (int)(rt * ((P + RhShape::BN - 1) / RhShape::BN));
+  e = gemm(g2, EPI_LOGIT);
   if (e != hipSuccess) return e;
   const dim3 wgrid((unsigned)((rows + 3) / 4));
+  if (k <= 4)
+    hipLaunchKernelGGL(relevance_topk_kernel<4>, wgrid, dim3(256), 0, st, logits, rows, P, k, prim, w);
+  else if (k <= 8)
+    hipLaunchKernelGGL(relevance_topk_kernel<8>, wgrid, dim3(256), 0, st, logits, rows, P, k, prim, w);
+  else if (k <= 16)
+    hipLaunchKernelGGL(relevance_topk_kernel<16>, wgrid, dim3(256), 0, st, logits, rows, P, k, prim, w);
+  else
+    hipLaunchKernelGGL(relevance_topk_kernel<32>, wgrid, dim3(256), 0, st, logits, rows, P, k, prim, w);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
 #define LOOKME_RW(DT_, K_)                                                                       \
   hipLaunchKernelGGL((relevance_weights_kernel<DT_, K_>), wgrid, dim3(256), 0, st,             \
                      static_cast<const char*>(q), scene, static_cast<const char*>(prim_keys), \

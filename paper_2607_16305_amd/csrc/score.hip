@@ -53,9 +53,6 @@ struct ScoreParams {
   uint64_t* route_part;     // routing, splits > 1: [tiles, splits, 16] (idx, score)
   int32_t* route_count;     // routing, splits > 1: [tiles] arrivals, left at zero
   int shared_rows;          // lookup: rows of a shared unit (at most)
-  int dense;                // lookup: rows 0..rows-1 all against one key set (the
-                            // relevance MLP's second layer), no buckets
-  int raw_out;              // lookup: write the top-k scores, not their softmax
   int32_t* out_idx;         // routing: scene[rows]; lookup: prim[rows, k]
   float* out_w;             // lookup: w[rows, k]
 };
@@ -77,14 +74,6 @@ __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int ken
   float v[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) v[r] = blk * 16 + 4 * g + r < kend ? acc[r] : -__builtin_inff();
-  if constexpr (LOOKUP) {
-    // per-key bias (the relevance MLP's b2); null for the primitive keys
-    if (bias != nullptr) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (blk * 16 + 4 * g + r < kend) v[r] += bias[blk * 16 + 4 * g + r];
-    }
-  }
   if constexpr (!LOOKUP) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -189,7 +178,7 @@ __device__ __forceinline__ void write_row(const ScoreParams& a, int64_t out_row,
     for (int e = 0; e < KL; ++e) {
       if (e < k) {
         po[e] = top_i[e];
-        wo[e] = a.raw_out ? top_s[e] : expf(top_s[e] - top_s[0]) * inv;
+        wo[e] = expf(top_s[e] - top_s[0]) * inv;
       }
     }
   }
@@ -197,7 +186,7 @@ __device__ __forceinline__ void write_row(const ScoreParams& a, int64_t out_row,
 
 template <bool LOOKUP>
 __device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, int slot) {
-  if constexpr (LOOKUP) return a.perm != nullptr ? a.perm[begin + slot] : begin + slot;
+  if constexpr (LOOKUP) return a.perm[begin + slot];
   else return begin + slot;
 }
 
@@ -481,28 +470,18 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   const char* keys;
   int key0 = 0, nk = a.nkeys, split = 0;
   if constexpr (LOOKUP) {
-    if (a.dense) {
-      // every row against the one key set: shared units of consecutive rows
-      begin = (int64_t)blockIdx.x * a.shared_rows;
-      if (begin >= a.rows) return;
-      nr = (int)min<int64_t>(a.shared_rows, a.rows - begin);
-      shared = true;
-      keys = a.keys;
-    } else {
-      // units in list order (the long shared units first), dealt to the
-      // XCDs in pairs: a scene whose bucket spans two units reads its keys
-      // into one XCD's L2 once, while a scene with many units is still
-      // spread over all
-      const int b = blockIdx.x, slot = b >> 3;
-      const int u = (slot >> 1) * 16 + (b & 7) * 2 + (slot & 1);
-      if (u >= *a.unit_count) return;
-      const int tag = a.unit_scene[u];
-      const int s = tag & ~UNIT_SHARED;
-      shared = (tag & UNIT_SHARED) != 0;
-      begin = a.unit_begin[u];
-      nr = min(shared ? a.shared_rows : UNIT_STREAM_ROWS, a.offsets[s + 1] - (int)begin);
-      keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
-    }
+    // units in list order (the long shared units first), dealt to the XCDs
+    // in pairs: a scene whose bucket spans two units reads its keys into one
+    // XCD's L2 once, while a scene with many units is still spread over all
+    const int b = blockIdx.x, slot = b >> 3;
+    const int u = (slot >> 1) * 16 + (b & 7) * 2 + (slot & 1);
+    if (u >= *a.unit_count) return;
+    const int tag = a.unit_scene[u];
+    const int s = tag & ~UNIT_SHARED;
+    shared = (tag & UNIT_SHARED) != 0;
+    begin = a.unit_begin[u];
+    nr = min(shared ? a.shared_rows : UNIT_STREAM_ROWS, a.offsets[s + 1] - (int)begin);
+    keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
   } else {
     const int R = a.route_rows;
     const int splits = R > 16 ? 1 : a.route_splits;
@@ -650,30 +629,6 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
   p.out_idx = prim;
   p.out_w = w;
   const int grid = (int)((ws.max_units + 15) / 16 * 16);   // whole pairs on every XCD
-  if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st);
-  if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st);
-  if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st);
-  return launch_dt<true, 32>(dt, p.ks, grid, p, st);
-}
-
-hipError_t launch_relevance_topk(int dt, const void* act, const void* w2, const float* b2,
-                                 int64_t rows, int hidden, int P, int k, int32_t* prim,
-                                 float* logits, hipStream_t st) {
-  ScoreParams p{};
-  p.q = static_cast<const char*>(act);
-  p.keys = static_cast<const char*>(w2);
-  p.bias = b2;
-  p.rows = rows;
-  p.row_bytes = (int64_t)hidden * (dt == DT_BF16 ? 2 : 4);
-  p.ks = (int)(p.row_bytes / 64);
-  p.shared_rows = shared_unit_rows(p.row_bytes, k);
-  p.nkeys = P;
-  p.k = k;
-  p.dense = 1;
-  p.raw_out = 1;
-  p.out_idx = prim;
-  p.out_w = logits;
-  const int grid = (int)((rows + p.shared_rows - 1) / p.shared_rows);
   if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st);
   if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st);
   if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st);

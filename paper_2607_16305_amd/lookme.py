@@ -244,6 +244,7 @@ class Table:
 
     def lookup_relevance(self, q, scene, act_out, prim_out, w_out, layers=1, stream=None):
         n = scene.numel() // layers
+        self.reserve(layers, n)
         lookme_lookup_relevance(self.handle, layers, n, q, scene, act_out, prim_out, w_out,
                                 stream)
 

@@ -160,15 +160,20 @@ def test_relevance_entry_points_validate(lib):
             == lk.LOOKME_ERR_INVALID
         assert S(lambda: lk.lookme_set_relevance(h, 0, FAKE, None, FAKE, None)) == \
             lk.LOOKME_ERR_INVALID
-        assert S(lambda: lk.lookme_set_relevance(h, 24, FAKE, None, FAKE, None)) == \
-            lk.LOOKME_ERR_UNSUPPORTED        # 48 bytes: not whole 64-byte steps
+        assert S(lambda: lk.lookme_set_relevance(h, 96, FAKE, None, FAKE, None)) == \
+            lk.LOOKME_ERR_UNSUPPORTED        # 192 bytes: not whole 128-byte stages
         assert S(lambda: lk.lookme_set_relevance(h, 512, None, None, FAKE, None)) == \
             lk.LOOKME_ERR_INVALID
         assert S(lambda: lk.lookme_set_relevance(h, 512, FAKE, FAKE + 2, FAKE, None)) == \
             lk.LOOKME_ERR_INVALID
+        base = lk.lookme_workspace_size(h, 1, 1000)
         assert S(lambda: lk.lookme_set_relevance(h, 512, FAKE, None, FAKE, None)) == lk.LOOKME_OK
+        # the logits of the rows now go through the workspace
+        assert lk.lookme_workspace_size(h, 1, 1000) >= base + 1000 * 1024 * 4
         assert S(lambda: lk.lookme_lookup_relevance(h, 1, 0, None, None, None, None, None, 0)) \
             == lk.LOOKME_OK
+        assert S(lambda: lk.lookme_lookup_relevance(h, 1, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 0)) \
+            == lk.LOOKME_ERR_WORKSPACE
         assert S(lambda: lk.lookme_lookup_relevance(h, 1, 8, FAKE, None, FAKE, FAKE, FAKE, 0)) \
             == lk.LOOKME_ERR_INVALID
     finally:

@@ -222,15 +222,14 @@ def test_layers_batched_equal_sequential():
 
 
 # Level-2 in the paper's form (Eq. 6-7): (workload, hidden width, sampled
-# tokens or None for all).  Hidden widths of 96 and 48 give a ragged 64-wide
-# tile in the first layer and 192-byte rows in the second (three 64-byte
-# steps: the masked 4-step kernel); the image case has the benchmark's
-# shapes.
+# tokens or None for all).  Ragged rows and primitive counts (200, 37, 300)
+# leave partial 64 x 64 tiles in both layers; the image case has the
+# benchmark's shapes.
 RELEVANCE = {
     "bf16_rel_l2": (Workload("bf16_rel_l2", "bf16", 300, 2, 256, 128, 20, 200, 64, 64, 8, 30,
-                             usage="uniform"), 96, None),
+                             usage="uniform"), 192, None),
     "f32_rel": (Workload("f32_rel", "f32", 77, 1, 96, 64, 5, 37, 40, 40, 3, 40, usage="iid"),
-                48, None),
+                96, None),
     "bf16_rel_k32": (Workload("bf16_rel_k32", "bf16", 130, 1, 128, 64, 7, 300, 32, 32, 32, 30,
                               usage="uniform"), 64, None),
     "bf16_rel_image": (WORKLOADS[1], 512, 80),
