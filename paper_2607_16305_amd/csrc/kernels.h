@@ -12,6 +12,11 @@ namespace lookme {
 // ---- projection: q[l, t, :] = round(x[t, :] . Wt[l]^T) --------------------
 hipError_t launch_project(int dt, const void* x, const void* wt, void* q, int64_t n, int d_in,
                           int d_e, int layers, hipStream_t st);
+// out[rows, N] = a w^T + bias (float32) on the projection's 256 x 256 tiles,
+// when the product has enough of them (at least 256 of 128 x 128) and K is
+// whole 128-byte stages; returns false (nothing launched) otherwise.
+bool launch_logits_gemm(int dt, const void* a, const void* w, const float* bias, float* out,
+                        int64_t rows, int N, int64_t kb, hipStream_t st);
 
 // ---- routing: scene[r] = argmax_s <q_r, K1[s]> + bias[s] over rows r -------
 // Three kernels, by batch size (route_plan):

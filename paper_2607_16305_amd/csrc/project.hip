@@ -218,10 +218,33 @@ __global__ __launch_bounds__(PJ_THREADS * KG) void project_kernel(
 // With NS >= 3 the fragments of stage s + 1 are read while the matrix cores
 // work on stage s; with NS = 2 the loads of stage s + 1 fly during stage s.
 // Needs K in whole KB-byte steps.
-template <int DT, int WM, int WN, int MI, int NJ, int KB, int NS>
+// EPI_F32_BIAS epilogue: C + bias[col] stored as float32 [M, N] (the relevance
+// MLP's logits), instead of the rounded, layer-scattered q.
+constexpr int EPI_Q = 0, EPI_F32_BIAS = 1;
+
+template <int MI, int NJ>
+__device__ __forceinline__ void store_f32_bias(const f32x4_t (&acc)[MI][NJ], float* __restrict__ C,
+                                               const float* __restrict__ bias, int64_t M, int N,
+                                               int64_t r0, int c0, int n16, int g) {
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int col = c0 + 16 * j + n16;
+    if (col >= N) continue;
+    const float b = bias != nullptr ? bias[col] : 0.f;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = r0 + 16 * i + 4 * g + r;
+        if (row < M) C[row * N + col] = acc[i][j][r] + b;
+      }
+  }
+}
+
+template <int DT, int WM, int WN, int MI, int NJ, int KB, int NS, int EPI = EPI_Q>
 __global__ __launch_bounds__(64 * WM * WN) void project_dtl_kernel(
     const char* __restrict__ A, const char* __restrict__ B, char* __restrict__ Q, int64_t M,
-    int N, int64_t k_bytes, int d_e, int tiles) {
+    int N, int64_t k_bytes, int d_e, int tiles, const float* __restrict__ bias) {
   using S = DtlShape<WM, WN, MI, NJ, KB>;
   static_assert(NS >= 2, "a stage in flight while one is used");
   __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
@@ -339,7 +362,10 @@ __global__ __launch_bounds__(64 * WM * WN) void project_dtl_kernel(
     if (s < nst) step(s, fa0, fb0, fa1, fb1);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
-  store_tile<DT, MI, NJ>(acc, Q, M, N, d_e, m0 + wm, n0 + wn, n16, g);
+  if constexpr (EPI == EPI_F32_BIAS)
+    store_f32_bias<MI, NJ>(acc, reinterpret_cast<float*>(Q), bias, M, N, m0 + wm, n0 + wn, n16, g);
+  else
+    store_tile<DT, MI, NJ>(acc, Q, M, N, d_e, m0 + wm, n0 + wn, n16, g);
 }
 
 // 16 waves in 4 x 4, each 64 x 64: 256 x 256 tiles, one workgroup per CU,
@@ -355,7 +381,7 @@ static void launch_dtl(const void* x, const void* wt, void* q, int64_t n, int N,
   hipLaunchKernelGGL((project_dtl_kernel<DT, WM, WN, MI, NJ, KB, NS>), dim3((unsigned)slots),
                      dim3(64 * WM * WN), 0, st, static_cast<const char*>(x),
                      static_cast<const char*>(wt), static_cast<char*>(q), n, N, kb, d_e,
-                     (int)tiles);
+                     (int)tiles, nullptr);
 }
 
 template <int DT, int BM, int BN, int D, int KG>
@@ -386,6 +412,28 @@ hipError_t launch_project(int dt, const void* x, const void* wt, void* q, int64_
   if (dt == DT_BF16) launch_tiles<DT_BF16, 32, 64, 4, 4>(x, wt, q, n, N, kb, d_e, st);
   else launch_tiles<DT_F32, 32, 64, 4, 4>(x, wt, q, n, N, kb, d_e, st);
   return hipGetLastError();
+}
+
+bool launch_logits_gemm(int dt, const void* a, const void* w, const float* bias, float* out,
+                        int64_t rows, int N, int64_t kb, hipStream_t st) {
+  const int64_t tiles128 = ((rows + 127) / 128) * ((N + 127) / 128);
+  if (tiles128 < 256 || kb % PD_KB != 0) return false;
+  using S = DtlShape<PD_WM, PD_WN, PD_MI, PD_NJ, PD_KB>;
+  const int64_t tiles = ((rows + S::BM - 1) / S::BM) * ((N + S::BN - 1) / S::BN);
+  const unsigned grid = (unsigned)((tiles + 7) / 8 * 8);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((project_dtl_kernel<DT_BF16, PD_WM, PD_WN, PD_MI, PD_NJ, PD_KB, PD_STAGES,
+                                           EPI_F32_BIAS>),
+                       dim3(grid), dim3(64 * PD_WM * PD_WN), 0, st, static_cast<const char*>(a),
+                       static_cast<const char*>(w), reinterpret_cast<char*>(out), rows, N, kb, N,
+                       (int)tiles, bias);
+  else
+    hipLaunchKernelGGL((project_dtl_kernel<DT_F32, PD_WM, PD_WN, PD_MI, PD_NJ, PD_KB, PD_STAGES,
+                                           EPI_F32_BIAS>),
+                       dim3(grid), dim3(64 * PD_WM * PD_WN), 0, st, static_cast<const char*>(a),
+                       static_cast<const char*>(w), reinterpret_cast<char*>(out), rows, N, kb, N,
+                       (int)tiles, bias);
+  return true;
 }
 
 }  // namespace lookme

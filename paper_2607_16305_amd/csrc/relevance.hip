@@ -8,7 +8,9 @@
 //                             operand-A row of token t being its query
 //                             followed by its scene's key (gathered per row,
 //                             K stages of 128 bytes straight into LDS);
-//   rel_gemm_kernel (logits)  r = a W2^T + b2 in float32, to the workspace;
+//   rel_gemm_kernel (logits)  r = a W2^T + b2 in float32, to the workspace
+//                             (large products: the projection's 256 x 256
+//                             tile kernel with a float32 + bias epilogue);
 //   relevance_topk_kernel     one wave per row: the k largest logits (lowest
 //                             p on ties), each lane keeping a sorted list of
 //                             its strided share, merged across the wave;
@@ -164,7 +166,10 @@ __global__ __launch_bounds__(256) void rel_gemm_kernel(RelGemmParams a) {
 // One wave per row of logits [rows, P]: lane l keeps a sorted list of the
 // KL largest of logits l, l + 64, ... (visited in increasing p, so a strict
 // '>' keeps the lower p first among equal values), then k rounds of a
-// butterfly arg max over the 64 lists give the row's top k in order.
+// butterfly arg max over the 64 lists give the row's top k in order.  A
+// value below T, the largest KL-th entry of the 64 lists (refreshed every
+// 4 values a lane), cannot reach the row's top KL and is skipped; values
+// equal to T are kept for the lower-index rule.
 template <int KL>
 __global__ __launch_bounds__(256) void relevance_topk_kernel(const float* __restrict__ logits,
                                                              int64_t rows, int P, int k,
@@ -178,20 +183,35 @@ __global__ __launch_bounds__(256) void relevance_topk_kernel(const float* __rest
   int li[KL];
 #pragma unroll
   for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
-  for (int p = lane; p < P; p += WAVE) {
-    const float x = r[p];
-    if (x > ls[KL - 1]) {
+  float T = -__builtin_inff();
+  for (int p0 = 0; p0 < P; p0 += 4 * WAVE) {
+    float x4[4];
 #pragma unroll
-      for (int e = KL - 1; e >= 1; --e) {
-        const bool above_prev = x > ls[e - 1];
-        const bool above_cur = x > ls[e];
-        const float s_keep = above_cur ? x : ls[e];
-        const int i_keep = above_cur ? p : li[e];
-        ls[e] = above_prev ? ls[e - 1] : s_keep;
-        li[e] = above_prev ? li[e - 1] : i_keep;
-      }
-      if (x > ls[0]) { ls[0] = x; li[0] = p; }
+    for (int u = 0; u < 4; ++u) {
+      const int p = p0 + u * WAVE + lane;
+      x4[u] = p < P ? r[p] : -__builtin_inff();
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float x = x4[u];
+      const int p = p0 + u * WAVE + lane;
+      if (x > ls[KL - 1] && x >= T) {
+#pragma unroll
+        for (int e = KL - 1; e >= 1; --e) {
+          const bool above_prev = x > ls[e - 1];
+          const bool above_cur = x > ls[e];
+          const float s_keep = above_cur ? x : ls[e];
+          const int i_keep = above_cur ? p : li[e];
+          ls[e] = above_prev ? ls[e - 1] : s_keep;
+          li[e] = above_prev ? li[e - 1] : i_keep;
+        }
+        if (x > ls[0]) { ls[0] = x; li[0] = p; }
+      }
+    }
+    float m = ls[KL - 1];
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+    T = m;
   }
   int head = 0;
   float hs = ls[0];
@@ -353,7 +373,11 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
   g2.cols = P;
   g2.ksplit = (int)(g2.k_bytes / RH_KB);
   g2.tiles = (int)(rt * ((P + RhShape::BN - 1) / RhShape::BN));
-  e = gemm(g2, EPI_LOGIT);
+  // large products on the projection's 256 x 256 tiles, small ones here
+  if (!launch_logits_gemm(dt, act, mlp.w2, mlp.b2, logits, rows, P, g2.k_bytes, st))
+    e = gemm(g2, EPI_LOGIT);
+  else
+    e = hipGetLastError();
   if (e != hipSuccess) return e;
   const dim3 wgrid((unsigned)((rows + 3) / 4));
   if (k <= 4)

@@ -223,8 +223,8 @@ def test_layers_batched_equal_sequential():
 
 # Level-2 in the paper's form (Eq. 6-7): (workload, hidden width, sampled
 # tokens or None for all).  Ragged rows and primitive counts (200, 37, 300)
-# leave partial 64 x 64 tiles in both layers; the image case has the
-# benchmark's shapes.
+# leave partial 64 x 64 tiles in both layers; the image and multi-scale
+# cases have the benchmarks' shapes.
 RELEVANCE = {
     "bf16_rel_l2": (Workload("bf16_rel_l2", "bf16", 300, 2, 256, 128, 20, 200, 64, 64, 8, 30,
                              usage="uniform"), 192, None),
@@ -233,6 +233,8 @@ RELEVANCE = {
     "bf16_rel_k32": (Workload("bf16_rel_k32", "bf16", 130, 1, 128, 64, 7, 300, 32, 32, 32, 30,
                               usage="uniform"), 64, None),
     "bf16_rel_image": (WORKLOADS[1], 512, 80),
+    # enough rows for the logits on the 256 x 256 projection tiles
+    "bf16_rel_multiscale": (WORKLOADS[2], 512, 80),
 }
 
 
