@@ -176,3 +176,18 @@ def relevance(q_rows, scene, scene_key_rows, w1_rows, b1, w2_rows, b2, prim_key_
         prims.append(chosen)
         ws.append([v / tot for v in ex])
     return a_rows, prims, ws
+
+
+def fusion_rows(r_rows, w_gate_rows, w_up_rows, w_down_rows, mant_bits):
+    """f of Eq. 10 by plain loops: exact rational products, silu in floating
+    point, one rounding of the inner activations (as a rational), then the
+    exact down product.  Returns rationals [m][d_h]."""
+    out = []
+    for r in r_rows:
+        u = []
+        for gw, uw in zip(w_gate_rows, w_up_rows):
+            g = float(dot(r, gw))
+            val = Fraction(g / (1.0 + math.exp(-g))) * dot(r, uw)
+            u.append(round_fraction(val, mant_bits))
+        out.append([dot(u, dw) for dw in w_down_rows])
+    return out

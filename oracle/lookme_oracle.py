@@ -26,6 +26,8 @@ What is computed, step by step (each function cites its passage):
   run         all of the above for L layers that share one table (Sec. 3.3,
               "Inter-Layer Sparse Activation": neighbouring layers retrieve
               similar primitives, so one table serves several layers)
+  fusion      Eq. 10 with the SwiGLU fusion f: the kept tokens receive
+              f(R) = W_down (silu(W_gate R) * (W_up R)) instead of R
   relevance_* Level-2 in the paper's own form (Eq. 6-7): a scene-shared
               two-layer MLP over [v_e, e_img[j]] gives relevance logits r_j;
               the top-k primitives by r are weighted by the softmax of
@@ -48,6 +50,9 @@ configured workloads; each is listed in the design notes of the repository):
     once to the storage dtype (the second layer runs on them as stored);
     e_img are the scene keys; the primitive rows whose cosine Eq. 7 takes are
     the primitive keys K2[j, p, :] (a zero vector has cosine 0).
+  * Fusion f (Eq. 10): a SwiGLU FFN d_v -> d_ff -> d_h per layer, silu(x) =
+    x / (1 + exp(-x)); R and the inner activations are rounded once to the
+    storage dtype (each is the input of a product, as stored), H + f(R) once.
 
 Inputs are numpy arrays.  bf16 tensors are passed as their raw uint16 bit
 patterns (numpy has no bf16) together with ``dtype="bf16"``; fp32 tensors as
@@ -363,3 +368,40 @@ def relevance_lookup(q: np.ndarray, scene: np.ndarray, a: np.ndarray, w2: np.nda
         r_top[t] = r[t, idx]
         w[t] = softmax_weights(z)
     return prim, w, r_top
+
+
+# ---------------------------------------------------------------------------
+# Sparse injection with the SwiGLU fusion (Eq. 10)
+# ---------------------------------------------------------------------------
+
+def silu(x: np.ndarray) -> np.ndarray:
+    """x * sigmoid(x)."""
+    return x / (1.0 + np.exp(-x))
+
+
+def fusion(r: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
+           dtype: str) -> np.ndarray:
+    """f in Eq. 10, a SwiGLU-style FFN from the retrieved width to the
+    backbone width: f(R) = W_down (silu(W_gate R) * (W_up R)).
+
+    r [m, d_v] (already rounded to dtype), w_gate and w_up [d_ff, d_v],
+    w_down [d_h, d_ff].  The inner activations are rounded once to dtype
+    before W_down.  Returns [m, d_h] float64 (not rounded)."""
+    u = round_to_dtype(silu(r @ w_gate.T) * (r @ w_up.T), dtype)
+    return u @ w_down.T
+
+
+def inject_fused(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarray,
+                 prim: np.ndarray, w: np.ndarray, kept: np.ndarray, w_gate: np.ndarray,
+                 w_up: np.ndarray, w_down: np.ndarray, dtype: str) -> np.ndarray:
+    """Sparse injection through the fusion (Eq. 10 and Eq. 2): for kept
+    tokens H[t, :] <- round(H[t, :] + f(round(R_img[t]))); every other row is
+    unchanged.  hidden [n, d_h], values [S*P, d_v]; returns float64."""
+    out = np.array(hidden, dtype=np.float64, copy=True)
+    kept = np.asarray(kept, dtype=np.int64)
+    if kept.size == 0:
+        return out
+    R = np.stack([retrieved(values, P, int(scene[t]), prim[t], w[t]) for t in kept])
+    F = fusion(round_to_dtype(R, dtype), w_gate, w_up, w_down, dtype)
+    out[kept] = round_to_dtype(hidden[kept] + F, dtype)
+    return out

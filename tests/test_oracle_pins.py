@@ -583,3 +583,70 @@ def test_relevance_invariants():
     prim3, w3, _ = O.relevance_lookup(q, scene, a, w2, b2, K2 * scale, k)
     assert prim3.tolist() == prim.tolist()
     np.testing.assert_allclose(w3, w, rtol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# Sparse injection through the SwiGLU fusion (Eq. 10)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_fusion_matches_brute_force(dtype):
+    """Catches a swapped gate/up pair, silu applied to the wrong factor, a
+    transposed W_down and a missing rounding of the inner activations."""
+    rng = np.random.default_rng(50)
+    m, d_v, d_ff, d_h = 4, 5, 6, 3
+    rnd = _bf16_values if dtype == "bf16" else (lambda r, sh, sc=1.0: r.standard_normal(sh) * sc)
+    R = rnd(rng, (m, d_v))
+    wg, wu, wd = rnd(rng, (d_ff, d_v), 0.7), rnd(rng, (d_ff, d_v), 0.7), rnd(rng, (d_h, d_ff), 0.7)
+    F = O.fusion(R, wg, wu, wd, dtype)
+    ref = B.fusion_rows(R.tolist(), wg.tolist(), wu.tolist(), wd.tolist(),
+                        8 if dtype == "bf16" else 24)
+    np.testing.assert_allclose(F, np.array([[float(v) for v in row] for row in ref]),
+                               rtol=1e-12, atol=1e-14)
+
+
+def test_fusion_closed_form():
+    """One inner unit: u = silu(a) * b, f = (2u, -u), with silu(a) =
+    a / (1 + e^-a) computed by hand."""
+    a, b = 1.5, -0.75
+    R = np.array([[a, b]])
+    F = O.fusion(R, np.array([[1.0, 0.0]]), np.array([[0.0, 1.0]]), np.array([[2.0], [-1.0]]),
+                 "f32")
+    u = float(np.float32(a / (1 + math.exp(-a)) * b))
+    np.testing.assert_allclose(F[0], [2 * u, -u], rtol=1e-15)
+    assert O.silu(np.array([0.0]))[0] == 0.0
+
+
+def test_inject_fused_touches_only_kept_rows_and_zero_up_is_identity():
+    """Rows outside the kept set keep their bits; W_up = 0 gives f = 0, so
+    the kept rows keep theirs too; a nonzero f changes exactly the kept
+    rows."""
+    rng = np.random.default_rng(51)
+    n, S, P, d_v, d_ff, d_h, k = 9, 2, 5, 4, 3, 6, 2
+    H = _bf16_values(rng, (n, d_h))
+    V = _bf16_values(rng, (S * P, d_v))
+    scene = rng.integers(0, S, n)
+    prim = np.stack([rng.permutation(P)[:k] for _ in range(n)])
+    w = np.full((n, k), 0.5)
+    kept = np.array([1, 4, 7])
+    wg = _bf16_values(rng, (d_ff, d_v))
+    wd = _bf16_values(rng, (d_h, d_ff))
+    out0 = O.inject_fused(H, V, P, scene, prim, w, kept, wg, np.zeros((d_ff, d_v)), wd, "bf16")
+    assert np.array_equal(out0, H)
+    wu = _bf16_values(rng, (d_ff, d_v))
+    out = O.inject_fused(H, V, P, scene, prim, w, kept, wg, wu, wd, "bf16")
+    others = np.setdiff1d(np.arange(n), kept)
+    assert np.array_equal(out[others], H[others])
+    assert not np.array_equal(out[kept], H[kept])
+
+
+def test_fusion_inner_unit_relabelling_invariance():
+    """Permuting the inner units (rows of W_gate and W_up, columns of W_down
+    alike) leaves f unchanged: catches gate/up rows and down columns indexed
+    differently."""
+    rng = np.random.default_rng(52)
+    R = rng.standard_normal((3, 7))
+    wg, wu, wd = rng.standard_normal((5, 7)), rng.standard_normal((5, 7)), rng.standard_normal((4, 5))
+    perm = rng.permutation(5)
+    np.testing.assert_allclose(O.fusion(R, wg[perm], wu[perm], wd[:, perm], "f32"),
+                               O.fusion(R, wg, wu, wd, "f32"), rtol=1e-12)
