@@ -215,6 +215,35 @@ lookme_status_t lookme_lookup_relevance(lookme_t h, int32_t layers, int64_t n, c
                                         float* w_out, void* stream);
 
 /*
+ * lookme_set_fusion -- registers the SwiGLU fusion f of Eq. 10, one per
+ * layer (borrowed, like the table):
+ *   w_gate, w_up [layers, d_ff, value_dim] dtype
+ *   w_down       [layers, d_h, d_ff] dtype
+ *   f_l(R) = w_down[l] (silu(w_gate[l] R) * (w_up[l] R)), silu(x) = x / (1 + e^-x)
+ * Needs d_ff * elem_size and value_dim * elem_size multiples of 128 bytes.
+ * From then on lookme_workspace_size includes the fusion's buffers (R and
+ * the inner activations of up to layers * n rows).
+ */
+lookme_status_t lookme_set_fusion(lookme_t h, int32_t layers, int32_t d_ff, int32_t d_h,
+                                  const void* w_gate, const void* w_up, const void* w_down);
+
+/*
+ * lookme_inject_fused -- sparse injection through the fusion (Eq. 10, Eq. 2)
+ * for a kept set (lookme_select): for every layer l and kept token t,
+ *   R = round(sum_i w[t,i] values[scene[t]*N_p + prim[t,i], :])   (value_dim)
+ *   U = round(silu(w_gate[l] R) * (w_up[l] R))                     (d_ff)
+ *   hidden[l, t, :] <- round(hidden[l, t, :] + w_down[l] U)        (d_h)
+ * float32 accumulation throughout; every other row keeps its bits.  kept ids
+ * outside [0, n) are clamped into it, and an id listed twice in a layer
+ * races on its row.  d_h must be the fusion's.  Needs the workspace of
+ * lookme_workspace_size (queried after lookme_set_fusion).
+ */
+lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                                    const int32_t* kept, const int32_t* scene,
+                                    const int32_t* prim, const float* w, void* hidden,
+                                    int32_t d_h, void* stream);
+
+/*
  * Measurement support (not part of the method).  When enabled, each kernel
  * group that route/lookup/inject launches is bracketed by a pair of HIP timing
  * events recorded on the call's stream.  lookme_profile_read waits for the

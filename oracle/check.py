@@ -283,6 +283,44 @@ def check_relevance_prim(act: np.ndarray, w2: np.ndarray, b2: np.ndarray, q: np.
     return w_orc
 
 
+def check_fused_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: int,
+                       scene: np.ndarray, prim: np.ndarray, w_lib: np.ndarray, kept: np.ndarray,
+                       w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray, rep: Report,
+                       tokens, contract_abs: float = 2e-2):
+    """C6 through the SwiGLU fusion (Eq. 10), on the library's kept set,
+    primitives and weights: rows outside the kept set keep their bits; kept
+    rows must equal round(H + f(round(R))) within the contract (bf16:
+    ``contract_abs`` max-abs; float32: 1e-4 * (|H| + |W_down| |U|), the
+    float32 products of d_v and d_ff terms staying far inside it).  h_in and
+    h_out_lib hold the rows of ``tokens``."""
+    kept_set = set(np.asarray(kept).tolist())
+    h_in_f = O.to_f64(h_in, dtype)
+    h_lib_f = O.to_f64(h_out_lib, dtype)
+    for r, t in enumerate(np.asarray(tokens)):
+        rep.count("hidden_row")
+        if int(t) not in kept_set:
+            if not np.array_equal(np.asarray(h_in[r]).view(np.uint8),
+                                  np.asarray(h_out_lib[r]).view(np.uint8)):
+                rep.fail(f"hidden: untouched row {t} modified")
+            continue
+        rows = int(scene[t]) * P + np.asarray(prim[t], dtype=np.int64)
+        V = values_rows(rows)
+        R = O.round_to_dtype(np.sum(np.asarray(w_lib[t], dtype=np.float64)[:, None] * V, axis=0),
+                             dtype)
+        U = O.round_to_dtype(O.silu(w_gate @ R) * (w_up @ R), dtype)
+        F = w_down @ U
+        exp = O.round_to_dtype(h_in_f[r] + F, dtype)
+        err = np.abs(h_lib_f[r] - exp)
+        if dtype == "bf16":
+            bad = err > contract_abs
+        else:
+            bad = err > 1e-4 * (np.abs(h_in_f[r]) + np.abs(w_down) @ np.abs(U))
+        if np.any(bad):
+            j = int(np.argmax(err))
+            rep.fail(f"hidden[{t}, {j}]: library {h_lib_f[r, j]!r}, expected {exp[j]!r}")
+        rep.notes["fused_max_abs"] = max(rep.notes.get("fused_max_abs", 0.0), float(err.max()))
+
+
 def check_kept(c: np.ndarray, n_keep: int, kept_lib: np.ndarray, rep: Report):
     """C5: the kept set equals the oracle's except for swaps among
     criticalities tied with the n_keep-th; ascending, unique, in range."""

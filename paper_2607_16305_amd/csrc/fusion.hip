@@ -1,0 +1,71 @@
+// Sparse injection through the SwiGLU fusion of Eq. 10 (arXiv 2607.16305,
+// Sec. 3.3): for the kept tokens of layer l, H <- round(H + f_l(R)) with
+// f_l(R) = W_down (silu(W_gate R) * (W_up R)).  R (the weighted row sums,
+// rounded) comes from launch_gather_rows; two products on the matrix cores
+// (tile_gemm.h), batched over the layers (blockIdx.y):
+//
+//   gate/up   U = round(silu(R W_gate^T) * (R W_up^T)): every tile computes
+//             32 columns of both products for the same rows and combines
+//             them in its epilogue;
+//   down      H[kept] = round(H[kept] + U W_down^T), written in place (the
+//             kept list of the layer maps a product row to its token).
+#include "common.h"
+#include "kernels.h"
+#include "tile_gemm.h"
+
+namespace lookme {
+
+hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int64_t n_keep,
+                         const int32_t* kept, int d_v, const void* r, void* u, void* hidden,
+                         hipStream_t st) {
+  if (n == 0 || n_keep == 0) return hipSuccess;
+  const int es = dt == DT_BF16 ? 2 : 4;
+  const int64_t rt = (n_keep + TgShape::BM - 1) / TgShape::BM;
+
+  TileGemmParams g1{};
+  g1.a0 = static_cast<const char*>(r);
+  g1.b = static_cast<const char*>(f.w_gate);
+  g1.b2 = static_cast<const char*>(f.w_up);
+  g1.out = static_cast<char*>(u);
+  g1.rows = n_keep;
+  g1.a_bytes = (int64_t)d_v * es;
+  g1.k_bytes = g1.a_bytes;
+  g1.a_batch = n_keep * g1.a_bytes;
+  g1.b_batch = (int64_t)f.d_ff * g1.k_bytes;
+  g1.out_batch = n_keep * (int64_t)f.d_ff * es;
+  g1.cols = f.d_ff;
+  g1.ksplit = (int)(g1.k_bytes / TG_KB);
+  g1.tiles = (int)(rt * ((f.d_ff + TgShape::BN / 2 - 1) / (TgShape::BN / 2)));
+  const dim3 grid1((unsigned)((g1.tiles + 7) / 8 * 8), (unsigned)layers);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_SWIGLU>), grid1, dim3(256), 0, st, g1);
+  else
+    hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_SWIGLU>), grid1, dim3(256), 0, st, g1);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  TileGemmParams g2{};
+  g2.a0 = static_cast<const char*>(u);
+  g2.b = static_cast<const char*>(f.w_down);
+  g2.out = static_cast<char*>(hidden);
+  g2.kept = kept;
+  g2.rows = n_keep;
+  g2.a_bytes = (int64_t)f.d_ff * es;
+  g2.k_bytes = g2.a_bytes;
+  g2.a_batch = n_keep * g2.a_bytes;
+  g2.b_batch = (int64_t)f.d_h * g2.k_bytes;
+  g2.n = n;
+  g2.n_keep = n_keep;
+  g2.out_ld = (int64_t)f.d_h * es;
+  g2.cols = f.d_h;
+  g2.ksplit = (int)(g2.k_bytes / TG_KB);
+  g2.tiles = (int)(rt * ((f.d_h + TgShape::BN - 1) / TgShape::BN));
+  const dim3 grid2((unsigned)((g2.tiles + 7) / 8 * 8), (unsigned)layers);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_RESID>), grid2, dim3(256), 0, st, g2);
+  else
+    hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_RESID>), grid2, dim3(256), 0, st, g2);
+  return hipGetLastError();
+}
+
+}  // namespace lookme

@@ -173,7 +173,10 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
   }
 }
 
-template <int DT, int K>
+// TO_R: the weighted row sum R of kept row j is rounded to the storage
+// dtype and written to row j of `hidden` (the fusion's input, [rows, d_v])
+// instead of being added into H.
+template <int DT, int K, bool TO_R = false>
 __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
     int64_t n, int64_t n_keep, const int32_t* __restrict__ kept_all,
     const int32_t* __restrict__ scene_all, const int32_t* __restrict__ prim_all,
@@ -200,14 +203,14 @@ __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
       wt[i] = 0.f;
     }
   }
-  char* h = hidden + row * h_bytes;
+  char* h = TO_R ? hidden + j * v_bytes : hidden + row * h_bytes;
   const int chunks = (int)(v_bytes / 16);
   for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
     u32x4_t vv[K];
 #pragma unroll
     for (int i = 0; i < K; ++i)
       if (i < k) vv[i] = ld16_nt(values + vrow[i] * v_bytes + (int64_t)c * 16);
-    const u32x4_t hv = ld16(h + (int64_t)c * 16);
+    const u32x4_t hv = TO_R ? u32x4_t{0, 0, 0, 0} : ld16(h + (int64_t)c * 16);
     u32x4_t out;
     if constexpr (DT == DT_BF16) {
       float acc[8];
@@ -244,7 +247,7 @@ __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
   }
 }
 
-template <int DT>
+template <int DT, bool TO_R = false>
 static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_t n_keep,
                             const int32_t* kept, const int32_t* scene, const int32_t* prim,
                             const float* w, const char* values, int S, int P, int64_t vb,
@@ -254,7 +257,7 @@ static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_
   const int ch = (int)(vb / 16);
   const int bs = ch >= INJ_THREADS ? INJ_THREADS : (ch + 63) / 64 * 64;
 #define LOOKME_INJ(K_)                                                                \
-  hipLaunchKernelGGL((inject_kernel<DT, K_>), grid, dim3(bs), 0, st, n, n_keep, kept, \
+  hipLaunchKernelGGL((inject_kernel<DT, K_, TO_R>), grid, dim3(bs), 0, st, n, n_keep, kept, \
                      scene, prim, w, values, S, P, kk, vb, hidden, hb)
   if (kk <= 4) LOOKME_INJ(4);
   else if (kk <= 8) LOOKME_INJ(8);
@@ -307,6 +310,24 @@ hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, con
     launch_inject_k<DT_F32>(k, grid, st, n, n_keep, kept, scene, prim, w,
                             static_cast<const char*>(values), S, P, (int64_t)d_v * es,
                             static_cast<char*>(hidden), (int64_t)d_h * es);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
+                              const int32_t* scene, const int32_t* prim, const float* w,
+                              const void* values, int S, int P, int d_v, int k, void* r_out,
+                              hipStream_t st) {
+  if (n == 0 || n_keep == 0) return hipSuccess;
+  const int es = dt == DT_BF16 ? 2 : 4;
+  const dim3 grid((unsigned)(layers * n_keep));
+  if (dt == DT_BF16)
+    launch_inject_k<DT_BF16, true>(k, grid, st, n, n_keep, kept, scene, prim, w,
+                                   static_cast<const char*>(values), S, P, (int64_t)d_v * es,
+                                   static_cast<char*>(r_out), 0);
+  else
+    launch_inject_k<DT_F32, true>(k, grid, st, n, n_keep, kept, scene, prim, w,
+                                  static_cast<const char*>(values), S, P, (int64_t)d_v * es,
+                                  static_cast<char*>(r_out), 0);
   return hipGetLastError();
 }
 

@@ -110,6 +110,25 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
                             int S, int P, int k, void* act, int32_t* prim, float* w,
                             float* logits, hipStream_t st);
 
+// ---- sparse injection through the SwiGLU fusion (Eq. 10) ----------------
+// Per layer l (tensors borrowed): w_gate, w_up [layers, d_ff, d_v] and
+// w_down [layers, d_h, d_ff] in the table's dtype.  launch_gather_rows
+// writes R [layers * n_keep, d_v] (rounded); launch_fusion then writes
+// U [layers * n_keep, d_ff] and adds W_down U into the kept rows of H.
+struct FusionFfn {
+  int layers, d_ff, d_h;
+  const void* w_gate;
+  const void* w_up;
+  const void* w_down;
+};
+hipError_t launch_gather_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
+                              const int32_t* scene, const int32_t* prim, const float* w,
+                              const void* values, int S, int P, int d_v, int k, void* r_out,
+                              hipStream_t st);
+hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int64_t n_keep,
+                         const int32_t* kept, int d_v, const void* r, void* u, void* hidden,
+                         hipStream_t st);
+
 // ---- Level-2 scoring of bucketed rows, fused top-k + softmax --------------
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st);

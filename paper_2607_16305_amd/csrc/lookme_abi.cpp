@@ -35,6 +35,7 @@ struct lookme_s {
   int64_t prof_count[LOOKME_GROUP_COUNT];
   double prof_ms[LOOKME_GROUP_COUNT];
   lookme::RelevanceMlp rel;                // hidden == 0: none registered
+  lookme::FusionFfn fus;                   // d_ff == 0: none registered
 };
 
 namespace {
@@ -66,7 +67,7 @@ constexpr int32_t MAX_SCENES = 16384;   // bucketing keeps one histogram per chu
 // Workspace layout for `layers` x `n` rows.
 struct Layout {
   size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, route_count,
-      route_part, crit_key, kept, rel_logits, total;
+      route_part, crit_key, kept, rel_logits, fus_r, fus_u, total;
 };
 
 // The leading bytes of the workspace hold counters that start at zero; they
@@ -74,7 +75,8 @@ struct Layout {
 // them at zero.
 constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_COUNTERS * 4;
 
-Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance) {
+Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance,
+              int32_t fusion_dff) {
   const int64_t rows = (int64_t)layers * n;
   const int64_t chunks = lookme::bucket_chunks(rows);
   const int64_t units = lookme::bucket_max_units(rows, d.num_scenes);
@@ -100,6 +102,10 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance)
   L.kept = take((size_t)rows * 4);
   // relevance logits [rows, P] float32, when an MLP is registered
   L.rel_logits = take(relevance ? (size_t)rows * d.prims_per_scene * 4 : 0);
+  // the fusion's R and inner activations of the kept rows (at most all rows)
+  const size_t es = (size_t)elem_size(d.dtype);
+  L.fus_r = take(fusion_dff > 0 ? (size_t)rows * d.value_dim * es : 0);
+  L.fus_u = take(fusion_dff > 0 ? (size_t)rows * fusion_dff * es : 0);
   L.total = off;
   return L;
 }
@@ -125,7 +131,7 @@ lookme_status_t check_layers_n(int32_t layers, int64_t n) {
 }
 
 lookme_status_t check_workspace(lookme_t h, int32_t layers, int64_t n, Layout* L) {
-  *L = layout(h->d, layers, n, h->rel.hidden > 0);
+  *L = layout(h->d, layers, n, h->rel.hidden > 0, h->fus.d_ff);
   if (h->ws == nullptr) return fail(LOOKME_ERR_WORKSPACE, "no workspace set");
   if (h->ws_bytes < L->total)
     return fail(LOOKME_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed for %d x %lld rows",
@@ -324,7 +330,7 @@ lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_toke
   LOOKME_TRY(check_handle(h));
   if (bytes == nullptr) return fail(LOOKME_ERR_INVALID, "bytes is NULL");
   LOOKME_TRY(check_layers_n(layers, n_tokens));
-  *bytes = layout(h->d, layers, n_tokens, h->rel.hidden > 0).total;
+  *bytes = layout(h->d, layers, n_tokens, h->rel.hidden > 0, h->fus.d_ff).total;
   return LOOKME_OK;
 }
 
@@ -528,6 +534,56 @@ lookme_status_t lookme_lookup_relevance(lookme_t h, int32_t layers, int64_t n, c
                                reinterpret_cast<float*>(static_cast<char*>(h->ws) + L.rel_logits),
                                st),
       "relevance lookup launch");
+}
+
+lookme_status_t lookme_set_fusion(lookme_t h, int32_t layers, int32_t d_ff, int32_t d_h,
+                                  const void* w_gate, const void* w_up, const void* w_down) {
+  LOOKME_TRY(check_handle(h));
+  const int es = elem_size(h->d.dtype);
+  if (layers < 1 || d_ff < 1 || d_h < 1)
+    return fail(LOOKME_ERR_INVALID, "layers, d_ff and d_h must be positive");
+  if (((int64_t)d_ff * es) % 128 != 0 || ((int64_t)h->d.value_dim * es) % 128 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED,
+                "d_ff * elem_size and value_dim * elem_size must be multiples of 128 bytes");
+  LOOKME_TRY(check_ptr(w_gate, "w_gate"));
+  LOOKME_TRY(check_ptr(w_up, "w_up"));
+  LOOKME_TRY(check_ptr(w_down, "w_down"));
+  h->fus = lookme::FusionFfn{layers, d_ff, d_h, w_gate, w_up, w_down};
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                                    const int32_t* kept, const int32_t* scene,
+                                    const int32_t* prim, const float* w, void* hidden,
+                                    int32_t d_h, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_keep(n, n_keep));
+  if (h->fus.d_ff < 1)
+    return fail(LOOKME_ERR_INVALID, "no fusion registered (lookme_set_fusion)");
+  if (layers > h->fus.layers)
+    return fail(LOOKME_ERR_INVALID, "%d layers, the fusion has %d", layers, h->fus.layers);
+  if (d_h != h->fus.d_h)
+    return fail(LOOKME_ERR_INVALID, "d_h %d, the fusion writes %d", d_h, h->fus.d_h);
+  if (n == 0 || n_keep == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(kept, "kept"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(prim, "prim"));
+  LOOKME_TRY(check_ptr(w, "w"));
+  LOOKME_TRY(check_ptr(hidden, "hidden"));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(h->ws);
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  LOOKME_TRY(hip_status(lookme::launch_gather_rows(d.dtype, layers, n, n_keep, kept, scene, prim,
+                                                   w, h->values, d.num_scenes, d.prims_per_scene,
+                                                   d.value_dim, d.top_k, ws + L.fus_r, st),
+                        "fusion gather launch"));
+  return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n_keep, kept, d.value_dim,
+                                          ws + L.fus_r, ws + L.fus_u, hidden, st),
+                    "fusion launch");
 }
 
 }  // extern "C"

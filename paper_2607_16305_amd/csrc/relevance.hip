@@ -3,12 +3,12 @@
 // per primitive, the top k primitives by logit are kept, and their weights
 // are the softmax of cos(v_e, e_{j,p}) + tanh(r_j[p]).  Four launches:
 //
-//   rel_gemm_kernel (hidden)  a = round(ReLU([q_t, K1[scene_t]] W1^T + b1)):
+//   tile_gemm_kernel (hidden)  a = round(ReLU([q_t, K1[scene_t]] W1^T + b1)):
 //                             64 x 64 output tiles on the matrix cores, the
 //                             operand-A row of token t being its query
 //                             followed by its scene's key (gathered per row,
 //                             K stages of 128 bytes straight into LDS);
-//   rel_gemm_kernel (logits)  r = a W2^T + b2 in float32, to the workspace
+//   tile_gemm_kernel (logits)  r = a W2^T + b2 in float32, to the workspace
 //                             (large products: the projection's 256 x 256
 //                             tile kernel with a float32 + bias epilogue);
 //   relevance_topk_kernel     one wave per row: the k largest logits (lowest
@@ -18,150 +18,10 @@
 //                             chosen primitive keys, + tanh of the logits,
 //                             softmax over the k.
 #include "common.h"
-#include "dtl.h"
 #include "kernels.h"
+#include "tile_gemm.h"
 
 namespace lookme {
-
-// 4 waves in 2 x 2, each 32 x 32 (2 x 2 MFMA tiles): 64 x 64 tiles, 128-byte
-// K stages, two of them
-using RhShape = DtlShape<2, 2, 2, 2, 128>;
-constexpr int RH_KB = 128;
-
-struct RelGemmParams {
-  const char* a0;           // operand-A rows: stages [0, ksplit) from a0 + row * a_bytes
-  const char* a1;           // stages [ksplit, nst) from a1 + sel(row) * a_bytes, or null
-  const int32_t* sel;       // [rows] row of a1 for each A row (clamped to [0, sel_rows))
-  const char* b;            // [cols, K] operand-B rows
-  const float* bias;        // [cols] or null
-  char* out;                // [rows, cols]: dtype (EPI_ACT) or float32 (EPI_LOGIT)
-  int64_t rows;
-  int64_t a_bytes;          // bytes of an A row half (a0 and a1 rows)
-  int64_t k_bytes;          // K in bytes, a multiple of 128
-  int sel_rows, cols, ksplit, tiles;
-};
-
-enum : int { EPI_ACT = 0, EPI_LOGIT = 1 };
-
-template <int DT, int EPI>
-__global__ __launch_bounds__(256) void rel_gemm_kernel(RelGemmParams a) {
-  using S = RhShape;
-  constexpr int MI = 2, NJ = 2, KB = RH_KB, KSL = KB / 64, WN = 2;
-  constexpr int ES = DT == DT_BF16 ? 2 : 4;
-  __shared__ __attribute__((aligned(1024))) char lds[2][S::STAGE];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n16 = lane & 15, g = lane >> 4;
-  const int wm = (wv / WN) * 16 * MI, wn = (wv % WN) * 16 * NJ;
-
-  const int tiles_n = (a.cols + S::BN - 1) / S::BN;
-  const int tile = xcd_remap(blockIdx.x, a.tiles);
-  if (tile < 0) return;
-  const int64_t m0 = (int64_t)(tile / tiles_n) * S::BM;
-  const int n0 = (tile % tiles_n) * S::BN;
-  const int nst = (int)(a.k_bytes / KB);
-
-  // load b covers tile row trow (A rows first, then B rows); an A row takes
-  // its first ksplit stages from p0 and the rest from p1 (the hidden layer:
-  // the token's query, then its scene's key); a B row is contiguous.  Rows
-  // past the edge are clamped (their outputs are not stored).
-  const char* p0[S::PER_WAVE];
-  const char* p1[S::PER_WAVE];
-  int split[S::PER_WAVE];
-#pragma unroll
-  for (int b = 0; b < S::PER_WAVE; ++b) {
-    const int trow = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
-    const int chunk = (lane % S::LPR) ^ blk_swz<KB>(trow & 15);
-    if (trow < S::BM) {
-      int64_t r = m0 + trow;
-      r = r < a.rows ? r : a.rows - 1;
-      p0[b] = a.a0 + r * a.a_bytes + chunk * 16;
-      if (a.a1 != nullptr) {
-        int s = a.sel[r];
-        s = s < 0 ? 0 : (s >= a.sel_rows ? a.sel_rows - 1 : s);
-        p1[b] = a.a1 + (int64_t)s * a.a_bytes + chunk * 16;
-      } else {
-        p1[b] = p0[b] + (int64_t)a.ksplit * KB;
-      }
-      split[b] = a.ksplit;
-    } else {
-      int r = n0 + trow - S::BM;
-      r = r < a.cols ? r : a.cols - 1;
-      p0[b] = a.b + (int64_t)r * a.k_bytes + chunk * 16;
-      p1[b] = p0[b];
-      split[b] = nst;
-    }
-  }
-  auto issue = [&](int stage) {
-    const int s = stage < nst ? stage : nst - 1;   // past the end: a harmless reload
-    char* dst = lds[stage & 1];
-#pragma unroll
-    for (int b = 0; b < S::PER_WAVE; ++b) {
-      const char* src =
-          s < split[b] ? p0[b] + (int64_t)s * KB : p1[b] + (int64_t)(s - split[b]) * KB;
-      load_lds16(src, dst + (wv * S::PER_WAVE + b) * 1024);
-    }
-  };
-
-  f32x4_t acc[MI][NJ];
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  issue(0);
-  for (int s = 0; s < nst; ++s) {
-    // stage s has landed everywhere and every read of stage s - 1 (the other
-    // buffer) has ended: load stage s + 1 there, multiply stage s (a plain
-    // s_barrier: the fence of __syncthreads would wait for every load)
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    issue(s + 1);
-    const char* buf = lds[s & 1];
-#pragma unroll
-    for (int ks = 0; ks < KSL; ++ks) {
-      u32x4_t fa[MI], fb[NJ];
-#pragma unroll
-      for (int i = 0; i < MI; ++i) fa[i] = read_frag<KB>(buf, wm + 16 * i, ks, n16, g);
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_chunk<DT>(fa[i], fb[j], acc[i][j]);
-    }
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
-
-  // the lane holds rows m0 + wm + 16 i + 4 g + r and column n0 + wn + 16 j +
-  // n16: + bias, then ReLU and one rounding to dtype (hidden layer) or a
-  // float32 store (logits)
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const int col = n0 + wn + 16 * j + n16;
-    if (col >= a.cols) continue;
-    const float bias = a.bias != nullptr ? a.bias[col] : 0.f;
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t row = m0 + wm + 16 * i + 4 * g + r;
-        if (row >= a.rows) continue;
-        const float z = acc[i][j][r] + bias;
-        if constexpr (EPI == EPI_LOGIT) {
-          reinterpret_cast<float*>(a.out)[row * a.cols + col] = z;
-        } else {
-          char* dst = a.out + (row * a.cols + col) * ES;
-          if constexpr (DT == DT_BF16)
-            *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16_rne(fmaxf(z, 0.f));
-          else
-            *reinterpret_cast<float*>(dst) = fmaxf(z, 0.f);
-        }
-      }
-  }
-}
 
 // One wave per row of logits [rows, P]: lane l keeps a sorted list of the
 // KL largest of logits l, l + 64, ... (visited in increasing p, so a strict
@@ -328,24 +188,24 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
                             float* logits, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
-  auto gemm = [&](const RelGemmParams& gp, int epi) {
+  auto gemm = [&](const TileGemmParams& gp, int epi) {
     const unsigned grid = (unsigned)((gp.tiles + 7) / 8 * 8);
     if (dt == DT_BF16) {
       if (epi == EPI_ACT)
-        hipLaunchKernelGGL((rel_gemm_kernel<DT_BF16, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
+        hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
       else
-        hipLaunchKernelGGL((rel_gemm_kernel<DT_BF16, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
+        hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
     } else {
       if (epi == EPI_ACT)
-        hipLaunchKernelGGL((rel_gemm_kernel<DT_F32, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
+        hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
       else
-        hipLaunchKernelGGL((rel_gemm_kernel<DT_F32, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
+        hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
     }
     return hipGetLastError();
   };
-  const int64_t rt = (rows + RhShape::BM - 1) / RhShape::BM;
+  const int64_t rt = (rows + TgShape::BM - 1) / TgShape::BM;
   // hidden layer: K = [query ; scene key]
-  RelGemmParams g1{};
+  TileGemmParams g1{};
   g1.a0 = static_cast<const char*>(q);
   g1.a1 = static_cast<const char*>(scene_keys);
   g1.sel = scene;
@@ -357,12 +217,12 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
   g1.k_bytes = 2 * g1.a_bytes;
   g1.sel_rows = S;
   g1.cols = mlp.hidden;
-  g1.ksplit = (int)(g1.a_bytes / RH_KB);
-  g1.tiles = (int)(rt * ((mlp.hidden + RhShape::BN - 1) / RhShape::BN));
+  g1.ksplit = (int)(g1.a_bytes / TG_KB);
+  g1.tiles = (int)(rt * ((mlp.hidden + TgShape::BN - 1) / TgShape::BN));
   hipError_t e = gemm(g1, EPI_ACT);
   if (e != hipSuccess) return e;
   // logits: r = a W2^T + b2, float32
-  RelGemmParams g2{};
+  TileGemmParams g2{};
   g2.a0 = static_cast<const char*>(act);
   g2.b = static_cast<const char*>(mlp.w2);
   g2.bias = mlp.b2;
@@ -371,8 +231,8 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
   g2.a_bytes = (int64_t)mlp.hidden * es;
   g2.k_bytes = g2.a_bytes;
   g2.cols = P;
-  g2.ksplit = (int)(g2.k_bytes / RH_KB);
-  g2.tiles = (int)(rt * ((P + RhShape::BN - 1) / RhShape::BN));
+  g2.ksplit = (int)(g2.k_bytes / TG_KB);
+  g2.tiles = (int)(rt * ((P + TgShape::BN - 1) / TgShape::BN));
   // large products on the projection's 256 x 256 tiles, small ones here
   if (!launch_logits_gemm(dt, act, mlp.w2, mlp.b2, logits, rows, P, g2.k_bytes, st))
     e = gemm(g2, EPI_LOGIT);

@@ -27,7 +27,8 @@ STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "HIP
 
 EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "lookme_route",
             "lookme_lookup", "lookme_inject", "lookme_select", "lookme_inject_kept",
-            "lookme_set_relevance", "lookme_lookup_relevance",
+            "lookme_set_relevance", "lookme_lookup_relevance", "lookme_set_fusion",
+            "lookme_inject_fused",
             "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
@@ -77,6 +78,10 @@ def load():
         "lookme_set_relevance": [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp],
         "lookme_lookup_relevance": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
                                     _vp],
+        "lookme_set_fusion": [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp,
+                              _vp],
+        "lookme_inject_fused": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp, _vp,
+                                _vp, _vp, _vp, ctypes.c_int32, _vp],
         "lookme_destroy": [_vp],
         "lookme_profile_enable": [_vp, ctypes.c_int32],
         "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
@@ -169,6 +174,16 @@ def lookme_lookup_relevance(h, layers, n, q, scene, act_out, prim_out, w_out, st
                                           _ptr(prim_out), _ptr(w_out), _stream(stream)))
 
 
+def lookme_set_fusion(h, layers, d_ff, d_h, w_gate, w_up, w_down):
+    _check(load().lookme_set_fusion(h, layers, d_ff, d_h, _ptr(w_gate), _ptr(w_up),
+                                    _ptr(w_down)))
+
+
+def lookme_inject_fused(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h, stream=None):
+    _check(load().lookme_inject_fused(h, layers, n, n_keep, _ptr(kept), _ptr(scene), _ptr(prim),
+                                      _ptr(w), _ptr(hidden), d_h, _stream(stream)))
+
+
 def lookme_destroy(h):
     if h:
         _check(load().lookme_destroy(h))
@@ -247,6 +262,17 @@ class Table:
         self.reserve(layers, n)
         lookme_lookup_relevance(self.handle, layers, n, q, scene, act_out, prim_out, w_out,
                                 stream)
+
+    def set_fusion(self, w_gate, w_up, w_down):
+        self.fusion = (w_gate, w_up, w_down)     # keep alive
+        L, d_ff, _ = w_gate.shape
+        lookme_set_fusion(self.handle, L, d_ff, w_down.shape[1], w_gate, w_up, w_down)
+
+    def inject_fused(self, kept, scene, prim, w, hidden, n_keep, layers=1, stream=None):
+        n = scene.numel() // layers
+        self.reserve(layers, n)
+        lookme_inject_fused(self.handle, layers, n, n_keep, kept, scene, prim, w, hidden,
+                            hidden.shape[-1], stream)
 
     def close(self):
         if self.handle:

@@ -38,6 +38,7 @@ CHUNK = 1 << 26
 TID_X, TID_K1, TID_K2, TID_V, TID_LABELS, TID_CENT, TID_PERM = 1, 2, 3, 4, 5, 6, 7
 TID_W, TID_DELTA, TID_H = 10, 20, 30
 TID_MLP_W1, TID_MLP_B1, TID_MLP_W2, TID_MLP_B2 = 40, 41, 42, 43
+TID_FUS_GATE, TID_FUS_UP, TID_FUS_DOWN = 50, 60, 70
 
 
 @dataclasses.dataclass(frozen=True)
@@ -233,3 +234,21 @@ def make_relevance(wl: Workload, seed: int, hidden: int, device="cpu") -> dict:
     w2 = _randn_rows(wl.prims, hidden, base + TID_MLP_W2, dev, math.sqrt(2.0 / hidden), dt)
     b2 = _randn_rows(1, wl.prims, base + TID_MLP_B2, dev, 0.1, torch.float32)[0]
     return dict(w1=w1, b1=b1.contiguous(), w2=w2, b2=b2.contiguous(), hidden=hidden)
+
+
+def make_fusion(wl: Workload, seed: int, d_ff: int, device="cpu") -> dict:
+    """Seeded SwiGLU fusion weights per layer (Eq. 10; the paper trains
+    them): W_gate, W_up [L, d_ff, d_v] ~ N(0, 1/d_v) and W_down [L, d_h, d_ff]
+    ~ N(0, 1/d_ff), in the workload's dtype."""
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[wl.dtype]
+    base = 1000 * seed
+    L = wl.layers
+    gate = torch.empty((L, d_ff, wl.d_v), dtype=dt, device=dev)
+    up = torch.empty((L, d_ff, wl.d_v), dtype=dt, device=dev)
+    down = torch.empty((L, wl.d_h, d_ff), dtype=dt, device=dev)
+    for l in range(L):
+        gate[l] = _randn_rows(d_ff, wl.d_v, base + TID_FUS_GATE + l, dev, 1.0 / math.sqrt(wl.d_v), dt)
+        up[l] = _randn_rows(d_ff, wl.d_v, base + TID_FUS_UP + l, dev, 1.0 / math.sqrt(wl.d_v), dt)
+        down[l] = _randn_rows(wl.d_h, d_ff, base + TID_FUS_DOWN + l, dev, 1.0 / math.sqrt(d_ff), dt)
+    return dict(w_gate=gate, w_up=up, w_down=down, d_ff=d_ff)

@@ -107,6 +107,51 @@ class RelevanceRun(Run):
         return self
 
 
+class FusedRun(Run):
+    """A pass whose injection goes through the SwiGLU fusion of Eq. 10:
+    route, lookup, the kept set (lookme_select), then lookme_inject_fused."""
+
+    def __init__(self, inp: dict, fus: dict, **kw):
+        super().__init__(inp, **kw)
+        self.fus = fus
+        self.table.set_fusion(fus["w_gate"], fus["w_up"], fus["w_down"])
+
+    def run(self):
+        inp, L = self.inp, self.L
+        self.table.route(inp["x"], inp["wt"], self.q, self.scene, layers=L, stream=self.stream)
+        self.table.lookup(self.q, self.scene, self.prim, self.w, layers=L, stream=self.stream)
+        self.table.select(inp["delta"], self.kept, self.n_keep, layers=L, stream=self.stream)
+        self.table.inject_fused(self.kept, self.scene, self.prim, self.w, self.hidden,
+                                self.n_keep, layers=L, stream=self.stream)
+        return self
+
+
+def check_fused_run(r: FusedRun, tokens=None) -> C.Report:
+    """The kept set in full and the fused injection on the sampled tokens
+    (routing and lookup are checked by check_run and are the same here)."""
+    torch.cuda.synchronize()
+    inp, fus = r.inp, r.fus
+    dt = dtype_name(inp["x"])
+    rep = C.Report()
+    toks = np.arange(r.n) if tokens is None else np.asarray(tokens)
+    tsel = torch.as_tensor(toks, device=r.dev)
+    values = inp["values"]
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    for l in range(r.L):
+        c = O.criticality(f64(inp["delta"][l]))
+        kept = to_np(r.kept[l])[: r.n_keep]
+        C.check_kept(c, r.n_keep, kept, rep)
+        C.check_fused_hidden(to_np(r.h_in[l][tsel]), to_np(r.hidden[l][tsel]), dt, values_rows,
+                             r.P, to_np(r.scene[l]), to_np(r.prim[l]), to_np(r.w[l]), kept,
+                             f64(fus["w_gate"][l]), f64(fus["w_up"][l]), f64(fus["w_down"][l]),
+                             rep, toks)
+    return rep.finish()
+
+
 def check_relevance_run(r: RelevanceRun, tokens=None) -> C.Report:
     """Stage-wise check of a relevance pass on the sampled tokens: q and the
     scene as in check_run, the hidden activations (C1 bound), the primitives

@@ -187,6 +187,38 @@ def test_relevance_entry_points_validate(lib):
         lk.lookme_destroy(h)
 
 
+def test_fusion_entry_points_validate(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        assert S(lambda: lk.lookme_inject_fused(h, 1, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 2048,
+                                                0)) == lk.LOOKME_ERR_INVALID     # none set
+        assert S(lambda: lk.lookme_set_fusion(h, 1, 0, 2048, FAKE, FAKE, FAKE)) == \
+            lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_fusion(h, 1, 96, 2048, FAKE, FAKE, FAKE)) == \
+            lk.LOOKME_ERR_UNSUPPORTED       # 192 bytes: not whole 128-byte stages
+        assert S(lambda: lk.lookme_set_fusion(h, 1, 2048, 2048, FAKE, None, FAKE)) == \
+            lk.LOOKME_ERR_INVALID
+        base = lk.lookme_workspace_size(h, 1, 100)
+        assert S(lambda: lk.lookme_set_fusion(h, 2, 2048, 2048, FAKE, FAKE, FAKE)) == \
+            lk.LOOKME_OK
+        assert lk.lookme_workspace_size(h, 1, 100) >= base + 100 * (2048 + 2048) * 2
+        assert S(lambda: lk.lookme_inject_fused(h, 3, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 2048,
+                                                0)) == lk.LOOKME_ERR_INVALID     # 3 > 2 layers
+        assert S(lambda: lk.lookme_inject_fused(h, 1, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 1024,
+                                                0)) == lk.LOOKME_ERR_INVALID     # wrong d_h
+        assert S(lambda: lk.lookme_inject_fused(h, 1, 8, 9, FAKE, FAKE, FAKE, FAKE, FAKE, 2048,
+                                                0)) == lk.LOOKME_ERR_INVALID     # n_keep > n
+        assert S(lambda: lk.lookme_inject_fused(h, 1, 8, 0, None, None, None, None, None, 2048,
+                                                0)) == lk.LOOKME_OK
+        assert S(lambda: lk.lookme_inject_fused(h, 1, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 2048,
+                                                0)) == lk.LOOKME_ERR_WORKSPACE
+    finally:
+        lk.lookme_destroy(h)
+
+
 def test_null_handle(lib):
     assert _status(lambda: lk.lookme_workspace_size(None, 1, 1))[0] == lk.LOOKME_ERR_INVALID
     assert _status(lambda: lk.lookme_route(None, 1, 1, 1, FAKE, FAKE, FAKE, FAKE, 0))[0] == \

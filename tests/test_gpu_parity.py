@@ -12,7 +12,8 @@ import pytest
 import torch
 
 from oracle import lookme_oracle as O
-from synth import WORKLOADS, Workload, make_inputs, make_integer_inputs, make_relevance
+from synth import (WORKLOADS, Workload, make_fusion, make_inputs, make_integer_inputs,
+                   make_relevance)
 
 pytestmark = pytest.mark.gpu
 
@@ -258,6 +259,43 @@ def test_relevance_lookup(name):
     torch.cuda.synchronize()
     for key in ("act", "prim", "w"):
         assert torch.equal(getattr(r, key), getattr(r2, key)), key
+
+
+# Sparse injection through the SwiGLU fusion (Eq. 10): (workload, d_ff,
+# sampled tokens or None).  Rows of unit scale (value_std 1) so that f is of
+# the order of H; ragged kept counts and widths (d_h 80, d_ff 192, n_keep
+# 90 and 11) leave partial tiles in both products.
+FUSION = {
+    "bf16_fus_l2": (Workload("bf16_fus_l2", "bf16", 300, 2, 256, 128, 20, 60, 128, 80, 8, 30,
+                             usage="uniform", value_std=1.0), 192, None),
+    "f32_fus": (Workload("f32_fus", "f32", 77, 1, 96, 64, 5, 37, 64, 48, 3, 15, usage="iid",
+                         value_std=1.0), 96, None),
+    "bf16_fus_image": (WORKLOADS[1].scaled(value_std=1.0), 2048, 80),
+}
+
+
+@pytest.mark.parametrize("name", list(FUSION))
+def test_fused_injection(name):
+    """lookme_select then lookme_inject_fused against the oracle's
+    round(H + f(round(R))) on the library's primitives; other rows keep
+    their bits; two passes from the same inputs agree bit for bit."""
+    from tests.harness import FusedRun, check_fused_run
+    wl, d_ff, sample = FUSION[name]
+    _announce(f"fusion {name}: {wl} d_ff {d_ff}")
+    inp = make_inputs(wl, seed=6, device=DEV)
+    fus = make_fusion(wl, 6, d_ff, device=DEV)
+    r = FusedRun(inp, fus).run()
+    toks = None
+    if sample:
+        kept0 = r.kept[0].cpu().numpy()[:40]
+        toks = np.unique(np.concatenate(
+            [np.random.default_rng(6).choice(wl.n_tokens, sample, replace=False), kept0]))
+    rep = check_fused_run(r, tokens=toks)
+    assert rep.ok, str(rep)
+    assert rep.decisions.get("hidden_row", 0) > 0
+    r2 = FusedRun(inp, fus, table=r.table).run()
+    torch.cuda.synchronize()
+    assert torch.equal(r.hidden, r2.hidden)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
