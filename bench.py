@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--relevance", type=int, default=0, metavar="HIDDEN",
                     help="Level-2 in the paper's form (relevance MLP of this hidden width, "
                          "seeded weights) instead of the key-scored Level-2")
+    ap.add_argument("--fusion", type=int, default=0, metavar="D_FF",
+                    help="inject through the SwiGLU fusion of Eq. 10 (inner width D_FF, seeded "
+                         "weights) instead of the prefix add of the retrieved rows")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -168,7 +171,7 @@ def stored_traffic(wl):
 
 
 class Bench:
-    def __init__(self, wl, seed, copies, relevance=0):
+    def __init__(self, wl, seed, copies, relevance=0, fusion=0):
         import torch
         from paper_2607_16305_amd import lookme as lk
         from synth import make_inputs
@@ -208,6 +211,14 @@ class Bench:
                 t.set_relevance(m["w1"], m["b1"], m["w2"], m["b2"])
                 t.reserve(L, n)          # the relevance logits need a larger workspace
             self.act = torch.empty((L, n, relevance), dtype=dt, device=dev)
+        self.fus = None
+        if fusion:
+            from synth import make_fusion
+            self.fus = make_fusion(wl, seed, fusion, device="cuda")
+            f = self.fus
+            for t in self.tables:
+                t.set_fusion(f["w_gate"], f["w_up"], f["w_down"])
+                t.reserve(L, n)          # the fusion's buffers enlarge the workspace
         # the kept set is selected on a second stream (default priority, as
         # the first) while routing and lookup run; two reusable events order
         # the streams within a step
@@ -239,8 +250,12 @@ class Bench:
             lk.lookme_lookup_relevance(h, L, n, self.q, self.scene, self.act, self.prim, self.w,
                                        self.stream)
         self.main.wait_event(self.ev_kept)
-        lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
-                              self.hidden, wl.d_h, self.stream)
+        if self.fus is None:
+            lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
+                                  self.hidden, wl.d_h, self.stream)
+        else:
+            lk.lookme_inject_fused(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
+                                   self.hidden, wl.d_h, self.stream)
 
     def timed(self, steps):
         torch = self.torch
@@ -291,6 +306,10 @@ class Bench:
         b["inject"] = keep * (k * wl.d_v * es + 2 * wl.d_v * es + k * 8 + 8)
         flops = {"project": 2 * n * wl.d_in * L * wl.d_e, "route": 2 * rows * wl.d_e * wl.scenes,
                  "score": 2 * rows * wl.d_e * wl.prims}
+        if self.fus is not None:
+            d_ff = self.fus["d_ff"]
+            flops["inject"] = 2 * keep * (2 * wl.d_v * d_ff + d_ff * wl.d_h)
+            b["inject"] = None
         if self.mlp is not None:
             hid = self.mlp["hidden"]
             # the two MLP layers (the cosines are 2 k d_e per row, negligible)
@@ -334,6 +353,10 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
         mlp = (O.to_f64(to_np(b.mlp["w1"]), dt), f(b.mlp["b1"]), O.to_f64(to_np(b.mlp["w2"]), dt),
                f(b.mlp["b2"]))
 
+    fusion = None
+    if b.fus is not None:
+        fusion = tuple(O.to_f64(to_np(b.fus[key]), dt) for key in ("w_gate", "w_up", "w_down"))
+
     # the sample is repeated until about min_seconds of CPU work have been
     # timed (the same inputs each time), so that the rate is not a single
     # short measurement
@@ -343,14 +366,16 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
             t0 = time.perf_counter()
             res = O.run(O.to_f64(x, dt), None if wt is None else O.to_f64(wt, dt),
                         O.to_f64(K1, dt), Rows(K2), Rows(V), None, O.to_f64(D, dt),
-                        O.to_f64(H, dt), k=wl.top_k, n_keep=n_keep, dtype=dt, mlp=mlp)
+                        O.to_f64(H, dt), k=wl.top_k, n_keep=n_keep, dtype=dt, mlp=mlp,
+                        fusion=fusion)
             el += time.perf_counter() - t0
             reps += 1
             assert res["hidden"].shape == (wl.layers, m, wl.d_h)
     return {"value": reps * wl.layers * m / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {m} of {wl.n_tokens} tokens x {wl.layers} layer(s), whole path "
                       f"(projection..injection, n_keep={n_keep}"
-                      f"{', relevance Level-2' if mlp is not None else ''}), float64 NumPy, "
+                      f"{', relevance Level-2' if mlp is not None else ''}"
+                      f"{', SwiGLU fusion' if fusion is not None else ''}), float64 NumPy, "
                       f"1 thread, {reps} repetitions, {el:.1f} s"}
 
 
@@ -374,7 +399,7 @@ def main():
     torch.cuda.set_device(0)
     if args.pmc_calibrate:
         calibration_copy()
-    b = Bench(wl, args.workload, args.copies, args.relevance)
+    b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion)
 
     for i in range(args.warmup):
         b.step(i)
@@ -429,7 +454,9 @@ def main():
                    "d_v": wl.d_v, "d_h": wl.d_h, "top_k": wl.top_k, "n_keep": wl.n_keep,
                    "usage": wl.usage, "table_copies": b.copies,
                    "level2": (f"relevance MLP, hidden {args.relevance}" if args.relevance
-                              else "primitive keys")},
+                              else "primitive keys"),
+                   "injection": (f"SwiGLU fusion, d_ff {args.fusion}" if args.fusion
+                                 else "prefix add of the retrieved rows")},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kern,

@@ -279,13 +279,15 @@ def inject(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarray,
 
 
 def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
-        k: int, n_keep: int, dtype: str, score: str = "dot", mlp=None):
+        k: int, n_keep: int, dtype: str, score: str = "dot", mlp=None, fusion=None):
     """Whole path for L layers sharing one table (Sec. 3.3 inter-layer reuse).
 
     x [n, d_in]; w_t [L, d_e, d_in] or None; delta [L, n, d_c];
     hidden [L, n, d_h]; all float64 values.  ``mlp`` = (w1, b1, w2, b2)
     selects Level-2 in the paper's form (relevance_hidden/relevance_lookup)
-    instead of the key-scored one.  Returns a dict of per-layer results:
+    instead of the key-scored one; ``fusion`` = (w_gate, w_up, w_down), each
+    with a leading layer axis, injects through f (inject_fused) instead of
+    the prefix add.  Returns a dict of per-layer results:
     q [L,n,d_e], scene [L,n], prim [L,n,k], w [L,n,k], kept [L,n_keep],
     hidden [L,n,d_h].
     """
@@ -302,7 +304,11 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
             a = relevance_hidden(q, sc, scene_keys, w1, b1, dtype)
             pr, ww, _ = relevance_lookup(q, sc, a, w2, b2, prim_keys, k)
         kept = select(criticality(delta[l]), n_keep)
-        h = inject(hidden[l], values, P, sc, pr, ww, kept, dtype)
+        if fusion is None:
+            h = inject(hidden[l], values, P, sc, pr, ww, kept, dtype)
+        else:
+            h = inject_fused(hidden[l], values, P, sc, pr, ww, kept, fusion[0][l], fusion[1][l],
+                             fusion[2][l], dtype)
         for name, v in zip(res, (q, sc, pr, ww, kept, h)):
             res[name].append(v)
     return {name: np.stack(v) for name, v in res.items()}

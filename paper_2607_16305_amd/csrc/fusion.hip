@@ -36,12 +36,7 @@ hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int6
   g1.cols = f.d_ff;
   g1.ksplit = (int)(g1.k_bytes / TG_KB);
   g1.tiles = (int)(rt * ((f.d_ff + TgShape::BN / 2 - 1) / (TgShape::BN / 2)));
-  const dim3 grid1((unsigned)((g1.tiles + 7) / 8 * 8), (unsigned)layers);
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_SWIGLU>), grid1, dim3(256), 0, st, g1);
-  else
-    hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_SWIGLU>), grid1, dim3(256), 0, st, g1);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_tile_gemm<EPI_SWIGLU>(dt, g1, layers, st);
   if (e != hipSuccess) return e;
 
   TileGemmParams g2{};
@@ -60,12 +55,7 @@ hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int6
   g2.cols = f.d_h;
   g2.ksplit = (int)(g2.k_bytes / TG_KB);
   g2.tiles = (int)(rt * ((f.d_h + TgShape::BN - 1) / TgShape::BN));
-  const dim3 grid2((unsigned)((g2.tiles + 7) / 8 * 8), (unsigned)layers);
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_RESID>), grid2, dim3(256), 0, st, g2);
-  else
-    hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_RESID>), grid2, dim3(256), 0, st, g2);
-  return hipGetLastError();
+  return launch_tile_gemm<EPI_RESID>(dt, g2, layers, st);
 }
 
 }  // namespace lookme

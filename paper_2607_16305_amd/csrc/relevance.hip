@@ -188,21 +188,6 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
                             float* logits, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
-  auto gemm = [&](const TileGemmParams& gp, int epi) {
-    const unsigned grid = (unsigned)((gp.tiles + 7) / 8 * 8);
-    if (dt == DT_BF16) {
-      if (epi == EPI_ACT)
-        hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
-      else
-        hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
-    } else {
-      if (epi == EPI_ACT)
-        hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_ACT>), dim3(grid), dim3(256), 0, st, gp);
-      else
-        hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI_LOGIT>), dim3(grid), dim3(256), 0, st, gp);
-    }
-    return hipGetLastError();
-  };
   const int64_t rt = (rows + TgShape::BM - 1) / TgShape::BM;
   // hidden layer: K = [query ; scene key]
   TileGemmParams g1{};
@@ -219,7 +204,7 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
   g1.cols = mlp.hidden;
   g1.ksplit = (int)(g1.a_bytes / TG_KB);
   g1.tiles = (int)(rt * ((mlp.hidden + TgShape::BN - 1) / TgShape::BN));
-  hipError_t e = gemm(g1, EPI_ACT);
+  hipError_t e = launch_tile_gemm<EPI_ACT>(dt, g1, 1, st);
   if (e != hipSuccess) return e;
   // logits: r = a W2^T + b2, float32
   TileGemmParams g2{};
@@ -235,7 +220,7 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
   g2.tiles = (int)(rt * ((P + TgShape::BN - 1) / TgShape::BN));
   // large products on the projection's 256 x 256 tiles, small ones here
   if (!launch_logits_gemm(dt, act, mlp.w2, mlp.b2, logits, rows, P, g2.k_bytes, st))
-    e = gemm(g2, EPI_LOGIT);
+    e = launch_tile_gemm<EPI_LOGIT>(dt, g2, 1, st);
   else
     e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -1,9 +1,14 @@
 // Small-tile product C = A B^T on the matrix cores for the MLP-shaped steps
 // (the relevance MLP of Eq. 6 and the SwiGLU fusion of Eq. 10): 64 x 64
 // output tiles, 4 waves in 2 x 2 (each 2 x 2 MFMA tiles), K in 128-byte
-// stages loaded straight into LDS (dtl.h), two stages, one in flight while
-// the other is multiplied.  blockIdx.y selects a batch (a layer) whose A, B
-// and output start a fixed stride further.  Epilogues:
+// stages loaded straight into LDS (dtl.h), a ring of NS stages, NS - 1 in
+// flight while one is multiplied.  These products have few rows and long K,
+// so the loads' latency, not the matrix cores, sets the pace: a small grid
+// takes a ring of 4 (64 KB of LDS, 2 workgroups a CU), a grid that would not
+// fit the chip at that occupancy a ring of 2 (32 KB, up to 5 a CU); see
+// launch_tile_gemm.
+// blockIdx.y selects a batch (a layer) whose A, B and output start a fixed
+// stride further.  Epilogues:
 //
 //   EPI_ACT     C + bias, ReLU, one rounding to the storage dtype, [rows, cols];
 //   EPI_LOGIT   C + bias as float32, [rows, cols];
@@ -47,13 +52,14 @@ struct TileGemmParams {
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
 
-template <int DT, int EPI>
+template <int DT, int EPI, int NS>
 __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
   using S = TgShape;
   constexpr int MI = 2, NJ = 2, KB = TG_KB, KSL = KB / 64, WN = 2;
   constexpr int ES = DT == DT_BF16 ? 2 : 4;
   constexpr int TCOLS = EPI == EPI_SWIGLU ? S::BN / 2 : S::BN;   // output columns a tile
-  __shared__ __attribute__((aligned(1024))) char lds[2][S::STAGE];
+  static_assert(NS >= 2, "a stage in flight while one is multiplied");
+  __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -112,7 +118,7 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
   }
   auto issue = [&](int stage) {
     const int s = stage < nst ? stage : nst - 1;   // past the end: a harmless reload
-    char* dst = lds[stage & 1];
+    char* dst = lds[stage % NS];
 #pragma unroll
     for (int b = 0; b < S::PER_WAVE; ++b) {
       const char* src =
@@ -127,16 +133,19 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  issue(0);
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i) issue(i);
   for (int s = 0; s < nst; ++s) {
-    // stage s has landed everywhere and every read of stage s - 1 (the other
-    // buffer) has ended: load stage s + 1 there, multiply stage s (a plain
-    // s_barrier: the fence of __syncthreads would wait for every load)
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // this wave's loads of stage s have landed once at most those of the
+    // NS - 2 younger stages are outstanding; the barrier makes every wave's
+    // visible and ends every read of stage s - 1, whose buffer the next
+    // loads fill (a plain s_barrier: the fence of __syncthreads would wait
+    // for every load in flight)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 2) * S::PER_WAVE) : "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    issue(s + 1);
-    const char* buf = lds[s & 1];
+    issue(s + NS - 1);
+    const char* buf = lds[s % NS];
 #pragma unroll
     for (int ks = 0; ks < KSL; ++ks) {
       u32x4_t fa[MI], fb[NJ];
@@ -227,6 +236,28 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
         }
     }
   }
+}
+
+// Launches the product over `batches` batches (blockIdx.y) with the ring
+// depth for its grid: 4 stages while every workgroup is resident at 2 a CU
+// (at most 512 over the chip's 256 CUs), else 2.
+template <int EPI>
+hipError_t launch_tile_gemm(int dt, const TileGemmParams& p, int batches, hipStream_t st) {
+  const unsigned gx = (unsigned)((p.tiles + 7) / 8 * 8);
+  const dim3 grid(gx, (unsigned)batches);
+  const bool deep = (int64_t)gx * batches <= 512;
+  if (dt == DT_BF16) {
+    if (deep)
+      hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI, 4>), grid, dim3(256), 0, st, p);
+    else
+      hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI, 2>), grid, dim3(256), 0, st, p);
+  } else {
+    if (deep)
+      hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI, 4>), grid, dim3(256), 0, st, p);
+    else
+      hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI, 2>), grid, dim3(256), 0, st, p);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace lookme

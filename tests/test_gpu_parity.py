@@ -271,6 +271,9 @@ FUSION = {
     "f32_fus": (Workload("f32_fus", "f32", 77, 1, 96, 64, 5, 37, 64, 48, 3, 15, usage="iid",
                          value_std=1.0), 96, None),
     "bf16_fus_image": (WORKLOADS[1].scaled(value_std=1.0), 2048, 80),
+    # a gate/up grid of 1024 workgroups: the product's two-stage ring
+    "bf16_fus_wide": (Workload("bf16_fus_wide", "bf16", 4000, 2, 256, 128, 20, 60, 256, 320, 8,
+                               25, usage="uniform", value_std=1.0), 1024, 60),
 }
 
 
