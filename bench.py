@@ -54,6 +54,10 @@ def parse():
     ap.add_argument("--fusion", type=int, default=0, metavar="D_FF",
                     help="inject through the SwiGLU fusion of Eq. 10 (inner width D_FF, seeded "
                          "weights) instead of the prefix add of the retrieved rows")
+    ap.add_argument("--netprop", type=int, default=0, metavar="M",
+                    help="with --fusion on a one-layer workload: the LookME layer's R is carried "
+                         "to M more layers by the propagation of Eq. 11 (seeded W_p), each "
+                         "injected through its own fusion")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -171,7 +175,7 @@ def stored_traffic(wl):
 
 
 class Bench:
-    def __init__(self, wl, seed, copies, relevance=0, fusion=0):
+    def __init__(self, wl, seed, copies, relevance=0, fusion=0, netprop=0):
         import torch
         from paper_2607_16305_amd import lookme as lk
         from synth import make_inputs
@@ -212,13 +216,21 @@ class Bench:
                 t.reserve(L, n)          # the relevance logits need a larger workspace
             self.act = torch.empty((L, n, relevance), dtype=dt, device=dev)
         self.fus = None
+        self.netprop = netprop
         if fusion:
-            from synth import make_fusion
-            self.fus = make_fusion(wl, seed, fusion, device="cuda")
+            from synth import make_fusion, make_propagation
+            self.fus = make_fusion(wl, seed, fusion, device="cuda", layers=L + netprop)
             f = self.fus
+            if netprop:
+                # the propagated layers' hidden states (synthetic: copies of
+                # the LookME layer's)
+                self.w_p_t = make_propagation(wl, seed, netprop, device="cuda")
+                self.hidden = inp["hidden"][:1].repeat(1 + netprop, 1, 1)
             for t in self.tables:
                 t.set_fusion(f["w_gate"], f["w_up"], f["w_down"])
-                t.reserve(L, n)          # the fusion's buffers enlarge the workspace
+                if netprop:
+                    t.set_propagation(self.w_p_t)
+                t.reserve(L + netprop, n)   # the fusion's buffers enlarge the workspace
         # the kept set is selected on a second stream (default priority, as
         # the first) while routing and lookup run; two reusable events order
         # the streams within a step
@@ -253,6 +265,10 @@ class Bench:
         if self.fus is None:
             lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
                                   self.hidden, wl.d_h, self.stream)
+        elif self.netprop:
+            lk.lookme_inject_propagated(h, self.netprop, n, wl.n_keep, self.kept[0], self.scene[0],
+                                        self.prim[0], self.w[0], self.hidden, wl.d_h,
+                                        self.stream)
         else:
             lk.lookme_inject_fused(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
                                    self.hidden, wl.d_h, self.stream)
@@ -308,7 +324,9 @@ class Bench:
                  "score": 2 * rows * wl.d_e * wl.prims}
         if self.fus is not None:
             d_ff = self.fus["d_ff"]
-            flops["inject"] = 2 * keep * (2 * wl.d_v * d_ff + d_ff * wl.d_h)
+            m = self.netprop
+            flops["inject"] = 2 * keep * ((1 + m) * (2 * wl.d_v * d_ff + d_ff * wl.d_h)
+                                          + m * wl.d_v * wl.d_v)
             b["inject"] = None
         if self.mlp is not None:
             hid = self.mlp["hidden"]
@@ -336,7 +354,7 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
     K2 = to_np(inp["prim_keys"])
     V = to_np(inp["values"])
     D = to_np(inp["delta"][:, :m])
-    H = to_np(inp["hidden"][:, :m])
+    H = to_np(b.hidden[:, :m] if b.netprop else inp["hidden"][:, :m])
 
     class Rows:
         """Table slices converted to float64 on access (the oracle indexes
@@ -356,6 +374,9 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
     fusion = None
     if b.fus is not None:
         fusion = tuple(O.to_f64(to_np(b.fus[key]), dt) for key in ("w_gate", "w_up", "w_down"))
+    w_p = None
+    if b.netprop:
+        w_p = O.to_f64(to_np(b.w_p_t), dt).transpose(0, 2, 1)
 
     # the sample is repeated until about min_seconds of CPU work have been
     # timed (the same inputs each time), so that the rate is not a single
@@ -367,15 +388,17 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
             res = O.run(O.to_f64(x, dt), None if wt is None else O.to_f64(wt, dt),
                         O.to_f64(K1, dt), Rows(K2), Rows(V), None, O.to_f64(D, dt),
                         O.to_f64(H, dt), k=wl.top_k, n_keep=n_keep, dtype=dt, mlp=mlp,
-                        fusion=fusion)
+                        fusion=fusion, propagation=w_p)
             el += time.perf_counter() - t0
             reps += 1
-            assert res["hidden"].shape == (wl.layers, m, wl.d_h)
+            assert res["hidden"].shape == (wl.layers + b.netprop, m, wl.d_h)
     return {"value": reps * wl.layers * m / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {m} of {wl.n_tokens} tokens x {wl.layers} layer(s), whole path "
                       f"(projection..injection, n_keep={n_keep}"
                       f"{', relevance Level-2' if mlp is not None else ''}"
-                      f"{', SwiGLU fusion' if fusion is not None else ''}), float64 NumPy, "
+                      f"{', SwiGLU fusion' if fusion is not None else ''}"
+                      f"{f', propagated to {b.netprop} more layers' if b.netprop else ''}), "
+                      f"float64 NumPy, "
                       f"1 thread, {reps} repetitions, {el:.1f} s"}
 
 
@@ -399,7 +422,9 @@ def main():
     torch.cuda.set_device(0)
     if args.pmc_calibrate:
         calibration_copy()
-    b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion)
+    if args.netprop and (not args.fusion or wl.layers != 1):
+        raise SystemExit("--netprop needs --fusion and a one-layer workload")
+    b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion, args.netprop)
 
     for i in range(args.warmup):
         b.step(i)
@@ -456,7 +481,8 @@ def main():
                    "level2": (f"relevance MLP, hidden {args.relevance}" if args.relevance
                               else "primitive keys"),
                    "injection": (f"SwiGLU fusion, d_ff {args.fusion}" if args.fusion
-                                 else "prefix add of the retrieved rows")},
+                                 else "prefix add of the retrieved rows"),
+                   "propagated_layers": args.netprop},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kern,

@@ -244,6 +244,40 @@ lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64
                                     int32_t d_h, void* stream);
 
 /*
+ * lookme_set_propagation -- registers the propagation projections of the
+ * inter-layer sparse activation (Sec. 3.3, Eq. 11), one for each of `steps`
+ * non-LookME layers after a LookME layer (borrowed, like the table):
+ *   w_p_t [steps, value_dim, value_dim] dtype, w_p_t[j][o][i] = W_p^(j+1)[i, o]
+ * (each matrix stored transposed, output-row-major, like the projection's W).
+ * The propagated rows keep the retrieved width value_dim.  Needs value_dim *
+ * elem_size a multiple of 128 bytes.
+ */
+lookme_status_t lookme_set_propagation(lookme_t h, int32_t steps, const void* w_p_t);
+
+/*
+ * lookme_inject_propagated -- sparse injection at a LookME layer and at the
+ * `steps` non-LookME layers after it (Eq. 10-11): one lookup and one kept set
+ * (the LookME layer's gate, reused by the layers after it), and for every
+ * kept token t and j = 0..steps:
+ *   R_0 = round(sum_i w[t,i] values[scene[t]*N_p + prim[t,i], :])
+ *   R_j = round(R_{j-1} W_p^j + R_{j-1})                            (j >= 1)
+ *   hidden[j, t, :] <- round(hidden[j, t, :] + f_j(R_j))
+ * with f_j layer j of the registered fusion (lookme_set_fusion: at least
+ * steps + 1 layers, d_h equal to the fusion's) and W_p^j projection j - 1 of
+ * lookme_set_propagation (at least `steps` registered).  kept [n_keep],
+ * scene [n], prim [n, top_k], w [n, top_k] are the LookME layer's (a
+ * one-layer select and lookup); hidden [steps + 1, n, d_h] holds the
+ * layers' hidden states, updated in place.  float32 accumulation, every other
+ * row keeps its bits; steps = 0 is lookme_inject_fused on one layer.  Needs
+ * the workspace of lookme_workspace_size(layers = steps + 1, n) queried after
+ * lookme_set_fusion.
+ */
+lookme_status_t lookme_inject_propagated(lookme_t h, int32_t steps, int64_t n, int64_t n_keep,
+                                         const int32_t* kept, const int32_t* scene,
+                                         const int32_t* prim, const float* w, void* hidden,
+                                         int32_t d_h, void* stream);
+
+/*
  * Measurement support (not part of the method).  When enabled, each kernel
  * group that route/lookup/inject launches is bracketed by a pair of HIP timing
  * events recorded on the call's stream.  lookme_profile_read waits for the

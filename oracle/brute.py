@@ -191,3 +191,23 @@ def fusion_rows(r_rows, w_gate_rows, w_up_rows, w_down_rows, mant_bits):
             u.append(round_fraction(val, mant_bits))
         out.append([dot(u, dw) for dw in w_down_rows])
     return out
+
+
+def propagate_rows(r_rows, w_p_mats, mant_bits):
+    """Eq. 11 by plain loops: R_j[o] = sum_i R_{j-1}[i] W_p^j[i][o] +
+    R_{j-1}[o], exact, then one rounding (as a rational) per element.
+    w_p_mats[j] is a list of d_v rows indexed [i][o].  Returns the list of
+    the m + 1 row lists (R_0 first)."""
+    chain = [[list(r) for r in r_rows]]
+    for wp in w_p_mats:
+        nxt = []
+        for r in chain[-1]:
+            row = []
+            for o in range(len(r)):
+                acc = Fraction(r[o])
+                for i in range(len(r)):
+                    acc += Fraction(r[i]) * Fraction(wp[i][o])
+                row.append(round_fraction(acc, mant_bits))
+            nxt.append(row)
+        chain.append(nxt)
+    return chain

@@ -321,6 +321,52 @@ def check_fused_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: 
         rep.notes["fused_max_abs"] = max(rep.notes.get("fused_max_abs", 0.0), float(err.max()))
 
 
+def check_propagated_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: int,
+                            scene: np.ndarray, prim: np.ndarray, w_lib: np.ndarray,
+                            kept: np.ndarray, w_p: np.ndarray, w_gate: np.ndarray,
+                            w_up: np.ndarray, w_down: np.ndarray, rep: Report, tokens,
+                            contract_abs: float = 2e-2):
+    """The LookME layer and the propagated layers after it (Eq. 10-11) on the
+    library's kept set, primitives and weights of the LookME layer: in every
+    layer j rows outside the kept set keep their bits, and kept rows equal
+    round(H_j + f_j(R_j)) with R_0 = round(R), R_j = round(R_{j-1} W_p^j +
+    R_{j-1}), within the contract of check_fused_hidden.  h_in and h_out_lib
+    hold [steps + 1, len(tokens), d_h]; w_p [steps, d_v, d_v] indexed
+    [input, output]."""
+    kept_set = set(np.asarray(kept).tolist())
+    steps = w_p.shape[0]
+    h_in_f = O.to_f64(h_in, dtype)
+    h_lib_f = O.to_f64(h_out_lib, dtype)
+    for r, t in enumerate(np.asarray(tokens)):
+        rep.count("hidden_row", steps + 1)
+        if int(t) not in kept_set:
+            if not np.array_equal(np.asarray(h_in[:, r]).view(np.uint8),
+                                  np.asarray(h_out_lib[:, r]).view(np.uint8)):
+                rep.fail(f"hidden: untouched row {t} modified")
+            continue
+        rows = int(scene[t]) * P + np.asarray(prim[t], dtype=np.int64)
+        V = values_rows(rows)
+        R = O.round_to_dtype(np.sum(np.asarray(w_lib[t], dtype=np.float64)[:, None] * V, axis=0),
+                             dtype)
+        for j in range(steps + 1):
+            if j > 0:
+                R = O.round_to_dtype(R @ w_p[j - 1] + R, dtype)
+            U = O.round_to_dtype(O.silu(w_gate[j] @ R) * (w_up[j] @ R), dtype)
+            F = w_down[j] @ U
+            exp = O.round_to_dtype(h_in_f[j, r] + F, dtype)
+            err = np.abs(h_lib_f[j, r] - exp)
+            if dtype == "bf16":
+                bad = err > contract_abs
+            else:
+                bad = err > 1e-4 * (np.abs(h_in_f[j, r]) + np.abs(w_down[j]) @ np.abs(U))
+            if np.any(bad):
+                c = int(np.argmax(err))
+                rep.fail(f"hidden[{j}, {t}, {c}]: library {h_lib_f[j, r, c]!r}, "
+                         f"expected {exp[c]!r}")
+            rep.notes["propagated_max_abs"] = max(rep.notes.get("propagated_max_abs", 0.0),
+                                                  float(err.max()))
+
+
 def check_kept(c: np.ndarray, n_keep: int, kept_lib: np.ndarray, rep: Report):
     """C5: the kept set equals the oracle's except for swaps among
     criticalities tied with the n_keep-th; ascending, unique, in range."""

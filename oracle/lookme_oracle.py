@@ -28,6 +28,9 @@ What is computed, step by step (each function cites its passage):
               similar primitives, so one table serves several layers)
   fusion      Eq. 10 with the SwiGLU fusion f: the kept tokens receive
               f(R) = W_down (silu(W_gate R) * (W_up R)) instead of R
+  propagate   Eq. 11 (inter-layer sparse activation): a non-LookME layer k
+              after LookME layer l carries R^(k) = R^(k-1) W_p^k + R^(k-1)
+              and reuses layer l's gate; inject_propagated applies f^k to it
   relevance_* Level-2 in the paper's own form (Eq. 6-7): a scene-shared
               two-layer MLP over [v_e, e_img[j]] gives relevance logits r_j;
               the top-k primitives by r are weighted by the softmax of
@@ -278,8 +281,46 @@ def inject(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarray,
     return out
 
 
+def propagate(r: np.ndarray, w_p: np.ndarray, dtype: str) -> np.ndarray:
+    """Eq. 11 chain: R^(0) = r, R^(j) = R^(j-1) W_p^j + R^(j-1) for j = 1..m,
+    each stored (rounded once to dtype) before the next step.
+
+    r [m_rows, d_v] (already rounded), w_p [m, d_v, d_v] in the paper's
+    orientation (input index first).  Returns [m + 1, m_rows, d_v]."""
+    out = [np.asarray(r, dtype=np.float64)]
+    for j in range(w_p.shape[0]):
+        prev = out[-1]
+        out.append(round_to_dtype(prev @ w_p[j] + prev, dtype))
+    return np.stack(out)
+
+
+def inject_propagated(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarray,
+                      prim: np.ndarray, w: np.ndarray, kept: np.ndarray, w_p: np.ndarray,
+                      w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
+                      dtype: str) -> np.ndarray:
+    """Injection at a LookME layer and the m = w_p.shape[0] non-LookME layers
+    after it (Eq. 10-11): the LookME layer's lookup (scene, prim, w) and gate
+    (kept) serve all of them; layer j's kept rows receive f_j(R^(j)) with
+    R^(j) from ``propagate``.
+
+    hidden [m + 1, n, d_h]; w_gate, w_up [>= m + 1, d_ff, d_v]; w_down
+    [>= m + 1, d_h, d_ff].  Returns float64 [m + 1, n, d_h]."""
+    out = np.array(hidden, dtype=np.float64, copy=True)
+    kept = np.asarray(kept, dtype=np.int64)
+    if kept.size == 0:
+        return out
+    R0 = round_to_dtype(
+        np.stack([retrieved(values, P, int(scene[t]), prim[t], w[t]) for t in kept]), dtype)
+    Rs = propagate(R0, w_p, dtype)
+    for j in range(Rs.shape[0]):
+        F = fusion(Rs[j], w_gate[j], w_up[j], w_down[j], dtype)
+        out[j, kept] = round_to_dtype(hidden[j, kept] + F, dtype)
+    return out
+
+
 def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
-        k: int, n_keep: int, dtype: str, score: str = "dot", mlp=None, fusion=None):
+        k: int, n_keep: int, dtype: str, score: str = "dot", mlp=None, fusion=None,
+        propagation=None):
     """Whole path for L layers sharing one table (Sec. 3.3 inter-layer reuse).
 
     x [n, d_in]; w_t [L, d_e, d_in] or None; delta [L, n, d_c];
@@ -287,11 +328,15 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
     selects Level-2 in the paper's form (relevance_hidden/relevance_lookup)
     instead of the key-scored one; ``fusion`` = (w_gate, w_up, w_down), each
     with a leading layer axis, injects through f (inject_fused) instead of
-    the prefix add.  Returns a dict of per-layer results:
-    q [L,n,d_e], scene [L,n], prim [L,n,k], w [L,n,k], kept [L,n_keep],
-    hidden [L,n,d_h].
+    the prefix add.  ``propagation`` = w_p [m, d_v, d_v] (with ``fusion`` of
+    at least m + 1 layers): one LookME layer whose R is carried to the m
+    layers after it (Eq. 11, inject_propagated); then hidden, w_t and delta
+    hold [m + 1, ...], [1, ...] and [1, ...].  Returns a dict of per-layer
+    results: q [L,n,d_e], scene [L,n], prim [L,n,k], w [L,n,k],
+    kept [L,n_keep], hidden [L,n,d_h] (with ``propagation``: L = 1 and
+    hidden [m + 1, n, d_h]).
     """
-    L = hidden.shape[0]
+    L = hidden.shape[0] if propagation is None else 1
     P = prim_keys.shape[1]
     res = {k_: [] for k_ in ("q", "scene", "prim", "w", "kept", "hidden")}
     for l in range(L):
@@ -304,14 +349,20 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
             a = relevance_hidden(q, sc, scene_keys, w1, b1, dtype)
             pr, ww, _ = relevance_lookup(q, sc, a, w2, b2, prim_keys, k)
         kept = select(criticality(delta[l]), n_keep)
-        if fusion is None:
+        if propagation is not None:
+            h = inject_propagated(hidden, values, P, sc, pr, ww, kept, propagation, fusion[0],
+                                  fusion[1], fusion[2], dtype)
+        elif fusion is None:
             h = inject(hidden[l], values, P, sc, pr, ww, kept, dtype)
         else:
             h = inject_fused(hidden[l], values, P, sc, pr, ww, kept, fusion[0][l], fusion[1][l],
                              fusion[2][l], dtype)
         for name, v in zip(res, (q, sc, pr, ww, kept, h)):
             res[name].append(v)
-    return {name: np.stack(v) for name, v in res.items()}
+    out = {name: np.stack(v) for name, v in res.items()}
+    if propagation is not None:
+        out["hidden"] = out["hidden"][0]
+    return out
 
 
 # ---------------------------------------------------------------------------

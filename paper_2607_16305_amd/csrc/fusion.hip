@@ -9,6 +9,11 @@
 //             them in its epilogue;
 //   down      H[kept] = round(H[kept] + U W_down^T), written in place (the
 //             kept list of the layer maps a product row to its token).
+//
+// The inter-layer propagation of Eq. 11 (launch_propagate) carries R from a
+// LookME layer to the layers after it: R_j = round(R_{j-1} W_p^j + R_{j-1}),
+// one product per layer (each needs the previous one), the residual added in
+// the epilogue.
 #include "common.h"
 #include "kernels.h"
 #include "tile_gemm.h"
@@ -16,8 +21,8 @@
 namespace lookme {
 
 hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int64_t n_keep,
-                         const int32_t* kept, int d_v, const void* r, void* u, void* hidden,
-                         hipStream_t st) {
+                         const int32_t* kept, int64_t kept_batch, int d_v, const void* r, void* u,
+                         void* hidden, hipStream_t st) {
   if (n == 0 || n_keep == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const int64_t rt = (n_keep + TgShape::BM - 1) / TgShape::BM;
@@ -50,12 +55,36 @@ hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int6
   g2.a_batch = n_keep * g2.a_bytes;
   g2.b_batch = (int64_t)f.d_h * g2.k_bytes;
   g2.n = n;
-  g2.n_keep = n_keep;
+  g2.kept_batch = kept_batch;
   g2.out_ld = (int64_t)f.d_h * es;
   g2.cols = f.d_h;
   g2.ksplit = (int)(g2.k_bytes / TG_KB);
   g2.tiles = (int)(rt * ((f.d_h + TgShape::BN - 1) / TgShape::BN));
   return launch_tile_gemm<EPI_RESID>(dt, g2, layers, st);
+}
+
+hipError_t launch_propagate(int dt, const void* w_p_t, int steps, int64_t n_keep, int d_v,
+                            void* r, hipStream_t st) {
+  if (n_keep == 0) return hipSuccess;
+  const int64_t es = dt == DT_BF16 ? 2 : 4;
+  const int64_t slice = n_keep * d_v * es;
+  const int64_t rt = (n_keep + TgShape::BM - 1) / TgShape::BM;
+  for (int j = 1; j <= steps; ++j) {
+    TileGemmParams g{};
+    g.a0 = static_cast<const char*>(r) + (j - 1) * slice;
+    g.res = g.a0;
+    g.b = static_cast<const char*>(w_p_t) + (int64_t)(j - 1) * d_v * d_v * es;
+    g.out = static_cast<char*>(r) + j * slice;
+    g.rows = n_keep;
+    g.a_bytes = (int64_t)d_v * es;
+    g.k_bytes = g.a_bytes;
+    g.cols = d_v;
+    g.ksplit = (int)(g.k_bytes / TG_KB);
+    g.tiles = (int)(rt * ((d_v + TgShape::BN - 1) / TgShape::BN));
+    const hipError_t e = launch_tile_gemm<EPI_ADD>(dt, g, 1, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace lookme

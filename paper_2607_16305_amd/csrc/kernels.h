@@ -114,7 +114,8 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
 // Per layer l (tensors borrowed): w_gate, w_up [layers, d_ff, d_v] and
 // w_down [layers, d_h, d_ff] in the table's dtype.  launch_gather_rows
 // writes R [layers * n_keep, d_v] (rounded); launch_fusion then writes
-// U [layers * n_keep, d_ff] and adds W_down U into the kept rows of H.
+// U [layers * n_keep, d_ff] and adds W_down U into the kept rows of H, the
+// kept list of layer l at kept + l * kept_batch (0: one list for all).
 struct FusionFfn {
   int layers, d_ff, d_h;
   const void* w_gate;
@@ -126,8 +127,13 @@ hipError_t launch_gather_rows(int dt, int layers, int64_t n, int64_t n_keep, con
                               const void* values, int S, int P, int d_v, int k, void* r_out,
                               hipStream_t st);
 hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int64_t n_keep,
-                         const int32_t* kept, int d_v, const void* r, void* u, void* hidden,
-                         hipStream_t st);
+                         const int32_t* kept, int64_t kept_batch, int d_v, const void* r, void* u,
+                         void* hidden, hipStream_t st);
+// Propagation of Eq. 11 over `steps` layers: r holds [steps + 1, n_keep, d_v]
+// (slice 0 given); slice j = round(slice j-1 W_p^j + slice j-1), with
+// w_p_t [steps, d_v, d_v] holding each W_p transposed (output-row-major).
+hipError_t launch_propagate(int dt, const void* w_p_t, int steps, int64_t n_keep, int d_v,
+                            void* r, hipStream_t st);
 
 // ---- Level-2 scoring of bucketed rows, fused top-k + softmax --------------
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,

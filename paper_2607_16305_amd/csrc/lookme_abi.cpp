@@ -36,6 +36,8 @@ struct lookme_s {
   double prof_ms[LOOKME_GROUP_COUNT];
   lookme::RelevanceMlp rel;                // hidden == 0: none registered
   lookme::FusionFfn fus;                   // d_ff == 0: none registered
+  int32_t prop_steps = 0;                  // Eq. 11 projections; 0: none registered
+  const void* prop_w = nullptr;            // [prop_steps, value_dim, value_dim], transposed
 };
 
 namespace {
@@ -552,6 +554,27 @@ lookme_status_t lookme_set_fusion(lookme_t h, int32_t layers, int32_t d_ff, int3
   return LOOKME_OK;
 }
 
+// Checks shared by the fused injections: a fusion of at least `layers`
+// layers writing rows of width d_h.
+lookme_status_t check_fusion(lookme_t h, int32_t layers, int32_t d_h) {
+  if (h->fus.d_ff < 1)
+    return fail(LOOKME_ERR_INVALID, "no fusion registered (lookme_set_fusion)");
+  if (layers > h->fus.layers)
+    return fail(LOOKME_ERR_INVALID, "%d layers, the fusion has %d", layers, h->fus.layers);
+  if (d_h != h->fus.d_h)
+    return fail(LOOKME_ERR_INVALID, "d_h %d, the fusion writes %d", d_h, h->fus.d_h);
+  return LOOKME_OK;
+}
+
+lookme_status_t check_lookup_ptrs(const int32_t* kept, const int32_t* scene, const int32_t* prim,
+                                  const float* w, void* hidden) {
+  LOOKME_TRY(check_ptr(kept, "kept"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(prim, "prim"));
+  LOOKME_TRY(check_ptr(w, "w"));
+  return check_ptr(hidden, "hidden");
+}
+
 lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
                                     const int32_t* kept, const int32_t* scene,
                                     const int32_t* prim, const float* w, void* hidden,
@@ -559,18 +582,9 @@ lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64
   LOOKME_TRY(check_handle(h));
   LOOKME_TRY(check_layers_n(layers, n));
   LOOKME_TRY(check_keep(n, n_keep));
-  if (h->fus.d_ff < 1)
-    return fail(LOOKME_ERR_INVALID, "no fusion registered (lookme_set_fusion)");
-  if (layers > h->fus.layers)
-    return fail(LOOKME_ERR_INVALID, "%d layers, the fusion has %d", layers, h->fus.layers);
-  if (d_h != h->fus.d_h)
-    return fail(LOOKME_ERR_INVALID, "d_h %d, the fusion writes %d", d_h, h->fus.d_h);
+  LOOKME_TRY(check_fusion(h, layers, d_h));
   if (n == 0 || n_keep == 0) return LOOKME_OK;
-  LOOKME_TRY(check_ptr(kept, "kept"));
-  LOOKME_TRY(check_ptr(scene, "scene"));
-  LOOKME_TRY(check_ptr(prim, "prim"));
-  LOOKME_TRY(check_ptr(w, "w"));
-  LOOKME_TRY(check_ptr(hidden, "hidden"));
+  LOOKME_TRY(check_lookup_ptrs(kept, scene, prim, w, hidden));
   Layout L;
   LOOKME_TRY(check_workspace(h, layers, n, &L));
   const lookme_desc_t& d = h->d;
@@ -581,8 +595,53 @@ lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64
                                                    w, h->values, d.num_scenes, d.prims_per_scene,
                                                    d.value_dim, d.top_k, ws + L.fus_r, st),
                         "fusion gather launch"));
-  return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n_keep, kept, d.value_dim,
-                                          ws + L.fus_r, ws + L.fus_u, hidden, st),
+  return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n_keep, kept, n_keep,
+                                          d.value_dim, ws + L.fus_r, ws + L.fus_u, hidden, st),
+                    "fusion launch");
+}
+
+lookme_status_t lookme_set_propagation(lookme_t h, int32_t steps, const void* w_p_t) {
+  LOOKME_TRY(check_handle(h));
+  if (steps < 1) return fail(LOOKME_ERR_INVALID, "steps must be positive");
+  if (((int64_t)h->d.value_dim * elem_size(h->d.dtype)) % 128 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "value_dim * elem_size must be a multiple of 128 bytes");
+  LOOKME_TRY(check_ptr(w_p_t, "w_p_t"));
+  h->prop_steps = steps;
+  h->prop_w = w_p_t;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_inject_propagated(lookme_t h, int32_t steps, int64_t n, int64_t n_keep,
+                                         const int32_t* kept, const int32_t* scene,
+                                         const int32_t* prim, const float* w, void* hidden,
+                                         int32_t d_h, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  if (steps < 0) return fail(LOOKME_ERR_INVALID, "steps must be >= 0 (got %d)", steps);
+  if (steps >= INT32_MAX) return fail(LOOKME_ERR_INVALID, "steps too large");
+  const int32_t layers = steps + 1;
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_keep(n, n_keep));
+  LOOKME_TRY(check_fusion(h, layers, d_h));
+  if (steps > h->prop_steps)
+    return fail(LOOKME_ERR_INVALID, "%d propagation steps, %d registered (lookme_set_propagation)",
+                steps, h->prop_steps);
+  if (n == 0 || n_keep == 0) return LOOKME_OK;
+  LOOKME_TRY(check_lookup_ptrs(kept, scene, prim, w, hidden));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(h->ws);
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  LOOKME_TRY(hip_status(lookme::launch_gather_rows(d.dtype, 1, n, n_keep, kept, scene, prim, w,
+                                                   h->values, d.num_scenes, d.prims_per_scene,
+                                                   d.value_dim, d.top_k, ws + L.fus_r, st),
+                        "fusion gather launch"));
+  LOOKME_TRY(hip_status(
+      lookme::launch_propagate(d.dtype, h->prop_w, steps, n_keep, d.value_dim, ws + L.fus_r, st),
+      "propagation launch"));
+  return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n_keep, kept, 0,
+                                          d.value_dim, ws + L.fus_r, ws + L.fus_u, hidden, st),
                     "fusion launch");
 }
 

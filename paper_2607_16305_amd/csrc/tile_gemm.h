@@ -1,5 +1,6 @@
 // Small-tile product C = A B^T on the matrix cores for the MLP-shaped steps
-// (the relevance MLP of Eq. 6 and the SwiGLU fusion of Eq. 10): 64 x 64
+// (the relevance MLP of Eq. 6, the SwiGLU fusion of Eq. 10 and the
+// propagation of Eq. 11): 64 x 64
 // output tiles, 4 waves in 2 x 2 (each 2 x 2 MFMA tiles), K in 128-byte
 // stages loaded straight into LDS (dtl.h), a ring of NS stages, NS - 1 in
 // flight while one is multiplied.  These products have few rows and long K,
@@ -16,7 +17,8 @@
 //               of B2 (up): u = silu(gate) * up, rounded, [rows, cols] with
 //               32 output columns a tile;
 //   EPI_RESID   H[out_row(r), c] = round(H + C) with out_row(r) = z * n +
-//               kept[z * n_keep + r] (the kept token of row r of layer z).
+//               kept[z * kept_batch + r] (the kept token of row r of layer z);
+//   EPI_ADD     round(C + res) with res [rows, cols], [rows, cols].
 //
 // An A row may take its first `ksplit` stages from a0 and the rest from a
 // gathered row of a1 (the relevance MLP's [query ; scene key] input).
@@ -30,7 +32,7 @@ namespace lookme {
 using TgShape = DtlShape<2, 2, 2, 2, 128>;
 constexpr int TG_KB = 128;
 
-enum : int { EPI_ACT = 0, EPI_LOGIT = 1, EPI_SWIGLU = 2, EPI_RESID = 3 };
+enum : int { EPI_ACT = 0, EPI_LOGIT = 1, EPI_SWIGLU = 2, EPI_RESID = 3, EPI_ADD = 4 };
 
 struct TileGemmParams {
   const char* a0;           // [rows, K] (or the first ksplit stages of a row)
@@ -40,12 +42,13 @@ struct TileGemmParams {
   const char* b2;           // EPI_SWIGLU: up rows [cols, K]
   const float* bias;        // [cols] or null (EPI_ACT, EPI_LOGIT)
   char* out;
-  const int32_t* kept;      // EPI_RESID: [batches, n_keep]
+  const int32_t* kept;      // EPI_RESID: kept list of batch z at kept + z * kept_batch
+  const char* res;          // EPI_ADD: [rows, cols]
   int64_t rows;
   int64_t a_bytes;          // bytes of an A row (of each part, when split)
   int64_t k_bytes;          // K in bytes, a multiple of 128
   int64_t a_batch, b_batch, out_batch;   // byte strides between batches
-  int64_t n, n_keep;        // EPI_RESID: tokens per layer, kept rows per layer
+  int64_t n, kept_batch;    // EPI_RESID: tokens per layer, stride of the kept lists
   int64_t out_ld;           // EPI_RESID: bytes of an H row
   int sel_rows, cols, ksplit, tiles;
 };
@@ -221,8 +224,15 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
               *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16_rne(fmaxf(c, 0.f));
             else
               *reinterpret_cast<float*>(dst) = fmaxf(c, 0.f);
+          } else if constexpr (EPI == EPI_ADD) {
+            const int64_t at = (row * a.cols + col) * ES;
+            if constexpr (DT == DT_BF16)
+              *reinterpret_cast<uint16_t*>(a.out + at) = (uint16_t)f32_to_bf16_rne(
+                  bf16lo(*reinterpret_cast<const uint16_t*>(a.res + at)) + c);
+            else
+              *reinterpret_cast<float*>(a.out + at) = *reinterpret_cast<const float*>(a.res + at) + c;
           } else {   // EPI_RESID
-            int64_t t = a.kept[z * a.n_keep + row];
+            int64_t t = a.kept[z * a.kept_batch + row];
             t = t < 0 ? 0 : (t >= a.n ? a.n - 1 : t);
             char* dst = a.out + (z * a.n + t) * a.out_ld + (int64_t)col * ES;
             if constexpr (DT == DT_BF16) {

@@ -28,7 +28,7 @@ STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "HIP
 EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "lookme_route",
             "lookme_lookup", "lookme_inject", "lookme_select", "lookme_inject_kept",
             "lookme_set_relevance", "lookme_lookup_relevance", "lookme_set_fusion",
-            "lookme_inject_fused",
+            "lookme_inject_fused", "lookme_set_propagation", "lookme_inject_propagated",
             "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
@@ -82,6 +82,9 @@ def load():
                               _vp],
         "lookme_inject_fused": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp, _vp,
                                 _vp, _vp, _vp, ctypes.c_int32, _vp],
+        "lookme_set_propagation": [_vp, ctypes.c_int32, _vp],
+        "lookme_inject_propagated": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
+                                     _vp, _vp, _vp, _vp, ctypes.c_int32, _vp],
         "lookme_destroy": [_vp],
         "lookme_profile_enable": [_vp, ctypes.c_int32],
         "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
@@ -184,6 +187,17 @@ def lookme_inject_fused(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h,
                                       _ptr(w), _ptr(hidden), d_h, _stream(stream)))
 
 
+def lookme_set_propagation(h, steps, w_p_t):
+    _check(load().lookme_set_propagation(h, steps, _ptr(w_p_t)))
+
+
+def lookme_inject_propagated(h, steps, n, n_keep, kept, scene, prim, w, hidden, d_h,
+                             stream=None):
+    _check(load().lookme_inject_propagated(h, steps, n, n_keep, _ptr(kept), _ptr(scene),
+                                           _ptr(prim), _ptr(w), _ptr(hidden), d_h,
+                                           _stream(stream)))
+
+
 def lookme_destroy(h):
     if h:
         _check(load().lookme_destroy(h))
@@ -273,6 +287,16 @@ class Table:
         self.reserve(layers, n)
         lookme_inject_fused(self.handle, layers, n, n_keep, kept, scene, prim, w, hidden,
                             hidden.shape[-1], stream)
+
+    def set_propagation(self, w_p_t):
+        self.propagation = w_p_t                 # keep alive
+        lookme_set_propagation(self.handle, w_p_t.shape[0], w_p_t)
+
+    def inject_propagated(self, kept, scene, prim, w, hidden, n_keep, steps, stream=None):
+        n = scene.numel()
+        self.reserve(steps + 1, n)
+        lookme_inject_propagated(self.handle, steps, n, n_keep, kept, scene, prim, w, hidden,
+                                 hidden.shape[-1], stream)
 
     def close(self):
         if self.handle:

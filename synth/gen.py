@@ -39,6 +39,7 @@ TID_X, TID_K1, TID_K2, TID_V, TID_LABELS, TID_CENT, TID_PERM = 1, 2, 3, 4, 5, 6,
 TID_W, TID_DELTA, TID_H = 10, 20, 30
 TID_MLP_W1, TID_MLP_B1, TID_MLP_W2, TID_MLP_B2 = 40, 41, 42, 43
 TID_FUS_GATE, TID_FUS_UP, TID_FUS_DOWN = 50, 60, 70
+TID_PROP = 80
 
 
 @dataclasses.dataclass(frozen=True)
@@ -236,14 +237,16 @@ def make_relevance(wl: Workload, seed: int, hidden: int, device="cpu") -> dict:
     return dict(w1=w1, b1=b1.contiguous(), w2=w2, b2=b2.contiguous(), hidden=hidden)
 
 
-def make_fusion(wl: Workload, seed: int, d_ff: int, device="cpu") -> dict:
+def make_fusion(wl: Workload, seed: int, d_ff: int, device="cpu", layers=None) -> dict:
     """Seeded SwiGLU fusion weights per layer (Eq. 10; the paper trains
     them): W_gate, W_up [L, d_ff, d_v] ~ N(0, 1/d_v) and W_down [L, d_h, d_ff]
-    ~ N(0, 1/d_ff), in the workload's dtype."""
+    ~ N(0, 1/d_ff), in the workload's dtype; L = ``layers`` or the
+    workload's layer count (at most 10)."""
     dev = torch.device(device)
     dt = TORCH_DTYPE[wl.dtype]
     base = 1000 * seed
-    L = wl.layers
+    L = layers or wl.layers
+    assert L <= 10
     gate = torch.empty((L, d_ff, wl.d_v), dtype=dt, device=dev)
     up = torch.empty((L, d_ff, wl.d_v), dtype=dt, device=dev)
     down = torch.empty((L, wl.d_h, d_ff), dtype=dt, device=dev)
@@ -252,3 +255,19 @@ def make_fusion(wl: Workload, seed: int, d_ff: int, device="cpu") -> dict:
         up[l] = _randn_rows(d_ff, wl.d_v, base + TID_FUS_UP + l, dev, 1.0 / math.sqrt(wl.d_v), dt)
         down[l] = _randn_rows(wl.d_h, d_ff, base + TID_FUS_DOWN + l, dev, 1.0 / math.sqrt(d_ff), dt)
     return dict(w_gate=gate, w_up=up, w_down=down, d_ff=d_ff)
+
+
+def make_propagation(wl: Workload, seed: int, steps: int, device="cpu") -> torch.Tensor:
+    """Seeded propagation projections of Eq. 11 (trained in the paper), one
+    per propagated layer (at most 10): W_p ~ N(0, 1/(4 d_v)), returned
+    transposed (output-row-major) as w_p_t [steps, d_v, d_v] in the
+    workload's dtype; the residual keeps R's scale within a factor of about
+    1.1 a step."""
+    assert 1 <= steps <= 10
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[wl.dtype]
+    out = torch.empty((steps, wl.d_v, wl.d_v), dtype=dt, device=dev)
+    for j in range(steps):
+        out[j] = _randn_rows(wl.d_v, wl.d_v, 1000 * seed + TID_PROP + j, dev,
+                             0.5 / math.sqrt(wl.d_v), dt)
+    return out

@@ -126,6 +126,56 @@ class FusedRun(Run):
         return self
 
 
+class PropagatedRun(Run):
+    """A LookME layer followed by ``steps`` non-LookME layers (Eq. 11): the
+    first layer's route, lookup and kept set, then lookme_inject_propagated
+    into the hidden states of all steps + 1 layers (the workload's layer
+    count)."""
+
+    def __init__(self, inp: dict, fus: dict, w_p_t: torch.Tensor, **kw):
+        super().__init__(inp, **kw)
+        self.fus, self.w_p_t = fus, w_p_t
+        self.steps = self.L - 1
+        self.table.set_fusion(fus["w_gate"], fus["w_up"], fus["w_down"])
+        if self.steps > 0:
+            self.table.set_propagation(w_p_t)
+
+    def run(self):
+        inp, st = self.inp, self.stream
+        self.table.route(inp["x"], inp["wt"][:1], self.q[:1], self.scene[:1], layers=1, stream=st)
+        self.table.lookup(self.q[:1], self.scene[:1], self.prim[:1], self.w[:1], layers=1,
+                          stream=st)
+        self.table.select(inp["delta"][:1], self.kept[:1], self.n_keep, layers=1, stream=st)
+        self.table.inject_propagated(self.kept[0], self.scene[0], self.prim[0], self.w[0],
+                                     self.hidden, self.n_keep, self.steps, stream=st)
+        return self
+
+
+def check_propagated_run(r: PropagatedRun, tokens=None) -> C.Report:
+    """The LookME layer's kept set in full and every layer's injected rows on
+    the sampled tokens."""
+    torch.cuda.synchronize()
+    inp, fus = r.inp, r.fus
+    dt = dtype_name(inp["x"])
+    rep = C.Report()
+    toks = np.arange(r.n) if tokens is None else np.asarray(tokens)
+    tsel = torch.as_tensor(toks, device=r.dev)
+    values = inp["values"]
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    c = O.criticality(f64(inp["delta"][0]))
+    kept = to_np(r.kept[0])[: r.n_keep]
+    C.check_kept(c, r.n_keep, kept, rep)
+    w_p = f64(r.w_p_t[: r.steps]).transpose(0, 2, 1) if r.steps else np.zeros((0, 1, 1))
+    C.check_propagated_hidden(to_np(r.h_in[:, tsel]), to_np(r.hidden[:, tsel]), dt, values_rows,
+                              r.P, to_np(r.scene[0]), to_np(r.prim[0]), to_np(r.w[0]), kept, w_p,
+                              f64(fus["w_gate"]), f64(fus["w_up"]), f64(fus["w_down"]), rep, toks)
+    return rep.finish()
+
+
 def check_fused_run(r: FusedRun, tokens=None) -> C.Report:
     """The kept set in full and the fused injection on the sampled tokens
     (routing and lookup are checked by check_run and are the same here)."""

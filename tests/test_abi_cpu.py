@@ -219,6 +219,38 @@ def test_fusion_entry_points_validate(lib):
         lk.lookme_destroy(h)
 
 
+def test_propagation_entry_points_validate(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        call = lambda steps, n=8, n_keep=2, d_h=2048, p=FAKE: lk.lookme_inject_propagated(
+            h, steps, n, n_keep, p, p, p, p, p, d_h, 0)
+        assert S(lambda: call(1)) == lk.LOOKME_ERR_INVALID          # no fusion
+        assert S(lambda: lk.lookme_set_propagation(h, 0, FAKE)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_propagation(h, 2, None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_fusion(h, 3, 2048, 2048, FAKE, FAKE, FAKE)) == lk.LOOKME_OK
+        assert S(lambda: call(-1)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(1)) == lk.LOOKME_ERR_INVALID          # no projections
+        assert S(lambda: lk.lookme_set_propagation(h, 2, FAKE)) == lk.LOOKME_OK
+        assert S(lambda: call(3)) == lk.LOOKME_ERR_INVALID          # 4 layers > fusion's 3
+        assert S(lambda: call(2, d_h=1024)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(2, n_keep=9)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(2, n_keep=0, p=None)) == lk.LOOKME_OK
+        assert S(lambda: call(2, p=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(2)) == lk.LOOKME_ERR_WORKSPACE
+        f32 = _desc(dtype=lk.LOOKME_F32, key_dim=512, value_dim=40, prims_per_scene=64,
+                    top_k=4, num_scenes=16)
+        h2 = lk.lookme_create(f32, FAKE, FAKE, FAKE)
+        try:   # 160-byte rows: not whole 128-byte stages
+            assert S(lambda: lk.lookme_set_propagation(h2, 1, FAKE)) == lk.LOOKME_ERR_UNSUPPORTED
+        finally:
+            lk.lookme_destroy(h2)
+    finally:
+        lk.lookme_destroy(h)
+
+
 def test_null_handle(lib):
     assert _status(lambda: lk.lookme_workspace_size(None, 1, 1))[0] == lk.LOOKME_ERR_INVALID
     assert _status(lambda: lk.lookme_route(None, 1, 1, 1, FAKE, FAKE, FAKE, FAKE, 0))[0] == \

@@ -181,3 +181,39 @@ def test_relevance_checks_accept_the_oracle_and_reject_planted_errors():
     rep = C.Report()
     C.check_relevance_hidden(a_bad, q, scene, keys, w1, b1, "f32", rep)
     assert not rep.ok
+
+
+def test_propagated_check_accepts_the_oracle_and_rejects_planted_errors():
+    """check_propagated_hidden on bf16 data: the oracle's own result passes;
+    a result built with W_p transposed, or with an untouched row changed,
+    fails."""
+    rng = np.random.default_rng(9)
+    n, S, P, d_v, d_ff, d_h, k, steps = 12, 3, 6, 16, 8, 10, 2, 2
+    bf = lambda a: O.round_to_dtype(a, "bf16")
+    H = bf(rng.standard_normal((steps + 1, n, d_h)))
+    V = bf(rng.standard_normal((S * P, d_v)))
+    scene = rng.integers(0, S, n)
+    prim = np.stack([rng.permutation(P)[:k] for _ in range(n)])
+    w = np.full((n, k), 0.5)
+    kept = np.array([1, 5, 6, 11])
+    wp = bf(rng.standard_normal((steps, d_v, d_v)) * 0.5)
+    wg = bf(rng.standard_normal((steps + 1, d_ff, d_v)))
+    wu = bf(rng.standard_normal((steps + 1, d_ff, d_v)))
+    wd = bf(rng.standard_normal((steps + 1, d_h, d_ff)))
+    bits = O.f64_to_bf16_bits
+    toks = np.arange(n)
+
+    def check(out):
+        rep = C.Report()
+        C.check_propagated_hidden(bits(H), bits(out), "bf16", lambda rows: V[rows], P, scene,
+                                  prim, w, kept, wp, wg, wu, wd, rep, toks)
+        return rep.finish()
+
+    good = O.inject_propagated(H, V, P, scene, prim, w, kept, wp, wg, wu, wd, "bf16")
+    assert check(good).ok
+    transposed = O.inject_propagated(H, V, P, scene, prim, w, kept, wp.transpose(0, 2, 1), wg,
+                                     wu, wd, "bf16")
+    assert not check(transposed).ok
+    touched = good.copy()
+    touched[2, 0, 3] = bf(touched[2, 0, 3] + 1.0)
+    assert not check(touched).ok

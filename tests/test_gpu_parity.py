@@ -13,7 +13,7 @@ import torch
 
 from oracle import lookme_oracle as O
 from synth import (WORKLOADS, Workload, make_fusion, make_inputs, make_integer_inputs,
-                   make_relevance)
+                   make_propagation, make_relevance)
 
 pytestmark = pytest.mark.gpu
 
@@ -299,6 +299,76 @@ def test_fused_injection(name):
     r2 = FusedRun(inp, fus, table=r.table).run()
     torch.cuda.synchronize()
     assert torch.equal(r.hidden, r2.hidden)
+
+
+# layers = the LookME layer + the propagated ones
+PROPAGATION = {
+    "bf16_prop_small": (Workload("bf16_prop_small", "bf16", 300, 3, 256, 128, 20, 60, 128, 80,
+                                 8, 30, usage="uniform", value_std=1.0), 192, None),
+    "f32_prop": (Workload("f32_prop", "f32", 77, 2, 96, 64, 5, 37, 64, 48, 3, 15, usage="iid",
+                          value_std=1.0), 96, None),
+    "bf16_prop_image": (WORKLOADS[1].scaled(layers=4, value_std=1.0), 2048, 80),
+}
+
+
+def _sample_with_kept(r, wl, sample, seed):
+    if not sample:
+        return None
+    kept0 = r.kept[0].cpu().numpy()[:40]
+    return np.unique(np.concatenate(
+        [np.random.default_rng(seed).choice(wl.n_tokens, sample, replace=False), kept0]))
+
+
+@pytest.mark.parametrize("name", list(PROPAGATION))
+def test_propagated_injection(name):
+    """One lookup and kept set at the LookME layer, R carried through the
+    propagation of Eq. 11 to the layers after it, each injected through its
+    own fusion: against the oracle's chain on the library's primitives and
+    weights; two passes agree bit for bit."""
+    from tests.harness import PropagatedRun, check_propagated_run
+    wl, d_ff, sample = PROPAGATION[name]
+    _announce(f"propagation {name}: {wl} d_ff {d_ff}")
+    inp = make_inputs(wl, seed=7, device=DEV)
+    fus = make_fusion(wl, 7, d_ff, device=DEV)
+    w_p_t = make_propagation(wl, 7, wl.layers - 1, device=DEV)
+    r = PropagatedRun(inp, fus, w_p_t).run()
+    rep = check_propagated_run(r, tokens=_sample_with_kept(r, wl, sample, 7))
+    assert rep.ok, str(rep)
+    assert rep.decisions.get("hidden_row", 0) > 0
+    r2 = PropagatedRun(inp, fus, w_p_t, table=r.table).run()
+    torch.cuda.synchronize()
+    assert torch.equal(r.hidden, r2.hidden)
+
+
+def test_propagated_special_cases_match_fused_injection():
+    """No steps: the same bits as lookme_inject_fused on one layer.  W_p = 0:
+    every R_j is R_0 exactly, so layer j gets the bits of lookme_inject_fused
+    over three layers that all carry the LookME layer's lookup and kept set."""
+    from tests.harness import FusedRun, PropagatedRun
+    wl = Workload("bf16_prop_eq", "bf16", 300, 3, 256, 128, 20, 60, 128, 80, 8, 30,
+                  usage="uniform", value_std=1.0)
+    _announce(f"propagation special cases: {wl}")
+    inp = make_inputs(wl, seed=8, device=DEV)
+    fus = make_fusion(wl, 8, 192, device=DEV)
+    zeros = torch.zeros((2, wl.d_v, wl.d_v), dtype=torch.bfloat16, device=DEV)
+    r = PropagatedRun(inp, fus, zeros).run()
+    n_keep = r.n_keep
+    rep3 = lambda t: t[:1].expand(3, *t.shape[1:]).contiguous()
+    hidden = inp["hidden"].clone()
+    r.table.inject_fused(rep3(r.kept), rep3(r.scene), rep3(r.prim), rep3(r.w), hidden, n_keep,
+                         layers=3)
+    torch.cuda.synchronize()
+    assert torch.equal(r.hidden, hidden)
+    assert not torch.equal(r.hidden[2], inp["hidden"][2])
+
+    one = {k: (v[:1].contiguous() if k in ("wt", "delta", "hidden") else v)
+           for k, v in inp.items()}
+    fus1 = {k: (v[:1].contiguous() if torch.is_tensor(v) else v) for k, v in fus.items()}
+    p0 = PropagatedRun(one, fus1, zeros).run()
+    f0 = FusedRun(one, fus1).run()
+    torch.cuda.synchronize()
+    assert p0.steps == 0
+    assert torch.equal(p0.hidden, f0.hidden)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])

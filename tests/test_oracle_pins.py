@@ -650,3 +650,91 @@ def test_fusion_inner_unit_relabelling_invariance():
     perm = rng.permutation(5)
     np.testing.assert_allclose(O.fusion(R, wg[perm], wu[perm], wd[:, perm], "f32"),
                                O.fusion(R, wg, wu, wd, "f32"), rtol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# Inter-layer propagation (Eq. 11)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_propagate_matches_brute_force(dtype):
+    """Three steps against exact rational loops with one rounding per step:
+    catches a transposed W_p, a missing residual, a missing or doubled
+    rounding between steps and steps applied out of order."""
+    rng = np.random.default_rng(53)
+    m, d_v, steps = 3, 6, 3
+    rnd = _bf16_values if dtype == "bf16" else (lambda r, sh, sc=1.0: r.standard_normal(sh) * sc)
+    R = O.round_to_dtype(rnd(rng, (m, d_v)), dtype)
+    wp = rnd(rng, (steps, d_v, d_v), 0.6)
+    chain = O.propagate(R, wp, dtype)
+    ref = B.propagate_rows(R.tolist(), [w.tolist() for w in wp], 8 if dtype == "bf16" else 24)
+    assert chain.shape == (steps + 1, m, d_v)
+    for j in range(steps + 1):
+        np.testing.assert_array_equal(chain[j], np.array([[float(v) for v in row]
+                                                          for row in ref[j]]))
+
+
+def test_propagate_orientation_and_order():
+    """W_p^1 moves input 0 into output 1 and W_p^2 input 1 into output 2 (a
+    matrix indexed [input, output], applied as R W_p): R_1[1] = R_0[1] + R_0[0]
+    and R_2[2] = R_0[2] + R_0[1] + R_0[0], every other column unchanged; the
+    transposed or reversed chain gives other sums."""
+    R = np.array([[1.0, 2.0, 4.0, 8.0], [-3.0, 5.0, 0.5, 1.0]])
+    wp = np.zeros((2, 4, 4))
+    wp[0, 0, 1] = 1.0
+    wp[1, 1, 2] = 1.0
+    chain = O.propagate(R, wp, "f32")
+    r1 = R.copy()
+    r1[:, 1] = R[:, 1] + R[:, 0]
+    r2 = r1.copy()
+    r2[:, 2] = R[:, 2] + R[:, 1] + R[:, 0]
+    np.testing.assert_array_equal(chain[0], R)
+    np.testing.assert_array_equal(chain[1], r1)
+    np.testing.assert_array_equal(chain[2], r2)
+
+
+def _prop_case(rng, n=10, S=2, P=5, d_v=4, d_ff=3, d_h=6, k=2, steps=2):
+    H = _bf16_values(rng, (steps + 1, n, d_h))
+    V = _bf16_values(rng, (S * P, d_v))
+    scene = rng.integers(0, S, n)
+    prim = np.stack([rng.permutation(P)[:k] for _ in range(n)])
+    w = np.full((n, k), 0.5)
+    kept = np.array([0, 3, 8])
+    wg = _bf16_values(rng, (steps + 1, d_ff, d_v))
+    wu = _bf16_values(rng, (steps + 1, d_ff, d_v))
+    wd = _bf16_values(rng, (steps + 1, d_h, d_ff))
+    return H, V, P, scene, prim, w, kept, wg, wu, wd
+
+
+def test_propagate_minus_identity_cancels():
+    """W_p = -I gives R_1 = R_0 - R_0 = 0 exactly and f(0) = 0, so the
+    propagated layer keeps its bits while the LookME layer's kept rows move;
+    rows outside the kept set keep theirs in every layer (the gate of the
+    LookME layer is reused, Eq. 11)."""
+    rng = np.random.default_rng(54)
+    H, V, P, scene, prim, w, kept, wg, wu, wd = _prop_case(rng, steps=1)
+    wp = -np.eye(V.shape[1])[None]
+    assert np.array_equal(O.propagate(np.ones((2, V.shape[1])), wp, "bf16")[1], np.zeros((2, 4)))
+    out = O.inject_propagated(H, V, P, scene, prim, w, kept, wp, wg, wu, wd, "bf16")
+    assert np.array_equal(out[1], H[1])
+    assert not np.array_equal(out[0, kept], H[0, kept])
+    others = np.setdiff1d(np.arange(H.shape[1]), kept)
+    assert np.array_equal(out[:, others], H[:, others])
+
+
+def test_inject_propagated_special_cases_reduce_to_inject_fused():
+    """No steps: the LookME layer alone, i.e. inject_fused on one layer.
+    W_p = 0 at every step: R_j = R_0, so layer j is inject_fused with f_j
+    on the LookME layer's lookup and kept set."""
+    rng = np.random.default_rng(55)
+    H, V, P, scene, prim, w, kept, wg, wu, wd = _prop_case(rng, steps=2)
+    d_v = V.shape[1]
+    out0 = O.inject_propagated(H[:1], V, P, scene, prim, w, kept, np.zeros((0, d_v, d_v)),
+                               wg, wu, wd, "bf16")
+    np.testing.assert_array_equal(
+        out0[0], O.inject_fused(H[0], V, P, scene, prim, w, kept, wg[0], wu[0], wd[0], "bf16"))
+    out = O.inject_propagated(H, V, P, scene, prim, w, kept, np.zeros((2, d_v, d_v)),
+                              wg, wu, wd, "bf16")
+    for j in range(3):
+        np.testing.assert_array_equal(
+            out[j], O.inject_fused(H[j], V, P, scene, prim, w, kept, wg[j], wu[j], wd[j], "bf16"))
