@@ -4,10 +4,9 @@
 // output tiles, 4 waves in 2 x 2 (each 2 x 2 MFMA tiles), K in 128-byte
 // stages loaded straight into LDS (dtl.h), a ring of NS stages, NS - 1 in
 // flight while one is multiplied.  These products have few rows and long K,
-// so the loads' latency, not the matrix cores, sets the pace: a small grid
-// takes a ring of 4 (64 KB of LDS, 2 workgroups a CU), a grid that would not
-// fit the chip at that occupancy a ring of 2 (32 KB, up to 5 a CU); see
-// launch_tile_gemm.
+// so the bytes in flight per CU over the loads' latency, not the matrix
+// cores, set the pace: the ring is as deep as the grid's occupancy allows
+// (launch_tile_gemm).
 // blockIdx.y selects a batch (a layer) whose A, B and output start a fixed
 // stride further.  Epilogues:
 //
@@ -22,6 +21,7 @@
 //
 // An A row may take its first `ksplit` stages from a0 and the rest from a
 // gathered row of a1 (the relevance MLP's [query ; scene key] input).
+
 #pragma once
 
 #include "common.h"
@@ -51,126 +51,48 @@ struct TileGemmParams {
   int64_t n, kept_batch;    // EPI_RESID: tokens per layer, stride of the kept lists
   int64_t out_ld;           // EPI_RESID: bytes of an H row
   int sel_rows, cols, ksplit, tiles;
+  int col_major;            // tile ids run down the row tiles of a column block first
 };
+
+// Origin of tile `tile`: row tiles of one column block are consecutive ids
+// when col_major (so they land on one XCD and share its L2 copy of the B
+// rows, which the larger operand then crosses HBM once), else the column
+// tiles of one row block.
+__device__ __forceinline__ void tile_origin(const TileGemmParams& a, int tile, int tcols,
+                                            int64_t* m0, int* n0) {
+  if (a.col_major) {
+    const int tiles_m = (int)((a.rows + TgShape::BM - 1) / TgShape::BM);
+    *m0 = (int64_t)(tile % tiles_m) * TgShape::BM;
+    *n0 = (tile / tiles_m) * tcols;
+  } else {
+    const int tiles_n = (a.cols + tcols - 1) / tcols;
+    *m0 = (int64_t)(tile / tiles_n) * TgShape::BM;
+    *n0 = (tile % tiles_n) * tcols;
+  }
+}
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
 
-template <int DT, int EPI, int NS>
-__global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
+// Epilogue of a 64 x 64 tile (tile index `tile` of batch z) from the
+// accumulators of thread tid: the lane holds rows m0 + wm + 16 i + 4 g + r and
+// tile columns wn + 16 j + n16.  xch: 4096 floats of LDS (EPI_SWIGLU only).
+template <int DT, int EPI>
+__device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (&acc)[2][2],
+                                              int64_t z, int tile, int tid, float* xch) {
   using S = TgShape;
-  constexpr int MI = 2, NJ = 2, KB = TG_KB, KSL = KB / 64, WN = 2;
+  constexpr int MI = 2, NJ = 2, WN = 2;
   constexpr int ES = DT == DT_BF16 ? 2 : 4;
-  constexpr int TCOLS = EPI == EPI_SWIGLU ? S::BN / 2 : S::BN;   // output columns a tile
-  static_assert(NS >= 2, "a stage in flight while one is multiplied");
-  __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  constexpr int TCOLS = EPI == EPI_SWIGLU ? S::BN / 2 : S::BN;
+  const int lane = tid & 63, wv = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
   const int wm = (wv / WN) * 16 * MI, wn = (wv % WN) * 16 * NJ;
-  const int64_t z = blockIdx.y;
-
-  const int tiles_n = (a.cols + TCOLS - 1) / TCOLS;
-  const int tile = xcd_remap(blockIdx.x, a.tiles);
-  if (tile < 0) return;
-  const int64_t m0 = (int64_t)(tile / tiles_n) * S::BM;
-  const int n0 = (tile % tiles_n) * TCOLS;
-  const int nst = (int)(a.k_bytes / KB);
-  const char* A0 = a.a0 + z * a.a_batch;
-  const char* B0 = a.b + z * a.b_batch;
-
-  // load b covers tile row trow (A rows first, then B rows); an A row takes
-  // its first ksplit stages from p0 and the rest from p1; a B row is
-  // contiguous.  Rows past the edge are clamped (their outputs are not
-  // stored).
-  const char* p0[S::PER_WAVE];
-  const char* p1[S::PER_WAVE];
-  int split[S::PER_WAVE];
-#pragma unroll
-  for (int b = 0; b < S::PER_WAVE; ++b) {
-    const int trow = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
-    const int chunk = (lane % S::LPR) ^ blk_swz<KB>(trow & 15);
-    if (trow < S::BM) {
-      int64_t r = m0 + trow;
-      r = r < a.rows ? r : a.rows - 1;
-      p0[b] = A0 + r * a.a_bytes + chunk * 16;
-      if (a.a1 != nullptr) {
-        int s = a.sel[r];
-        s = s < 0 ? 0 : (s >= a.sel_rows ? a.sel_rows - 1 : s);
-        p1[b] = a.a1 + (int64_t)s * a.a_bytes + chunk * 16;
-      } else {
-        p1[b] = p0[b] + (int64_t)a.ksplit * KB;
-      }
-      split[b] = a.ksplit;
-    } else {
-      int c = trow - S::BM;
-      const char* base = B0;
-      if constexpr (EPI == EPI_SWIGLU) {
-        // rows 0..31 of the B part: gate rows, 32..63: the same up rows
-        if (c >= TCOLS) {
-          base = a.b2 + z * a.b_batch;
-          c -= TCOLS;
-        }
-      }
-      int r = n0 + c;
-      r = r < a.cols ? r : a.cols - 1;
-      p0[b] = base + (int64_t)r * a.k_bytes + chunk * 16;
-      p1[b] = p0[b];
-      split[b] = nst;
-    }
-  }
-  auto issue = [&](int stage) {
-    const int s = stage < nst ? stage : nst - 1;   // past the end: a harmless reload
-    char* dst = lds[stage % NS];
-#pragma unroll
-    for (int b = 0; b < S::PER_WAVE; ++b) {
-      const char* src =
-          s < split[b] ? p0[b] + (int64_t)s * KB : p1[b] + (int64_t)(s - split[b]) * KB;
-      load_lds16(src, dst + (wv * S::PER_WAVE + b) * 1024);
-    }
-  };
-
-  f32x4_t acc[MI][NJ];
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-  for (int i = 0; i < NS - 1; ++i) issue(i);
-  for (int s = 0; s < nst; ++s) {
-    // this wave's loads of stage s have landed once at most those of the
-    // NS - 2 younger stages are outstanding; the barrier makes every wave's
-    // visible and ends every read of stage s - 1, whose buffer the next
-    // loads fill (a plain s_barrier: the fence of __syncthreads would wait
-    // for every load in flight)
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 2) * S::PER_WAVE) : "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    issue(s + NS - 1);
-    const char* buf = lds[s % NS];
-#pragma unroll
-    for (int ks = 0; ks < KSL; ++ks) {
-      u32x4_t fa[MI], fb[NJ];
-#pragma unroll
-      for (int i = 0; i < MI; ++i) fa[i] = read_frag<KB>(buf, wm + 16 * i, ks, n16, g);
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_chunk<DT>(fa[i], fb[j], acc[i][j]);
-    }
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
-
-  // the lane holds rows m0 + wm + 16 i + 4 g + r and tile column wn + 16 j +
-  // n16
+  int64_t m0;
+  int n0;
+  tile_origin(a, tile, TCOLS, &m0, &n0);
   if constexpr (EPI == EPI_SWIGLU) {
-    // the up half (waves with wn = 32) passes its tile through the idle
-    // stage buffer to the gate half (wn = 0) of the same rows
-    float* xch = reinterpret_cast<float*>(&lds[0][0]);
-    __syncthreads();   // every wave is done with the stage buffers
+    // the up half (waves with wn = 32) passes its tile through LDS to the
+    // gate half (wn = 0) of the same rows
+    __syncthreads();   // every wave is done with the LDS the exchange reuses
     if (wn != 0) {
 #pragma unroll
       for (int i = 0; i < MI; ++i)
@@ -203,66 +125,233 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
         }
     }
   } else {
+    // every load (biases, kept rows, H or residual values) is issued before
+    // the first store: as far as the compiler knows a store may alias a later
+    // load, which would otherwise serialise the elements one round trip each.
+    // The loads are unconditional, from addresses clamped into the operands
+    // (a load under a branch gets a wait of its own where the paths meet).
+    int col[NJ], ccol[NJ];
+    float bias[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      const int col = n0 + wn + 16 * j + n16;
-      if (col >= a.cols) continue;
-      const float bias =
-          (EPI == EPI_ACT || EPI == EPI_LOGIT) && a.bias != nullptr ? a.bias[col] : 0.f;
+      col[j] = n0 + wn + 16 * j + n16;
+      ccol[j] = col[j] < a.cols ? col[j] : a.cols - 1;
+      bias[j] = 0.f;
+      if constexpr (EPI == EPI_ACT || EPI == EPI_LOGIT)
+        if (a.bias != nullptr) bias[j] = a.bias[ccol[j]];
+    }
+    int64_t orow[MI][4];   // output row: the tile row, or (EPI_RESID) its H row
+    bool rok[MI][4];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = m0 + wm + 16 * i + 4 * g + r;
+        rok[i][r] = row < a.rows;
+        orow[i][r] = rok[i][r] ? row : a.rows - 1;
+        if constexpr (EPI == EPI_RESID) {
+          int64_t t = a.kept[z * a.kept_batch + orow[i][r]];
+          t = t < 0 ? 0 : (t >= a.n ? a.n - 1 : t);
+          orow[i][r] = z * a.n + t;
+        }
+      }
+    float old[NJ][MI][4];   // EPI_RESID: H, EPI_ADD: the residual
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int64_t row = m0 + wm + 16 * i + 4 * g + r;
-          if (row >= a.rows) continue;
-          const float c = acc[i][j][r] + bias;
-          if constexpr (EPI == EPI_LOGIT) {
-            reinterpret_cast<float*>(a.out)[row * a.cols + col] = c;
-          } else if constexpr (EPI == EPI_ACT) {
-            char* dst = a.out + (row * a.cols + col) * ES;
+          old[j][i][r] = 0.f;
+          if constexpr (EPI == EPI_RESID || EPI == EPI_ADD) {
+            const char* src = EPI == EPI_RESID
+                                  ? a.out + orow[i][r] * a.out_ld + (int64_t)ccol[j] * ES
+                                  : a.res + (orow[i][r] * a.cols + ccol[j]) * ES;
             if constexpr (DT == DT_BF16)
-              *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16_rne(fmaxf(c, 0.f));
+              old[j][i][r] = bf16lo(*reinterpret_cast<const uint16_t*>(src));
             else
-              *reinterpret_cast<float*>(dst) = fmaxf(c, 0.f);
-          } else if constexpr (EPI == EPI_ADD) {
-            const int64_t at = (row * a.cols + col) * ES;
-            if constexpr (DT == DT_BF16)
-              *reinterpret_cast<uint16_t*>(a.out + at) = (uint16_t)f32_to_bf16_rne(
-                  bf16lo(*reinterpret_cast<const uint16_t*>(a.res + at)) + c);
-            else
-              *reinterpret_cast<float*>(a.out + at) = *reinterpret_cast<const float*>(a.res + at) + c;
-          } else {   // EPI_RESID
-            int64_t t = a.kept[z * a.kept_batch + row];
-            t = t < 0 ? 0 : (t >= a.n ? a.n - 1 : t);
-            char* dst = a.out + (z * a.n + t) * a.out_ld + (int64_t)col * ES;
-            if constexpr (DT == DT_BF16) {
-              uint16_t* h = reinterpret_cast<uint16_t*>(dst);
-              *h = (uint16_t)f32_to_bf16_rne(bf16lo(*h) + c);
-            } else {
-              float* h = reinterpret_cast<float*>(dst);
-              *h = *h + c;
-            }
+              old[j][i][r] = *reinterpret_cast<const float*>(src);
           }
+        }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      if (col[j] >= a.cols) continue;
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (!rok[i][r]) continue;
+          const float c = acc[i][j][r] + bias[j];
+          if constexpr (EPI == EPI_LOGIT) {
+            reinterpret_cast<float*>(a.out)[orow[i][r] * a.cols + col[j]] = c;
+            continue;
+          }
+          float v;
+          char* dst;
+          if constexpr (EPI == EPI_ACT) {
+            v = fmaxf(c, 0.f);
+            dst = a.out + (orow[i][r] * a.cols + col[j]) * ES;
+          } else if constexpr (EPI == EPI_ADD) {
+            v = old[j][i][r] + c;
+            dst = a.out + (orow[i][r] * a.cols + col[j]) * ES;
+          } else {   // EPI_RESID
+            v = old[j][i][r] + c;
+            dst = a.out + orow[i][r] * a.out_ld + (int64_t)col[j] * ES;
+          }
+          if constexpr (DT == DT_BF16)
+            *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16_rne(v);
+          else
+            *reinterpret_cast<float*>(dst) = v;
         }
     }
   }
 }
 
-// Launches the product over `batches` batches (blockIdx.y) with the ring
-// depth for its grid: 4 stages while every workgroup is resident at 2 a CU
-// (at most 512 over the chip's 256 CUs), else 2.
+template <int DT, int EPI, int NS>
+__global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
+  using S = TgShape;
+  constexpr int MI = 2, NJ = 2, KB = TG_KB, KSL = KB / 64, WN = 2;
+  constexpr int TCOLS = EPI == EPI_SWIGLU ? S::BN / 2 : S::BN;   // output columns a tile
+  static_assert(NS >= 2, "a stage in flight while one is multiplied");
+  __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n16 = lane & 15, g = lane >> 4;
+  const int wm = (wv / WN) * 16 * MI, wn = (wv % WN) * 16 * NJ;
+  const int64_t z = blockIdx.y;
+
+  const int tile = xcd_remap(blockIdx.x, a.tiles);
+  if (tile < 0) return;
+  int64_t m0;
+  int n0;
+  tile_origin(a, tile, TCOLS, &m0, &n0);
+  const int nst = (int)(a.k_bytes / KB);
+  const char* A0 = a.a0 + z * a.a_batch;
+  const char* B0 = a.b + z * a.b_batch;
+
+  // load b covers tile row trow (A rows first, then B rows); an A row takes
+  // its first ksplit stages from p0 and the rest from p1; a B row is
+  // contiguous.  Rows past the edge are clamped (their outputs are not
+  // stored).
+  const char* p0[S::PER_WAVE];
+  const char* p1[S::PER_WAVE];
+  int split_at[S::PER_WAVE];
+  int sel[S::PER_WAVE];   // gathered a1 rows, loaded together (one branch, no wait each)
+  if (a.a1 != nullptr) {
+#pragma unroll
+    for (int b = 0; b < S::PER_WAVE; ++b) {
+      const int trow = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
+      int64_t r = m0 + (trow < S::BM ? trow : 0);
+      r = r < a.rows ? r : a.rows - 1;
+      sel[b] = a.sel[r];
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < S::PER_WAVE; ++b) {
+    const int trow = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
+    const int chunk = (lane % S::LPR) ^ blk_swz<KB>(trow & 15);
+    if (trow < S::BM) {
+      int64_t r = m0 + trow;
+      r = r < a.rows ? r : a.rows - 1;
+      p0[b] = A0 + r * a.a_bytes + chunk * 16;
+      if (a.a1 != nullptr) {
+        int s = sel[b];
+        s = s < 0 ? 0 : (s >= a.sel_rows ? a.sel_rows - 1 : s);
+        p1[b] = a.a1 + (int64_t)s * a.a_bytes + chunk * 16;
+      } else {
+        p1[b] = p0[b] + (int64_t)a.ksplit * KB;
+      }
+      split_at[b] = a.ksplit;
+    } else {
+      int c = trow - S::BM;
+      const char* base = B0;
+      if constexpr (EPI == EPI_SWIGLU) {
+        // rows 0..31 of the B part: gate rows, 32..63: the same up rows
+        if (c >= TCOLS) {
+          base = a.b2 + z * a.b_batch;
+          c -= TCOLS;
+        }
+      }
+      int r = n0 + c;
+      r = r < a.cols ? r : a.cols - 1;
+      p0[b] = base + (int64_t)r * a.k_bytes + chunk * 16;
+      p1[b] = p0[b];
+      split_at[b] = nst;
+    }
+  }
+  auto issue = [&](int i) {
+    const int s = i < nst ? i : nst - 1;   // past the end: a harmless reload
+    char* dst = lds[i % NS];
+#pragma unroll
+    for (int b = 0; b < S::PER_WAVE; ++b) {
+      const char* src = s < split_at[b] ? p0[b] + (int64_t)s * KB
+                                        : p1[b] + (int64_t)(s - split_at[b]) * KB;
+      load_lds16(src, dst + (wv * S::PER_WAVE + b) * 1024);
+    }
+  };
+
+  f32x4_t acc[MI][NJ];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i) issue(i);
+  for (int i = 0; i < nst; ++i) {
+    // this wave's loads of stage i have landed once at most those of the
+    // NS - 2 younger stages are outstanding; the barrier makes every wave's
+    // visible and ends every read of stage i - 1, whose buffer the next
+    // loads fill (a plain s_barrier: the fence of __syncthreads would wait
+    // for every load in flight)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 2) * S::PER_WAVE) : "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(i + NS - 1);
+    const char* buf = lds[i % NS];
+#pragma unroll
+    for (int ks = 0; ks < KSL; ++ks) {
+      u32x4_t fa[MI], fb[NJ];
+#pragma unroll
+      for (int ii = 0; ii < MI; ++ii) fa[ii] = read_frag<KB>(buf, wm + 16 * ii, ks, n16, g);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
+#pragma unroll
+      for (int ii = 0; ii < MI; ++ii)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[ii][j] = mfma_chunk<DT>(fa[ii], fb[j], acc[ii][j]);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
+
+  tile_epilogue<DT, EPI>(a, acc, z, tile, tid, reinterpret_cast<float*>(&lds[0][0]));
+}
+
+// Launches the product over `batches` batches (blockIdx.y), tiles in the
+// order that keeps the larger operand's rows on one XCD, with the deepest
+// ring its grid's occupancy allows: 8 stages (128 KB of LDS) while every
+// workgroup has a CU of its own (at most 256), 4 (64 KB) while all are
+// resident at 2 a CU (at most 512), else 2 (32 KB, up to 5 a CU).
 template <int EPI>
-hipError_t launch_tile_gemm(int dt, const TileGemmParams& p, int batches, hipStream_t st) {
+hipError_t launch_tile_gemm(int dt, TileGemmParams p, int batches, hipStream_t st) {
+  // column-major tile order when B has at least as many rows as A
+  p.col_major = (int64_t)p.cols * (EPI == EPI_SWIGLU ? 2 : 1) >= p.rows;
   const unsigned gx = (unsigned)((p.tiles + 7) / 8 * 8);
   const dim3 grid(gx, (unsigned)batches);
-  const bool deep = (int64_t)gx * batches <= 512;
+  const int64_t wgs = (int64_t)gx * batches;
+  const int ns = wgs <= 256 ? 8 : (wgs <= 512 ? 4 : 2);
   if (dt == DT_BF16) {
-    if (deep)
+    if (ns == 8)
+      hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI, 8>), grid, dim3(256), 0, st, p);
+    else if (ns == 4)
       hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI, 4>), grid, dim3(256), 0, st, p);
     else
       hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI, 2>), grid, dim3(256), 0, st, p);
   } else {
-    if (deep)
+    if (ns == 8)
+      hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI, 8>), grid, dim3(256), 0, st, p);
+    else if (ns == 4)
       hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI, 4>), grid, dim3(256), 0, st, p);
     else
       hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI, 2>), grid, dim3(256), 0, st, p);
