@@ -211,3 +211,28 @@ def propagate_rows(r_rows, w_p_mats, mant_bits):
             nxt.append(row)
         chain.append(nxt)
     return chain
+
+
+def multiscale_rows(h_rows, w_he_rows, r_scale_rows, mant_bits):
+    """Eq. 8 by plain loops for each token: q = round(h W_{h->e}) exactly
+    rounded, logits (q . R^m) / sqrt(d) as exact rationals evaluated in
+    floating point, alpha by repeated max subtraction, then sum_m alpha_m R^m
+    as rationals.  h_rows [t][d_h], w_he_rows [d_h][d_v] (input index first),
+    r_scale_rows [t][M][d_v].  Returns rationals [t][d_v]."""
+    out = []
+    for h, rs in zip(h_rows, r_scale_rows):
+        d_v = len(rs[0])
+        q = []
+        for o in range(d_v):
+            acc = Fraction(0)
+            for i in range(len(h)):
+                acc += Fraction(h[i]) * Fraction(w_he_rows[i][o])
+            q.append(round_fraction(acc, mant_bits))
+        logits = [float(dot(q, r)) / math.sqrt(d_v) for r in rs]
+        top = max(logits)
+        e = [math.exp(v - top) for v in logits]
+        tot = sum(e)
+        alpha = [Fraction(v / tot) for v in e]
+        out.append([sum((a * Fraction(r[c]) for a, r in zip(alpha, rs)), Fraction(0))
+                    for c in range(d_v)])
+    return out

@@ -31,6 +31,10 @@ What is computed, step by step (each function cites its passage):
   propagate   Eq. 11 (inter-layer sparse activation): a non-LookME layer k
               after LookME layer l carries R^(k) = R^(k-1) W_p^k + R^(k-1)
               and reuses layer l's gate; inject_propagated applies f^k to it
+  multiscale  Sec. 3.2 "Multi-scale image retrieval", Eq. 8: M scales, each
+              routed and looked up in its own scene partition of the table;
+              a token-wise softmax router over the M retrieved rows, queried
+              by the token's hidden state through W_{h->e}, mixes them
   relevance_* Level-2 in the paper's own form (Eq. 6-7): a scene-shared
               two-layer MLP over [v_e, e_img[j]] gives relevance logits r_j;
               the top-k primitives by r are weighted by the softmax of
@@ -316,6 +320,68 @@ def inject_propagated(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.
         F = fusion(Rs[j], w_gate[j], w_up[j], w_down[j], dtype)
         out[j, kept] = round_to_dtype(hidden[j, kept] + F, dtype)
     return out
+
+
+def multiscale_mix(q: np.ndarray, r_scales: np.ndarray) -> np.ndarray:
+    """Eq. 8's router for one token: alpha = softmax over the M scales of
+    (q . R^m) / sqrt(d), d the width of q and of the rows; returns
+    sum_m alpha_m R^m (float64, not rounded).  q [d], r_scales [M, d]."""
+    logits = (r_scales @ q) / np.sqrt(q.shape[0])
+    z = logits - np.max(logits)
+    alpha = np.exp(z) / np.sum(np.exp(z))
+    return alpha @ r_scales
+
+
+def inject_multiscale(hidden: np.ndarray, values: np.ndarray, P: int, scenes_per_scale: int,
+                      scene: np.ndarray, prim: np.ndarray, w: np.ndarray, kept: np.ndarray,
+                      w_he: np.ndarray, dtype: str) -> np.ndarray:
+    """Multi-scale injection (Eq. 8, then Eq. 10 and Eq. 2 in the prefix-add
+    form): scale m's lookup (scene [M, n] local to its partition, whose
+    scenes start at m * scenes_per_scale; prim, w [M, n, k]) gives the
+    retrieved row R^m_t, stored (rounded); the router query is the token's
+    hidden state projected, q_t = round(H[t] W_{h->e}); for kept tokens
+    H[t, :d_v] <- round(H[t, :d_v] + multiscale_mix(q_t, [R^1_t .. R^M_t])).
+
+    hidden [n, d_h] (the states before injection serve as the router's
+    H_img), w_he [d_h, d_v] in the paper's orientation.  Returns float64."""
+    out = np.array(hidden, dtype=np.float64, copy=True)
+    kept = np.asarray(kept, dtype=np.int64)
+    M = scene.shape[0]
+    d_v = values.shape[1]
+    for t in kept:
+        R = np.stack([
+            round_to_dtype(retrieved(values, P, m * scenes_per_scale + int(scene[m, t]),
+                                     prim[m, t], w[m, t]), dtype) for m in range(M)])
+        q = round_to_dtype(hidden[t] @ w_he, dtype)
+        out[t, :d_v] = round_to_dtype(hidden[t, :d_v] + multiscale_mix(q, R), dtype)
+    return out
+
+
+def run_multiscale(x_scales, w_t_scales, scene_keys, prim_keys, values, delta, hidden, w_he, *,
+                   k: int, n_keep: int, dtype: str):
+    """One layer's image pathway over M scales (Sec. 3.2 multi-scale
+    retrieval): scale m projects its own tokens x_scales[m] with its own W
+    and is routed and looked up within scene partition m (the S scenes split
+    evenly); the kept set comes from delta; the rows are mixed by the router
+    and injected.  x_scales [M, n, d_in], w_t_scales [M, d_e, d_in],
+    delta [n, d_c], hidden [n, d_h], w_he [d_h, d_v].  Returns a dict:
+    q [M, n, d_e], scene [M, n] (local), prim, w [M, n, k], kept [n_keep],
+    hidden [n, d_h]."""
+    M = x_scales.shape[0]
+    S, P = prim_keys.shape[0], prim_keys.shape[1]
+    if S % M:
+        raise ValueError("the scenes must split evenly over the scales")
+    Sm = S // M
+    qs, scs, prs, ws = [], [], [], []
+    for m in range(M):
+        q = project(x_scales[m], w_t_scales[m], dtype)
+        sc = route(q, scene_keys[m * Sm:(m + 1) * Sm])
+        pr, ww, _ = lookup(q, sc, prim_keys[m * Sm:(m + 1) * Sm], k)
+        qs.append(q), scs.append(sc), prs.append(pr), ws.append(ww)
+    scene, prim, w = np.stack(scs), np.stack(prs), np.stack(ws)
+    kept = select(criticality(delta), n_keep)
+    h = inject_multiscale(hidden, values, P, Sm, scene, prim, w, kept, w_he, dtype)
+    return {"q": np.stack(qs), "scene": scene, "prim": prim, "w": w, "kept": kept, "hidden": h}
 
 
 def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,

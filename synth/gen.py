@@ -40,6 +40,7 @@ TID_W, TID_DELTA, TID_H = 10, 20, 30
 TID_MLP_W1, TID_MLP_B1, TID_MLP_W2, TID_MLP_B2 = 40, 41, 42, 43
 TID_FUS_GATE, TID_FUS_UP, TID_FUS_DOWN = 50, 60, 70
 TID_PROP = 80
+TID_MS_X, TID_MS_W, TID_MS_HE = 90, 100, 110
 
 
 @dataclasses.dataclass(frozen=True)
@@ -271,3 +272,24 @@ def make_propagation(wl: Workload, seed: int, steps: int, device="cpu") -> torch
         out[j] = _randn_rows(wl.d_v, wl.d_v, 1000 * seed + TID_PROP + j, dev,
                              0.5 / math.sqrt(wl.d_v), dt)
     return out
+
+
+def make_multiscale(wl: Workload, seed: int, scales: int, device="cpu") -> dict:
+    """Seeded inputs of multi-scale retrieval (Sec. 3.2, Eq. 8) over the
+    workload's table split into ``scales`` scene partitions (at most 10):
+    per-scale tokens x [M, n, d_in] iid N(0, 1) (features of M encoder
+    layers), per-scale projections W^T [M, d_e, d_in] ~ N(0, 1/d_in) and the
+    router projection W_{h->e} stored transposed, w_he_t [d_v, d_h] ~
+    N(0, 1/d_h), in the workload's dtype (the paper trains them)."""
+    assert 1 <= scales <= 10 and wl.scenes % scales == 0
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[wl.dtype]
+    base = 1000 * seed
+    n = wl.n_tokens
+    x = torch.empty((scales, n, wl.d_in), dtype=dt, device=dev)
+    wt = torch.empty((scales, wl.d_e, wl.d_in), dtype=dt, device=dev)
+    for m in range(scales):
+        x[m] = _randn_rows(n, wl.d_in, base + TID_MS_X + m, dev, 1.0, dt)
+        wt[m] = _randn_rows(wl.d_e, wl.d_in, base + TID_MS_W + m, dev, 1.0 / math.sqrt(wl.d_in), dt)
+    w_he_t = _randn_rows(wl.d_v, wl.d_h, base + TID_MS_HE, dev, 1.0 / math.sqrt(wl.d_h), dt)
+    return dict(x=x, wt=wt, w_he_t=w_he_t, scales=scales)

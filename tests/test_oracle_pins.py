@@ -738,3 +738,124 @@ def test_inject_propagated_special_cases_reduce_to_inject_fused():
     for j in range(3):
         np.testing.assert_array_equal(
             out[j], O.inject_fused(H[j], V, P, scene, prim, w, kept, wg[j], wu[j], wd[j], "bf16"))
+
+
+# --------------------------------------------------------------------------
+# Multi-scale retrieval with the token-wise router (Eq. 8)
+# --------------------------------------------------------------------------
+
+def _ms_case(rng, n=8, M=2, Sm=3, P=5, d_v=4, d_h=6, k=2):
+    H = _bf16_values(rng, (n, d_h))
+    V = _bf16_values(rng, (M * Sm * P, d_v))
+    scene = rng.integers(0, Sm, (M, n))
+    prim = np.stack([np.stack([rng.permutation(P)[:k] for _ in range(n)]) for _ in range(M)])
+    w = rng.dirichlet(np.ones(k), (M, n))
+    kept = np.array([1, 2, 6])
+    return H, V, P, Sm, scene, prim, w, kept
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_multiscale_injection_matches_brute_force(dtype):
+    """inject_multiscale against exact rational loops for the router query,
+    logits, softmax over scales and mix (k = 1 with weight 1, so R^m is a
+    table row exactly; a square W_{h->e}, so a transposed one differs):
+    catches a transposed W_{h->e}, a missing 1/sqrt(d), a softmax over the
+    wrong axis, an unrounded query and a scale reading another partition."""
+    rng = np.random.default_rng(56)
+    n, M, Sm, P, d = 4, 3, 2, 3, 4
+    rnd = _bf16_values if dtype == "bf16" else (lambda r, sh, sc=1.0: r.standard_normal(sh) * sc)
+    H = O.round_to_dtype(rnd(rng, (n, d), 1.5), dtype)
+    W = O.round_to_dtype(rnd(rng, (d, d), 1.5), dtype)
+    V = O.round_to_dtype(rnd(rng, (M * Sm * P, d), 2.0), dtype)
+    scene = rng.integers(0, Sm, (M, n))
+    prim = rng.integers(0, P, (M, n, 1))
+    w = np.ones((M, n, 1))
+    kept = np.arange(n)
+    got = O.inject_multiscale(H, V, P, Sm, scene, prim, w, kept, W, dtype)
+    R = [[V[(m * Sm + scene[m, t]) * P + prim[m, t, 0]].tolist() for m in range(M)]
+         for t in range(n)]
+    mix = B.multiscale_rows(H.tolist(), W.tolist(), R, 8 if dtype == "bf16" else 24)
+    exp = O.round_to_dtype(H + np.array([[float(v) for v in row] for row in mix]), dtype)
+    np.testing.assert_array_equal(got, exp)
+
+
+def test_multiscale_one_scale_adds_the_rounded_row():
+    """M = 1: the router weight is 1, so a kept row gets round(H + round(R))."""
+    rng = np.random.default_rng(57)
+    H, V, P, Sm, scene, prim, w, kept = _ms_case(rng, M=1)
+    out = O.inject_multiscale(H, V, P, Sm, scene, prim, w, kept,
+                              _bf16_values(rng, (H.shape[1], V.shape[1])), "bf16")
+    for t in kept:
+        R = O.round_to_dtype(O.retrieved(V, P, int(scene[0, t]), prim[0, t], w[0, t]), "bf16")
+        np.testing.assert_array_equal(out[t, :4], O.round_to_dtype(H[t, :4] + R, "bf16"))
+    others = np.setdiff1d(np.arange(H.shape[0]), kept)
+    np.testing.assert_array_equal(out[others], H[others])
+
+
+def test_multiscale_zero_router_takes_the_mean_and_scales_use_their_partitions():
+    """W_{h->e} = 0: equal logits, weights 1/M, the mean of the scales' rows;
+    scale m reads rows of its own partition (scenes from m * Sm)."""
+    rng = np.random.default_rng(58)
+    H, V, P, Sm, scene, prim, w, kept = _ms_case(rng, M=3)
+    out = O.inject_multiscale(H, V, P, Sm, scene, prim, w, kept, np.zeros((H.shape[1], 4)), "bf16")
+    for t in kept:
+        R = [O.round_to_dtype(O.retrieved(V, P, m * Sm + int(scene[m, t]), prim[m, t], w[m, t]),
+                              "bf16") for m in range(3)]
+        np.testing.assert_allclose(out[t, :4], O.round_to_dtype(H[t, :4] + sum(R) / 3, "bf16"),
+                                   rtol=0, atol=0)
+
+
+def test_multiscale_planted_scale_wins_and_scale_order_does_not_matter():
+    """A router query aligned with scale 1's row by a margin of 1000 in the
+    logit puts all weight there (exp(-1000) = 0): round(H + R^1).  Reordering
+    the scales (their table partitions and lookups alike) changes nothing."""
+    rng = np.random.default_rng(59)
+    H, V, P, Sm, scene, prim, w, kept = _ms_case(rng, n=4, M=2, d_v=4, d_h=4, k=1)
+    kept = np.array([2])
+    prim[:, 2, 0] = 0
+    scene[:, 2] = 0
+    w[:, 2, 0] = 1.0
+    V[0 * Sm * P] = [1.0, 0.0, 0.0, 0.0]          # scale 0's row for token 2
+    V[1 * Sm * P] = [0.0, 1.0, 0.0, 0.0]          # scale 1's row
+    H[2] = [0.0, 1.0, 0.0, 0.0]
+    W = np.eye(4) * 2000.0                        # q = (0, 2000, 0, 0): logits 0 and 1000
+    out = O.inject_multiscale(H, V, P, Sm, scene, prim, w, kept, W, "f32")
+    np.testing.assert_array_equal(out[2], [0.0, 2.0, 0.0, 0.0])
+    # scales swapped: partition blocks exchanged, lookups exchanged
+    V2 = np.concatenate([V[Sm * P:], V[:Sm * P]])
+    out2 = O.inject_multiscale(H, V2, P, Sm, scene[::-1], prim[::-1], w[::-1], kept, W, "f32")
+    np.testing.assert_array_equal(out2, out)
+    H3, V3, P3, Sm3, sc3, pr3, w3, kept3 = _ms_case(np.random.default_rng(60), M=3)
+    W3 = _bf16_values(np.random.default_rng(61), (H3.shape[1], 4))
+    perm = [2, 0, 1]
+    V3p = np.concatenate([V3[m * Sm3 * P3:(m + 1) * Sm3 * P3] for m in perm])
+    np.testing.assert_array_equal(
+        O.inject_multiscale(H3, V3p, P3, Sm3, sc3[perm], pr3[perm], w3[perm], kept3, W3, "bf16"),
+        O.inject_multiscale(H3, V3, P3, Sm3, sc3, pr3, w3, kept3, W3, "bf16"))
+
+
+def test_run_multiscale_routes_each_scale_within_its_partition():
+    """One scale reproduces the single-scale path's q, scene, prim and w; a
+    key planted in partition 0 that beats every other key moves scale 0's
+    routing onto it and leaves scale 1's untouched."""
+    rng = np.random.default_rng(62)
+    n, d_in, d_e, S, P, d_v, d_h, k = 12, 8, 8, 4, 6, 4, 6, 2
+    x = rng.standard_normal((2, n, d_in))
+    wt = rng.standard_normal((2, d_e, d_in))
+    K1 = rng.standard_normal((S, d_e))
+    K2 = rng.standard_normal((S, P, d_e))
+    V = rng.standard_normal((S * P, d_v))
+    D = rng.standard_normal((n, 5))
+    H = rng.standard_normal((n, d_h))
+    Whe = rng.standard_normal((d_h, d_v))
+    one = O.run_multiscale(x[:1], wt[:1], K1, K2, V, D, H, Whe, k=k, n_keep=4, dtype="f32")
+    ref = O.run(x[0], wt[:1], K1, K2, V, None, D[None], H[None], k=k, n_keep=4, dtype="f32")
+    for key in ("q", "scene", "prim", "w"):
+        np.testing.assert_array_equal(one[key][0], ref[key][0])
+    two = O.run_multiscale(x, wt, K1, K2, V, D, H, Whe, k=k, n_keep=4, dtype="f32")
+    assert np.all(two["scene"] < S // 2)
+    K1p = K1.copy()
+    K1p[1] = 1e6 * np.sign(two["q"][0].sum(axis=0))   # partition 0's second key
+    planted = O.run_multiscale(x, wt, K1p, K2, V, D, H, Whe, k=k, n_keep=4, dtype="f32")
+    assert np.mean(planted["scene"][0] == 1) > 0.5
+    np.testing.assert_array_equal(planted["scene"][1], two["scene"][1])
