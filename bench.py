@@ -58,6 +58,10 @@ def parse():
                     help="with --fusion on a one-layer workload: the LookME layer's R is carried "
                          "to M more layers by the propagation of Eq. 11 (seeded W_p), each "
                          "injected through its own fusion")
+    ap.add_argument("--scales", type=int, default=0, metavar="M",
+                    help="multi-scale image retrieval (Eq. 8) on a one-layer workload: M scales "
+                         "(seeded tokens and rankers) each routed and looked up in its own scene "
+                         "partition, mixed by the token-wise router and injected")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -175,7 +179,7 @@ def stored_traffic(wl):
 
 
 class Bench:
-    def __init__(self, wl, seed, copies, relevance=0, fusion=0, netprop=0):
+    def __init__(self, wl, seed, copies, relevance=0, fusion=0, netprop=0, scales=0):
         import torch
         from paper_2607_16305_amd import lookme as lk
         from synth import make_inputs
@@ -231,6 +235,25 @@ class Bench:
                 if netprop:
                     t.set_propagation(self.w_p_t)
                 t.reserve(L + netprop, n)   # the fusion's buffers enlarge the workspace
+        self.scales = scales
+        self.handles = [t.handle for t in self.tables]
+        if scales:
+            from synth import make_multiscale
+            self.ms = make_multiscale(wl, seed, scales, device="cuda")
+            # stacked per-scale outputs (row m of each is 16-byte aligned: n % 4 == 0)
+            self.q = torch.empty((scales, n, wl.d_e), dtype=dt, device=dev)
+            self.scene = torch.empty((scales, n), dtype=torch.int32, device=dev)
+            self.prim = torch.empty((scales, n, k), dtype=torch.int32, device=dev)
+            self.w = torch.empty((scales, n, k), dtype=torch.float32, device=dev)
+            self.scale_tables = []
+            for t in self.tables:
+                t.set_multiscale(scales, self.ms["w_he_t"])
+                t.reserve(1, n)
+                views = [t.scale_view(m, scales) for m in range(scales)]
+                for v in views:
+                    v.reserve(1, n)
+                self.scale_tables.append(views)
+                self.handles += [v.handle for v in views]
         # the kept set is selected on a second stream (default priority, as
         # the first) while routing and lookup run; two reusable events order
         # the streams within a step
@@ -255,6 +278,17 @@ class Bench:
         lk.lookme_select(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.kept,
                          self.side_handle)
         self.ev_kept.record(self.side)
+        if self.scales:
+            ms = self.ms
+            for m, v in enumerate(self.scale_tables[i % self.copies]):
+                lk.lookme_route(v.handle, 1, n, wl.d_in, ms["x"][m], ms["wt"][m], self.q[m],
+                                self.scene[m], self.stream)
+                lk.lookme_lookup(v.handle, 1, n, self.q[m], self.scene[m], self.prim[m],
+                                 self.w[m], self.stream)
+            self.main.wait_event(self.ev_kept)
+            lk.lookme_inject_multiscale(h, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
+                                        self.hidden[0], wl.d_h, self.stream)
+            return
         lk.lookme_route(h, L, n, wl.d_in, inp["x"], inp["wt"], self.q, self.scene, self.stream)
         if self.mlp is None:
             lk.lookme_lookup(h, L, n, self.q, self.scene, self.prim, self.w, self.stream)
@@ -285,22 +319,22 @@ class Bench:
     def profiled(self, steps):
         """Per-kernel-group times from the library's HIP events (launch stream)."""
         lk = self.lk
-        for t in self.tables:
-            lk.lookme_profile_read(t.handle, 0, reset=True)
-            lk.lookme_profile_enable(t.handle, True)
+        for h in self.handles:
+            lk.lookme_profile_read(h, 0, reset=True)
+            lk.lookme_profile_enable(h, True)
         self.timed(steps)
         out = {}
         for g, name in enumerate(lk.GROUPS):
             cnt, ms = 0, 0.0
-            for t in self.tables:
-                c, m = lk.lookme_profile_read(t.handle, g)
+            for h in self.handles:
+                c, m = lk.lookme_profile_read(h, g)
                 cnt += c
                 ms += m
             if cnt:
                 out[name] = ms / cnt
-        for t in self.tables:
-            lk.lookme_profile_enable(t.handle, False)
-            lk.lookme_profile_read(t.handle, 0, reset=True)
+        for h in self.handles:
+            lk.lookme_profile_enable(h, False)
+            lk.lookme_profile_read(h, 0, reset=True)
         return out   # average milliseconds per launch
 
     def algorithmic_bytes(self):
@@ -310,18 +344,30 @@ class Bench:
         L, n, k = wl.layers, wl.n_tokens, wl.top_k
         rows = L * n
         nonempty = int(torch.unique(self.scene).numel())
+        scenes = wl.scenes
+        if self.scales:
+            # a launch of each group serves one scale: its rows and partition;
+            # the used scenes averaged over the scales
+            nonempty = sum(int(torch.unique(self.scene[m]).numel())
+                           for m in range(self.scales)) / self.scales
+            scenes = wl.scenes // self.scales
         keep = L * wl.n_keep
         b = {}
         b["project"] = (n * wl.d_in + L * wl.d_e * wl.d_in + rows * wl.d_e) * es
-        b["route"] = (rows * wl.d_e + wl.scenes * wl.d_e) * es + rows * 4
-        b["score"] = (nonempty * wl.prims * wl.d_e * es      # key stream of each used scene
+        b["route"] = (rows * wl.d_e + scenes * wl.d_e) * es + rows * 4
+        b["score"] = int(nonempty * wl.prims * wl.d_e * es   # key stream of each used scene
                       + rows * wl.d_e * es                    # queries
                       + rows * 4                              # bucketed row ids
                       + rows * k * 8)                         # prim + weights written
         b["norm"] = rows * wl.crit_dim * es + rows * 4
         b["inject"] = keep * (k * wl.d_v * es + 2 * wl.d_v * es + k * 8 + 8)
-        flops = {"project": 2 * n * wl.d_in * L * wl.d_e, "route": 2 * rows * wl.d_e * wl.scenes,
+        flops = {"project": 2 * n * wl.d_in * L * wl.d_e, "route": 2 * rows * wl.d_e * scenes,
                  "score": 2 * rows * wl.d_e * wl.prims}
+        if self.scales:
+            # the router's query product; the gather and mix move
+            # n_keep (M k d_v + 2 M d_v + 2 d_v) elements besides
+            flops["inject"] = 2 * keep * wl.d_h * wl.d_v
+            b["inject"] = None
         if self.fus is not None:
             d_ff = self.fus["d_ff"]
             m = self.netprop
@@ -363,6 +409,8 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
             self.a, self.shape = a, a.shape
 
         def __getitem__(self, i):
+            if isinstance(i, slice):       # a partition (multi-scale): still lazy
+                return Rows(self.a[i])
             return O.to_f64(self.a[i], dt)
 
     mlp = None
@@ -382,6 +430,25 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
     # timed (the same inputs each time), so that the rate is not a single
     # short measurement
     reps, el = 0, 0.0
+    if b.scales:
+        ms = b.ms
+        xs = O.to_f64(to_np(ms["x"][:, :m]), dt)
+        wts = O.to_f64(to_np(ms["wt"]), dt)
+        w_he = O.to_f64(to_np(ms["w_he_t"]), dt).T
+        with threadpool_limits(limits=1):
+            while reps == 0 or el < min_seconds:
+                t0 = time.perf_counter()
+                res = O.run_multiscale(xs, wts, O.to_f64(K1, dt), Rows(K2), Rows(V),
+                                       O.to_f64(D[0], dt), O.to_f64(H[0], dt), w_he, k=wl.top_k,
+                                       n_keep=n_keep, dtype=dt)
+                el += time.perf_counter() - t0
+                reps += 1
+                assert res["hidden"].shape == (m, wl.d_h)
+        return {"value": reps * m / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+                "sample": f"first {m} of {wl.n_tokens} image positions x {b.scales} scales, "
+                          f"whole path (per-scale projection, routing and lookup, select, "
+                          f"router mix and injection, n_keep={n_keep}), float64 NumPy, "
+                          f"1 thread, {reps} repetitions, {el:.1f} s"}
     with threadpool_limits(limits=1):
         while reps == 0 or el < min_seconds:
             t0 = time.perf_counter()
@@ -424,7 +491,12 @@ def main():
         calibration_copy()
     if args.netprop and (not args.fusion or wl.layers != 1):
         raise SystemExit("--netprop needs --fusion and a one-layer workload")
-    b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion, args.netprop)
+    if args.scales and (wl.layers != 1 or args.relevance or args.fusion or wl.n_tokens % 4
+                        or wl.scenes % args.scales):
+        raise SystemExit("--scales needs a one-layer workload (tokens a multiple of 4, scenes "
+                         "divisible by the scales) without --relevance or --fusion")
+    b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion, args.netprop,
+              args.scales)
 
     for i in range(args.warmup):
         b.step(i)
@@ -451,7 +523,8 @@ def main():
                     "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS,
                     "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
-                    "traffic": stored_traffic(wl),
+                    # counters were taken on the single-scale launch
+                    "traffic": None if args.scales else stored_traffic(wl),
                     "algorithmic_bytes_per_launch": bytes_["score"], "nonempty_scenes": nonempty}
     else:
         # the relevance lookup is a pair of dense products: judged on the
@@ -482,7 +555,7 @@ def main():
                               else "primitive keys"),
                    "injection": (f"SwiGLU fusion, d_ff {args.fusion}" if args.fusion
                                  else "prefix add of the retrieved rows"),
-                   "propagated_layers": args.netprop},
+                   "propagated_layers": args.netprop, "scales": args.scales},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kern,

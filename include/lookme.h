@@ -278,6 +278,41 @@ lookme_status_t lookme_inject_propagated(lookme_t h, int32_t steps, int64_t n, i
                                          int32_t d_h, void* stream);
 
 /*
+ * lookme_set_multiscale -- registers the token-wise router of multi-scale
+ * image retrieval (Sec. 3.2, Eq. 8) on the handle of the whole table:
+ *   scales  M in [1, 8]; the num_scenes scenes split into M equal partitions,
+ *           scale m owning scenes [m S/M, (m+1) S/M) (each scale is routed and
+ *           looked up on a handle created over its partition's slices of
+ *           scene_keys, prim_keys and values: its own ranker);
+ *   w_he_t  [value_dim, d_h] dtype, W_{h->e} stored transposed (output-row-
+ *           major), borrowed; it projects a hidden state to the width of the
+ *           retrieved rows.
+ * Needs d_h >= value_dim and d_h * elem_size a multiple of 128 bytes.  From
+ * then on lookme_workspace_size includes the router's buffers.
+ */
+lookme_status_t lookme_set_multiscale(lookme_t h, int32_t scales, int32_t d_h,
+                                      const void* w_he_t);
+
+/*
+ * lookme_inject_multiscale -- multi-scale injection of one layer (Eq. 8, then
+ * Eq. 10 and Eq. 2): scene [M, n] (scale m's scene ids, local to its
+ * partition), prim [M, n, top_k] and w [M, n, top_k] are the M scales'
+ * lookups, kept [n_keep] the layer's kept set (lookme_select).  For every
+ * kept token t:
+ *   R^m = round(sum_i w[m,t,i] values[(m S/M + scene[m,t]) N_p + prim[m,t,i], :])
+ *   q   = round(hidden[t, :] W_{h->e})                 (the states before the add)
+ *   a   = softmax over m of (q . R^m) / sqrt(value_dim)
+ *   hidden[t, :value_dim] <- round(hidden[t, :value_dim] + sum_m a_m R^m)
+ * float32 accumulation; every other row keeps its bits.  hidden [n, d_h],
+ * d_h equal to the registered one.  Needs the workspace of
+ * lookme_workspace_size(1, n) queried after lookme_set_multiscale.
+ */
+lookme_status_t lookme_inject_multiscale(lookme_t h, int64_t n, int64_t n_keep,
+                                         const int32_t* kept, const int32_t* scene,
+                                         const int32_t* prim, const float* w, void* hidden,
+                                         int32_t d_h, void* stream);
+
+/*
  * Measurement support (not part of the method).  When enabled, each kernel
  * group that route/lookup/inject launches is bracketed by a pair of HIP timing
  * events recorded on the call's stream.  lookme_profile_read waits for the

@@ -367,6 +367,54 @@ def check_propagated_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows
                                                   float(err.max()))
 
 
+def check_multiscale_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: int,
+                            scenes_per_scale: int, scene: np.ndarray, prim: np.ndarray,
+                            w_lib: np.ndarray, kept: np.ndarray, w_he: np.ndarray, rep: Report,
+                            tokens, contract_abs: float = 2e-2):
+    """Multi-scale injection (Eq. 8) on the library's kept set and per-scale
+    primitives and weights: rows outside the kept set, and columns from d_v
+    on, keep their bits; the first d_v columns of kept rows equal
+    round(H + mix(round(H W_{h->e}), [round(R^m)])) within the contract (bf16:
+    ``contract_abs`` max-abs; float32: 1e-4 * (|H| + sum_m |R^m|)).  scene,
+    prim, w_lib [M, n, ...]; w_he [d_h, d_v]; h_in, h_out_lib hold the rows
+    of ``tokens``."""
+    kept_set = set(np.asarray(kept).tolist())
+    M = scene.shape[0]
+    d_v = w_he.shape[1]
+    h_in_f = O.to_f64(h_in, dtype)
+    h_lib_f = O.to_f64(h_out_lib, dtype)
+    for r, t in enumerate(np.asarray(tokens)):
+        rep.count("hidden_row")
+        if int(t) not in kept_set:
+            if not np.array_equal(np.asarray(h_in[r]).view(np.uint8),
+                                  np.asarray(h_out_lib[r]).view(np.uint8)):
+                rep.fail(f"hidden: untouched row {t} modified")
+            continue
+        if not np.array_equal(np.asarray(h_in[r, d_v:]).view(np.uint8),
+                              np.asarray(h_out_lib[r, d_v:]).view(np.uint8)):
+            rep.fail(f"hidden: row {t} modified past column {d_v}")
+        R = []
+        for m in range(M):
+            rows = (m * scenes_per_scale + int(scene[m, t])) * P + np.asarray(prim[m, t],
+                                                                              dtype=np.int64)
+            R.append(O.round_to_dtype(
+                np.sum(np.asarray(w_lib[m, t], dtype=np.float64)[:, None] * values_rows(rows),
+                       axis=0), dtype))
+        R = np.stack(R)
+        q = O.round_to_dtype(h_in_f[r] @ w_he, dtype)
+        exp = O.round_to_dtype(h_in_f[r, :d_v] + O.multiscale_mix(q, R), dtype)
+        err = np.abs(h_lib_f[r, :d_v] - exp)
+        if dtype == "bf16":
+            bad = err > contract_abs
+        else:
+            bad = err > 1e-4 * (np.abs(h_in_f[r, :d_v]) + np.sum(np.abs(R), axis=0))
+        if np.any(bad):
+            c = int(np.argmax(err))
+            rep.fail(f"hidden[{t}, {c}]: library {h_lib_f[r, c]!r}, expected {exp[c]!r}")
+        rep.notes["multiscale_max_abs"] = max(rep.notes.get("multiscale_max_abs", 0.0),
+                                              float(err.max()))
+
+
 def check_kept(c: np.ndarray, n_keep: int, kept_lib: np.ndarray, rep: Report):
     """C5: the kept set equals the oracle's except for swaps among
     criticalities tied with the n_keep-th; ascending, unique, in range."""

@@ -174,21 +174,25 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
 }
 
 // TO_R: the weighted row sum R of kept row j is rounded to the storage
-// dtype and written to row j of `hidden` (the fusion's input, [rows, d_v])
-// instead of being added into H.
+// dtype and written to row j of `hidden` (the fusion's or the multi-scale
+// router's input, [rows, d_v]) instead of being added into H.  Layer l reads
+// its kept list at kept + l * kept_batch (0: one list for all layers) and
+// its scenes (clamped into [0, S)) from scene l * scene_step of the table
+// (multi-scale: scale l's partition).
 template <int DT, int K, bool TO_R = false>
 __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
     int64_t n, int64_t n_keep, const int32_t* __restrict__ kept_all,
     const int32_t* __restrict__ scene_all, const int32_t* __restrict__ prim_all,
     const float* __restrict__ w_all, const char* __restrict__ values, int S, int P, int k,
-    int64_t v_bytes, char* __restrict__ hidden, int64_t h_bytes) {
+    int64_t v_bytes, char* __restrict__ hidden, int64_t h_bytes, int64_t kept_batch,
+    int scene_step) {
   const int64_t j = blockIdx.x;
   const int64_t layer = j / n_keep;
-  int64_t t = kept_all[j];   // [layers, n_keep], row-major
+  int64_t t = kept_all[layer * kept_batch + (j - layer * n_keep)];
   t = t < 0 ? 0 : (t >= n ? n - 1 : t);
   const int64_t row = layer * n + t;
   int s = scene_all[row];
-  s = s < 0 ? 0 : (s >= S ? S - 1 : s);
+  s = (s < 0 ? 0 : (s >= S ? S - 1 : s)) + (int)layer * scene_step;
   int64_t vrow[K];
   float wt[K];
 #pragma unroll
@@ -251,14 +255,14 @@ template <int DT, bool TO_R = false>
 static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_t n_keep,
                             const int32_t* kept, const int32_t* scene, const int32_t* prim,
                             const float* w, const char* values, int S, int P, int64_t vb,
-                            char* hidden, int64_t hb) {
+                            char* hidden, int64_t hb, int64_t kept_batch, int scene_step) {
   // as many whole waves as the row has 16-byte chunks (up to 256 threads):
   // narrow rows leave no thread idle, and the CU holds more workgroups
   const int ch = (int)(vb / 16);
   const int bs = ch >= INJ_THREADS ? INJ_THREADS : (ch + 63) / 64 * 64;
 #define LOOKME_INJ(K_)                                                                \
   hipLaunchKernelGGL((inject_kernel<DT, K_, TO_R>), grid, dim3(bs), 0, st, n, n_keep, kept, \
-                     scene, prim, w, values, S, P, kk, vb, hidden, hb)
+                     scene, prim, w, values, S, P, kk, vb, hidden, hb, kept_batch, scene_step)
   if (kk <= 4) LOOKME_INJ(4);
   else if (kk <= 8) LOOKME_INJ(8);
   else if (kk <= 16) LOOKME_INJ(16);
@@ -305,29 +309,29 @@ hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, con
   if (dt == DT_BF16)
     launch_inject_k<DT_BF16>(k, grid, st, n, n_keep, kept, scene, prim, w,
                              static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                             static_cast<char*>(hidden), (int64_t)d_h * es);
+                             static_cast<char*>(hidden), (int64_t)d_h * es, n_keep, 0);
   else
     launch_inject_k<DT_F32>(k, grid, st, n, n_keep, kept, scene, prim, w,
                             static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                            static_cast<char*>(hidden), (int64_t)d_h * es);
+                            static_cast<char*>(hidden), (int64_t)d_h * es, n_keep, 0);
   return hipGetLastError();
 }
 
 hipError_t launch_gather_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
                               const int32_t* scene, const int32_t* prim, const float* w,
                               const void* values, int S, int P, int d_v, int k, void* r_out,
-                              hipStream_t st) {
+                              hipStream_t st, int64_t kept_batch, int scene_step) {
   if (n == 0 || n_keep == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const dim3 grid((unsigned)(layers * n_keep));
   if (dt == DT_BF16)
     launch_inject_k<DT_BF16, true>(k, grid, st, n, n_keep, kept, scene, prim, w,
                                    static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                                   static_cast<char*>(r_out), 0);
+                                   static_cast<char*>(r_out), 0, kept_batch, scene_step);
   else
     launch_inject_k<DT_F32, true>(k, grid, st, n, n_keep, kept, scene, prim, w,
                                   static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                                  static_cast<char*>(r_out), 0);
+                                  static_cast<char*>(r_out), 0, kept_batch, scene_step);
   return hipGetLastError();
 }
 

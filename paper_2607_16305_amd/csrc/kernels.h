@@ -122,10 +122,13 @@ struct FusionFfn {
   const void* w_up;
   const void* w_down;
 };
+// kept_batch: stride between the layers' kept lists (0: one list for all);
+// scene_step: scene offset of each layer in the table (multi-scale
+// partitions; the layer's own scene ids are clamped into [0, S)).
 hipError_t launch_gather_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
                               const int32_t* scene, const int32_t* prim, const float* w,
                               const void* values, int S, int P, int d_v, int k, void* r_out,
-                              hipStream_t st);
+                              hipStream_t st, int64_t kept_batch, int scene_step);
 hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int64_t n_keep,
                          const int32_t* kept, int64_t kept_batch, int d_v, const void* r, void* u,
                          void* hidden, hipStream_t st);
@@ -134,6 +137,19 @@ hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int6
 // w_p_t [steps, d_v, d_v] holding each W_p transposed (output-row-major).
 hipError_t launch_propagate(int dt, const void* w_p_t, int steps, int64_t n_keep, int d_v,
                             void* r, hipStream_t st);
+
+// ---- multi-scale retrieval with the token-wise router (Eq. 8) -------------
+// Scale m's lookup (scene [M, n] local to partition m of S / M scenes, prim
+// and w [M, n, k]) gives R^m of every kept token, gathered and rounded into
+// r [M, n_keep, d_v]; q = round(H[kept] W_he) into q [n_keep, d_v] (w_he_t
+// [d_v, d_h], output-row-major); then H[t, :d_v] = round(H + sum_m alpha_m
+// R^m) with alpha = softmax_m(q . R^m / sqrt(d_v)).
+constexpr int MS_MAX_SCALES = 8;
+hipError_t launch_multiscale(int dt, int scales, int64_t n, int64_t n_keep, const int32_t* kept,
+                             const int32_t* scene, const int32_t* prim, const float* w,
+                             const void* values, int S, int P, int d_v, int k,
+                             const void* w_he_t, int d_h, void* hidden, void* r, void* q,
+                             hipStream_t st);
 
 // ---- Level-2 scoring of bucketed rows, fused top-k + softmax --------------
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,

@@ -38,6 +38,9 @@ struct lookme_s {
   lookme::FusionFfn fus;                   // d_ff == 0: none registered
   int32_t prop_steps = 0;                  // Eq. 11 projections; 0: none registered
   const void* prop_w = nullptr;            // [prop_steps, value_dim, value_dim], transposed
+  int32_t ms_scales = 0;                   // Eq. 8 router; 0: none registered
+  int32_t ms_dh = 0;
+  const void* ms_w = nullptr;              // W_{h->e} transposed, [value_dim, ms_dh]
 };
 
 namespace {
@@ -69,7 +72,7 @@ constexpr int32_t MAX_SCENES = 16384;   // bucketing keeps one histogram per chu
 // Workspace layout for `layers` x `n` rows.
 struct Layout {
   size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, route_count,
-      route_part, crit_key, kept, rel_logits, fus_r, fus_u, total;
+      route_part, crit_key, kept, rel_logits, fus_r, fus_u, ms_r, ms_q, total;
 };
 
 // The leading bytes of the workspace hold counters that start at zero; they
@@ -78,7 +81,7 @@ struct Layout {
 constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_COUNTERS * 4;
 
 Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance,
-              int32_t fusion_dff) {
+              int32_t fusion_dff, int32_t scales) {
   const int64_t rows = (int64_t)layers * n;
   const int64_t chunks = lookme::bucket_chunks(rows);
   const int64_t units = lookme::bucket_max_units(rows, d.num_scenes);
@@ -108,6 +111,9 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance,
   const size_t es = (size_t)elem_size(d.dtype);
   L.fus_r = take(fusion_dff > 0 ? (size_t)rows * d.value_dim * es : 0);
   L.fus_u = take(fusion_dff > 0 ? (size_t)rows * fusion_dff * es : 0);
+  // the multi-scale router's retrieved rows [scales, rows, d_v] and queries
+  L.ms_r = take(scales > 0 ? (size_t)scales * rows * d.value_dim * es : 0);
+  L.ms_q = take(scales > 0 ? (size_t)rows * d.value_dim * es : 0);
   L.total = off;
   return L;
 }
@@ -133,7 +139,7 @@ lookme_status_t check_layers_n(int32_t layers, int64_t n) {
 }
 
 lookme_status_t check_workspace(lookme_t h, int32_t layers, int64_t n, Layout* L) {
-  *L = layout(h->d, layers, n, h->rel.hidden > 0, h->fus.d_ff);
+  *L = layout(h->d, layers, n, h->rel.hidden > 0, h->fus.d_ff, h->ms_scales);
   if (h->ws == nullptr) return fail(LOOKME_ERR_WORKSPACE, "no workspace set");
   if (h->ws_bytes < L->total)
     return fail(LOOKME_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed for %d x %lld rows",
@@ -332,7 +338,7 @@ lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_toke
   LOOKME_TRY(check_handle(h));
   if (bytes == nullptr) return fail(LOOKME_ERR_INVALID, "bytes is NULL");
   LOOKME_TRY(check_layers_n(layers, n_tokens));
-  *bytes = layout(h->d, layers, n_tokens, h->rel.hidden > 0, h->fus.d_ff).total;
+  *bytes = layout(h->d, layers, n_tokens, h->rel.hidden > 0, h->fus.d_ff, h->ms_scales).total;
   return LOOKME_OK;
 }
 
@@ -593,7 +599,8 @@ lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64
   Timed tm(h, LOOKME_GROUP_INJECT, st);
   LOOKME_TRY(hip_status(lookme::launch_gather_rows(d.dtype, layers, n, n_keep, kept, scene, prim,
                                                    w, h->values, d.num_scenes, d.prims_per_scene,
-                                                   d.value_dim, d.top_k, ws + L.fus_r, st),
+                                                   d.value_dim, d.top_k, ws + L.fus_r, st,
+                                                   n_keep, 0),
                         "fusion gather launch"));
   return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n_keep, kept, n_keep,
                                           d.value_dim, ws + L.fus_r, ws + L.fus_u, hidden, st),
@@ -635,7 +642,8 @@ lookme_status_t lookme_inject_propagated(lookme_t h, int32_t steps, int64_t n, i
   Timed tm(h, LOOKME_GROUP_INJECT, st);
   LOOKME_TRY(hip_status(lookme::launch_gather_rows(d.dtype, 1, n, n_keep, kept, scene, prim, w,
                                                    h->values, d.num_scenes, d.prims_per_scene,
-                                                   d.value_dim, d.top_k, ws + L.fus_r, st),
+                                                   d.value_dim, d.top_k, ws + L.fus_r, st,
+                                                   n_keep, 0),
                         "fusion gather launch"));
   LOOKME_TRY(hip_status(
       lookme::launch_propagate(d.dtype, h->prop_w, steps, n_keep, d.value_dim, ws + L.fus_r, st),
@@ -643,6 +651,52 @@ lookme_status_t lookme_inject_propagated(lookme_t h, int32_t steps, int64_t n, i
   return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n_keep, kept, 0,
                                           d.value_dim, ws + L.fus_r, ws + L.fus_u, hidden, st),
                     "fusion launch");
+}
+
+lookme_status_t lookme_set_multiscale(lookme_t h, int32_t scales, int32_t d_h,
+                                      const void* w_he_t) {
+  LOOKME_TRY(check_handle(h));
+  const lookme_desc_t& d = h->d;
+  if (scales < 1 || scales > lookme::MS_MAX_SCALES)
+    return fail(LOOKME_ERR_UNSUPPORTED, "scales must be in [1, %d] (got %d)",
+                lookme::MS_MAX_SCALES, scales);
+  if (d.num_scenes % scales != 0)
+    return fail(LOOKME_ERR_INVALID, "%d scenes do not split evenly over %d scales",
+                d.num_scenes, scales);
+  LOOKME_TRY(check_hidden_dim(d, d_h));
+  if (((int64_t)d_h * elem_size(d.dtype)) % 128 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "d_h * elem_size must be a multiple of 128 bytes");
+  LOOKME_TRY(check_ptr(w_he_t, "w_he_t"));
+  h->ms_scales = scales;
+  h->ms_dh = d_h;
+  h->ms_w = w_he_t;
+  return LOOKME_OK;
+}
+
+lookme_status_t lookme_inject_multiscale(lookme_t h, int64_t n, int64_t n_keep,
+                                         const int32_t* kept, const int32_t* scene,
+                                         const int32_t* prim, const float* w, void* hidden,
+                                         int32_t d_h, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  if (h->ms_scales < 1)
+    return fail(LOOKME_ERR_INVALID, "no multi-scale router registered (lookme_set_multiscale)");
+  LOOKME_TRY(check_layers_n(h->ms_scales, n));
+  LOOKME_TRY(check_keep(n, n_keep));
+  if (d_h != h->ms_dh)
+    return fail(LOOKME_ERR_INVALID, "d_h %d, the router reads %d", d_h, h->ms_dh);
+  if (n == 0 || n_keep == 0) return LOOKME_OK;
+  LOOKME_TRY(check_lookup_ptrs(kept, scene, prim, w, hidden));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, 1, n, &L));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(h->ws);
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  return hip_status(lookme::launch_multiscale(d.dtype, h->ms_scales, n, n_keep, kept, scene,
+                                              prim, w, h->values, d.num_scenes,
+                                              d.prims_per_scene, d.value_dim, d.top_k, h->ms_w,
+                                              d_h, hidden, ws + L.ms_r, ws + L.ms_q, st),
+                    "multi-scale injection launch");
 }
 
 }  // extern "C"

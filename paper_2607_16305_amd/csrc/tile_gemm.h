@@ -17,7 +17,8 @@
 //               32 output columns a tile;
 //   EPI_RESID   H[out_row(r), c] = round(H + C) with out_row(r) = z * n +
 //               kept[z * kept_batch + r] (the kept token of row r of layer z);
-//   EPI_ADD     round(C + res) with res [rows, cols], [rows, cols].
+//   EPI_ADD     round(C + res) with res [rows, cols], [rows, cols];
+//   EPI_STORE   round(C), [rows, cols].
 //
 // An A row may take its first `ksplit` stages from a0 and the rest from a
 // gathered row of a1 (the relevance MLP's [query ; scene key] input).
@@ -32,7 +33,7 @@ namespace lookme {
 using TgShape = DtlShape<2, 2, 2, 2, 128>;
 constexpr int TG_KB = 128;
 
-enum : int { EPI_ACT = 0, EPI_LOGIT = 1, EPI_SWIGLU = 2, EPI_RESID = 3, EPI_ADD = 4 };
+enum : int { EPI_ACT = 0, EPI_LOGIT = 1, EPI_SWIGLU = 2, EPI_RESID = 3, EPI_ADD = 4, EPI_STORE = 5 };
 
 struct TileGemmParams {
   const char* a0;           // [rows, K] (or the first ksplit stages of a row)
@@ -188,8 +189,8 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
           }
           float v;
           char* dst;
-          if constexpr (EPI == EPI_ACT) {
-            v = fmaxf(c, 0.f);
+          if constexpr (EPI == EPI_ACT || EPI == EPI_STORE) {
+            v = EPI == EPI_ACT ? fmaxf(c, 0.f) : c;
             dst = a.out + (orow[i][r] * a.cols + col[j]) * ES;
           } else if constexpr (EPI == EPI_ADD) {
             v = old[j][i][r] + c;

@@ -29,6 +29,7 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_lookup", "lookme_inject", "lookme_select", "lookme_inject_kept",
             "lookme_set_relevance", "lookme_lookup_relevance", "lookme_set_fusion",
             "lookme_inject_fused", "lookme_set_propagation", "lookme_inject_propagated",
+            "lookme_set_multiscale", "lookme_inject_multiscale",
             "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
@@ -83,6 +84,9 @@ def load():
         "lookme_inject_fused": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp, _vp,
                                 _vp, _vp, _vp, ctypes.c_int32, _vp],
         "lookme_set_propagation": [_vp, ctypes.c_int32, _vp],
+        "lookme_set_multiscale": [_vp, ctypes.c_int32, ctypes.c_int32, _vp],
+        "lookme_inject_multiscale": [_vp, ctypes.c_int64, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
+                                     ctypes.c_int32, _vp],
         "lookme_inject_propagated": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
                                      _vp, _vp, _vp, _vp, ctypes.c_int32, _vp],
         "lookme_destroy": [_vp],
@@ -198,6 +202,15 @@ def lookme_inject_propagated(h, steps, n, n_keep, kept, scene, prim, w, hidden, 
                                            _stream(stream)))
 
 
+def lookme_set_multiscale(h, scales, d_h, w_he_t):
+    _check(load().lookme_set_multiscale(h, scales, d_h, _ptr(w_he_t)))
+
+
+def lookme_inject_multiscale(h, n, n_keep, kept, scene, prim, w, hidden, d_h, stream=None):
+    _check(load().lookme_inject_multiscale(h, n, n_keep, _ptr(kept), _ptr(scene), _ptr(prim),
+                                           _ptr(w), _ptr(hidden), d_h, _stream(stream)))
+
+
 def lookme_destroy(h):
     if h:
         _check(load().lookme_destroy(h))
@@ -296,6 +309,26 @@ class Table:
         n = scene.numel()
         self.reserve(steps + 1, n)
         lookme_inject_propagated(self.handle, steps, n, n_keep, kept, scene, prim, w, hidden,
+                                 hidden.shape[-1], stream)
+
+    def scale_view(self, m: int, scales: int) -> "Table":
+        """A table over scale m's partition (scenes [m S/M, (m+1) S/M)) of
+        this table's tensors (views, no copies), for that scale's routing and
+        lookup."""
+        scene_keys, prim_keys, values, _ = self.tensors
+        S, P = prim_keys.shape[0], prim_keys.shape[1]
+        Sm = S // scales
+        return Table(scene_keys[m * Sm:(m + 1) * Sm], prim_keys[m * Sm:(m + 1) * Sm],
+                     values[m * Sm * P:(m + 1) * Sm * P], self.desc.top_k)
+
+    def set_multiscale(self, scales, w_he_t):
+        self.multiscale = w_he_t                 # keep alive
+        lookme_set_multiscale(self.handle, scales, w_he_t.shape[1], w_he_t)
+
+    def inject_multiscale(self, kept, scene, prim, w, hidden, n_keep, stream=None):
+        n = hidden.shape[0]
+        self.reserve(1, n)
+        lookme_inject_multiscale(self.handle, n, n_keep, kept, scene, prim, w, hidden,
                                  hidden.shape[-1], stream)
 
     def close(self):

@@ -176,6 +176,88 @@ def check_propagated_run(r: PropagatedRun, tokens=None) -> C.Report:
     return rep.finish()
 
 
+class MultiScaleRun:
+    """Multi-scale image pathway of one layer (Sec. 3.2, Eq. 8): scale m's
+    tokens are projected, routed and looked up on a table over its scene
+    partition (Table.scale_view), the kept set comes from the layer's
+    criticality, and lookme_inject_multiscale mixes the scales' rows into the
+    hidden states."""
+
+    def __init__(self, inp: dict, ms: dict, table: lk.Table | None = None, stream=None):
+        self.inp, self.ms = inp, ms
+        x = ms["x"]
+        self.M, self.n = ms["scales"], x.shape[1]
+        self.k, self.n_keep = inp["k"], inp["n_keep"]
+        S, P, d_e = inp["prim_keys"].shape
+        self.S, self.P, self.d_e = S, P, d_e
+        self.dev = x.device
+        self.stream = stream
+        self.table = table or lk.Table(inp["scene_keys"], inp["prim_keys"], inp["values"], self.k)
+        self.table.set_multiscale(self.M, ms["w_he_t"])
+        self.table.reserve(1, self.n)
+        self.scales = [self.table.scale_view(m, self.M) for m in range(self.M)]
+        M, n, k = self.M, self.n, self.k
+        # one buffer per scale (16-byte aligned whatever n is), stacked into
+        # the [M, n, ...] tensors that the injection reads
+        self.qs = [torch.empty((n, d_e), dtype=x.dtype, device=self.dev) for _ in range(M)]
+        self.scenes = [torch.full((n,), -7, dtype=torch.int32, device=self.dev) for _ in range(M)]
+        self.prims = [torch.full((n, k), -7, dtype=torch.int32, device=self.dev)
+                      for _ in range(M)]
+        self.ws = [torch.full((n, k), -7.0, dtype=torch.float32, device=self.dev)
+                   for _ in range(M)]
+        self.kept = torch.full((max(self.n_keep, 1),), -7, dtype=torch.int32, device=self.dev)
+        self.h_in = self.inp["hidden"][0].clone()
+        self.hidden = self.inp["hidden"][0].clone()
+
+    def run(self):
+        ms, st = self.ms, self.stream
+        for m, t in enumerate(self.scales):
+            t.route(ms["x"][m], ms["wt"][m:m + 1], self.qs[m], self.scenes[m], layers=1,
+                    stream=st)
+            t.lookup(self.qs[m], self.scenes[m], self.prims[m], self.ws[m], layers=1, stream=st)
+        self.q, self.scene = torch.stack(self.qs), torch.stack(self.scenes)
+        self.prim, self.w = torch.stack(self.prims), torch.stack(self.ws)
+        self.table.select(self.inp["delta"][:1], self.kept, self.n_keep, layers=1, stream=st)
+        self.table.inject_multiscale(self.kept, self.scene, self.prim, self.w, self.hidden,
+                                     self.n_keep, stream=st)
+        return self
+
+
+def check_multiscale_run(r: MultiScaleRun, tokens=None) -> C.Report:
+    """Every scale's projection, routing (within its partition) and lookup on
+    the sampled tokens, the kept set in full, and the mixed injection."""
+    torch.cuda.synchronize()
+    inp, ms = r.inp, r.ms
+    dt = dtype_name(inp["x"])
+    rep = C.Report()
+    toks = np.arange(r.n) if tokens is None else np.asarray(tokens)
+    tsel = torch.as_tensor(toks, device=r.dev)
+    Sm = r.S // r.M
+    K1 = f64(inp["scene_keys"])
+    prim_keys, values = inp["prim_keys"], inp["values"]
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    w_lib = to_np(r.w)
+    for m in range(r.M):
+        q_bits = to_np(r.q[m])[toks]
+        C.check_projection(q_bits, f64(ms["x"][m][tsel]), f64(ms["wt"][m]), dt, rep)
+        q_lib = O.to_f64(q_bits, dt)
+        scene = to_np(r.scene[m]).astype(np.int64)
+        C.check_scene(q_lib, K1[m * Sm:(m + 1) * Sm], None, "dot", scene[toks], rep)
+        C.check_prim(q_lib, scene[toks], lambda s, m=m: f64(prim_keys[m * Sm + s]), r.k, "dot",
+                     to_np(r.prim[m])[toks], w_lib[m][toks], rep)
+    c = O.criticality(f64(inp["delta"][0]))
+    kept = to_np(r.kept)[: r.n_keep]
+    C.check_kept(c, r.n_keep, kept, rep)
+    C.check_multiscale_hidden(to_np(r.h_in[tsel]), to_np(r.hidden[tsel]), dt, values_rows, r.P, Sm,
+                              to_np(r.scene), to_np(r.prim), w_lib, kept,
+                              f64(ms["w_he_t"]).T, rep, toks)
+    return rep.finish()
+
+
 def check_fused_run(r: FusedRun, tokens=None) -> C.Report:
     """The kept set in full and the fused injection on the sampled tokens
     (routing and lookup are checked by check_run and are the same here)."""

@@ -251,6 +251,33 @@ def test_propagation_entry_points_validate(lib):
         lk.lookme_destroy(h)
 
 
+def test_multiscale_entry_points_validate(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        call = lambda n=8, n_keep=2, d_h=2048, p=FAKE: lk.lookme_inject_multiscale(
+            h, n, n_keep, p, p, p, p, p, d_h, 0)
+        assert S(lambda: call()) == lk.LOOKME_ERR_INVALID                    # none registered
+        assert S(lambda: lk.lookme_set_multiscale(h, 0, 2048, FAKE)) == lk.LOOKME_ERR_UNSUPPORTED
+        assert S(lambda: lk.lookme_set_multiscale(h, 9, 2048, FAKE)) == lk.LOOKME_ERR_UNSUPPORTED
+        assert S(lambda: lk.lookme_set_multiscale(h, 3, 2048, FAKE)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_multiscale(h, 2, 1024, FAKE)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_multiscale(h, 2, 2056, FAKE)) == lk.LOOKME_ERR_UNSUPPORTED
+        assert S(lambda: lk.lookme_set_multiscale(h, 2, 2048, None)) == lk.LOOKME_ERR_INVALID
+        base = lk.lookme_workspace_size(h, 1, 100)
+        assert S(lambda: lk.lookme_set_multiscale(h, 2, 2048, FAKE)) == lk.LOOKME_OK
+        assert lk.lookme_workspace_size(h, 1, 100) >= base + 3 * 100 * 2048 * 2
+        assert S(lambda: call(d_h=4096)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(n_keep=9)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(n_keep=0, p=None)) == lk.LOOKME_OK
+        assert S(lambda: call(p=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call()) == lk.LOOKME_ERR_WORKSPACE
+    finally:
+        lk.lookme_destroy(h)
+
+
 def test_null_handle(lib):
     assert _status(lambda: lk.lookme_workspace_size(None, 1, 1))[0] == lk.LOOKME_ERR_INVALID
     assert _status(lambda: lk.lookme_route(None, 1, 1, 1, FAKE, FAKE, FAKE, FAKE, 0))[0] == \

@@ -217,3 +217,33 @@ def test_propagated_check_accepts_the_oracle_and_rejects_planted_errors():
     touched = good.copy()
     touched[2, 0, 3] = bf(touched[2, 0, 3] + 1.0)
     assert not check(touched).ok
+
+
+def test_multiscale_check_accepts_the_oracle_and_rejects_planted_errors():
+    """check_multiscale_hidden on bf16 data: the oracle's result passes; one
+    computed without the partition offset of each scale, or with a column
+    past d_v changed, fails."""
+    rng = np.random.default_rng(10)
+    n, M, Sm, P, d_v, d_h, k = 10, 2, 3, 5, 16, 24, 2
+    bf = lambda a: O.round_to_dtype(a, "bf16")
+    H = bf(rng.standard_normal((n, d_h)))
+    V = bf(rng.standard_normal((M * Sm * P, d_v)) * 2)
+    scene = rng.integers(0, Sm, (M, n))
+    prim = np.stack([np.stack([rng.permutation(P)[:k] for _ in range(n)]) for _ in range(M)])
+    w = rng.dirichlet(np.ones(k), (M, n))
+    kept = np.array([0, 3, 4, 9])
+    W = bf(rng.standard_normal((d_h, d_v)) / np.sqrt(d_h))
+    bits = O.f64_to_bf16_bits
+
+    def check(out):
+        rep = C.Report()
+        C.check_multiscale_hidden(bits(H), bits(out), "bf16", lambda rows: V[rows], P, Sm, scene,
+                                  prim, w, kept, W, rep, np.arange(n))
+        return rep.finish()
+
+    good = O.inject_multiscale(H, V, P, Sm, scene, prim, w, kept, W, "bf16")
+    assert check(good).ok
+    assert not check(O.inject_multiscale(H, V, P, 0, scene, prim, w, kept, W, "bf16")).ok
+    bad = good.copy()
+    bad[3, d_v + 2] = bf(bad[3, d_v + 2] + 1.0)
+    assert not check(bad).ok

@@ -13,7 +13,7 @@ import torch
 
 from oracle import lookme_oracle as O
 from synth import (WORKLOADS, Workload, make_fusion, make_inputs, make_integer_inputs,
-                   make_propagation, make_relevance)
+                   make_multiscale, make_propagation, make_relevance)
 
 pytestmark = pytest.mark.gpu
 
@@ -369,6 +369,41 @@ def test_propagated_special_cases_match_fused_injection():
     torch.cuda.synchronize()
     assert p0.steps == 0
     assert torch.equal(p0.hidden, f0.hidden)
+
+
+# (workload, scales, sampled tokens or None for all)
+MULTISCALE = {
+    "bf16_ms_small": (Workload("bf16_ms_small", "bf16", 300, 1, 256, 128, 20, 60, 128, 192, 8,
+                               30, usage="iid", value_std=1.0), 2, None),
+    "f32_ms_three": (Workload("f32_ms_three", "f32", 77, 1, 96, 64, 15, 37, 64, 96, 3, 20,
+                              usage="iid", value_std=1.0), 3, None),
+    "bf16_ms_image": (WORKLOADS[1].scaled(value_std=1.0), 2, 80),
+}
+
+
+@pytest.mark.parametrize("name", list(MULTISCALE))
+def test_multiscale_injection(name):
+    """Per-scale projection, routing within the scale's scene partition and
+    lookup, the kept set, and the router's mix of the scales' rows (Eq. 8)
+    against the oracle; two passes agree bit for bit."""
+    from tests.harness import MultiScaleRun, check_multiscale_run
+    wl, scales, sample = MULTISCALE[name]
+    _announce(f"multi-scale {name}: {wl} scales {scales}")
+    inp = make_inputs(wl, seed=9, device=DEV)
+    ms = make_multiscale(wl, 9, scales, device=DEV)
+    r = MultiScaleRun(inp, ms).run()
+    toks = None
+    if sample:
+        kept0 = r.kept.cpu().numpy()[:40]
+        toks = np.unique(np.concatenate(
+            [np.random.default_rng(9).choice(wl.n_tokens, sample, replace=False), kept0]))
+    rep = check_multiscale_run(r, tokens=toks)
+    assert rep.ok, str(rep)
+    assert min(rep.decisions.get(kind, 0) for kind in ("scene", "prim", "hidden_row")) > 0
+    r2 = MultiScaleRun(inp, ms, table=r.table).run()
+    torch.cuda.synchronize()
+    assert torch.equal(r.hidden, r2.hidden)
+    assert int(r.scene.max()) < wl.scenes // scales
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
