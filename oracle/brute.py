@@ -236,3 +236,26 @@ def multiscale_rows(h_rows, w_he_rows, r_scale_rows, mant_bits):
         out.append([sum((a * Fraction(r[c]) for a, r in zip(alpha, rs)), Fraction(0))
                     for c in range(d_v)])
     return out
+
+
+def gate(delta_rows, w_g, pos=None):
+    """Hard SKA gate (Eq. 9) by exact rational dot products: the indices i
+    (into pos, or rows when pos is None) with Delta_{pos[i]} . W_g > 0."""
+    rows = list(range(len(delta_rows))) if pos is None else list(pos)
+    out = []
+    for i, r in enumerate(rows):
+        if dot(delta_rows[r], w_g) > 0:
+            out.append(i)
+    return out
+
+
+def inject_text(hidden_rows, table_rows, pos, ids, kept, rounder):
+    """Text pathway (Eq. 1): H[pos[i]] <- round(H[pos[i]] + E[ids[i]]) for
+    the open gates i, in exact rational arithmetic."""
+    out = [list(map(Fraction, r)) for r in hidden_rows]
+    d_t = len(table_rows[0])
+    for i in kept:
+        t = pos[i]
+        for j in range(d_t):
+            out[t][j] = rounder(Fraction(hidden_rows[t][j]) + Fraction(table_rows[ids[i]][j]))
+    return out

@@ -520,3 +520,79 @@ def check_hidden(h_in: np.ndarray, h_out_lib, dtype: str, values_rows, P: int,
             if np.any(err > bound + 1e-30):
                 rep.fail(f"hidden[{t}]: float32 error beyond 1e-5 relative")
     return worst
+
+
+def check_gate(delta: np.ndarray, w_g: np.ndarray, kept_lib, rep: Report, pos=None):
+    """The learned SKA gate (Eq. 9): the library's open set equals the
+    oracle's {i : Delta_i . W_g > 0} except for gates whose logit lies within
+    the tie band of zero, |z_i| <= 1e-5 * sum_j |Delta_ij W_g,j| (the relative
+    rule applied to the size of the summed terms), each counted as an
+    exemption; strictly ascending and in range.
+
+    delta [rows, d_c] float64 (the rows the gate reads are delta[pos] when pos
+    is given); kept_lib the library's open indices (its first count entries).
+    """
+    rows = delta if pos is None else delta[np.asarray(pos, dtype=np.int64)]
+    n = rows.shape[0]
+    kept_lib = np.asarray(kept_lib, dtype=np.int64)
+    rep.count("gate", max(1, n))
+    if kept_lib.size and (np.any(kept_lib < 0) or np.any(kept_lib >= n)):
+        rep.fail("gate: index out of range")
+        return
+    if np.any(np.diff(kept_lib) <= 0):
+        rep.fail("gate: not strictly ascending")
+        return
+    ref = O.gate(rows, w_g)
+    if np.array_equal(ref, kept_lib):
+        return
+    z = O.gate_logits(rows, w_g)
+    band = REL_TIE * (np.abs(rows) @ np.abs(np.asarray(w_g, dtype=np.float64)))
+    diff = np.setxor1d(ref, kept_lib)
+    for i in diff:
+        if abs(z[i]) > band[i]:
+            rep.fail(f"gate: row {i} (z={z[i]!r}) {'opened' if i in kept_lib else 'closed'} "
+                     f"against the oracle")
+            return
+    rep.exempt("gate", int(diff.size))
+
+
+def check_text_hidden(h_in: np.ndarray, h_out_lib, dtype: str, table: np.ndarray, pos, ids,
+                      kept, rep: Report, contract_abs: float = 2e-2):
+    """The text pathway's injection (Eq. 1, Eq. 10) recomputed with the
+    library's open set: rows not at an open text position keep their bits,
+    columns >= d_t keep their bits, and the sum H + E_text[u] (exact in
+    float64) must come back correctly rounded: a float32 addition of two
+    stored values rounds once, so bf16 results may differ from the direct
+    rounding only where the float32 sum was itself inexact (counted in the
+    notes, bounded by the contract) and float32 results must be bit-exact."""
+    h_in_f = O.to_f64(h_in, dtype)
+    h_lib_f = O.to_f64(h_out_lib, dtype)
+    d_t = table.shape[1]
+    touched = {int(pos[i]): int(ids[i]) for i in np.asarray(kept, dtype=np.int64)}
+    for t in range(h_in.shape[0]):
+        rep.count("text_row")
+        if t not in touched:
+            if not np.array_equal(np.asarray(h_in[t]).view(np.uint8),
+                                  np.asarray(h_out_lib[t]).view(np.uint8)):
+                rep.fail(f"text: untouched row {t} modified")
+            continue
+        if not np.array_equal(np.asarray(h_in[t, d_t:]).view(np.uint8),
+                              np.asarray(h_out_lib[t, d_t:]).view(np.uint8)):
+            rep.fail(f"text: row {t} columns >= d_t modified")
+        exact = h_in_f[t, :d_t] + table[touched[t]]
+        want = O.round_to_dtype(exact, dtype)
+        got = h_lib_f[t, :d_t]
+        if dtype == "f32":
+            if not np.array_equal(got, want):
+                rep.fail(f"text: row {t} differs from the correctly rounded float32 sum")
+        else:
+            err = float(np.max(np.abs(got - want)))
+            if err > contract_abs:
+                rep.fail(f"text: row {t} max-abs {err:.3g} > {contract_abs}")
+            s32 = exact.astype(np.float32).astype(np.float64)
+            ok = (got == want) | (got == O.round_to_dtype(s32, dtype))
+            if not np.all(ok):
+                rep.fail(f"text: row {t}: {int((~ok).sum())} elements neither the direct nor "
+                         f"the float32-then-bf16 rounding")
+            rep.notes["text_double_rounded"] = (rep.notes.get("text_double_rounded", 0)
+                                                + int(np.sum(got != want)))

@@ -39,6 +39,15 @@ What is computed, step by step (each function cites its passage):
               two-layer MLP over [v_e, e_img[j]] gives relevance logits r_j;
               the top-k primitives by r are weighted by the softmax of
               cos(v_e, e_{j,p}) + tanh(r_j[p])
+  gate        Eq. 9 at inference: the hard, noise-free SKA gate keeps the
+              positions with Delta_i W_g > 0 (a learned gate, variable count)
+  text        Sec. 3.2 "Text embedding index-based lookup" (Eq. 1):
+              R_text = E_text[u] at the text positions; inject_text adds it
+  lookme_layer  Eq. 3: one LookME layer, L_dec(H_in) plus the text, image and
+              cross-modal pathways' gated injections in that order; the
+              cross-modal pathway queries the two-level lookup with L_dec(H_in)
+              itself at every position (Sec. 3.2, cross-modal embedding
+              hierarchical two-level lookup)
 
 Readings of the paper taken here (the paper is silent or differs from the
 configured workloads; each is listed in the design notes of the repository):
@@ -528,3 +537,107 @@ def inject_fused(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarr
     F = fusion(round_to_dtype(R, dtype), w_gate, w_up, w_down, dtype)
     out[kept] = round_to_dtype(hidden[kept] + F, dtype)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Learned SKA gate (Eq. 9), the text pathway (Sec. 3.2, ID lookup) and one
+# whole LookME layer with its three pathways (Eq. 3)
+# ---------------------------------------------------------------------------
+
+def gate_logits(delta: np.ndarray, w_g: np.ndarray) -> np.ndarray:
+    """Argument of the SKA gate (Eq. 9): z_i = Delta_i W_g, with W_g a
+    single column of width d_c.  delta [n, d_c], w_g [d_c] -> [n]."""
+    return delta @ np.asarray(w_g, dtype=np.float64)
+
+
+def gate(delta: np.ndarray, w_g: np.ndarray, pos: np.ndarray | None = None) -> np.ndarray:
+    """The SKA gate as it acts at inference (Eq. 9-10): the Gumbel-Sigmoid is
+    hard and noise-free, so g_i = 1 exactly when sigma(z_i) > 1/2, i.e. when
+    z_i > 0 (z_i = 0 stays closed).  The gate reads the rows of delta at the
+    pathway's positions ``pos`` (all rows when None) and returns the indices
+    i (into ``pos``) of the open gates in ascending order: the positions
+    R[g] of Eq. 10 takes."""
+    rows = delta if pos is None else delta[np.asarray(pos, dtype=np.int64)]
+    return np.flatnonzero(gate_logits(rows, w_g) > 0).astype(np.int32)
+
+
+def text_rows(table: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """Text pathway retrieval (Eq. 1 and Sec. 3.2 "Text embedding index-based
+    lookup"): R_text = E_text[u], one table row per text token id."""
+    return table[np.asarray(ids, dtype=np.int64)]
+
+
+def inject_text(hidden: np.ndarray, table: np.ndarray, pos: np.ndarray, ids: np.ndarray,
+                kept: np.ndarray, dtype: str) -> np.ndarray:
+    """Sparse injection of the text pathway (Eq. 10 with the prefix add):
+    for every open gate i, H[pos[i], :d_t] <- round(H[pos[i], :d_t] +
+    E_text[ids[i]]); every other element unchanged.  hidden [n, d_h], table
+    [V, d_t]; returns float64 values of dtype."""
+    out = np.array(hidden, dtype=np.float64, copy=True)
+    d_t = table.shape[1]
+    pos = np.asarray(pos, dtype=np.int64)
+    for i in np.asarray(kept, dtype=np.int64):
+        t = pos[i]
+        out[t, :d_t] = round_to_dtype(hidden[t, :d_t] + text_rows(table, [ids[i]])[0], dtype)
+    return out
+
+
+def lookme_layer(h_dec: np.ndarray, delta: np.ndarray, *, dtype: str, text=None, image=None,
+                 cross=None):
+    """One LookME layer (Eq. 3): H_out = L_dec(H_in) + S(R_text) + S(R_img)
+    + S(R_cross), the pathways' sparse injections fused into the backbone
+    one after another in that order, each a residual add rounded once to
+    dtype.  Every pathway reads the layer's inputs, not a partly injected
+    state: the image and cross-modal queries and all three gates are taken
+    before the first add.
+
+    h_dec [n, d_h]  L_dec(H_in), the decoder layer's output (float64 values)
+    delta [n, d_c]  Delta = Attn(H_in), shared by the three gates (Eq. 9)
+    text  = (pos [n_t], ids [n_t], table [V, d_t], w_g [d_c]): the text
+            positions and their token ids (Sec. 3.2, text pathway)
+    image = (start, x [n_i, d_in], w_t [d_e, d_in], scene_keys, prim_keys,
+            values, k, w_g): image positions start .. start + n_i - 1, whose
+            encoder embeddings x are projected and looked up (Eq. 4-7)
+    cross = (w_t [d_e, d_h], scene_keys, prim_keys, values, k, w_g): every
+            position, queried by its own h_dec row (Sec. 3.2, cross-modal
+            pathway), against the pathway's own table
+    A pathway given as None is absent.  Returns a dict with "hidden" and the
+    per-pathway results (gates, scenes, primitives, weights)."""
+    out = np.array(h_dec, dtype=np.float64, copy=True)
+    res = {}
+    plans = []
+    if text is not None:
+        pos, ids, table, w_g = text
+        kept = gate(delta, w_g, pos)
+        res["text_kept"] = kept
+        plans.append(("text", pos, ids, table, kept))
+    if image is not None:
+        start, x, w_t, sk, pk, vals, k, w_g = image
+        n_i = x.shape[0]
+        q = project(x, w_t, dtype)
+        sc = route(q, sk)
+        pr, ww, _ = lookup(q, sc, pk, k)
+        kept = gate(delta[start:start + n_i], w_g)
+        res.update(img_q=q, img_scene=sc, img_prim=pr, img_w=ww, img_kept=kept)
+        plans.append(("image", start, n_i, vals, sk.shape[0], pk.shape[1], sc, pr, ww, kept))
+    if cross is not None:
+        w_t, sk, pk, vals, k, w_g = cross
+        q = project(h_dec, w_t, dtype)
+        sc = route(q, sk)
+        pr, ww, _ = lookup(q, sc, pk, k)
+        kept = gate(delta, w_g)
+        res.update(cross_q=q, cross_scene=sc, cross_prim=pr, cross_w=ww, cross_kept=kept)
+        plans.append(("cross", vals, pk.shape[1], sc, pr, ww, kept))
+    for plan in plans:
+        if plan[0] == "text":
+            _, pos, ids, table, kept = plan
+            out = inject_text(out, table, pos, ids, kept, dtype)
+        elif plan[0] == "image":
+            _, start, n_i, vals, _, P, sc, pr, ww, kept = plan
+            out[start:start + n_i] = inject(out[start:start + n_i], vals, P, sc, pr, ww, kept,
+                                            dtype)
+        else:
+            _, vals, P, sc, pr, ww, kept = plan
+            out = inject(out, vals, P, sc, pr, ww, kept, dtype)
+    res["hidden"] = out
+    return res

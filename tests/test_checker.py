@@ -247,3 +247,54 @@ def test_multiscale_check_accepts_the_oracle_and_rejects_planted_errors():
     bad = good.copy()
     bad[3, d_v + 2] = bf(bad[3, d_v + 2] + 1.0)
     assert not check(bad).ok
+
+
+def test_gate_checker_accepts_oracle_exempts_near_zero_and_rejects_flips():
+    rng = np.random.default_rng(30)
+    D = O.round_to_bf16(rng.standard_normal((200, 24)))
+    wg = O.round_to_bf16(rng.standard_normal(24))
+    kept = O.gate(D, wg)
+    rep = C.Report()
+    C.check_gate(D, wg, kept, rep)
+    assert rep.finish().ok and not rep.exemptions
+    # a logit planted at a few ulps above zero may go either way
+    D2 = D.copy()
+    D2[7] = 0.0
+    D2[7, 0], D2[7, 1] = 1.0, -(1.0 - 2.0 ** -20)
+    wg2 = wg.copy()
+    wg2[0], wg2[1] = 1.0, 1.0
+    ref = O.gate(D2, wg2)
+    assert 7 in ref
+    rep = C.Report()
+    C.check_gate(D2, wg2, np.setdiff1d(ref, [7]), rep)
+    assert rep.finish().ok and rep.exemptions == {"gate": 1}
+    # a clear sign flip, a duplicate and an unsorted list are rejected
+    bad = np.union1d(kept, [int(np.argmin(O.gate_logits(D, wg)))])
+    for wrong in (bad, np.concatenate([kept[:3], kept[2:]]), kept[::-1]):
+        rep = C.Report()
+        C.check_gate(D, wg, wrong, rep)
+        assert not rep.finish().ok
+    pos = rng.permutation(200)[:50]
+    rep = C.Report()
+    C.check_gate(D, wg, O.gate(D, wg, pos), rep, pos=pos)
+    assert rep.finish().ok
+
+
+def test_text_checker_accepts_oracle_and_rejects_wrong_rows():
+    rng = np.random.default_rng(31)
+    table = O.round_to_bf16(rng.standard_normal((17, 6)) * 0.5)
+    H = O.round_to_bf16(rng.standard_normal((12, 9)))
+    pos, ids, kept = np.array([11, 2, 5, 0]), np.array([3, 16, 3, 8]), np.array([0, 1, 3])
+    out = O.inject_text(H, table, pos, ids, kept, "bf16")
+    hb, ob = O.from_f64(H, "bf16"), O.from_f64(out, "bf16")
+    rep = C.Report()
+    C.check_text_hidden(hb, ob, "bf16", table, pos, ids, kept, rep)
+    assert rep.finish().ok, str(rep)
+    wrong = O.from_f64(O.inject_text(H, table, pos, ids[::-1], kept, "bf16"), "bf16")
+    rep = C.Report()
+    C.check_text_hidden(hb, wrong, "bf16", table, pos, ids, kept, rep)
+    assert not rep.finish().ok
+    extra = O.from_f64(O.inject_text(H, table, pos, ids, np.arange(4), "bf16"), "bf16")
+    rep = C.Report()
+    C.check_text_hidden(hb, extra, "bf16", table, pos, ids, kept, rep)
+    assert not rep.finish().ok

@@ -859,3 +859,153 @@ def test_run_multiscale_routes_each_scale_within_its_partition():
     planted = O.run_multiscale(x, wt, K1p, K2, V, D, H, Whe, k=k, n_keep=4, dtype="f32")
     assert np.mean(planted["scene"][0] == 1) > 0.5
     np.testing.assert_array_equal(planted["scene"][1], two["scene"][1])
+
+
+# --------------------------------------------------------------------------
+# Learned SKA gate (Eq. 9), text pathway (Eq. 1), one LookME layer (Eq. 3)
+# --------------------------------------------------------------------------
+
+def test_gate_matches_exact_rational_brute_force_with_exact_zeros():
+    """Catches a wrong threshold (>= instead of >), a transposed operand or a
+    dropped row: small-integer Delta and W_g make many logits exactly 0,
+    which must stay closed, and every other sign is exact."""
+    rng = np.random.default_rng(70)
+    delta = rng.integers(-2, 3, size=(60, 6)).astype(np.float64)
+    w_g = rng.integers(-2, 3, size=6).astype(np.float64)
+    z = [B.dot(r, w_g.tolist()) for r in delta.tolist()]
+    assert sum(1 for v in z if v == 0) >= 3      # the case is exercised
+    assert O.gate(delta, w_g).tolist() == B.gate(delta.tolist(), w_g.tolist())
+    pos = rng.permutation(60)[:25]
+    assert O.gate(delta, w_g, pos).tolist() == B.gate(delta.tolist(), w_g.tolist(),
+                                                      pos.tolist())
+
+
+def test_gate_planted_signs_and_degenerate_weights():
+    """Planted: Delta_i = gamma_i e_3 and W_g = e_3 open exactly where
+    gamma_i > 0; W_g = 0 closes every gate; a positive scale of W_g changes
+    nothing and a negated W_g opens exactly the complement (no zero logits in
+    Gaussian data)."""
+    rng = np.random.default_rng(71)
+    gamma = rng.standard_normal(40)
+    delta = np.zeros((40, 5))
+    delta[:, 3] = gamma
+    e3 = np.eye(5)[3]
+    assert O.gate(delta, e3).tolist() == np.flatnonzero(gamma > 0).tolist()
+    assert O.gate(delta, np.zeros(5)).size == 0
+    d2 = _bf16_values(rng, (300, 16))
+    w = _bf16_values(rng, 16)
+    a = O.gate(d2, w)
+    np.testing.assert_array_equal(a, O.gate(d2, 2.0 ** 7 * w))
+    b = O.gate(d2, -w)
+    assert np.intersect1d(a, b).size == 0
+    np.testing.assert_array_equal(np.union1d(a, b), np.arange(300))
+    # opens about half the gates on zero-mean data, in ascending order
+    assert 100 < a.size < 200 and np.all(np.diff(a) > 0)
+
+
+def test_inject_text_matches_brute_force_and_float32_addition():
+    """Catches a wrong row (id vs position), a write outside the open gates or
+    a second rounding: exact rational brute force in bf16, and in float32 the
+    result must equal numpy's own float32 addition (one correctly rounded
+    add) bit for bit."""
+    rng = np.random.default_rng(72)
+    V, d_t, d_h, n = 11, 5, 7, 9
+    table = _bf16_values(rng, (V, d_t), 0.5)
+    hidden = _bf16_values(rng, (n, d_h))
+    pos = np.array([8, 0, 3, 5, 6])
+    ids = np.array([4, 4, 10, 0, 7])
+    kept = np.array([0, 1, 3])
+    got = O.inject_text(hidden, table, pos, ids, kept, "bf16")
+    ref = B.inject_text(hidden.tolist(), table.tolist(), pos.tolist(), ids.tolist(),
+                        kept.tolist(), B.round_bf16)
+    for t in range(n):
+        assert [Fraction(float(v)) for v in got[t]] == ref[t]
+    # untouched: positions 3 (gate closed), 6 (closed), 1, 2, 4, 7 (not text)
+    for t in (1, 2, 3, 4, 6, 7):
+        np.testing.assert_array_equal(got[t], hidden[t])
+    h32 = rng.standard_normal((n, d_h)).astype(np.float32)
+    t32 = rng.standard_normal((V, d_t)).astype(np.float32)
+    g32 = O.inject_text(h32.astype(np.float64), t32.astype(np.float64), pos, ids, kept, "f32")
+    want = h32.copy()
+    for i in kept:
+        want[pos[i], :d_t] = h32[pos[i], :d_t] + t32[ids[i]]
+    np.testing.assert_array_equal(g32.astype(np.float32), want)
+    zero = O.inject_text(np.zeros((n, d_h)), table, pos, ids, np.arange(5), "bf16")
+    np.testing.assert_array_equal(zero[8, :d_t], table[4])
+    np.testing.assert_array_equal(zero[0, :d_t], table[4])
+
+
+def _layer_inputs(seed, n=20, d_h=16, d_c=12, start=6, n_i=9):
+    rng = np.random.default_rng(seed)
+    d_in, d_e, S, P, d_v, k, V, d_t = 10, 8, 4, 6, 12, 3, 13, 10
+    h_dec = _bf16_values(rng, (n, d_h))
+    delta = _bf16_values(rng, (n, d_c))
+    text_pos = np.array([0, 1, 2, 3, 17, 19])
+    text = (text_pos, rng.integers(0, V, size=text_pos.size), _bf16_values(rng, (V, d_t), 0.5),
+            _bf16_values(rng, d_c))
+    image = (start, _bf16_values(rng, (n_i, d_in)), _bf16_values(rng, (d_e, d_in), 0.3),
+             O.round_to_bf16(_unit(rng, (S, d_e))), O.round_to_bf16(_unit(rng, (S, P, d_e))),
+             _bf16_values(rng, (S * P, d_v), 0.5), k, _bf16_values(rng, d_c))
+    cross = (_bf16_values(rng, (d_e, d_h), 0.3), O.round_to_bf16(_unit(rng, (S, d_e))),
+             O.round_to_bf16(_unit(rng, (S, P, d_e))), _bf16_values(rng, (S * P, d_v), 0.5),
+             k, _bf16_values(rng, d_c))
+    return h_dec, delta, text, image, cross
+
+
+def test_lookme_layer_closed_gates_and_single_pathways():
+    """W_g = 0 for every pathway leaves L_dec(H_in) bit-identical; with one
+    pathway present the layer reduces to that pathway's own injection (text:
+    inject_text at the gated positions; image: route/lookup/inject on the
+    image block; cross: the same on every position, queried by h_dec)."""
+    h_dec, delta, text, image, cross = _layer_inputs(73)
+    zt = text[:3] + (np.zeros_like(text[3]),)
+    zi = image[:7] + (np.zeros_like(image[7]),)
+    zc = cross[:5] + (np.zeros_like(cross[5]),)
+    r = O.lookme_layer(h_dec, delta, dtype="bf16", text=zt, image=zi, cross=zc)
+    np.testing.assert_array_equal(r["hidden"], h_dec)
+    rt = O.lookme_layer(h_dec, delta, dtype="bf16", text=text)
+    kept_t = B.gate(delta.tolist(), text[3].tolist(), text[0].tolist())
+    assert kept_t and rt["text_kept"].tolist() == kept_t
+    ref = B.inject_text(h_dec.tolist(), text[2].tolist(), text[0].tolist(), text[1].tolist(),
+                        kept_t, B.round_bf16)
+    np.testing.assert_array_equal(rt["hidden"], np.array([[float(v) for v in r_] for r_ in ref]))
+    start, x, w_t, sk, pk, vals, k, w_g = image
+    ri = O.lookme_layer(h_dec, delta, dtype="bf16", image=image)
+    q = B.project(x.tolist(), w_t.tolist(), B.round_bf16)
+    sc = B.route(q, sk.tolist())
+    S, P, d_e = pk.shape
+    prim, top = B.lookup_flat_sim(q, sc, pk.reshape(S * P, d_e).tolist(), P, k)
+    assert ri["img_scene"].tolist() == sc and ri["img_prim"].tolist() == prim
+    kept_i = B.gate(delta[start:start + x.shape[0]].tolist(), w_g.tolist())
+    assert kept_i and ri["img_kept"].tolist() == kept_i
+    blk = B.inject(h_dec[start:start + x.shape[0]].tolist(), vals.tolist(), P, sc, prim,
+                   ri["img_w"].tolist(), kept_i, B.round_bf16)
+    want = h_dec.copy()
+    want[start:start + x.shape[0]] = np.array([[float(v) for v in r_] for r_ in blk])
+    np.testing.assert_array_equal(ri["hidden"], want)
+    rc = O.lookme_layer(h_dec, delta, dtype="bf16", cross=cross)
+    qc = B.project(h_dec.tolist(), cross[0].tolist(), B.round_bf16)
+    assert rc["cross_scene"].tolist() == B.route(qc, cross[1].tolist())
+    kept_c = B.gate(delta.tolist(), cross[5].tolist())
+    assert kept_c and rc["cross_kept"].tolist() == kept_c
+
+
+def test_lookme_layer_pathways_read_the_layer_inputs_and_add_in_order():
+    """The cross-modal query is L_dec(H_in), not a partly injected state: the
+    full layer's cross-modal lookup equals the cross-only layer's even with
+    loud text and image rows.  The adds run text, image, cross, each rounded:
+    the full result equals chaining the three single-pathway layers, each on
+    the previous result, with the cross-modal lookup kept from h_dec."""
+    h_dec, delta, text, image, cross = _layer_inputs(74)
+    full = O.lookme_layer(h_dec, delta, dtype="bf16", text=text, image=image, cross=cross)
+    rc = O.lookme_layer(h_dec, delta, dtype="bf16", cross=cross)
+    for name in ("cross_q", "cross_scene", "cross_prim", "cross_w", "cross_kept"):
+        np.testing.assert_array_equal(full[name], rc[name])
+    a = O.lookme_layer(h_dec, delta, dtype="bf16", text=text)["hidden"]
+    b = O.lookme_layer(a, delta, dtype="bf16", image=image)["hidden"]
+    c = O.inject(b, cross[3], cross[2].shape[1], rc["cross_scene"], rc["cross_prim"],
+                 rc["cross_w"], rc["cross_kept"], "bf16")
+    np.testing.assert_array_equal(full["hidden"], c)
+    # the text and image positions overlap the cross-modal ones: a changed
+    # order would round differently somewhere
+    assert np.intersect1d(text[0][full["text_kept"]], full["cross_kept"]).size > 0
