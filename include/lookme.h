@@ -313,6 +313,98 @@ lookme_status_t lookme_inject_multiscale(lookme_t h, int64_t n, int64_t n_keep,
                                          int32_t d_h, void* stream);
 
 /*
+ * lookme_gate -- the learned SKA gate of the intra-layer sparse activation
+ * (Sec. 3.3, Eq. 9) as it acts at inference: the Gumbel-Sigmoid is hard and
+ * noise-free, so entry i of a layer opens exactly when
+ *   z_i = Delta_{row(i)} . W_g > 0                (z_i = 0 stays closed)
+ * with row(i) = pos[i] (pos non-NULL: the pathway's positions in a longer
+ * sequence, e.g. the text positions) or i.  Per pathway and layer it gives
+ * the variable set of positions whose retrieved rows Eq. 10 injects.
+ *   delta     [layers, delta_rows, d_c] dtype, Delta = Attn(H_in) of each layer
+ *   pos       [n] int32 row of each entry (clamped into [0, delta_rows)), or
+ *             NULL (then delta_rows >= n and entry i reads row i)
+ *   w_g       [layers, d_c] dtype, each layer's gate projection W_g
+ *   kept_out  [layers, n] int32: the open entries i of layer l in ascending
+ *             order, then -1 up to n
+ *   count_out [layers] int32: the number of open entries of each layer
+ * z is accumulated in float32 (fused multiply-adds over d_c) and compared
+ * with 0 in that precision.  d_c * elem_size a multiple of 16 bytes.  n = 0
+ * writes count_out = 0 and nothing else.  Needs the workspace of
+ * lookme_workspace_size(layers, n); it uses the same part as lookme_select,
+ * so a gate and a select on one handle must not run concurrently.
+ */
+lookme_status_t lookme_gate(lookme_t h, int32_t layers, int64_t n, const void* delta,
+                            int64_t delta_rows, int32_t d_c, const int32_t* pos, const void* w_g,
+                            int32_t* kept_out, int32_t* count_out, void* stream);
+
+/*
+ * lookme_inject_gated -- lookme_inject_kept for the counted lists of
+ * lookme_gate (Eq. 10 with the learned gate, prefix add of Eq. 2):
+ *   kept  [layers, n] int32, layer l's open token ids in its first count[l]
+ *         entries (the rest is not read)
+ *   count [layers] int32, read on the device
+ * scene, prim, w and hidden as for lookme_inject_kept.  Launches layers * n
+ * workgroups, those past a layer's count end at once.  Needs no workspace.
+ */
+lookme_status_t lookme_inject_gated(lookme_t h, int32_t layers, int64_t n, const int32_t* kept,
+                                    const int32_t* count, const int32_t* scene,
+                                    const int32_t* prim, const float* w, void* hidden,
+                                    int32_t d_h, void* stream);
+
+/*
+ * lookme_inject_fused_gated -- lookme_inject_fused (Eq. 10 through the
+ * SwiGLU fusion f) for the counted lists of lookme_gate: kept [layers, n]
+ * and count [layers] as for lookme_inject_gated, S(R) = g . f(R[g]) on the
+ * open rows only.  Needs the workspace of lookme_workspace_size(layers, n)
+ * queried after lookme_set_fusion.
+ */
+lookme_status_t lookme_inject_fused_gated(lookme_t h, int32_t layers, int64_t n,
+                                          const int32_t* kept, const int32_t* count,
+                                          const int32_t* scene, const int32_t* prim,
+                                          const float* w, void* hidden, int32_t d_h,
+                                          void* stream);
+
+/*
+ * lookme_inject_propagated_gated -- lookme_inject_propagated (Eq. 11) with
+ * the LookME layer's learned gate reused by the layers after it: kept [n]
+ * int32 holds the open token ids in its first count[0] entries (a one-layer
+ * lookme_gate), count [1] int32 is read on the device.  Everything else as
+ * for lookme_inject_propagated; the workspace of
+ * lookme_workspace_size(steps + 1, n) queried after lookme_set_fusion.
+ */
+lookme_status_t lookme_inject_propagated_gated(lookme_t h, int32_t steps, int64_t n,
+                                               const int32_t* kept, const int32_t* count,
+                                               const int32_t* scene, const int32_t* prim,
+                                               const float* w, void* hidden, int32_t d_h,
+                                               void* stream);
+
+/*
+ * lookme_inject_text -- the text pathway of a LookME layer (Sec. 3.2, "Text
+ * embedding index-based lookup", Eq. 1): a text position's token id indexes
+ * the layer's text table, R_text = E_text[u], and the open entries of the
+ * pathway's gate (Eq. 9-10) add it into their hidden rows:
+ *   for the first count[0] entries j of kept (all n_text of them when count
+ *   is NULL; kept NULL: j itself), with i = kept[j]:
+ *     hidden[pos[i], :d_t] <- round(hidden[pos[i], :d_t] + table[ids[i], :])
+ * float32 sum, one rounding; every other element keeps its bits.
+ *   dtype  lookme_dtype_t of table and hidden (no handle: the text table is
+ *          not the image table)
+ *   table  [vocab, d_t], borrowed for the call
+ *   pos    [n_text] int32 text positions in [0, n) (clamped), pairwise
+ *          distinct (two entries on one position race)
+ *   ids    [n_text] int32 token ids in [0, vocab) (clamped)
+ *   kept   [n_text] int32 entries of pos/ids (lookme_gate with pos), or NULL
+ *   count  [1] int32 on the device, or NULL
+ *   hidden [n, d_h], updated in place
+ * Requires d_t <= d_h and d_t * elem_size, d_h * elem_size multiples of 16
+ * bytes.  n_text = 0 does nothing.  Needs no workspace.
+ */
+lookme_status_t lookme_inject_text(int32_t dtype, const void* table, int64_t vocab, int32_t d_t,
+                                   int64_t n_text, const int32_t* pos, const int32_t* ids,
+                                   const int32_t* kept, const int32_t* count, void* hidden,
+                                   int64_t n, int32_t d_h, void* stream);
+
+/*
  * Measurement support (not part of the method).  When enabled, each kernel
  * group that route/lookup/inject launches is bracketed by a pair of HIP timing
  * events recorded on the call's stream.  lookme_profile_read waits for the

@@ -99,4 +99,29 @@ __device__ __forceinline__ int xcd_remap(int b, int count) {
   return u < count ? u : -1;
 }
 
+// Inclusive prefix sum over the threads of one wave.
+__device__ __forceinline__ int wave_scan_incl(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int o = __shfl_up(v, d, 64);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Inclusive prefix sum over the first `waves` waves of the block (all
+// threads of the block must call it; threads beyond them pass 0).
+template <int MAXW>
+__device__ __forceinline__ int block_scan_incl(int v, int* wsum) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int incl = wave_scan_incl(v);
+  if (lane == 63 && wv < MAXW) wsum[wv] = incl;
+  __syncthreads();
+  int off = 0;
+  for (int w = 0; w < wv && w < MAXW; ++w) off += wsum[w];
+  __syncthreads();
+  return incl + off;
+}
+
 }  // namespace lookme

@@ -22,7 +22,7 @@ namespace lookme {
 
 hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int64_t n_keep,
                          const int32_t* kept, int64_t kept_batch, int d_v, const void* r, void* u,
-                         void* hidden, hipStream_t st) {
+                         void* hidden, hipStream_t st, const int32_t* count) {
   if (n == 0 || n_keep == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const int64_t rt = (n_keep + TgShape::BM - 1) / TgShape::BM;
@@ -41,6 +41,8 @@ hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int6
   g1.cols = f.d_ff;
   g1.ksplit = (int)(g1.k_bytes / TG_KB);
   g1.tiles = (int)(rt * ((f.d_ff + TgShape::BN / 2 - 1) / (TgShape::BN / 2)));
+  g1.count = count;
+  g1.count_step = kept_batch != 0 ? 1 : 0;
   hipError_t e = launch_tile_gemm<EPI_SWIGLU>(dt, g1, layers, st);
   if (e != hipSuccess) return e;
 
@@ -60,11 +62,13 @@ hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int6
   g2.cols = f.d_h;
   g2.ksplit = (int)(g2.k_bytes / TG_KB);
   g2.tiles = (int)(rt * ((f.d_h + TgShape::BN - 1) / TgShape::BN));
+  g2.count = count;
+  g2.count_step = g1.count_step;
   return launch_tile_gemm<EPI_RESID>(dt, g2, layers, st);
 }
 
 hipError_t launch_propagate(int dt, const void* w_p_t, int steps, int64_t n_keep, int d_v,
-                            void* r, hipStream_t st) {
+                            void* r, hipStream_t st, const int32_t* count) {
   if (n_keep == 0) return hipSuccess;
   const int64_t es = dt == DT_BF16 ? 2 : 4;
   const int64_t slice = n_keep * d_v * es;
@@ -81,6 +85,8 @@ hipError_t launch_propagate(int dt, const void* w_p_t, int steps, int64_t n_keep
     g.cols = d_v;
     g.ksplit = (int)(g.k_bytes / TG_KB);
     g.tiles = (int)(rt * ((d_v + TgShape::BN - 1) / TgShape::BN));
+    g.count = count;
+    g.count_step = 0;
     const hipError_t e = launch_tile_gemm<EPI_ADD>(dt, g, 1, st);
     if (e != hipSuccess) return e;
   }

@@ -59,31 +59,6 @@ __global__ __launch_bounds__(NORM_WAVES * WAVE) void crit_norm_kernel(
   if (lane == 0) key[r] = as_u32(acc);
 }
 
-// Inclusive prefix sum over the threads of one wave.
-__device__ __forceinline__ int wave_scan_incl(int v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int o = __shfl_up(v, d, 64);
-    if (lane >= d) v += o;
-  }
-  return v;
-}
-
-// Inclusive prefix sum over the first `waves` waves of the block (all
-// threads of the block must call it; threads beyond them pass 0).
-template <int MAXW>
-__device__ __forceinline__ int block_scan_incl(int v, int* wsum) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int incl = wave_scan_incl(v);
-  if (lane == 63 && wv < MAXW) wsum[wv] = incl;
-  __syncthreads();
-  int off = 0;
-  for (int w = 0; w < wv && w < MAXW; ++w) off += wsum[w];
-  __syncthreads();
-  return incl + off;
-}
-
 // CN > 0: a layer's keys (n <= CN) are first copied to LDS, so that the four
 // passes and the compaction read them there instead of from L2 (one global
 // round trip instead of five).  Element i sits at i + i / 32: the padding
@@ -178,16 +153,20 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
 // router's input, [rows, d_v]) instead of being added into H.  Layer l reads
 // its kept list at kept + l * kept_batch (0: one list for all layers) and
 // its scenes (clamped into [0, S)) from scene l * scene_step of the table
-// (multi-scale: scale l's partition).
+// (multi-scale: scale l's partition).  With a count array only the first
+// count entries of a kept list are used (count[l], or count[0] for a list
+// shared by all layers).
 template <int DT, int K, bool TO_R = false>
 __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
     int64_t n, int64_t n_keep, const int32_t* __restrict__ kept_all,
     const int32_t* __restrict__ scene_all, const int32_t* __restrict__ prim_all,
     const float* __restrict__ w_all, const char* __restrict__ values, int S, int P, int k,
     int64_t v_bytes, char* __restrict__ hidden, int64_t h_bytes, int64_t kept_batch,
-    int scene_step) {
+    int scene_step, const int32_t* __restrict__ count) {
   const int64_t j = blockIdx.x;
   const int64_t layer = j / n_keep;
+  // counted lists (the learned gate): entries past the list's count are unused
+  if (count != nullptr && j - layer * n_keep >= count[kept_batch != 0 ? layer : 0]) return;
   int64_t t = kept_all[layer * kept_batch + (j - layer * n_keep)];
   t = t < 0 ? 0 : (t >= n ? n - 1 : t);
   const int64_t row = layer * n + t;
@@ -255,14 +234,16 @@ template <int DT, bool TO_R = false>
 static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_t n_keep,
                             const int32_t* kept, const int32_t* scene, const int32_t* prim,
                             const float* w, const char* values, int S, int P, int64_t vb,
-                            char* hidden, int64_t hb, int64_t kept_batch, int scene_step) {
+                            char* hidden, int64_t hb, int64_t kept_batch, int scene_step,
+                            const int32_t* count = nullptr) {
   // as many whole waves as the row has 16-byte chunks (up to 256 threads):
   // narrow rows leave no thread idle, and the CU holds more workgroups
   const int ch = (int)(vb / 16);
   const int bs = ch >= INJ_THREADS ? INJ_THREADS : (ch + 63) / 64 * 64;
 #define LOOKME_INJ(K_)                                                                \
   hipLaunchKernelGGL((inject_kernel<DT, K_, TO_R>), grid, dim3(bs), 0, st, n, n_keep, kept, \
-                     scene, prim, w, values, S, P, kk, vb, hidden, hb, kept_batch, scene_step)
+                     scene, prim, w, values, S, P, kk, vb, hidden, hb, kept_batch, scene_step, \
+                     count)
   if (kk <= 4) LOOKME_INJ(4);
   else if (kk <= 8) LOOKME_INJ(8);
   else if (kk <= 16) LOOKME_INJ(16);
@@ -302,36 +283,39 @@ hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint3
 hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
                               const int32_t* scene, const int32_t* prim, const float* w,
                               const void* values, int S, int P, int d_v, int k, void* hidden,
-                              int d_h, hipStream_t st) {
+                              int d_h, hipStream_t st, const int32_t* count) {
   if (n == 0 || n_keep == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const dim3 grid((unsigned)(layers * n_keep));
   if (dt == DT_BF16)
     launch_inject_k<DT_BF16>(k, grid, st, n, n_keep, kept, scene, prim, w,
                              static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                             static_cast<char*>(hidden), (int64_t)d_h * es, n_keep, 0);
+                             static_cast<char*>(hidden), (int64_t)d_h * es, n_keep, 0, count);
   else
     launch_inject_k<DT_F32>(k, grid, st, n, n_keep, kept, scene, prim, w,
                             static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                            static_cast<char*>(hidden), (int64_t)d_h * es, n_keep, 0);
+                            static_cast<char*>(hidden), (int64_t)d_h * es, n_keep, 0, count);
   return hipGetLastError();
 }
 
 hipError_t launch_gather_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
                               const int32_t* scene, const int32_t* prim, const float* w,
                               const void* values, int S, int P, int d_v, int k, void* r_out,
-                              hipStream_t st, int64_t kept_batch, int scene_step) {
+                              hipStream_t st, int64_t kept_batch, int scene_step,
+                              const int32_t* count) {
   if (n == 0 || n_keep == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const dim3 grid((unsigned)(layers * n_keep));
   if (dt == DT_BF16)
     launch_inject_k<DT_BF16, true>(k, grid, st, n, n_keep, kept, scene, prim, w,
                                    static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                                   static_cast<char*>(r_out), 0, kept_batch, scene_step);
+                                   static_cast<char*>(r_out), 0, kept_batch, scene_step,
+                                   count);
   else
     launch_inject_k<DT_F32, true>(k, grid, st, n, n_keep, kept, scene, prim, w,
                                   static_cast<const char*>(values), S, P, (int64_t)d_v * es,
-                                  static_cast<char*>(r_out), 0, kept_batch, scene_step);
+                                  static_cast<char*>(r_out), 0, kept_batch, scene_step,
+                                  count);
   return hipGetLastError();
 }
 

@@ -128,15 +128,20 @@ struct FusionFfn {
 hipError_t launch_gather_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
                               const int32_t* scene, const int32_t* prim, const float* w,
                               const void* values, int S, int P, int d_v, int k, void* r_out,
-                              hipStream_t st, int64_t kept_batch, int scene_step);
+                              hipStream_t st, int64_t kept_batch, int scene_step,
+                              const int32_t* count = nullptr);
+// count (or null): the kept lists are counted (the learned gate), layer l
+// using its first count[l] entries (count[0] when kept_batch is 0); n_keep
+// is then the lists' capacity.
 hipError_t launch_fusion(int dt, const FusionFfn& f, int layers, int64_t n, int64_t n_keep,
                          const int32_t* kept, int64_t kept_batch, int d_v, const void* r, void* u,
-                         void* hidden, hipStream_t st);
+                         void* hidden, hipStream_t st, const int32_t* count = nullptr);
 // Propagation of Eq. 11 over `steps` layers: r holds [steps + 1, n_keep, d_v]
 // (slice 0 given); slice j = round(slice j-1 W_p^j + slice j-1), with
 // w_p_t [steps, d_v, d_v] holding each W_p transposed (output-row-major).
+// count (or null): only the first count[0] rows of each slice are live.
 hipError_t launch_propagate(int dt, const void* w_p_t, int steps, int64_t n_keep, int d_v,
-                            void* r, hipStream_t st);
+                            void* r, hipStream_t st, const int32_t* count = nullptr);
 
 // ---- multi-scale retrieval with the token-wise router (Eq. 8) -------------
 // Scale m's lookup (scene [M, n] local to partition m of S / M scenes, prim
@@ -163,6 +168,23 @@ hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint3
 hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
                               const int32_t* scene, const int32_t* prim, const float* w,
                               const void* values, int S, int P, int d_v, int k, void* hidden,
-                              int d_h, hipStream_t st);
+                              int d_h, hipStream_t st, const int32_t* count = nullptr);
+
+// ---- learned SKA gate (Eq. 9) ---------------------------------------------
+// z [layers * n] float32 scratch; kept [layers, n] gets each layer's open
+// entries ascending, then -1; count [layers] their number.  Entry i of layer
+// l reads row pos[i] (or i) of delta + l * delta_rows * d_c.
+hipError_t launch_gate(int dt, int layers, int64_t n, const void* delta, int64_t delta_rows,
+                       int d_c, const int32_t* pos, const void* w_g, float* z, int32_t* kept,
+                       int32_t* count, hipStream_t st);
+
+// ---- text pathway (Eq. 1) -------------------------------------------------
+// For the first count[0] entries j of kept (all n_text entries when kept is
+// null; count null: all of kept's n_text): i = kept[j],
+// hidden[pos[i], :d_t] = round(hidden[pos[i], :d_t] + table[ids[i]]).
+hipError_t launch_text_inject(int dt, int64_t n_text, const int32_t* kept, const int32_t* count,
+                              const int32_t* pos, const int32_t* ids, const void* table,
+                              int64_t vocab, int d_t, void* hidden, int64_t n, int d_h,
+                              hipStream_t st);
 
 }  // namespace lookme

@@ -653,6 +653,152 @@ lookme_status_t lookme_inject_propagated(lookme_t h, int32_t steps, int64_t n, i
                     "fusion launch");
 }
 
+lookme_status_t lookme_gate(lookme_t h, int32_t layers, int64_t n, const void* delta,
+                            int64_t delta_rows, int32_t d_c, const int32_t* pos, const void* w_g,
+                            int32_t* kept_out, int32_t* count_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_crit_dim(h->d, d_c));
+  LOOKME_TRY(check_ptr(count_out, "count_out"));
+  if (n > 0) {
+    if (delta_rows < 1)
+      return fail(LOOKME_ERR_INVALID, "delta_rows must be positive (got %lld)",
+                  (long long)delta_rows);
+    if (pos == nullptr && delta_rows < n)
+      return fail(LOOKME_ERR_INVALID, "delta_rows %lld < n %lld with no pos list",
+                  (long long)delta_rows, (long long)n);
+    if ((int64_t)layers * delta_rows > (int64_t)INT32_MAX)
+      return fail(LOOKME_ERR_UNSUPPORTED, "layers * delta_rows exceeds 2^31 - 1 rows");
+    LOOKME_TRY(check_ptr(delta, "delta"));
+    LOOKME_TRY(check_ptr(w_g, "w_g"));
+    LOOKME_TRY(check_ptr(kept_out, "kept_out"));
+    if (pos != nullptr) LOOKME_TRY(check_ptr(pos, "pos"));
+  }
+  float* z = nullptr;
+  if (n > 0) {
+    Layout L;
+    LOOKME_TRY(check_workspace(h, layers, n, &L));
+    z = reinterpret_cast<float*>(static_cast<char*>(h->ws) + L.crit_key);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Timed tm(h, LOOKME_GROUP_NORM, st);
+  return hip_status(lookme::launch_gate(h->d.dtype, layers, n, delta, delta_rows, d_c, pos, w_g,
+                                        z, kept_out, count_out, st),
+                    "gate launch");
+}
+
+lookme_status_t lookme_inject_gated(lookme_t h, int32_t layers, int64_t n, const int32_t* kept,
+                                    const int32_t* count, const int32_t* scene,
+                                    const int32_t* prim, const float* w, void* hidden,
+                                    int32_t d_h, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_hidden_dim(h->d, d_h));
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(count, "count"));
+  LOOKME_TRY(check_lookup_ptrs(kept, scene, prim, w, hidden));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  return hip_status(lookme::launch_inject_rows(d.dtype, layers, n, n, kept, scene, prim, w,
+                                               h->values, d.num_scenes, d.prims_per_scene,
+                                               d.value_dim, d.top_k, hidden, d_h, st, count),
+                    "gated inject launch");
+}
+
+lookme_status_t lookme_inject_fused_gated(lookme_t h, int32_t layers, int64_t n,
+                                          const int32_t* kept, const int32_t* count,
+                                          const int32_t* scene, const int32_t* prim,
+                                          const float* w, void* hidden, int32_t d_h,
+                                          void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_fusion(h, layers, d_h));
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(count, "count"));
+  LOOKME_TRY(check_lookup_ptrs(kept, scene, prim, w, hidden));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(h->ws);
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  LOOKME_TRY(hip_status(lookme::launch_gather_rows(d.dtype, layers, n, n, kept, scene, prim, w,
+                                                   h->values, d.num_scenes, d.prims_per_scene,
+                                                   d.value_dim, d.top_k, ws + L.fus_r, st, n, 0,
+                                                   count),
+                        "fusion gather launch"));
+  return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n, kept, n, d.value_dim,
+                                          ws + L.fus_r, ws + L.fus_u, hidden, st, count),
+                    "fusion launch");
+}
+
+lookme_status_t lookme_inject_propagated_gated(lookme_t h, int32_t steps, int64_t n,
+                                               const int32_t* kept, const int32_t* count,
+                                               const int32_t* scene, const int32_t* prim,
+                                               const float* w, void* hidden, int32_t d_h,
+                                               void* stream) {
+  LOOKME_TRY(check_handle(h));
+  if (steps < 0 || steps >= INT32_MAX)
+    return fail(LOOKME_ERR_INVALID, "steps must be in [0, 2^31 - 2] (got %d)", steps);
+  const int32_t layers = steps + 1;
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_fusion(h, layers, d_h));
+  if (steps > h->prop_steps)
+    return fail(LOOKME_ERR_INVALID, "%d propagation steps, %d registered (lookme_set_propagation)",
+                steps, h->prop_steps);
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(count, "count"));
+  LOOKME_TRY(check_lookup_ptrs(kept, scene, prim, w, hidden));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(h->ws);
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  LOOKME_TRY(hip_status(lookme::launch_gather_rows(d.dtype, 1, n, n, kept, scene, prim, w,
+                                                   h->values, d.num_scenes, d.prims_per_scene,
+                                                   d.value_dim, d.top_k, ws + L.fus_r, st, n, 0,
+                                                   count),
+                        "fusion gather launch"));
+  LOOKME_TRY(hip_status(lookme::launch_propagate(d.dtype, h->prop_w, steps, n, d.value_dim,
+                                                 ws + L.fus_r, st, count),
+                        "propagation launch"));
+  return hip_status(lookme::launch_fusion(d.dtype, h->fus, layers, n, n, kept, 0, d.value_dim,
+                                          ws + L.fus_r, ws + L.fus_u, hidden, st, count),
+                    "fusion launch");
+}
+
+lookme_status_t lookme_inject_text(int32_t dtype, const void* table, int64_t vocab, int32_t d_t,
+                                   int64_t n_text, const int32_t* pos, const int32_t* ids,
+                                   const int32_t* kept, const int32_t* count, void* hidden,
+                                   int64_t n, int32_t d_h, void* stream) {
+  if (dtype != LOOKME_F32 && dtype != LOOKME_BF16)
+    return fail(LOOKME_ERR_INVALID, "unknown dtype %d", dtype);
+  const int es = elem_size(dtype);
+  if (vocab < 1 || d_t < 1 || d_h < 1)
+    return fail(LOOKME_ERR_INVALID, "vocab, d_t and d_h must be positive");
+  if (d_t > d_h) return fail(LOOKME_ERR_INVALID, "d_t %d exceeds d_h %d", d_t, d_h);
+  if (((int64_t)d_t * es) % 16 != 0 || ((int64_t)d_h * es) % 16 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "d_t and d_h times elem_size must be multiples of 16");
+  if (vocab > (int64_t)INT32_MAX) return fail(LOOKME_ERR_UNSUPPORTED, "vocab exceeds 2^31 - 1");
+  if (n_text < 0 || n < 0) return fail(LOOKME_ERR_INVALID, "n_text and n must be >= 0");
+  if (n_text > (int64_t)INT32_MAX / 2)
+    return fail(LOOKME_ERR_UNSUPPORTED, "n_text exceeds 2^30");
+  if (n_text == 0) return LOOKME_OK;
+  if (n < 1) return fail(LOOKME_ERR_INVALID, "text entries given for n = 0 positions");
+  LOOKME_TRY(check_ptr(table, "table"));
+  LOOKME_TRY(check_ptr(pos, "pos"));
+  LOOKME_TRY(check_ptr(ids, "ids"));
+  LOOKME_TRY(check_ptr(hidden, "hidden"));
+  if (kept != nullptr) LOOKME_TRY(check_ptr(kept, "kept"));
+  if (count != nullptr) LOOKME_TRY(check_ptr(count, "count"));
+  return hip_status(lookme::launch_text_inject(dtype, n_text, kept, count, pos, ids, table, vocab,
+                                               d_t, hidden, n, d_h,
+                                               static_cast<hipStream_t>(stream)),
+                    "text inject launch");
+}
+
 lookme_status_t lookme_set_multiscale(lookme_t h, int32_t scales, int32_t d_h,
                                       const void* w_he_t) {
   LOOKME_TRY(check_handle(h));

@@ -8,7 +8,8 @@
 // cores, set the pace: the ring is as deep as the grid's occupancy allows
 // (launch_tile_gemm).
 // blockIdx.y selects a batch (a layer) whose A, B and output start a fixed
-// stride further.  Epilogues:
+// stride further.  With a count array, batch z has count[z] live rows (at
+// most `rows`, which sizes the grid); the tiles beyond them do nothing.  Epilogues:
 //
 //   EPI_ACT     C + bias, ReLU, one rounding to the storage dtype, [rows, cols];
 //   EPI_LOGIT   C + bias as float32, [rows, cols];
@@ -45,6 +46,8 @@ struct TileGemmParams {
   char* out;
   const int32_t* kept;      // EPI_RESID: kept list of batch z at kept + z * kept_batch
   const char* res;          // EPI_ADD: [rows, cols]
+  const int32_t* count;     // or null: batch z uses only its first count[z * count_step]
+                            // rows (a gate's counted kept list); tiles past them end at once
   int64_t rows;
   int64_t a_bytes;          // bytes of an A row (of each part, when split)
   int64_t k_bytes;          // K in bytes, a multiple of 128
@@ -53,6 +56,7 @@ struct TileGemmParams {
   int64_t out_ld;           // EPI_RESID: bytes of an H row
   int sel_rows, cols, ksplit, tiles;
   int col_major;            // tile ids run down the row tiles of a column block first
+  int count_step;           // 1: a count per batch, 0: one count for all
 };
 
 // Origin of tile `tile`: row tiles of one column block are consecutive ids
@@ -79,7 +83,8 @@ __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); 
 // tile columns wn + 16 j + n16.  xch: 4096 floats of LDS (EPI_SWIGLU only).
 template <int DT, int EPI>
 __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (&acc)[2][2],
-                                              int64_t z, int tile, int tid, float* xch) {
+                                              int64_t z, int tile, int tid, float* xch,
+                                              int64_t rows) {
   using S = TgShape;
   constexpr int MI = 2, NJ = 2, WN = 2;
   constexpr int ES = DT == DT_BF16 ? 2 : 4;
@@ -115,7 +120,7 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t row = m0 + wm + 16 * i + 4 * g + r;
-          if (row >= a.rows) continue;
+          if (row >= rows) continue;
           const float up = xch[(((wv / WN) * MI * NJ + i * NJ + j) * 4 + r) * WAVE + lane];
           const float u = silu_f(acc[i][j][r]) * up;
           char* dst = U + (row * a.cols + col) * ES;
@@ -148,8 +153,8 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t row = m0 + wm + 16 * i + 4 * g + r;
-        rok[i][r] = row < a.rows;
-        orow[i][r] = rok[i][r] ? row : a.rows - 1;
+        rok[i][r] = row < rows;
+        orow[i][r] = rok[i][r] ? row : rows - 1;
         if constexpr (EPI == EPI_RESID) {
           int64_t t = a.kept[z * a.kept_batch + orow[i][r]];
           t = t < 0 ? 0 : (t >= a.n ? a.n - 1 : t);
@@ -227,6 +232,12 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
   int64_t m0;
   int n0;
   tile_origin(a, tile, TCOLS, &m0, &n0);
+  int64_t rows = a.rows;   // live rows of this batch
+  if (a.count != nullptr) {
+    const int64_t c = a.count[z * a.count_step];
+    rows = c < rows ? c : rows;
+    if (m0 >= rows) return;   // the whole workgroup: no barrier is left waiting
+  }
   const int nst = (int)(a.k_bytes / KB);
   const char* A0 = a.a0 + z * a.a_batch;
   const char* B0 = a.b + z * a.b_batch;
@@ -244,7 +255,7 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
     for (int b = 0; b < S::PER_WAVE; ++b) {
       const int trow = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
       int64_t r = m0 + (trow < S::BM ? trow : 0);
-      r = r < a.rows ? r : a.rows - 1;
+      r = r < rows ? r : rows - 1;
       sel[b] = a.sel[r];
     }
   }
@@ -254,7 +265,7 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
     const int chunk = (lane % S::LPR) ^ blk_swz<KB>(trow & 15);
     if (trow < S::BM) {
       int64_t r = m0 + trow;
-      r = r < a.rows ? r : a.rows - 1;
+      r = r < rows ? r : rows - 1;
       p0[b] = A0 + r * a.a_bytes + chunk * 16;
       if (a.a1 != nullptr) {
         int s = sel[b];
@@ -326,7 +337,7 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
 
-  tile_epilogue<DT, EPI>(a, acc, z, tile, tid, reinterpret_cast<float*>(&lds[0][0]));
+  tile_epilogue<DT, EPI>(a, acc, z, tile, tid, reinterpret_cast<float*>(&lds[0][0]), rows);
 }
 
 // Launches the product over `batches` batches (blockIdx.y), tiles in the

@@ -29,8 +29,9 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_lookup", "lookme_inject", "lookme_select", "lookme_inject_kept",
             "lookme_set_relevance", "lookme_lookup_relevance", "lookme_set_fusion",
             "lookme_inject_fused", "lookme_set_propagation", "lookme_inject_propagated",
-            "lookme_set_multiscale", "lookme_inject_multiscale",
-            "lookme_destroy", "lookme_last_error",
+            "lookme_set_multiscale", "lookme_inject_multiscale", "lookme_gate",
+            "lookme_inject_gated", "lookme_inject_fused_gated", "lookme_inject_propagated_gated",
+            "lookme_inject_text", "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
 GROUPS = ("project", "route", "bucket", "score", "norm", "select", "inject")
@@ -89,6 +90,17 @@ def load():
                                      ctypes.c_int32, _vp],
         "lookme_inject_propagated": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
                                      _vp, _vp, _vp, _vp, ctypes.c_int32, _vp],
+        "lookme_gate": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, ctypes.c_int64, ctypes.c_int32,
+                        _vp, _vp, _vp, _vp, _vp],
+        "lookme_inject_gated": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
+                                _vp, ctypes.c_int32, _vp],
+        "lookme_inject_fused_gated": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                      _vp, _vp, ctypes.c_int32, _vp],
+        "lookme_inject_propagated_gated": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp,
+                                           _vp, _vp, _vp, ctypes.c_int32, _vp],
+        "lookme_inject_text": [ctypes.c_int32, _vp, ctypes.c_int64, ctypes.c_int32,
+                               ctypes.c_int64, _vp, _vp, _vp, _vp, _vp, ctypes.c_int64,
+                               ctypes.c_int32, _vp],
         "lookme_destroy": [_vp],
         "lookme_profile_enable": [_vp, ctypes.c_int32],
         "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
@@ -211,6 +223,46 @@ def lookme_inject_multiscale(h, n, n_keep, kept, scene, prim, w, hidden, d_h, st
                                            _ptr(w), _ptr(hidden), d_h, _stream(stream)))
 
 
+def lookme_gate(h, layers, n, delta, delta_rows, d_c, pos, w_g, kept_out, count_out,
+                stream=None):
+    _check(load().lookme_gate(h, layers, n, _ptr(delta), delta_rows, d_c, _ptr(pos), _ptr(w_g),
+                              _ptr(kept_out), _ptr(count_out), _stream(stream)))
+
+
+def lookme_inject_gated(h, layers, n, kept, count, scene, prim, w, hidden, d_h, stream=None):
+    _check(load().lookme_inject_gated(h, layers, n, _ptr(kept), _ptr(count), _ptr(scene),
+                                      _ptr(prim), _ptr(w), _ptr(hidden), d_h, _stream(stream)))
+
+
+def lookme_inject_fused_gated(h, layers, n, kept, count, scene, prim, w, hidden, d_h,
+                              stream=None):
+    _check(load().lookme_inject_fused_gated(h, layers, n, _ptr(kept), _ptr(count), _ptr(scene),
+                                            _ptr(prim), _ptr(w), _ptr(hidden), d_h,
+                                            _stream(stream)))
+
+
+def lookme_inject_propagated_gated(h, steps, n, kept, count, scene, prim, w, hidden, d_h,
+                                   stream=None):
+    _check(load().lookme_inject_propagated_gated(h, steps, n, _ptr(kept), _ptr(count),
+                                                 _ptr(scene), _ptr(prim), _ptr(w), _ptr(hidden),
+                                                 d_h, _stream(stream)))
+
+
+def lookme_inject_text(dtype, table, vocab, d_t, n_text, pos, ids, kept, count, hidden, n, d_h,
+                       stream=None):
+    _check(load().lookme_inject_text(dtype, _ptr(table), vocab, d_t, n_text, _ptr(pos),
+                                     _ptr(ids), _ptr(kept), _ptr(count), _ptr(hidden), n, d_h,
+                                     _stream(stream)))
+
+
+def inject_text(table, pos, ids, hidden, kept=None, count=None, stream=None):
+    """lookme_inject_text on torch tensors: table [V, d_t], pos and ids
+    [n_text] int32, hidden [n, d_h] (updated in place)."""
+    lookme_inject_text(DTYPE_CODE[table.dtype], table, table.shape[0], table.shape[1],
+                       pos.numel(), pos, ids, kept, count, hidden, hidden.shape[0],
+                       hidden.shape[1], stream)
+
+
 def lookme_destroy(h):
     if h:
         _check(load().lookme_destroy(h))
@@ -330,6 +382,33 @@ class Table:
         self.reserve(1, n)
         lookme_inject_multiscale(self.handle, n, n_keep, kept, scene, prim, w, hidden,
                                  hidden.shape[-1], stream)
+
+    def gate(self, delta, w_g, kept_out, count_out, pos=None, layers=1, stream=None):
+        """lookme_gate: delta [layers, rows, d_c] (or [rows, d_c]); pos [n] or
+        None (n = rows); w_g [layers, d_c]; kept_out [layers, n]; count_out
+        [layers]."""
+        rows = delta.numel() // (layers * delta.shape[-1])
+        n = rows if pos is None else pos.numel()
+        self.reserve(layers, n)
+        lookme_gate(self.handle, layers, n, delta, rows, delta.shape[-1], pos, w_g, kept_out,
+                    count_out, stream)
+
+    def inject_gated(self, kept, count, scene, prim, w, hidden, layers=1, stream=None):
+        n = scene.numel() // layers
+        lookme_inject_gated(self.handle, layers, n, kept, count, scene, prim, w, hidden,
+                            hidden.shape[-1], stream)
+
+    def inject_fused_gated(self, kept, count, scene, prim, w, hidden, layers=1, stream=None):
+        n = scene.numel() // layers
+        self.reserve(layers, n)
+        lookme_inject_fused_gated(self.handle, layers, n, kept, count, scene, prim, w, hidden,
+                                  hidden.shape[-1], stream)
+
+    def inject_propagated_gated(self, kept, count, scene, prim, w, hidden, steps, stream=None):
+        n = scene.numel()
+        self.reserve(steps + 1, n)
+        lookme_inject_propagated_gated(self.handle, steps, n, kept, count, scene, prim, w, hidden,
+                                       hidden.shape[-1], stream)
 
     def close(self):
         if self.handle:

@@ -6,5 +6,5 @@ one piece shared by the tests, the benchmark and the CPU oracle's callers.
 """
 
 from .gen import (Workload, WORKLOADS, make_inputs, make_integer_inputs,  # noqa: F401
-                  make_fusion, make_multiscale, make_propagation, make_relevance,
-                  n_keep_for)
+                  make_fusion, make_gate, make_layer, make_multiscale, make_propagation,
+                  make_relevance, make_text, n_keep_for)

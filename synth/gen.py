@@ -41,6 +41,9 @@ TID_MLP_W1, TID_MLP_B1, TID_MLP_W2, TID_MLP_B2 = 40, 41, 42, 43
 TID_FUS_GATE, TID_FUS_UP, TID_FUS_DOWN = 50, 60, 70
 TID_PROP = 80
 TID_MS_X, TID_MS_W, TID_MS_HE = 90, 100, 110
+TID_GATE, TID_TEXT_TAB, TID_TEXT_IDS, TID_TEXT_POS = 120, 130, 131, 132
+TID_CROSS_W, TID_CROSS_K1, TID_CROSS_K2, TID_CROSS_V, TID_HDEC, TID_SEQ_DELTA = (
+    140, 141, 142, 143, 144, 145)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -293,3 +296,76 @@ def make_multiscale(wl: Workload, seed: int, scales: int, device="cpu") -> dict:
         wt[m] = _randn_rows(wl.d_e, wl.d_in, base + TID_MS_W + m, dev, 1.0 / math.sqrt(wl.d_in), dt)
     w_he_t = _randn_rows(wl.d_v, wl.d_h, base + TID_MS_HE, dev, 1.0 / math.sqrt(wl.d_h), dt)
     return dict(x=x, wt=wt, w_he_t=w_he_t, scales=scales)
+
+
+def make_gate(wl: Workload, seed: int, device="cpu", layers=None, tid: int = TID_GATE) -> torch.Tensor:
+    """Seeded SKA gate projections (Eq. 9; trained in the paper), one column
+    per layer: w_g [L, d_c] ~ N(0, 1/d_c) in the workload's dtype, so that
+    z = Delta W_g is of the order of ||Delta|| / sqrt(d_c) and about half of
+    the gates open on zero-mean Delta.  ``tid`` separates the pathways'
+    gates."""
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[wl.dtype]
+    L = layers or wl.layers
+    return _randn_rows(L, wl.crit_dim, 1000 * seed + tid, dev, 1.0 / math.sqrt(wl.crit_dim), dt)
+
+
+def make_text(seed: int, vocab: int, d_t: int, pos: torch.Tensor, dtype: str = "bf16",
+              device="cpu", value_std: float = 0.02) -> dict:
+    """Seeded text pathway inputs (Sec. 3.2, Eq. 1): a text table
+    [vocab, d_t] ~ N(0, value_std) and token ids uniform in [0, vocab) for
+    the given text positions ``pos`` [n_text] (int32)."""
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[dtype]
+    table = _randn_rows(vocab, d_t, 1000 * seed + TID_TEXT_TAB, dev, value_std, dt)
+    g = _gen(1000 * seed + TID_TEXT_IDS, 0, dev)
+    ids = torch.randint(0, vocab, (pos.numel(),), generator=g, device=dev, dtype=torch.int64)
+    return dict(table=table, pos=pos.to(device=dev, dtype=torch.int32).contiguous(),
+                ids=ids.to(torch.int32), vocab=vocab, d_t=d_t)
+
+
+def make_layer(wl: Workload, seed: int, text_before: int, text_after: int, vocab: int,
+               d_t: int, cross_scenes: int, cross_prims: int, cross_k: int,
+               device="cpu") -> dict:
+    """One LookME layer's inputs (Eq. 3) over a sequence of text_before text
+    positions, the workload's n_tokens image positions, then text_after text
+    positions:
+      image   the workload's inputs (make_inputs; its first layer is used)
+              for the image block [text_before, text_before + n_tokens);
+      h_dec   L_dec(H_in) [n_seq, d_h] iid N(0, 1);
+      delta   Delta = Attn(H_in) [n_seq, d_c], rows a_t z_t with a_t
+              log-normal and z_t ~ N(0, I / d_c) as for the image workload;
+      text    make_text over the text positions, table [vocab, d_t];
+      cross   the cross-modal pathway's own table: cross_scenes x cross_prims
+              unit-norm keys of width d_e, rows [S P, d_h] ~ N(0, value_std),
+              and its query projection W^T [d_e, d_h] ~ N(0, 1/d_h);
+      gates   w_g [3, d_c] (text, image, cross) from make_gate.
+    """
+    dev = torch.device(device)
+    dt = TORCH_DTYPE[wl.dtype]
+    base = 1000 * seed
+    img = make_inputs(wl.scaled(layers=1), seed, device)
+    n_img = wl.n_tokens
+    n_seq = text_before + n_img + text_after
+    pos = torch.cat([torch.arange(0, text_before),
+                     torch.arange(text_before + n_img, n_seq)]).to(torch.int32)
+    text = make_text(seed, vocab, d_t, pos, wl.dtype, device, wl.value_std)
+    h_dec = _randn_rows(n_seq, wl.d_h, base + TID_HDEC, dev, 1.0, dt)
+    g = _gen(base + TID_SEQ_DELTA, 0, dev)
+    a = torch.exp(torch.randn((n_seq, 1), generator=g, device=dev, dtype=torch.float32))
+    z = _randn_rows(n_seq, wl.crit_dim, base + TID_SEQ_DELTA + 500, dev,
+                    1.0 / math.sqrt(wl.crit_dim), torch.float32)
+    delta = (a * z).to(dt)
+    cross = dict(
+        wt=_randn_rows(wl.d_e, wl.d_h, base + TID_CROSS_W, dev, 1.0 / math.sqrt(wl.d_h),
+                       dt).unsqueeze(0),
+        scene_keys=_randn_rows(cross_scenes, wl.d_e, base + TID_CROSS_K1, dev, 1.0, dt,
+                               normalize=True),
+        prim_keys=_randn_rows(cross_scenes * cross_prims, wl.d_e, base + TID_CROSS_K2, dev, 1.0,
+                              dt, normalize=True).view(cross_scenes, cross_prims, wl.d_e),
+        values=_randn_rows(cross_scenes * cross_prims, wl.d_h, base + TID_CROSS_V, dev,
+                           wl.value_std, dt),
+        k=cross_k)
+    w_g = torch.cat([make_gate(wl, seed, device, 1, TID_GATE + 10 * p) for p in range(3)])
+    return dict(workload=wl, image=img, start=text_before, n_seq=n_seq, h_dec=h_dec,
+                delta=delta, text=text, cross=cross, w_g=w_g)

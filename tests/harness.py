@@ -385,3 +385,263 @@ def check_run(r: Run, tokens=None, layers=None) -> C.Report:
                        scene, prim, lambda t: w_of[t], kept, rep, tokens=toks,
                        w_lib_of=lambda t: w[t])
     return rep.finish()
+
+
+class GatedRun(Run):
+    """A pass with the learned SKA gate (Eq. 9-10): route and lookup, the
+    gate of every layer (lookme_gate: a counted, ascending kept list), then
+    the injection for those lists -- the prefix add (mode "plain",
+    lookme_inject_gated), the SwiGLU fusion ("fused") or the fusion with the
+    gate reused by ``steps`` propagated layers ("propagated", Eq. 11)."""
+
+    def __init__(self, inp: dict, w_g: torch.Tensor, mode: str = "plain", fus=None,
+                 w_p_t=None, **kw):
+        super().__init__(inp, with_kept=False, **kw)
+        self.w_g, self.mode, self.fus, self.w_p_t = w_g, mode, fus, w_p_t
+        self.steps = self.L - 1 if mode == "propagated" else 0
+        if mode in ("fused", "propagated"):
+            self.table.set_fusion(fus["w_gate"], fus["w_up"], fus["w_down"])
+        if self.steps > 0:
+            self.table.set_propagation(w_p_t)
+        gl = 1 if mode == "propagated" else self.L
+        self.glayers = gl
+        self.kept = torch.full((gl, self.n), -7, dtype=torch.int32, device=self.dev)
+        self.count = torch.full((gl,), -7, dtype=torch.int32, device=self.dev)
+
+    def run(self):
+        inp, st, gl = self.inp, self.stream, self.glayers
+        wt = None if inp["wt"] is None else inp["wt"][:gl]
+        self.table.route(inp["x"], wt, self.q[:gl], self.scene[:gl], layers=gl, stream=st)
+        self.table.lookup(self.q[:gl], self.scene[:gl], self.prim[:gl], self.w[:gl], layers=gl,
+                          stream=st)
+        self.table.gate(inp["delta"][:gl], self.w_g[:gl], self.kept, self.count, layers=gl,
+                        stream=st)
+        if self.mode == "plain":
+            self.table.inject_gated(self.kept, self.count, self.scene, self.prim, self.w,
+                                    self.hidden, layers=gl, stream=st)
+        elif self.mode == "fused":
+            self.table.inject_fused_gated(self.kept, self.count, self.scene, self.prim, self.w,
+                                          self.hidden, layers=gl, stream=st)
+        else:
+            self.table.inject_propagated_gated(self.kept[0], self.count, self.scene[0],
+                                               self.prim[0], self.w[0], self.hidden, self.steps,
+                                               stream=st)
+        return self
+
+
+def check_gated_run(r: GatedRun, tokens=None) -> C.Report:
+    """Every layer's gate in full (open set, ascending, -1 tail, count) and
+    the injected rows of the sampled tokens against the oracle, on the
+    library's lookup (routing and lookup themselves are checked by check_run
+    on the same kernels)."""
+    torch.cuda.synchronize()
+    inp = r.inp
+    dt = dtype_name(inp["x"])
+    rep = C.Report()
+    toks = np.arange(r.n) if tokens is None else np.asarray(tokens)
+    tsel = torch.as_tensor(toks, device=r.dev)
+    values = inp["values"]
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    counts = to_np(r.count)
+    kept_all = to_np(r.kept)
+    kepts = []
+    for l in range(r.glayers):
+        c = int(counts[l])
+        if not 0 <= c <= r.n:
+            rep.fail(f"gate: count {c} of layer {l} outside [0, {r.n}]")
+            return rep.finish()
+        if np.any(kept_all[l, c:] != -1):
+            rep.fail(f"gate: layer {l} list not -1 past its count")
+        C.check_gate(f64(inp["delta"][l]), f64(r.w_g[l]), kept_all[l, :c], rep)
+        kepts.append(kept_all[l, :c])
+    if r.mode == "plain":
+        prim_keys = inp["prim_keys"]
+        for l in range(r.L):
+            prim, w = to_np(r.prim[l]), to_np(r.w[l])
+            scene = to_np(r.scene[l]).astype(np.int64)
+            q_lib = O.to_f64(to_np(r.q[l])[toks], dt)
+            w_orc = C.check_prim(q_lib, scene[toks], lambda s: f64(prim_keys[s]), r.k, "dot",
+                                 prim[toks], w[toks], rep)
+            w_of = {int(t): w_orc[i] for i, t in enumerate(toks)}
+            C.check_hidden(to_np(r.h_in[l][tsel]), to_np(r.hidden[l][tsel]), dt, values_rows,
+                           r.P, scene, prim, lambda t: w_of[t], kepts[l], rep, tokens=toks,
+                           w_lib_of=lambda t, w=w: w[t])
+    elif r.mode == "fused":
+        fus = r.fus
+        for l in range(r.L):
+            C.check_fused_hidden(to_np(r.h_in[l][tsel]), to_np(r.hidden[l][tsel]), dt,
+                                 values_rows, r.P, to_np(r.scene[l]), to_np(r.prim[l]),
+                                 to_np(r.w[l]), kepts[l], f64(fus["w_gate"][l]),
+                                 f64(fus["w_up"][l]), f64(fus["w_down"][l]), rep, toks)
+    else:
+        fus = r.fus
+        w_p = f64(r.w_p_t[: r.steps]).transpose(0, 2, 1) if r.steps else np.zeros((0, 1, 1))
+        C.check_propagated_hidden(to_np(r.h_in[:, tsel]), to_np(r.hidden[:, tsel]), dt,
+                                  values_rows, r.P, to_np(r.scene[0]), to_np(r.prim[0]),
+                                  to_np(r.w[0]), kepts[0], w_p, f64(fus["w_gate"]),
+                                  f64(fus["w_up"]), f64(fus["w_down"]), rep, toks)
+    return rep.finish()
+
+
+class LayerRun:
+    """One LookME layer (Eq. 3) over a sequence of text and image positions:
+    the cross-modal pathway routes and looks up every position's L_dec(H_in)
+    row against its own table, the image pathway the image block's encoder
+    embeddings, each pathway's gate reads Delta at its positions, and then the
+    text, image and cross-modal injections are added in that order -- every
+    step a library call (lookme_route / lookup / gate / inject_text /
+    inject_gated)."""
+
+    def __init__(self, lay: dict, stream=None):
+        self.lay = lay
+        img, cr, tx = lay["image"], lay["cross"], lay["text"]
+        self.dev = lay["h_dec"].device
+        dt = lay["h_dec"].dtype
+        self.stream = stream
+        self.start, self.n_seq = lay["start"], lay["n_seq"]
+        self.n_img = img["x"].shape[0]
+        self.k, self.kc = img["k"], cr["k"]
+        d_e = img["prim_keys"].shape[2]
+        self.img_table = lk.Table(img["scene_keys"], img["prim_keys"], img["values"], self.k)
+        self.cross_table = lk.Table(cr["scene_keys"], cr["prim_keys"], cr["values"], self.kc)
+        self.img_table.reserve(1, max(self.n_img, tx["pos"].numel()))
+        self.cross_table.reserve(1, self.n_seq)
+        ni, ns, nt = self.n_img, self.n_seq, tx["pos"].numel()
+        mk = lambda shape, dtype, fill: torch.full(shape, fill, dtype=dtype, device=self.dev)
+        self.q_img, self.q_c = mk((ni, d_e), dt, 0), mk((ns, d_e), dt, 0)
+        self.scene_img, self.scene_c = mk((ni,), torch.int32, -7), mk((ns,), torch.int32, -7)
+        self.prim_img = mk((ni, self.k), torch.int32, -7)
+        self.prim_c = mk((ns, self.kc), torch.int32, -7)
+        self.w_img = mk((ni, self.k), torch.float32, -7.0)
+        self.w_c = mk((ns, self.kc), torch.float32, -7.0)
+        self.kept_t, self.kept_i, self.kept_c = (mk((nt,), torch.int32, -7),
+                                                 mk((ni,), torch.int32, -7),
+                                                 mk((ns,), torch.int32, -7))
+        # one 16-byte row per pathway's count (text, image, cross)
+        self.count = mk((3, 4), torch.int32, -7)
+        self.hidden = lay["h_dec"].clone()
+
+    def run(self):
+        lay, st = self.lay, self.stream
+        img, cr, tx = lay["image"], lay["cross"], lay["text"]
+        s0, s1 = self.start, self.start + self.n_img
+        # every pathway reads the layer's inputs before the first add
+        self.cross_table.route(lay["h_dec"], cr["wt"], self.q_c, self.scene_c, stream=st)
+        self.cross_table.lookup(self.q_c, self.scene_c, self.prim_c, self.w_c, stream=st)
+        self.img_table.route(img["x"], img["wt"][:1], self.q_img, self.scene_img, stream=st)
+        self.img_table.lookup(self.q_img, self.scene_img, self.prim_img, self.w_img, stream=st)
+        c_t, c_i, c_c = self.count[0, :1], self.count[1, :1], self.count[2, :1]
+        self.img_table.gate(lay["delta"], lay["w_g"][0:1], self.kept_t, c_t, pos=tx["pos"],
+                            stream=st)
+        self.img_table.gate(lay["delta"][s0:s1], lay["w_g"][1:2], self.kept_i, c_i, stream=st)
+        self.cross_table.gate(lay["delta"], lay["w_g"][2:3], self.kept_c, c_c, stream=st)
+        lk.inject_text(tx["table"], tx["pos"], tx["ids"], self.hidden, self.kept_t, c_t,
+                       stream=st)
+        self.img_table.inject_gated(self.kept_i, c_i, self.scene_img, self.prim_img, self.w_img,
+                                    self.hidden[s0:s1], stream=st)
+        self.cross_table.inject_gated(self.kept_c, c_c, self.scene_c, self.prim_c, self.w_c,
+                                      self.hidden, stream=st)
+        return self
+
+
+def check_layer_run(r: LayerRun, tokens=None) -> C.Report:
+    """Stage-wise check of one LookME layer: both pathways' projections,
+    scenes and primitives on the sampled positions (C1-C4), the three gates
+    in full, and the layer output recomputed in float64 from the library's
+    decisions and weights with one rounding per add (text, image, cross):
+    untouched rows bit-identical; touched elements within two bf16 ulps, at
+    most 0.5% of them off the recomputed value (float32: within 1e-5 of the
+    summed magnitudes)."""
+    torch.cuda.synchronize()
+    lay = r.lay
+    img, cr, tx = lay["image"], lay["cross"], lay["text"]
+    dt = dtype_name(lay["h_dec"])
+    rep = C.Report()
+    ni, ns = r.n_img, r.n_seq
+    s0 = r.start
+    h_dec = f64(lay["h_dec"])
+    delta = f64(lay["delta"])
+    w_g = f64(lay["w_g"])
+    counts = to_np(r.count)[:, 0]
+    pos, ids = to_np(tx["pos"]).astype(np.int64), to_np(tx["ids"]).astype(np.int64)
+    kept_t = to_np(r.kept_t)[: counts[0]]
+    kept_i = to_np(r.kept_i)[: counts[1]]
+    kept_c = to_np(r.kept_c)[: counts[2]]
+    C.check_gate(delta, w_g[0], kept_t, rep, pos=pos)
+    C.check_gate(delta[s0:s0 + ni], w_g[1], kept_i, rep)
+    C.check_gate(delta, w_g[2], kept_c, rep)
+    # the two lookups on sampled positions
+    ti = np.arange(ni) if tokens is None else np.asarray(tokens)[np.asarray(tokens) < ni]
+    tc = np.arange(ns) if tokens is None else np.asarray(tokens)
+    for name, x, wt, sk, pk, q, sc, pr, w, tk, k in (
+            ("image", img["x"], img["wt"][0], img["scene_keys"], img["prim_keys"], r.q_img,
+             r.scene_img, r.prim_img, r.w_img, ti, r.k),
+            ("cross", lay["h_dec"], cr["wt"][0], cr["scene_keys"], cr["prim_keys"], r.q_c,
+             r.scene_c, r.prim_c, r.w_c, tc, r.kc)):
+        tsel = torch.as_tensor(tk, device=r.dev)
+        q_bits = to_np(q)[tk]
+        C.check_projection(q_bits, f64(x[tsel]), f64(wt), dt, rep)
+        q_lib = O.to_f64(q_bits, dt)
+        scene = to_np(sc).astype(np.int64)
+        C.check_scene(q_lib, f64(sk), None, "dot", scene[tk], rep)
+        C.check_prim(q_lib, scene[tk], lambda s, pk=pk: f64(pk[s]), k, "dot", to_np(pr)[tk],
+                     to_np(w)[tk], rep)
+    # the layer output from the library's decisions, one rounding per add
+    want = h_dec.copy()
+    mag = np.abs(h_dec)
+    touched = np.zeros(ns, dtype=bool)
+    table = tx["table"]
+    d_t = table.shape[1]
+    for i in kept_t:
+        t = pos[i]
+        row = f64(table[int(ids[i])])
+        want[t, :d_t] = O.round_to_dtype(want[t, :d_t] + row, dt)
+        mag[t, :d_t] += np.abs(row)
+        touched[t] = True
+    for pathway, kept, sc, pr, w, vals, P, off in (
+            ("image", kept_i, r.scene_img, r.prim_img, r.w_img, img["values"],
+             img["prim_keys"].shape[1], s0),
+            ("cross", kept_c, r.scene_c, r.prim_c, r.w_c, cr["values"], cr["prim_keys"].shape[1],
+             0)):
+        scene, prim, w = to_np(sc).astype(np.int64), to_np(pr).astype(np.int64), to_np(w)
+        d_v = vals.shape[1]
+        for t in kept:
+            rows = torch.as_tensor(scene[t] * P + prim[t], device=vals.device, dtype=torch.long)
+            V = f64(vals[rows])
+            ww = w[t].astype(np.float64)
+            tt = off + int(t)
+            want[tt, :d_v] = O.round_to_dtype(want[tt, :d_v] + np.sum(ww[:, None] * V, axis=0),
+                                              dt)
+            mag[tt, :d_v] += np.sum(np.abs(ww[:, None] * V), axis=0)
+            touched[tt] = True
+    got_bits = to_np(r.hidden)
+    in_bits = to_np(lay["h_dec"])
+    got = O.to_f64(got_bits, dt)
+    rows = np.arange(ns) if tokens is None else np.union1d(np.asarray(tokens),
+                                                           np.flatnonzero(touched)[:4096])
+    off_count, n_el = 0, 0
+    for t in rows:
+        rep.count("layer_row")
+        if not touched[t]:
+            if not np.array_equal(got_bits[t].view(np.uint8), in_bits[t].view(np.uint8)):
+                rep.fail(f"layer: untouched position {t} modified")
+            continue
+        d = np.abs(got[t] - want[t])
+        if dt == "bf16":
+            ulp = np.ldexp(1.0, np.frexp(np.maximum(np.abs(want[t]), 2.0 ** -126))[1] - 8)
+            bad = d > 2 * ulp
+        else:
+            bad = d > 1e-5 * mag[t] + 1e-30
+        if np.any(bad):
+            rep.fail(f"layer: position {t}: {int(bad.sum())} elements beyond the bound")
+        off_count += int(np.sum(d > 0))
+        n_el += d.size
+    rep.notes["layer_elements_off"] = off_count
+    if dt == "bf16" and n_el and off_count > 0.005 * n_el:
+        rep.fail(f"layer: {off_count} of {n_el} touched elements off the recomputed value")
+    rep.notes["layer_open"] = [int(c) for c in counts]
+    return rep.finish()

@@ -283,3 +283,50 @@ def test_null_handle(lib):
     assert _status(lambda: lk.lookme_route(None, 1, 1, 1, FAKE, FAKE, FAKE, FAKE, 0))[0] == \
         lk.LOOKME_ERR_INVALID
     lk.lookme_destroy(None)
+
+
+def test_gate_and_text_entry_points_validate(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        gate = lambda n=8, rows=8, d_c=2048, pos=None, p=FAKE, c=FAKE: lk.lookme_gate(
+            h, 1, n, p, rows, d_c, pos, p, p, c, 0)
+        assert S(lambda: gate(c=None)) == lk.LOOKME_ERR_INVALID          # count_out needed
+        assert S(lambda: gate(d_c=1001)) == lk.LOOKME_ERR_UNSUPPORTED     # 2002 B rows
+        assert S(lambda: gate(rows=4)) == lk.LOOKME_ERR_INVALID          # rows < n, no pos
+        assert S(lambda: gate(rows=0)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: gate(p=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: gate(pos=FAKE + 4)) == lk.LOOKME_ERR_INVALID     # misaligned
+        assert S(lambda: gate()) == lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: gate(rows=4, pos=FAKE)) == lk.LOOKME_ERR_WORKSPACE
+        inj = lambda n=8, d_h=2048, c=FAKE, p=FAKE: lk.lookme_inject_gated(
+            h, 1, n, p, c, p, p, p, p, d_h, 0)
+        assert S(lambda: inj(d_h=1024)) == lk.LOOKME_ERR_INVALID          # d_v > d_h
+        assert S(lambda: inj(c=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: inj(p=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: inj(n=0, p=None, c=None)) == lk.LOOKME_OK
+        fus = lambda n=8, c=FAKE: lk.lookme_inject_fused_gated(h, 1, n, FAKE, c, FAKE, FAKE,
+                                                               FAKE, FAKE, 2048, 0)
+        assert S(lambda: fus()) == lk.LOOKME_ERR_INVALID                  # no fusion
+        prop = lambda steps=1: lk.lookme_inject_propagated_gated(h, steps, 8, FAKE, FAKE, FAKE,
+                                                                 FAKE, FAKE, FAKE, 2048, 0)
+        assert S(lambda: prop(-1)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: lk.lookme_set_fusion(h, 2, 2048, 2048, FAKE, FAKE, FAKE)) == lk.LOOKME_OK
+        assert S(lambda: fus(c=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: fus()) == lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: prop(1)) == lk.LOOKME_ERR_INVALID                # no projections
+    finally:
+        lk.lookme_destroy(h)
+    txt = lambda dt=lk.LOOKME_BF16, V=100, d_t=64, n_text=5, d_h=64, n=9, p=FAKE, kept=None: \
+        lk.lookme_inject_text(dt, p, V, d_t, n_text, p, p, kept, None, p, n, d_h, 0)
+    S = lambda f: _status(f)[0]
+    assert S(lambda: txt(dt=5)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: txt(V=0)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: txt(d_t=128)) == lk.LOOKME_ERR_INVALID             # d_t > d_h
+    assert S(lambda: txt(d_t=4)) == lk.LOOKME_ERR_UNSUPPORTED            # 8-byte rows
+    assert S(lambda: txt(n=0)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: txt(p=None)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: txt(kept=FAKE + 8)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: txt(n_text=0, p=None)) == lk.LOOKME_OK
