@@ -62,6 +62,14 @@ def parse():
                     help="multi-scale image retrieval (Eq. 8) on a one-layer workload: M scales "
                          "(seeded tokens and rankers) each routed and looked up in its own scene "
                          "partition, mixed by the token-wise router and injected")
+    ap.add_argument("--gate", action="store_true",
+                    help="the kept set of each layer from the learned SKA gate of Eq. 9 "
+                         "(seeded W_g; open where Delta W_g > 0, a variable count) instead of "
+                         "the top n_keep by criticality")
+    ap.add_argument("--layer", action="store_true",
+                    help="time one whole LookME layer (Eq. 3) on a sequence of 64 + 192 text "
+                         "positions around the workload's image block: text, image and "
+                         "cross-modal pathways, each with its learned gate")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -179,7 +187,8 @@ def stored_traffic(wl):
 
 
 class Bench:
-    def __init__(self, wl, seed, copies, relevance=0, fusion=0, netprop=0, scales=0):
+    def __init__(self, wl, seed, copies, relevance=0, fusion=0, netprop=0, scales=0,
+                 gate=False):
         import torch
         from paper_2607_16305_amd import lookme as lk
         from synth import make_inputs
@@ -236,6 +245,13 @@ class Bench:
                     t.set_propagation(self.w_p_t)
                 t.reserve(L + netprop, n)   # the fusion's buffers enlarge the workspace
         self.scales = scales
+        self.gate = gate
+        if gate:
+            from synth import make_gate
+            gl = 1 if netprop else L
+            self.w_g = make_gate(wl, seed, device="cuda", layers=gl)
+            self.kept = torch.empty((gl, n), dtype=torch.int32, device=dev)
+            self.count = torch.zeros((gl,), dtype=torch.int32, device=dev)
         self.handles = [t.handle for t in self.tables]
         if scales:
             from synth import make_multiscale
@@ -275,8 +291,13 @@ class Bench:
         # workgroups it would slow
         self.ev_start.record(self.main)
         self.side.wait_event(self.ev_start)
-        lk.lookme_select(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.kept,
-                         self.side_handle)
+        if self.gate:
+            gl = self.w_g.shape[0]
+            lk.lookme_gate(h, gl, n, inp["delta"], n, wl.crit_dim, None, self.w_g, self.kept,
+                           self.count, self.side_handle)
+        else:
+            lk.lookme_select(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.kept,
+                             self.side_handle)
         self.ev_kept.record(self.side)
         if self.scales:
             ms = self.ms
@@ -296,7 +317,18 @@ class Bench:
             lk.lookme_lookup_relevance(h, L, n, self.q, self.scene, self.act, self.prim, self.w,
                                        self.stream)
         self.main.wait_event(self.ev_kept)
-        if self.fus is None:
+        if self.gate:
+            if self.fus is None:
+                lk.lookme_inject_gated(h, L, n, self.kept, self.count, self.scene, self.prim,
+                                       self.w, self.hidden, wl.d_h, self.stream)
+            elif self.netprop:
+                lk.lookme_inject_propagated_gated(h, self.netprop, n, self.kept[0], self.count,
+                                                  self.scene[0], self.prim[0], self.w[0],
+                                                  self.hidden, wl.d_h, self.stream)
+            else:
+                lk.lookme_inject_fused_gated(h, L, n, self.kept, self.count, self.scene,
+                                             self.prim, self.w, self.hidden, wl.d_h, self.stream)
+        elif self.fus is None:
             lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
                                   self.hidden, wl.d_h, self.stream)
         elif self.netprop:
@@ -352,6 +384,9 @@ class Bench:
                            for m in range(self.scales)) / self.scales
             scenes = wl.scenes // self.scales
         keep = L * wl.n_keep
+        if self.gate:
+            # the open rows (the gate's count varies with the inputs, not the step)
+            keep = int(self.count.sum().item())
         b = {}
         b["project"] = (n * wl.d_in + L * wl.d_e * wl.d_in + rows * wl.d_e) * es
         b["route"] = (rows * wl.d_e + scenes * wl.d_e) * es + rows * 4
@@ -360,6 +395,9 @@ class Bench:
                       + rows * 4                              # bucketed row ids
                       + rows * k * 8)                         # prim + weights written
         b["norm"] = rows * wl.crit_dim * es + rows * 4
+        if self.gate:
+            gl = self.w_g.shape[0]
+            b["norm"] = gl * n * wl.crit_dim * es + gl * wl.crit_dim * es + gl * n * 4
         b["inject"] = keep * (k * wl.d_v * es + 2 * wl.d_v * es + k * 8 + 8)
         flops = {"project": 2 * n * wl.d_in * L * wl.d_e, "route": 2 * rows * wl.d_e * scenes,
                  "score": 2 * rows * wl.d_e * wl.prims}
@@ -380,6 +418,138 @@ class Bench:
             flops["score"] = 2 * rows * 2 * wl.d_e * hid + 2 * rows * hid * wl.prims
             b["score"] = None
         return b, flops, nonempty
+
+
+class LayerBench:
+    """One whole LookME layer (Eq. 3) per step on a sequence of TEXT_BEFORE
+    text positions, the workload's image block and TEXT_AFTER text
+    positions: the cross-modal pathway routes and looks up every position's
+    L_dec(H_in) row in its own table (the paper's N_s = 512 scenes of
+    N_p = 256 primitives, top-8), the image pathway the image block's
+    embeddings in the workload's table; the three learned gates run on a
+    second stream meanwhile (they read only Delta), then the text, image and
+    cross-modal injections are added in that order."""
+
+    TEXT_BEFORE, TEXT_AFTER, VOCAB = 64, 192, 151936
+    CROSS_SCENES, CROSS_PRIMS, CROSS_K = 512, 256, 8
+
+    def __init__(self, wl, seed):
+        import torch
+        from paper_2607_16305_amd import lookme as lk
+        from synth import make_layer
+        self.torch, self.lk, self.wl = torch, lk, wl
+        self.lay = lay = make_layer(wl, seed, self.TEXT_BEFORE, self.TEXT_AFTER, self.VOCAB,
+                                    wl.d_h, self.CROSS_SCENES, self.CROSS_PRIMS, self.CROSS_K,
+                                    device="cuda")
+        img, cr = lay["image"], lay["cross"]
+        self.n_seq, self.start, self.n_img = lay["n_seq"], lay["start"], wl.n_tokens
+        self.n_text = lay["text"]["pos"].numel()
+        self.img = lk.Table(img["scene_keys"], img["prim_keys"], img["values"], wl.top_k)
+        self.cross = lk.Table(cr["scene_keys"], cr["prim_keys"], cr["values"], self.CROSS_K)
+        self.img.reserve(1, max(self.n_img, self.n_text))
+        self.cross.reserve(1, self.n_seq)
+        dev, dt = lay["h_dec"].device, lay["h_dec"].dtype
+        e = lambda shape, dtype: torch.empty(shape, dtype=dtype, device=dev)
+        ni, ns = self.n_img, self.n_seq
+        self.q_i, self.q_c = e((ni, wl.d_e), dt), e((ns, wl.d_e), dt)
+        self.sc_i, self.sc_c = e((ni,), torch.int32), e((ns,), torch.int32)
+        self.pr_i, self.pr_c = e((ni, wl.top_k), torch.int32), e((ns, self.CROSS_K), torch.int32)
+        self.w_i, self.w_c = e((ni, wl.top_k), torch.float32), e((ns, self.CROSS_K), torch.float32)
+        self.k_t, self.k_i, self.k_c = (e((self.n_text,), torch.int32), e((ni,), torch.int32),
+                                        e((ns,), torch.int32))
+        self.count = torch.zeros((3, 4), dtype=torch.int32, device=dev)   # a 16-byte row each
+        self.hidden = lay["h_dec"].clone()
+        self.main = torch.cuda.current_stream()
+        self.side = torch.cuda.Stream()
+        self.ev_start, self.ev_gates = torch.cuda.Event(), torch.cuda.Event()
+        self.handles = [self.img.handle, self.cross.handle]
+        torch.cuda.synchronize()
+
+    def step(self, i):
+        lk, wl, lay = self.lk, self.wl, self.lay
+        img, cr, tx = lay["image"], lay["cross"], lay["text"]
+        st, side = self.main.cuda_stream, self.side.cuda_stream
+        hi, hc = self.img.handle, self.cross.handle
+        s0, s1 = self.start, self.start + self.n_img
+        ct, ci, cc = self.count[0, :1], self.count[1, :1], self.count[2, :1]
+        d_c = lay["delta"].shape[1]
+        self.ev_start.record(self.main)
+        self.side.wait_event(self.ev_start)
+        lk.lookme_gate(hi, 1, self.n_text, lay["delta"], self.n_seq, d_c, tx["pos"],
+                       lay["w_g"][0], self.k_t, ct, side)
+        lk.lookme_gate(hi, 1, self.n_img, lay["delta"][s0:s1], self.n_img, d_c, None,
+                       lay["w_g"][1], self.k_i, ci, side)
+        lk.lookme_gate(hc, 1, self.n_seq, lay["delta"], self.n_seq, d_c, None, lay["w_g"][2],
+                       self.k_c, cc, side)
+        self.ev_gates.record(self.side)
+        lk.lookme_route(hc, 1, self.n_seq, wl.d_h, lay["h_dec"], cr["wt"], self.q_c, self.sc_c, st)
+        lk.lookme_lookup(hc, 1, self.n_seq, self.q_c, self.sc_c, self.pr_c, self.w_c, st)
+        lk.lookme_route(hi, 1, self.n_img, wl.d_in, img["x"], img["wt"], self.q_i, self.sc_i, st)
+        lk.lookme_lookup(hi, 1, self.n_img, self.q_i, self.sc_i, self.pr_i, self.w_i, st)
+        self.main.wait_event(self.ev_gates)
+        lk.lookme_inject_text(lk.DTYPE_CODE[tx["table"].dtype], tx["table"], tx["vocab"],
+                              tx["d_t"], self.n_text, tx["pos"], tx["ids"], self.k_t, ct,
+                              self.hidden, self.n_seq, wl.d_h, st)
+        lk.lookme_inject_gated(hi, 1, self.n_img, self.k_i, ci, self.sc_i, self.pr_i, self.w_i,
+                               self.hidden[s0:s1], wl.d_h, st)
+        lk.lookme_inject_gated(hc, 1, self.n_seq, self.k_c, cc, self.sc_c, self.pr_c, self.w_c,
+                               self.hidden, wl.d_h, st)
+
+    timed = Bench.timed
+
+    def profiled(self, steps):
+        """Per-kernel-group times of each pathway's handle (HIP events on the
+        launch streams), milliseconds per launch."""
+        lk = self.lk
+        for h in self.handles:
+            lk.lookme_profile_read(h, 0, reset=True)
+            lk.lookme_profile_enable(h, True)
+        self.timed(steps)
+        out = {}
+        for h, name in zip(self.handles, ("image", "cross")):
+            for g, grp in enumerate(lk.GROUPS):
+                c, ms = lk.lookme_profile_read(h, g)
+                if c:
+                    out[f"{name}.{grp}"] = ms / c
+            lk.lookme_profile_enable(h, False)
+            lk.lookme_profile_read(h, 0, reset=True)
+        return out
+
+
+def run_layer(args, wl):
+    b = LayerBench(wl, args.workload)
+    for i in range(args.warmup):
+        b.step(i)
+    el = b.timed(args.steps)
+    ms_step = el * 1000.0 / args.steps
+    prof = b.profiled(args.steps)
+    es = b.lay["h_dec"].element_size()
+    nonempty = int(b.torch.unique(b.sc_i).numel())
+    score_bytes = int(nonempty * wl.prims * wl.d_e * es + wl.n_tokens * wl.d_e * es
+                      + wl.n_tokens * 4 + wl.n_tokens * wl.top_k * 8)
+    score_ms = prof.get("image.score")
+    achieved = score_bytes / (score_ms * 1e-3) / 1e9 if score_ms else None
+    counts = b.count[:, 0].tolist()
+    line = {
+        "metric": METRIC, "value": round(b.n_seq / (el / args.steps), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"layer_{wl.name}_text{b.n_text}", "positions": b.n_seq,
+                   "image_positions": b.n_img, "text_positions": b.n_text,
+                   "text_vocab": b.VOCAB, "cross_table": [b.CROSS_SCENES, b.CROSS_PRIMS,
+                                                          b.CROSS_K],
+                   "open_gates": {"text": counts[0], "image": counts[1], "cross": counts[2]},
+                   "d_h": wl.d_h, "d_e": wl.d_e},
+        "roofline": {"bound": "hbm", "kernel": "score_kernel of the image pathway",
+                     "achieved": round(achieved, 1) if achieved else None,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
+                     "traffic": None, "algorithmic_bytes_per_launch": score_bytes},
+        "cpu_baseline": None,
+        "kernels": {k: {"avg_us": round(v * 1000.0, 3)} for k, v in prof.items()},
+    }
+    print(json.dumps(line), flush=True)
 
 
 def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
@@ -425,6 +595,7 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
     w_p = None
     if b.netprop:
         w_p = O.to_f64(to_np(b.w_p_t), dt).transpose(0, 2, 1)
+    w_g = O.to_f64(to_np(b.w_g), dt) if b.gate else None
 
     # the sample is repeated until about min_seconds of CPU work have been
     # timed (the same inputs each time), so that the rate is not a single
@@ -455,13 +626,14 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
             res = O.run(O.to_f64(x, dt), None if wt is None else O.to_f64(wt, dt),
                         O.to_f64(K1, dt), Rows(K2), Rows(V), None, O.to_f64(D, dt),
                         O.to_f64(H, dt), k=wl.top_k, n_keep=n_keep, dtype=dt, mlp=mlp,
-                        fusion=fusion, propagation=w_p)
+                        fusion=fusion, propagation=w_p, w_g=w_g)
             el += time.perf_counter() - t0
             reps += 1
             assert res["hidden"].shape == (wl.layers + b.netprop, m, wl.d_h)
     return {"value": reps * wl.layers * m / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {m} of {wl.n_tokens} tokens x {wl.layers} layer(s), whole path "
-                      f"(projection..injection, n_keep={n_keep}"
+                      f"(projection..injection, "
+                      f"{'learned gate' if w_g is not None else f'n_keep={n_keep}'}"
                       f"{', relevance Level-2' if mlp is not None else ''}"
                       f"{', SwiGLU fusion' if fusion is not None else ''}"
                       f"{f', propagated to {b.netprop} more layers' if b.netprop else ''}), "
@@ -495,8 +667,15 @@ def main():
                         or wl.scenes % args.scales):
         raise SystemExit("--scales needs a one-layer workload (tokens a multiple of 4, scenes "
                          "divisible by the scales) without --relevance or --fusion")
+    if args.layer:
+        if args.relevance or args.fusion or args.scales or args.gate or wl.layers != 1:
+            raise SystemExit("--layer runs the layer's own pathways on a one-layer workload")
+        run_layer(args, wl)
+        return
+    if args.gate and args.scales:
+        raise SystemExit("--gate is not combined with --scales")
     b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion, args.netprop,
-              args.scales)
+              args.scales, args.gate)
 
     for i in range(args.warmup):
         b.step(i)
@@ -555,7 +734,9 @@ def main():
                               else "primitive keys"),
                    "injection": (f"SwiGLU fusion, d_ff {args.fusion}" if args.fusion
                                  else "prefix add of the retrieved rows"),
-                   "propagated_layers": args.netprop, "scales": args.scales},
+                   "propagated_layers": args.netprop, "scales": args.scales,
+                   "kept_set": ("learned gate, " + "+".join(str(c) for c in b.count.tolist())
+                                + " open" if args.gate else f"top {wl.n_keep} by criticality")},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kern,

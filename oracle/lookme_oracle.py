@@ -395,7 +395,7 @@ def run_multiscale(x_scales, w_t_scales, scene_keys, prim_keys, values, delta, h
 
 def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
         k: int, n_keep: int, dtype: str, score: str = "dot", mlp=None, fusion=None,
-        propagation=None):
+        propagation=None, w_g=None):
     """Whole path for L layers sharing one table (Sec. 3.3 inter-layer reuse).
 
     x [n, d_in]; w_t [L, d_e, d_in] or None; delta [L, n, d_c];
@@ -406,7 +406,9 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
     the prefix add.  ``propagation`` = w_p [m, d_v, d_v] (with ``fusion`` of
     at least m + 1 layers): one LookME layer whose R is carried to the m
     layers after it (Eq. 11, inject_propagated); then hidden, w_t and delta
-    hold [m + 1, ...], [1, ...] and [1, ...].  Returns a dict of per-layer
+    hold [m + 1, ...], [1, ...] and [1, ...].  ``w_g`` [L, d_c]: the kept set
+    of layer l is the learned gate's (Eq. 9, ``gate``) instead of the top
+    n_keep by criticality (n_keep is then not used).  Returns a dict of per-layer
     results: q [L,n,d_e], scene [L,n], prim [L,n,k], w [L,n,k],
     kept [L,n_keep], hidden [L,n,d_h] (with ``propagation``: L = 1 and
     hidden [m + 1, n, d_h]).
@@ -423,7 +425,10 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
             w1, b1, w2, b2 = mlp
             a = relevance_hidden(q, sc, scene_keys, w1, b1, dtype)
             pr, ww, _ = relevance_lookup(q, sc, a, w2, b2, prim_keys, k)
-        kept = select(criticality(delta[l]), n_keep)
+        if w_g is None:
+            kept = select(criticality(delta[l]), n_keep)
+        else:
+            kept = gate(delta[l], w_g[l])
         if propagation is not None:
             h = inject_propagated(hidden, values, P, sc, pr, ww, kept, propagation, fusion[0],
                                   fusion[1], fusion[2], dtype)
@@ -434,7 +439,8 @@ def run(x, w_t, scene_keys, prim_keys, values, bias, delta, hidden, *,
                              fusion[2][l], dtype)
         for name, v in zip(res, (q, sc, pr, ww, kept, h)):
             res[name].append(v)
-    out = {name: np.stack(v) for name, v in res.items()}
+    out = {name: (np.stack(v) if name != "kept" or w_g is None else v)
+           for name, v in res.items()}     # gated kept lists differ in length
     if propagation is not None:
         out["hidden"] = out["hidden"][0]
     return out

@@ -1009,3 +1009,32 @@ def test_lookme_layer_pathways_read_the_layer_inputs_and_add_in_order():
     # the text and image positions overlap the cross-modal ones: a changed
     # order would round differently somewhere
     assert np.intersect1d(text[0][full["text_kept"]], full["cross_kept"]).size > 0
+
+
+def test_run_with_learned_gate_composes_gate_and_inject():
+    """run(w_g=...) keeps exactly the gate's positions of each layer and
+    injects them as inject does; a gate that opens where the criticality
+    select keeps gives the same result as the select."""
+    inp, k = _tiny_inputs(75, L=2)
+    rng = np.random.default_rng(75)
+    w_g = _bf16_values(rng, (2, inp["delta"].shape[2]))
+    r = O.run(**inp, k=k, n_keep=0, dtype="bf16", w_g=w_g)
+    P = inp["prim_keys"].shape[1]
+    for l in range(2):
+        kept = B.gate(inp["delta"][l].tolist(), w_g[l].tolist())
+        assert r["kept"][l].tolist() == kept
+        want = O.inject(inp["hidden"][l], inp["values"], P, r["scene"][l], r["prim"][l],
+                        r["w"][l], np.array(kept), "bf16")
+        np.testing.assert_array_equal(r["hidden"][l], want)
+    # planted: Delta_t = c_t e_0 with W_g = e_0 opens the positive c_t, which
+    # (all |c| distinct) are the top n_keep by norm when the rest are tiny
+    one = dict(inp)
+    n, d_c = inp["delta"].shape[1], inp["delta"].shape[2]
+    c = np.concatenate([np.arange(1, 9) * 1.0, -np.arange(1, n - 7) * 2.0 ** -12])
+    d = np.zeros((1, n, d_c))
+    d[0, :, 0] = c
+    one.update(delta=d, hidden=inp["hidden"][:1], w_t=inp["w_t"][:1])
+    a = O.run(**one, k=k, n_keep=8, dtype="bf16")
+    b = O.run(**one, k=k, n_keep=0, dtype="bf16", w_g=np.eye(d_c)[:1])
+    np.testing.assert_array_equal(a["kept"][0], b["kept"][0])
+    np.testing.assert_array_equal(a["hidden"], b["hidden"])
