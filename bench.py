@@ -70,6 +70,9 @@ def parse():
                     help="time one whole LookME layer (Eq. 3) on a sequence of 64 + 192 text "
                          "positions around the workload's image block: text, image and "
                          "cross-modal pathways, each with its learned gate")
+    ap.add_argument("--two-streams", action="store_true",
+                    help="select the kept set on a second stream even where the lookup's "
+                         "bucketing launch can carry it (batches of at most 1024 rows)")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -188,7 +191,7 @@ def stored_traffic(wl):
 
 class Bench:
     def __init__(self, wl, seed, copies, relevance=0, fusion=0, netprop=0, scales=0,
-                 gate=False):
+                 gate=False, two_streams=False):
         import torch
         from paper_2607_16305_amd import lookme as lk
         from synth import make_inputs
@@ -253,6 +256,11 @@ class Bench:
             self.kept = torch.empty((gl, n), dtype=torch.int32, device=dev)
             self.count = torch.zeros((gl,), dtype=torch.int32, device=dev)
         self.handles = [t.handle for t in self.tables]
+        # small batches: the select rides in the lookup's bucketing launch on
+        # the one stream (lookme_lookup_select); a second stream's waits would
+        # cost more than the select itself
+        self.one_stream = (not two_streams and L * n <= 1024 and not relevance and not scales
+                           and not gate and not netprop)
         if scales:
             from synth import make_multiscale
             self.ms = make_multiscale(wl, seed, scales, device="cuda")
@@ -285,6 +293,18 @@ class Bench:
         lk, wl, inp = self.lk, self.wl, self.inp
         h = self.tables[i % self.copies].handle
         L, n = wl.layers, wl.n_tokens
+        if self.one_stream:
+            lk.lookme_route(h, L, n, wl.d_in, inp["x"], inp["wt"], self.q, self.scene,
+                            self.stream)
+            lk.lookme_lookup_select(h, L, n, self.q, self.scene, self.prim, self.w, wl.n_keep,
+                                    inp["delta"], wl.crit_dim, self.kept, self.stream)
+            if self.fus is None:
+                lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim,
+                                      self.w, self.hidden, wl.d_h, self.stream)
+            else:
+                lk.lookme_inject_fused(h, L, n, wl.n_keep, self.kept, self.scene, self.prim,
+                                       self.w, self.hidden, wl.d_h, self.stream)
+            return
         # the select starts after the previous step's inject (which reads the
         # kept buffer it overwrites) and runs beside the projection and
         # routing; measured faster than beside the Level-2 lookup, whose
@@ -675,7 +695,7 @@ def main():
     if args.gate and args.scales:
         raise SystemExit("--gate is not combined with --scales")
     b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion, args.netprop,
-              args.scales, args.gate)
+              args.scales, args.gate, args.two_streams)
 
     for i in range(args.warmup):
         b.step(i)
@@ -735,6 +755,8 @@ def main():
                    "injection": (f"SwiGLU fusion, d_ff {args.fusion}" if args.fusion
                                  else "prefix add of the retrieved rows"),
                    "propagated_layers": args.netprop, "scales": args.scales,
+                   "select": ("norms in the bucketing launch, top-n_keep in the Level-2 launch (one stream)" if b.one_stream
+                              else "second stream beside projection and routing"),
                    "kept_set": ("learned gate, " + "+".join(str(c) for c in b.count.tolist())
                                 + " open" if args.gate else f"top {wl.n_keep} by criticality")},
         "roofline": roofline,

@@ -131,6 +131,27 @@ lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void*
                               void* stream);
 
 /*
+ * lookme_lookup_select -- lookme_lookup and lookme_select of the same batch
+ * in one call on one stream, for callers that would otherwise order a second
+ * stream around the select (each cross-stream wait costs microseconds, which
+ * at small batches is a tenth of the path).  For batches of at most 1024
+ * rows (layers * n) the criticality norms of Eq. 9 are computed by extra
+ * workgroups of the bucketing launch, and when n <= 4096 each layer's top
+ * n_keep select (Eq. 10) runs as one extra workgroup of the Level-2 launch,
+ * beside the scoring units; what does not fit runs as its own kernels after
+ * the bucketing.  The results are the same bits as lookme_lookup followed by
+ * lookme_select:
+ *   prim_out, w_out as for lookme_lookup; kept_out [layers, n_keep] int32
+ *   ascending (unused when n_keep = 0); crit [layers, n, d_c].
+ * Requires what both calls require; needs the workspace of
+ * lookme_workspace_size(layers, n).
+ */
+lookme_status_t lookme_lookup_select(lookme_t h, int32_t layers, int64_t n, const void* q,
+                                     const int32_t* scene, int32_t* prim_out, float* w_out,
+                                     int64_t n_keep, const void* crit, int32_t d_c,
+                                     int32_t* kept_out, void* stream);
+
+/*
  * lookme_inject -- sparse injection (Eq. 9-10) and residual add (Eq. 2).
  *   crit     [layers, n, d_c]   Delta of each layer (the attention update);
  *                               criticality c_t = ||crit_t||_2

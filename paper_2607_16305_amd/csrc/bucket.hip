@@ -13,6 +13,7 @@
 // Within a bucket rows keep ascending order.  Scene values outside [0, S)
 // are clamped (results for such rows are undefined; memory stays in bounds).
 #include "common.h"
+#include "crit.h"
 #include "kernels.h"
 
 #include <algorithm>
@@ -200,12 +201,11 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_scatter_kernel(
 }
 
 // All three passes in one workgroup, for batches of at most one chunk
-// (saves two launches where launch latency dominates).
-__global__ __launch_bounds__(BK_THREADS) void bucket_small_kernel(
+// (saves two launches where launch latency dominates); hist: S ints of LDS.
+__device__ __forceinline__ void bucket_small_body(
     const int32_t* __restrict__ scene, int64_t rows, int S, int sbits, int shared_rows,
     int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ unit_scene,
-    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count) {
-  extern __shared__ int hist[];
+    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count, int* hist) {
   for (int i = threadIdx.x; i < S; i += BK_THREADS) hist[i] = 0;
   __syncthreads();
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -239,6 +239,64 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_small_kernel(
       offsets, unit_scene, unit_begin, unit_count);
   __syncthreads();
   if (valid) perm[hist[s] + rank] = t;
+}
+
+__global__ __launch_bounds__(BK_THREADS) void bucket_small_kernel(
+    const int32_t* __restrict__ scene, int64_t rows, int S, int sbits, int shared_rows,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ unit_scene,
+    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count) {
+  extern __shared__ int hist[];
+  bucket_small_body(scene, rows, S, sbits, shared_rows, offsets, perm, unit_scene, unit_begin,
+                    unit_count, hist);
+}
+
+// The bucketing of a small batch with the criticality norms of the same rows
+// (Eq. 9; independent of it) in the launch: workgroup 0 buckets, the others
+// compute the norms of BK_WAVES * NORM_ROWS_PER_WAVE rows each with the body
+// of crit_norm_kernel (same bits).
+constexpr int NORM_ROWS_PER_WAVE = 2;
+
+template <int DT>
+__global__ __launch_bounds__(BK_THREADS) void bucket_norm_kernel(
+    const int32_t* __restrict__ scene, int64_t rows, int S, int sbits, int shared_rows,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ unit_scene,
+    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count,
+    const char* __restrict__ crit, int64_t row_bytes, uint32_t* __restrict__ key) {
+  extern __shared__ int hist[];
+  if (blockIdx.x == 0) {
+    bucket_small_body(scene, rows, S, sbits, shared_rows, offsets, perm, unit_scene, unit_begin,
+                      unit_count, hist);
+    return;
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t nwg = gridDim.x - 1;
+  const int chunks = (int)(row_bytes / 16);
+  for (int64_t r = (int64_t)(blockIdx.x - 1) * BK_WAVES + wv; r < rows; r += nwg * BK_WAVES) {
+    const float acc = row_sumsq<DT>(crit + r * row_bytes, chunks, lane);
+    if (lane == 0) key[r] = as_u32(acc);
+  }
+}
+
+bool launch_bucket_norms(int dt, const int32_t* scene, int64_t rows, int S, int shared_rows,
+                         const BucketWs& ws, const void* crit, int d_c, uint32_t* key,
+                         hipStream_t st) {
+  if (rows == 0 || bucket_chunks(rows) != 1) return false;
+  int sbits = 0;
+  while ((1 << sbits) < S) ++sbits;
+  const int per_wg = BK_WAVES * NORM_ROWS_PER_WAVE;
+  const dim3 grid((unsigned)(1 + (rows + per_wg - 1) / per_wg));
+  const int64_t rb = (int64_t)d_c * (dt == DT_BF16 ? 2 : 4);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(bucket_norm_kernel<DT_BF16>, grid, dim3(BK_THREADS),
+                       (size_t)S * sizeof(int), st, scene, rows, S, sbits, shared_rows,
+                       ws.offsets, ws.perm, ws.unit_scene, ws.unit_begin, ws.unit_count,
+                       static_cast<const char*>(crit), rb, key);
+  else
+    hipLaunchKernelGGL(bucket_norm_kernel<DT_F32>, grid, dim3(BK_THREADS),
+                       (size_t)S * sizeof(int), st, scene, rows, S, sbits, shared_rows,
+                       ws.offsets, ws.perm, ws.unit_scene, ws.unit_begin, ws.unit_count,
+                       static_cast<const char*>(crit), rb, key);
+  return true;
 }
 
 hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, int shared_rows,

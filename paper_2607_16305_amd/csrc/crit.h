@@ -1,0 +1,167 @@
+// Criticality and the top-n_keep select of the sparse injection (arXiv
+// 2607.16305, Sec. 3.3, Eq. 9-10): the bodies shared by the stand-alone
+// kernels (inject.hip) and by the bucketing launch that carries the select
+// beside the bucketing of small batches (bucket.hip), so that both give the
+// same bits.
+//
+//   row_sumsq    one wave streams a row of Delta once (NORM_UNROLL 16-byte
+//                loads of a lane in flight) and returns its fp32 sum of
+//                squares, accumulated in a fixed order; stored as its bit
+//                pattern, it orders like the norm (non-negative floats order
+//                like their bits, and the square root keeps the order);
+//   select_layer one workgroup (1024 or 256 threads): 4-pass MSB-first radix select of
+//                the n_keep-th largest key (keys cached in LDS when they
+//                fit), then an order-preserving compaction (block prefix
+//                sums) of the kept token ids.
+#pragma once
+
+#include "common.h"
+
+namespace lookme {
+
+constexpr int NORM_UNROLL = 4;
+constexpr int SEL_THREADS = 1024;
+constexpr int SEL_WAVES = SEL_THREADS / WAVE;
+
+// CN > 0: a layer's keys (n <= CN) are first copied to LDS, so that the four
+// passes and the compaction read them there instead of from L2 (one global
+// round trip instead of five).  Element i sits at i + i / 32: the padding
+// keeps threads that walk ranges of 32 keys on distinct banks.  Launchers
+// take the smallest cache that holds n: the small one leaves room on the CU
+// for the workgroups of a kernel that runs beside the select.
+constexpr int SEL_CACHE_SMALL = 4096, SEL_CACHE_N = 32768;
+
+template <int DT>
+__device__ __forceinline__ float row_sumsq(const char* __restrict__ p, int chunks, int lane) {
+  float acc0 = 0.f, acc1 = 0.f;
+  // chunks past the row re-read its last chunk and are not summed (a
+  // 4096-element bf16 row is two rounds)
+  for (int c0 = lane; c0 < chunks; c0 += NORM_UNROLL * WAVE) {
+    u32x4_t vv[NORM_UNROLL];
+#pragma unroll
+    for (int u = 0; u < NORM_UNROLL; ++u) {
+      const int c = c0 + u * WAVE;
+      vv[u] = ld16_nt(p + (int64_t)(c < chunks ? c : chunks - 1) * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < NORM_UNROLL; ++u) {
+      if (c0 + u * WAVE >= chunks) continue;
+      const u32x4_t v = vv[u];
+      if constexpr (DT == DT_BF16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = bf16lo(v[e]), hi = bf16hi(v[e]);
+          acc0 = fmaf(lo, lo, acc0);
+          acc1 = fmaf(hi, hi, acc1);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float f = as_f32(v[e]);
+          if (e & 1) acc1 = fmaf(f, f, acc1);
+          else acc0 = fmaf(f, f, acc0);
+        }
+      }
+    }
+  }
+  float acc = acc0 + acc1;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d, 64);
+  return acc;
+}
+
+// LDS words of select_layer's key cache for CN keys.
+constexpr int sel_cache_words(int cn) { return cn > 0 ? cn + cn / 32 : 1; }
+
+// The kept set of one layer: kept[0 .. n_keep) = the n_keep tokens of
+// largest key (ties: lowest token), ascending.  Called by all THREADS (a
+// multiple of 256) threads of a workgroup; cache: sel_cache_words(CN) words
+// of LDS.  COHERENT: the keys were written by other workgroups of the same
+// launch (read with device-scope loads; needs CN > 0, n <= CN).
+template <int CN, bool COHERENT, int THREADS = SEL_THREADS>
+__device__ __forceinline__ void select_layer(const uint32_t* __restrict__ gkey, int64_t n,
+                                             int64_t n_keep, int32_t* __restrict__ kept,
+                                             uint32_t* cache) {
+  constexpr bool CACHED = CN > 0;
+  constexpr int WAVES = THREADS / WAVE;
+  static_assert(CACHED || !COHERENT, "coherent reads go through the LDS cache");
+  static_assert(THREADS % 256 == 0, "a thread per radix bin");
+  __shared__ int hist[256];
+  __shared__ int wsum[WAVES];
+  __shared__ uint32_t s_prefix;
+  __shared__ int s_need;
+  if (n_keep == 0) return;
+  const int tid = threadIdx.x;
+  if constexpr (CACHED) {
+    for (int i = tid; i < n; i += THREADS) {
+      if constexpr (COHERENT)
+        cache[i + (i >> 5)] = __hip_atomic_load(gkey + i, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+      else
+        cache[i + (i >> 5)] = gkey[i];
+    }
+    __syncthreads();
+  }
+  auto key = [&](int64_t i) -> uint32_t {
+    if constexpr (CACHED) return cache[i + (i >> 5)];
+    else return gkey[i];
+  };
+  // every thread owns a contiguous range of tokens
+  const int64_t per = (n + THREADS - 1) / THREADS;
+  const int64_t i0 = min<int64_t>(n, tid * per), i1 = min<int64_t>(n, i0 + per);
+
+  // ---- radix select (MSB first, 8 bits a pass): the n_keep-th largest T ----
+  uint32_t prefix = 0, mask = 0;
+  int need = (int)n_keep;   // rank from the top still to be located
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (tid < 256) hist[tid] = 0;
+    __syncthreads();
+    for (int64_t i = i0; i < i1; ++i) {
+      const uint32_t k = key(i);
+      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1);
+    }
+    __syncthreads();
+    // thread t looks at bin 255 - t: cum = keys in bins >= that bin
+    const int b = 255 - tid;
+    const int h = tid < 256 ? hist[b] : 0;
+    const int cum = block_scan_incl<4>(h, wsum);
+    if (tid < 256 && cum - h < need && need <= cum) {
+      s_prefix = prefix | ((uint32_t)b << shift);
+      s_need = need - (cum - h);
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    need = s_need;
+    mask |= 255u << shift;
+  }
+  const uint32_t T = prefix;   // kept: keys > T, plus the first `need` keys == T
+  const int take_eq = need;
+
+  // ---- order-preserving compaction: one block scan of per-thread counts ----
+  int n_gt = 0, n_eq = 0;
+  for (int64_t i = i0; i < i1; ++i) {
+    const uint32_t k = key(i);
+    n_gt += k > T;
+    n_eq += k == T;
+  }
+  const int gt_before = block_scan_incl<WAVES>(n_gt, wsum) - n_gt;
+  const int eq_before = block_scan_incl<WAVES>(n_eq, wsum) - n_eq;
+  int g = gt_before, e = eq_before;
+  for (int64_t i = i0; i < i1; ++i) {
+    const uint32_t k = key(i);
+    if (k > T) {
+      const int pos = g + min(e, take_eq);
+      if (pos < n_keep) kept[pos] = (int32_t)i;
+      ++g;
+    } else if (k == T) {
+      if (e < take_eq) {
+        const int pos = g + e;
+        if (pos < n_keep) kept[pos] = (int32_t)i;
+      }
+      ++e;
+    }
+  }
+}
+
+}  // namespace lookme

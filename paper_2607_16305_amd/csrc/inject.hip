@@ -16,13 +16,12 @@
 //               in flight together), fp32 weighted sum in a fixed order, one
 //               rounding of H + sum, in-place store.
 #include "common.h"
+#include "crit.h"
 #include "kernels.h"
 
 namespace lookme {
 
 constexpr int NORM_WAVES = 4;
-constexpr int SEL_THREADS = 1024;
-constexpr int SEL_WAVES = SEL_THREADS / WAVE;
 constexpr int INJ_THREADS = 256;
 
 template <int DT>
@@ -32,120 +31,18 @@ __global__ __launch_bounds__(NORM_WAVES * WAVE) void crit_norm_kernel(
   const int lane = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * NORM_WAVES + (threadIdx.x >> 6);
   if (r >= rows) return;
-  const char* p = crit + r * row_bytes;
-  const int chunks = (int)(row_bytes / 16);
-  float acc0 = 0.f, acc1 = 0.f;
-  for (int c = lane; c < chunks; c += WAVE) {
-    const u32x4_t v = ld16_nt(p + (int64_t)c * 16);
-    if constexpr (DT == DT_BF16) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float lo = bf16lo(v[e]), hi = bf16hi(v[e]);
-        acc0 = fmaf(lo, lo, acc0);
-        acc1 = fmaf(hi, hi, acc1);
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float f = as_f32(v[e]);
-        if (e & 1) acc1 = fmaf(f, f, acc1);
-        else acc0 = fmaf(f, f, acc0);
-      }
-    }
-  }
-  float acc = acc0 + acc1;
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d, 64);
+  const float acc = row_sumsq<DT>(crit + r * row_bytes, (int)(row_bytes / 16), lane);
   if (lane == 0) key[r] = as_u32(acc);
 }
-
-// CN > 0: a layer's keys (n <= CN) are first copied to LDS, so that the four
-// passes and the compaction read them there instead of from L2 (one global
-// round trip instead of five).  Element i sits at i + i / 32: the padding
-// keeps threads that walk ranges of 32 keys on distinct banks.  The launcher
-// takes the smallest cache that holds n: the small one leaves room on the CU
-// for the workgroups of a kernel that runs beside the select.
-constexpr int SEL_CACHE_SMALL = 4096, SEL_CACHE_N = 32768;
 
 template <int CN>
 __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
     const uint32_t* __restrict__ key_all, int64_t n, int64_t n_keep,
     int32_t* __restrict__ kept_all) {
-  constexpr bool CACHED = CN > 0;
-  __shared__ int hist[256];
-  __shared__ int wsum[SEL_WAVES];
-  __shared__ uint32_t s_prefix;
-  __shared__ int s_need;
-  __shared__ uint32_t cache[CACHED ? CN + CN / 32 : 1];
+  __shared__ uint32_t cache[sel_cache_words(CN)];
   const int layer = blockIdx.x;
-  const uint32_t* gkey = key_all + (int64_t)layer * n;
-  int32_t* kept = kept_all + (int64_t)layer * n_keep;
-  if (n_keep == 0) return;
-  const int tid = threadIdx.x;
-  if constexpr (CACHED) {
-    for (int i = tid; i < n; i += SEL_THREADS) cache[i + (i >> 5)] = gkey[i];
-    __syncthreads();
-  }
-  auto key = [&](int64_t i) -> uint32_t {
-    if constexpr (CACHED) return cache[i + (i >> 5)];
-    else return gkey[i];
-  };
-  // every thread owns a contiguous range of tokens
-  const int64_t per = (n + SEL_THREADS - 1) / SEL_THREADS;
-  const int64_t i0 = min<int64_t>(n, tid * per), i1 = min<int64_t>(n, i0 + per);
-
-  // ---- radix select (MSB first, 8 bits a pass): the n_keep-th largest T ----
-  uint32_t prefix = 0, mask = 0;
-  int need = (int)n_keep;   // rank from the top still to be located
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();
-    for (int64_t i = i0; i < i1; ++i) {
-      const uint32_t k = key(i);
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1);
-    }
-    __syncthreads();
-    // thread t looks at bin 255 - t: cum = keys in bins >= that bin
-    const int b = 255 - tid;
-    const int h = tid < 256 ? hist[b] : 0;
-    const int cum = block_scan_incl<4>(h, wsum);
-    if (tid < 256 && cum - h < need && need <= cum) {
-      s_prefix = prefix | ((uint32_t)b << shift);
-      s_need = need - (cum - h);
-    }
-    __syncthreads();
-    prefix = s_prefix;
-    need = s_need;
-    mask |= 255u << shift;
-  }
-  const uint32_t T = prefix;   // kept: keys > T, plus the first `need` keys == T
-  const int take_eq = need;
-
-  // ---- order-preserving compaction: one block scan of per-thread counts ----
-  int n_gt = 0, n_eq = 0;
-  for (int64_t i = i0; i < i1; ++i) {
-    const uint32_t k = key(i);
-    n_gt += k > T;
-    n_eq += k == T;
-  }
-  const int gt_before = block_scan_incl<SEL_WAVES>(n_gt, wsum) - n_gt;
-  const int eq_before = block_scan_incl<SEL_WAVES>(n_eq, wsum) - n_eq;
-  int g = gt_before, e = eq_before;
-  for (int64_t i = i0; i < i1; ++i) {
-    const uint32_t k = key(i);
-    if (k > T) {
-      const int pos = g + min(e, take_eq);
-      if (pos < n_keep) kept[pos] = (int32_t)i;
-      ++g;
-    } else if (k == T) {
-      if (e < take_eq) {
-        const int pos = g + e;
-        if (pos < n_keep) kept[pos] = (int32_t)i;
-      }
-      ++e;
-    }
-  }
+  select_layer<CN, false>(key_all + (int64_t)layer * n, n, n_keep,
+                          kept_all + (int64_t)layer * n_keep, cache);
 }
 
 // TO_R: the weighted row sum R of kept row j is rounded to the storage

@@ -235,6 +235,76 @@ lookme_status_t run_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_keep
                     "inject launch");
 }
 
+lookme_status_t check_lookup_out(const void* q, const int32_t* scene, int32_t* prim_out,
+                                 float* w_out) {
+  LOOKME_TRY(check_ptr(q, "q"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(prim_out, "prim_out"));
+  return check_ptr(w_out, "w_out");
+}
+
+// The sparse-injection select carried by a lookup (lookme_lookup_select).
+struct SelectArgs {
+  const void* crit;
+  int32_t d_c;
+  int64_t n_keep;
+  int32_t* kept;
+};
+
+// bucketing and Level-2 scoring, with the select of `sel` carried along:
+// its norms in the bucketing launch (small batches) and its select in the
+// Level-2 launch (n <= SEL_SIDE_MAX_N); what does not fit runs as its own
+// kernels after the bucketing
+lookme_status_t run_lookup(lookme_t h, const Layout& L, int32_t layers, int64_t n, const void* q,
+                           const int32_t* scene, int32_t* prim_out, float* w_out,
+                           const SelectArgs* sel, hipStream_t st) {
+  const lookme_desc_t& d = h->d;
+  const int64_t rows = (int64_t)layers * n;
+  char* ws = static_cast<char*>(h->ws);
+  lookme::BucketWs b{};
+  b.chunk_hist = reinterpret_cast<int32_t*>(ws + L.chunk_hist);
+  b.local_rank = reinterpret_cast<int32_t*>(ws + L.local_rank);
+  b.offsets = reinterpret_cast<int32_t*>(ws + L.offsets);
+  b.perm = reinterpret_cast<int32_t*>(ws + L.perm);
+  b.unit_scene = reinterpret_cast<int32_t*>(ws + L.unit_scene);
+  b.unit_begin = reinterpret_cast<int32_t*>(ws + L.unit_begin);
+  b.unit_count = reinterpret_cast<int32_t*>(ws + L.unit_count);
+  b.chunks = lookme::bucket_chunks(rows);
+  b.max_units = lookme::bucket_max_units(rows, d.num_scenes);
+  uint32_t* key = reinterpret_cast<uint32_t*>(ws + L.crit_key);
+  const bool select = sel != nullptr && sel->n_keep > 0;
+  {
+    Timed tm(h, LOOKME_GROUP_BUCKET, st);
+    const int shared_rows =
+        lookme::shared_unit_rows((int64_t)d.key_dim * elem_size(d.dtype), d.top_k);
+    bool normed = false;
+    if (select)
+      normed = lookme::launch_bucket_norms(d.dtype, scene, rows, d.num_scenes, shared_rows, b,
+                                           sel->crit, sel->d_c, key, st);
+    if (normed) {
+      LOOKME_TRY(hip_status(hipGetLastError(), "bucketing + norms launch"));
+    } else {
+      LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, shared_rows, b, st),
+                            "bucketing launch"));
+      if (select)
+        LOOKME_TRY(hip_status(lookme::launch_crit_norm(d.dtype, rows, sel->crit, sel->d_c, key,
+                                                       st),
+                              "criticality launch"));
+    }
+  }
+  const bool ride = select && n <= lookme::SEL_SIDE_MAX_N;
+  if (select && !ride)
+    LOOKME_TRY(hip_status(lookme::launch_crit_select(layers, n, sel->n_keep, key, sel->kept, st),
+                          "select launch"));
+  const lookme::SideSelect side{layers, n, select ? sel->n_keep : 0, key,
+                                select ? sel->kept : nullptr};
+  Timed tm(h, LOOKME_GROUP_SCORE, st);
+  return hip_status(lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
+                                          d.prims_per_scene, d.top_k, prim_out, w_out, st,
+                                          ride ? &side : nullptr),
+                    "lookup launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -410,37 +480,32 @@ lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void*
   LOOKME_TRY(check_handle(h));
   LOOKME_TRY(check_layers_n(layers, n));
   if (n == 0) return LOOKME_OK;
-  LOOKME_TRY(check_ptr(q, "q"));
-  LOOKME_TRY(check_ptr(scene, "scene"));
-  LOOKME_TRY(check_ptr(prim_out, "prim_out"));
-  LOOKME_TRY(check_ptr(w_out, "w_out"));
+  LOOKME_TRY(check_lookup_out(q, scene, prim_out, w_out));
   Layout L;
   LOOKME_TRY(check_workspace(h, layers, n, &L));
-  const lookme_desc_t& d = h->d;
-  const int64_t rows = (int64_t)layers * n;
-  char* ws = static_cast<char*>(h->ws);
-  lookme::BucketWs b{};
-  b.chunk_hist = reinterpret_cast<int32_t*>(ws + L.chunk_hist);
-  b.local_rank = reinterpret_cast<int32_t*>(ws + L.local_rank);
-  b.offsets = reinterpret_cast<int32_t*>(ws + L.offsets);
-  b.perm = reinterpret_cast<int32_t*>(ws + L.perm);
-  b.unit_scene = reinterpret_cast<int32_t*>(ws + L.unit_scene);
-  b.unit_begin = reinterpret_cast<int32_t*>(ws + L.unit_begin);
-  b.unit_count = reinterpret_cast<int32_t*>(ws + L.unit_count);
-  b.chunks = lookme::bucket_chunks(rows);
-  b.max_units = lookme::bucket_max_units(rows, d.num_scenes);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  {
-    Timed tm(h, LOOKME_GROUP_BUCKET, st);
-    const int shared_rows =
-        lookme::shared_unit_rows((int64_t)d.key_dim * elem_size(d.dtype), d.top_k);
-    LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, shared_rows, b, st),
-                          "bucketing launch"));
+  return run_lookup(h, L, layers, n, q, scene, prim_out, w_out, nullptr,
+                    static_cast<hipStream_t>(stream));
+}
+
+lookme_status_t lookme_lookup_select(lookme_t h, int32_t layers, int64_t n, const void* q,
+                                     const int32_t* scene, int32_t* prim_out, float* w_out,
+                                     int64_t n_keep, const void* crit, int32_t d_c,
+                                     int32_t* kept_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_keep(n, n_keep));
+  LOOKME_TRY(check_crit_dim(h->d, d_c));
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_lookup_out(q, scene, prim_out, w_out));
+  if (n_keep > 0) {
+    LOOKME_TRY(check_ptr(crit, "crit"));
+    LOOKME_TRY(check_ptr(kept_out, "kept_out"));
   }
-  Timed tm(h, LOOKME_GROUP_SCORE, st);
-  return hip_status(lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
-                                          d.prims_per_scene, d.top_k, prim_out, w_out, st),
-                    "lookup launch");
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  const SelectArgs sel{crit, d_c, n_keep, kept_out};
+  return run_lookup(h, L, layers, n, q, scene, prim_out, w_out, n_keep > 0 ? &sel : nullptr,
+                    static_cast<hipStream_t>(stream));
 }
 
 lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,

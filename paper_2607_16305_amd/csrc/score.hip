@@ -23,6 +23,7 @@
 //    up to 4 (8) tiles.  Lists are merged inside the wave (4 lanes per row).
 //    Suits large buckets and routing of many rows.
 #include "common.h"
+#include "crit.h"
 #include "dtl.h"
 #include "kernels.h"
 #include "route_merge.h"
@@ -55,6 +56,12 @@ struct ScoreParams {
   int shared_rows;          // lookup: rows of a shared unit (at most)
   int32_t* out_idx;         // routing: scene[rows]; lookup: prim[rows, k]
   float* out_w;             // lookup: w[rows, k]
+  // lookup with the select of the batch riding along (side0 > 0): launch
+  // slot side0 + l selects layer l's kept set
+  int side0;
+  int64_t crit_n, n_keep;
+  const uint32_t* crit_key; // [layers * crit_n] criticality keys
+  int32_t* kept;            // [layers, n_keep]
 };
 
 template <int KS, bool MASKED>
@@ -456,6 +463,19 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
 
 // KS: compile-time number of chunk steps; with MASKED, steps >= ks are
 // skipped (row widths that are not a power-of-two multiple of 64 bytes).
+// The select of the batch carried by a Level-2 launch (Eq. 9-10): slot
+// side0 + l selects layer l's kept set from its criticality keys (computed
+// by an earlier launch), with the keys cached in `smem`: the body of
+// crit_select_kernel on the launch's 256 threads, so the bits are its.
+template <int KS>
+__device__ __forceinline__ void side_select(const ScoreParams& a, char* smem) {
+  const int layer = blockIdx.x - a.side0;
+  select_layer<SEL_SIDE_MAX_N, false, SC_THREADS>(a.crit_key + (int64_t)layer * a.crit_n,
+                                                  a.crit_n, a.n_keep,
+                                                  a.kept + (int64_t)layer * a.n_keep,
+                                                  reinterpret_cast<uint32_t*>(smem));
+}
+
 // KL: per-lane candidate list length (>= k) for lookup; 1 for routing.
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
 __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
@@ -463,6 +483,13 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   constexpr int STAGE_BYTES = (LOOKUP ? shared_nbuf(KS) : 2) * KS * 1024;
   constexpr int SMEM = MERGE_BYTES > STAGE_BYTES ? MERGE_BYTES : STAGE_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  if constexpr (LOOKUP) {
+    static_assert(SMEM >= sel_cache_words(SEL_SIDE_MAX_N) * 4, "the side select's key cache");
+    if (a.side0 > 0 && (int)blockIdx.x >= a.side0) {
+      side_select<KS>(a, smem);
+      return;
+    }
+  }
 
   int64_t begin;
   int nr;
@@ -612,7 +639,8 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
 }
 
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
-                         int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st) {
+                         int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st,
+                         const SideSelect* side) {
   ScoreParams p{};
   p.q = static_cast<const char*>(q);
   p.keys = static_cast<const char*>(prim_keys);
@@ -628,7 +656,15 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
   p.k = k;
   p.out_idx = prim;
   p.out_w = w;
-  const int grid = (int)((ws.max_units + 15) / 16 * 16);   // whole pairs on every XCD
+  int grid = (int)((ws.max_units + 15) / 16 * 16);   // whole pairs on every XCD
+  if (side != nullptr && side->n_keep > 0 && side->n > 0) {
+    p.side0 = grid;
+    p.crit_n = side->n;
+    p.n_keep = side->n_keep;
+    p.crit_key = side->key;
+    p.kept = side->kept;
+    grid += side->layers;
+  }
   if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st);
   if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st);
   if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st);

@@ -31,7 +31,7 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_inject_fused", "lookme_set_propagation", "lookme_inject_propagated",
             "lookme_set_multiscale", "lookme_inject_multiscale", "lookme_gate",
             "lookme_inject_gated", "lookme_inject_fused_gated", "lookme_inject_propagated_gated",
-            "lookme_inject_text", "lookme_destroy", "lookme_last_error",
+            "lookme_inject_text", "lookme_lookup_select", "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
 GROUPS = ("project", "route", "bucket", "score", "norm", "select", "inject")
@@ -101,6 +101,8 @@ def load():
         "lookme_inject_text": [ctypes.c_int32, _vp, ctypes.c_int64, ctypes.c_int32,
                                ctypes.c_int64, _vp, _vp, _vp, _vp, _vp, ctypes.c_int64,
                                ctypes.c_int32, _vp],
+        "lookme_lookup_select": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                 ctypes.c_int64, _vp, ctypes.c_int32, _vp, _vp],
         "lookme_destroy": [_vp],
         "lookme_profile_enable": [_vp, ctypes.c_int32],
         "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
@@ -223,6 +225,13 @@ def lookme_inject_multiscale(h, n, n_keep, kept, scene, prim, w, hidden, d_h, st
                                            _ptr(w), _ptr(hidden), d_h, _stream(stream)))
 
 
+def lookme_lookup_select(h, layers, n, q, scene, prim_out, w_out, n_keep, crit, d_c, kept_out,
+                         stream=None):
+    _check(load().lookme_lookup_select(h, layers, n, _ptr(q), _ptr(scene), _ptr(prim_out),
+                                       _ptr(w_out), n_keep, _ptr(crit), d_c, _ptr(kept_out),
+                                       _stream(stream)))
+
+
 def lookme_gate(h, layers, n, delta, delta_rows, d_c, pos, w_g, kept_out, count_out,
                 stream=None):
     _check(load().lookme_gate(h, layers, n, _ptr(delta), delta_rows, d_c, _ptr(pos), _ptr(w_g),
@@ -321,6 +330,13 @@ class Table:
         self.reserve(layers, n)
         lookme_inject(self.handle, layers, n, n_keep, crit, crit.shape[-1], scene, prim, w,
                       hidden, hidden.shape[-1], kept_out, stream)
+
+    def lookup_select(self, q, scene, prim_out, w_out, crit, kept_out, n_keep, layers=1,
+                      stream=None):
+        n = scene.numel() // layers
+        self.reserve(layers, n)
+        lookme_lookup_select(self.handle, layers, n, q, scene, prim_out, w_out, n_keep, crit,
+                             crit.shape[-1], kept_out, stream)
 
     def select(self, crit, kept_out, n_keep, layers=1, stream=None):
         n = crit.numel() // (layers * crit.shape[-1])

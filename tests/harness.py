@@ -85,6 +85,18 @@ class Run:
         return self
 
 
+def run_fused_select(r: Run) -> Run:
+    """The pass of ``r`` with lookme_lookup_select (the select carried by the
+    lookup's bucketing launch, one stream), then lookme_inject_kept."""
+    inp, L = r.inp, r.L
+    r.table.route(inp["x"], inp["wt"], r.q, r.scene, layers=L, stream=r.stream)
+    r.table.lookup_select(r.q, r.scene, r.prim, r.w, inp["delta"], r.kept, r.n_keep, layers=L,
+                          stream=r.stream)
+    r.table.inject_kept(r.kept, r.scene, r.prim, r.w, r.hidden, r.n_keep, layers=L,
+                        stream=r.stream)
+    return r
+
+
 class RelevanceRun(Run):
     """A pass with Level-2 in the paper's form (Eq. 6-7): routing, the
     relevance lookup (hidden activations, primitives, weights), then the kept

@@ -206,6 +206,46 @@ def test_select_on_second_stream_then_inject_kept(name):
         assert torch.equal(getattr(ref, key), getattr(r, key)), key
 
 
+@pytest.mark.parametrize("name", ["bf16_ragged_l2", "f32_proj_l3", "bf16_one_token",
+                                  "bf16_k32_shared", "bf16_many_tokens", "image"])
+def test_lookup_select_one_launch(name):
+    """lookme_lookup_select (the select riding in the bucketing launch for
+    batches of at most 1024 rows, after it otherwise): the oracle's results,
+    the same bits as lookme_lookup + lookme_select, and again on a second
+    call (the arrival counters were left at zero)."""
+    from tests.harness import Run, check_run, run_fused_select
+    wl = WORKLOADS[1] if name == "image" else SMALL[name]
+    _announce(f"lookup_select {name}")
+    inp = make_inputs(wl, seed=32, device=DEV)
+    ref = Run(inp).run()
+    for rep_i in range(2):
+        r = run_fused_select(Run(inp, table=ref.table))
+        toks = np.arange(0, wl.n_tokens, 7) if wl.n_tokens > 2000 else None
+        rep = check_run(r, tokens=toks)
+        assert rep.ok, str(rep)
+        for key in ("q", "scene", "prim", "w", "kept", "hidden"):
+            assert torch.equal(getattr(ref, key), getattr(r, key)), (rep_i, key)
+
+
+def test_lookup_select_integer_ties_and_edges():
+    """Exact integer criticalities (many equal norms at the cut): the fused
+    select keeps the lowest tokens like the stand-alone one; n_keep = n and
+    n_keep = 0."""
+    from tests.harness import Run, run_fused_select
+    _announce("lookup_select ties")
+    inp = make_integer_inputs(n=211, S=7, P=45, d_e=128, d_v=32, d_h=48, k=6, n_keep=70,
+                              seed=5, dtype="bf16", device=DEV, layers=2)
+    for n_keep in (70, 211, 1):
+        ref = Run(inp, n_keep=n_keep).run()
+        r = run_fused_select(Run(inp, n_keep=n_keep, table=ref.table))
+        torch.cuda.synchronize()
+        for key in ("prim", "w", "kept", "hidden"):
+            assert torch.equal(getattr(ref, key), getattr(r, key)), (n_keep, key)
+    r = run_fused_select(Run(inp, n_keep=0))
+    torch.cuda.synchronize()
+    assert torch.equal(r.hidden, r.h_in)
+
+
 def test_layers_batched_equal_sequential():
     from tests.harness import Run
     wl = SMALL["bf16_ragged_l2"].scaled(layers=3)
