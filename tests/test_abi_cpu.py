@@ -330,3 +330,24 @@ def test_gate_and_text_entry_points_validate(lib):
     assert S(lambda: txt(p=None)) == lk.LOOKME_ERR_INVALID
     assert S(lambda: txt(kept=FAKE + 8)) == lk.LOOKME_ERR_INVALID
     assert S(lambda: txt(n_text=0, p=None)) == lk.LOOKME_OK
+
+
+def test_lookup_select_validates(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        call = lambda n=8, n_keep=2, d_c=2048, p=FAKE, crit=FAKE, kept=FAKE: \
+            lk.lookme_lookup_select(h, 1, n, p, p, p, p, n_keep, crit, d_c, kept, 0)
+        assert S(lambda: call(n_keep=9)) == lk.LOOKME_ERR_INVALID        # n_keep > n
+        assert S(lambda: call(n_keep=-1)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(d_c=1001)) == lk.LOOKME_ERR_UNSUPPORTED    # 2002-byte rows
+        assert S(lambda: call(p=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(crit=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(kept=FAKE + 4)) == lk.LOOKME_ERR_INVALID   # misaligned
+        assert S(lambda: call(n_keep=0, crit=None, kept=None)) == lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: call()) == lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: call(n=0, n_keep=0, p=None, crit=None, kept=None)) == lk.LOOKME_OK
+    finally:
+        lk.lookme_destroy(h)
