@@ -477,15 +477,17 @@ __device__ __forceinline__ void side_select(const ScoreParams& a, char* smem) {
 }
 
 // KL: per-lane candidate list length (>= k) for lookup; 1 for routing.
-template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
+// SIDE (lookup only): launch slots from a.side0 on run side_select; a
+// separate instantiation, so that the kernels without it keep their code.
+template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool SIDE = false>
 __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   constexpr int MERGE_BYTES = SC_WAVES * 4 * 16 * KL * 8;
   constexpr int STAGE_BYTES = (LOOKUP ? shared_nbuf(KS) : 2) * KS * 1024;
   constexpr int SMEM = MERGE_BYTES > STAGE_BYTES ? MERGE_BYTES : STAGE_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-  if constexpr (LOOKUP) {
+  if constexpr (LOOKUP && SIDE) {
     static_assert(SMEM >= sel_cache_words(SEL_SIDE_MAX_N) * 4, "the side select's key cache");
-    if (a.side0 > 0 && (int)blockIdx.x >= a.side0) {
+    if ((int)blockIdx.x >= a.side0) {
       side_select<KS>(a, smem);
       return;
     }
@@ -531,11 +533,11 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
 // Launchers
 // ---------------------------------------------------------------------------
 
-template <int DT, bool LOOKUP, int KL>
+template <int DT, bool LOOKUP, int KL, bool SIDE = false>
 static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t st) {
-#define LOOKME_SCORE_LAUNCH(KS_, M_)                                                          \
-  hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL>), dim3(grid), dim3(SC_THREADS), 0, \
-                     st, p)
+#define LOOKME_SCORE_LAUNCH(KS_, M_)                                                       \
+  hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL, SIDE>), dim3(grid),            \
+                     dim3(SC_THREADS), 0, st, p)
   // the compiled step count follows score_ks(), which also sizes the units
   switch (ks) {
     case 4: LOOKME_SCORE_LAUNCH(4, false); break;
@@ -552,6 +554,11 @@ static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t 
 
 template <bool LOOKUP, int KL>
 static hipError_t launch_dt(int dt, int ks, int grid, const ScoreParams& p, hipStream_t st) {
+  if constexpr (LOOKUP) {
+    if (p.side0 > 0)
+      return dt == DT_BF16 ? launch_ks<DT_BF16, true, KL, true>(ks, grid, p, st)
+                           : launch_ks<DT_F32, true, KL, true>(ks, grid, p, st);
+  }
   return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL>(ks, grid, p, st)
                        : launch_ks<DT_F32, LOOKUP, KL>(ks, grid, p, st);
 }
