@@ -1,8 +1,8 @@
 // Criticality and the top-n_keep select of the sparse injection (arXiv
 // 2607.16305, Sec. 3.3, Eq. 9-10): the bodies shared by the stand-alone
-// kernels (inject.hip) and by the bucketing launch that carries the select
-// beside the bucketing of small batches (bucket.hip), so that both give the
-// same bits.
+// kernels (inject.hip) and by the launches that carry them beside the
+// bucketing and the Level-2 scoring of small batches (bucket.hip, score.hip),
+// so that all give the same bits.
 //
 //   row_sumsq    one wave streams a row of Delta once (NORM_UNROLL 16-byte
 //                loads of a lane in flight) and returns its fp32 sum of
@@ -76,15 +76,13 @@ constexpr int sel_cache_words(int cn) { return cn > 0 ? cn + cn / 32 : 1; }
 // The kept set of one layer: kept[0 .. n_keep) = the n_keep tokens of
 // largest key (ties: lowest token), ascending.  Called by all THREADS (a
 // multiple of 256) threads of a workgroup; cache: sel_cache_words(CN) words
-// of LDS.  COHERENT: the keys were written by other workgroups of the same
-// launch (read with device-scope loads; needs CN > 0, n <= CN).
-template <int CN, bool COHERENT, int THREADS = SEL_THREADS>
+// of LDS.
+template <int CN, int THREADS = SEL_THREADS>
 __device__ __forceinline__ void select_layer(const uint32_t* __restrict__ gkey, int64_t n,
                                              int64_t n_keep, int32_t* __restrict__ kept,
                                              uint32_t* cache) {
   constexpr bool CACHED = CN > 0;
   constexpr int WAVES = THREADS / WAVE;
-  static_assert(CACHED || !COHERENT, "coherent reads go through the LDS cache");
   static_assert(THREADS % 256 == 0, "a thread per radix bin");
   __shared__ int hist[256];
   __shared__ int wsum[WAVES];
@@ -93,13 +91,7 @@ __device__ __forceinline__ void select_layer(const uint32_t* __restrict__ gkey, 
   if (n_keep == 0) return;
   const int tid = threadIdx.x;
   if constexpr (CACHED) {
-    for (int i = tid; i < n; i += THREADS) {
-      if constexpr (COHERENT)
-        cache[i + (i >> 5)] = __hip_atomic_load(gkey + i, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-      else
-        cache[i + (i >> 5)] = gkey[i];
-    }
+    for (int i = tid; i < n; i += THREADS) cache[i + (i >> 5)] = gkey[i];
     __syncthreads();
   }
   auto key = [&](int64_t i) -> uint32_t {

@@ -41,7 +41,7 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
     int32_t* __restrict__ kept_all) {
   __shared__ uint32_t cache[sel_cache_words(CN)];
   const int layer = blockIdx.x;
-  select_layer<CN, false>(key_all + (int64_t)layer * n, n, n_keep,
+  select_layer<CN>(key_all + (int64_t)layer * n, n, n_keep,
                           kept_all + (int64_t)layer * n_keep, cache);
 }
 

@@ -470,7 +470,7 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
 template <int KS>
 __device__ __forceinline__ void side_select(const ScoreParams& a, char* smem) {
   const int layer = blockIdx.x - a.side0;
-  select_layer<SEL_SIDE_MAX_N, false, SC_THREADS>(a.crit_key + (int64_t)layer * a.crit_n,
+  select_layer<SEL_SIDE_MAX_N, SC_THREADS>(a.crit_key + (int64_t)layer * a.crit_n,
                                                   a.crit_n, a.n_keep,
                                                   a.kept + (int64_t)layer * a.n_keep,
                                                   reinterpret_cast<uint32_t*>(smem));
