@@ -260,7 +260,7 @@ class Bench:
         # the one stream (lookme_lookup_select); a second stream's waits would
         # cost more than the select itself
         self.one_stream = (not two_streams and L * n <= 1024 and not relevance and not scales
-                           and not gate and not netprop)
+                           and not netprop)
         if scales:
             from synth import make_multiscale
             self.ms = make_multiscale(wl, seed, scales, device="cuda")
@@ -293,6 +293,18 @@ class Bench:
         lk, wl, inp = self.lk, self.wl, self.inp
         h = self.tables[i % self.copies].handle
         L, n = wl.layers, wl.n_tokens
+        if self.one_stream and self.gate:
+            lk.lookme_route(h, L, n, wl.d_in, inp["x"], inp["wt"], self.q, self.scene,
+                            self.stream)
+            lk.lookme_lookup_gate(h, L, n, self.q, self.scene, self.prim, self.w, inp["delta"],
+                                  wl.crit_dim, self.w_g, self.kept, self.count, self.stream)
+            if self.fus is None:
+                lk.lookme_inject_gated(h, L, n, self.kept, self.count, self.scene, self.prim,
+                                       self.w, self.hidden, wl.d_h, self.stream)
+            else:
+                lk.lookme_inject_fused_gated(h, L, n, self.kept, self.count, self.scene,
+                                             self.prim, self.w, self.hidden, wl.d_h, self.stream)
+            return
         if self.one_stream:
             lk.lookme_route(h, L, n, wl.d_in, inp["x"], inp["wt"], self.q, self.scene,
                             self.stream)
@@ -755,7 +767,10 @@ def main():
                    "injection": (f"SwiGLU fusion, d_ff {args.fusion}" if args.fusion
                                  else "prefix add of the retrieved rows"),
                    "propagated_layers": args.netprop, "scales": args.scales,
-                   "select": ("norms in the bucketing launch, top-n_keep in the Level-2 launch (one stream)" if b.one_stream
+                   "select": (("gate logits in the bucketing launch, compaction in the Level-2 "
+                               "launch (one stream)" if args.gate else
+                               "norms in the bucketing launch, top-n_keep in the Level-2 launch "
+                               "(one stream)") if b.one_stream
                               else "second stream beside projection and routing"),
                    "kept_set": ("learned gate, " + "+".join(str(c) for c in b.count.tolist())
                                 + " open" if args.gate else f"top {wl.n_keep} by criticality")},

@@ -359,6 +359,25 @@ lookme_status_t lookme_gate(lookme_t h, int32_t layers, int64_t n, const void* d
                             int32_t* kept_out, int32_t* count_out, void* stream);
 
 /*
+ * lookme_lookup_gate -- lookme_lookup and lookme_gate (with pos = NULL,
+ * delta_rows = n) of the same batch in one call on one stream, as
+ * lookme_lookup_select is for the top-n_keep select: for batches of at most
+ * 1024 rows the gate's logits are computed by extra workgroups of the
+ * bucketing launch and, when n <= 4096, each layer's open rows are compacted
+ * by one extra workgroup of the Level-2 launch; otherwise the gate's kernels
+ * run after the bucketing.  The same bits as the two calls:
+ *   delta [layers, n, d_c], w_g [layers, d_c]; kept_out [layers, n] (open
+ *   token ids ascending, then -1), count_out [layers]; prim_out, w_out as
+ *   for lookme_lookup.
+ * Needs the workspace of lookme_workspace_size(layers, n); uses the part that
+ * lookme_select and lookme_gate use.
+ */
+lookme_status_t lookme_lookup_gate(lookme_t h, int32_t layers, int64_t n, const void* q,
+                                   const int32_t* scene, int32_t* prim_out, float* w_out,
+                                   const void* delta, int32_t d_c, const void* w_g,
+                                   int32_t* kept_out, int32_t* count_out, void* stream);
+
+/*
  * lookme_inject_gated -- lookme_inject_kept for the counted lists of
  * lookme_gate (Eq. 10 with the learned gate, prefix add of Eq. 2):
  *   kept  [layers, n] int32, layer l's open token ids in its first count[l]

@@ -250,18 +250,21 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_small_kernel(
                     unit_count, hist);
 }
 
-// The bucketing of a small batch with the criticality norms of the same rows
-// (Eq. 9; independent of it) in the launch: workgroup 0 buckets, the others
-// compute the norms of BK_WAVES * NORM_ROWS_PER_WAVE rows each with the body
-// of crit_norm_kernel (same bits).
+// The bucketing of a small batch with the per-row signal of the sparse
+// injection of the same rows (Eq. 9; independent of it) in the launch:
+// workgroup 0 buckets, the others compute for BK_WAVES * NORM_ROWS_PER_WAVE
+// rows each either the criticality norm (w_g null: the body of
+// crit_norm_kernel) or the learned gate's logit Delta_r . W_g of the row's
+// layer (n rows a layer: the body of gate_logit_kernel), the same bits.
 constexpr int NORM_ROWS_PER_WAVE = 2;
 
-template <int DT>
+template <int DT, bool GATE>
 __global__ __launch_bounds__(BK_THREADS) void bucket_norm_kernel(
     const int32_t* __restrict__ scene, int64_t rows, int S, int sbits, int shared_rows,
     int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ unit_scene,
     int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count,
-    const char* __restrict__ crit, int64_t row_bytes, uint32_t* __restrict__ key) {
+    const char* __restrict__ crit, int64_t row_bytes, uint32_t* __restrict__ key,
+    const char* __restrict__ w_g, int64_t n) {
   extern __shared__ int hist[];
   if (blockIdx.x == 0) {
     bucket_small_body(scene, rows, S, sbits, shared_rows, offsets, perm, unit_scene, unit_begin,
@@ -272,30 +275,37 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_norm_kernel(
   const int64_t nwg = gridDim.x - 1;
   const int chunks = (int)(row_bytes / 16);
   for (int64_t r = (int64_t)(blockIdx.x - 1) * BK_WAVES + wv; r < rows; r += nwg * BK_WAVES) {
-    const float acc = row_sumsq<DT>(crit + r * row_bytes, chunks, lane);
+    float acc;
+    if constexpr (GATE)
+      acc = row_dot<DT>(crit + r * row_bytes, w_g + (r / n) * row_bytes, chunks, lane);
+    else
+      acc = row_sumsq<DT>(crit + r * row_bytes, chunks, lane);
     if (lane == 0) key[r] = as_u32(acc);
   }
 }
 
 bool launch_bucket_norms(int dt, const int32_t* scene, int64_t rows, int S, int shared_rows,
                          const BucketWs& ws, const void* crit, int d_c, uint32_t* key,
-                         hipStream_t st) {
+                         hipStream_t st, const void* w_g, int64_t n) {
   if (rows == 0 || bucket_chunks(rows) != 1) return false;
   int sbits = 0;
   while ((1 << sbits) < S) ++sbits;
   const int per_wg = BK_WAVES * NORM_ROWS_PER_WAVE;
   const dim3 grid((unsigned)(1 + (rows + per_wg - 1) / per_wg));
   const int64_t rb = (int64_t)d_c * (dt == DT_BF16 ? 2 : 4);
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL(bucket_norm_kernel<DT_BF16>, grid, dim3(BK_THREADS),
-                       (size_t)S * sizeof(int), st, scene, rows, S, sbits, shared_rows,
-                       ws.offsets, ws.perm, ws.unit_scene, ws.unit_begin, ws.unit_count,
-                       static_cast<const char*>(crit), rb, key);
-  else
-    hipLaunchKernelGGL(bucket_norm_kernel<DT_F32>, grid, dim3(BK_THREADS),
-                       (size_t)S * sizeof(int), st, scene, rows, S, sbits, shared_rows,
-                       ws.offsets, ws.perm, ws.unit_scene, ws.unit_begin, ws.unit_count,
-                       static_cast<const char*>(crit), rb, key);
+#define LOOKME_BUCKET_NORM(DT_, G_)                                                         \
+  hipLaunchKernelGGL((bucket_norm_kernel<DT_, G_>), grid, dim3(BK_THREADS),                  \
+                     (size_t)S * sizeof(int), st, scene, rows, S, sbits, shared_rows,          \
+                     ws.offsets, ws.perm, ws.unit_scene, ws.unit_begin, ws.unit_count,         \
+                     static_cast<const char*>(crit), rb, key, static_cast<const char*>(w_g), n)
+  if (dt == DT_BF16) {
+    if (w_g != nullptr) LOOKME_BUCKET_NORM(DT_BF16, true);
+    else LOOKME_BUCKET_NORM(DT_BF16, false);
+  } else {
+    if (w_g != nullptr) LOOKME_BUCKET_NORM(DT_F32, true);
+    else LOOKME_BUCKET_NORM(DT_F32, false);
+  }
+#undef LOOKME_BUCKET_NORM
   return true;
 }
 

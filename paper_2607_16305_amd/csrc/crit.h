@@ -1,5 +1,5 @@
-// Criticality and the top-n_keep select of the sparse injection (arXiv
-// 2607.16305, Sec. 3.3, Eq. 9-10): the bodies shared by the stand-alone
+// Criticality, the top-n_keep select and the learned gate of the sparse
+// injection (arXiv 2607.16305, Sec. 3.3, Eq. 9-10): the bodies shared by the stand-alone
 // kernels (inject.hip) and by the launches that carry them beside the
 // bucketing and the Level-2 scoring of small batches (bucket.hip, score.hip),
 // so that all give the same bits.
@@ -9,10 +9,12 @@
 //                squares, accumulated in a fixed order; stored as its bit
 //                pattern, it orders like the norm (non-negative floats order
 //                like their bits, and the square root keeps the order);
-//   select_layer one workgroup (1024 or 256 threads): 4-pass MSB-first radix select of
-//                the n_keep-th largest key (keys cached in LDS when they
-//                fit), then an order-preserving compaction (block prefix
-//                sums) of the kept token ids.
+//   select_layer one workgroup (1024 or 256 threads): 4-pass MSB-first radix
+//                select of the n_keep-th largest key (keys cached in LDS when
+//                they fit), then an order-preserving compaction (block prefix
+//                sums) of the kept token ids;
+//   row_dot, gate_compact_layer  the learned SKA gate's logit z = Delta_i W_g
+//                and the ascending compaction of its open rows (Eq. 9).
 #pragma once
 
 #include "common.h"
@@ -68,6 +70,84 @@ __device__ __forceinline__ float row_sumsq(const char* __restrict__ p, int chunk
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d, 64);
   return acc;
+}
+
+// z = row . w (the SKA gate's logit of Eq. 9) by one wave: NORM_UNROLL 16-byte
+// loads of the row and of w in flight per lane, fp32 fused multiply-adds in a
+// fixed order, then the wave sum.
+template <int DT>
+__device__ __forceinline__ float row_dot(const char* __restrict__ p, const char* __restrict__ w,
+                                         int chunks, int lane) {
+  float acc = 0.f;
+  for (int c0 = lane; c0 < chunks; c0 += NORM_UNROLL * WAVE) {
+    u32x4_t dv[NORM_UNROLL], wv[NORM_UNROLL];
+#pragma unroll
+    for (int u = 0; u < NORM_UNROLL; ++u) {
+      const int c = c0 + u * WAVE;
+      const int cc = c < chunks ? c : chunks - 1;
+      dv[u] = ld16_nt(p + (int64_t)cc * 16);
+      wv[u] = ld16(w + (int64_t)cc * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < NORM_UNROLL; ++u) {
+      if (c0 + u * WAVE >= chunks) continue;
+      if constexpr (DT == DT_BF16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc = fmaf(bf16lo(dv[u][e]), bf16lo(wv[u][e]), acc);
+          acc = fmaf(bf16hi(dv[u][e]), bf16hi(wv[u][e]), acc);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = fmaf(as_f32(dv[u][e]), as_f32(wv[u][e]), acc);
+      }
+    }
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d, 64);
+  return acc;
+}
+
+// The open gates of one layer in ascending order (Eq. 9-10: z > 0; z = 0
+// stays closed): every thread owns GATE_PER_THREAD consecutive rows (their
+// signs packed in one register), a block prefix sum of the per-thread counts
+// places each open row; kept[count ..  n) = -1 and *count = the number open.
+// Called by all THREADS threads of a workgroup.
+constexpr int GATE_PER_THREAD = 32;
+
+template <int THREADS>
+__device__ __forceinline__ void gate_compact_layer(const float* __restrict__ z, int64_t n,
+                                                   int32_t* __restrict__ kept,
+                                                   int32_t* __restrict__ count) {
+  constexpr int SPAN = THREADS * GATE_PER_THREAD;   // rows a round
+  __shared__ int wsum[THREADS / WAVE];
+  __shared__ int s_total;
+  const int tid = threadIdx.x;
+  int64_t base = 0;   // open rows in earlier rounds
+  for (int64_t r0 = 0; r0 < n; r0 += SPAN) {
+    const int64_t i0 = r0 + (int64_t)tid * GATE_PER_THREAD;
+    uint32_t open = 0;
+#pragma unroll
+    for (int b = 0; b < GATE_PER_THREAD; ++b) {
+      const int64_t i = i0 + b;
+      const float v = z[i < n ? i : n - 1];   // every load issued, none under a branch
+      if (i < n && v > 0.f) open |= 1u << b;
+    }
+    const int c = __popc(open);
+    const int incl = block_scan_incl<THREADS / WAVE>(c, wsum);
+    if (tid == THREADS - 1) s_total = incl;
+    int64_t slot = base + incl - c;
+    while (open != 0) {
+      const int b = __ffs(open) - 1;
+      open &= open - 1;
+      kept[slot++] = (int32_t)(i0 + b);
+    }
+    __syncthreads();
+    base += s_total;
+    __syncthreads();   // s_total is rewritten by the next round
+  }
+  for (int64_t i = base + tid; i < n; i += THREADS) kept[i] = -1;
+  if (tid == 0) *count = (int32_t)base;
 }
 
 // LDS words of select_layer's key cache for CN keys.

@@ -92,13 +92,15 @@ int64_t bucket_chunks(int64_t rows);
 int64_t bucket_max_units(int64_t rows, int S);
 hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, int shared_rows,
                          const BucketWs& ws, hipStream_t st);
-// launch_bucket for a batch of at most one chunk with the criticality norms
-// of Eq. 9 (crit [rows, d_c] -> key [rows], the bits of launch_crit_norm)
-// computed by extra workgroups of the same launch; false (nothing launched)
-// when the batch is larger.
+// launch_bucket for a batch of at most one chunk with the per-row signal of
+// the sparse injection computed by extra workgroups of the same launch: the
+// criticality norms of Eq. 9 (w_g null: crit [rows, d_c] -> key [rows], the
+// bits of launch_crit_norm) or the learned gate's logits (w_g [rows / n, d_c]
+// per layer of n rows -> key as float z, the bits of launch_gate's); false
+// (nothing launched) when the batch is larger.
 bool launch_bucket_norms(int dt, const int32_t* scene, int64_t rows, int S, int shared_rows,
                          const BucketWs& ws, const void* crit, int d_c, uint32_t* key,
-                         hipStream_t st);
+                         hipStream_t st, const void* w_g = nullptr, int64_t n = 0);
 
 // ---- Level-2 in the paper's form (Eq. 6-7): relevance MLP ----------------
 // The MLP's tensors are borrowed from the caller: w1 [hidden, 2 d_e] and
@@ -167,13 +169,16 @@ hipError_t launch_multiscale(int dt, int scales, int64_t n, int64_t n_keep, cons
 // The sparse-injection select (Eq. 9-10) of the same batch carried by the
 // Level-2 launch: one extra workgroup per layer selects that layer's kept set
 // [n_keep] (kept + l * n_keep) from its criticality keys (key + l * n, from
-// an earlier launch).  Needs n <= SEL_SIDE_MAX_N.
+// an earlier launch); or, with `count` set, compacts the open rows of the
+// learned gate from its logits (key + l * n as float) into kept + l * n
+// (ascending, -1 tail) and count[l].  Needs n <= SEL_SIDE_MAX_N.
 constexpr int SEL_SIDE_MAX_N = 4096;
 struct SideSelect {
   int layers;
   int64_t n, n_keep;
   const uint32_t* key;
   int32_t* kept;
+  int32_t* count = nullptr;
 };
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st,

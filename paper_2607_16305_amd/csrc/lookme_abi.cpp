@@ -243,12 +243,16 @@ lookme_status_t check_lookup_out(const void* q, const int32_t* scene, int32_t* p
   return check_ptr(w_out, "w_out");
 }
 
-// The sparse-injection select carried by a lookup (lookme_lookup_select).
+// The sparse-injection select carried by a lookup: the top n_keep by
+// criticality (lookme_lookup_select), or the learned gate when w_g is set
+// (lookme_lookup_gate: kept [layers, n] and count [layers]).
 struct SelectArgs {
   const void* crit;
   int32_t d_c;
   int64_t n_keep;
   int32_t* kept;
+  const void* w_g = nullptr;
+  int32_t* count = nullptr;
 };
 
 // bucketing and Level-2 scoring, with the select of `sel` carried along:
@@ -272,32 +276,39 @@ lookme_status_t run_lookup(lookme_t h, const Layout& L, int32_t layers, int64_t 
   b.chunks = lookme::bucket_chunks(rows);
   b.max_units = lookme::bucket_max_units(rows, d.num_scenes);
   uint32_t* key = reinterpret_cast<uint32_t*>(ws + L.crit_key);
-  const bool select = sel != nullptr && sel->n_keep > 0;
+  const bool gate = sel != nullptr && sel->w_g != nullptr;
+  const bool select = sel != nullptr && (sel->n_keep > 0 || gate);
+  bool normed = false;
   {
     Timed tm(h, LOOKME_GROUP_BUCKET, st);
     const int shared_rows =
         lookme::shared_unit_rows((int64_t)d.key_dim * elem_size(d.dtype), d.top_k);
-    bool normed = false;
     if (select)
       normed = lookme::launch_bucket_norms(d.dtype, scene, rows, d.num_scenes, shared_rows, b,
-                                           sel->crit, sel->d_c, key, st);
+                                           sel->crit, sel->d_c, key, st,
+                                           gate ? sel->w_g : nullptr, n);
     if (normed) {
       LOOKME_TRY(hip_status(hipGetLastError(), "bucketing + norms launch"));
     } else {
       LOOKME_TRY(hip_status(lookme::launch_bucket(scene, rows, d.num_scenes, shared_rows, b, st),
                             "bucketing launch"));
-      if (select)
-        LOOKME_TRY(hip_status(lookme::launch_crit_norm(d.dtype, rows, sel->crit, sel->d_c, key,
-                                                       st),
-                              "criticality launch"));
     }
   }
-  const bool ride = select && n <= lookme::SEL_SIDE_MAX_N;
-  if (select && !ride)
-    LOOKME_TRY(hip_status(lookme::launch_crit_select(layers, n, sel->n_keep, key, sel->kept, st),
-                          "select launch"));
-  const lookme::SideSelect side{layers, n, select ? sel->n_keep : 0, key,
-                                select ? sel->kept : nullptr};
+  const bool ride = select && normed && n <= lookme::SEL_SIDE_MAX_N;
+  if (select && !ride) {
+    // the select's (or gate's) own kernels, after the bucketing
+    if (gate)
+      LOOKME_TRY(hip_status(lookme::launch_gate(d.dtype, layers, n, sel->crit, n, sel->d_c,
+                                                nullptr, sel->w_g,
+                                                reinterpret_cast<float*>(key), sel->kept,
+                                                sel->count, st),
+                            "gate launch"));
+    else
+      LOOKME_TRY(run_select(h, L, layers, n, sel->n_keep, sel->crit, sel->d_c, sel->kept, st));
+  }
+  lookme::SideSelect side{layers, n, select ? sel->n_keep : 0, key,
+                          select ? sel->kept : nullptr};
+  if (gate) side.count = sel->count;
   Timed tm(h, LOOKME_GROUP_SCORE, st);
   return hip_status(lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
                                           d.prims_per_scene, d.top_k, prim_out, w_out, st,
@@ -505,6 +516,28 @@ lookme_status_t lookme_lookup_select(lookme_t h, int32_t layers, int64_t n, cons
   LOOKME_TRY(check_workspace(h, layers, n, &L));
   const SelectArgs sel{crit, d_c, n_keep, kept_out};
   return run_lookup(h, L, layers, n, q, scene, prim_out, w_out, n_keep > 0 ? &sel : nullptr,
+                    static_cast<hipStream_t>(stream));
+}
+
+lookme_status_t lookme_lookup_gate(lookme_t h, int32_t layers, int64_t n, const void* q,
+                                   const int32_t* scene, int32_t* prim_out, float* w_out,
+                                   const void* delta, int32_t d_c, const void* w_g,
+                                   int32_t* kept_out, int32_t* count_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_crit_dim(h->d, d_c));
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_lookup_out(q, scene, prim_out, w_out));
+  LOOKME_TRY(check_ptr(delta, "delta"));
+  LOOKME_TRY(check_ptr(w_g, "w_g"));
+  LOOKME_TRY(check_ptr(kept_out, "kept_out"));
+  LOOKME_TRY(check_ptr(count_out, "count_out"));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, layers, n, &L));
+  SelectArgs sel{delta, d_c, 0, kept_out};
+  sel.w_g = w_g;
+  sel.count = count_out;
+  return run_lookup(h, L, layers, n, q, scene, prim_out, w_out, &sel,
                     static_cast<hipStream_t>(stream));
 }
 

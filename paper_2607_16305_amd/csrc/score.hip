@@ -60,8 +60,9 @@ struct ScoreParams {
   // slot side0 + l selects layer l's kept set
   int side0;
   int64_t crit_n, n_keep;
-  const uint32_t* crit_key; // [layers * crit_n] criticality keys
-  int32_t* kept;            // [layers, n_keep]
+  const uint32_t* crit_key; // [layers * crit_n] criticality keys (gate: logits)
+  int32_t* kept;            // [layers, n_keep] (gate: [layers, crit_n])
+  int32_t* gate_count;      // null: top-n_keep select; else the gate's counts [layers]
 };
 
 template <int KS, bool MASKED>
@@ -466,10 +467,18 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
 // The select of the batch carried by a Level-2 launch (Eq. 9-10): slot
 // side0 + l selects layer l's kept set from its criticality keys (computed
 // by an earlier launch), with the keys cached in `smem`: the body of
-// crit_select_kernel on the launch's 256 threads, so the bits are its.
+// crit_select_kernel on the launch's 256 threads, so the bits are its; or
+// compacts layer l's open gates from their logits (gate_compact_kernel's
+// body).
 template <int KS>
 __device__ __forceinline__ void side_select(const ScoreParams& a, char* smem) {
   const int layer = blockIdx.x - a.side0;
+  if (a.gate_count != nullptr) {
+    gate_compact_layer<SC_THREADS>(
+        reinterpret_cast<const float*>(a.crit_key) + (int64_t)layer * a.crit_n, a.crit_n,
+        a.kept + (int64_t)layer * a.crit_n, a.gate_count + layer);
+    return;
+  }
   select_layer<SEL_SIDE_MAX_N, SC_THREADS>(a.crit_key + (int64_t)layer * a.crit_n,
                                                   a.crit_n, a.n_keep,
                                                   a.kept + (int64_t)layer * a.n_keep,
@@ -664,12 +673,13 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
   p.out_idx = prim;
   p.out_w = w;
   int grid = (int)((ws.max_units + 15) / 16 * 16);   // whole pairs on every XCD
-  if (side != nullptr && side->n_keep > 0 && side->n > 0) {
+  if (side != nullptr && (side->n_keep > 0 || side->count != nullptr) && side->n > 0) {
     p.side0 = grid;
     p.crit_n = side->n;
     p.n_keep = side->n_keep;
     p.crit_key = side->key;
     p.kept = side->kept;
+    p.gate_count = side->count;
     grid += side->layers;
   }
   if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st);

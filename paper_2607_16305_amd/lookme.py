@@ -31,7 +31,8 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_inject_fused", "lookme_set_propagation", "lookme_inject_propagated",
             "lookme_set_multiscale", "lookme_inject_multiscale", "lookme_gate",
             "lookme_inject_gated", "lookme_inject_fused_gated", "lookme_inject_propagated_gated",
-            "lookme_inject_text", "lookme_lookup_select", "lookme_destroy", "lookme_last_error",
+            "lookme_inject_text", "lookme_lookup_select", "lookme_lookup_gate",
+            "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read")
 
 GROUPS = ("project", "route", "bucket", "score", "norm", "select", "inject")
@@ -103,6 +104,8 @@ def load():
                                ctypes.c_int32, _vp],
         "lookme_lookup_select": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp,
                                  ctypes.c_int64, _vp, ctypes.c_int32, _vp, _vp],
+        "lookme_lookup_gate": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
+                               ctypes.c_int32, _vp, _vp, _vp, _vp],
         "lookme_destroy": [_vp],
         "lookme_profile_enable": [_vp, ctypes.c_int32],
         "lookme_profile_read": [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
@@ -232,6 +235,13 @@ def lookme_lookup_select(h, layers, n, q, scene, prim_out, w_out, n_keep, crit, 
                                        _stream(stream)))
 
 
+def lookme_lookup_gate(h, layers, n, q, scene, prim_out, w_out, delta, d_c, w_g, kept_out,
+                       count_out, stream=None):
+    _check(load().lookme_lookup_gate(h, layers, n, _ptr(q), _ptr(scene), _ptr(prim_out),
+                                     _ptr(w_out), _ptr(delta), d_c, _ptr(w_g), _ptr(kept_out),
+                                     _ptr(count_out), _stream(stream)))
+
+
 def lookme_gate(h, layers, n, delta, delta_rows, d_c, pos, w_g, kept_out, count_out,
                 stream=None):
     _check(load().lookme_gate(h, layers, n, _ptr(delta), delta_rows, d_c, _ptr(pos), _ptr(w_g),
@@ -337,6 +347,13 @@ class Table:
         self.reserve(layers, n)
         lookme_lookup_select(self.handle, layers, n, q, scene, prim_out, w_out, n_keep, crit,
                              crit.shape[-1], kept_out, stream)
+
+    def lookup_gate(self, q, scene, prim_out, w_out, delta, w_g, kept_out, count_out, layers=1,
+                    stream=None):
+        n = scene.numel() // layers
+        self.reserve(layers, n)
+        lookme_lookup_gate(self.handle, layers, n, q, scene, prim_out, w_out, delta,
+                           delta.shape[-1], w_g, kept_out, count_out, stream)
 
     def select(self, crit, kept_out, n_keep, layers=1, stream=None):
         n = crit.numel() // (layers * crit.shape[-1])

@@ -351,3 +351,21 @@ def test_lookup_select_validates(lib):
         assert S(lambda: call(n=0, n_keep=0, p=None, crit=None, kept=None)) == lk.LOOKME_OK
     finally:
         lk.lookme_destroy(h)
+
+
+def test_lookup_gate_validates(lib):
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        call = lambda n=8, d_c=2048, p=FAKE, wg=FAKE, cnt=FAKE: lk.lookme_lookup_gate(
+            h, 1, n, p, p, p, p, p, d_c, wg, p, cnt, 0)
+        assert S(lambda: call(d_c=1001)) == lk.LOOKME_ERR_UNSUPPORTED
+        assert S(lambda: call(wg=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(cnt=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call(p=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: call()) == lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: call(n=0, p=None, wg=None, cnt=None)) == lk.LOOKME_OK
+    finally:
+        lk.lookme_destroy(h)

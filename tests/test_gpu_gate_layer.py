@@ -247,3 +247,53 @@ def test_lookme_layer(name):
     assert rep.ok, str(rep)
     opened = rep.notes["layer_open"]
     assert all(o > 0 for o in opened), opened
+
+
+@pytest.mark.parametrize("name", ["gp_bf16_l2", "gp_f32_l3", "one_token", "image", "many"])
+def test_lookup_gate_one_launch(name):
+    """lookme_lookup_gate (the gate's logits in the bucketing launch and its
+    compaction in the Level-2 launch for batches of at most 1024 rows, its own
+    kernels after the bucketing otherwise): the same bits as lookme_lookup +
+    lookme_gate, the gate against the oracle, and again on a second call."""
+    from tests.harness import f64, to_np
+    cases = {
+        "gp_bf16_l2": Workload("gp", "bf16", 300, 2, 768, 512, 20, 200, 392, 520, 8, 33,
+                               usage="uniform"),
+        "gp_f32_l3": Workload("gp32", "f32", 77, 3, 96, 256, 5, 37, 36, 40, 3, 40),
+        "one_token": Workload("one", "bf16", 1, 1, 64, 64, 9, 24, 16, 16, 4, 100),
+        "image": WORKLOADS[1],
+        "many": Workload("many", "bf16", 40000, 1, 64, 64, 8, 16, 16, 16, 2, 10),
+    }
+    wl = cases[name]
+    _announce(f"lookup_gate {name}")
+    from paper_2607_16305_amd import lookme as lk
+    inp = make_inputs(wl, seed=21, device=DEV)
+    w_g = make_gate(wl, 21, device=DEV)
+    L, n, k = wl.layers, wl.n_tokens, wl.top_k
+    t = lk.Table(inp["scene_keys"], inp["prim_keys"], inp["values"], k)
+    q = torch.empty((L, n, wl.d_e), dtype=inp["x"].dtype, device=DEV)
+    scene = torch.empty((L, n), dtype=torch.int32, device=DEV)
+    t.route(inp["x"], inp["wt"], q, scene, layers=L)
+    outs = []
+    for mode in ("two_calls", "one", "one_again"):
+        prim = torch.full((L, n, k), -7, dtype=torch.int32, device=DEV)
+        w = torch.full((L, n, k), -7.0, dtype=torch.float32, device=DEV)
+        kept = torch.full((L, n), -7, dtype=torch.int32, device=DEV)
+        count = torch.full((L,), -7, dtype=torch.int32, device=DEV)
+        if mode == "two_calls":
+            t.lookup(q, scene, prim, w, layers=L)
+            t.gate(inp["delta"], w_g, kept, count, layers=L)
+        else:
+            t.lookup_gate(q, scene, prim, w, inp["delta"], w_g, kept, count, layers=L)
+        torch.cuda.synchronize()
+        outs.append((prim, w, kept, count))
+    for o in outs[1:]:
+        for a, b, key in zip(outs[0], o, ("prim", "w", "kept", "count")):
+            assert torch.equal(a, b), key
+    rep = C.Report()
+    cnt, kk = to_np(outs[1][3]), to_np(outs[1][2])
+    for l in range(L):
+        c = int(cnt[l])
+        assert np.all(kk[l, c:] == -1)
+        C.check_gate(f64(inp["delta"][l]), f64(w_g[l]), kk[l, :c], rep)
+    assert rep.finish().ok, str(rep)
