@@ -458,9 +458,10 @@ class LayerBench:
     positions: the cross-modal pathway routes and looks up every position's
     L_dec(H_in) row in its own table (the paper's N_s = 512 scenes of
     N_p = 256 primitives, top-8), the image pathway the image block's
-    embeddings in the workload's table; the three learned gates run on a
-    second stream meanwhile (they read only Delta), then the text, image and
-    cross-modal injections are added in that order."""
+    embeddings in the workload's table, each with its learned gate carried
+    by the lookup's launches (lookme_lookup_gate); the text gate runs on its
+    own; then the text, image and cross-modal injections are added in that
+    order.  One stream."""
 
     TEXT_BEFORE, TEXT_AFTER, VOCAB = 64, 192, 151936
     CROSS_SCENES, CROSS_PRIMS, CROSS_K = 512, 256, 8
@@ -492,33 +493,27 @@ class LayerBench:
         self.count = torch.zeros((3, 4), dtype=torch.int32, device=dev)   # a 16-byte row each
         self.hidden = lay["h_dec"].clone()
         self.main = torch.cuda.current_stream()
-        self.side = torch.cuda.Stream()
-        self.ev_start, self.ev_gates = torch.cuda.Event(), torch.cuda.Event()
         self.handles = [self.img.handle, self.cross.handle]
         torch.cuda.synchronize()
 
     def step(self, i):
         lk, wl, lay = self.lk, self.wl, self.lay
         img, cr, tx = lay["image"], lay["cross"], lay["text"]
-        st, side = self.main.cuda_stream, self.side.cuda_stream
+        st = self.main.cuda_stream
         hi, hc = self.img.handle, self.cross.handle
         s0, s1 = self.start, self.start + self.n_img
         ct, ci, cc = self.count[0, :1], self.count[1, :1], self.count[2, :1]
         d_c = lay["delta"].shape[1]
-        self.ev_start.record(self.main)
-        self.side.wait_event(self.ev_start)
-        lk.lookme_gate(hi, 1, self.n_text, lay["delta"], self.n_seq, d_c, tx["pos"],
-                       lay["w_g"][0], self.k_t, ct, side)
-        lk.lookme_gate(hi, 1, self.n_img, lay["delta"][s0:s1], self.n_img, d_c, None,
-                       lay["w_g"][1], self.k_i, ci, side)
-        lk.lookme_gate(hc, 1, self.n_seq, lay["delta"], self.n_seq, d_c, None, lay["w_g"][2],
-                       self.k_c, cc, side)
-        self.ev_gates.record(self.side)
+        # one stream: the image and cross-modal gates ride in their lookups'
+        # launches, the text gate is its own pair of launches
         lk.lookme_route(hc, 1, self.n_seq, wl.d_h, lay["h_dec"], cr["wt"], self.q_c, self.sc_c, st)
-        lk.lookme_lookup(hc, 1, self.n_seq, self.q_c, self.sc_c, self.pr_c, self.w_c, st)
+        lk.lookme_lookup_gate(hc, 1, self.n_seq, self.q_c, self.sc_c, self.pr_c, self.w_c,
+                              lay["delta"], d_c, lay["w_g"][2], self.k_c, cc, st)
         lk.lookme_route(hi, 1, self.n_img, wl.d_in, img["x"], img["wt"], self.q_i, self.sc_i, st)
-        lk.lookme_lookup(hi, 1, self.n_img, self.q_i, self.sc_i, self.pr_i, self.w_i, st)
-        self.main.wait_event(self.ev_gates)
+        lk.lookme_lookup_gate(hi, 1, self.n_img, self.q_i, self.sc_i, self.pr_i, self.w_i,
+                              lay["delta"][s0:s1], d_c, lay["w_g"][1], self.k_i, ci, st)
+        lk.lookme_gate(hi, 1, self.n_text, lay["delta"], self.n_seq, d_c, tx["pos"],
+                       lay["w_g"][0], self.k_t, ct, st)
         lk.lookme_inject_text(lk.DTYPE_CODE[tx["table"].dtype], tx["table"], tx["vocab"],
                               tx["d_t"], self.n_text, tx["pos"], tx["ids"], self.k_t, ct,
                               self.hidden, self.n_seq, wl.d_h, st)
