@@ -144,7 +144,8 @@ lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void*
  *   prim_out, w_out as for lookme_lookup; kept_out [layers, n_keep] int32
  *   ascending (unused when n_keep = 0); crit [layers, n, d_c].
  * Requires what both calls require; needs the workspace of
- * lookme_workspace_size(layers, n).
+ * lookme_workspace_size(layers, n) and uses the part that lookme_select uses
+ * (the two must not run concurrently on one handle).
  */
 lookme_status_t lookme_lookup_select(lookme_t h, int32_t layers, int64_t n, const void* q,
                                      const int32_t* scene, int32_t* prim_out, float* w_out,
