@@ -75,6 +75,10 @@ SMALL = {
     # more tokens per layer than the select kernel caches in LDS
     "bf16_many_tokens": Workload("bf16_many_tokens", "bf16", 40000, 1, 64, 64, 8, 16, 16, 16, 2,
                                  10, usage="iid"),
+    # the largest scene count the bucketing holds (one LDS histogram entry a
+    # scene), with a ragged key width
+    "bf16_max_scenes": Workload("bf16_max_scenes", "bf16", 3000, 1, 96, 96, 16384, 4, 32, 48,
+                                2, 20, usage="uniform"),
     # same size, K not in whole 128-byte steps: the register-staged kernel
     "f32_ragged_k_proj_l4": Workload("f32_ragged_k_proj_l4", "f32", 2100, 4, 48, 512, 5, 24, 32,
                                      32, 3, 30, usage="iid"),
@@ -207,14 +211,17 @@ def test_select_on_second_stream_then_inject_kept(name):
 
 
 @pytest.mark.parametrize("name", ["bf16_ragged_l2", "f32_proj_l3", "bf16_one_token",
-                                  "bf16_k32_shared", "bf16_many_tokens", "image"])
+                                  "bf16_k32_shared", "bf16_many_tokens", "image",
+                                  "max_scenes_small"])
 def test_lookup_select_one_launch(name):
     """lookme_lookup_select (the select riding in the bucketing launch for
     batches of at most 1024 rows, after it otherwise): the oracle's results,
     the same bits as lookme_lookup + lookme_select, and again on a second
     call (the arrival counters were left at zero)."""
     from tests.harness import Run, check_run, run_fused_select
-    wl = WORKLOADS[1] if name == "image" else SMALL[name]
+    wl = (WORKLOADS[1] if name == "image" else
+          SMALL["bf16_max_scenes"].scaled(n_tokens=1000) if name == "max_scenes_small" else
+          SMALL[name])
     _announce(f"lookup_select {name}")
     inp = make_inputs(wl, seed=32, device=DEV)
     ref = Run(inp).run()
