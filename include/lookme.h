@@ -68,9 +68,11 @@ typedef struct {
                                value_dim * elem_size must be a multiple of 16 bytes  */
   int32_t top_k;            /* T~ (Eq. 6): 1 <= top_k <= min(N_p, LOOKME_KMAX)       */
   int32_t dtype;            /* lookme_dtype_t of keys, values, queries, hidden       */
-  int32_t score;            /* lookme_score_t; this build implements DOT (the dot
-                               score of the configured workloads); COS (the cosine
-                               of Eq. 5 and Eq. 7) returns LOOKME_ERR_UNSUPPORTED    */
+  int32_t score;            /* lookme_score_t: DOT, the dot product of the configured
+                               workloads, or COS, the cosine of Eq. 5 and Eq. 7
+                               (q.k / (||q|| ||k||), 0 for a zero vector), used by
+                               routing (plus the bias) and by the key-scored
+                               Level-2, whose softmax then runs over the k cosines */
 } lookme_desc_t;
 
 /*
@@ -138,9 +140,9 @@ lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void*
  * rows (layers * n) the criticality norms of Eq. 9 are computed by extra
  * workgroups of the bucketing launch, and when n <= 4096 each layer's top
  * n_keep select (Eq. 10) runs as one extra workgroup of the Level-2 launch,
- * beside the scoring units; what does not fit runs as its own kernels after
- * the bucketing.  The results are the same bits as lookme_lookup followed by
- * lookme_select:
+ * beside the scoring units; what does not fit (and any batch of a handle
+ * with COS scores) runs as its own kernels after the bucketing.  The results
+ * are the same bits as lookme_lookup followed by lookme_select:
  *   prim_out, w_out as for lookme_lookup; kept_out [layers, n_keep] int32
  *   ascending (unused when n_keep = 0); crit [layers, n, d_c].
  * Requires what both calls require; needs the workspace of

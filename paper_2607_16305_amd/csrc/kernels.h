@@ -42,10 +42,11 @@ struct RoutePlan {
   int per_split;          // DTL: 256-key tiles; STREAM: keys (a multiple of 64)
   int64_t part_entries;
 };
-RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes);
+// cos: cosine scores, which only the scoring kernel's modes implement
+RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes, bool cos = false);
 hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
                         int32_t* scene, int64_t rows, int d_e, int S, uint64_t* part,
-                        int32_t* count, hipStream_t st);
+                        int32_t* count, hipStream_t st, bool cos = false);
 hipError_t launch_route_dtl(int dt, const void* q, const void* scene_keys, const float* bias,
                             int32_t* scene, int64_t rows, int d_e, int S, const RoutePlan& plan,
                             uint64_t* part, int32_t* count, hipStream_t st);
@@ -182,7 +183,7 @@ struct SideSelect {
 };
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st,
-                         const SideSelect* side = nullptr);
+                         const SideSelect* side = nullptr, bool cos = false);
 
 // ---- criticality, select and injection ------------------------------------
 hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uint32_t* key,

@@ -95,7 +95,8 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance,
   L.unit_count = take(256);   // counters first: the region zeroed at set-up
   L.route_count = take((size_t)lookme::ROUTE_COUNTERS * 4);
   const lookme::RoutePlan plan =
-      lookme::route_plan(rows, d.num_scenes, (int64_t)d.key_dim * elem_size(d.dtype));
+      lookme::route_plan(rows, d.num_scenes, (int64_t)d.key_dim * elem_size(d.dtype),
+                         d.score == LOOKME_SCORE_COS);
   L.route_part = take((size_t)plan.part_entries * 8);
   L.chunk_hist = take((size_t)chunks * d.num_scenes * 4);
   L.local_rank = take((size_t)rows * 4);
@@ -278,12 +279,14 @@ lookme_status_t run_lookup(lookme_t h, const Layout& L, int32_t layers, int64_t 
   uint32_t* key = reinterpret_cast<uint32_t*>(ws + L.crit_key);
   const bool gate = sel != nullptr && sel->w_g != nullptr;
   const bool select = sel != nullptr && (sel->n_keep > 0 || gate);
+  // the Level-2 kernels that carry a select score dot products only
+  const bool cos = d.score == LOOKME_SCORE_COS;
   bool normed = false;
   {
     Timed tm(h, LOOKME_GROUP_BUCKET, st);
     const int shared_rows =
         lookme::shared_unit_rows((int64_t)d.key_dim * elem_size(d.dtype), d.top_k);
-    if (select)
+    if (select && !cos)
       normed = lookme::launch_bucket_norms(d.dtype, scene, rows, d.num_scenes, shared_rows, b,
                                            sel->crit, sel->d_c, key, st,
                                            gate ? sel->w_g : nullptr, n);
@@ -312,7 +315,7 @@ lookme_status_t run_lookup(lookme_t h, const Layout& L, int32_t layers, int64_t 
   Timed tm(h, LOOKME_GROUP_SCORE, st);
   return hip_status(lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
                                           d.prims_per_scene, d.top_k, prim_out, w_out, st,
-                                          ride ? &side : nullptr),
+                                          ride ? &side : nullptr, cos),
                     "lookup launch");
 }
 
@@ -352,8 +355,6 @@ lookme_status_t lookme_create(const lookme_desc_t* desc, const void* scene_keys,
     return fail(LOOKME_ERR_UNSUPPORTED, "num_scenes %d above %d", d.num_scenes, MAX_SCENES);
   if ((int64_t)d.num_scenes * d.prims_per_scene > (int64_t)INT32_MAX)
     return fail(LOOKME_ERR_UNSUPPORTED, "num_scenes * prims_per_scene exceeds 2^31 - 1 rows");
-  if (d.score == LOOKME_SCORE_COS)
-    return fail(LOOKME_ERR_UNSUPPORTED, "cosine scoring is not implemented in this build");
   LOOKME_TRY(check_ptr(scene_keys, "scene_keys"));
   LOOKME_TRY(check_ptr(prim_keys, "prim_keys"));
   LOOKME_TRY(check_ptr(values, "values"));
@@ -481,7 +482,8 @@ lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in
   return hip_status(
       lookme::launch_route(d.dtype, q_out, h->scene_keys, h->bias, scene_out, rows, d.key_dim,
                            d.num_scenes, reinterpret_cast<uint64_t*>(ws + L.route_part),
-                           reinterpret_cast<int32_t*>(ws + L.route_count), st),
+                           reinterpret_cast<int32_t*>(ws + L.route_count), st,
+                           d.score == LOOKME_SCORE_COS),
       "routing launch");
 }
 

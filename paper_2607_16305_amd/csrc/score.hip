@@ -22,6 +22,12 @@
 //    one 16-row query tile (two for routing); the key stream is paid once for
 //    up to 4 (8) tiles.  Lists are merged inside the wave (4 lanes per row).
 //    Suits large buckets and routing of many rows.
+//
+// COS (the cosine of Eq. 5 and Eq. 7 instead of the dot product): each
+// score is scaled by 1/||q|| 1/||k||, both norms taken from the fragments the
+// matrix cores already read (a query row's once per unit, a key's once per
+// 16-key block, over the 4 lane groups that hold its chunks); a zero vector
+// gives 0.  No extra load, so the load pipelines are those of the dot form.
 #include "common.h"
 #include "crit.h"
 #include "dtl.h"
@@ -54,6 +60,7 @@ struct ScoreParams {
   uint64_t* route_part;     // routing, splits > 1: [tiles, splits, 16] (idx, score)
   int32_t* route_count;     // routing, splits > 1: [tiles] arrivals, left at zero
   int shared_rows;          // lookup: rows of a shared unit (at most)
+  int cos;                  // cosine scores (Eq. 5, Eq. 7) instead of dot products
   int32_t* out_idx;         // routing: scene[rows]; lookup: prim[rows, k]
   float* out_w;             // lookup: w[rows, k]
   // lookup with the select of the batch riding along (side0 > 0): launch
@@ -71,6 +78,39 @@ __device__ __forceinline__ void load_row_frags(u32x4_t (&f)[KS], const char* row
   const char* p = row_ptr + g * 16;
 #pragma unroll
   for (int j = 0; j < KS; ++j) f[j] = (!MASKED || j < ks) ? ld16(p + j * 64) : u32x4_t{0, 0, 0, 0};
+}
+
+template <int DT>
+__device__ __forceinline__ float chunk_sumsq(u32x4_t v, float acc) {
+  if constexpr (DT == DT_BF16) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc = fmaf(bf16lo(v[e]), bf16lo(v[e]), acc);
+      acc = fmaf(bf16hi(v[e]), bf16hi(v[e]), acc);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc = fmaf(as_f32(v[e]), as_f32(v[e]), acc);
+  }
+  return acc;
+}
+
+// The sum over the 4 lane groups (lanes n, n + 16, n + 32, n + 48) that hold
+// the chunks of one row.
+__device__ __forceinline__ float sum_lane_groups(float v) {
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
+  return v;
+}
+
+__device__ __forceinline__ float inv_norm(float sq) { return sq > 0.f ? rsqrtf(sq) : 0.f; }
+
+// Cosine scaling of a tile's 4 scores (keys 4g + r of the block, query row
+// n): knsq holds, in every lane of row n', the squared norm of key n'.
+__device__ __forceinline__ f32x4_t cos_scale(f32x4_t acc, float qinv, float knsq, int g) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) acc[r] *= qinv * inv_norm(__shfl(knsq, 4 * g + r, 64));
+  return acc;
 }
 
 // Scores of 4 keys (blk*16 + 4g + r) for one query row folded into the
@@ -203,7 +243,7 @@ __device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, i
 // ---------------------------------------------------------------------------
 // key0, nkeys: the unit's key range (routing may split the keys; Level-2
 // units take all P keys of their scene, key0 = 0).
-template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
+template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool COS>
 __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, int64_t begin,
                                             int nr, const char* keys, int key0, int nkeys,
                                             int split) {
@@ -238,12 +278,18 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
   // have read it.  The refill is unconditional (past the wave's range it
   // re-reads the last block, an L2 hit): a conditional load would make the
   // compiler wait for every load before each block.
+  float qinv = 0.f;   // COS: 1 / ||q|| of the lane's row (after the query landed)
   auto score_block = [&](u32x4_t (&buf)[KS], int next) {
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    float knsq = 0.f;
 #pragma unroll
     for (int j = 0; j < KS; ++j)
-      if (!MASKED || j < a.ks) acc = mfma_chunk<DT>(buf[j], qb[j], acc);
+      if (!MASKED || j < a.ks) {
+        acc = mfma_chunk<DT>(buf[j], qb[j], acc);
+        if constexpr (COS) knsq = chunk_sumsq<DT>(buf[j], knsq);
+      }
     load_block(buf, min(next, kb1 - 1));
+    if constexpr (COS) acc = cos_scale(acc, qinv, sum_lane_groups(knsq), g);
     return acc;
   };
 
@@ -251,6 +297,13 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
   // that at the loop head only key loads are outstanding, oldest first, on
   // every path into it (otherwise the per-block waits become conservative).
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if constexpr (COS) {
+    float qsq = 0.f;
+#pragma unroll
+    for (int j = 0; j < KS; ++j)
+      if (!MASKED || j < a.ks) qsq = chunk_sumsq<DT>(qb[j], qsq);
+    qinv = inv_norm(sum_lane_groups(qsq));
+  }
   if (kb0 < kb1) {
     u32x4_t ka[KS];
     load_block(ka, kb0);
@@ -313,7 +366,7 @@ constexpr int shared_nbuf(int ks) {
                                           : SH_LDS_BYTES / (ks * 1024);
 }
 
-template <int DT, int KS, bool MASKED, bool LOOKUP, int KL>
+template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool COS>
 __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, int64_t begin,
                                             int nr, const char* keys) {
   constexpr int BLOCK_BYTES = KS * 1024;
@@ -338,6 +391,20 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
       load_row_frags<KS, MASKED>(q1, a.q + row_id<LOOKUP>(a, begin, s1) * a.row_bytes, g, a.ks);
     }
   }
+  float qinv0 = 0.f, qinv1 = 0.f;   // COS: 1 / ||q|| of the lane's rows, once they landed
+  auto qnorms = [&]() {
+    if constexpr (COS) {
+      float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+      for (int j = 0; j < KS; ++j)
+        if (!MASKED || j < a.ks) {
+          s0 = chunk_sumsq<DT>(q0[j], s0);
+          if constexpr (TWO_TILES) s1 = chunk_sumsq<DT>(q1[j], s1);
+        }
+      qinv0 = inv_norm(sum_lane_groups(s0));
+      qinv1 = inv_norm(sum_lane_groups(s1));
+    }
+  };
   float ls0[KL], ls1[KL];
   int li0[KL], li1[KL];
 #pragma unroll
@@ -351,6 +418,7 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
     if (!has0) return;                 // a wave without rows only helps to load
     f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
     const char* base = smem + buf * BLOCK_BYTES + lane * 16;
+    float knsq = 0.f;
 #pragma unroll
     for (int j = 0; j < KS; ++j) {
       if (!MASKED || j < a.ks) {
@@ -358,7 +426,13 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
         acc0 = mfma_chunk<DT>(kf, q0[j], acc0);
         if constexpr (TWO_TILES)
           if (has1) acc1 = mfma_chunk<DT>(kf, q1[j], acc1);
+        if constexpr (COS) knsq = chunk_sumsq<DT>(kf, knsq);
       }
+    }
+    if constexpr (COS) {
+      knsq = sum_lane_groups(knsq);
+      acc0 = cos_scale(acc0, qinv0, knsq, g);
+      acc1 = cos_scale(acc1, qinv1, knsq, g);
     }
     fold_scores<LOOKUP, KL>(acc0, blk, g, nkeys, a.bias, ls0, li0);
     if (has1) fold_scores<LOOKUP, KL>(acc1, blk, g, nkeys, a.bias, ls1, li1);
@@ -387,6 +461,7 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
       }
     };
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
+    qnorms();
 #pragma unroll
     for (int b = 0; b < NBUF - 1; ++b) issue(b);
     for (int blk = 0; blk < nblk; ++blk) {
@@ -425,6 +500,7 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
     // Pipeline: at the top of step b the LDS buffer b%2 holds block b, the
     // register set for block b+1 and the one for block b+2 are in flight.
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
+    qnorms();
     u32x4_t r0[CPT], r1[CPT];
     gload(r0, 0);
     asm volatile("" ::: "memory");
@@ -488,7 +564,7 @@ __device__ __forceinline__ void side_select(const ScoreParams& a, char* smem) {
 // KL: per-lane candidate list length (>= k) for lookup; 1 for routing.
 // SIDE (lookup only): launch slots from a.side0 on run side_select; a
 // separate instantiation, so that the kernels without it keep their code.
-template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool SIDE = false>
+template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool SIDE = false, bool COS = false>
 __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   constexpr int MERGE_BYTES = SC_WAVES * 4 * 16 * KL * 8;
   constexpr int STAGE_BYTES = (LOOKUP ? shared_nbuf(KS) : 2) * KS * 1024;
@@ -534,18 +610,18 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     nk = min(a.route_kps, a.nkeys - key0);
     keys = a.keys + (int64_t)key0 * a.row_bytes;
   }
-  if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL>(a, smem, begin, nr, keys);
-  else stream_unit<DT, KS, MASKED, LOOKUP, KL>(a, smem, begin, nr, keys, key0, nk, split);
+  if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys);
+  else stream_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, key0, nk, split);
 }
 
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 
-template <int DT, bool LOOKUP, int KL, bool SIDE = false>
+template <int DT, bool LOOKUP, int KL, bool SIDE = false, bool COS = false>
 static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t st) {
 #define LOOKME_SCORE_LAUNCH(KS_, M_)                                                       \
-  hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL, SIDE>), dim3(grid),            \
+  hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL, SIDE, COS>), dim3(grid),       \
                      dim3(SC_THREADS), 0, st, p)
   // the compiled step count follows score_ks(), which also sizes the units
   switch (ks) {
@@ -563,6 +639,9 @@ static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t 
 
 template <bool LOOKUP, int KL>
 static hipError_t launch_dt(int dt, int ks, int grid, const ScoreParams& p, hipStream_t st) {
+  if (p.cos)   // cosine scores (never with a carried select)
+    return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL, false, true>(ks, grid, p, st)
+                         : launch_ks<DT_F32, LOOKUP, KL, false, true>(ks, grid, p, st);
   if constexpr (LOOKUP) {
     if (p.side0 > 0)
       return dt == DT_BF16 ? launch_ks<DT_BF16, true, KL, true>(ks, grid, p, st)
@@ -584,11 +663,13 @@ static int route_unit_rows(int64_t rows, int shared_rows) {
 
 static int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
-RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes) {
+RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes, bool cos) {
   RoutePlan p{ROUTE_SHARED, 1, S, 0};
   if (rows <= 0 || S <= 0) return p;
   const int64_t blocks = (rows + ROUTE_DTL_ROWS - 1) / ROUTE_DTL_ROWS;
-  if (rows >= ROUTE_DTL_MIN_ROWS && blocks < ROUTE_DTL_MAX_BLOCKS && row_bytes % 128 == 0) {
+  // the tile kernel scores dot products only
+  if (!cos && rows >= ROUTE_DTL_MIN_ROWS && blocks < ROUTE_DTL_MAX_BLOCKS &&
+      row_bytes % 128 == 0) {
     // enough 128-row blocks for the matrix-core kernel but too few to fill
     // the chip with the shared-mode units; split the key tiles until about
     // 512 workgroups run (and at most ROUTE_DTL_MAX_TPS tiles stay with one
@@ -629,7 +710,7 @@ RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes) {
 
 hipError_t launch_route(int dt, const void* q, const void* scene_keys, const float* bias,
                         int32_t* scene, int64_t rows, int d_e, int S, uint64_t* part,
-                        int32_t* count, hipStream_t st) {
+                        int32_t* count, hipStream_t st, bool cos) {
   if (rows == 0) return hipSuccess;
   ScoreParams p{};
   p.q = static_cast<const char*>(q);
@@ -642,7 +723,8 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
   p.k = 1;
   p.route_rows = route_unit_rows(rows, shared_unit_rows(p.row_bytes, 0));
   p.out_idx = scene;
-  const RoutePlan plan = route_plan(rows, S, p.row_bytes);
+  p.cos = cos ? 1 : 0;
+  const RoutePlan plan = route_plan(rows, S, p.row_bytes, cos);
   if (plan.mode == ROUTE_DTL)
     return launch_route_dtl(dt, q, scene_keys, bias, scene, rows, d_e, S, plan, part, count, st);
   p.route_rows = plan.mode == ROUTE_STREAM ? UNIT_STREAM_ROWS : p.route_rows;
@@ -656,8 +738,9 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
 
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st,
-                         const SideSelect* side) {
+                         const SideSelect* side, bool cos) {
   ScoreParams p{};
+  p.cos = cos ? 1 : 0;
   p.q = static_cast<const char*>(q);
   p.keys = static_cast<const char*>(prim_keys);
   p.perm = ws.perm;

@@ -34,8 +34,9 @@ class Run:
     """Outputs of one pass of the path (device tensors) plus the inputs."""
 
     def __init__(self, inp: dict, n_keep: int | None = None, k: int | None = None,
-                 table: lk.Table | None = None, with_kept=True, stream=None):
+                 table: lk.Table | None = None, with_kept=True, stream=None, score: str = "dot"):
         self.inp = inp
+        self.score = score
         x, wt = inp["x"], inp["wt"]
         self.dev = x.device
         self.L = inp["hidden"].shape[0]
@@ -44,8 +45,9 @@ class Run:
         self.n_keep = n_keep if n_keep is not None else inp["n_keep"]
         S, P, d_e = inp["prim_keys"].shape
         self.S, self.P, self.d_e = S, P, d_e
-        self.table = table or lk.Table(inp["scene_keys"], inp["prim_keys"], inp["values"],
-                                       self.k, inp.get("bias"))
+        self.table = table or lk.Table(
+            inp["scene_keys"], inp["prim_keys"], inp["values"], self.k, inp.get("bias"),
+            score=lk.LOOKME_SCORE_COS if score == "cos" else lk.LOOKME_SCORE_DOT)
         self.table.reserve(self.L, self.n)
         L, n = self.L, self.n
         dt = x.dtype
@@ -378,12 +380,12 @@ def check_run(r: Run, tokens=None, layers=None) -> C.Report:
         q_lib = O.to_f64(q_lib_bits, dt)
         # C2: scene on the library's q
         scene = to_np(r.scene[l]).astype(np.int64)
-        C.check_scene(q_lib, K1, bias, "dot", scene[toks], rep)
+        C.check_scene(q_lib, K1, bias, r.score, scene[toks], rep)
         # C3/C4: primitives under the library's scene
         prim = to_np(r.prim[l])
         w = to_np(r.w[l])
-        w_orc = C.check_prim(q_lib, scene[toks], scene_keys_of, r.k, "dot", prim[toks], w[toks],
-                             rep)
+        w_orc = C.check_prim(q_lib, scene[toks], scene_keys_of, r.k, r.score, prim[toks],
+                             w[toks], rep)
         w_of = {int(t): w_orc[i] for i, t in enumerate(toks)}
         # C5: kept set (global)
         c = O.criticality(f64(inp["delta"][l]))

@@ -59,7 +59,7 @@ def _status(fn):
     (dict(key_dim=1024), lk.LOOKME_ERR_UNSUPPORTED),          # 4096 B > 2048 B (fp32)
     (dict(value_dim=3), lk.LOOKME_ERR_UNSUPPORTED),
     (dict(num_scenes=20000), lk.LOOKME_ERR_UNSUPPORTED),
-    (dict(score=lk.LOOKME_SCORE_COS), lk.LOOKME_ERR_UNSUPPORTED),
+    (dict(score=5), lk.LOOKME_ERR_INVALID),
 ])
 def test_create_rejects(lib, kw, status):
     st, msg = _status(lambda: lk.lookme_create(_desc(**kw), FAKE, FAKE, FAKE))

@@ -253,6 +253,51 @@ def test_lookup_select_integer_ties_and_edges():
     assert torch.equal(r.hidden, r.h_in)
 
 
+def _cos_inputs(wl, seed):
+    """The workload's inputs with keys of uneven norms (each key row scaled by
+    a factor in [0.25, 4), one key of each table zero), one zero query row
+    and a scene bias: the cosine then ranks differently from the dot
+    product."""
+    inp = make_inputs(wl, seed=seed, device=DEV)
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    S, P, d_e = inp["prim_keys"].shape
+    f1 = torch.exp2(torch.rand((S, 1), generator=g) * 4 - 2).to(DEV)
+    f2 = torch.exp2(torch.rand((S, P, 1), generator=g) * 4 - 2).to(DEV)
+    k1 = (inp["scene_keys"].float() * f1).to(inp["scene_keys"].dtype)
+    k2 = (inp["prim_keys"].float() * f2).to(inp["prim_keys"].dtype)
+    k1[S // 2] = 0
+    k2[0, P // 2] = 0
+    inp["scene_keys"], inp["prim_keys"] = k1.contiguous(), k2.contiguous()
+    inp["x"] = inp["x"].clone()
+    inp["x"][1] = 0
+    inp["bias"] = (torch.randn(S, generator=g) * 0.05).to(DEV)
+    return inp
+
+
+@pytest.mark.parametrize("name", ["bf16_ragged_l2", "f32_proj_l3", "bf16_k32_shared",
+                                  "bf16_zipf_tiles", "bf16_many_tokens", "f32_k16_shared"])
+def test_cosine_scores(name):
+    """COS handles (the cosine of Eq. 5 and Eq. 7): routing with the bias and
+    Level-2 against the oracle's cosines, in the streaming and shared units;
+    the one-stream select falls back to its own kernels and stays the same
+    bits."""
+    from tests.harness import Run, check_run, run_fused_select
+    wl = SMALL[name]
+    _announce(f"cosine {name}")
+    inp = _cos_inputs(wl, 41)
+    toks = np.arange(0, wl.n_tokens, 5) if wl.n_tokens > 5000 else None
+    r = Run(inp, score="cos").run()
+    rep = check_run(r, tokens=toks)
+    assert rep.ok, str(rep)
+    d = Run(inp, score="dot").run()
+    torch.cuda.synchronize()
+    assert not torch.equal(r.w, d.w)          # the cosine form was taken
+    f = run_fused_select(Run(inp, table=r.table, score="cos"))
+    torch.cuda.synchronize()
+    for key in ("scene", "prim", "w", "kept", "hidden"):
+        assert torch.equal(getattr(r, key), getattr(f, key)), key
+
+
 def test_layers_batched_equal_sequential():
     from tests.harness import Run
     wl = SMALL["bf16_ragged_l2"].scaled(layers=3)
