@@ -450,14 +450,17 @@ lookme_status_t lookme_inject_text(int32_t dtype, const void* table, int64_t voc
 /*
  * Measurement support (not part of the method).  When enabled, each kernel
  * group that route/lookup/inject launches is bracketed by a pair of HIP timing
- * events recorded on the call's stream.  lookme_profile_read waits for the
+ * events recorded on the call's stream; the Level-2 scoring launch of the
+ * bucketed lookups (lookme_lookup, lookme_lookup_select, lookme_lookup_gate)
+ * instead records its own start and end in its pair (an extended launch), so
+ * its time is the kernel's duration alone.  lookme_profile_read waits for the
  * recorded events, adds their durations to per-group totals and returns the
  * totals since the last reset.  Groups (lookme_group_t):
  *   PROJECT  query projection GEMM          ROUTE   Level-1 scoring + arg max
  *   BUCKET   scene bucketing (3 kernels)    SCORE   Level-2 scoring + top-k + softmax
  *   NORM     criticality norms              SELECT  top-n_keep select + compaction
  *   INJECT   row gather + residual add
- * Timing events cost a few microseconds of launch overhead per group; leave
+ * Recorded events cost a few microseconds of launch overhead per group; leave
  * profiling off when measuring end-to-end throughput.
  */
 typedef enum {

@@ -183,7 +183,8 @@ struct SideSelect {
 };
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st,
-                         const SideSelect* side = nullptr, bool cos = false);
+                         const SideSelect* side = nullptr, bool cos = false,
+                         const hipEvent_t* stamp = nullptr);
 
 // ---- criticality, select and injection ------------------------------------
 hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uint32_t* key,

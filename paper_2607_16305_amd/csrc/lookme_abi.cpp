@@ -201,6 +201,44 @@ class Timed {
   bool armed_ = false;
 };
 
+// Hands a pair of timing events, when profiling is on, to a launch of one
+// kernel that records its own start and end in them (hipExtLaunchKernelGGL):
+// the kernel's duration, without the gaps that recorded events add.
+class Stamped {
+ public:
+  Stamped(lookme_t h, int group) : h_(h) {
+    if (!h->profiling) return;
+    t_.group = group;
+    if (take_event(h, &ev_[0]) != hipSuccess) return;
+    if (take_event(h, &ev_[1]) != hipSuccess) {
+      h->spare.push_back(ev_[0]);
+      return;
+    }
+    armed_ = true;
+  }
+  const hipEvent_t* events() const { return armed_ ? ev_ : nullptr; }
+  // ok: the launch went in, so it records both events
+  void done(bool ok) {
+    if (!armed_) return;
+    armed_ = false;
+    if (ok) {
+      t_.start = ev_[0];
+      t_.stop = ev_[1];
+      h_->pending.push_back(t_);
+    } else {
+      h_->spare.push_back(ev_[0]);
+      h_->spare.push_back(ev_[1]);
+    }
+  }
+  ~Stamped() { done(false); }
+
+ private:
+  lookme_t h_;
+  TimedLaunch t_{};
+  hipEvent_t ev_[2] = {nullptr, nullptr};
+  bool armed_ = false;
+};
+
 #define LOOKME_TRY(expr)                    \
   do {                                      \
     lookme_status_t st_ = (expr);           \
@@ -312,11 +350,12 @@ lookme_status_t run_lookup(lookme_t h, const Layout& L, int32_t layers, int64_t 
   lookme::SideSelect side{layers, n, select ? sel->n_keep : 0, key,
                           select ? sel->kept : nullptr};
   if (gate) side.count = sel->count;
-  Timed tm(h, LOOKME_GROUP_SCORE, st);
-  return hip_status(lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
-                                          d.prims_per_scene, d.top_k, prim_out, w_out, st,
-                                          ride ? &side : nullptr, cos),
-                    "lookup launch");
+  Stamped tm(h, LOOKME_GROUP_SCORE);
+  const hipError_t e = lookme::launch_lookup(d.dtype, q, h->prim_keys, b, d.key_dim,
+                                             d.prims_per_scene, d.top_k, prim_out, w_out, st,
+                                             ride ? &side : nullptr, cos, tm.events());
+  tm.done(e == hipSuccess);
+  return hip_status(e, "lookup launch");
 }
 
 }  // namespace

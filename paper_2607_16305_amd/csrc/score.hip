@@ -28,6 +28,8 @@
 // matrix cores already read (a query row's once per unit, a key's once per
 // 16-key block, over the 4 lane groups that hold its chunks); a zero vector
 // gives 0.  No extra load, so the load pipelines are those of the dot form.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "crit.h"
 #include "dtl.h"
@@ -619,10 +621,19 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
 // ---------------------------------------------------------------------------
 
 template <int DT, bool LOOKUP, int KL, bool SIDE = false, bool COS = false>
-static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t st) {
-#define LOOKME_SCORE_LAUNCH(KS_, M_)                                                       \
-  hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL, SIDE, COS>), dim3(grid),       \
-                     dim3(SC_THREADS), 0, st, p)
+static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t st,
+                            const hipEvent_t* stamp) {
+  // with a stamp pair, the launch itself records the kernel's start and end
+  // in the two events (its own duration, without the gaps of recorded events)
+#define LOOKME_SCORE_LAUNCH(KS_, M_)                                                         \
+  do {                                                                                     \
+    if (stamp != nullptr)                                                                  \
+      hipExtLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL, SIDE, COS>), dim3(grid),  \
+                            dim3(SC_THREADS), 0, st, stamp[0], stamp[1], 0, p);           \
+    else                                                                                   \
+      hipLaunchKernelGGL((score_kernel<DT, KS_, M_, LOOKUP, KL, SIDE, COS>), dim3(grid),     \
+                         dim3(SC_THREADS), 0, st, p);                                      \
+  } while (0)
   // the compiled step count follows score_ks(), which also sizes the units
   switch (ks) {
     case 4: LOOKME_SCORE_LAUNCH(4, false); break;
@@ -638,17 +649,18 @@ static hipError_t launch_ks(int ks, int grid, const ScoreParams& p, hipStream_t 
 }
 
 template <bool LOOKUP, int KL>
-static hipError_t launch_dt(int dt, int ks, int grid, const ScoreParams& p, hipStream_t st) {
+static hipError_t launch_dt(int dt, int ks, int grid, const ScoreParams& p, hipStream_t st,
+                            const hipEvent_t* stamp = nullptr) {
   if (p.cos)   // cosine scores (never with a carried select)
-    return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL, false, true>(ks, grid, p, st)
-                         : launch_ks<DT_F32, LOOKUP, KL, false, true>(ks, grid, p, st);
+    return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL, false, true>(ks, grid, p, st, stamp)
+                         : launch_ks<DT_F32, LOOKUP, KL, false, true>(ks, grid, p, st, stamp);
   if constexpr (LOOKUP) {
     if (p.side0 > 0)
-      return dt == DT_BF16 ? launch_ks<DT_BF16, true, KL, true>(ks, grid, p, st)
-                           : launch_ks<DT_F32, true, KL, true>(ks, grid, p, st);
+      return dt == DT_BF16 ? launch_ks<DT_BF16, true, KL, true>(ks, grid, p, st, stamp)
+                           : launch_ks<DT_F32, true, KL, true>(ks, grid, p, st, stamp);
   }
-  return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL>(ks, grid, p, st)
-                       : launch_ks<DT_F32, LOOKUP, KL>(ks, grid, p, st);
+  return dt == DT_BF16 ? launch_ks<DT_BF16, LOOKUP, KL>(ks, grid, p, st, stamp)
+                       : launch_ks<DT_F32, LOOKUP, KL>(ks, grid, p, st, stamp);
 }
 
 static inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
@@ -738,7 +750,7 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
 
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st,
-                         const SideSelect* side, bool cos) {
+                         const SideSelect* side, bool cos, const hipEvent_t* stamp) {
   ScoreParams p{};
   p.cos = cos ? 1 : 0;
   p.q = static_cast<const char*>(q);
@@ -765,10 +777,10 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
     p.gate_count = side->count;
     grid += side->layers;
   }
-  if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st);
-  if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st);
-  if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st);
-  return launch_dt<true, 32>(dt, p.ks, grid, p, st);
+  if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st, stamp);
+  if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st, stamp);
+  if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st, stamp);
+  return launch_dt<true, 32>(dt, p.ks, grid, p, st, stamp);
 }
 
 }  // namespace lookme
