@@ -186,12 +186,25 @@ class Timed {
   Timed(lookme_t h, int group, hipStream_t st) : h_(h), st_(st) {
     if (!h->profiling) return;
     t_.group = group;
-    if (take_event(h, &t_.start) != hipSuccess || take_event(h, &t_.stop) != hipSuccess) return;
+    if (take_event(h, &t_.start) != hipSuccess) return;
+    if (take_event(h, &t_.stop) != hipSuccess) {
+      h->spare.push_back(t_.start);
+      return;
+    }
     armed_ = hipEventRecord(t_.start, st) == hipSuccess;
+    if (!armed_) {
+      h->spare.push_back(t_.start);
+      h->spare.push_back(t_.stop);
+    }
   }
   ~Timed() {
     if (!armed_) return;
-    if (hipEventRecord(t_.stop, st_) == hipSuccess) h_->pending.push_back(t_);
+    if (hipEventRecord(t_.stop, st_) == hipSuccess) {
+      h_->pending.push_back(t_);
+    } else {
+      h_->spare.push_back(t_.start);
+      h_->spare.push_back(t_.stop);
+    }
   }
 
  private:

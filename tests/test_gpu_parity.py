@@ -234,6 +234,45 @@ def test_lookup_select_one_launch(name):
             assert torch.equal(getattr(ref, key), getattr(r, key)), (rep_i, key)
 
 
+def test_profiling_hooks_time_every_group_and_change_nothing():
+    """With the measurement hooks on, every group of a pass is timed once per
+    launch (the Level-2 launch through its own start/end stamps, the others
+    through events recorded around them), the durations are positive and
+    below a second, a reset clears them, and the outputs carry the same bits
+    as with the hooks off."""
+    from paper_2607_16305_amd import lookme as lk
+    from tests.harness import Run, run_fused_select
+    _announce("profiling hooks")
+    inp = make_inputs(SMALL["bf16_ragged_l2"], seed=41, device=DEV)
+    ref = run_fused_select(Run(inp))
+    torch.cuda.synchronize()
+    h = ref.table.handle
+    lk.lookme_profile_enable(h, True)
+    try:
+        for g in range(len(lk.GROUPS)):
+            lk.lookme_profile_read(h, g, reset=True)
+        passes = 3
+        for _ in range(passes):
+            r = run_fused_select(Run(inp, table=ref.table))
+        torch.cuda.synchronize()
+        for key in ("q", "scene", "prim", "w", "kept", "hidden"):
+            assert torch.equal(getattr(ref, key), getattr(r, key)), key
+        for name in ("project", "route", "bucket", "score", "inject"):
+            count, ms = lk.lookme_profile_read(h, lk.GROUPS.index(name))
+            assert count == passes, (name, count)
+            assert 0.0 < ms < 1000.0 * passes, (name, ms)
+        g = lk.GROUPS.index("score")
+        count, _ = lk.lookme_profile_read(h, g, reset=True)
+        assert count == passes
+        assert lk.lookme_profile_read(h, g) == (0, 0.0)
+    finally:
+        lk.lookme_profile_enable(h, False)
+    r = run_fused_select(Run(inp, table=ref.table))
+    torch.cuda.synchronize()
+    assert lk.lookme_profile_read(h, lk.GROUPS.index("score"))[0] == 0
+    assert torch.equal(ref.prim, r.prim) and torch.equal(ref.hidden, r.hidden)
+
+
 def test_lookup_select_integer_ties_and_edges():
     """Exact integer criticalities (many equal norms at the cut): the fused
     select keeps the lowest tokens like the stand-alone one; n_keep = n and
