@@ -337,6 +337,20 @@ lookme_status_t lookme_inject_multiscale(lookme_t h, int64_t n, int64_t n_keep,
                                          int32_t d_h, void* stream);
 
 /*
+ * lookme_inject_multiscale_gated -- lookme_inject_multiscale for the counted
+ * list of lookme_gate (Eq. 8 with the learned gate of Eq. 9-10): kept [n]
+ * int32 holds the layer's open token ids in its first count[0] entries (the
+ * rest is not read), count [1] int32 is read on the device; scene, prim, w,
+ * hidden and the workspace as for lookme_inject_multiscale, whose result it
+ * gives bit for bit for the same set.  Launches for n entries; those past the
+ * count do nothing.  count NULL or no router registered: INVALID.
+ */
+lookme_status_t lookme_inject_multiscale_gated(lookme_t h, int64_t n, const int32_t* kept,
+                                               const int32_t* count, const int32_t* scene,
+                                               const int32_t* prim, const float* w, void* hidden,
+                                               int32_t d_h, void* stream);
+
+/*
  * lookme_gate -- the learned SKA gate of the intra-layer sparse activation
  * (Sec. 3.3, Eq. 9) as it acts at inference: the Gumbel-Sigmoid is hard and
  * noise-free, so entry i of a layer opens exactly when

@@ -164,7 +164,7 @@ hipError_t launch_multiscale(int dt, int scales, int64_t n, int64_t n_keep, cons
                              const int32_t* scene, const int32_t* prim, const float* w,
                              const void* values, int S, int P, int d_v, int k,
                              const void* w_he_t, int d_h, void* hidden, void* r, void* q,
-                             hipStream_t st);
+                             hipStream_t st, const int32_t* count = nullptr);
 
 // ---- Level-2 scoring of bucketed rows, fused top-k + softmax --------------
 // The sparse-injection select (Eq. 9-10) of the same batch carried by the

@@ -997,4 +997,30 @@ lookme_status_t lookme_inject_multiscale(lookme_t h, int64_t n, int64_t n_keep,
                     "multi-scale injection launch");
 }
 
+lookme_status_t lookme_inject_multiscale_gated(lookme_t h, int64_t n, const int32_t* kept,
+                                               const int32_t* count, const int32_t* scene,
+                                               const int32_t* prim, const float* w, void* hidden,
+                                               int32_t d_h, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  if (h->ms_scales < 1)
+    return fail(LOOKME_ERR_INVALID, "no multi-scale router registered (lookme_set_multiscale)");
+  LOOKME_TRY(check_layers_n(h->ms_scales, n));
+  if (d_h != h->ms_dh)
+    return fail(LOOKME_ERR_INVALID, "d_h %d, the router reads %d", d_h, h->ms_dh);
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(count, "count"));
+  LOOKME_TRY(check_lookup_ptrs(kept, scene, prim, w, hidden));
+  Layout L;
+  LOOKME_TRY(check_workspace(h, 1, n, &L));
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(h->ws);
+  Timed tm(h, LOOKME_GROUP_INJECT, st);
+  return hip_status(lookme::launch_multiscale(d.dtype, h->ms_scales, n, n, kept, scene, prim, w,
+                                              h->values, d.num_scenes, d.prims_per_scene,
+                                              d.value_dim, d.top_k, h->ms_w, d_h, hidden,
+                                              ws + L.ms_r, ws + L.ms_q, st, count),
+                    "multi-scale injection launch");
+}
+
 }  // extern "C"

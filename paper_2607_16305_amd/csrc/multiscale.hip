@@ -27,9 +27,10 @@ template <int DT>
 __global__ __launch_bounds__(MS_THREADS) void ms_router_kernel(
     int64_t n, int64_t n_keep, const int32_t* __restrict__ kept, int M,
     const char* __restrict__ q, const char* __restrict__ r, char* __restrict__ hidden,
-    int64_t h_bytes, int64_t v_bytes, float inv_sqrt_d) {
+    int64_t h_bytes, int64_t v_bytes, float inv_sqrt_d, const int32_t* __restrict__ count) {
   __shared__ float red[MS_MAX_SCALES][MS_THREADS / WAVE];
   const int64_t j = blockIdx.x;
+  if (count != nullptr && j >= *count) return;   // past a counted list's end
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int nw = (int)(blockDim.x / WAVE);
   int64_t t = kept[j];
@@ -134,12 +135,12 @@ hipError_t launch_multiscale(int dt, int scales, int64_t n, int64_t n_keep, cons
                              const int32_t* scene, const int32_t* prim, const float* w,
                              const void* values, int S, int P, int d_v, int k,
                              const void* w_he_t, int d_h, void* hidden, void* r, void* q,
-                             hipStream_t st) {
+                             hipStream_t st, const int32_t* count) {
   if (n == 0 || n_keep == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const int Sm = S / scales;
   hipError_t e = launch_gather_rows(dt, scales, n, n_keep, kept, scene, prim, w, values, Sm, P,
-                                    d_v, k, r, st, 0, Sm);
+                                    d_v, k, r, st, 0, Sm, count);
   if (e != hipSuccess) return e;
 
   // q = round(H[kept] W_he): every K stage of an A row comes from the kept
@@ -156,6 +157,8 @@ hipError_t launch_multiscale(int dt, int scales, int64_t n, int64_t n_keep, cons
   g.k_bytes = g.a_bytes;
   g.cols = d_v;
   g.ksplit = 0;
+  g.count = count;   // a counted list: rows past count[0] are skipped
+  g.count_step = 0;
   g.tiles = (int)(((n_keep + TgShape::BM - 1) / TgShape::BM) *
                   ((d_v + TgShape::BN - 1) / TgShape::BN));
   e = launch_tile_gemm<EPI_STORE>(dt, g, 1, st);
@@ -169,12 +172,12 @@ hipError_t launch_multiscale(int dt, int scales, int64_t n, int64_t n_keep, cons
     hipLaunchKernelGGL(ms_router_kernel<DT_BF16>, dim3((unsigned)n_keep), dim3(bs), 0, st, n,
                        n_keep, kept, scales, static_cast<const char*>(q),
                        static_cast<const char*>(r), static_cast<char*>(hidden),
-                       (int64_t)d_h * es, vb, inv_sqrt_d);
+                       (int64_t)d_h * es, vb, inv_sqrt_d, count);
   else
     hipLaunchKernelGGL(ms_router_kernel<DT_F32>, dim3((unsigned)n_keep), dim3(bs), 0, st, n,
                        n_keep, kept, scales, static_cast<const char*>(q),
                        static_cast<const char*>(r), static_cast<char*>(hidden),
-                       (int64_t)d_h * es, vb, inv_sqrt_d);
+                       (int64_t)d_h * es, vb, inv_sqrt_d, count);
   return hipGetLastError();
 }
 

@@ -29,7 +29,8 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_lookup", "lookme_inject", "lookme_select", "lookme_inject_kept",
             "lookme_set_relevance", "lookme_lookup_relevance", "lookme_set_fusion",
             "lookme_inject_fused", "lookme_set_propagation", "lookme_inject_propagated",
-            "lookme_set_multiscale", "lookme_inject_multiscale", "lookme_gate",
+            "lookme_set_multiscale", "lookme_inject_multiscale",
+            "lookme_inject_multiscale_gated", "lookme_gate",
             "lookme_inject_gated", "lookme_inject_fused_gated", "lookme_inject_propagated_gated",
             "lookme_inject_text", "lookme_lookup_select", "lookme_lookup_gate",
             "lookme_destroy", "lookme_last_error",
@@ -93,6 +94,8 @@ def load():
                                      _vp, _vp, _vp, _vp, ctypes.c_int32, _vp],
         "lookme_gate": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, ctypes.c_int64, ctypes.c_int32,
                         _vp, _vp, _vp, _vp, _vp],
+        "lookme_inject_multiscale_gated": [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp, _vp,
+                                           ctypes.c_int32, _vp],
         "lookme_inject_gated": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
                                 _vp, ctypes.c_int32, _vp],
         "lookme_inject_fused_gated": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp, _vp,
@@ -251,6 +254,12 @@ def lookme_gate(h, layers, n, delta, delta_rows, d_c, pos, w_g, kept_out, count_
 def lookme_inject_gated(h, layers, n, kept, count, scene, prim, w, hidden, d_h, stream=None):
     _check(load().lookme_inject_gated(h, layers, n, _ptr(kept), _ptr(count), _ptr(scene),
                                       _ptr(prim), _ptr(w), _ptr(hidden), d_h, _stream(stream)))
+
+
+def lookme_inject_multiscale_gated(h, n, kept, count, scene, prim, w, hidden, d_h, stream=None):
+    _check(load().lookme_inject_multiscale_gated(h, n, _ptr(kept), _ptr(count), _ptr(scene),
+                                                 _ptr(prim), _ptr(w), _ptr(hidden), d_h,
+                                                 _stream(stream)))
 
 
 def lookme_inject_fused_gated(h, layers, n, kept, count, scene, prim, w, hidden, d_h,
@@ -415,6 +424,12 @@ class Table:
         self.reserve(1, n)
         lookme_inject_multiscale(self.handle, n, n_keep, kept, scene, prim, w, hidden,
                                  hidden.shape[-1], stream)
+
+    def inject_multiscale_gated(self, kept, count, scene, prim, w, hidden, stream=None):
+        n = hidden.shape[0]
+        self.reserve(1, n)
+        lookme_inject_multiscale_gated(self.handle, n, kept, count, scene, prim, w, hidden,
+                                       hidden.shape[-1], stream)
 
     def gate(self, delta, w_g, kept_out, count_out, pos=None, layers=1, stream=None):
         """lookme_gate: delta [layers, rows, d_c] (or [rows, d_c]); pos [n] or

@@ -259,7 +259,10 @@ def test_multiscale_entry_points_validate(lib):
         S = lambda f: _status(f)[0]
         call = lambda n=8, n_keep=2, d_h=2048, p=FAKE: lk.lookme_inject_multiscale(
             h, n, n_keep, p, p, p, p, p, d_h, 0)
+        gated = lambda n=8, c=FAKE, d_h=2048, p=FAKE: lk.lookme_inject_multiscale_gated(
+            h, n, p, c, p, p, p, p, d_h, 0)
         assert S(lambda: call()) == lk.LOOKME_ERR_INVALID                    # none registered
+        assert S(lambda: gated()) == lk.LOOKME_ERR_INVALID
         assert S(lambda: lk.lookme_set_multiscale(h, 0, 2048, FAKE)) == lk.LOOKME_ERR_UNSUPPORTED
         assert S(lambda: lk.lookme_set_multiscale(h, 9, 2048, FAKE)) == lk.LOOKME_ERR_UNSUPPORTED
         assert S(lambda: lk.lookme_set_multiscale(h, 3, 2048, FAKE)) == lk.LOOKME_ERR_INVALID
@@ -274,6 +277,11 @@ def test_multiscale_entry_points_validate(lib):
         assert S(lambda: call(n_keep=0, p=None)) == lk.LOOKME_OK
         assert S(lambda: call(p=None)) == lk.LOOKME_ERR_INVALID
         assert S(lambda: call()) == lk.LOOKME_ERR_WORKSPACE
+        assert S(lambda: gated(d_h=4096)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: gated(c=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: gated(p=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: gated(n=0, c=None, p=None)) == lk.LOOKME_OK
+        assert S(lambda: gated()) == lk.LOOKME_ERR_WORKSPACE
     finally:
         lk.lookme_destroy(h)
 

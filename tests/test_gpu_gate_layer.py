@@ -184,6 +184,60 @@ def test_gated_injection(name):
             assert torch.equal(hid[0], r.hidden[l]), f"layer {l}"
 
 
+SMALL_MS = {
+    "ms_bf16": (Workload("ms_bf16", "bf16", 300, 1, 256, 128, 20, 60, 128, 192, 8, 30,
+                         value_std=1.0), 2),
+    "ms_f32_three": (Workload("ms_f32", "f32", 77, 1, 96, 64, 15, 37, 64, 96, 3, 20,
+                              value_std=1.0), 3),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL_MS))
+def test_gated_multiscale_injection(name):
+    """The learned gate with the multi-scale router (Eq. 8-10): the gate's
+    counted list into lookme_inject_multiscale_gated gives the oracle's mix of
+    the scales' rows on the open tokens (and the gate the oracle's set), and
+    the same bits as lookme_inject_multiscale given that set as a plain list."""
+    from paper_2607_16305_amd import lookme as lk
+    from synth import make_multiscale
+    from tests.harness import MultiScaleRun, f64, to_np
+    wl, scales = SMALL_MS[name]
+    _announce(f"gated multi-scale {name}: {wl}")
+    inp = make_inputs(wl, seed=12, device=DEV)
+    ms = make_multiscale(wl, 12, scales, device=DEV)
+    r = MultiScaleRun(inp, ms).run()
+    w_g = make_gate(wl, 12, device=DEV, layers=1)
+    n = r.n
+    kept = torch.full((n,), -7, dtype=torch.int32, device=DEV)
+    count = torch.full((4,), -7, dtype=torch.int32, device=DEV)
+    r.table.gate(inp["delta"][0], w_g, kept, count[:1])
+    hid = r.h_in.clone()
+    r.table.inject_multiscale_gated(kept, count[:1], r.scene, r.prim, r.w, hid)
+    torch.cuda.synchronize()
+    c = int(count[0])
+    assert 0 < c < n
+    kept_np = kept.cpu().numpy()
+    rep = C.Report()
+    C.check_gate(f64(inp["delta"][0]), f64(w_g[0]), kept_np[:c], rep)
+    dt = "bf16" if inp["x"].dtype == torch.bfloat16 else "f32"
+    values = inp["values"]
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    toks = np.arange(n)
+    C.check_multiscale_hidden(to_np(r.h_in), to_np(hid), dt, values_rows, r.P, r.S // r.M,
+                              to_np(r.scene), to_np(r.prim), to_np(r.w), kept_np[:c],
+                              f64(ms["w_he_t"]).T, rep, toks)
+    rep = rep.finish()
+    assert rep.ok, str(rep)
+    plain = r.h_in.clone()
+    r.table.inject_multiscale(kept[:c].contiguous(), r.scene, r.prim, r.w, plain, c)
+    torch.cuda.synchronize()
+    assert torch.equal(plain, hid)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_text_injection(dtype):
     """The text pathway: the gate over the text positions, then
