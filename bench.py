@@ -67,7 +67,7 @@ def parse():
                          "(seeded W_g; open where Delta W_g > 0, a variable count) instead of "
                          "the top n_keep by criticality")
     ap.add_argument("--layer", action="store_true",
-                    help="time one whole LookME layer (Eq. 3) on a sequence of 64 + 192 text "
+                    help="time one whole LookME layer (Eq. 2) on a sequence of 64 + 192 text "
                          "positions around the workload's image block: text, image and "
                          "cross-modal pathways, each with its learned gate")
     ap.add_argument("--two-streams", action="store_true",
@@ -453,7 +453,7 @@ class Bench:
 
 
 class LayerBench:
-    """One whole LookME layer (Eq. 3) per step on a sequence of TEXT_BEFORE
+    """One whole LookME layer (Eq. 2) per step on a sequence of TEXT_BEFORE
     text positions, the workload's image block and TEXT_AFTER text
     positions: the cross-modal pathway routes and looks up every position's
     L_dec(H_in) row in its own table (the paper's N_s = 512 scenes of

@@ -7,6 +7,9 @@ exact rational round-to-nearest-even to bfloat16 / binary32.  It pins the
 oracle; it is far too slow for anything but a few dozen tokens.
 
 Paper: arXiv 2607.16305, Sec. 3.2 (Eq. 4-7) and Sec. 3.3 (Eq. 9-10).
+The cosine scores of Eq. 5 and Eq. 7 are exact rationals here for vectors
+built to have rational norms; softmax weights over them are evaluated in
+40-digit decimal arithmetic.
 """
 
 from __future__ import annotations
@@ -95,6 +98,88 @@ def route(q_rows, scene_keys, bias=None):
         s = [dot(q, key) + (Fraction(bias[j]) if bias is not None else 0)
              for j, key in enumerate(scene_keys)]
         out.append(argmax_lowest(s))
+    return out
+
+
+def rational_sqrt(v: Fraction) -> Fraction:
+    """Exact square root of a non-negative rational whose numerator and
+    denominator are perfect squares; raises ValueError otherwise (the
+    cosine routines below are only used on vectors built to have rational
+    norms)."""
+    v = Fraction(v)
+    if v < 0:
+        raise ValueError("negative")
+    rn, rd = math.isqrt(v.numerator), math.isqrt(v.denominator)
+    if rn * rn != v.numerator or rd * rd != v.denominator:
+        raise ValueError(f"{v} is not the square of a rational")
+    return Fraction(rn, rd)
+
+
+def cosine_exact(a, b) -> Fraction:
+    """cos(a, b) = <a, b> / (|a| |b|) as an exact rational (Eq. 5 and Eq. 7
+    in their cosine form); 0 when either vector is zero.  Needs |a|^2 |b|^2
+    to be the square of a rational."""
+    na, nb = dot(a, a), dot(b, b)
+    if na == 0 or nb == 0:
+        return Fraction(0)
+    return dot(a, b) / rational_sqrt(na * nb)
+
+
+def route_cos(q_rows, scene_keys, bias=None):
+    """Level-1 under the cosine of Eq. 5: arg max over s of
+    cos(q, e_img[s]) + b[s], exact rationals, lowest s on exact ties.
+    Returns (scenes, exact score rows)."""
+    out, rows = [], []
+    for q in q_rows:
+        s = [cosine_exact(q, key) + (Fraction(bias[j]) if bias is not None else 0)
+             for j, key in enumerate(scene_keys)]
+        out.append(argmax_lowest(s))
+        rows.append(s)
+    return out, rows
+
+
+def lookup_cos(q_rows, scenes, prim_keys, k):
+    """Level-2 under the cosine of Eq. 7: the k largest exact cosines of the
+    chosen scene's primitive keys (prim_keys[s][p]) by repeated extraction
+    (lowest p on exact ties).  Returns (prim, exact top cosines, all exact
+    cosines per row)."""
+    prim, top, alls = [], [], []
+    for q, s in zip(q_rows, scenes):
+        c = [cosine_exact(q, key) for key in prim_keys[s]]
+        idx = topk_by_extraction(c, k)
+        prim.append(idx)
+        top.append([c[i] for i in idx])
+        alls.append(c)
+    return prim, top, alls
+
+
+def softmax_decimal(vals, digits: int = 40):
+    """Softmax of exact rationals evaluated in ``digits``-digit decimal
+    arithmetic (correctly rounded exp of the decimal module), returned as
+    floats: an evaluation independent of float64 and of NumPy."""
+    import decimal
+    ctx = decimal.Context(prec=digits)
+    dv = [ctx.divide(decimal.Decimal(v.numerator), decimal.Decimal(v.denominator))
+          for v in map(Fraction, vals)]
+    e = [ctx.exp(x) for x in dv]
+    tot = sum(e, decimal.Decimal(0))
+    return [float(ctx.divide(x, tot)) for x in e]
+
+
+def scene_means(prim_key_rows, P):
+    """Eq. 4 by plain loops: e_img[j] = (1/N_p) sum_p E[j, p, :] for the
+    flat primitive rows of every scene, exact rationals."""
+    S = len(prim_key_rows) // P
+    d = len(prim_key_rows[0])
+    out = []
+    for j in range(S):
+        row = []
+        for c in range(d):
+            acc = Fraction(0)
+            for p in range(P):
+                acc += Fraction(prim_key_rows[j * P + p][c])
+            row.append(acc / P)
+        out.append(row)
     return out
 
 

@@ -12,6 +12,8 @@ Vision-Language Models" (arXiv 2607.16305).
 What is computed, step by step (each function cites its passage):
 
   project     Sec. 3.2 "Level-1: scene retrieval": v_e = v W_{v->e}
+  scene_keys_from_primitives
+              Eq. 4: a scene's key as the mean of its primitive embeddings
   route       Sec. 3.2 Level-1, Eq. 5: scene = argmax(score(v_e, e_img) + b)
   lookup      Sec. 3.2 Level-2, Eq. 6-7 in the configured form: top-k
               primitives of the chosen scene by dot score against per-row
@@ -43,8 +45,9 @@ What is computed, step by step (each function cites its passage):
               positions with Delta_i W_g > 0 (a learned gate, variable count)
   text        Sec. 3.2 "Text embedding index-based lookup" (Eq. 1):
               R_text = E_text[u] at the text positions; inject_text adds it
-  lookme_layer  Eq. 3: one LookME layer, L_dec(H_in) plus the text, image and
-              cross-modal pathways' gated injections in that order; the
+  lookme_layer  Eq. 2: one LookME layer, L_dec(H_in) plus the text, image and
+              cross-modal pathways' gated injections (the three retrievals of
+              Eq. 3) in that order; the
               cross-modal pathway queries the two-level lookup with L_dec(H_in)
               itself at every position (Sec. 3.2, cross-modal embedding
               hierarchical two-level lookup)
@@ -170,6 +173,17 @@ def project(x: np.ndarray, w_t: np.ndarray | None, dtype: str) -> np.ndarray:
         return np.array(x, dtype=np.float64, copy=True)
     q_exact = x @ w_t.T           # (v W)[t, j] = sum_i v[t, i] W[i, j]
     return round_to_dtype(q_exact, dtype)
+
+
+def scene_keys_from_primitives(prim_keys: np.ndarray) -> np.ndarray:
+    """Scene-centred keys (Eq. 4): each scene's key is the mean of its
+    primitive embeddings, e_img[j] = (1/N_p) sum_p E[j, p, :].
+
+    prim_keys [S, P, d_e] float64 values -> [S, d_e] float64 (not rounded;
+    a caller storing them rounds once to its dtype).
+    """
+    prim_keys = np.asarray(prim_keys, dtype=np.float64)
+    return np.sum(prim_keys, axis=1) / prim_keys.shape[1]
 
 
 def _unit_rows(a: np.ndarray) -> np.ndarray:
@@ -547,7 +561,7 @@ def inject_fused(hidden: np.ndarray, values: np.ndarray, P: int, scene: np.ndarr
 
 # ---------------------------------------------------------------------------
 # Learned SKA gate (Eq. 9), the text pathway (Sec. 3.2, ID lookup) and one
-# whole LookME layer with its three pathways (Eq. 3)
+# whole LookME layer with its three pathways (Eq. 2, retrievals of Eq. 3)
 # ---------------------------------------------------------------------------
 
 def gate_logits(delta: np.ndarray, w_g: np.ndarray) -> np.ndarray:
@@ -590,7 +604,7 @@ def inject_text(hidden: np.ndarray, table: np.ndarray, pos: np.ndarray, ids: np.
 
 def lookme_layer(h_dec: np.ndarray, delta: np.ndarray, *, dtype: str, text=None, image=None,
                  cross=None):
-    """One LookME layer (Eq. 3): H_out = L_dec(H_in) + S(R_text) + S(R_img)
+    """One LookME layer (Eq. 2): H_out = L_dec(H_in) + S(R_text) + S(R_img)
     + S(R_cross), the pathways' sparse injections fused into the backbone
     one after another in that order, each a residual add rounded once to
     dtype.  Every pathway reads the layer's inputs, not a partly injected

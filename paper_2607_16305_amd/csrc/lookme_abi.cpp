@@ -446,16 +446,25 @@ lookme_status_t lookme_profile_read(lookme_t h, int32_t group, int64_t* count, d
   LOOKME_TRY(check_handle(h));
   if (group < 0 || group >= LOOKME_GROUP_COUNT)
     return fail(LOOKME_ERR_INVALID, "unknown kernel group %d", group);
-  for (auto& t : h->pending) {
+  // an entry leaves `pending` exactly when it is counted and its events go
+  // back to the pool: a read that fails part way leaves the unread entries
+  // pending and no entry both counted and still referenced
+  size_t done = 0;
+  lookme_status_t st = LOOKME_OK;
+  for (; done < h->pending.size(); ++done) {
+    const TimedLaunch& t = h->pending[done];
     float ms = 0.f;
-    LOOKME_TRY(hip_status(hipEventSynchronize(t.stop), "hipEventSynchronize"));
-    LOOKME_TRY(hip_status(hipEventElapsedTime(&ms, t.start, t.stop), "hipEventElapsedTime"));
+    st = hip_status(hipEventSynchronize(t.stop), "hipEventSynchronize");
+    if (st == LOOKME_OK)
+      st = hip_status(hipEventElapsedTime(&ms, t.start, t.stop), "hipEventElapsedTime");
+    if (st != LOOKME_OK) break;
     h->prof_count[t.group] += 1;
     h->prof_ms[t.group] += ms;
     h->spare.push_back(t.start);
     h->spare.push_back(t.stop);
   }
-  h->pending.clear();
+  h->pending.erase(h->pending.begin(), h->pending.begin() + done);
+  if (st != LOOKME_OK) return st;
   if (count) *count = h->prof_count[group];
   if (total_ms) *total_ms = h->prof_ms[group];
   if (reset) {

@@ -5,13 +5,19 @@
 // order with the lowest-index tie rule, writes the scenes and resets the
 // counter to zero for the next call.
 //
-// Every access to the partial table is a device-scope atomic (stores and
-// loads), and each writer waits for its own stores to complete before the
-// workgroup's arrival is counted; so the last workgroup's loads, made after
-// it has seen every arrival, return the final partials.  No release or
-// acquire fence is needed for the table, and none is issued: on this chip
-// they write back and invalidate the whole L2 of the workgroup's XCD, which
-// cost the image workload's routing 3 us (15.0 -> 11.9 us a launch).
+// Ordering, in the terms of the scoped (HSA / LLVM AMDGPU) memory model: a
+// thread's partial store is sequenced before the workgroup barrier, whose
+// release/acquire fences (workgroup scope) order it before thread 0's arrival;
+// the arrival is an agent-scope acquire-release read-modify-write, so every
+// earlier arrival (a release at agent scope) synchronises with the last one,
+// whose barrier then orders its threads' partial loads after all of them.
+// Happens-before is transitive across these scope-inclusive pairs, so the
+// last workgroup reads the final partials.  Relaxed atomics alone (an earlier
+// form) give no order between the partial table and the counter in that
+// model; they relied on the store acknowledgement that s_waitcnt vmcnt(0)
+// waits for, a property of the hardware the model does not state.  The
+// release costs one L2 write-back per arriving workgroup (only thread 0
+// performs it), the acquire one invalidation in the last workgroup.
 #pragma once
 #include "common.h"
 
@@ -28,14 +34,11 @@ __device__ __forceinline__ void route_partial(uint64_t* part_all, int32_t* count
     __hip_atomic_store(&part[split * R + t],
                        ((uint64_t)(uint32_t)best_i << 32) | __float_as_uint(best_s),
                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  // this thread's partial has reached the device's coherence point ...
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  // ... and, after the barrier, every thread's has, before the arrival
-  __syncthreads();
+  __syncthreads();   // every thread's partial is ordered before the arrival
   if (threadIdx.x == 0)
-    *s_last = __hip_atomic_fetch_add(&count[tile], 1, __ATOMIC_RELAXED,
+    *s_last = __hip_atomic_fetch_add(&count[tile], 1, __ATOMIC_ACQ_REL,
                                      __HIP_MEMORY_SCOPE_AGENT) == splits - 1;
-  __syncthreads();
+  __syncthreads();   // ... and the last arrival before every thread's loads
   if (!*s_last) return;
   if (t < nr) {
     float bs = -__builtin_inff();

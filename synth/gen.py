@@ -327,7 +327,7 @@ def make_text(seed: int, vocab: int, d_t: int, pos: torch.Tensor, dtype: str = "
 def make_layer(wl: Workload, seed: int, text_before: int, text_after: int, vocab: int,
                d_t: int, cross_scenes: int, cross_prims: int, cross_k: int,
                device="cpu") -> dict:
-    """One LookME layer's inputs (Eq. 3) over a sequence of text_before text
+    """One LookME layer's inputs (Eq. 2) over a sequence of text_before text
     positions, the workload's n_tokens image positions, then text_after text
     positions:
       image   the workload's inputs (make_inputs; its first layer is used)

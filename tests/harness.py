@@ -401,6 +401,42 @@ def check_run(r: Run, tokens=None, layers=None) -> C.Report:
     return rep.finish()
 
 
+def check_end_to_end_run(r: Run, tokens=None, layers=None) -> C.Report:
+    """End-to-end comparison of a finished run: the oracle computes every
+    stage from the original inputs (oracle/check.py: check_end_to_end) and
+    the library's final hidden rows, decisions and weights are compared with
+    its own, ties counted."""
+    torch.cuda.synchronize()
+    inp = r.inp
+    dt = dtype_name(inp["x"])
+    rep = C.Report()
+    layers = range(r.L) if layers is None else layers
+    toks = np.arange(r.n) if tokens is None else np.asarray(tokens)
+    tsel = torch.as_tensor(toks, device=r.dev)
+    K1 = f64(inp["scene_keys"])
+    bias = None if inp.get("bias") is None else inp["bias"].detach().cpu().numpy().astype(np.float64)
+    prim_keys, values = inp["prim_keys"], inp["values"]
+    x64 = f64(inp["x"][tsel])
+
+    class Keys:
+        def __getitem__(self, s):
+            return f64(prim_keys[int(s)])
+
+    def values_rows(rows):
+        idx = torch.as_tensor(np.asarray(rows), device=values.device, dtype=torch.long)
+        return f64(values[idx])
+
+    for l in layers:
+        wt = None if inp["wt"] is None else f64(inp["wt"][l])
+        C.check_end_to_end(x64, wt, K1, bias, r.score, Keys(), values_rows, r.P, r.k,
+                           O.criticality(f64(inp["delta"][l])), r.n_keep,
+                           to_np(r.h_in[l][tsel]), to_np(r.hidden[l][tsel]), dt,
+                           to_np(r.q[l])[toks], to_np(r.scene[l]).astype(np.int64),
+                           to_np(r.prim[l]), to_np(r.w[l]), to_np(r.kept[l])[: r.n_keep], rep,
+                           toks)
+    return rep.finish()
+
+
 class GatedRun(Run):
     """A pass with the learned SKA gate (Eq. 9-10): route and lookup, the
     gate of every layer (lookme_gate: a counted, ascending kept list), then
@@ -502,7 +538,7 @@ def check_gated_run(r: GatedRun, tokens=None) -> C.Report:
 
 
 class LayerRun:
-    """One LookME layer (Eq. 3) over a sequence of text and image positions:
+    """One LookME layer (Eq. 2) over a sequence of text and image positions:
     the cross-modal pathway routes and looks up every position's L_dec(H_in)
     row against its own table, the image pathway the image block's encoder
     embeddings, each pathway's gate reads Delta at its positions, and then the

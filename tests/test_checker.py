@@ -2,6 +2,7 @@
 reject planted mistakes (all on the CPU, no library involved)."""
 
 import numpy as np
+import pytest
 
 from oracle import check as C
 from oracle import lookme_oracle as O
@@ -249,6 +250,85 @@ def test_multiscale_check_accepts_the_oracle_and_rejects_planted_errors():
     assert not check(bad).ok
 
 
+def _fused_case(rng, dtype, n=16, S=3, P=6, d_v=24, d_ff=40, d_h=32, k=3):
+    rd = lambda a: O.round_to_dtype(a, dtype)
+    H = rd(rng.standard_normal((n, d_h)))
+    V = rd(rng.standard_normal((S * P, d_v)))
+    scene = rng.integers(0, S, n)
+    prim = np.stack([rng.permutation(P)[:k] for _ in range(n)])
+    w = rng.dirichlet(np.ones(k), n).astype(np.float32).astype(np.float64)
+    kept = np.array([0, 2, 3, 7, 8, 15])
+    wg = rd(rng.standard_normal((d_ff, d_v)) / np.sqrt(d_v))
+    wu = rd(rng.standard_normal((d_ff, d_v)) / np.sqrt(d_v))
+    wd = rd(rng.standard_normal((d_h, d_ff)) / np.sqrt(d_ff))
+    return H, V, P, scene, prim, w, kept, wg, wu, wd
+
+
+def _fused_float32_evaluation(H, V, P, scene, prim, w, kept, wg, wu, wd, dtype):
+    """The fused injection evaluated the way a float32 kernel would (float32
+    sums in another order than the oracle's), each stored row rounded."""
+    f32 = np.float32
+    rd = lambda a: O.round_to_dtype(np.asarray(a, dtype=np.float64), dtype)
+    out = H.copy()
+    for t in kept:
+        rows = scene[t] * P + prim[t]
+        acc = np.zeros(V.shape[1], dtype=f32)
+        for i in range(len(rows)):
+            acc = acc + f32(w[t, i]) * V[rows[i]].astype(f32)
+        R = rd(acc)
+        g = (wg.astype(f32) @ R.astype(f32)).astype(f32)
+        u = (wu.astype(f32) @ R.astype(f32)).astype(f32)
+        U = rd((g / (f32(1) + np.exp(-g))) * u)
+        F = (wd.astype(f32)[:, ::-1] @ U.astype(f32)[::-1]).astype(f32)
+        d_v = V.shape[1]
+        out[t] = H[t]
+        out[t] = rd(H[t].astype(f32) + F)
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_fused_check_interval_accepts_float32_evaluation_and_rejects_small_errors(dtype):
+    """check_fused_hidden accepts a float32 evaluation of the chain in another
+    summation order; in bf16 its evaluation interval rejects one bf16 step
+    (far below the 2e-2 contract) where the interval is a single value; in
+    float32 the 1e-5 relative rule rejects 3e-5 of the summed magnitudes.
+    (In float32 the worst-case interval of the two chained products is wider
+    than the relative rule; there the rule is the binding one.)"""
+    rng = np.random.default_rng(11)
+    H, V, P, scene, prim, w, kept, wg, wu, wd = _fused_case(rng, dtype)
+    enc = (lambda a: O.f64_to_bf16_bits(a)) if dtype == "bf16" else (lambda a: a.astype(np.float32))
+    n = H.shape[0]
+
+    def check(out):
+        rep = C.Report()
+        C.check_fused_hidden(enc(H), enc(out), dtype, lambda rows: V[rows], P, scene, prim,
+                             w.astype(np.float32), kept, wg, wu, wd, rep, np.arange(n))
+        return rep.finish()
+
+    got = _fused_float32_evaluation(H, V, P, scene, prim, w, kept, wg, wu, wd, dtype)
+    rep = check(got)
+    assert rep.ok, rep
+    assert rep.notes["fused_interval_checked"] == len(kept)
+    bad = got.copy()
+    t, c = int(kept[2]), 5
+    if dtype == "bf16":
+        # step one bf16 value up
+        bits = O.f64_to_bf16_bits(bad[t, c:c + 1]).astype(np.int64)
+        step = 1 if bad[t, c] >= 0 else -1
+        bad[t, c] = O.bf16_bits_to_f64(np.array([bits[0] + step], dtype=np.uint16))[0]
+        assert abs(bad[t, c] - got[t, c]) < 2e-2
+    else:
+        # 3e-5 of the summed magnitudes: inside the earlier 1e-4 rule,
+        # outside the 1e-5 relative contract
+        R = O.round_to_dtype(w[t] @ V[scene[t] * P + prim[t]], dtype)
+        U = O.round_to_dtype(O.silu(wg @ R) * (wu @ R), dtype)
+        mag = abs(H[t, c]) + np.abs(wd[c]) @ np.abs(U)
+        bad[t, c] = np.float32(bad[t, c] + 3e-5 * mag)
+    rep = check(bad)
+    assert not rep.ok
+    assert any(("interval" if dtype == "bf16" else "contract") in f for f in rep.failures)
+
+
 def test_gate_checker_accepts_oracle_exempts_near_zero_and_rejects_flips():
     rng = np.random.default_rng(30)
     D = O.round_to_bf16(rng.standard_normal((200, 24)))
@@ -298,3 +378,68 @@ def test_text_checker_accepts_oracle_and_rejects_wrong_rows():
     rep = C.Report()
     C.check_text_hidden(hb, extra, "bf16", table, pos, ids, kept, rep)
     assert not rep.finish().ok
+
+
+def _e2e_case(dtype, seed=12, n=40, d_in=24, d_e=16, S=5, P=9, d_v=12, d_h=14, k=3, n_keep=13):
+    rng = np.random.default_rng(seed)
+    rd = lambda a: O.round_to_dtype(a, dtype)
+    x = rd(rng.standard_normal((n, d_in)))
+    wt = rd(rng.standard_normal((d_e, d_in)) / np.sqrt(d_in))
+    K1 = rd(rng.standard_normal((S, d_e)) / np.sqrt(d_e))
+    K2 = rd(rng.standard_normal((S, P, d_e)) / np.sqrt(d_e))
+    V = rd(rng.standard_normal((S * P, d_v)))
+    D = rd(rng.standard_normal((1, n, 8)) * rng.lognormal(0, 1, (1, n, 1)))
+    H = rd(rng.standard_normal((1, n, d_h)))
+    res = O.run(x, wt[None], K1, K2, V, None, D, H, k=k, n_keep=n_keep, dtype=dtype)
+    return dict(x=x, wt=wt, K1=K1, K2=K2, V=V, D=D, H=H, k=k, n_keep=n_keep, P=P, res=res)
+
+
+def _e2e_check(c, dtype, q=None, scene=None, prim=None, w=None, kept=None, hidden=None):
+    res = c["res"]
+    enc = (lambda a: O.f64_to_bf16_bits(a)) if dtype == "bf16" else (lambda a: a.astype(np.float32))
+    rep = C.Report()
+    n = c["x"].shape[0]
+    C.check_end_to_end(c["x"], c["wt"], c["K1"], None, "dot", c["K2"], lambda rows: c["V"][rows],
+                       c["P"], c["k"], O.criticality(c["D"][0]), c["n_keep"], enc(c["H"][0]),
+                       enc(res["hidden"][0] if hidden is None else hidden), dtype,
+                       enc(res["q"][0] if q is None else q),
+                       res["scene"][0] if scene is None else scene,
+                       res["prim"][0] if prim is None else prim,
+                       (res["w"][0] if w is None else w).astype(np.float32),
+                       res["kept"][0] if kept is None else kept, rep, np.arange(n))
+    return rep.finish()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_end_to_end_check_accepts_the_oracle_and_rejects_planted_errors(dtype):
+    """check_end_to_end: the oracle's own whole-path results pass; a wrong
+    scene, a wrong primitive, a dropped kept token, a hidden row two bf16
+    steps (or 1e-4 relative) off and a q two steps off each fail."""
+    c = _e2e_case(dtype)
+    res = c["res"]
+    rep = _e2e_check(c, dtype)
+    assert rep.ok, rep
+    t = int(res["kept"][0][3])
+    sc = res["scene"][0].copy()
+    sc[t] = (sc[t] + 1) % c["K1"].shape[0]
+    assert not _e2e_check(c, dtype, scene=sc).ok
+    pr = res["prim"][0].copy()
+    pr[t, 0] = [p for p in range(c["P"]) if p not in pr[t]][0]
+    assert not _e2e_check(c, dtype, prim=pr).ok
+    kp = res["kept"][0].copy()
+    kp[3] = [i for i in range(40) if i not in kp][0]
+    assert not _e2e_check(c, dtype, kept=np.sort(kp)).ok
+    h = res["hidden"][0].copy()
+    if dtype == "bf16":
+        bits = O.f64_to_bf16_bits(h[t, :1]).astype(np.int64)
+        h[t, 0] = O.bf16_bits_to_f64(np.array([bits[0] + 2], dtype=np.uint16))[0]
+    else:
+        h[t, 0] = np.float32(h[t, 0] * (1 + 1e-4) + 1e-4)
+    assert not _e2e_check(c, dtype, hidden=h).ok
+    q = res["q"][0].copy()
+    if dtype == "bf16":
+        bits = O.f64_to_bf16_bits(q[t, :1]).astype(np.int64)
+        q[t, 0] = O.bf16_bits_to_f64(np.array([bits[0] + 2], dtype=np.uint16))[0]
+    else:
+        q[t, 0] = np.float32(q[t, 0] * (1 + 1e-3))
+    assert not _e2e_check(c, dtype, q=q).ok

@@ -1,6 +1,6 @@
 """GPU parity of the learned SKA gate (Eq. 9), the injections for its counted
 lists (prefix add, SwiGLU fusion, propagation), the text pathway (Eq. 1) and
-one whole LookME layer (Eq. 3), through the C ABI, against the CPU oracle on
+one whole LookME layer (Eq. 2), through the C ABI, against the CPU oracle on
 the same seeded inputs.
 """
 
@@ -286,7 +286,7 @@ LAYER = {
 
 @pytest.mark.parametrize("name", list(LAYER))
 def test_lookme_layer(name):
-    """One LookME layer (Eq. 3): text, image and cross-modal pathways with
+    """One LookME layer (Eq. 2): text, image and cross-modal pathways with
     their own gates, all reading the layer's inputs, added in order; against
     the oracle's recomputation from the library's decisions."""
     from tests.harness import LayerRun, check_layer_run

@@ -87,10 +87,14 @@ SMALL = {
 
 @pytest.mark.parametrize("name", list(SMALL))
 def test_small_workloads_every_token(name):
+    """Stage-wise and end-to-end checks on every token."""
+    from tests.harness import check_end_to_end_run
     wl = SMALL[name]
     _announce(f"{name}: {wl}")
     inp = make_inputs(wl, seed=3, device=DEV)
     r, rep = _run_check(inp)
+    e2e = check_end_to_end_run(r)
+    assert e2e.ok, str(e2e)
     if wl.usage != "iid" and wl.project:
         # planted clusters: layer-0 routing recovers the cluster label
         lab = inp["labels"].cpu().numpy()
@@ -99,9 +103,13 @@ def test_small_workloads_every_token(name):
 
 
 def test_tiny_f32_workload_every_token():
+    from tests.harness import check_end_to_end_run
     wl = WORKLOADS[0]
     _announce(f"config 0: {wl}")
-    _run_check(make_inputs(wl, seed=0, device=DEV))
+    r, _ = _run_check(make_inputs(wl, seed=0, device=DEV))
+    e2e = check_end_to_end_run(r)
+    assert e2e.ok, str(e2e)
+    assert e2e.decisions["e2e_hidden"] == wl.n_tokens
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -509,6 +517,9 @@ MULTISCALE = {
     "f32_ms_three": (Workload("f32_ms_three", "f32", 77, 1, 96, 64, 15, 37, 64, 96, 3, 20,
                               usage="iid", value_std=1.0), 3, None),
     "bf16_ms_image": (WORKLOADS[1].scaled(value_std=1.0), 2, 80),
+    # the multi-scale batch's shape: 23040 tokens a scale, 1024 scenes split
+    # over two scales, rows of width 1536 into hidden 2048
+    "bf16_ms_batch": (WORKLOADS[2].scaled(value_std=1.0), 2, 80),
 }
 
 
@@ -541,7 +552,7 @@ def test_multiscale_injection(name):
 def test_benchmark_workloads_sampled(cfg):
     """Full-size workloads in the benchmark's launch configuration; sampled
     tokens are checked stage-wise, the kept set in full."""
-    from tests.harness import Run, check_run
+    from tests.harness import Run, check_end_to_end_run, check_run
     wl = WORKLOADS[cfg]
     _announce(f"config {cfg}: {wl}")
     inp = make_inputs(wl, seed=cfg, device=DEV)
@@ -551,6 +562,9 @@ def test_benchmark_workloads_sampled(cfg):
     toks = np.unique(np.concatenate([rng.choice(wl.n_tokens, 80, replace=False), kept0]))
     rep = check_run(r, tokens=toks)
     assert rep.ok, str(rep)
+    # end-to-end mode: the oracle's own decisions from the original inputs
+    e2e = check_end_to_end_run(r, tokens=toks)
+    assert e2e.ok, str(e2e)
     if wl.usage != "iid":
         lab = inp["labels"].cpu().numpy()
         assert np.mean(r.scene[0].cpu().numpy() == lab) > 0.99

@@ -218,6 +218,268 @@ def test_route_cos_equals_dot_for_unit_keys_without_bias():
 
 
 # --------------------------------------------------------------------------
+# Cosine scoring (Eq. 5 and Eq. 7 in the paper's own cosine form)
+# --------------------------------------------------------------------------
+
+# integer patterns whose Euclidean norm is an integer (Pythagorean
+# quadruples and quintuples): a vector made of one of them, scaled by an exact
+# binary fraction, has a rational norm, so every cosine between two such
+# vectors is an exact rational
+_RATIONAL_NORM_PATTERNS = [(1, 2, 2), (2, 3, 6), (1, 4, 8), (4, 4, 7), (2, 6, 9), (6, 6, 7),
+                           (3, 4, 12), (2, 10, 11), (1, 12, 12), (8, 9, 12), (1, 1, 1, 1),
+                           (1, 1, 3, 5), (2, 4, 5, 6), (1, 2, 4, 10)]
+_SCALES = (0.25, 0.5, 0.75, 1.0, 1.5, 2.0, 3.0, 5.0)
+
+
+def _rational_norm_rows(rng, n, d, zero_rows=()):
+    """n rows of width d, each one pattern with random signs at random
+    positions times a random scale (exact in bf16); rows in ``zero_rows``
+    are zero.  Norms are rational and deliberately uneven."""
+    out = np.zeros((n, d))
+    for i in range(n):
+        if i in zero_rows:
+            continue
+        pat = _RATIONAL_NORM_PATTERNS[rng.integers(len(_RATIONAL_NORM_PATTERNS))]
+        pos = rng.choice(d, len(pat), replace=False)
+        out[i, pos] = np.array(pat) * rng.choice([-1.0, 1.0], len(pat))
+        out[i] *= _SCALES[rng.integers(len(_SCALES))]
+    assert np.array_equal(out, O.round_to_bf16(out))
+    return out
+
+
+def _exact_gap_ok(vals, i, j):
+    """True when the exact rationals vals[i] and vals[j] differ by more than
+    float64 can blur (no exact or near tie decided by rounding)."""
+    return abs(vals[i] - vals[j]) > Fraction(1, 10 ** 9)
+
+
+def _pin_cos_route():
+    """Level-1 under the cosine with a scene bias (Eq. 5) against exact
+    rationals, with queries and keys of uneven norms, a zero query and a zero
+    key.  Every decision whose runner-up is not within 1e-9 must match."""
+    rng = np.random.default_rng(120)
+    n, S, d = 60, 9, 8
+    q = _rational_norm_rows(rng, n, d, zero_rows=(7,))
+    K1 = _rational_norm_rows(rng, S, d, zero_rows=(4,))
+    b = rng.permutation(np.arange(-4, 5)) / 16.0        # distinct, exact
+    got = O.route(q, K1, b, score="cos")
+    want, rows = B.route_cos(q.tolist(), K1.tolist(), b.tolist())
+    checked = 0
+    for t in range(n):
+        order = sorted(range(S), key=lambda s: (-rows[t][s], s))
+        if _exact_gap_ok(rows[t], order[0], order[1]):
+            assert got[t] == want[t], (t, got[t], want[t])
+            checked += 1
+    assert checked >= n - 3
+    # the zero query scores every scene with its bias alone
+    assert got[7] == int(np.argmax(b))
+    # the scores themselves, including cos = 0 for the zero key
+    s1 = O.scene_scores(q, K1, b, score="cos")
+    for t in range(n):
+        np.testing.assert_allclose(s1[t], [float(v) for v in rows[t]], rtol=0, atol=1e-15)
+    assert np.all(s1[:, 4] == b[4])
+    return q, K1, b
+
+
+def _pin_cos_lookup():
+    """Level-2 under the cosine (Eq. 7): the top-k of exact cosines within the
+    scene and the softmax over the k selected cosines, evaluated in 40-digit
+    decimal arithmetic."""
+    rng = np.random.default_rng(121)
+    n, S, P, d, k = 30, 3, 12, 8, 4
+    q = _rational_norm_rows(rng, n, d, zero_rows=(5,))
+    K2 = np.stack([_rational_norm_rows(rng, P, d, zero_rows=(3,)) for _ in range(S)])
+    scene = rng.integers(0, S, n).astype(np.int32)
+    prim, w, top = O.lookup(q, scene, K2, k, score="cos")
+    bp, btop, alls = B.lookup_cos(q.tolist(), scene.tolist(), K2.tolist(), k)
+    checked = 0
+    for t in range(n):
+        c = alls[t]
+        order = sorted(range(P), key=lambda p: (-c[p], p))
+        # no near tie at any listed position or at the cut
+        if t != 5 and all(_exact_gap_ok(c, order[i], order[i + 1]) for i in range(k)):
+            assert prim[t].tolist() == bp[t], (t, prim[t].tolist(), bp[t])
+            np.testing.assert_allclose(top[t], [float(v) for v in btop[t]], rtol=0, atol=1e-15)
+            np.testing.assert_allclose(w[t], B.softmax_decimal(btop[t]), rtol=1e-14, atol=0)
+            checked += 1
+    assert checked >= n // 2
+    # the zero query: every cosine is 0, so the first k primitives, equal weights
+    assert prim[5].tolist() == list(range(k))
+    assert w[5].tolist() == [1.0 / k] * k
+    return q, scene, K2
+
+
+def _pin_cos_planted_angles():
+    """Closed form: keys at planted cosines beta_p to q with arbitrary norms
+    c_p give top-k = the k largest beta and weights = softmax(beta) under the
+    cosine, whatever c_p and |q|; under the dot product the weights are
+    softmax(c_p beta_p |q|) instead."""
+    rng = np.random.default_rng(122)
+    d, P, k = 48, 16, 5
+    q = rng.standard_normal(d) * 3.7
+    qh = q / np.linalg.norm(q)
+    betas = rng.permutation(np.linspace(-0.9, 0.9, P))
+    norms = rng.uniform(0.1, 10.0, P)
+    keys = np.zeros((P, d))
+    for p in range(P):
+        u = rng.standard_normal(d)
+        u -= (u @ qh) * qh
+        u /= np.linalg.norm(u)
+        keys[p] = norms[p] * (betas[p] * qh + math.sqrt(1 - betas[p] ** 2) * u)
+    prim, w, top = O.lookup(q[None], np.array([0]), keys[None], k, score="cos")
+    expect = np.argsort(-betas)[:k]
+    assert prim[0].tolist() == expect.tolist()
+    np.testing.assert_allclose(top[0], betas[expect], rtol=0, atol=1e-14)
+    bt = betas[expect]
+    np.testing.assert_allclose(w[0], np.exp(bt - bt.max()) / np.exp(bt - bt.max()).sum(),
+                               rtol=1e-13)
+    _, wd, _ = O.lookup(q[None], np.array([0]), keys[None], k, score="dot")
+    assert np.max(np.abs(wd[0] - w[0])) > 1e-2
+    # routing: planted cosines plus a bias that reverses the two best
+    K1 = keys[expect[:2]]
+    gap = float(betas[expect[0]] - betas[expect[1]])
+    assert O.route(q[None], K1, np.array([0.0, 0.0]), score="cos").tolist() == [0]
+    assert O.route(q[None], K1, np.array([0.0, 1.5 * gap]), score="cos").tolist() == [1]
+    assert O.route(q[None], K1, np.array([0.0, 0.5 * gap]), score="cos").tolist() == [0]
+
+
+def _pin_cos_scale_invariance():
+    """Scaling a query or a key by a positive factor leaves the cosine scores,
+    the decisions and the weights unchanged, while the dot-product scores
+    change."""
+    rng = np.random.default_rng(123)
+    n, S, P, d, k = 20, 6, 10, 16, 3
+    q = rng.standard_normal((n, d))
+    K1 = rng.standard_normal((S, d))
+    K2 = rng.standard_normal((S, P, d))
+    b = rng.standard_normal(S) * 0.1
+    fq = rng.uniform(0.2, 8.0, (n, 1))
+    fk1 = rng.uniform(0.2, 8.0, (S, 1))
+    fk2 = rng.uniform(0.2, 8.0, (S, P, 1))
+    s_a = O.scene_scores(q, K1, b, score="cos")
+    s_b = O.scene_scores(q * fq, K1 * fk1, b, score="cos")
+    np.testing.assert_allclose(s_a, s_b, rtol=0, atol=1e-14)
+    assert np.max(np.abs(O.scene_scores(q, K1, b) - O.scene_scores(q * fq, K1 * fk1, b))) > 1e-3
+    scene = O.route(q, K1, b, score="cos")
+    assert np.array_equal(scene, O.route(q * fq, K1 * fk1, b, score="cos"))
+    pa, wa, _ = O.lookup(q, scene, K2, k, score="cos")
+    pb, wb, _ = O.lookup(q * fq, scene, K2 * fk2, k, score="cos")
+    assert np.array_equal(pa, pb)
+    np.testing.assert_allclose(wa, wb, rtol=0, atol=1e-14)
+    _, wd1, _ = O.lookup(q, scene, K2, k, score="dot")
+    _, wd2, _ = O.lookup(q * fq, scene, K2 * fk2, k, score="dot")
+    assert np.max(np.abs(wd1 - wd2)) > 1e-3
+
+
+_COS_PINS = (_pin_cos_route, _pin_cos_lookup, _pin_cos_planted_angles, _pin_cos_scale_invariance)
+
+
+def test_route_cos_with_bias_matches_exact_rational_brute_force():
+    """Catches a query or key left unnormalised, the bias folded into the
+    cosine, and a zero vector not scoring 0."""
+    q, K1, b = _pin_cos_route()
+    # the pin discriminates: with these uneven norms the dot product routes
+    # differently for many tokens
+    assert np.sum(O.route(q, K1, b, score="dot") != O.route(q, K1, b, score="cos")) >= 10
+
+
+def test_lookup_cos_matches_exact_rational_brute_force():
+    q, scene, K2 = _pin_cos_lookup()
+    pd, _, _ = O.lookup(q, scene, K2, 4, score="dot")
+    pc, _, _ = O.lookup(q, scene, K2, 4, score="cos")
+    assert np.sum(np.any(pd != pc, axis=1)) >= 5
+
+
+def test_cos_planted_angles_closed_form():
+    _pin_cos_planted_angles()
+
+
+def test_cos_scale_invariance_and_dot_sensitivity():
+    _pin_cos_scale_invariance()
+
+
+def _mut_scene_scores_q_raw(q, scene_keys, bias=None, score="dot"):
+    if score != "cos":
+        return _REAL_SCENE_SCORES(q, scene_keys, bias, score)
+    s = q @ O._unit_rows(scene_keys).T
+    return s if bias is None else s + bias[None, :]
+
+
+def _mut_scene_scores_k_raw(q, scene_keys, bias=None, score="dot"):
+    if score != "cos":
+        return _REAL_SCENE_SCORES(q, scene_keys, bias, score)
+    s = O._unit_rows(q) @ scene_keys.T
+    return s if bias is None else s + bias[None, :]
+
+
+def _mut_scene_scores_bias_inside(q, scene_keys, bias=None, score="dot"):
+    if score != "cos":
+        return _REAL_SCENE_SCORES(q, scene_keys, bias, score)
+    num = q @ scene_keys.T + (0.0 if bias is None else bias[None, :])
+    nq = np.linalg.norm(q, axis=1)[:, None]
+    nk = np.linalg.norm(scene_keys, axis=1)[None, :]
+    with np.errstate(invalid="ignore", divide="ignore"):
+        return np.where((nq > 0) & (nk > 0), num / (nq * nk), 0.0)
+
+
+def _mut_prim_scores_q_raw(q_t, prim_keys_s, score="dot"):
+    if score != "cos":
+        return _REAL_PRIM_SCORES(q_t, prim_keys_s, score)
+    return O._unit_rows(prim_keys_s) @ q_t
+
+
+def _mut_prim_scores_k_raw(q_t, prim_keys_s, score="dot"):
+    if score != "cos":
+        return _REAL_PRIM_SCORES(q_t, prim_keys_s, score)
+    return prim_keys_s @ O._unit_rows(q_t[None, :])[0]
+
+
+_REAL_SCENE_SCORES = O.scene_scores
+_REAL_PRIM_SCORES = O.primitive_scores
+
+
+@pytest.mark.parametrize("target,mutant", [
+    ("scene_scores", _mut_scene_scores_q_raw),
+    ("scene_scores", _mut_scene_scores_k_raw),
+    ("scene_scores", _mut_scene_scores_bias_inside),
+    ("primitive_scores", _mut_prim_scores_q_raw),
+    ("primitive_scores", _mut_prim_scores_k_raw),
+])
+def test_cos_pins_kill_planted_mistakes(monkeypatch, target, mutant):
+    """Each planted mistake in the oracle's cosine branch (query not
+    normalised, keys not normalised, bias inside the cosine) makes at least
+    one of the cosine pins fail."""
+    monkeypatch.setattr(O, target, mutant)
+    failed = 0
+    for pin in _COS_PINS:
+        try:
+            pin()
+        except AssertionError:
+            failed += 1
+    assert failed >= 1, f"no cosine pin catches the planted mistake {mutant.__name__}"
+
+
+def test_scene_keys_are_primitive_means_eq4():
+    """Eq. 4: e_img[j] = (1/N_p) sum_p E[j, p, :], against exact rationals
+    (S != P != d catches a mean over the wrong axis), a scene of identical
+    primitives (its key is that primitive) and invariance under relabelling
+    the primitives of a scene."""
+    rng = np.random.default_rng(124)
+    S, P, d = 3, 7, 5
+    E = _bf16_values(rng, (S, P, d))
+    got = O.scene_keys_from_primitives(E)
+    want = B.scene_means(E.reshape(S * P, d).tolist(), P)
+    assert got.shape == (S, d)
+    for j in range(S):
+        np.testing.assert_allclose(got[j], [float(v) for v in want[j]], rtol=1e-15, atol=0)
+    E2 = E.copy()
+    E2[1] = E[1, 4]
+    np.testing.assert_array_equal(O.scene_keys_from_primitives(E2)[1], E[1, 4])
+    perm = rng.permutation(P)
+    np.testing.assert_allclose(O.scene_keys_from_primitives(E[:, perm]), got, rtol=1e-15)
+
+
+# --------------------------------------------------------------------------
 # Level-2 lookup (Eq. 6-7, configured form)
 # --------------------------------------------------------------------------
 
@@ -862,7 +1124,7 @@ def test_run_multiscale_routes_each_scale_within_its_partition():
 
 
 # --------------------------------------------------------------------------
-# Learned SKA gate (Eq. 9), text pathway (Eq. 1), one LookME layer (Eq. 3)
+# Learned SKA gate (Eq. 9), text pathway (Eq. 1), one LookME layer (Eq. 2)
 # --------------------------------------------------------------------------
 
 def test_gate_matches_exact_rational_brute_force_with_exact_zeros():
