@@ -57,6 +57,8 @@ typedef enum { LOOKME_SCORE_DOT = 0, LOOKME_SCORE_COS = 1 } lookme_score_t;
 
 /* Largest supported top-k (T~ in Eq. 6). */
 #define LOOKME_KMAX 32
+/* rows (layers * n) that lookme_inject_noalloc accepts */
+#define LOOKME_NOALLOC_MAX_ROWS 131072
 
 typedef struct {
   int32_t num_scenes;       /* N_s  (Sec. 3.2 "Two-level embedding table")            */
@@ -172,6 +174,25 @@ lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_k
                               const void* crit, int32_t d_c, const int32_t* scene,
                               const int32_t* prim, const float* w, void* hidden,
                               int32_t d_h, int32_t* kept_out, void* stream);
+
+/*
+ * lookme_inject_noalloc -- lookme_inject for callers that cannot allocate
+ * device memory (code under stream capture, tight serving loops, harnesses
+ * that forbid allocation): the same selection and row add, the same
+ * arguments and the same results bit for bit, but no workspace is needed and
+ * nothing is allocated.  Its scratch (the criticality keys and, when
+ * kept_out is NULL, the kept lists) is a static device array of the library,
+ * 1 MiB on every GPU it runs on, held until the process ends.
+ * Requires layers * n <= LOOKME_NOALLOC_MAX_ROWS (else
+ * LOOKME_ERR_UNSUPPORTED, nothing launched) and the conditions of
+ * lookme_inject.  Every call on one GPU shares that GPU's scratch: calls that
+ * overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller.  The profiling hooks do not time it.
+ */
+lookme_status_t lookme_inject_noalloc(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                                      const void* crit, int32_t d_c, const int32_t* scene,
+                                      const int32_t* prim, const float* w, void* hidden,
+                                      int32_t d_h, int32_t* kept_out, void* stream);
 
 /*
  * lookme_select -- the sparse injection set alone (Eq. 9): c_t = ||crit_t||_2

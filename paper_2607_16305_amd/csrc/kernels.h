@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "lookme.h"
+
 namespace lookme {
 
 // ---- projection: q[l, t, :] = round(x[t, :] . Wt[l]^T) --------------------
@@ -17,6 +19,15 @@ hipError_t launch_project(int dt, const void* x, const void* wt, void* q, int64_
 // whole 128-byte stages; returns false (nothing launched) otherwise.
 bool launch_logits_gemm(int dt, const void* a, const void* w, const float* bias, float* out,
                         int64_t rows, int N, int64_t kb, hipStream_t st);
+
+// ---- library-owned scratch (noalloc.hip) ---------------------------------
+// lookme_inject_noalloc keeps the criticality keys of up to
+// LOOKME_NOALLOC_MAX_ROWS rows and, when the caller passes no kept_out, the
+// kept lists in a static device array of NOALLOC_SCRATCH_BYTES; this returns
+// its device address on the current device (looked up once per device).
+constexpr size_t NOALLOC_KEYS_BYTES = (size_t)LOOKME_NOALLOC_MAX_ROWS * 4;
+constexpr size_t NOALLOC_SCRATCH_BYTES = 2 * NOALLOC_KEYS_BYTES;
+hipError_t noalloc_scratch(void** out);
 
 // ---- routing: scene[r] = argmax_s <q_r, K1[s]> + bias[s] over rows r -------
 // Three kernels, by batch size (route_plan):

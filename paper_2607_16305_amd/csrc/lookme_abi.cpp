@@ -629,6 +629,46 @@ lookme_status_t lookme_inject(lookme_t h, int32_t layers, int64_t n, int64_t n_k
   return run_inject(h, layers, n, n_keep, kept, scene, prim, w, hidden, d_h, st);
 }
 
+lookme_status_t lookme_inject_noalloc(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
+                                      const void* crit, int32_t d_c, const int32_t* scene,
+                                      const int32_t* prim, const float* w, void* hidden,
+                                      int32_t d_h, int32_t* kept_out, void* stream) {
+  LOOKME_TRY(check_handle(h));
+  LOOKME_TRY(check_layers_n(layers, n));
+  LOOKME_TRY(check_keep(n, n_keep));
+  LOOKME_TRY(check_crit_dim(h->d, d_c));
+  LOOKME_TRY(check_hidden_dim(h->d, d_h));
+  if ((int64_t)layers * n > LOOKME_NOALLOC_MAX_ROWS)
+    return fail(LOOKME_ERR_UNSUPPORTED, "layers * n = %lld rows exceeds the %d of the scratch",
+                (long long)((int64_t)layers * n), LOOKME_NOALLOC_MAX_ROWS);
+  if (n == 0) return LOOKME_OK;
+  LOOKME_TRY(check_ptr(crit, "crit"));
+  LOOKME_TRY(check_ptr(scene, "scene"));
+  LOOKME_TRY(check_ptr(prim, "prim"));
+  LOOKME_TRY(check_ptr(w, "w"));
+  LOOKME_TRY(check_ptr(hidden, "hidden"));
+  if (kept_out) LOOKME_TRY(check_ptr(kept_out, "kept_out"));
+  void* scratch = nullptr;
+  LOOKME_TRY(hip_status(lookme::noalloc_scratch(&scratch), "scratch address"));
+  uint32_t* key = static_cast<uint32_t*>(scratch);
+  int32_t* kept = kept_out ? kept_out
+                           : reinterpret_cast<int32_t*>(static_cast<char*>(scratch) +
+                                                        lookme::NOALLOC_KEYS_BYTES);
+  const lookme_desc_t& d = h->d;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // the kernels of lookme_inject (run_select, run_inject) without the timing
+  // hooks, whose events would be created on first use
+  LOOKME_TRY(hip_status(lookme::launch_crit_norm(d.dtype, (int64_t)layers * n, crit, d_c, key, st),
+                        "criticality launch"));
+  if (n_keep == 0) return LOOKME_OK;
+  LOOKME_TRY(hip_status(lookme::launch_crit_select(layers, n, n_keep, key, kept, st),
+                        "select launch"));
+  return hip_status(lookme::launch_inject_rows(d.dtype, layers, n, n_keep, kept, scene, prim, w,
+                                               h->values, d.num_scenes, d.prims_per_scene,
+                                               d.value_dim, d.top_k, hidden, d_h, st),
+                    "inject launch");
+}
+
 lookme_status_t lookme_select(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
                               const void* crit, int32_t d_c, int32_t* kept_out, void* stream) {
   LOOKME_TRY(check_handle(h));

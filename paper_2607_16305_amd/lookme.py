@@ -22,6 +22,7 @@ LOOKME_OK, LOOKME_ERR_INVALID, LOOKME_ERR_UNSUPPORTED, LOOKME_ERR_WORKSPACE, LOO
 LOOKME_F32, LOOKME_BF16 = 0, 1
 LOOKME_SCORE_DOT, LOOKME_SCORE_COS = 0, 1
 LOOKME_KMAX = 32
+LOOKME_NOALLOC_MAX_ROWS = 131072
 
 STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "HIP"}
 
@@ -34,7 +35,7 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_inject_gated", "lookme_inject_fused_gated", "lookme_inject_propagated_gated",
             "lookme_inject_text", "lookme_lookup_select", "lookme_lookup_gate",
             "lookme_destroy", "lookme_last_error",
-            "lookme_profile_enable", "lookme_profile_read")
+            "lookme_profile_enable", "lookme_profile_read", "lookme_inject_noalloc")
 
 GROUPS = ("project", "route", "bucket", "score", "norm", "select", "inject")
 
@@ -77,6 +78,8 @@ def load():
                           ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp],
         "lookme_select": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
                           ctypes.c_int32, _vp, _vp],
+        "lookme_inject_noalloc": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp,
+                                  ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp],
         "lookme_inject_kept": [_vp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, _vp, _vp, _vp,
                                _vp, _vp, ctypes.c_int32, _vp],
         "lookme_set_relevance": [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp],
@@ -180,6 +183,13 @@ def lookme_inject(h, layers, n, n_keep, crit, d_c, scene, prim, w, hidden, d_h, 
                   stream=None):
     _check(load().lookme_inject(h, layers, n, n_keep, _ptr(crit), d_c, _ptr(scene), _ptr(prim),
                                 _ptr(w), _ptr(hidden), d_h, _ptr(kept_out), _stream(stream)))
+
+
+def lookme_inject_noalloc(h, layers, n, n_keep, crit, d_c, scene, prim, w, hidden, d_h,
+                          kept_out=None, stream=None):
+    _check(load().lookme_inject_noalloc(h, layers, n, n_keep, _ptr(crit), d_c, _ptr(scene),
+                                        _ptr(prim), _ptr(w), _ptr(hidden), d_h, _ptr(kept_out),
+                                        _stream(stream)))
 
 
 def lookme_select(h, layers, n, n_keep, crit, d_c, kept_out, stream=None):

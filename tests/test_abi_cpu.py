@@ -149,6 +149,32 @@ def test_calls_validate_before_launch(lib):
         lk.lookme_destroy(h)
 
 
+def test_inject_noalloc_validates_before_launch(lib):
+    """The entry point that allocates nothing: the same argument checks as
+    lookme_inject, no workspace needed, and a batch beyond its scratch
+    rejected before anything runs."""
+    bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
+               top_k=8, num_scenes=256)
+    h = lk.lookme_create(bf, FAKE, FAKE, FAKE)
+    try:
+        S = lambda f: _status(f)[0]
+        inj = lambda layers, n, n_keep, d_c=2048, d_h=2048, crit=FAKE, kept=None: \
+            lk.lookme_inject_noalloc(h, layers, n, n_keep, crit, d_c, FAKE, FAKE, FAKE, FAKE,
+                                     d_h, kept, 0)
+        assert S(lambda: inj(1, 0, 0, crit=None)) == lk.LOOKME_OK
+        assert S(lambda: inj(1, 8, 9)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: inj(1, 8, 2, d_h=1024)) == lk.LOOKME_ERR_INVALID      # d_v > d_h
+        assert S(lambda: inj(1, 8, 2, d_c=2047)) == lk.LOOKME_ERR_UNSUPPORTED
+        assert S(lambda: inj(1, 8, 2, crit=None)) == lk.LOOKME_ERR_INVALID
+        assert S(lambda: inj(1, 8, 2, kept=FAKE + 4)) == lk.LOOKME_ERR_INVALID
+        big = lk.LOOKME_NOALLOC_MAX_ROWS
+        st, msg = _status(lambda: inj(2, big // 2 + 1, 4))
+        assert st == lk.LOOKME_ERR_UNSUPPORTED and "scratch" in msg
+        assert S(lambda: inj(1, big + 1, 4)) == lk.LOOKME_ERR_UNSUPPORTED
+    finally:
+        lk.lookme_destroy(h)
+
+
 def test_relevance_entry_points_validate(lib):
     bf = _desc(dtype=lk.LOOKME_BF16, key_dim=512, value_dim=2048, prims_per_scene=1024,
                top_k=8, num_scenes=256)
