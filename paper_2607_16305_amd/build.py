@@ -1,6 +1,6 @@
 """Build liblookme.so (the C-ABI library and its gfx950 kernels) in-tree.
 
-    python -m paper_2607_16305_amd.build [--jobs N]
+    python -m paper_2607_16305_amd.build [--jobs N] [--incremental]
 
 Every source under csrc/ is compiled by hipcc for gfx950 only, then linked
 into paper_2607_16305_amd/liblookme.so next to this file.
@@ -37,8 +37,26 @@ def sources():
                   if f.endswith((".hip", ".cpp")))
 
 
-def _compile(src: str) -> str:
+def _inputs_key(src: str) -> str:
+    """Hash of what an object depends on: the flags, the source and every
+    header of the library (conservative: any header change rebuilds all)."""
+    import hashlib
+    h = hashlib.sha256(" ".join(COMMON_FLAGS).encode())
+    for f in [src] + sorted(os.path.join(d, x) for d in (CSRC, os.path.join(ROOT, "include"))
+                            for x in os.listdir(d) if x.endswith(".h")):
+        with open(f, "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()
+
+
+def _compile(src: str, incremental: bool = False) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
+    key_file = obj + ".key"
+    key = _inputs_key(src)
+    if incremental and os.path.exists(obj) and os.path.exists(key_file):
+        with open(key_file) as fh:
+            if fh.read() == key:
+                return obj
     cmd = [HIPCC, *COMMON_FLAGS, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
@@ -47,15 +65,21 @@ def _compile(src: str) -> str:
         raise RuntimeError(f"hipcc failed for {src}:\n{err}")
     if err.strip():
         sys.stderr.write(err + "\n")
+    with open(key_file, "w") as fh:
+        fh.write(key)
     return obj
 
 
-def build(jobs: int | None = None) -> str:
+def build(jobs: int | None = None, incremental: bool = False) -> str:
+    """Compile every source (or, with ``incremental``, only those whose
+    inputs changed since their object was built) and link the library."""
     os.makedirs(BUILD, exist_ok=True)
     srcs = sources()
     jobs = jobs or min(len(srcs), max(1, (os.cpu_count() or 2) - 1))
+    # the slowest source first, so that it does not start last
+    srcs.sort(key=lambda f: -os.path.getsize(f))
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(_compile, srcs))
+        objs = list(ex.map(lambda f: _compile(f, incremental), srcs))
     tmp = LIB + ".tmp"
     # -z defs: an unresolved symbol (say a kernel stub that was never
     # instantiated) fails the link instead of the first load
@@ -70,4 +94,7 @@ def build(jobs: int | None = None) -> str:
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=None)
-    print(build(ap.parse_args().jobs))
+    ap.add_argument("--incremental", action="store_true",
+                    help="recompile only sources whose inputs changed")
+    args = ap.parse_args()
+    print(build(args.jobs, args.incremental))

@@ -13,6 +13,8 @@
 // share a row are merged in key order.  When a batch has few row blocks the
 // key tiles are split over several workgroups and the partial arg maxima
 // meet in route_partial (route_merge.h).
+#include <type_traits>
+
 #include "common.h"
 #include "dtl.h"
 #include "kernels.h"
@@ -75,32 +77,47 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
     s_bias[i] = (a.bias != nullptr && key < a.S) ? a.bias[key] : 0.f;
   }
 
-  // load b of a stage covers tile rows [trow - lane / LPR, + RPI): the query
-  // rows come first, then the 256 key rows of the stage's tile; rows past
-  // either operand are clamped into it (they feed no stored result)
-  int trow[S::PER_WAVE], chunk[S::PER_WAVE];
+  // First key of tile t: a ragged last tile is moved back to end at the
+  // last scene, so every key row it reads exists; its keys below t * 256
+  // repeat the previous tile's and are masked in the epilogue.  With fewer
+  // scenes than a tile there is one tile, at 0.
+  auto tile_start = [&](int t) { return a.S < S::BN ? 0 : min(t * S::BN, a.S - S::BN); };
+  // load b of a stage covers tile rows [(wv PER_WAVE + b) RPI, + RPI): the
+  // query rows come first, then the 256 key rows of the stage's tile.  RPI
+  // divides BM, so a load reads either query rows or key rows: the choice is
+  // uniform over the wave, and the address is a uniform base (operand, row
+  // block or key tile, K stage) plus a 32-bit lane offset fixed for the
+  // launch (both operands are far below 4 GiB).  Rows past either operand
+  // are clamped into it (they feed no stored result); only a ragged last key
+  // tile needs its offsets clamped again.
+  // lane offset of load b from its base: the row block's first query row
+  // (query loads) or the key tile's first key row (key loads)
+  uint32_t off[S::PER_WAVE];
 #pragma unroll
   for (int b = 0; b < S::PER_WAVE; ++b) {
-    trow[b] = (wv * S::PER_WAVE + b) * S::RPI + lane / S::LPR;
-    chunk[b] = (lane % S::LPR) ^ blk_swz<KB>(trow[b] & 15);
+    const int row0 = (wv * S::PER_WAVE + b) * S::RPI;       // uniform
+    const int trow = row0 + lane / S::LPR;
+    const uint32_t chunk = (uint32_t)(((lane % S::LPR) ^ blk_swz<KB>(trow & 15)) * 16);
+    if (row0 < S::BM) {
+      const int64_t r = min<int64_t>(m0 + trow, a.rows - 1) - m0;   // >= 0: m0 < rows
+      off[b] = (uint32_t)(r * a.k_bytes) + chunk;
+    } else {
+      // fewer scenes than a tile: one tile, rows past the last scene read it
+      const int kr = a.S < S::BN ? min(trow - S::BM, a.S - 1) : trow - S::BM;
+      off[b] = (uint32_t)(kr * a.k_bytes) + chunk;
+    }
   }
+  const char* q_base = a.q + m0 * a.k_bytes;
   auto issue = [&](int sigma) {
     const int sg = sigma < total ? sigma : total - 1;   // past the end: a harmless reload
     const int tile = kt0 + sg / nst, s = sg % nst;
     char* dst = lds[sigma % NS];
+    const char* k_base = a.keys + (int64_t)tile_start(tile) * a.k_bytes + s * KB;
+    const char* qs_base = q_base + s * KB;
 #pragma unroll
     for (int b = 0; b < S::PER_WAVE; ++b) {
-      const char* src;
-      if (trow[b] < S::BM) {
-        int64_t r = m0 + trow[b];
-        r = r < a.rows ? r : a.rows - 1;
-        src = a.q + r * a.k_bytes;
-      } else {
-        int r = tile * S::BN + trow[b] - S::BM;
-        r = r < a.S ? r : a.S - 1;
-        src = a.keys + (int64_t)r * a.k_bytes;
-      }
-      load_lds16(src + (int64_t)s * KB + chunk[b] * 16, dst + (wv * S::PER_WAVE + b) * 1024);
+      const bool is_q = (wv * S::PER_WAVE + b) * S::RPI < S::BM;   // uniform
+      load_lds16((is_q ? qs_base : k_base) + off[b], dst + (wv * S::PER_WAVE + b) * 1024);
     }
   };
 
@@ -132,39 +149,59 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
     asm volatile("" ::: "memory");
     issue(sigma + NS - 1);
     const char* buf = lds[sigma % NS];
+    // the first stage of a tile starts its accumulators from zero (the MFMA
+    // takes a zero operand; no register is cleared)
+    auto stage = [&](auto first) {
 #pragma unroll
-    for (int ks = 0; ks < KSL; ++ks) {
-      u32x4_t fa[MI], fb[NJ];
+      for (int ks = 0; ks < KSL; ++ks) {
+        u32x4_t fa[MI], fb[NJ];
 #pragma unroll
-      for (int i = 0; i < MI; ++i) fa[i] = read_frag<KB>(buf, wm + 16 * i, ks, n16, g);
+        for (int i = 0; i < MI; ++i) fa[i] = read_frag<KB>(buf, wm + 16 * i, ks, n16, g);
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_chunk<DT>(fa[i], fb[j], acc[i][j]);
-    }
-    if (sigma % nst == nst - 1) {
-      // the tile is complete: the lane holds rows wm + 16 i + 4 g + r and
-      // keys tile * 256 + wn + 16 j + n16 (increasing in j: '>' keeps the first)
-      const int tl = sigma / nst;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        const int kin = tl * S::BN + wn + 16 * j + n16;   // index within the unit's keys
-        const int key = kt0 * S::BN + kin;
-        const float b = s_bias[kin];
+        for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float v = key < a.S ? acc[i][j][r] + b : -__builtin_inff();
-            if (v > bs[i][r]) {
-              bs[i][r] = v;
-              bi[i][r] = key;
-            }
-            acc[i][j][r] = 0.f;
-          }
+          for (int j = 0; j < NJ; ++j)
+            acc[i][j] = mfma_chunk<DT>(fa[i], fb[j],
+                                       (decltype(first)::value && ks == 0)
+                                           ? f32x4_t{0.f, 0.f, 0.f, 0.f} : acc[i][j]);
       }
+    };
+    if (sigma % nst == 0) stage(std::true_type{});
+    else stage(std::false_type{});
+    if (sigma % nst == nst - 1) {
+      // the tile is complete: the lane holds rows wm + 16 i + 4 g + r and
+      // keys key0 + 16 j (increasing in j, and above every earlier tile's,
+      // so a strict '>' keeps the lowest key on exact ties).  Keys past the
+      // last scene (a ragged last tile) get a bias of -inf.
+      const int tl = sigma / nst;
+      const int tile = kt0 + tl;
+      const int key0 = tile_start(tile) + wn + n16;   // key of j = 0
+      float bj[NJ];
+      int kj[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        kj[j] = key0 + 16 * j;
+        bj[j] = s_bias[max(kj[j] - kt0 * S::BN, 0)];
+      }
+      if ((tile + 1) * S::BN > a.S) {
+        // ragged last tile: keys already scored by the previous tile, and
+        // with fewer scenes than a tile the rows past the last scene
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          if (kj[j] < tile * S::BN || kj[j] >= a.S) bj[j] = -__builtin_inff();
+      }
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const float v = acc[i][j][r] + bj[j];
+            bi[i][r] = v > bs[i][r] ? kj[j] : bi[i][r];
+            bs[i][r] = fmaxf(bs[i][r], v);
+          }
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave

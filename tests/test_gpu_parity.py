@@ -112,12 +112,15 @@ def test_tiny_f32_workload_every_token():
     assert e2e.decisions["e2e_hidden"] == wl.n_tokens
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_integer_scores_tie_break_exactly(dtype):
+@pytest.mark.parametrize("dtype,n,S", [("bf16", 211, 7), ("f32", 211, 7), ("bf16", 4500, 300),
+                                       ("f32", 4400, 600)])
+def test_integer_scores_tie_break_exactly(dtype, n, S):
     """Exact integer scores: every tie (scene, primitive, kept token) must go
     to the lowest index, with no tolerance and no exemption."""
     _announce(f"integer ties {dtype}")
-    inp = make_integer_inputs(n=211, S=7, P=45, d_e=128, d_v=32, d_h=48, k=6, n_keep=70,
+    # n >= 4096: routing on the matrix-core tile kernel, whose last key tile
+    # is ragged (moved back to end at the last scene)
+    inp = make_integer_inputs(n=n, S=S, P=45, d_e=128, d_v=32, d_h=48, k=6, n_keep=70,
                               seed=5, dtype=dtype, device=DEV, layers=2)
     _, rep = _run_check(inp)
     assert not rep.exemptions, rep.exemptions
@@ -136,6 +139,10 @@ SPLIT_ROUTE = {
     # fp32, 2 key tiles (256 + 44) over 2 workgroups
     "tiles_f32": (Workload("f32_tile_route", "f32", 4200, 1, 128, 128, 300, 16, 32, 32, 4, 20,
                            usage="iid"), False),
+    # 313 row blocks, 4 key tiles (the last of 232 keys, read from key 744 on)
+    # in 2 ranges of 2 tiles: a workgroup crosses into the ragged tile
+    "tiles_multi_bias": (Workload("bf16_tile_route_multi", "bf16", 40000, 1, 128, 128, 1000, 4,
+                                  16, 16, 2, 10, usage="uniform"), True),
 }
 
 
