@@ -18,6 +18,10 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 __device__ __forceinline__ void load_lds16(const void* src, char* lds_dst) {
   __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)lds_dst, 16, 0, 0);
 }
+// The same with the nontemporal hint (data read once: the Level-2 keys).
+__device__ __forceinline__ void load_lds16_nt(const void* src, char* lds_dst) {
+  __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)lds_dst, 16, 0, 2);
+}
 
 // chunk c of row r of a block sits in slot c ^ blk_swz(r): rows that share a
 // bank window get distinct slots for one chunk index.  For 128-byte rows,

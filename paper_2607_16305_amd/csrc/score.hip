@@ -241,6 +241,75 @@ __device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, i
 }
 
 // ---------------------------------------------------------------------------
+// Level-2 key blocks in LDS
+// ---------------------------------------------------------------------------
+// A 16-key block of a scene (16 consecutive key rows: 16 row_bytes contiguous
+// bytes, row_bytes = 64 ks) is copied straight from global memory into an
+// LDS image by ks load instructions of one KiB each: instruction i reads the
+// block's bytes [1024 i, 1024 i + 1024), a whole contiguous KiB, with the
+// nontemporal hint (every key is read once).  That form streams from HBM at
+// ~7 TB/s on this chip, against ~6.1 TB/s for 16 rows x 64 bytes an
+// instruction (the operand order), measured at the Zipf workload's shape.
+// Lane L's 16 bytes land at image byte 1024 i + 16 L, i.e. row
+// r = (64 i + L) / C, slot s = (64 i + L) % C (C = 4 ks chunks a row), and the
+// lane reads chunk s ^ swz(r) of that row: the chunks of a row are permuted
+// inside groups of G (16 when C is a multiple of 16), so that the fragment
+// reads (16 rows, one chunk index) hit distinct banks.  The operand fragment
+// of lane (g, n) at step j is row n, chunk 4 j + g, at image byte
+// n row_bytes + ((4 j + g) ^ swz(n)) 16.
+struct KeyImage {
+  int C;         // chunks a row
+  int G;         // swizzle group (a power of two dividing C, at most 16)
+  int64_t rb;    // row bytes
+  __device__ __forceinline__ int swz(int r) const { return r & (G - 1); }
+  // byte of the block that lane L of load instruction i reads (row r of the
+  // image; rr: the key row actually read, r unless clamped)
+  __device__ __forceinline__ uint32_t src_off(int i, int L, int rr) const {
+    const int e = 64 * i + L, r = e / C, sl = e - r * C;
+    return (uint32_t)(rr * rb) + (uint32_t)((sl ^ swz(r)) * 16);
+  }
+  __device__ __forceinline__ int row_of(int i, int L) const { return (64 * i + L) / C; }
+  __device__ __forceinline__ uint32_t frag_off(int j, int g, int n) const {
+    return (uint32_t)(n * rb) + (uint32_t)((((4 * j + g) ^ swz(n))) * 16);
+  }
+};
+
+template <int KS, bool MASKED>
+__device__ __forceinline__ KeyImage key_image(const ScoreParams& a) {
+  KeyImage im;
+  im.rb = a.row_bytes;
+  im.C = MASKED ? 4 * a.ks : 4 * KS;
+  const int low = im.C & -im.C;
+  im.G = low < 16 ? low : 16;
+  return im;
+}
+
+// Loads the block of key rows [row0, row0 + 16) (rows from kend on read row
+// kend - 1: they are masked by index when scored) into `img`: instructions
+// i = i0, i0 + istep, ... < ks.  off[t] holds src_off for instruction
+// i0 + istep t of an unclamped block.
+template <int KS, bool MASKED, int NT>
+__device__ __forceinline__ void load_key_block(const KeyImage& im, const ScoreParams& a,
+                                               const char* keys, int row0, int kend,
+                                               const uint32_t (&off)[NT], int i0, int istep,
+                                               char* img, int lane) {
+  const char* src = keys + (int64_t)row0 * im.rb;
+  const bool ragged = row0 + 16 > kend;   // uniform
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int i = i0 + istep * t;
+    if (MASKED && i >= a.ks) break;
+    uint32_t o = off[t];
+    if (ragged) {
+      const int r = im.row_of(i, lane);
+      const int rr = row0 + r < kend ? r : kend - 1 - row0;
+      o = im.src_off(i, lane, rr);
+    }
+    load_lds16_nt(src + o, img + i * 1024);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Streaming mode: <= 16 rows, key blocks split over the waves
 // ---------------------------------------------------------------------------
 // key0, nkeys: the unit's key range (routing may split the keys; Level-2
@@ -357,6 +426,117 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
   if (L == 0 && t < nr) write_row<LOOKUP, KL>(a, row_id<LOOKUP>(a, begin, t), top_s, top_i);
 }
 
+// Level-2 streaming units with the key blocks staged in LDS (KS <= 16): as
+// stream_unit, each wave scores its quarter of the scene's keys against the
+// unit's <= 16 query rows, but every block goes straight from global memory
+// into the wave's LDS block image (load_key_block: contiguous KiB loads,
+// nontemporal).  As soon as a block's fragments are in registers the next
+// block's loads are issued into the image, so they fly while the block is
+// multiplied and folded.  The waves never wait for each other until the
+// merge.  LDS: 4 waves x KS KiB, so that two workgroups fit a CU.
+template <int DT, int KS, bool MASKED, int KL, bool COS>
+__device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem, int64_t begin,
+                                                int nr, const char* keys) {
+  constexpr int NL = SC_WAVES * 4;   // candidate lists per query row
+  constexpr int BLOCK = KS * 1024;
+  static_assert(KS <= 16, "fragments of a block held in registers");
+  float (*cand_s)[16][KL] = reinterpret_cast<float (*)[16][KL]>(smem);
+  int (*cand_i)[16][KL] = reinterpret_cast<int (*)[16][KL]>(smem + NL * 16 * KL * 4);
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = lane & 15, g = lane >> 4;
+  const int nkeys = a.nkeys;
+  const KeyImage im = key_image<KS, MASKED>(a);
+  char* img = smem + wv * BLOCK;
+
+  u32x4_t qb[KS];
+  load_row_frags<KS, MASKED>(qb, a.q + row_id<true>(a, begin, n < nr ? n : nr - 1) * a.row_bytes,
+                             g, a.ks);
+
+  const int nblk = (nkeys + 15) >> 4;
+  const int bpw = (nblk + SC_WAVES - 1) / SC_WAVES;
+  const int kb0 = wv * bpw;
+  const int kb1 = min(nblk, kb0 + bpw);
+  const int kend = min(nkeys, kb1 * 16);
+
+  uint32_t off[KS];
+#pragma unroll
+  for (int i = 0; i < KS; ++i) off[i] = (!MASKED || i < a.ks) ? im.src_off(i, lane, im.row_of(i, lane)) : 0u;
+  // fragment offsets inside the image: step j = 4 m + t at fbase[t] + 256 m
+  // (C a multiple of 16: the swizzle only permutes the low two bits of j)
+  uint32_t fbase[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) fbase[t] = im.frag_off(t, g, n);
+
+  float ls[KL];
+  int li[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
+
+  auto issue = [&](int blk) {
+    load_key_block<KS, MASKED, KS>(im, a, keys, blk * 16, kend, off, 0, 1, img, lane);
+  };
+
+  // the query fragments land before the key stream starts
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  float qinv = 0.f;
+  if constexpr (COS) {
+    float qsq = 0.f;
+#pragma unroll
+    for (int j = 0; j < KS; ++j)
+      if (!MASKED || j < a.ks) qsq = chunk_sumsq<DT>(qb[j], qsq);
+    qinv = inv_norm(sum_lane_groups(qsq));
+  }
+  if (kb0 < kb1) issue(kb0);
+  for (int blk = kb0; blk < kb1; ++blk) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // block blk is in the image
+    u32x4_t kf[KS];
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      if (!MASKED || j < a.ks) {
+        const uint32_t fo = MASKED ? im.frag_off(j, g, n) : fbase[j & 3] + 256 * (j >> 2);
+        kf[j] = *reinterpret_cast<const u32x4_t*>(img + fo);
+      }
+    }
+    // every read of the image has returned: refill it with the next block
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (blk + 1 < kb1) issue(blk + 1);
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    float knsq = 0.f;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      if (!MASKED || j < a.ks) {
+        acc = mfma_chunk<DT>(kf[j], qb[j], acc);
+        if constexpr (COS) knsq = chunk_sumsq<DT>(kf[j], knsq);
+      }
+    }
+    if constexpr (COS) acc = cos_scale(acc, qinv, sum_lane_groups(knsq), g);
+    fold_scores<true, KL>(acc, blk, g, kend, nullptr, ls, li);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
+
+  // merge: thread (t, L) owns list L of query row t (the lists reuse the
+  // images, so every wave must be done with its own first)
+  __syncthreads();
+  const int list = wv * 4 + g;
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    cand_s[list][n][e] = ls[e];
+    cand_i[list][n][e] = li[e];
+  }
+  __syncthreads();
+  const int t = threadIdx.x / NL;
+  const int L = threadIdx.x % NL;
+  float ms[KL];
+  int mi[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) { ms[e] = cand_s[L][t][e]; mi[e] = cand_i[L][t][e]; }
+  float top_s[KL];
+  int top_i[KL];
+  merge_lists<KL, 4>(ms, mi, a.k, 1, top_s, top_i);
+  if (L == 0 && t < nr) write_row<true, KL>(a, row_id<true>(a, begin, t), top_s, top_i);
+}
+
 // ---------------------------------------------------------------------------
 // Shared mode: up to 128 rows, every key block staged once in LDS
 // ---------------------------------------------------------------------------
@@ -367,6 +547,10 @@ constexpr int shared_nbuf(int ks) {
          : SH_LDS_BYTES / (ks * 1024) > 8 ? 8
                                           : SH_LDS_BYTES / (ks * 1024);
 }
+// Level-2: block images in the ring of a shared unit.  Up to 16 steps the
+// kernel's LDS holds the streaming units' 4 images (one per wave), and the
+// ring takes all 4 of them.
+constexpr int lookup_ring(int ks) { return ks <= 16 ? 4 : shared_nbuf(ks); }
 
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool COS>
 __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, int64_t begin,
@@ -416,15 +600,23 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
   }
 
   const int nblk = (nkeys + 15) >> 4;
+  // Level-2 block images (KeyImage): step j = 4 m + t at fbase[t] + 256 m
+  const KeyImage im = key_image<KS, MASKED>(a);
+  uint32_t fbase[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) fbase[t] = im.frag_off(t, g, n);
   auto compute = [&](int buf, int blk) {
     if (!has0) return;                 // a wave without rows only helps to load
     f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
     const char* base = smem + buf * BLOCK_BYTES + lane * 16;
+    const char* ibase = smem + buf * BLOCK_BYTES;
     float knsq = 0.f;
 #pragma unroll
     for (int j = 0; j < KS; ++j) {
       if (!MASKED || j < a.ks) {
-        const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(base + j * 1024);
+        const uint32_t fo = MASKED ? im.frag_off(j, g, n) : fbase[j & 3] + 256 * (j >> 2);
+        const u32x4_t kf = LOOKUP ? *reinterpret_cast<const u32x4_t*>(ibase + fo)
+                                  : *reinterpret_cast<const u32x4_t*>(base + j * 1024);
         acc0 = mfma_chunk<DT>(kf, q0[j], acc0);
         if constexpr (TWO_TILES)
           if (has1) acc1 = mfma_chunk<DT>(kf, q1[j], acc1);
@@ -441,38 +633,39 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
   };
 
   if constexpr (LOOKUP) {
-    // LDS image of a block: segment j (1 KiB) holds, at lane slot L, chunk
-    // 4j + (L >> 4) of key row (L & 15): exactly the operand-A fragment of
-    // lane L at step j, so each wave reads it with one conflict-free 16-byte
-    // load per lane.  The segments go straight from global memory to LDS
-    // (global_load_lds: lane L's 16 bytes land at slot L), segment j by wave
-    // j % 4, into a ring of NBUF block images: NBUF - 1 blocks are in flight
+    // The key blocks go straight from global memory into a ring of NBUF
+    // block images (load_key_block: contiguous KiB loads, nontemporal; load
+    // instruction i of a block by wave i % 4): NBUF - 1 blocks are in flight
     // while one is multiplied, and no register holds them on the way.
-    constexpr int NBUF = shared_nbuf(KS);
-    constexpr int PW = KS / SC_WAVES;    // load instructions per wave and block
-    auto issue = [&](int blk) {
-      char* dst = smem + (blk % NBUF) * BLOCK_BYTES;
-      blk = min(blk, nblk - 1);          // past the end: a harmless reload
-      const char* src = keys + (int64_t)min(blk * 16 + n, nkeys - 1) * a.row_bytes + g * 16;
+    constexpr int NBUF = lookup_ring(KS);
+    constexpr int PW = (KS + SC_WAVES - 1) / SC_WAVES;   // load instructions per wave and block
+    uint32_t off[PW];
 #pragma unroll
-      for (int i = 0; i < PW; ++i) {
-        const int j = wv + SC_WAVES * i;
-        // masked steps reload the last real one (never multiplied)
-        const int jj = MASKED ? min(j, a.ks - 1) : j;
-        load_lds16(src + jj * 64, dst + j * 1024);
-      }
+    for (int t = 0; t < PW; ++t) {
+      const int i = wv + SC_WAVES * t;
+      off[t] = (i < (MASKED ? a.ks : KS)) ? im.src_off(i, lane, im.row_of(i, lane)) : 0u;
+    }
+    // only existing blocks are loaded (nothing is read twice from HBM)
+    auto issue = [&](int blk) {
+      if (blk < nblk)
+        load_key_block<KS, MASKED, PW>(im, a, keys, blk * 16, nkeys, off, wv, SC_WAVES,
+                                       smem + (blk % NBUF) * BLOCK_BYTES, lane);
     };
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
     qnorms();
 #pragma unroll
     for (int b = 0; b < NBUF - 1; ++b) issue(b);
     for (int blk = 0; blk < nblk; ++blk) {
-      // this wave's segments of block blk have landed once at most those of
-      // the NBUF - 2 younger blocks are outstanding; the barrier makes every
-      // wave's visible and ends every read of block blk - 1, whose image the
-      // next loads overwrite (a plain s_barrier: the fence of __syncthreads
-      // would wait for every load in flight)
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 2) * PW) : "memory");
+      // this wave's loads of block blk have landed once at most those of the
+      // NBUF - 2 younger blocks are outstanding (near the end, or with masked
+      // steps, when fewer instructions are younger: once all have); the
+      // barrier makes every wave's visible and ends every read of block
+      // blk - 1, whose image the next loads overwrite (a plain s_barrier: the
+      // fence of __syncthreads would wait for every load in flight)
+      if (!MASKED && wv + SC_WAVES * (PW - 1) < KS && blk + NBUF - 2 < nblk)
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 2) * PW) : "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
       issue(blk + NBUF - 1);
@@ -569,8 +762,10 @@ __device__ __forceinline__ void side_select(const ScoreParams& a, char* smem) {
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool SIDE = false, bool COS = false>
 __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   constexpr int MERGE_BYTES = SC_WAVES * 4 * 16 * KL * 8;
-  constexpr int STAGE_BYTES = (LOOKUP ? shared_nbuf(KS) : 2) * KS * 1024;
-  constexpr int SMEM = MERGE_BYTES > STAGE_BYTES ? MERGE_BYTES : STAGE_BYTES;
+  constexpr int STAGE_BYTES = (LOOKUP ? lookup_ring(KS) : 2) * KS * 1024;
+  constexpr int SIDE_BYTES = (LOOKUP && SIDE) ? (int)sel_cache_words(SEL_SIDE_MAX_N) * 4 : 0;
+  constexpr int SMEM0 = MERGE_BYTES > STAGE_BYTES ? MERGE_BYTES : STAGE_BYTES;
+  constexpr int SMEM = SMEM0 > SIDE_BYTES ? SMEM0 : SIDE_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   if constexpr (LOOKUP && SIDE) {
     static_assert(SMEM >= sel_cache_words(SEL_SIDE_MAX_N) * 4, "the side select's key cache");
@@ -613,6 +808,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     keys = a.keys + (int64_t)key0 * a.row_bytes;
   }
   if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys);
+  else if constexpr (LOOKUP && KS <= 16) stream_unit_lds<DT, KS, MASKED, KL, COS>(a, smem, begin, nr, keys);
   else stream_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, key0, nk, split);
 }
 
