@@ -287,12 +287,16 @@ __device__ __forceinline__ KeyImage key_image(const ScoreParams& a) {
 // Loads the block of key rows [row0, row0 + 16) (rows from kend on read row
 // kend - 1: they are masked by index when scored) into `img`: instructions
 // i = i0, i0 + istep, ... < ks.  off[t] holds src_off for instruction
-// i0 + istep t of an unclamped block.
+// i0 + istep t of an unclamped block.  nt (uniform): the nontemporal hint,
+// for keys no other unit reads; the units of a bucket cut into several read
+// the same keys and keep the temporal policy, so the later ones find them
+// in L2 (measured: 4-layer workload 318 -> 302 us; with the hint on every
+// unit the single-unit buckets run faster, multi-scale 195 -> 174 us).
 template <int KS, bool MASKED, int NT>
 __device__ __forceinline__ void load_key_block(const KeyImage& im, const ScoreParams& a,
                                                const char* keys, int row0, int kend,
                                                const uint32_t (&off)[NT], int i0, int istep,
-                                               char* img, int lane) {
+                                               char* img, int lane, bool nt = true) {
   const char* src = keys + (int64_t)row0 * im.rb;
   const bool ragged = row0 + 16 > kend;   // uniform
 #pragma unroll
@@ -305,7 +309,8 @@ __device__ __forceinline__ void load_key_block(const KeyImage& im, const ScorePa
       const int rr = row0 + r < kend ? r : kend - 1 - row0;
       o = im.src_off(i, lane, rr);
     }
-    load_lds16_nt(src + o, img + i * 1024);
+    if (nt) load_lds16_nt(src + o, img + i * 1024);
+    else load_lds16(src + o, img + i * 1024);
   }
 }
 
@@ -552,9 +557,11 @@ constexpr int shared_nbuf(int ks) {
 // ring takes all 4 of them.
 constexpr int lookup_ring(int ks) { return ks <= 16 ? 4 : shared_nbuf(ks); }
 
+// multi (Level-2): the unit's bucket is cut into several units, which all
+// read the scene's keys.
 template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool COS>
 __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, int64_t begin,
-                                            int nr, const char* keys) {
+                                            int nr, const char* keys, bool multi = false) {
   constexpr int BLOCK_BYTES = KS * 1024;
   constexpr int CPT = KS / 4;          // routing: 16-byte chunks per thread per key block
   const int tid = threadIdx.x;
@@ -645,11 +652,13 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
       const int i = wv + SC_WAVES * t;
       off[t] = (i < (MASKED ? a.ks : KS)) ? im.src_off(i, lane, im.row_of(i, lane)) : 0u;
     }
-    // only existing blocks are loaded (nothing is read twice from HBM)
+    // only existing blocks are loaded (nothing is read twice from HBM); the
+    // keys of a bucket cut into several units are read by each of them
+    const bool nt = !multi;
     auto issue = [&](int blk) {
       if (blk < nblk)
         load_key_block<KS, MASKED, PW>(im, a, keys, blk * 16, nkeys, off, wv, SC_WAVES,
-                                       smem + (blk % NBUF) * BLOCK_BYTES, lane);
+                                       smem + (blk % NBUF) * BLOCK_BYTES, lane, nt);
     };
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
     qnorms();
@@ -780,6 +789,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   bool shared;
   const char* keys;
   int key0 = 0, nk = a.nkeys, split = 0;
+  bool multi = false;
   if constexpr (LOOKUP) {
     // units in list order (the long shared units first), dealt to the XCDs
     // in pairs: a scene whose bucket spans two units reads its keys into one
@@ -792,6 +802,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     shared = (tag & UNIT_SHARED) != 0;
     begin = a.unit_begin[u];
     nr = min(shared ? a.shared_rows : UNIT_STREAM_ROWS, a.offsets[s + 1] - (int)begin);
+    multi = a.offsets[s + 1] - a.offsets[s] > a.shared_rows;
     keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
   } else {
     const int R = a.route_rows;
@@ -807,7 +818,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     nk = min(a.route_kps, a.nkeys - key0);
     keys = a.keys + (int64_t)key0 * a.row_bytes;
   }
-  if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys);
+  if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, multi);
   else if constexpr (LOOKUP && KS <= 16) stream_unit_lds<DT, KS, MASKED, KL, COS>(a, smem, begin, nr, keys);
   else stream_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, key0, nk, split);
 }
