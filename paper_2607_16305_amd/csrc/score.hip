@@ -97,12 +97,41 @@ __device__ __forceinline__ float chunk_sumsq(u32x4_t v, float acc) {
   return acc;
 }
 
+// Both values of the lane pairs (L, L ^ 32) and (L, L ^ 16), from the
+// gfx950 permlane swaps (vector instructions, no LDS round trip): with both
+// operands equal to v, lane L gets {v[L], v[L ^ 32]} (resp. L ^ 16) as the
+// two results, in an order that does not matter to a sum or a max.
+__device__ __forceinline__ void pair32(float v, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void pair16(float v, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+
 // The sum over the 4 lane groups (lanes n, n + 16, n + 32, n + 48) that hold
-// the chunks of one row.
+// the chunks of one row (added in the order (L, L^16) then the pairs, the same
+// in every lane of the group).
 __device__ __forceinline__ float sum_lane_groups(float v) {
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
+  float a, b;
+  pair16(v, a, b);
+  v = a + b;
+  pair32(v, a, b);
+  return a + b;
+}
+
+// The maximum over the same 4 lanes.
+__device__ __forceinline__ float max_lane_groups(float v) {
+  float a, b;
+  pair16(v, a, b);
+  v = fmaxf(a, b);
+  pair32(v, a, b);
+  return fmaxf(a, b);
 }
 
 __device__ __forceinline__ float inv_norm(float sq) { return sq > 0.f ? rsqrtf(sq) : 0.f; }
@@ -142,9 +171,7 @@ __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int ken
     // reach the row's top k (that list holds k keys at least as large), so
     // it is dropped; values equal to T stay, for the lower-index rule.
     const int p0 = blk * 16 + 4 * g;
-    float T = ls[KL - 1];
-    T = fmaxf(T, __shfl_xor(T, 16, 64));
-    T = fmaxf(T, __shfl_xor(T, 32, 64));
+    const float T = max_lane_groups(ls[KL - 1]);
 #pragma unroll
     for (int round = 0; round < 4; ++round) {
       float x = v[0];
@@ -155,18 +182,18 @@ __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int ken
       if (!(x >= T)) x = -__builtin_inff();
       if (!__any(x > ls[KL - 1])) break;
       const int p = p0 + w;
+      // sorted insertion, the list descending: entry e becomes ls[e-1] if x
+      // beats it, else x if x beats ls[e], else stays: the median of the
+      // three values (one instruction), and the index by the same two tests
 #pragma unroll
       for (int e = KL - 1; e >= 1; --e) {
         const bool above_prev = x > ls[e - 1];
         const bool above_cur = x > ls[e];
-        const float s_keep = above_cur ? x : ls[e];
-        const int i_keep = above_cur ? p : li[e];
-        ls[e] = above_prev ? ls[e - 1] : s_keep;
-        li[e] = above_prev ? li[e - 1] : i_keep;
+        li[e] = above_prev ? li[e - 1] : (above_cur ? p : li[e]);
+        ls[e] = __builtin_amdgcn_fmed3f(x, ls[e - 1], ls[e]);
       }
-      const bool top = x > ls[0];
-      ls[0] = top ? x : ls[0];
-      li[0] = top ? p : li[0];
+      li[0] = x > ls[0] ? p : li[0];
+      ls[0] = fmaxf(x, ls[0]);
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         if (r == w) v[r] = -__builtin_inff();
