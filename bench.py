@@ -9,17 +9,19 @@ while lookme_route runs on the first (the kept set depends on neither routing
 nor lookup), then lookme_inject_kept adds the rows.  The metric is tokens
 looked up and injected per second, counting tokens x layers.
 
-The default workload is a single image on one layer (1024 tokens, 256 scenes
-x 1024 primitives, 1 GiB table, bf16).  To keep one step from finding the
-previous step's keys in the 256 MiB Infinity Cache, the table is held in
-several copies and consecutive steps use different copies.
+The default workload is the largest one that fits one GPU: 32768 tokens
+(32 images of 1024) against 4096 scenes x 4096 primitives with Zipf(1.1)
+scene popularity (a 32 GiB value table and 16 GiB of primitive keys, bf16).
+Smaller workloads (--workload 1..3) reuse a table in several copies so that
+consecutive steps cannot find the previous step's keys in the 256 MiB
+Infinity Cache.
 
 Printed: one JSON line with the throughput, the roofline of the dominant
 kernel (Level-2 scoring: its key stream is HBM-bound) measured with HIP
 events inside the library on the launch stream, and the CPU oracle's
 throughput on a bounded sample of the same workload.
 
-    python bench.py [--steps K] [--warmup W] [--workload 1] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload 0..4] [--no-cpu-baseline]
 """
 
 from __future__ import annotations
@@ -143,7 +145,7 @@ def _per_dispatch(rows, counter, match):
     return list(vals.values())
 
 
-def summarise_traffic(fetch_dir: str, write_dir: str, wl, algorithmic: int):
+def summarise_traffic(fetch_dir: str, write_dir: str, wl, wl_index: int, algorithmic: int):
     """Scale FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the scoring kernel by
     what the same counters read for the 256 MiB calibration kernel."""
     fr, wr = _counter_rows(fetch_dir), _counter_rows(write_dir)
@@ -172,10 +174,13 @@ def summarise_traffic(fetch_dir: str, write_dir: str, wl, algorithmic: int):
         "traffic_over_algorithmic": (fetch_b + write_b) / algorithmic,
         "commands": [
             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <FETCH_DIR> -o run -- "
-            "python3 bench.py --steps 20 --warmup 2 --no-cpu-baseline --pmc-calibrate",
+            f"python3 bench.py --workload {wl_index} --steps 20 --warmup 2 --no-cpu-baseline "
+            "--pmc-calibrate",
             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <WRITE_DIR> -o run -- "
-            "python3 bench.py --steps 20 --warmup 2 --no-cpu-baseline --pmc-calibrate",
-            "python3 bench.py --traffic-from <FETCH_DIR> <WRITE_DIR> <BENCH_JSON>"],
+            f"python3 bench.py --workload {wl_index} --steps 20 --warmup 2 --no-cpu-baseline "
+            "--pmc-calibrate",
+            f"python3 bench.py --workload {wl_index} --traffic-from <FETCH_DIR> <WRITE_DIR> "
+            "<BENCH_JSON>"],
     }
     with open(traffic_path(wl.name), "w") as fh:
         json.dump(out, fh, indent=1)
@@ -739,7 +744,7 @@ def main():
             line = json.load(fh)
         if line["config"]["workload"] != wl.name:
             raise SystemExit("the bench line is for another workload")
-        out = summarise_traffic(args.traffic_from[0], args.traffic_from[1], wl,
+        out = summarise_traffic(args.traffic_from[0], args.traffic_from[1], wl, args.workload,
                                 line["roofline"]["algorithmic_bytes_per_launch"])
         print(json.dumps(out))
         return
