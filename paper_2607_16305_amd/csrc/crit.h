@@ -115,13 +115,27 @@ __device__ __forceinline__ float row_dot(const char* __restrict__ p, const char*
 // Called by all THREADS threads of a workgroup.
 constexpr int GATE_PER_THREAD = 32;
 
+// LDS words the select and the gate compaction work in (counts, scan
+// partials, the located prefix).  The caller passes them: a kernel that
+// also stages operands by direct-to-LDS loads keeps all of its LDS in one
+// object (with several, the compiler puts a load wait before every LDS read
+// that follows those loads).
+struct SelLds {
+  int hist[256];
+  int wsum[SEL_WAVES];
+  uint32_t prefix;
+  int need;
+  int total;
+};
+
 template <int THREADS>
 __device__ __forceinline__ void gate_compact_layer(const float* __restrict__ z, int64_t n,
                                                    int32_t* __restrict__ kept,
-                                                   int32_t* __restrict__ count) {
+                                                   int32_t* __restrict__ count, SelLds& sl) {
   constexpr int SPAN = THREADS * GATE_PER_THREAD;   // rows a round
-  __shared__ int wsum[THREADS / WAVE];
-  __shared__ int s_total;
+  static_assert(THREADS / WAVE <= SEL_WAVES, "scan partials");
+  int* wsum = sl.wsum;
+  int& s_total = sl.total;
   const int tid = threadIdx.x;
   int64_t base = 0;   // open rows in earlier rounds
   for (int64_t r0 = 0; r0 < n; r0 += SPAN) {
@@ -160,14 +174,15 @@ constexpr int sel_cache_words(int cn) { return cn > 0 ? cn + cn / 32 : 1; }
 template <int CN, int THREADS = SEL_THREADS>
 __device__ __forceinline__ void select_layer(const uint32_t* __restrict__ gkey, int64_t n,
                                              int64_t n_keep, int32_t* __restrict__ kept,
-                                             uint32_t* cache) {
+                                             uint32_t* cache, SelLds& sl) {
   constexpr bool CACHED = CN > 0;
   constexpr int WAVES = THREADS / WAVE;
   static_assert(THREADS % 256 == 0, "a thread per radix bin");
-  __shared__ int hist[256];
-  __shared__ int wsum[WAVES];
-  __shared__ uint32_t s_prefix;
-  __shared__ int s_need;
+  static_assert(WAVES <= SEL_WAVES, "scan partials");
+  int* hist = sl.hist;
+  int* wsum = sl.wsum;
+  uint32_t& s_prefix = sl.prefix;
+  int& s_need = sl.need;
   if (n_keep == 0) return;
   const int tid = threadIdx.x;
   if constexpr (CACHED) {

@@ -48,9 +48,10 @@ __global__ __launch_bounds__(GATE_WAVES * WAVE) void gate_logit_kernel(
 __global__ __launch_bounds__(GATE_THREADS) void gate_compact_kernel(
     const float* __restrict__ z_all, int64_t n, int32_t* __restrict__ kept_all,
     int32_t* __restrict__ count) {
+  __shared__ SelLds sl;
   const int layer = blockIdx.x;
   gate_compact_layer<GATE_THREADS>(z_all + (int64_t)layer * n, n, kept_all + (int64_t)layer * n,
-                                   count + layer);
+                                   count + layer, sl);
 }
 
 hipError_t launch_gate(int dt, int layers, int64_t n, const void* delta, int64_t delta_rows,

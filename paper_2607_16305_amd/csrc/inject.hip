@@ -40,9 +40,10 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
     const uint32_t* __restrict__ key_all, int64_t n, int64_t n_keep,
     int32_t* __restrict__ kept_all) {
   __shared__ uint32_t cache[sel_cache_words(CN)];
+  __shared__ SelLds sl;
   const int layer = blockIdx.x;
-  select_layer<CN>(key_all + (int64_t)layer * n, n, n_keep,
-                          kept_all + (int64_t)layer * n_keep, cache);
+  select_layer<CN>(key_all + (int64_t)layer * n, n, n_keep, kept_all + (int64_t)layer * n_keep,
+                   cache, sl);
 }
 
 // TO_R: the weighted row sum R of kept row j is rounded to the storage

@@ -47,12 +47,23 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
   using S = RtShape;
   constexpr int MI = RT_MI, NJ = RT_NJ, KB = RT_KB, KSL = KB / 64, NS = RT_NS;
   constexpr int THREADS = 64 * RT_WM * RT_WN;
-  __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
-  __shared__ float s_bias[ROUTE_DTL_MAX_TPS * S::BN];
-  __shared__ float m_s[RT_WN][S::BM];
-  __shared__ int m_i[RT_WN][S::BM];
   static_assert(NS >= 2, "a stage in flight while one is multiplied");
-  __shared__ int s_last;
+  // All of the kernel's LDS is one object.  With several __shared__ objects
+  // the compiler tags their accesses with alias scopes and then, finding the
+  // stage buffers' direct-to-LDS loads and fragment reads in one scope, puts
+  // a vmcnt(0) wait after every stage's loads, before the first fragment
+  // read: the next stage's loads then never overlap this stage's products.
+  // Without scopes it leaves the ordering to the explicit waits below.
+  constexpr int BIAS_OFF = NS * S::STAGE;
+  constexpr int MS_OFF = BIAS_OFF + ROUTE_DTL_MAX_TPS * S::BN * 4;
+  constexpr int MI_OFF = MS_OFF + RT_WN * S::BM * 4;
+  constexpr int LAST_OFF = MI_OFF + RT_WN * S::BM * 4;
+  __shared__ __attribute__((aligned(1024))) char smem[LAST_OFF + 16];
+  char (*lds)[S::STAGE] = reinterpret_cast<char (*)[S::STAGE]>(smem);
+  float* s_bias = reinterpret_cast<float*>(smem + BIAS_OFF);
+  float (*m_s)[S::BM] = reinterpret_cast<float (*)[S::BM]>(smem + MS_OFF);
+  int (*m_i)[S::BM] = reinterpret_cast<int (*)[S::BM]>(smem + MI_OFF);
+  int* s_last = reinterpret_cast<int*>(smem + LAST_OFF);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -243,7 +254,7 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
     return;
   }
   route_partial<S::BM>(a.part, a.count, a.splits, a.scene, rb, split, tid < S::BM ? tid : S::BM,
-                       nr, best_s, best_i, &s_last);
+                       nr, best_s, best_i, s_last);
 }
 
 hipError_t launch_route_dtl(int dt, const void* q, const void* scene_keys, const float* bias,

@@ -448,10 +448,12 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
   if constexpr (!LOOKUP) {
     top_i[0] += key0;
     if (a.route_splits > 1) {
-      __shared__ int s_last;
+      // the arrival flag sits past the candidate lists (the kernel's LDS is
+      // one object; see score_kernel)
+      int* s_last = reinterpret_cast<int*>(smem + NL * 16 * KL * 8);
       route_partial<UNIT_STREAM_ROWS>(a.route_part, a.route_count, a.route_splits, a.out_idx,
                                       begin / 16, split, L == 0 ? t : 16, nr, top_s[0], top_i[0],
-                                      &s_last);
+                                      s_last);
       return;
     }
   }
@@ -777,19 +779,23 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
 // crit_select_kernel on the launch's 256 threads, so the bits are its; or
 // compacts layer l's open gates from their logits (gate_compact_kernel's
 // body).
+// The key cache takes the first SIDE_CACHE_BYTES of `smem`, the select's
+// other words the SelLds after it.
+constexpr int SIDE_CACHE_BYTES = (sel_cache_words(SEL_SIDE_MAX_N) * 4 + 15) / 16 * 16;
+
 template <int KS>
 __device__ __forceinline__ void side_select(const ScoreParams& a, char* smem) {
   const int layer = blockIdx.x - a.side0;
+  SelLds& sl = *reinterpret_cast<SelLds*>(smem + SIDE_CACHE_BYTES);
   if (a.gate_count != nullptr) {
     gate_compact_layer<SC_THREADS>(
         reinterpret_cast<const float*>(a.crit_key) + (int64_t)layer * a.crit_n, a.crit_n,
-        a.kept + (int64_t)layer * a.crit_n, a.gate_count + layer);
+        a.kept + (int64_t)layer * a.crit_n, a.gate_count + layer, sl);
     return;
   }
-  select_layer<SEL_SIDE_MAX_N, SC_THREADS>(a.crit_key + (int64_t)layer * a.crit_n,
-                                                  a.crit_n, a.n_keep,
-                                                  a.kept + (int64_t)layer * a.n_keep,
-                                                  reinterpret_cast<uint32_t*>(smem));
+  select_layer<SEL_SIDE_MAX_N, SC_THREADS>(a.crit_key + (int64_t)layer * a.crit_n, a.crit_n,
+                                           a.n_keep, a.kept + (int64_t)layer * a.n_keep,
+                                           reinterpret_cast<uint32_t*>(smem), sl);
 }
 
 // KL: per-lane candidate list length (>= k) for lookup; 1 for routing.
@@ -799,12 +805,16 @@ template <int DT, int KS, bool MASKED, bool LOOKUP, int KL, bool SIDE = false, b
 __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   constexpr int MERGE_BYTES = SC_WAVES * 4 * 16 * KL * 8;
   constexpr int STAGE_BYTES = (LOOKUP ? lookup_ring(KS) : 2) * KS * 1024;
-  constexpr int SIDE_BYTES = (LOOKUP && SIDE) ? (int)sel_cache_words(SEL_SIDE_MAX_N) * 4 : 0;
+  constexpr int SIDE_BYTES = (LOOKUP && SIDE) ? SIDE_CACHE_BYTES + (int)sizeof(SelLds) : 0;
   constexpr int SMEM0 = MERGE_BYTES > STAGE_BYTES ? MERGE_BYTES : STAGE_BYTES;
   constexpr int SMEM = SMEM0 > SIDE_BYTES ? SMEM0 : SIDE_BYTES;
-  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  // all of the kernel's LDS is this one object (with several, the compiler
+  // puts a load wait before every LDS read that follows a direct-to-LDS
+  // load); 16 bytes past the rest hold the split routing's arrival flag
+  static_assert(SMEM >= MERGE_BYTES, "candidate lists");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM + 16];
   if constexpr (LOOKUP && SIDE) {
-    static_assert(SMEM >= sel_cache_words(SEL_SIDE_MAX_N) * 4, "the side select's key cache");
+    static_assert(SMEM >= SIDE_CACHE_BYTES + (int)sizeof(SelLds), "the side select's LDS");
     if ((int)blockIdx.x >= a.side0) {
       side_select<KS>(a, smem);
       return;
