@@ -22,15 +22,18 @@
 
 namespace lookme {
 
-// WM x WN waves, each MI x NJ MFMA tiles; K stages of KB bytes, NS buffers
-constexpr int RT_WM = 2, RT_WN = 4, RT_MI = 4, RT_NJ = 4, RT_KB = 128, RT_NS = 2;
+// WM x WN waves, each MI x NJ MFMA tiles; K stages of KB bytes
+constexpr int RT_WM = 2, RT_WN = 4, RT_MI = 4, RT_NJ = 4, RT_KB = 128;
 using RtShape = DtlShape<RT_WM, RT_WN, RT_MI, RT_NJ, RT_KB>;
 static_assert(RtShape::BM == ROUTE_DTL_ROWS && RtShape::BN == ROUTE_DTL_KEYS, "tile shape");
+// Stage buffers: three (two in flight while one is multiplied), or two when
+// a bias table must fit beside them (16 KiB for the largest key range).
+constexpr int rt_stages(bool bias) { return bias ? 2 : 3; }
 
 struct RouteDtlParams {
   const char* q;         // [rows, d_e]
   const char* keys;      // [S, d_e]
-  const float* bias;     // [S] or null
+  const float* bias;     // [S] (the BIAS instantiation only)
   int64_t rows;
   int64_t k_bytes;       // d_e * elem size, a multiple of 128
   int S;
@@ -42,10 +45,10 @@ struct RouteDtlParams {
   int32_t* count;
 };
 
-template <int DT>
+template <int DT, bool BIAS>
 __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlParams a) {
   using S = RtShape;
-  constexpr int MI = RT_MI, NJ = RT_NJ, KB = RT_KB, KSL = KB / 64, NS = RT_NS;
+  constexpr int MI = RT_MI, NJ = RT_NJ, KB = RT_KB, KSL = KB / 64, NS = rt_stages(BIAS);
   constexpr int THREADS = 64 * RT_WM * RT_WN;
   static_assert(NS >= 2, "a stage in flight while one is multiplied");
   // All of the kernel's LDS is one object.  With several __shared__ objects
@@ -53,17 +56,18 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
   // stage buffers' direct-to-LDS loads and fragment reads in one scope, puts
   // a vmcnt(0) wait after every stage's loads, before the first fragment
   // read: the next stage's loads then never overlap this stage's products.
-  // Without scopes it leaves the ordering to the explicit waits below.
+  // Without scopes it leaves the ordering to the explicit waits below.  The
+  // merge arrays and the arrival flag reuse the stage buffers (after the
+  // last stage); the bias table has its own words.
   constexpr int BIAS_OFF = NS * S::STAGE;
-  constexpr int MS_OFF = BIAS_OFF + ROUTE_DTL_MAX_TPS * S::BN * 4;
-  constexpr int MI_OFF = MS_OFF + RT_WN * S::BM * 4;
-  constexpr int LAST_OFF = MI_OFF + RT_WN * S::BM * 4;
-  __shared__ __attribute__((aligned(1024))) char smem[LAST_OFF + 16];
+  constexpr int BIAS_BYTES = BIAS ? ROUTE_DTL_MAX_TPS * S::BN * 4 : 0;
+  static_assert(RT_WN * S::BM * 8 + 16 <= NS * S::STAGE, "merge arrays in the stage buffers");
+  __shared__ __attribute__((aligned(1024))) char smem[BIAS_OFF + BIAS_BYTES];
   char (*lds)[S::STAGE] = reinterpret_cast<char (*)[S::STAGE]>(smem);
   float* s_bias = reinterpret_cast<float*>(smem + BIAS_OFF);
-  float (*m_s)[S::BM] = reinterpret_cast<float (*)[S::BM]>(smem + MS_OFF);
-  int (*m_i)[S::BM] = reinterpret_cast<int (*)[S::BM]>(smem + MI_OFF);
-  int* s_last = reinterpret_cast<int*>(smem + LAST_OFF);
+  float (*m_s)[S::BM] = reinterpret_cast<float (*)[S::BM]>(smem);
+  int (*m_i)[S::BM] = reinterpret_cast<int (*)[S::BM]>(smem + RT_WN * S::BM * 4);
+  int* s_last = reinterpret_cast<int*>(smem + RT_WN * S::BM * 8);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -78,14 +82,17 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
   const int64_t m0 = rb * S::BM;
   const int ntiles = (a.S + S::BN - 1) / S::BN;
   const int kt0 = split * a.tps, kt1 = min(ntiles, kt0 + a.tps);
+  const int nt = kt1 - kt0;              // key tiles of this unit
   const int nst = (int)(a.k_bytes / KB);
-  const int total = (kt1 - kt0) * nst;   // K stages of this unit, tile by tile
+  const int total = nt * nst;            // K stages of this unit, tile by tile
 
-  // the bias of the unit's keys (0 past the last scene: those keys are
-  // masked by index anyway)
-  for (int i = tid; i < (kt1 - kt0) * S::BN; i += THREADS) {
-    const int key = kt0 * S::BN + i;
-    s_bias[i] = (a.bias != nullptr && key < a.S) ? a.bias[key] : 0.f;
+  if constexpr (BIAS) {
+    // the bias of the unit's keys (0 past the last scene: those keys are
+    // masked by index anyway)
+    for (int i = tid; i < nt * S::BN; i += THREADS) {
+      const int key = kt0 * S::BN + i;
+      s_bias[i] = key < a.S ? a.bias[key] : 0.f;
+    }
   }
 
   // First key of tile t: a ragged last tile is moved back to end at the
@@ -99,8 +106,7 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
   // uniform over the wave, and the address is a uniform base (operand, row
   // block or key tile, K stage) plus a 32-bit lane offset fixed for the
   // launch (both operands are far below 4 GiB).  Rows past either operand
-  // are clamped into it (they feed no stored result); only a ragged last key
-  // tile needs its offsets clamped again.
+  // are clamped into it (they feed no stored result).
   // lane offset of load b from its base: the row block's first query row
   // (query loads) or the key tile's first key row (key loads)
   uint32_t off[S::PER_WAVE];
@@ -119,16 +125,27 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
     }
   }
   const char* q_base = a.q + m0 * a.k_bytes;
-  auto issue = [&](int sigma) {
-    const int sg = sigma < total ? sigma : total - 1;   // past the end: a harmless reload
-    const int tile = kt0 + sg / nst, s = sg % nst;
-    char* dst = lds[sigma % NS];
-    const char* k_base = a.keys + (int64_t)tile_start(tile) * a.k_bytes + s * KB;
-    const char* qs_base = q_base + s * KB;
+  // the producer's position (tile within the unit, K stage, buffer), kept
+  // as wave-uniform counters; past the unit's last stage it stays there (a
+  // harmless reload keeps every wave's count of loads in flight the same)
+  int p_tile = 0, p_stage = 0, p_buf = 0;
+  auto issue = [&]() {
+    char* dst = lds[p_buf];
+    const char* k_base = a.keys + (int64_t)tile_start(kt0 + p_tile) * a.k_bytes + p_stage * KB;
+    const char* qs_base = q_base + p_stage * KB;
 #pragma unroll
     for (int b = 0; b < S::PER_WAVE; ++b) {
       const bool is_q = (wv * S::PER_WAVE + b) * S::RPI < S::BM;   // uniform
       load_lds16((is_q ? qs_base : k_base) + off[b], dst + (wv * S::PER_WAVE + b) * 1024);
+    }
+    p_buf = p_buf == NS - 1 ? 0 : p_buf + 1;
+    if (++p_stage == nst) {
+      if (p_tile + 1 < nt) {
+        p_stage = 0;
+        ++p_tile;
+      } else {
+        p_stage = nst - 1;
+      }
     }
   };
 
@@ -147,7 +164,9 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
   }
 
 #pragma unroll
-  for (int i = 0; i < NS - 1; ++i) issue(i);
+  for (int i = 0; i < NS - 1; ++i) issue();
+  // the consumer's position: tile within the unit, K stage, buffer
+  int c_tile = 0, c_stage = 0, c_buf = 0;
   for (int sigma = 0; sigma < total; ++sigma) {
     // this wave's loads of stage sigma have landed once at most those of the
     // NS - 2 younger stages are outstanding; the barrier makes every wave's
@@ -158,8 +177,8 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NS - 2) * S::PER_WAVE) : "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    issue(sigma + NS - 1);
-    const char* buf = lds[sigma % NS];
+    issue();
+    const char* buf = lds[c_buf];
     // the first stage of a tile starts its accumulators from zero (the MFMA
     // takes a zero operand; no register is cleared)
     auto stage = [&](auto first) {
@@ -179,22 +198,22 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
                                            ? f32x4_t{0.f, 0.f, 0.f, 0.f} : acc[i][j]);
       }
     };
-    if (sigma % nst == 0) stage(std::true_type{});
+    if (c_stage == 0) stage(std::true_type{});
     else stage(std::false_type{});
-    if (sigma % nst == nst - 1) {
+    c_buf = c_buf == NS - 1 ? 0 : c_buf + 1;
+    if (c_stage == nst - 1) {
       // the tile is complete: the lane holds rows wm + 16 i + 4 g + r and
       // keys key0 + 16 j (increasing in j, and above every earlier tile's,
       // so a strict '>' keeps the lowest key on exact ties).  Keys past the
       // last scene (a ragged last tile) get a bias of -inf.
-      const int tl = sigma / nst;
-      const int tile = kt0 + tl;
+      const int tile = kt0 + c_tile;
       const int key0 = tile_start(tile) + wn + n16;   // key of j = 0
       float bj[NJ];
       int kj[NJ];
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         kj[j] = key0 + 16 * j;
-        bj[j] = s_bias[max(kj[j] - kt0 * S::BN, 0)];
+        bj[j] = BIAS ? s_bias[max(kj[j] - kt0 * S::BN, 0)] : 0.f;
       }
       if ((tile + 1) * S::BN > a.S) {
         // ragged last tile: keys already scored by the previous tile, and
@@ -213,9 +232,16 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
             bi[i][r] = v > bs[i][r] ? kj[j] : bi[i][r];
             bs[i][r] = fmaxf(bs[i][r], v);
           }
+      c_stage = 0;
+      ++c_tile;
+    } else {
+      ++c_stage;
     }
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
+  // no load into LDS outlives the wave, and every wave is done with the
+  // stage buffers before the merge arrays overwrite them
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
 
   // merge the 16 lanes of a row group (keys n16 + 16 j of every tile), then
   // the 4 waves that share rows, in key order
@@ -274,10 +300,14 @@ hipError_t launch_route_dtl(int dt, const void* q, const void* scene_keys, const
   p.part = part;
   p.count = count;
   const unsigned grid = (unsigned)((p.units + 7) / 8 * 8);
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL(route_dtl_kernel<DT_BF16>, dim3(grid), dim3(64 * RT_WM * RT_WN), 0, st, p);
-  else
-    hipLaunchKernelGGL(route_dtl_kernel<DT_F32>, dim3(grid), dim3(64 * RT_WM * RT_WN), 0, st, p);
+  const dim3 block(64 * RT_WM * RT_WN);
+  if (dt == DT_BF16) {
+    if (bias != nullptr) hipLaunchKernelGGL((route_dtl_kernel<DT_BF16, true>), dim3(grid), block, 0, st, p);
+    else hipLaunchKernelGGL((route_dtl_kernel<DT_BF16, false>), dim3(grid), block, 0, st, p);
+  } else {
+    if (bias != nullptr) hipLaunchKernelGGL((route_dtl_kernel<DT_F32, true>), dim3(grid), block, 0, st, p);
+    else hipLaunchKernelGGL((route_dtl_kernel<DT_F32, false>), dim3(grid), block, 0, st, p);
+  }
   return hipGetLastError();
 }
 
