@@ -5,10 +5,11 @@
 //   1. per 1024-row chunk: a histogram over scenes and, for every row, its
 //      rank among equal-scene rows earlier in the chunk (wave match masks
 //      built from ballots over the scene bits, then the 16 waves in order);
-//   2. one workgroup: per-scene prefix over chunks, exclusive scan over
-//      scenes (wavefront prefix sums) giving bucket offsets, and the Level-2
-//      work list (a bucket of <= 16 rows is one streaming unit, a larger one
-//      is cut into shared units of <= 128 rows);
+//   2. per scene (a thread each): prefix over chunks; then one workgroup:
+//      exclusive scan over scenes (wavefront prefix sums) giving bucket
+//      offsets, and the Level-2 work list (a bucket of <= 16 rows is one
+//      streaming unit, a larger one is cut into shared units of <= 128 rows;
+//      the two kinds alternate in the list);
 //   3. per chunk: perm[offset + chunk prefix + rank] = row.
 // Within a bucket rows keep ascending order.  Scene values outside [0, S)
 // are clamped (results for such rows are undefined; memory stays in bounds).
@@ -32,20 +33,33 @@ __device__ __forceinline__ int stream_units(int size) {
   return (size > 0 && size <= UNIT_STREAM_ROWS) ? 1 : 0;
 }
 
-// Writes the units of scene s: shared ones at index sh, a streaming one at st.
-__device__ __forceinline__ void write_units(int s, int offset, int size, int sh, int st,
-                                            int shared_rows, int32_t* unit_scene,
+// List position of shared unit i and of streaming unit j (nb shared and ns
+// streaming units in all): the two kinds alternate while both last, shared
+// first, then the rest of the longer kind.  A CU then tends to hold one
+// shared unit (matrix-core and vector work on keys mostly found in L2) and
+// one streaming unit (HBM-bound) at a time; with the shared units first, the
+// Zipf workload's 487 of them filled every slot for the first ~300 us while
+// the key stream from HBM ran at about half its rate.
+__device__ __forceinline__ int shared_pos(int i, int ns) { return i < ns ? 2 * i : ns + i; }
+__device__ __forceinline__ int stream_pos(int j, int nb) { return j < nb ? 2 * j + 1 : nb + j; }
+
+// Writes the units of scene s: shared ones as shared units sh.., a streaming
+// one as streaming unit st (list positions from shared_pos / stream_pos).
+__device__ __forceinline__ void write_units(int s, int offset, int size, int sh, int st, int nb,
+                                            int ns, int shared_rows, int32_t* unit_scene,
                                             int32_t* unit_begin) {
   if (size == 0) return;
   if (size <= UNIT_STREAM_ROWS) {
-    unit_scene[st] = s;
-    unit_begin[st] = offset;
+    const int p = stream_pos(st, nb);
+    unit_scene[p] = s;
+    unit_begin[p] = offset;
     return;
   }
   const int units = shared_units(size, shared_rows);
   for (int u = 0; u < units; ++u) {
-    unit_scene[sh + u] = s | UNIT_SHARED;
-    unit_begin[sh + u] = offset + u * shared_rows;
+    const int p = shared_pos(sh + u, ns);
+    unit_scene[p] = s | UNIT_SHARED;
+    unit_begin[p] = offset + u * shared_rows;
   }
 }
 
@@ -146,11 +160,11 @@ __device__ __forceinline__ void offsets_and_units(int S, int shared_rows, SizeOf
   }
   int tot[3];
   block_excl_scan3(v, tot);
-  int row = v[0], sh = v[1], st = tot[1] + v[2];
+  int row = v[0], sh = v[1], st = v[2];
   for (int s = s0; s < s1; ++s) {
     const int size = size_of(s);
     set_offset(s, row);
-    write_units(s, row, size, sh, st, shared_rows, unit_scene, unit_begin);
+    write_units(s, row, size, sh, st, tot[1], tot[2], shared_rows, unit_scene, unit_begin);
     row += size;
     sh += shared_units(size, shared_rows);
     st += stream_units(size);
@@ -161,29 +175,59 @@ __device__ __forceinline__ void offsets_and_units(int S, int shared_rows, SizeOf
   }
 }
 
+// Per-scene exclusive prefix of the chunk histograms over the chunks (in
+// place), and the bucket sizes into offsets[] for bucket_scan_kernel: one
+// thread a scene, CB chunk loads in flight (a single workgroup walking every
+// scene took ~20 us on the Zipf workload, one dependent load round after
+// another).
+constexpr int COL_THREADS = 256;
+
+__global__ __launch_bounds__(COL_THREADS) void bucket_colscan_kernel(
+    int32_t* __restrict__ chunk_hist, int64_t chunks, int S, int32_t* __restrict__ offsets) {
+  constexpr int CB = 32;
+  const int s = blockIdx.x * COL_THREADS + threadIdx.x;
+  if (s >= S) return;
+  int run = 0;
+  for (int64_t c0 = 0; c0 < chunks; c0 += CB) {
+    int h[CB];
+#pragma unroll
+    for (int i = 0; i < CB; ++i) h[i] = c0 + i < chunks ? chunk_hist[(c0 + i) * S + s] : 0;
+#pragma unroll
+    for (int i = 0; i < CB; ++i) {
+      if (c0 + i < chunks) chunk_hist[(c0 + i) * S + s] = run;
+      run += h[i];
+    }
+  }
+  offsets[s] = run;
+}
+
+// COLS: the per-scene prefix over chunks ran in bucket_colscan_kernel (the
+// bucket sizes are in offsets[]); otherwise this workgroup takes it first,
+// eight chunk loads in flight a thread (few scenes and chunks: one launch
+// less).
+template <bool COLS>
 __global__ __launch_bounds__(BK_THREADS) void bucket_scan_kernel(
     int32_t* __restrict__ chunk_hist, int64_t chunks, int S, int shared_rows,
-    int32_t* __restrict__ offsets,
-    int32_t* __restrict__ unit_scene, int32_t* __restrict__ unit_begin,
-    int32_t* __restrict__ unit_count) {
-  // 1. per-scene prefix over chunks; bucket sizes go to offsets[] for now
-  // (loads are batched so that eight chunk reads are in flight at a time)
-  for (int s = threadIdx.x; s < S; s += BK_THREADS) {
-    int run = 0;
-    for (int64_t c0 = 0; c0 < chunks; c0 += 8) {
-      int h[8];
+    int32_t* __restrict__ offsets, int32_t* __restrict__ unit_scene,
+    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count) {
+  if constexpr (!COLS) {
+    for (int s = threadIdx.x; s < S; s += BK_THREADS) {
+      int run = 0;
+      for (int64_t c0 = 0; c0 < chunks; c0 += 8) {
+        int h[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) h[i] = c0 + i < chunks ? chunk_hist[(c0 + i) * S + s] : 0;
+        for (int i = 0; i < 8; ++i) h[i] = c0 + i < chunks ? chunk_hist[(c0 + i) * S + s] : 0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        if (c0 + i < chunks) chunk_hist[(c0 + i) * S + s] = run;
-        run += h[i];
+        for (int i = 0; i < 8; ++i) {
+          if (c0 + i < chunks) chunk_hist[(c0 + i) * S + s] = run;
+          run += h[i];
+        }
       }
+      offsets[s] = run;
     }
-    offsets[s] = run;
+    __syncthreads();
   }
-  __syncthreads();
-  // 2. exclusive scan of the sizes over scenes: offsets and the work list
+  // exclusive scan of the bucket sizes over scenes: offsets and the work list
   offsets_and_units(
       S, shared_rows, [&](int s) { return offsets[s]; },
       [&](int s, int off) { offsets[s] = off; }, offsets, unit_scene, unit_begin, unit_count);
@@ -324,8 +368,21 @@ hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, int shared_r
   hipLaunchKernelGGL(bucket_hist_kernel, dim3((unsigned)chunks), dim3(BK_THREADS),
                      (size_t)S * sizeof(int), st, scene, rows, S, sbits, ws.chunk_hist,
                      ws.local_rank);
-  hipLaunchKernelGGL(bucket_scan_kernel, dim3(1), dim3(BK_THREADS), 0, st, ws.chunk_hist, chunks,
-                     S, shared_rows, ws.offsets, ws.unit_scene, ws.unit_begin, ws.unit_count);
+  // the prefix over chunks in its own launch once the one workgroup would
+  // need more than four dependent load rounds for it
+  const int64_t rounds = ((S + BK_THREADS - 1) / BK_THREADS) * ((chunks + 7) / 8);
+  if (rounds > 4) {
+    hipLaunchKernelGGL(bucket_colscan_kernel,
+                       dim3((unsigned)((S + COL_THREADS - 1) / COL_THREADS)), dim3(COL_THREADS), 0,
+                       st, ws.chunk_hist, chunks, S, ws.offsets);
+    hipLaunchKernelGGL(bucket_scan_kernel<true>, dim3(1), dim3(BK_THREADS), 0, st, ws.chunk_hist,
+                       chunks, S, shared_rows, ws.offsets, ws.unit_scene, ws.unit_begin,
+                       ws.unit_count);
+  } else {
+    hipLaunchKernelGGL(bucket_scan_kernel<false>, dim3(1), dim3(BK_THREADS), 0, st, ws.chunk_hist,
+                       chunks, S, shared_rows, ws.offsets, ws.unit_scene, ws.unit_begin,
+                       ws.unit_count);
+  }
   hipLaunchKernelGGL(bucket_scatter_kernel, dim3((unsigned)chunks), dim3(BK_THREADS), 0, st,
                      scene, rows, S, ws.chunk_hist, ws.local_rank, ws.offsets, ws.perm);
   return hipGetLastError();

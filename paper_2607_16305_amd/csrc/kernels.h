@@ -65,9 +65,9 @@ hipError_t launch_route_dtl(int dt, const void* q, const void* scene_keys, const
 // ---- bucketing of rows by scene -----------------------------------------
 // Level-2 work units: a bucket of at most UNIT_STREAM_ROWS rows is one
 // streaming unit; a larger bucket is cut into shared units of at most
-// shared_unit_rows() rows, tagged with UNIT_SHARED in unit_scene.  The work
-// list holds every shared unit first (they are the long ones), then the
-// streaming units, each part in scene order.
+// shared_unit_rows() rows, tagged with UNIT_SHARED in unit_scene.  In the
+// work list the two kinds alternate (shared first) while both last, then the
+// rest of the longer kind follows; each kind keeps scene order.
 constexpr int UNIT_STREAM_ROWS = 16;
 constexpr int32_t UNIT_SHARED = 1 << 30;
 // Chunk steps (64 bytes of a key row each) the scoring kernel is compiled

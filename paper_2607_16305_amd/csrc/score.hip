@@ -828,11 +828,12 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   int key0 = 0, nk = a.nkeys, split = 0;
   bool multi = false;
   if constexpr (LOOKUP) {
-    // units in list order (the long shared units first), dealt to the XCDs
-    // in pairs: a scene whose bucket spans two units reads its keys into one
-    // XCD's L2 once, while a scene with many units is still spread over all
+    // units in list order (shared and streaming alternating), dealt to the
+    // XCDs in fours: two consecutive shared units of a bucket cut into
+    // several (list positions 4q and 4q + 2) read their keys into one XCD's
+    // L2, while a scene with many units is still spread over all
     const int b = blockIdx.x, slot = b >> 3;
-    const int u = (slot >> 1) * 16 + (b & 7) * 2 + (slot & 1);
+    const int u = (slot >> 2) * 32 + (b & 7) * 4 + (slot & 3);
     if (u >= *a.unit_count) return;
     const int tag = a.unit_scene[u];
     const int s = tag & ~UNIT_SHARED;
@@ -1011,7 +1012,7 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
   p.k = k;
   p.out_idx = prim;
   p.out_w = w;
-  int grid = (int)((ws.max_units + 15) / 16 * 16);   // whole pairs on every XCD
+  int grid = (int)((ws.max_units + 31) / 32 * 32);   // whole fours on every XCD
   if (side != nullptr && (side->n_keep > 0 || side->count != nullptr) && side->n > 0) {
     p.side0 = grid;
     p.crit_n = side->n;
