@@ -80,6 +80,9 @@ def parse():
     ap.add_argument("--two-streams", action="store_true",
                     help="select the kept set on a second stream even where the lookup's "
                          "bucketing launch can carry it (batches of at most 1024 rows)")
+    ap.add_argument("--select-on-main", action="store_true",
+                    help="run the select on the launch stream before routing instead of on a "
+                         "second stream beside it (times its kernels without the overlap)")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -174,10 +177,10 @@ def summarise_traffic(fetch_dir: str, write_dir: str, wl, wl_index: int, algorit
         "traffic_over_algorithmic": (fetch_b + write_b) / algorithmic,
         "commands": [
             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <FETCH_DIR> -o run -- "
-            f"python3 bench.py --workload {wl_index} --steps 20 --warmup 2 --no-cpu-baseline "
+            f"python3 bench.py --workload {wl_index} --steps 20 --warmup 2 --reps 1 --no-cpu-baseline "
             "--pmc-calibrate",
             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <WRITE_DIR> -o run -- "
-            f"python3 bench.py --workload {wl_index} --steps 20 --warmup 2 --no-cpu-baseline "
+            f"python3 bench.py --workload {wl_index} --steps 20 --warmup 2 --reps 1 --no-cpu-baseline "
             "--pmc-calibrate",
             f"python3 bench.py --workload {wl_index} --traffic-from <FETCH_DIR> <WRITE_DIR> "
             "<BENCH_JSON>"],
@@ -201,7 +204,7 @@ def stored_traffic(wl):
 
 class Bench:
     def __init__(self, wl, seed, copies, relevance=0, fusion=0, netprop=0, scales=0,
-                 gate=False, two_streams=False):
+                 gate=False, two_streams=False, select_on_main=False):
         import torch
         from paper_2607_16305_amd import lookme as lk
         from synth import make_inputs
@@ -266,6 +269,7 @@ class Bench:
             self.kept = torch.empty((gl, n), dtype=torch.int32, device=dev)
             self.count = torch.zeros((gl,), dtype=torch.int32, device=dev)
         self.handles = [t.handle for t in self.tables]
+        self.select_on_main = select_on_main
         # small batches: the select rides in the lookup's bucketing launch on
         # the one stream (lookme_lookup_select); a second stream's waits would
         # cost more than the select itself
@@ -331,13 +335,16 @@ class Bench:
         # kept buffer it overwrites) and runs beside the projection and
         # routing; measured faster than beside the Level-2 lookup, whose
         # workgroups it would slow
+        if self.select_on_main and not self.gate:
+            lk.lookme_select(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.kept,
+                             self.stream)
         self.ev_start.record(self.main)
         self.side.wait_event(self.ev_start)
         if self.gate:
             gl = self.w_g.shape[0]
             lk.lookme_gate(h, gl, n, inp["delta"], n, wl.crit_dim, None, self.w_g, self.kept,
                            self.count, self.side_handle)
-        else:
+        elif not self.select_on_main:
             lk.lookme_select(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.kept,
                              self.side_handle)
         self.ev_kept.record(self.side)
@@ -766,7 +773,7 @@ def main():
     if args.gate and args.scales:
         raise SystemExit("--gate is not combined with --scales")
     b = Bench(wl, args.workload, args.copies, args.relevance, args.fusion, args.netprop,
-              args.scales, args.gate, args.two_streams)
+              args.scales, args.gate, args.two_streams, args.select_on_main)
 
     for i in range(args.warmup):
         b.step(i)
@@ -835,6 +842,7 @@ def main():
                                "launch (one stream)" if args.gate else
                                "norms in the bucketing launch, top-n_keep in the Level-2 launch "
                                "(one stream)") if b.one_stream
+                              else "launch stream, before routing" if b.select_on_main
                               else "second stream beside projection and routing"),
                    "kept_set": ("learned gate, " + "+".join(str(c) for c in b.count.tolist())
                                 + " open" if args.gate else f"top {wl.n_keep} by criticality")},
