@@ -457,6 +457,23 @@ lookme_status_t lookme_inject_propagated_gated(lookme_t h, int32_t steps, int64_
                                                void* stream);
 
 /*
+ * lookme_scene_keys -- scene-centred keys (Sec. 3.2, Level-1, Eq. 4): a
+ * scene's key is the mean of its primitive embeddings,
+ *   scene_keys[s, :] = round( (sum over p of prim_keys[s, p, :]) / N_p ),
+ * each element summed in float32 in increasing p, divided by N_p once and
+ * rounded once to the dtype.  A preparation step for tables whose scene
+ * keys are not given (the configured workloads give them): its output can be
+ * passed to lookme_create as scene_keys.
+ *   desc        num_scenes, prims_per_scene, key_dim and dtype are used (the
+ *               rest is ignored); key_dim * elem_size a multiple of 16 bytes
+ *   prim_keys   [N_s, N_p, d_e] of dtype, read once
+ *   scene_keys  [N_s, d_e] of dtype, written (must not overlap prim_keys)
+ * Needs no handle and no workspace.
+ */
+lookme_status_t lookme_scene_keys(const lookme_desc_t* desc, const void* prim_keys,
+                                  void* scene_keys, void* stream);
+
+/*
  * lookme_inject_text -- the text pathway of a LookME layer (Sec. 3.2, "Text
  * embedding index-based lookup", Eq. 1): a text position's token id indexes
  * the layer's text table, R_text = E_text[u], and the open entries of the

@@ -163,6 +163,27 @@ def _iv_add_store(h: np.ndarray, cf, rf, dtype: str):
 # Stage checks
 # ---------------------------------------------------------------------------
 
+def check_scene_keys(keys_lib, prim_keys, dtype: str, rep: Report):
+    """Eq. 4 scene-centred keys: the library's [S, d_e] against the oracle's
+    exact mean of each scene's primitive keys (prim_keys [S, P, d_e] in the
+    stored form of ``dtype``).  A float32 sum of P terms in any order errs by
+    at most (P - 1) 2^-24 sum|x| and the division by P adds one rounding, so
+    the stored key must lie between the roundings of mean -/+ E with
+    E = (P + 1) 2^-24 (sum|x| / P + |mean|)."""
+    pk = O.to_f64(np.asarray(prim_keys), dtype)
+    P = pk.shape[1]
+    mean = O.scene_keys_from_primitives(pk)
+    E = (P + 1) * U32 * (np.sum(np.abs(pk), axis=1) / P + np.abs(mean))
+    lo, hi = O.round_to_dtype(mean - E, dtype), O.round_to_dtype(mean + E, dtype)
+    got = O.to_f64(keys_lib, dtype)
+    rep.count("scene_key", got.shape[0])
+    bad = (got < lo) | (got > hi)
+    if np.any(bad):
+        s, c = np.argwhere(bad)[0]
+        rep.fail(f"scene key [{s}, {c}]: {got[s, c]!r} outside [{lo[s, c]!r}, {hi[s, c]!r}] "
+                 f"(mean {mean[s, c]!r}); {int(bad.sum())} elements")
+
+
 def check_q(q_lib, q_orc, dtype: str, rep: Report, max_ulp: int = 1):
     """C1 (exact copies): every element within ``max_ulp`` of the oracle's."""
     d = ulp_distance(q_lib, q_orc, dtype)

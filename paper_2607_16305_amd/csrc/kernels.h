@@ -219,6 +219,10 @@ hipError_t launch_gate(int dt, int layers, int64_t n, const void* delta, int64_t
 // For the first count[0] entries j of kept (all n_text entries when kept is
 // null; count null: all of kept's n_text): i = kept[j],
 // hidden[pos[i], :d_t] = round(hidden[pos[i], :d_t] + table[ids[i]]).
+// Scene-centred keys of Eq. 4 (scene_keys.hip): scene_keys[s] = round(sum_p
+// prim_keys[s, p] / P), float32 sum in p order.
+hipError_t launch_scene_keys(int dt, const void* prim_keys, int S, int P, int d_e,
+                             void* scene_keys, hipStream_t st);
 hipError_t launch_text_inject(int dt, int64_t n_text, const int32_t* kept, const int32_t* count,
                               const int32_t* pos, const int32_t* ids, const void* table,
                               int64_t vocab, int d_t, void* hidden, int64_t n, int d_h,

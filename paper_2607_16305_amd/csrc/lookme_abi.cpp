@@ -970,6 +970,26 @@ lookme_status_t lookme_inject_propagated_gated(lookme_t h, int32_t steps, int64_
                     "fusion launch");
 }
 
+lookme_status_t lookme_scene_keys(const lookme_desc_t* desc, const void* prim_keys,
+                                  void* scene_keys, void* stream) {
+  if (desc == nullptr) return fail(LOOKME_ERR_INVALID, "desc is NULL");
+  const lookme_desc_t d = *desc;
+  if (d.dtype != LOOKME_F32 && d.dtype != LOOKME_BF16)
+    return fail(LOOKME_ERR_INVALID, "unknown dtype %d", d.dtype);
+  if (d.num_scenes < 1 || d.prims_per_scene < 1 || d.key_dim < 1)
+    return fail(LOOKME_ERR_INVALID, "num_scenes, prims_per_scene and key_dim must be positive");
+  if (((int64_t)d.key_dim * elem_size(d.dtype)) % 16 != 0)
+    return fail(LOOKME_ERR_UNSUPPORTED, "key_dim * elem_size must be a multiple of 16 bytes");
+  if ((int64_t)d.num_scenes * d.prims_per_scene > (int64_t)INT32_MAX)
+    return fail(LOOKME_ERR_UNSUPPORTED, "num_scenes * prims_per_scene exceeds 2^31 - 1 rows");
+  LOOKME_TRY(check_ptr(prim_keys, "prim_keys"));
+  LOOKME_TRY(check_ptr(scene_keys, "scene_keys"));
+  return hip_status(lookme::launch_scene_keys(d.dtype, prim_keys, d.num_scenes,
+                                              d.prims_per_scene, d.key_dim, scene_keys,
+                                              static_cast<hipStream_t>(stream)),
+                    "scene keys launch");
+}
+
 lookme_status_t lookme_inject_text(int32_t dtype, const void* table, int64_t vocab, int32_t d_t,
                                    int64_t n_text, const int32_t* pos, const int32_t* ids,
                                    const int32_t* kept, const int32_t* count, void* hidden,

@@ -34,6 +34,7 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_inject_multiscale_gated", "lookme_gate",
             "lookme_inject_gated", "lookme_inject_fused_gated", "lookme_inject_propagated_gated",
             "lookme_inject_text", "lookme_lookup_select", "lookme_lookup_gate",
+            "lookme_scene_keys",
             "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read", "lookme_inject_noalloc")
 
@@ -105,6 +106,7 @@ def load():
                                       _vp, _vp, ctypes.c_int32, _vp],
         "lookme_inject_propagated_gated": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp,
                                            _vp, _vp, _vp, ctypes.c_int32, _vp],
+        "lookme_scene_keys": [ctypes.POINTER(lookme_desc_t), _vp, _vp, _vp],
         "lookme_inject_text": [ctypes.c_int32, _vp, ctypes.c_int64, ctypes.c_int32,
                                ctypes.c_int64, _vp, _vp, _vp, _vp, _vp, ctypes.c_int64,
                                ctypes.c_int32, _vp],
@@ -284,6 +286,22 @@ def lookme_inject_propagated_gated(h, steps, n, kept, count, scene, prim, w, hid
     _check(load().lookme_inject_propagated_gated(h, steps, n, _ptr(kept), _ptr(count),
                                                  _ptr(scene), _ptr(prim), _ptr(w), _ptr(hidden),
                                                  d_h, _stream(stream)))
+
+
+def lookme_scene_keys(desc, prim_keys, scene_keys, stream=None):
+    _check(load().lookme_scene_keys(ctypes.byref(desc) if desc is not None else None,
+                                    _ptr(prim_keys), _ptr(scene_keys), _stream(stream)))
+
+
+def scene_keys(prim_keys, stream=None):
+    """lookme_scene_keys on a torch tensor prim_keys [S, P, d_e]: returns the
+    [S, d_e] scene keys of Eq. 4 (a new tensor of the same dtype)."""
+    import torch
+    S, P, d_e = prim_keys.shape
+    out = torch.empty((S, d_e), dtype=prim_keys.dtype, device=prim_keys.device)
+    desc = lookme_desc_t(S, P, d_e, d_e, 1, DTYPE_CODE[prim_keys.dtype], 0)
+    lookme_scene_keys(desc, prim_keys, out, stream)
+    return out
 
 
 def lookme_inject_text(dtype, table, vocab, d_t, n_text, pos, ids, kept, count, hidden, n, d_h,

@@ -403,3 +403,20 @@ def test_lookup_gate_validates(lib):
         assert S(lambda: call(n=0, p=None, wg=None, cnt=None)) == lk.LOOKME_OK
     finally:
         lk.lookme_destroy(h)
+
+
+def test_scene_keys_validates(lib):
+    """lookme_scene_keys (Eq. 4) rejects bad descriptors and pointers before
+    any launch (no GPU needed)."""
+    S = lambda f: _status(f)[0]
+    sk = lambda p=FAKE, o=FAKE, **kw: lk.lookme_scene_keys(_desc(**kw), p, o, 0)
+    assert S(lambda: lk.lookme_scene_keys(None, FAKE, FAKE, 0)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: sk(dtype=7)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: sk(num_scenes=0)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: sk(prims_per_scene=0)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: sk(key_dim=0)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: sk(key_dim=6, dtype=lk.LOOKME_BF16)) == lk.LOOKME_ERR_UNSUPPORTED  # 12 B
+    assert S(lambda: sk(num_scenes=1 << 16, prims_per_scene=1 << 16)) == \
+        lk.LOOKME_ERR_UNSUPPORTED
+    assert S(lambda: sk(p=None)) == lk.LOOKME_ERR_INVALID
+    assert S(lambda: sk(o=FAKE + 4)) == lk.LOOKME_ERR_INVALID

@@ -443,3 +443,43 @@ def test_end_to_end_check_accepts_the_oracle_and_rejects_planted_errors(dtype):
     else:
         q[t, 0] = np.float32(q[t, 0] * (1 + 1e-3))
     assert not _e2e_check(c, dtype, q=q).ok
+
+
+def test_scene_key_check_accepts_float32_means_and_rejects_errors():
+    """check_scene_keys: a float32 running sum divided by P (either storage
+    dtype) passes; a key off by one bf16 ulp where the bound is tight, or a
+    sum that skips a primitive, fails."""
+    rng = np.random.default_rng(7)
+    S, P, d = 6, 300, 16
+    pk32 = rng.standard_normal((S, P, d)).astype(np.float32)
+    acc = np.zeros((S, d), dtype=np.float32)
+    for p in range(P):                                  # the library's order, float32
+        acc = (acc + pk32[:, p, :]).astype(np.float32)
+    lib32 = (acc / np.float32(P)).astype(np.float32)
+    rep = C.Report()
+    C.check_scene_keys(lib32, pk32, "f32", rep)
+    assert rep.ok, rep
+    # the same means stored as bf16 (keys of bf16 values, rounded once more)
+    pkb = O.round_to_dtype(pk32.astype(np.float64), "bf16").astype(np.float32)
+    accb = np.zeros((S, d), dtype=np.float32)
+    for p in range(P):
+        accb = (accb + pkb[:, p, :]).astype(np.float32)
+    libb = O.f64_to_bf16_bits(O.round_to_dtype((accb / np.float32(P)).astype(np.float64),
+                                               "bf16"))
+    rep = C.Report()
+    C.check_scene_keys(libb, O.f64_to_bf16_bits(pkb.astype(np.float64)), "bf16", rep)
+    assert rep.ok, rep
+    # planted mistakes: one primitive left out, and the sum not divided
+    bad = ((acc - pk32[:, 0, :]) / np.float32(P)).astype(np.float32)
+    rep = C.Report()
+    C.check_scene_keys(bad, pk32, "f32", rep)
+    assert not rep.ok
+    rep = C.Report()
+    C.check_scene_keys(acc, pk32, "f32", rep)
+    assert not rep.ok
+    # integer keys with P a power of two: the mean is exact in float32 and passes
+    ik = rng.integers(-2, 3, size=(3, 256, 8)).astype(np.float32)
+    exact = (ik.sum(axis=1) / 256).astype(np.float32)
+    rep = C.Report()
+    C.check_scene_keys(exact, ik, "f32", rep)
+    assert rep.ok, rep

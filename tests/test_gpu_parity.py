@@ -577,3 +577,44 @@ def test_benchmark_workloads_sampled(cfg):
         assert np.mean(r.scene[0].cpu().numpy() == lab) > 0.99
     del inp, r
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("case", ["bf16_ragged", "f32_small", "bf16_zipf_prims"])
+def test_scene_keys_eq4(case):
+    """lookme_scene_keys (Eq. 4) against the oracle's exact means within the
+    float32 summation bound (oracle/check.py:check_scene_keys), on the
+    primitive keys of seeded workloads: ragged sizes, fp32, and 4096
+    primitives a scene as in the Zipf workload."""
+    from oracle import check as C
+    from paper_2607_16305_amd import lookme as lk
+    from tests.harness import to_np
+    wl = {"bf16_ragged": SMALL["bf16_ragged_l2"], "f32_small": SMALL["f32_proj_l3"],
+          "bf16_zipf_prims": Workload("bf16_zipf_prims", "bf16", 16, 1, 512, 512, 48, 4096,
+                                      64, 64, 16, 20)}[case]
+    _announce(f"scene keys {case}: S={wl.scenes} P={wl.prims} d_e={wl.d_e} {wl.dtype}")
+    inp = make_inputs(wl, seed=3, device=DEV)
+    pk = inp["prim_keys"]
+    keys = lk.scene_keys(pk)
+    torch.cuda.synchronize()
+    rep = C.Report()
+    C.check_scene_keys(to_np(keys.cpu()), to_np(pk.cpu()), wl.dtype, rep)
+    assert rep.ok, str(rep)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_scene_keys_exact_on_integer_keys(dtype):
+    """Integer keys in [-2, 2] with P a power of two: every float32 partial
+    sum is exact and so is the division, so the library's keys must be the
+    correctly rounded means bit for bit."""
+    from paper_2607_16305_amd import lookme as lk
+    from tests.harness import to_np
+    _announce(f"scene keys exact {dtype}")
+    g = torch.Generator(device="cpu").manual_seed(11)
+    S, P, d = 5, 1024, 96 if dtype == "bf16" else 48
+    ik = torch.randint(-2, 3, (S, P, d), generator=g).to(torch.float32)
+    pk = ik.to(torch.bfloat16 if dtype == "bf16" else torch.float32).to(DEV)
+    keys = lk.scene_keys(pk)
+    torch.cuda.synchronize()
+    exact = O.round_to_dtype(ik.double().numpy().sum(axis=1) / P, dtype)
+    got = O.to_f64(to_np(keys.cpu()), dtype)
+    assert np.array_equal(got, exact)
