@@ -157,6 +157,22 @@ lookme_status_t lookme_lookup_select(lookme_t h, int32_t layers, int64_t n, cons
                                      int32_t* kept_out, void* stream);
 
 /*
+ * Index checks of the row adds.  Every entry point that gathers table rows
+ * for kept tokens (lookme_inject, lookme_inject_kept, lookme_inject_noalloc,
+ * the gated, fused, propagated and multi-scale injections) checks each kept
+ * entry's token id (in [0, n)), its scene (in [0, N_s), or in its scale's
+ * partition) and its k primitives (in [0, N_p)) on the device.  An entry
+ * with any of them out of range is not injected (its hidden row keeps its
+ * bits; where the rows feed the fusion or the scale mix, its retrieved row is
+ * zero) and is counted in the library's per-GPU index-error count instead.
+ *
+ * lookme_index_errors -- *count = the number of such entries since the last
+ * call on the current GPU, and resets it.  Ordered on `stream` and
+ * synchronises it (a debugging aid: the adds themselves never wait on it).
+ */
+lookme_status_t lookme_index_errors(void* stream, uint64_t* count);
+
+/*
  * lookme_inject -- sparse injection (Eq. 9-10) and residual add (Eq. 2).
  *   crit     [layers, n, d_c]   Delta of each layer (the attention update);
  *                               criticality c_t = ||crit_t||_2
@@ -214,9 +230,10 @@ lookme_status_t lookme_select(lookme_t h, int32_t layers, int64_t n, int64_t n_k
  * lookme_inject_kept -- the gather and residual add of lookme_inject (Eq. 10,
  * Eq. 2) for a kept set computed beforehand:
  *   kept [layers, n_keep] int32   token ids of each layer (kept_out of
- *                                 lookme_select); ids outside [0, n) are
- *                                 clamped into it, and an id listed twice in
- *                                 a layer races on its row of hidden
+ *                                 lookme_select); an id outside [0, n) is
+ *                                 not injected and is counted (see
+ *                                 lookme_index_errors), and an id listed
+ *                                 twice in a layer races on its row of hidden
  * The other arguments as for lookme_inject; the result is the same when kept
  * is the set lookme_select writes.  Needs no workspace.
  */
@@ -278,9 +295,9 @@ lookme_status_t lookme_set_fusion(lookme_t h, int32_t layers, int32_t d_ff, int3
  *   R = round(sum_i w[t,i] values[scene[t]*N_p + prim[t,i], :])   (value_dim)
  *   U = round(silu(w_gate[l] R) * (w_up[l] R))                     (d_ff)
  *   hidden[l, t, :] <- round(hidden[l, t, :] + w_down[l] U)        (d_h)
- * float32 accumulation throughout; every other row keeps its bits.  kept ids
- * outside [0, n) are clamped into it, and an id listed twice in a layer
- * races on its row.  d_h must be the fusion's.  Needs the workspace of
+ * float32 accumulation throughout; every other row keeps its bits.  A kept id
+ * outside [0, n) is not injected and is counted (lookme_index_errors), and
+ * an id listed twice in a layer races on its row.  d_h must be the fusion's.  Needs the workspace of
  * lookme_workspace_size (queried after lookme_set_fusion).
  */
 lookme_status_t lookme_inject_fused(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,

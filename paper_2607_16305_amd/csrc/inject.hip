@@ -46,14 +46,20 @@ __global__ __launch_bounds__(SEL_THREADS) void crit_select_kernel(
                    cache, sl);
 }
 
+// Rows of the injections whose kept id, scene or primitive index lay outside
+// its range since the counter was last read (lookme_index_errors): such a
+// row is not injected (in TO_R form its R row is written as zeros), so a
+// caller's bad index is counted instead of adding some other row into H.
+__device__ unsigned long long g_index_errors;
+
 // TO_R: the weighted row sum R of kept row j is rounded to the storage
 // dtype and written to row j of `hidden` (the fusion's or the multi-scale
 // router's input, [rows, d_v]) instead of being added into H.  Layer l reads
 // its kept list at kept + l * kept_batch (0: one list for all layers) and
-// its scenes (clamped into [0, S)) from scene l * scene_step of the table
-// (multi-scale: scale l's partition).  With a count array only the first
-// count entries of a kept list are used (count[l], or count[0] for a list
-// shared by all layers).
+// its scenes (in [0, S)) from scene l * scene_step of the table (multi-scale:
+// scale l's partition).  With a count array only the first count entries of
+// a kept list are used (count[l], or count[0] for a list shared by all
+// layers).
 template <int DT, int K, bool TO_R = false>
 __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
     int64_t n, int64_t n_keep, const int32_t* __restrict__ kept_all,
@@ -65,18 +71,29 @@ __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
   const int64_t layer = j / n_keep;
   // counted lists (the learned gate): entries past the list's count are unused
   if (count != nullptr && j - layer * n_keep >= count[kept_batch != 0 ? layer : 0]) return;
-  int64_t t = kept_all[layer * kept_batch + (j - layer * n_keep)];
-  t = t < 0 ? 0 : (t >= n ? n - 1 : t);
+  const int chunks = (int)(v_bytes / 16);
+  // an index out of range: count the row once and leave it out (every
+  // index below is uniform over the workgroup)
+  auto reject = [&]() {
+    if (threadIdx.x == 0) atomicAdd(&g_index_errors, 1ull);
+    if constexpr (TO_R)
+      for (int c = threadIdx.x; c < chunks; c += blockDim.x)
+        st16(hidden + j * v_bytes + (int64_t)c * 16, u32x4_t{0, 0, 0, 0});
+  };
+  const int64_t t = kept_all[layer * kept_batch + (j - layer * n_keep)];
+  if (t < 0 || t >= n) return reject();
   const int64_t row = layer * n + t;
-  int s = scene_all[row];
-  s = (s < 0 ? 0 : (s >= S ? S - 1 : s)) + (int)layer * scene_step;
+  const int s0 = scene_all[row];
+  if (s0 < 0 || s0 >= S) return reject();
+  const int s = s0 + (int)layer * scene_step;
   int64_t vrow[K];
   float wt[K];
+  bool bad = false;
 #pragma unroll
   for (int i = 0; i < K; ++i) {
     if (i < k) {
-      int p = prim_all[row * k + i];
-      p = p < 0 ? 0 : (p >= P ? P - 1 : p);
+      const int p = prim_all[row * k + i];
+      bad |= p < 0 || p >= P;
       vrow[i] = (int64_t)s * P + p;
       wt[i] = w_all[row * k + i];
     } else {
@@ -84,8 +101,8 @@ __global__ __launch_bounds__(INJ_THREADS) void inject_kernel(
       wt[i] = 0.f;
     }
   }
+  if (bad) return reject();
   char* h = TO_R ? hidden + j * v_bytes : hidden + row * h_bytes;
-  const int chunks = (int)(v_bytes / 16);
   for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
     u32x4_t vv[K];
 #pragma unroll
@@ -176,6 +193,19 @@ hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint3
     hipLaunchKernelGGL(crit_select_kernel<0>, dim3(layers), dim3(SEL_THREADS), 0, st, key, n,
                        n_keep, kept);
   return hipGetLastError();
+}
+
+hipError_t take_index_errors(hipStream_t st, uint64_t* out) {
+  static const unsigned long long zero = 0;
+  unsigned long long v = 0;
+  hipError_t e = hipMemcpyFromSymbolAsync(&v, HIP_SYMBOL(g_index_errors), sizeof(v), 0,
+                                          hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyToSymbolAsync(HIP_SYMBOL(g_index_errors), &zero, sizeof(zero), 0,
+                               hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e == hipSuccess) *out = v;
+  return e;
 }
 
 hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,

@@ -202,6 +202,9 @@ hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uin
                             hipStream_t st);
 hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint32_t* key,
                               int32_t* kept, hipStream_t st);
+// The injections' count of rows with an index out of range (see
+// inject_kernel), read and reset on `st` (synchronising it).
+hipError_t take_index_errors(hipStream_t st, uint64_t* out);
 hipError_t launch_inject_rows(int dt, int layers, int64_t n, int64_t n_keep, const int32_t* kept,
                               const int32_t* scene, const int32_t* prim, const float* w,
                               const void* values, int S, int P, int d_v, int k, void* hidden,

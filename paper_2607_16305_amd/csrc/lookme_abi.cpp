@@ -970,6 +970,12 @@ lookme_status_t lookme_inject_propagated_gated(lookme_t h, int32_t steps, int64_
                     "fusion launch");
 }
 
+lookme_status_t lookme_index_errors(void* stream, uint64_t* count) {
+  if (count == nullptr) return fail(LOOKME_ERR_INVALID, "count is NULL");
+  return hip_status(lookme::take_index_errors(static_cast<hipStream_t>(stream), count),
+                    "reading the index-error count");
+}
+
 lookme_status_t lookme_scene_keys(const lookme_desc_t* desc, const void* prim_keys,
                                   void* scene_keys, void* stream) {
   if (desc == nullptr) return fail(LOOKME_ERR_INVALID, "desc is NULL");

@@ -34,7 +34,7 @@ EXPORTED = ("lookme_create", "lookme_workspace_size", "lookme_set_workspace", "l
             "lookme_inject_multiscale_gated", "lookme_gate",
             "lookme_inject_gated", "lookme_inject_fused_gated", "lookme_inject_propagated_gated",
             "lookme_inject_text", "lookme_lookup_select", "lookme_lookup_gate",
-            "lookme_scene_keys",
+            "lookme_scene_keys", "lookme_index_errors",
             "lookme_destroy", "lookme_last_error",
             "lookme_profile_enable", "lookme_profile_read", "lookme_inject_noalloc")
 
@@ -107,6 +107,7 @@ def load():
         "lookme_inject_propagated_gated": [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp,
                                            _vp, _vp, _vp, ctypes.c_int32, _vp],
         "lookme_scene_keys": [ctypes.POINTER(lookme_desc_t), _vp, _vp, _vp],
+        "lookme_index_errors": [_vp, ctypes.POINTER(ctypes.c_uint64)],
         "lookme_inject_text": [ctypes.c_int32, _vp, ctypes.c_int64, ctypes.c_int32,
                                ctypes.c_int64, _vp, _vp, _vp, _vp, _vp, ctypes.c_int64,
                                ctypes.c_int32, _vp],
@@ -286,6 +287,14 @@ def lookme_inject_propagated_gated(h, steps, n, kept, count, scene, prim, w, hid
     _check(load().lookme_inject_propagated_gated(h, steps, n, _ptr(kept), _ptr(count),
                                                  _ptr(scene), _ptr(prim), _ptr(w), _ptr(hidden),
                                                  d_h, _stream(stream)))
+
+
+def lookme_index_errors(stream=None):
+    """Kept entries left out for an index out of range since the last call
+    (read and reset; synchronises the stream)."""
+    v = ctypes.c_uint64(0)
+    _check(load().lookme_index_errors(_stream(stream), ctypes.byref(v)))
+    return v.value
 
 
 def lookme_scene_keys(desc, prim_keys, scene_keys, stream=None):

@@ -420,3 +420,8 @@ def test_scene_keys_validates(lib):
         lk.LOOKME_ERR_UNSUPPORTED
     assert S(lambda: sk(p=None)) == lk.LOOKME_ERR_INVALID
     assert S(lambda: sk(o=FAKE + 4)) == lk.LOOKME_ERR_INVALID
+
+
+def test_index_errors_validates(lib):
+    """lookme_index_errors needs somewhere to write the count."""
+    assert lib.lookme_index_errors(None, None) == lk.LOOKME_ERR_INVALID

@@ -618,3 +618,45 @@ def test_scene_keys_exact_on_integer_keys(dtype):
     exact = O.round_to_dtype(ik.double().numpy().sum(axis=1) / P, dtype)
     got = O.to_f64(to_np(keys.cpu()), dtype)
     assert np.array_equal(got, exact)
+
+
+def test_out_of_range_indices_are_counted_not_injected():
+    """Kept entries with a token id, scene or primitive out of range are left
+    out (their hidden rows keep their bits), every other kept row gets the
+    same bits as with a clean list, and lookme_index_errors reports the bad
+    entries once (then zero)."""
+    from paper_2607_16305_amd import lookme as lk
+    from tests.harness import Run
+    wl = SMALL["bf16_ragged_l2"]
+    _announce("index errors bf16_ragged_l2")
+    inp = make_inputs(wl, seed=5, device=DEV)
+    ref = Run(inp).run()
+    torch.cuda.synchronize()
+    assert lk.lookme_index_errors() == 0   # nothing counted by a clean pass
+    L, n = ref.L, ref.n
+    kept = ref.kept.clone()
+    scene = ref.scene.clone()
+    prim = ref.prim.clone()
+    bad_tokens = []
+    kept[0, 0] = -1                          # token id below the range
+    kept[1, 1] = n                           # and above it
+    t2 = int(kept[0, 2])
+    scene[0, t2] = wl.scenes                 # scene out of range
+    t3 = int(kept[1, 3])
+    prim[1, t3, wl.top_k - 1] = wl.prims     # one primitive out of range
+    bad_tokens = [(0, t2), (1, t3)]
+    hidden = inp["hidden"].clone()
+    ref.table.inject_kept(kept, scene, prim, ref.w, hidden, ref.n_keep, layers=L)
+    assert lk.lookme_index_errors() == 4
+    assert lk.lookme_index_errors() == 0
+    # the bad entries' rows (where they exist) keep their bits
+    for l, t in bad_tokens:
+        assert torch.equal(hidden[l, t], inp["hidden"][l, t])
+    # every other kept row as injected by the clean pass; the rest untouched
+    skip = {(0, int(ref.kept[0, 0])), (1, int(ref.kept[1, 1]))} | set(bad_tokens)
+    for l in range(L):
+        for t in ref.kept[l].tolist():
+            if (l, t) in skip:
+                assert torch.equal(hidden[l, t], inp["hidden"][l, t])
+            else:
+                assert torch.equal(hidden[l, t], ref.hidden[l, t]), (l, t)
