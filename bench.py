@@ -98,8 +98,10 @@ def parse():
 
 CALIB_BYTES = 256 << 20
 SCORE_KERNEL = "score_kernel"
-KERNEL_SOURCES = ("paper_2607_16305_amd/csrc/score.hip", "paper_2607_16305_amd/csrc/common.h",
-                  "paper_2607_16305_amd/csrc/kernels.h", "paper_2607_16305_amd/csrc/crit.h")
+KERNEL_SOURCES = ("paper_2607_16305_amd/csrc/score.hip", "paper_2607_16305_amd/csrc/topk.h",
+                  "paper_2607_16305_amd/csrc/common.h", "paper_2607_16305_amd/csrc/kernels.h",
+                  "paper_2607_16305_amd/csrc/crit.h", "paper_2607_16305_amd/csrc/dtl.h",
+                  "paper_2607_16305_amd/csrc/route_merge.h")
 
 
 def kernel_source_sha() -> str:

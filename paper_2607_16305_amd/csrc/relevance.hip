@@ -1,25 +1,33 @@
 // Level-2 in the paper's own form (arXiv 2607.16305, Sec. 3.2, Eq. 6-7):
 // a scene-shared two-layer MLP on [v_e, e_img[j]] gives one relevance logit
 // per primitive, the top k primitives by logit are kept, and their weights
-// are the softmax of cos(v_e, e_{j,p}) + tanh(r_j[p]).  Four launches:
+// are the softmax of cos(v_e, e_{j,p}) + tanh(r_j[p]).  Launches:
 //
 //   tile_gemm_kernel (hidden)  a = round(ReLU([q_t, K1[scene_t]] W1^T + b1)):
 //                             64 x 64 output tiles on the matrix cores, the
 //                             operand-A row of token t being its query
 //                             followed by its scene's key (gathered per row,
 //                             K stages of 128 bytes straight into LDS);
-//   tile_gemm_kernel (logits)  r = a W2^T + b2 in float32, to the workspace
-//                             (large products: the projection's 256 x 256
-//                             tile kernel with a float32 + bias epilogue);
-//   relevance_topk_kernel     one wave per row: the k largest logits (lowest
-//                             p on ties), each lane keeping a sorted list of
-//                             its strided share, merged across the wave;
+//   relevance_topk_fused_kernel  r = a W2^T + b2 and its top k per row in one
+//                             pass: 64 rows a unit (a 16-row tile a wave),
+//                             the rows of W2 streamed through a ring of LDS
+//                             block images as the Level-2 scoring kernel
+//                             streams a scene's keys, each score + b2 folded
+//                             into per-lane sorted lists, no logit written;
+//                             with few row blocks the rows of W2 are split
+//                             over several units and relevance_merge_kernel
+//                             merges their lists;
 //   relevance_weights_kernel  one wave per row: the k cosines against the
 //                             chosen primitive keys, + tanh of the logits,
 //                             softmax over the k.
+// Hidden widths the fused kernel does not take (rows other than 512 or 1024
+// bytes) run the logits as a product into the workspace (float32) and
+// relevance_topk_kernel (one wave per row) instead.
 #include "common.h"
+#include "dtl.h"
 #include "kernels.h"
 #include "tile_gemm.h"
+#include "topk.h"
 
 namespace lookme {
 
@@ -105,6 +113,225 @@ __global__ __launch_bounds__(256) void relevance_topk_kernel(const float* __rest
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fused second layer and top-k
+// ---------------------------------------------------------------------------
+struct RelTopkParams {
+  const char* act;      // [rows, hidden] hidden activations (storage dtype)
+  const char* w2;       // [P, hidden]
+  const float* b2;      // [P]
+  int64_t rows;
+  int64_t row_bytes;    // hidden * elem size: 64 KS
+  int P, k;
+  int splits;           // ranges of W2 rows per row block
+  int kps;              // W2 rows per range (a multiple of 16)
+  int units;            // row blocks * splits
+  int32_t* prim;        // [rows, k] (splits == 1)
+  float* top;           // [rows, k] the k logits, best first (splits == 1)
+  uint64_t* part;       // [rows, splits, k] (idx << 32 | logit bits) (splits > 1)
+};
+
+constexpr int RT_WAVES = 4, RT_THREADS = RT_WAVES * WAVE, RT_ROWS = 16 * RT_WAVES;
+constexpr int RT_NBUF = 4;       // block images in the ring: three in flight while one is used
+constexpr int RT_MAX_KPS = 4096; // W2 rows of one range: their b2 is kept in LDS
+
+// One unit: rows [64 b, 64 b + 64) of the batch against W2 rows [kps s,
+// kps s + kps), split s.  Wave w holds the query fragments of rows
+// 64 b + 16 w + n (lane (g, n): chunks 4 j + g) and scores each 16-key block
+// (keys as MFMA operand A, rows as B), adds b2 and keeps per-lane sorted
+// lists of the KL best (values below the largest k-th entry of the row's
+// four lists dropped; keys arrive in increasing index, so equal logits keep
+// the lower index first); the four lists of a row are merged inside the
+// wave.  The blocks go straight from global memory into a ring of LDS
+// images (contiguous KiB loads, the layout of KeyImage), every wave issuing
+// its share of each block's loads; W2 is read by every row block, so the
+// loads keep the temporal cache policy.  The range's b2 is copied to LDS
+// first (zero past its end), so the loop's only global loads are the ring's,
+// whose count the waits below name.
+template <int DT, int KS, int KL>
+__global__ __launch_bounds__(RT_THREADS) void relevance_topk_fused_kernel(RelTopkParams a) {
+  constexpr int BLOCK = KS * 1024;
+  constexpr int PW = KS / RT_WAVES;   // load instructions a wave issues per block
+  static_assert(KS % RT_WAVES == 0 && KS <= 16, "whole load shares, fragments in registers");
+  // one LDS object (ring, then the range's b2): a second one would make the
+  // compiler wait for every load into LDS before each read of the ring
+  __shared__ __attribute__((aligned(1024))) char smem[RT_NBUF * BLOCK + RT_MAX_KPS * 4];
+  float* bl = reinterpret_cast<float*>(smem + RT_NBUF * BLOCK);
+  const int u = xcd_remap(blockIdx.x, a.units);
+  if (u < 0) return;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = lane & 15, g = lane >> 4;
+  const int64_t rb = u / a.splits;
+  const int split = u % a.splits;
+  const int64_t r0 = rb * RT_ROWS;
+  const int nr = (int)min<int64_t>(RT_ROWS, a.rows - r0);
+  const bool has_rows = 16 * wv < nr;   // waves without rows only help to load
+  const int k0 = split * a.kps, k1 = min(a.P, k0 + a.kps);
+  const int b0 = k0 >> 4, b1 = (k1 + 15) >> 4;
+
+  for (int i = threadIdx.x; i < (b1 - b0) * 16; i += RT_THREADS)
+    bl[i] = k0 + i < k1 ? a.b2[k0 + i] : 0.f;
+  __syncthreads();
+
+  u32x4_t qf[KS];
+  {
+    const char* row = a.act + (r0 + min(16 * wv + n, nr - 1)) * a.row_bytes + g * 16;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) qf[j] = ld16(row + j * 64);
+  }
+  KeyImage im;
+  im.rb = a.row_bytes;
+  im.C = 4 * KS;
+  im.G = im.C < 16 ? im.C : 16;
+  uint32_t off[PW];
+#pragma unroll
+  for (int t = 0; t < PW; ++t) {
+    const int i = wv + RT_WAVES * t;
+    off[t] = im.src_off(i, lane, im.row_of(i, lane));
+  }
+  uint32_t fbase[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) fbase[t] = im.frag_off(t, g, n);
+  // the loads of block blk of W2 (rows from P on read row P - 1: they are
+  // masked by index when folded)
+  auto issue = [&](int blk) {
+    if (blk >= b1) return;
+    const int row0 = blk * 16;
+    const bool ragged = row0 + 16 > a.P;   // uniform
+    const char* src = a.w2 + (int64_t)row0 * a.row_bytes;
+    char* img = smem + ((blk - b0) % RT_NBUF) * BLOCK;
+#pragma unroll
+    for (int t = 0; t < PW; ++t) {
+      const int i = wv + RT_WAVES * t;
+      uint32_t o = off[t];
+      if (ragged) {
+        const int r = im.row_of(i, lane);
+        o = im.src_off(i, lane, row0 + r < a.P ? r : a.P - 1 - row0);
+      }
+      load_lds16(src + o, img + i * 1024);
+    }
+  };
+
+  float ls[KL];
+  int li[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
+#pragma unroll
+  for (int b = 0; b < RT_NBUF - 1; ++b) issue(b0 + b);
+  for (int blk = b0; blk < b1; ++blk) {
+    // this wave's loads of block blk have landed once at most those of the
+    // RT_NBUF - 2 younger blocks are outstanding (near the end, once all
+    // have); the barrier makes every wave's visible and ends every read of
+    // block blk - 1, whose image the next loads overwrite (a plain
+    // s_barrier: the fence of __syncthreads would wait for every load)
+    if (blk + RT_NBUF - 2 < b1)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((RT_NBUF - 2) * PW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(blk + RT_NBUF - 1);
+    if (has_rows) {
+      const char* img = smem + ((blk - b0) % RT_NBUF) * BLOCK;
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < KS; ++j) {
+        const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(img + fbase[j & 3] + 256 * (j >> 2));
+        acc = mfma_chunk<DT>(kf, qf[j], acc);
+      }
+      fold_scores<true, KL, true>(acc, blk, g, k1, bl + (blk - b0) * 16, ls, li);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
+  if (!has_rows) return;
+  float top_s[KL];
+  int top_i[KL];
+  merge_lists<KL, 2>(ls, li, a.k, 16, top_s, top_i);
+  const int slot = 16 * wv + n;
+  if (g != 0 || slot >= nr) return;
+  const int64_t t = r0 + slot;
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    if (e < a.k) {
+      if (a.splits == 1) {
+        a.prim[t * a.k + e] = top_i[e];
+        a.top[t * a.k + e] = top_s[e];
+      } else {
+        a.part[(t * a.splits + split) * a.k + e] =
+            ((uint64_t)(uint32_t)top_i[e] << 32) | __float_as_uint(top_s[e]);
+      }
+    }
+  }
+}
+
+// One wave per row: lane j < splits holds range j's list of the row; the
+// butterfly of merge_lists over 16 lanes orders their union by the rule of
+// one unit over all of W2 (a range with fewer than k rows pads its list
+// with -inf, which the P >= k real logits outrank).
+template <int KL>
+__global__ __launch_bounds__(256) void relevance_merge_kernel(const uint64_t* __restrict__ part,
+                                                              int64_t rows, int splits, int k,
+                                                              int32_t* __restrict__ prim,
+                                                              float* __restrict__ top) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= rows) return;
+  float ls[KL], ms[KL];
+  int li[KL], mi[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    ls[e] = -__builtin_inff();
+    li[e] = -1;
+    if (lane < splits && e < k) {
+      const uint64_t v = part[(t * splits + lane) * k + e];
+      ls[e] = __uint_as_float((uint32_t)v);
+      li[e] = (int)(v >> 32);
+    }
+  }
+  merge_lists<KL, 4>(ls, li, k, 1, ms, mi);
+  if (lane != 0) return;
+#pragma unroll
+  for (int e = 0; e < KL; ++e)
+    if (e < k) {
+      prim[t * k + e] = mi[e];
+      top[t * k + e] = ms[e];
+    }
+}
+
+// Ranges of W2 rows per row block: enough units to fill the chip's 512
+// resident workgroups, each range at least 128 rows (and k), and as many as
+// keep a range's b2 within its LDS space; 0 when that takes more than 16.
+static int relevance_splits(int64_t row_blocks, int P, int k) {
+  int splits = 1;
+  while (splits < 16 && row_blocks * splits < 512 && P / (2 * splits) >= 128 &&
+         P / (2 * splits) >= k)
+    splits *= 2;
+  while (splits <= 16 && (P + splits - 1) / splits > RT_MAX_KPS) splits *= 2;
+  return splits <= 16 ? splits : 0;
+}
+
+template <int DT, int KS, int KL>
+static hipError_t launch_topk_fused(const RelTopkParams& p0, float* part_ws, hipStream_t st) {
+  RelTopkParams p = p0;
+  const int64_t row_blocks = (p.rows + RT_ROWS - 1) / RT_ROWS;
+  p.splits = relevance_splits(row_blocks, p.P, p.k);
+  p.kps = ((p.P + p.splits - 1) / p.splits + 15) / 16 * 16;
+  p.splits = (p.P + p.kps - 1) / p.kps;   // no empty range
+  // the lists of a split live in the logits' workspace ([rows, P] float32)
+  if (p.splits > 1 && (int64_t)p.splits * p.k * 2 > p.P) return hipErrorInvalidValue;
+  p.units = (int)(row_blocks * p.splits);
+  p.part = reinterpret_cast<uint64_t*>(part_ws);
+  hipLaunchKernelGGL((relevance_topk_fused_kernel<DT, KS, KL>), dim3((unsigned)((p.units + 7) / 8 * 8)),
+                     dim3(RT_THREADS), 0, st, p);
+  if (p.splits > 1)
+    hipLaunchKernelGGL((relevance_merge_kernel<KL>), dim3((unsigned)((p.rows + 3) / 4)), dim3(256), 0,
+                       st, p.part, p.rows, p.splits, p.k, p.prim, p.top);
+  return hipGetLastError();
+}
+
 // One wave per row: cosines of q_t with its k chosen primitive keys, plus
 // tanh of their logits (read from w), softmax over the k, written to w.
 template <int DT, int K>
@@ -182,6 +409,30 @@ __global__ __launch_bounds__(256) void relevance_weights_kernel(
   if (lane < k) w[t * k + lane] = ex / sum;
 }
 
+static hipError_t launch_relevance_weights(int dt, const void* q, const int32_t* scene,
+                                           const void* prim_keys, const int32_t* prim, float* w,
+                                           int64_t rows, int S, int P, int k, int64_t q_bytes,
+                                           hipStream_t st) {
+  const dim3 wgrid((unsigned)((rows + 3) / 4));
+#define LOOKME_RW(DT_, K_)                                                                       \
+  hipLaunchKernelGGL((relevance_weights_kernel<DT_, K_>), wgrid, dim3(256), 0, st,             \
+                     static_cast<const char*>(q), scene, static_cast<const char*>(prim_keys), \
+                     prim, w, rows, S, P, k, q_bytes)
+  if (dt == DT_BF16) {
+    if (k <= 4) LOOKME_RW(DT_BF16, 4);
+    else if (k <= 8) LOOKME_RW(DT_BF16, 8);
+    else if (k <= 16) LOOKME_RW(DT_BF16, 16);
+    else LOOKME_RW(DT_BF16, 32);
+  } else {
+    if (k <= 4) LOOKME_RW(DT_F32, 4);
+    else if (k <= 8) LOOKME_RW(DT_F32, 8);
+    else if (k <= 16) LOOKME_RW(DT_F32, 16);
+    else LOOKME_RW(DT_F32, 32);
+  }
+#undef LOOKME_RW
+  return hipGetLastError();
+}
+
 hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const void* scene_keys,
                             const void* prim_keys, const RelevanceMlp& mlp, int64_t rows, int d_e,
                             int S, int P, int k, void* act, int32_t* prim, float* w,
@@ -206,6 +457,41 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
   g1.tiles = (int)(rt * ((mlp.hidden + TgShape::BN - 1) / TgShape::BN));
   hipError_t e = launch_tile_gemm<EPI_ACT>(dt, g1, 1, st);
   if (e != hipSuccess) return e;
+  const int64_t hb = (int64_t)mlp.hidden * es;
+  if ((hb == 1024 || hb == 512) && relevance_splits((rows + RT_ROWS - 1) / RT_ROWS, P, k) > 0) {
+    // second layer and top-k fused (no float32 logits written); the ranges'
+    // lists of a split go to the logits' workspace
+    RelTopkParams p{};
+    p.act = static_cast<const char*>(act);
+    p.w2 = static_cast<const char*>(mlp.w2);
+    p.b2 = mlp.b2;
+    p.rows = rows;
+    p.row_bytes = hb;
+    p.P = P;
+    p.k = k;
+    p.prim = prim;
+    p.top = w;
+#define LOOKME_RT(KS_)                                                                 \
+  do {                                                                                 \
+    if (dt == DT_BF16) {                                                               \
+      if (k <= 4) e = launch_topk_fused<DT_BF16, KS_, 4>(p, logits, st);               \
+      else if (k <= 8) e = launch_topk_fused<DT_BF16, KS_, 8>(p, logits, st);          \
+      else if (k <= 16) e = launch_topk_fused<DT_BF16, KS_, 16>(p, logits, st);        \
+      else e = launch_topk_fused<DT_BF16, KS_, 32>(p, logits, st);                     \
+    } else {                                                                           \
+      if (k <= 4) e = launch_topk_fused<DT_F32, KS_, 4>(p, logits, st);                \
+      else if (k <= 8) e = launch_topk_fused<DT_F32, KS_, 8>(p, logits, st);           \
+      else if (k <= 16) e = launch_topk_fused<DT_F32, KS_, 16>(p, logits, st);         \
+      else e = launch_topk_fused<DT_F32, KS_, 32>(p, logits, st);                      \
+    }                                                                                  \
+  } while (0)
+    if (hb == 1024) LOOKME_RT(16);
+    else LOOKME_RT(8);
+#undef LOOKME_RT
+    if (e != hipSuccess) return e;
+    return launch_relevance_weights(dt, q, scene, prim_keys, prim, w, rows, S, P, k,
+                                    (int64_t)d_e * es, st);
+  }
   // logits: r = a W2^T + b2, float32
   TileGemmParams g2{};
   g2.a0 = static_cast<const char*>(act);
@@ -235,23 +521,8 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
     hipLaunchKernelGGL(relevance_topk_kernel<32>, wgrid, dim3(256), 0, st, logits, rows, P, k, prim, w);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-#define LOOKME_RW(DT_, K_)                                                                       \
-  hipLaunchKernelGGL((relevance_weights_kernel<DT_, K_>), wgrid, dim3(256), 0, st,             \
-                     static_cast<const char*>(q), scene, static_cast<const char*>(prim_keys), \
-                     prim, w, rows, S, P, k, (int64_t)d_e * es)
-  if (dt == DT_BF16) {
-    if (k <= 4) LOOKME_RW(DT_BF16, 4);
-    else if (k <= 8) LOOKME_RW(DT_BF16, 8);
-    else if (k <= 16) LOOKME_RW(DT_BF16, 16);
-    else LOOKME_RW(DT_BF16, 32);
-  } else {
-    if (k <= 4) LOOKME_RW(DT_F32, 4);
-    else if (k <= 8) LOOKME_RW(DT_F32, 8);
-    else if (k <= 16) LOOKME_RW(DT_F32, 16);
-    else LOOKME_RW(DT_F32, 32);
-  }
-#undef LOOKME_RW
-  return hipGetLastError();
+  return launch_relevance_weights(dt, q, scene, prim_keys, prim, w, rows, S, P, k,
+                                  (int64_t)d_e * es, st);
 }
 
 }  // namespace lookme

@@ -371,8 +371,19 @@ def test_layers_batched_equal_sequential():
 # Level-2 in the paper's form (Eq. 6-7): (workload, hidden width, sampled
 # tokens or None for all).  Ragged rows and primitive counts (200, 37, 300)
 # leave partial 64 x 64 tiles in both layers; the image and multi-scale
-# cases have the benchmarks' shapes.
+# cases have the benchmarks' shapes.  Hidden rows of 512 or 1024 bytes take
+# the fused second layer + top-k: the "fused" cases cover both widths in
+# both dtypes, a ragged last block of W2 rows (P 37, 300, 1000), W2 split
+# into ranges merged afterwards (P 300 over 2, P 1000 over 4 with a short
+# last range, the image shape over 8) and one range of 4096 rows (Zipf).
 RELEVANCE = {
+    "bf16_rel_fused_h256": (Workload("bf16_rel_fused_h256", "bf16", 130, 1, 128, 64, 7, 300, 32,
+                                     32, 32, 30, usage="uniform"), 256, None),
+    "f32_rel_fused_h128": (Workload("f32_rel_fused_h128", "f32", 77, 1, 96, 64, 5, 37, 40, 40,
+                                    3, 40, usage="iid"), 128, None),
+    "f32_rel_fused_h256": (Workload("f32_rel_fused_h256", "f32", 200, 1, 96, 64, 6, 1000, 40, 40,
+                                    8, 40, usage="uniform"), 256, None),
+    "bf16_rel_zipf": (WORKLOADS[4], 512, 40),
     "bf16_rel_l2": (Workload("bf16_rel_l2", "bf16", 300, 2, 256, 128, 20, 200, 64, 64, 8, 30,
                              usage="uniform"), 192, None),
     "f32_rel": (Workload("f32_rel", "f32", 77, 1, 96, 64, 5, 37, 40, 40, 3, 40, usage="iid"),
