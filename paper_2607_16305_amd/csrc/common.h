@@ -19,6 +19,7 @@ enum : int { DT_F32 = 0, DT_BF16 = 1 };
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int WAVE = 64;
@@ -81,8 +82,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 // Ordering used by every selection: larger score first, equal scores by
 // smaller index.  Index -1 marks an empty slot (score -inf).
+// (bitwise operators: with || and && the compiler branches on the exec mask)
 __device__ __forceinline__ bool beats(float s, int i, float t, int j) {
-  return s > t || (s == t && (unsigned)i < (unsigned)j);
+  return (s > t) | ((s == t) & ((unsigned)i < (unsigned)j));
 }
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }

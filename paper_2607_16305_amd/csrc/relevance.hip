@@ -8,12 +8,15 @@
 //                             operand-A row of token t being its query
 //                             followed by its scene's key (gathered per row,
 //                             K stages of 128 bytes straight into LDS);
-//   relevance_topk_fused_kernel  r = a W2^T + b2 and its top k per row in one
-//                             pass: 64 rows a unit (a 16-row tile a wave),
-//                             the rows of W2 streamed through a ring of LDS
-//                             block images as the Level-2 scoring kernel
+//   relevance_topk32_kernel / relevance_topk_fused_kernel
+//                             r = a W2^T + b2 and its top k per row in one
+//                             pass, the rows of W2 streamed through a ring of
+//                             LDS block images as the Level-2 scoring kernel
 //                             streams a scene's keys, each score + b2 folded
-//                             into per-lane sorted lists, no logit written;
+//                             into per-lane sorted lists, no logit written:
+//                             bf16 batches of 4096 rows or more with k <= 16
+//                             on 32 x 32 tiles (128 rows a unit, 32 a wave),
+//                             the rest on 16 x 16 tiles (64 rows a unit);
 //                             with few row blocks the rows of W2 are split
 //                             over several units and relevance_merge_kernel
 //                             merges their lists;
@@ -139,15 +142,16 @@ constexpr int RT_MAX_KPS = 4096; // W2 rows of one range: their b2 is kept in LD
 // kps s + kps), split s.  Wave w holds the query fragments of rows
 // 64 b + 16 w + n (lane (g, n): chunks 4 j + g) and scores each 16-key block
 // (keys as MFMA operand A, rows as B), adds b2 and keeps per-lane sorted
-// lists of the KL best (values below the largest k-th entry of the row's
-// four lists dropped; keys arrive in increasing index, so equal logits keep
-// the lower index first); the four lists of a row are merged inside the
-// wave.  The blocks go straight from global memory into a ring of LDS
-// images (contiguous KiB loads, the layout of KeyImage), every wave issuing
-// its share of each block's loads; W2 is read by every row block, so the
-// loads keep the temporal cache policy.  The range's b2 is copied to LDS
-// first (zero past its end), so the loop's only global loads are the ring's,
-// whose count the waits below name.
+// lists of the KL best (values below the bound of fold_scores dropped; keys
+// arrive in increasing index, so equal logits keep the lower index first);
+// the four lists of a row are merged inside the wave.  The blocks go
+// straight from global memory into a ring of LDS images (contiguous KiB
+// loads, the layout of KeyImage), every wave issuing its share of each
+// block's loads; W2 is read by every row block, so the loads keep the
+// temporal cache policy.  The range's b2 is copied to LDS first (zero past
+// its end), so the loop's only global loads are the ring's, whose count the
+// waits below name.  (float32, and lists longer than 16, and small batches;
+// bf16 otherwise takes the 32 x 32 form below.)
 template <int DT, int KS, int KL>
 __global__ __launch_bounds__(RT_THREADS) void relevance_topk_fused_kernel(RelTopkParams a) {
   constexpr int BLOCK = KS * 1024;
@@ -217,6 +221,7 @@ __global__ __launch_bounds__(RT_THREADS) void relevance_topk_fused_kernel(RelTop
   int li[KL];
 #pragma unroll
   for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
+  const bool tight = a.k == KL;
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
 #pragma unroll
@@ -242,7 +247,7 @@ __global__ __launch_bounds__(RT_THREADS) void relevance_topk_fused_kernel(RelTop
         const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(img + fbase[j & 3] + 256 * (j >> 2));
         acc = mfma_chunk<DT>(kf, qf[j], acc);
       }
-      fold_scores<true, KL, true>(acc, blk, g, k1, bl + (blk - b0) * 16, ls, li);
+      fold_scores<true, KL, true>(acc, blk, g, k1, bl + (blk - b0) * 16, ls, li, tight);
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
@@ -267,32 +272,258 @@ __global__ __launch_bounds__(RT_THREADS) void relevance_topk_fused_kernel(RelTop
   }
 }
 
-// One wave per row: lane j < splits holds range j's list of the row; the
-// butterfly of merge_lists over 16 lanes orders their union by the rule of
-// one unit over all of W2 (a range with fewer than k rows pads its list
-// with -inf, which the P >= k real logits outrank).
+// ---------------------------------------------------------------------------
+// bf16: the second layer on 32 x 32 tiles
+// ---------------------------------------------------------------------------
+// A unit is 128 rows (32 a wave) against a range of W2 rows taken 32 at a
+// time: v_mfma_f32_32x32x16_bf16 with the 32 keys as operand A and the
+// wave's 32 rows as B leaves lane (h, n) = (L >> 5, L & 31) with the 16
+// scores of keys 8 j + 4 h + r (j, r < 4) of the block for row n, so a row's
+// candidates sit in two lanes (n, n + 32) instead of four, each lane folds 16
+// values at a time, and every key fragment read from LDS feeds a 32-row
+// product: per (row, key) pair about half the list upkeep and half the LDS
+// reads of the 16 x 16 form.  The keys stream through the same ring of
+// 16-row LDS block images (a 32-key block is two consecutive images: key m
+// in image m >> 4, row m & 15); the B operand of step s is the 16 bytes
+// [32 s + 16 h, +16) of the lane's row, A the same bytes of key n's row.
+// 32 WAVES-row units and a ring of WAVES x 16 KiB of 16-row images (at most
+// 16 images); the library runs WAVES = 4: 128-row units, a 64 KiB ring
+// (4 images at 1 KiB rows: one 32-key block in flight while one is used; 8
+// at 512 bytes: three) and two workgroups a CU.  (A 256-row form with a
+// 128 KiB ring, one workgroup a CU, measured slower at the Zipf shape.)
+template <int KS, int WAVES>
+constexpr int r32_images() {
+  return (WAVES * 16 * 1024) / (KS * 1024) > 16 ? 16 : (WAVES * 16 * 1024) / (KS * 1024);
+}
+
+// 16 scores of one row (keys pbase + 8 (i >> 2) + (i & 3)) folded into the
+// lane's sorted list: the largest first, the first of equal values (the
+// lower key) first, one wave-wide insertion round per value that still
+// beats some lane's list; values below T (see fold_scores) are dropped.
 template <int KL>
+__device__ __forceinline__ void fold16(float (&v)[16], int pbase, float T, float (&ls)[KL],
+                                       int (&li)[KL]) {
+#pragma unroll 1
+  for (int round = 0; round < 16; ++round) {
+    float x = v[0];
+    int w = 0;
+#pragma unroll
+    for (int i = 1; i < 16; ++i) {
+      const bool gt = v[i] > x;
+      x = gt ? v[i] : x;
+      w = gt ? i : w;
+    }
+    if (!(x >= T)) x = -__builtin_inff();
+    if (!__any(x > ls[KL - 1])) break;
+    const int p = pbase + 8 * (w >> 2) + (w & 3);
+#pragma unroll
+    for (int e = KL - 1; e >= 1; --e) {
+      const bool above_prev = x > ls[e - 1];
+      const bool above_cur = x > ls[e];
+      const int kept = above_cur ? p : li[e];
+      li[e] = above_prev ? li[e - 1] : kept;
+      ls[e] = __builtin_amdgcn_fmed3f(x, ls[e - 1], ls[e]);
+    }
+    li[0] = x > ls[0] ? p : li[0];
+    ls[0] = fmaxf(x, ls[0]);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = i == w ? -__builtin_inff() : v[i];
+  }
+}
+
+// The maximum (minimum) over lanes L and L ^ 32.
+__device__ __forceinline__ float max_half(float v) {
+  float a, b;
+  pair32(v, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float min_half(float v) {
+  float a, b;
+  pair32(v, a, b);
+  return fminf(a, b);
+}
+
+template <int KS, int KL, int WAVES>
+__global__ __launch_bounds__(WAVES * WAVE) void relevance_topk32_kernel(RelTopkParams a) {
+  constexpr int IMG = KS * 1024;                 // one 16-row image
+  constexpr int NIMG = r32_images<KS, WAVES>();  // images in the ring (an even count)
+  constexpr int NB = NIMG / 2;                   // 32-key blocks in the ring
+  constexpr int NS = 2 * KS;                     // 32-byte K steps a row
+  constexpr int PW = 2 * KS / WAVES;             // load instructions a wave issues per block
+  constexpr int ROWS = 32 * WAVES;
+  static_assert(NB >= 2 && (2 * KS) % WAVES == 0, "ring of at least two blocks, whole shares");
+  // one LDS object (ring, then the range's b2)
+  __shared__ __attribute__((aligned(1024))) char smem[NIMG * IMG + RT_MAX_KPS * 4];
+  float* bl = reinterpret_cast<float*>(smem + NIMG * IMG);
+  const int u = xcd_remap(blockIdx.x, a.units);
+  if (u < 0) return;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = lane & 31, h = lane >> 5;
+  const int64_t rb = u / a.splits;
+  const int split = u % a.splits;
+  const int64_t r0 = rb * ROWS;
+  const int nr = (int)min<int64_t>(ROWS, a.rows - r0);
+  const bool has_rows = 32 * wv < nr;   // waves without rows only help to load
+  const int k0 = split * a.kps, k1 = min(a.P, k0 + a.kps);
+  const int b0 = k0 >> 5, b1 = (k1 + 31) >> 5;
+
+  for (int i = threadIdx.x; i < (b1 - b0) * 32; i += WAVES * WAVE)
+    bl[i] = k0 + i < k1 ? a.b2[k0 + i] : 0.f;
+  __syncthreads();
+
+  u32x4_t qf[NS];
+  {
+    const char* row = a.act + (r0 + min(32 * wv + n, nr - 1)) * a.row_bytes + h * 16;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qf[s] = ld16(row + s * 32);
+  }
+  KeyImage im;
+  im.rb = a.row_bytes;
+  im.C = 4 * KS;
+  im.G = 16;
+  // load instruction t of a block (t < 2 KS): image t / KS, instruction
+  // t % KS of it; wave w issues t = w + WAVES q.  off: the lane's byte in
+  // the block (a block of 32 whole W2 rows is contiguous)
+  uint32_t off[PW];
+#pragma unroll
+  for (int q = 0; q < PW; ++q) {
+    const int t = wv + WAVES * q;
+    const int img = t / KS, i = t % KS;
+    off[q] = (uint32_t)(img * 16 * a.row_bytes) + im.src_off(i, lane, im.row_of(i, lane));
+  }
+  // fragment of step s = 8 m + t: key n (image n >> 4, row n & 15), chunk
+  // 2 s + h, at fb[t] + 256 m of the block's first image
+  uint32_t fb[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    fb[t] = (uint32_t)((n >> 4) * IMG) + (uint32_t)((n & 15) * a.row_bytes) +
+            (uint32_t)(((2 * t + h) ^ (n & 15)) * 16);
+  auto issue = [&](int blk) {
+    if (blk >= b1) return;
+    char* ring = smem + ((blk - b0) % NB) * 2 * IMG;
+    if ((blk + 1) * 32 <= a.P) {   // uniform: 32 whole rows of W2
+      const char* src = a.w2 + (int64_t)blk * 32 * a.row_bytes;
+#pragma unroll
+      for (int q = 0; q < PW; ++q) {
+        const int t = wv + WAVES * q;
+        load_lds16(src + off[q], ring + (t / KS) * IMG + (t % KS) * 1024);
+      }
+      return;
+    }
+#pragma unroll
+    for (int q = 0; q < PW; ++q) {
+      // the last block: rows from P on read row P - 1 (masked by index when
+      // folded); an image wholly past P reads row P - 1 throughout
+      const int t = wv + WAVES * q;
+      const int img = t / KS, i = t % KS;
+      const int row0 = blk * 32 + img * 16;
+      const int r = im.row_of(i, lane);
+      const int base_row = min(row0, a.P - 1);
+      const uint32_t o = im.src_off(i, lane, min(row0 + r, a.P - 1) - base_row);
+      load_lds16(a.w2 + (int64_t)base_row * a.row_bytes + o, ring + img * IMG + i * 1024);
+    }
+  };
+
+  float ls[KL];
+  int li[KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) { ls[e] = -__builtin_inff(); li[e] = -1; }
+  const bool tight = a.k == KL;
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
+#pragma unroll
+  for (int b = 0; b < NB - 1; ++b) issue(b0 + b);
+  for (int blk = b0; blk < b1; ++blk) {
+    // this wave's loads of block blk have landed once at most those of the
+    // NB - 2 younger blocks are outstanding (near the end, once all have);
+    // the barrier makes every wave's visible and ends every read of block
+    // blk - 1, whose images the next loads overwrite
+    if (blk + NB - 2 < b1)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NB - 2) * PW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(blk + NB - 1);
+    if (has_rows) {
+      const char* ring = smem + ((blk - b0) % NB) * 2 * IMG;
+      f32x16_t acc = {};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(ring + fb[s & 7] + 256 * (s >> 3));
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                      __builtin_bit_cast(bf16x8_t, qf[s]), acc,
+                                                      0, 0, 0);
+      }
+      // scores + b2 (keys past k1 at -inf), then the lists
+      const int pbase = blk * 32 + 4 * h;
+      const float* bb = bl + (blk - b0) * 32 + 4 * h;
+      float v[16];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4_t bv = *reinterpret_cast<const f32x4_t*>(bb + 8 * j);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          v[4 * j + r] = pbase + 8 * j + r < k1 ? acc[4 * j + r] + bv[r] : -__builtin_inff();
+      }
+      float T = max_half(ls[KL - 1]);
+      if (tight) T = fmaxf(T, min_half(ls[KL / 2 - 1]));
+      fold16<KL>(v, pbase, T, ls, li);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
+  if (!has_rows) return;
+  float top_s[KL];
+  int top_i[KL];
+  merge_lists<KL, 1>(ls, li, a.k, 32, top_s, top_i);
+  const int slot = 32 * wv + n;
+  if (h != 0 || slot >= nr) return;
+  const int64_t t = r0 + slot;
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    if (e < a.k) {
+      if (a.splits == 1) {
+        a.prim[t * a.k + e] = top_i[e];
+        a.top[t * a.k + e] = top_s[e];
+      } else {
+        a.part[(t * a.splits + split) * a.k + e] =
+            ((uint64_t)(uint32_t)top_i[e] << 32) | __float_as_uint(top_s[e]);
+      }
+    }
+  }
+}
+
+// The lists of the ranges of a split merged per row: SPL lanes a row (the
+// next power of two >= splits), 64 / SPL rows a wave; lane j < splits of a
+// row's group holds range j's list, the butterfly of merge_lists over the
+// group orders their union by the rule of one unit over all of W2 (a range
+// with fewer than k rows pads its list with -inf, which the P >= k real
+// logits outrank).
+template <int KL, int LOG>
 __global__ __launch_bounds__(256) void relevance_merge_kernel(const uint64_t* __restrict__ part,
                                                               int64_t rows, int splits, int k,
                                                               int32_t* __restrict__ prim,
                                                               float* __restrict__ top) {
+  constexpr int SPL = 1 << LOG;
   const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= rows) return;
+  const int j = lane & (SPL - 1);
+  const int64_t t = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> LOG;
+  const bool live = t < rows;   // lanes past the last row join the shuffles with empty lists
   float ls[KL], ms[KL];
   int li[KL], mi[KL];
 #pragma unroll
   for (int e = 0; e < KL; ++e) {
     ls[e] = -__builtin_inff();
     li[e] = -1;
-    if (lane < splits && e < k) {
-      const uint64_t v = part[(t * splits + lane) * k + e];
+    if (live && j < splits && e < k) {
+      const uint64_t v = part[(t * splits + j) * k + e];
       ls[e] = __uint_as_float((uint32_t)v);
       li[e] = (int)(v >> 32);
     }
   }
-  merge_lists<KL, 4>(ls, li, k, 1, ms, mi);
-  if (lane != 0) return;
+  merge_lists<KL, LOG>(ls, li, k, 1, ms, mi);
+  if (!live || j != 0) return;
 #pragma unroll
   for (int e = 0; e < KL; ++e)
     if (e < k) {
@@ -313,23 +544,67 @@ static int relevance_splits(int64_t row_blocks, int P, int k) {
   return splits <= 16 ? splits : 0;
 }
 
+// The split's lists merged per row (nothing to do for one range).
+template <int KL>
+static hipError_t launch_merge(const RelTopkParams& p, hipStream_t st) {
+  if (p.splits > 1) {
+    const int log = p.splits <= 2 ? 1 : p.splits <= 4 ? 2 : p.splits <= 8 ? 3 : 4;
+    const dim3 grid((unsigned)(((p.rows << log) + 255) / 256));
+    if (log == 1)
+      hipLaunchKernelGGL((relevance_merge_kernel<KL, 1>), grid, dim3(256), 0, st, p.part, p.rows,
+                         p.splits, p.k, p.prim, p.top);
+    else if (log == 2)
+      hipLaunchKernelGGL((relevance_merge_kernel<KL, 2>), grid, dim3(256), 0, st, p.part, p.rows,
+                         p.splits, p.k, p.prim, p.top);
+    else if (log == 3)
+      hipLaunchKernelGGL((relevance_merge_kernel<KL, 3>), grid, dim3(256), 0, st, p.part, p.rows,
+                         p.splits, p.k, p.prim, p.top);
+    else
+      hipLaunchKernelGGL((relevance_merge_kernel<KL, 4>), grid, dim3(256), 0, st, p.part, p.rows,
+                         p.splits, p.k, p.prim, p.top);
+  }
+  return hipGetLastError();
+}
+
 template <int DT, int KS, int KL>
-static hipError_t launch_topk_fused(const RelTopkParams& p0, float* part_ws, hipStream_t st) {
+static hipError_t launch_topk16(const RelTopkParams& p0, float* part_ws, hipStream_t st) {
   RelTopkParams p = p0;
   const int64_t row_blocks = (p.rows + RT_ROWS - 1) / RT_ROWS;
   p.splits = relevance_splits(row_blocks, p.P, p.k);
+  if (p.splits < 1) return hipErrorInvalidValue;
   p.kps = ((p.P + p.splits - 1) / p.splits + 15) / 16 * 16;
   p.splits = (p.P + p.kps - 1) / p.kps;   // no empty range
   // the lists of a split live in the logits' workspace ([rows, P] float32)
   if (p.splits > 1 && (int64_t)p.splits * p.k * 2 > p.P) return hipErrorInvalidValue;
   p.units = (int)(row_blocks * p.splits);
   p.part = reinterpret_cast<uint64_t*>(part_ws);
-  hipLaunchKernelGGL((relevance_topk_fused_kernel<DT, KS, KL>), dim3((unsigned)((p.units + 7) / 8 * 8)),
-                     dim3(RT_THREADS), 0, st, p);
-  if (p.splits > 1)
-    hipLaunchKernelGGL((relevance_merge_kernel<KL>), dim3((unsigned)((p.rows + 3) / 4)), dim3(256), 0,
-                       st, p.part, p.rows, p.splits, p.k, p.prim, p.top);
-  return hipGetLastError();
+  hipLaunchKernelGGL((relevance_topk_fused_kernel<DT, KS, KL>),
+                     dim3((unsigned)((p.units + 7) / 8 * 8)), dim3(RT_THREADS), 0, st, p);
+  return launch_merge<KL>(p, st);
+}
+
+template <int KS, int KL, int WAVES>
+static hipError_t launch_topk32(const RelTopkParams& p0, float* part_ws, hipStream_t st) {
+  RelTopkParams p = p0;
+  const int64_t row_blocks = (p.rows + 32 * WAVES - 1) / (32 * WAVES);
+  p.splits = relevance_splits(row_blocks, p.P, p.k);
+  if (p.splits < 1) return hipErrorInvalidValue;
+  p.kps = ((p.P + p.splits - 1) / p.splits + 31) / 32 * 32;
+  p.splits = (p.P + p.kps - 1) / p.kps;   // no empty range
+  if (p.kps > RT_MAX_KPS) return hipErrorInvalidValue;
+  if (p.splits > 1 && (int64_t)p.splits * p.k * 2 > p.P) return hipErrorInvalidValue;
+  p.units = (int)(row_blocks * p.splits);
+  p.part = reinterpret_cast<uint64_t*>(part_ws);
+  hipLaunchKernelGGL((relevance_topk32_kernel<KS, KL, WAVES>),
+                     dim3((unsigned)((p.units + 7) / 8 * 8)), dim3(WAVES * WAVE), 0, st, p);
+  return launch_merge<KL>(p, st);
+}
+
+template <int DT, int KS, int KL>
+static hipError_t launch_topk_fused(const RelTopkParams& p, float* part_ws, hipStream_t st) {
+  if constexpr (DT == DT_BF16 && KL <= 16)
+    if (p.rows >= 4096) return launch_topk32<KS, KL, 4>(p, part_ws, st);
+  return launch_topk16<DT, KS, KL>(p, part_ws, st);
 }
 
 // One wave per row: cosines of q_t with its k chosen primitive keys, plus
@@ -458,7 +733,7 @@ hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const v
   hipError_t e = launch_tile_gemm<EPI_ACT>(dt, g1, 1, st);
   if (e != hipSuccess) return e;
   const int64_t hb = (int64_t)mlp.hidden * es;
-  if ((hb == 1024 || hb == 512) && relevance_splits((rows + RT_ROWS - 1) / RT_ROWS, P, k) > 0) {
+  if ((hb == 1024 || hb == 512) && relevance_splits((rows + 63) / 64, P, k) > 0) {
     // second layer and top-k fused (no float32 logits written); the ranges'
     // lists of a split go to the logits' workspace
     RelTopkParams p{};

@@ -45,6 +45,15 @@ __device__ __forceinline__ float max_lane_groups(float v) {
   return fmaxf(a, b);
 }
 
+// The minimum over the same 4 lanes.
+__device__ __forceinline__ float min_lane_groups(float v) {
+  float a, b;
+  pair16(v, a, b);
+  v = fminf(a, b);
+  pair32(v, a, b);
+  return fminf(a, b);
+}
+
 __device__ __forceinline__ float inv_norm(float sq) { return sq > 0.f ? rsqrtf(sq) : 0.f; }
 
 // Cosine scaling of a tile's 4 scores (keys 4g + r of the block, query row
@@ -59,10 +68,12 @@ __device__ __forceinline__ f32x4_t cos_scale(f32x4_t acc, float qinv, float knsq
 // lane's running result: arg max (routing, with the scene bias) or a sorted
 // list of the KL best (Level-2; with LBIAS, bias points at the 16 biases of
 // this block in LDS, the relevance logits' b2, 0 for keys past kend, and
-// each key's is added first).
+// each key's is added first).  `tight` (only when the lists are exactly k
+// long) also drops values below the smallest KL/4-th entry of the row's
+// four lists: those four lists hold k values at least that large.
 template <bool LOOKUP, int KL, bool LBIAS = false>
 __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int kend, const float* bias,
-                                            float (&ls)[KL], int (&li)[KL]) {
+                                            float (&ls)[KL], int (&li)[KL], bool tight = false) {
   float v[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) v[r] = blk * 16 + 4 * g + r < kend ? acc[r] : -__builtin_inff();
@@ -86,11 +97,13 @@ __device__ __forceinline__ void fold_scores(f32x4_t acc, int blk, int g, int ken
     // lane's list: the rounds are wave-wide (branch-free sorted insertion),
     // and after the first blocks a round is rarely needed by any lane, so
     // most blocks cost one vote instead of four insertions.  A value below
-    // T, the largest k-th entry of the row's 4 lists in this wave, cannot
-    // reach the row's top k (that list holds k keys at least as large), so
-    // it is dropped; values equal to T stay, for the lower-index rule.
+    // T, the largest last entry of the row's 4 lists in this wave, cannot
+    // reach the row's top k (that list holds KL >= k keys at least as
+    // large), so it is dropped; values equal to T stay, for the lower-index
+    // rule.
     const int p0 = blk * 16 + 4 * g;
-    const float T = max_lane_groups(ls[KL - 1]);
+    float T = max_lane_groups(ls[KL - 1]);
+    if (tight) T = fmaxf(T, min_lane_groups(ls[KL / 4 - 1]));
 #pragma unroll
     for (int round = 0; round < 4; ++round) {
       float x = v[0];
@@ -146,16 +159,19 @@ __device__ __forceinline__ void merge_lists(const float (&ls)[KL], const int (&l
       }
       top_s[e] = bs;
       top_i[e] = bi;
-      if (hi == bi && hs == bs) {   // this list supplied the winner
-        ++head;
-        float ns = -__builtin_inff();
-        int ni = -1;
+      // the list that supplied the winner moves its head on (selects, not
+      // branches)
+      const bool won = (hi == bi) & (hs == bs);
+      head += won ? 1 : 0;
+      float ns = -__builtin_inff();
+      int ni = -1;
 #pragma unroll
-        for (int x = 1; x < KL; ++x)
-          if (x == head) { ns = ls[x]; ni = li[x]; }
-        hs = ns;
-        hi = ni;
+      for (int x = 1; x < KL; ++x) {
+        ns = x == head ? ls[x] : ns;
+        ni = x == head ? li[x] : ni;
       }
+      hs = won ? ns : hs;
+      hi = won ? ni : hi;
     }
   }
 }

@@ -372,13 +372,18 @@ def test_layers_batched_equal_sequential():
 # tokens or None for all).  Ragged rows and primitive counts (200, 37, 300)
 # leave partial 64 x 64 tiles in both layers; the image and multi-scale
 # cases have the benchmarks' shapes.  Hidden rows of 512 or 1024 bytes take
-# the fused second layer + top-k: the "fused" cases cover both widths in
-# both dtypes, a ragged last block of W2 rows (P 37, 300, 1000), W2 split
-# into ranges merged afterwards (P 300 over 2, P 1000 over 4 with a short
-# last range, the image shape over 8) and one range of 4096 rows (Zipf).
+# the fused second layer + top-k (bf16 with k <= 16: the 32 x 32 tile form,
+# else 16 x 16): the "fused" cases cover both widths in both dtypes and both
+# forms, a ragged last block of W2 rows (P 37, 300, 1000; at P 300 the last
+# 32-key block's second image lies wholly past P), W2 split into ranges
+# merged afterwards (P 300 over 2, P 1000 over 4 with a short last range, the
+# image shape over 8), a unit with rows for one wave only (130 rows) and one
+# range of 4096 rows (Zipf).
 RELEVANCE = {
     "bf16_rel_fused_h256": (Workload("bf16_rel_fused_h256", "bf16", 130, 1, 128, 64, 7, 300, 32,
                                      32, 32, 30, usage="uniform"), 256, None),
+    "bf16_rel_fused_h256_k8": (Workload("bf16_rel_fused_h256_k8", "bf16", 130, 1, 128, 64, 7, 300,
+                                        32, 32, 8, 30, usage="uniform"), 256, None),
     "f32_rel_fused_h128": (Workload("f32_rel_fused_h128", "f32", 77, 1, 96, 64, 5, 37, 40, 40,
                                     3, 40, usage="iid"), 128, None),
     "f32_rel_fused_h256": (Workload("f32_rel_fused_h256", "f32", 200, 1, 96, 64, 6, 1000, 40, 40,
