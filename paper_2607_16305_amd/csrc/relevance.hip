@@ -684,11 +684,184 @@ __global__ __launch_bounds__(256) void relevance_weights_kernel(
   if (lane < k) w[t * k + lane] = ex / sum;
 }
 
+// The same weights with the products on the matrix cores, for rows of
+// 64 KS bytes and k < 32: one wave per row.  The row's k chosen keys and its
+// query form the rows of 16-row operand tiles (key m at row m, the query at
+// row k; NT = 1 tile when k < 16, else 2), gathered straight into MFMA
+// fragments (lane (g, n): tile row n, chunks 4 j + g), and the products of
+// the tiles with themselves give every number the weights need: a key's
+// squared norm on the diagonal, key . q in the query's column, ||q||^2 at
+// the query's diagonal entry.  One gather of k + 1 rows, no cross-lane sums;
+// the vector form (below) covers the other widths and k = 32.  At k = 16
+// (NT = 0) the keys fill one tile and every lane also loads its query
+// fragments: key . q is the product with the query in every column, ||q||^2
+// comes from the fragments (a second tile holding the query alone costs
+// more load instructions than this).
+template <int DT, int KS, int NT>
+__global__ __launch_bounds__(256) void relevance_weights_mma_kernel(
+    const char* __restrict__ q, const int32_t* __restrict__ scene,
+    const char* __restrict__ prim_keys, const int32_t* __restrict__ prim, float* __restrict__ w,
+    int64_t rows, int S, int P, int k) {
+  constexpr int64_t RB = 64 * KS;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= rows) return;
+  const int n = lane & 15, g = lane >> 4;
+  int s = scene[t];
+  s = s < 0 ? 0 : (s >= S ? S - 1 : s);
+  if constexpr (NT == 0) {
+    u32x4_t kf[KS], qf[KS];
+    int p = prim[t * k + n];
+    p = p < 0 ? 0 : (p >= P ? P - 1 : p);
+    const char* kr_ = prim_keys + ((int64_t)s * P + p) * RB + g * 16;
+    const char* qr = q + t * RB + g * 16;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      kf[j] = ld16(kr_ + j * 64);
+      qf[j] = ld16(qr + j * 64);
+    }
+    float qq = 0.f;
+#pragma unroll
+    for (int j = 0; j < KS; ++j) qq = chunk_sumsq<DT>(qf[j], qq);
+    qq = sum_lane_groups(qq);
+    f32x4_t dq = {0.f, 0.f, 0.f, 0.f}, kk = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      dq = mfma_chunk<DT>(kf[j], qf[j], dq);   // [key 4g + r][any column] = key . q
+      kk = mfma_chunk<DT>(kf[j], kf[j], kk);   // [key 4g + r][key n]
+    }
+    float z[4], mx = -__builtin_inff();
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float ee = __shfl(kk[r], 16 * g + 4 * g + r, 64);
+      const float den = sqrtf(qq) * sqrtf(ee);
+      const float c = den > 0.f ? dq[r] / den : 0.f;
+      z[r] = c + tanhf(w[t * 16 + 4 * g + r]);
+      mx = fmaxf(mx, z[r]);
+    }
+    mx = max_lane_groups(mx);
+    float ex[4], sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      ex[r] = expf(z[r] - mx);
+      sum += ex[r];
+    }
+    sum = sum_lane_groups(sum);
+    if (n == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) w[t * 16 + 4 * g + r] = ex[r] / sum;
+    return;
+  }
+  constexpr int NTT = NT > 0 ? NT : 1;
+  // operand rows: m < k key prim[m], m == k the query, past it zero
+  u32x4_t f[NTT][KS];
+#pragma unroll
+  for (int T = 0; T < NTT; ++T) {
+    const int m = 16 * T + n;
+    const char* src = q + t * RB;
+    if (m < k) {
+      int p = prim[t * k + m];
+      p = p < 0 ? 0 : (p >= P ? P - 1 : p);
+      src = prim_keys + ((int64_t)s * P + p) * RB;
+    }
+#pragma unroll
+    for (int j = 0; j < KS; ++j)
+      f[T][j] = m <= k ? ld16(src + g * 16 + j * 64) : u32x4_t{0, 0, 0, 0};
+  }
+  // products: G[T] = tile T x tile T^T, and with two tiles C = tile 0 x
+  // tile 1^T (keys 0..15 against keys 16.. and the query); lane (g, n) holds
+  // [row 4g + r][row n]
+  const int kt = k >> 4, kr = k & 15;   // the query's tile and row
+  f32x4_t G[NTT], C = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int T = 0; T < NTT; ++T) {
+    G[T] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KS; ++j) G[T] = mfma_chunk<DT>(f[T][j], f[T][j], G[T]);
+  }
+  if constexpr (NT == 2) {
+#pragma unroll
+    for (int j = 0; j < KS; ++j) C = mfma_chunk<DT>(f[0][j], f[1][j], C);
+  }
+  // ||q||^2: the query's diagonal entry, in lane (kr >> 2, kr), element kr & 3
+  float qq = 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float v = __shfl(G[NTT - 1][r], 16 * (kr >> 2) + kr, 64);
+    qq = (kr & 3) == r ? v : qq;
+  }
+  // lanes n == kr hold key (4g + r) . q of each tile: tile kt in its own
+  // product, tile 0 (when the query is in tile 1) in C
+  float z[NTT][4];
+#pragma unroll
+  for (int T = 0; T < NTT; ++T) {
+    const f32x4_t dq = (NT == 2 && T == 0) ? C : G[T];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      // ||key 4g + r||^2 sits in lane (g, 4g + r), element r, of G[T]
+      const float ee = __shfl(G[T][r], 16 * g + 4 * g + r, 64);
+      const int m = 16 * T + 4 * g + r;
+      const float den = sqrtf(qq) * sqrtf(ee);
+      const float c = den > 0.f ? dq[r] / den : 0.f;
+      z[T][r] = m < k ? c + tanhf(w[t * k + m]) : -__builtin_inff();
+    }
+  }
+  float mx = -__builtin_inff();
+#pragma unroll
+  for (int T = 0; T < NTT; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) mx = fmaxf(mx, z[T][r]);
+  mx = max_lane_groups(mx);
+  float ex[NTT][4], sum = 0.f;
+#pragma unroll
+  for (int T = 0; T < NTT; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      ex[T][r] = 16 * T + 4 * g + r < k ? expf(z[T][r] - mx) : 0.f;
+      sum += ex[T][r];
+    }
+  sum = sum_lane_groups(sum);
+  if (n != kr) return;
+#pragma unroll
+  for (int T = 0; T < NTT; ++T)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * T + 4 * g + r;
+      if (m < k) w[t * k + m] = ex[T][r] / sum;
+    }
+}
+
 static hipError_t launch_relevance_weights(int dt, const void* q, const int32_t* scene,
                                            const void* prim_keys, const int32_t* prim, float* w,
                                            int64_t rows, int S, int P, int k, int64_t q_bytes,
                                            hipStream_t st) {
   const dim3 wgrid((unsigned)((rows + 3) / 4));
+  if ((q_bytes == 1024 || q_bytes == 512) && k < 32) {
+#define LOOKME_RWM(DT_, KS_)                                                                     \
+  do {                                                                                           \
+    if (k < 16)                                                                                  \
+      hipLaunchKernelGGL((relevance_weights_mma_kernel<DT_, KS_, 1>), wgrid, dim3(256), 0, st,   \
+                         static_cast<const char*>(q), scene,                                     \
+                         static_cast<const char*>(prim_keys), prim, w, rows, S, P, k);           \
+    else if (k == 16)                                                                            \
+      hipLaunchKernelGGL((relevance_weights_mma_kernel<DT_, KS_, 0>), wgrid, dim3(256), 0, st,   \
+                         static_cast<const char*>(q), scene,                                     \
+                         static_cast<const char*>(prim_keys), prim, w, rows, S, P, k);           \
+    else                                                                                         \
+      hipLaunchKernelGGL((relevance_weights_mma_kernel<DT_, KS_, 2>), wgrid, dim3(256), 0, st,   \
+                         static_cast<const char*>(q), scene,                                     \
+                         static_cast<const char*>(prim_keys), prim, w, rows, S, P, k);           \
+  } while (0)
+    if (dt == DT_BF16) {
+      if (q_bytes == 1024) LOOKME_RWM(DT_BF16, 16);
+      else LOOKME_RWM(DT_BF16, 8);
+    } else {
+      if (q_bytes == 1024) LOOKME_RWM(DT_F32, 16);
+      else LOOKME_RWM(DT_F32, 8);
+    }
+#undef LOOKME_RWM
+    return hipGetLastError();
+  }
 #define LOOKME_RW(DT_, K_)                                                                       \
   hipLaunchKernelGGL((relevance_weights_kernel<DT_, K_>), wgrid, dim3(256), 0, st,             \
                      static_cast<const char*>(q), scene, static_cast<const char*>(prim_keys), \

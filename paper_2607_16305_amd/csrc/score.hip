@@ -83,20 +83,6 @@ __device__ __forceinline__ void load_row_frags(u32x4_t (&f)[KS], const char* row
   for (int j = 0; j < KS; ++j) f[j] = (!MASKED || j < ks) ? ld16(p + j * 64) : u32x4_t{0, 0, 0, 0};
 }
 
-template <int DT>
-__device__ __forceinline__ float chunk_sumsq(u32x4_t v, float acc) {
-  if constexpr (DT == DT_BF16) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc = fmaf(bf16lo(v[e]), bf16lo(v[e]), acc);
-      acc = fmaf(bf16hi(v[e]), bf16hi(v[e]), acc);
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc = fmaf(as_f32(v[e]), as_f32(v[e]), acc);
-  }
-  return acc;
-}
 
 template <bool LOOKUP, int KL>
 __device__ __forceinline__ void write_row(const ScoreParams& a, int64_t out_row,

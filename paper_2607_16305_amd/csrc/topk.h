@@ -54,6 +54,22 @@ __device__ __forceinline__ float min_lane_groups(float v) {
   return fminf(a, b);
 }
 
+// The sum of squares of a 16-byte chunk's elements added to acc.
+template <int DT>
+__device__ __forceinline__ float chunk_sumsq(u32x4_t v, float acc) {
+  if constexpr (DT == DT_BF16) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc = fmaf(bf16lo(v[e]), bf16lo(v[e]), acc);
+      acc = fmaf(bf16hi(v[e]), bf16hi(v[e]), acc);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc = fmaf(as_f32(v[e]), as_f32(v[e]), acc);
+  }
+  return acc;
+}
+
 __device__ __forceinline__ float inv_norm(float sq) { return sq > 0.f ? rsqrtf(sq) : 0.f; }
 
 // Cosine scaling of a tile's 4 scores (keys 4g + r of the block, query row

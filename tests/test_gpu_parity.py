@@ -389,6 +389,18 @@ RELEVANCE = {
     "f32_rel_fused_h256": (Workload("f32_rel_fused_h256", "f32", 200, 1, 96, 64, 6, 1000, 40, 40,
                                     8, 40, usage="uniform"), 256, None),
     "bf16_rel_zipf": (WORKLOADS[4], 512, 40),
+    # query rows of 512 and 1024 bytes with k < 32 take the weights on the
+    # matrix cores: both widths, both dtypes, k < 16 (one tile with the
+    # query), k = 16 (the query broadcast) and k = 20 (two tiles); k = 32
+    # the vector form
+    "bf16_rel_wmma_k32": (Workload("bf16_rel_wmma_k32", "bf16", 90, 1, 256, 256, 5, 300, 32, 32,
+                                   32, 30, usage="uniform"), 128, None),
+    "f32_rel_wmma_d128": (Workload("f32_rel_wmma_d128", "f32", 70, 1, 128, 128, 4, 100, 32, 32, 8,
+                                   30, usage="uniform"), 64, None),
+    "f32_rel_wmma_k16": (Workload("f32_rel_wmma_k16", "f32", 50, 1, 128, 128, 3, 90, 32, 32, 16,
+                                  30, usage="iid"), 64, None),
+    "f32_rel_wmma_k20": (Workload("f32_rel_wmma_k20", "f32", 60, 1, 256, 256, 3, 150, 32, 32, 20,
+                                  30, usage="iid"), 96, None),
     "bf16_rel_l2": (Workload("bf16_rel_l2", "bf16", 300, 2, 256, 128, 20, 200, 64, 64, 8, 30,
                              usage="uniform"), 192, None),
     "f32_rel": (Workload("f32_rel", "f32", 77, 1, 96, 64, 5, 37, 40, 40, 3, 40, usage="iid"),
