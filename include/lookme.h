@@ -253,7 +253,13 @@ lookme_status_t lookme_inject_kept(lookme_t h, int32_t layers, int64_t n, int64_
  *   b2      [prims_per_scene] float32, or NULL for zero
  * Needs key_dim * elem_size a multiple of 128 bytes.  Replaces an earlier
  * registration.  From then on lookme_workspace_size includes the lookup's
- * logits, layers * n * prims_per_scene float32.
+ * logits, layers * n * prims_per_scene float32, and a per-scene table
+ * T[s] = W1[:, key_dim:] scene_keys[s] + b1 (num_scenes * h float32) that
+ * the first lookme_lookup_relevance after this call (or after
+ * lookme_set_workspace) computes into the workspace and later calls reuse:
+ * the first layer then multiplies only the query half per row.  The
+ * workspace must be left alone between calls, and a change of the scene
+ * keys, w1 or b1 in place needs this call again.
  */
 lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
                                      const float* b1, const void* w2, const float* b2);
@@ -263,7 +269,8 @@ lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
  * the MLP of lookme_set_relevance:
  *   q, scene   as for lookme_lookup (q [layers, n, d_e], scene [layers, n])
  *   act_out    [layers, n, h] dtype: a = round(ReLU(W1 [q ; scene_keys[scene]]
- *              + b1)), float32 accumulation, one rounding to dtype
+ *              + b1)), float32 accumulation (the query half per row plus the
+ *              per-scene table), one rounding to dtype
  *   prim_out   [layers, n, k] int32: the k primitives p of largest logit
  *              r_p = <W2[p], a> + b2[p] (ties: lowest p), logit-descending
  *   w_out      [layers, n, k] float32: softmax over the k of

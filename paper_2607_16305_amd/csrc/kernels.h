@@ -126,7 +126,12 @@ struct RelevanceMlp {
   const void* w2;
   const float* b2;
 };
-hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const void* scene_keys,
+// The per-scene half of the MLP's first layer, tab[s] = K1[s] W1b^T + b1
+// ([S, hidden] float32; W1b the columns of W1 that multiply the scene key).
+hipError_t launch_relevance_table(int dt, const void* scene_keys, const RelevanceMlp& mlp, int S,
+                                  int d_e, float* tab, hipStream_t st);
+// Level-2 in the paper's form for `rows` rows; tab from launch_relevance_table.
+hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const float* tab,
                             const void* prim_keys, const RelevanceMlp& mlp, int64_t rows, int d_e,
                             int S, int P, int k, void* act, int32_t* prim, float* w,
                             float* logits, hipStream_t st);

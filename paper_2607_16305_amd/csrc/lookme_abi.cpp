@@ -35,6 +35,7 @@ struct lookme_s {
   int64_t prof_count[LOOKME_GROUP_COUNT];
   double prof_ms[LOOKME_GROUP_COUNT];
   lookme::RelevanceMlp rel;                // hidden == 0: none registered
+  bool rel_tab_ready = false;              // the workspace holds rel's per-scene table
   lookme::FusionFfn fus;                   // d_ff == 0: none registered
   int32_t prop_steps = 0;                  // Eq. 11 projections; 0: none registered
   const void* prop_w = nullptr;            // [prop_steps, value_dim, value_dim], transposed
@@ -72,7 +73,7 @@ constexpr int32_t MAX_SCENES = 16384;   // bucketing keeps one histogram per chu
 // Workspace layout for `layers` x `n` rows.
 struct Layout {
   size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, route_count,
-      route_part, crit_key, kept, rel_logits, fus_r, fus_u, ms_r, ms_q, total;
+      route_part, crit_key, kept, rel_tab, rel_logits, fus_r, fus_u, ms_r, ms_q, total;
 };
 
 // The leading bytes of the workspace hold counters that start at zero; they
@@ -80,7 +81,7 @@ struct Layout {
 // them at zero.
 constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_COUNTERS * 4;
 
-Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance,
+Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, int32_t relevance,
               int32_t fusion_dff, int32_t scales) {
   const int64_t rows = (int64_t)layers * n;
   const int64_t chunks = lookme::bucket_chunks(rows);
@@ -94,6 +95,9 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance,
   };
   L.unit_count = take(256);   // counters first: the region zeroed at set-up
   L.route_count = take((size_t)lookme::ROUTE_COUNTERS * 4);
+  // the relevance MLP's per-scene table [S, hidden] float32, kept across
+  // calls: at an offset that does not depend on the batch
+  L.rel_tab = take(relevance ? (size_t)d.num_scenes * relevance * 4 : 0);
   const lookme::RoutePlan plan =
       lookme::route_plan(rows, d.num_scenes, (int64_t)d.key_dim * elem_size(d.dtype),
                          d.score == LOOKME_SCORE_COS);
@@ -106,7 +110,8 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, bool relevance,
   L.unit_begin = take((size_t)units * 4);
   L.crit_key = take((size_t)rows * 4);
   L.kept = take((size_t)rows * 4);
-  // relevance logits [rows, P] float32, when an MLP is registered
+  // relevance logits [rows, P] float32, when an MLP is registered (the
+  // lists of a split second layer, or the logits of the unfused widths)
   L.rel_logits = take(relevance ? (size_t)rows * d.prims_per_scene * 4 : 0);
   // the fusion's R and inner activations of the kept rows (at most all rows)
   const size_t es = (size_t)elem_size(d.dtype);
@@ -140,7 +145,7 @@ lookme_status_t check_layers_n(int32_t layers, int64_t n) {
 }
 
 lookme_status_t check_workspace(lookme_t h, int32_t layers, int64_t n, Layout* L) {
-  *L = layout(h->d, layers, n, h->rel.hidden > 0, h->fus.d_ff, h->ms_scales);
+  *L = layout(h->d, layers, n, h->rel.hidden, h->fus.d_ff, h->ms_scales);
   if (h->ws == nullptr) return fail(LOOKME_ERR_WORKSPACE, "no workspace set");
   if (h->ws_bytes < L->total)
     return fail(LOOKME_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed for %d x %lld rows",
@@ -481,7 +486,7 @@ lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_toke
   LOOKME_TRY(check_handle(h));
   if (bytes == nullptr) return fail(LOOKME_ERR_INVALID, "bytes is NULL");
   LOOKME_TRY(check_layers_n(layers, n_tokens));
-  *bytes = layout(h->d, layers, n_tokens, h->rel.hidden > 0, h->fus.d_ff, h->ms_scales).total;
+  *bytes = layout(h->d, layers, n_tokens, h->rel.hidden, h->fus.d_ff, h->ms_scales).total;
   return LOOKME_OK;
 }
 
@@ -495,6 +500,7 @@ lookme_status_t lookme_set_workspace(lookme_t h, void* dev_ptr, size_t bytes) {
   LOOKME_TRY(hip_status(hipMemset(dev_ptr, 0, ZEROED_BYTES), "hipMemset(workspace counters)"));
   h->ws = dev_ptr;
   h->ws_bytes = bytes;
+  h->rel_tab_ready = false;
   return LOOKME_OK;
 }
 
@@ -715,6 +721,7 @@ lookme_status_t lookme_set_relevance(lookme_t h, int32_t hidden, const void* w1,
       (b2 != nullptr && (reinterpret_cast<uintptr_t>(b2) & 3u)))
     return fail(LOOKME_ERR_INVALID, "b1 and b2 must be 4-byte aligned");
   h->rel = lookme::RelevanceMlp{hidden, w1, b1, w2, b2};
+  h->rel_tab_ready = false;
   return LOOKME_OK;
 }
 
@@ -736,8 +743,16 @@ lookme_status_t lookme_lookup_relevance(lookme_t h, int32_t layers, int64_t n, c
   const lookme_desc_t& d = h->d;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Timed tm(h, LOOKME_GROUP_SCORE, st);
+  float* tab = reinterpret_cast<float*>(static_cast<char*>(h->ws) + L.rel_tab);
+  if (!h->rel_tab_ready) {
+    // the per-scene half of the first layer, once per MLP and workspace
+    LOOKME_TRY(hip_status(lookme::launch_relevance_table(d.dtype, h->scene_keys, h->rel,
+                                                         d.num_scenes, d.key_dim, tab, st),
+                          "relevance table launch"));
+    h->rel_tab_ready = true;
+  }
   return hip_status(
-      lookme::launch_relevance(d.dtype, q, scene, h->scene_keys, h->prim_keys, h->rel,
+      lookme::launch_relevance(d.dtype, q, scene, tab, h->prim_keys, h->rel,
                                (int64_t)layers * n, d.key_dim, d.num_scenes, d.prims_per_scene,
                                d.top_k, act_out, prim_out, w_out,
                                reinterpret_cast<float*>(static_cast<char*>(h->ws) + L.rel_logits),

@@ -881,29 +881,51 @@ static hipError_t launch_relevance_weights(int dt, const void* q, const int32_t*
   return hipGetLastError();
 }
 
-hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const void* scene_keys,
+hipError_t launch_relevance_table(int dt, const void* scene_keys, const RelevanceMlp& mlp, int S,
+                                  int d_e, float* tab, hipStream_t st) {
+  const int es = dt == DT_BF16 ? 2 : 4;
+  // tab = K1 W1b^T + b1: W1 is [hidden, 2 d_e], W1b its last d_e columns
+  TileGemmParams g{};
+  g.a0 = static_cast<const char*>(scene_keys);
+  g.b = static_cast<const char*>(mlp.w1) + (int64_t)d_e * es;
+  g.b_ld = 2 * (int64_t)d_e * es;
+  g.bias = mlp.b1;
+  g.out = reinterpret_cast<char*>(tab);
+  g.rows = S;
+  g.a_bytes = (int64_t)d_e * es;
+  g.k_bytes = g.a_bytes;
+  g.cols = mlp.hidden;
+  g.ksplit = (int)(g.a_bytes / TG_KB);
+  g.tiles = (int)(((S + TgShape::BM - 1) / TgShape::BM) *
+                  ((mlp.hidden + TgShape::BN - 1) / TgShape::BN));
+  return launch_tile_gemm<EPI_LOGIT>(dt, g, 1, st);
+}
+
+hipError_t launch_relevance(int dt, const void* q, const int32_t* scene, const float* tab,
                             const void* prim_keys, const RelevanceMlp& mlp, int64_t rows, int d_e,
                             int S, int P, int k, void* act, int32_t* prim, float* w,
                             float* logits, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
   const int64_t rt = (rows + TgShape::BM - 1) / TgShape::BM;
-  // hidden layer: K = [query ; scene key]
+  // hidden layer: ReLU(q W1a^T + tab[scene]), W1a the first d_e columns of W1
+  // (the scene half and b1 are in the table: half the first layer's
+  // products of the joint form, computed once per scene instead of per row)
   TileGemmParams g1{};
   g1.a0 = static_cast<const char*>(q);
-  g1.a1 = static_cast<const char*>(scene_keys);
   g1.sel = scene;
+  g1.tab = tab;
   g1.b = static_cast<const char*>(mlp.w1);
-  g1.bias = mlp.b1;
+  g1.b_ld = 2 * (int64_t)d_e * es;
   g1.out = static_cast<char*>(act);
   g1.rows = rows;
   g1.a_bytes = (int64_t)d_e * es;
-  g1.k_bytes = 2 * g1.a_bytes;
+  g1.k_bytes = g1.a_bytes;
   g1.sel_rows = S;
   g1.cols = mlp.hidden;
   g1.ksplit = (int)(g1.a_bytes / TG_KB);
   g1.tiles = (int)(rt * ((mlp.hidden + TgShape::BN - 1) / TgShape::BN));
-  hipError_t e = launch_tile_gemm<EPI_ACT>(dt, g1, 1, st);
+  hipError_t e = launch_tile_gemm<EPI_ACT_TAB>(dt, g1, 1, st);
   if (e != hipSuccess) return e;
   const int64_t hb = (int64_t)mlp.hidden * es;
   if ((hb == 1024 || hb == 512) && relevance_splits((rows + 63) / 64, P, k) > 0) {

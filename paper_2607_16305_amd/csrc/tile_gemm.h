@@ -19,7 +19,10 @@
 //   EPI_RESID   H[out_row(r), c] = round(H + C) with out_row(r) = z * n +
 //               kept[z * kept_batch + r] (the kept token of row r of layer z);
 //   EPI_ADD     round(C + res) with res [rows, cols], [rows, cols];
-//   EPI_STORE   round(C), [rows, cols].
+//   EPI_STORE   round(C), [rows, cols];
+//   EPI_ACT_TAB C + tab[sel[row]] (a float32 row of [sel_rows, cols]: the
+//               relevance MLP's per-scene half of the first layer, b1
+//               included), ReLU, one rounding, [rows, cols].
 //
 // An A row may take its first `ksplit` stages from a0 and the rest from a
 // gathered row of a1 (the relevance MLP's [query ; scene key] input).
@@ -34,7 +37,10 @@ namespace lookme {
 using TgShape = DtlShape<2, 2, 2, 2, 128>;
 constexpr int TG_KB = 128;
 
-enum : int { EPI_ACT = 0, EPI_LOGIT = 1, EPI_SWIGLU = 2, EPI_RESID = 3, EPI_ADD = 4, EPI_STORE = 5 };
+enum : int {
+  EPI_ACT = 0, EPI_LOGIT = 1, EPI_SWIGLU = 2, EPI_RESID = 3, EPI_ADD = 4, EPI_STORE = 5,
+  EPI_ACT_TAB = 6
+};
 
 struct TileGemmParams {
   const char* a0;           // [rows, K] (or the first ksplit stages of a row)
@@ -46,11 +52,13 @@ struct TileGemmParams {
   char* out;
   const int32_t* kept;      // EPI_RESID: kept list of batch z at kept + z * kept_batch
   const char* res;          // EPI_ADD: [rows, cols]
+  const float* tab;         // EPI_ACT_TAB: [sel_rows, cols], row sel[r] added to row r
   const int32_t* count;     // or null: batch z uses only its first count[z * count_step]
                             // rows (a gate's counted kept list); tiles past them end at once
   int64_t rows;
   int64_t a_bytes;          // bytes of an A row (of each part, when split)
   int64_t k_bytes;          // K in bytes, a multiple of 128
+  int64_t b_ld;             // bytes between B rows (0: k_bytes; a column slice of a wider B)
   int64_t a_batch, b_batch, out_batch;   // byte strides between batches
   int64_t n, kept_batch;    // EPI_RESID: tokens per layer, stride of the kept lists
   int64_t out_ld;           // EPI_RESID: bytes of an H row
@@ -147,6 +155,7 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
         if (a.bias != nullptr) bias[j] = a.bias[ccol[j]];
     }
     int64_t orow[MI][4];   // output row: the tile row, or (EPI_RESID) its H row
+    int64_t trow[MI][4];   // EPI_ACT_TAB: the row's table row
     bool rok[MI][4];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -160,8 +169,12 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
           t = t < 0 ? 0 : (t >= a.n ? a.n - 1 : t);
           orow[i][r] = z * a.n + t;
         }
+        if constexpr (EPI == EPI_ACT_TAB) {
+          const int s = a.sel[orow[i][r]];
+          trow[i][r] = s < 0 ? 0 : (s >= a.sel_rows ? a.sel_rows - 1 : s);
+        }
       }
-    float old[NJ][MI][4];   // EPI_RESID: H, EPI_ADD: the residual
+    float old[NJ][MI][4];   // EPI_RESID: H, EPI_ADD: the residual, EPI_ACT_TAB: the table
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
@@ -169,6 +182,8 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           old[j][i][r] = 0.f;
+          if constexpr (EPI == EPI_ACT_TAB)
+            old[j][i][r] = a.tab[trow[i][r] * a.cols + ccol[j]];
           if constexpr (EPI == EPI_RESID || EPI == EPI_ADD) {
             const char* src = EPI == EPI_RESID
                                   ? a.out + orow[i][r] * a.out_ld + (int64_t)ccol[j] * ES
@@ -196,6 +211,9 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
           char* dst;
           if constexpr (EPI == EPI_ACT || EPI == EPI_STORE) {
             v = EPI == EPI_ACT ? fmaxf(c, 0.f) : c;
+            dst = a.out + (orow[i][r] * a.cols + col[j]) * ES;
+          } else if constexpr (EPI == EPI_ACT_TAB) {
+            v = fmaxf(c + old[j][i][r], 0.f);
             dst = a.out + (orow[i][r] * a.cols + col[j]) * ES;
           } else if constexpr (EPI == EPI_ADD) {
             v = old[j][i][r] + c;
@@ -287,7 +305,7 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
       }
       int r = n0 + c;
       r = r < a.cols ? r : a.cols - 1;
-      p0[b] = base + (int64_t)r * a.k_bytes + chunk * 16;
+      p0[b] = base + (int64_t)r * (a.b_ld != 0 ? a.b_ld : a.k_bytes) + chunk * 16;
       p1[b] = p0[b];
       split_at[b] = nst;
     }

@@ -435,6 +435,28 @@ def test_relevance_lookup(name):
         assert torch.equal(getattr(r, key), getattr(r2, key)), key
 
 
+def test_relevance_table_follows_registration():
+    """The per-scene half of the first layer is computed once per
+    registration and workspace: re-registering another MLP, or the first
+    one again, gives what a fresh handle gives, bit for bit."""
+    from tests.harness import RelevanceRun
+    wl = Workload("bf16_rel_tab", "bf16", 200, 1, 128, 128, 9, 64, 32, 32, 8, 30, usage="uniform")
+    _announce(f"relevance table refresh: {wl}")
+    inp = make_inputs(wl, seed=11, device=DEV)
+    mlp_a = make_relevance(wl, 11, 256, device=DEV)
+    mlp_b = make_relevance(wl, 12, 256, device=DEV)
+    ra = RelevanceRun(inp, mlp_a).run()
+    act_a = ra.act.clone()
+    rb = RelevanceRun(inp, mlp_b, table=ra.table).run()       # re-registers B on A's handle
+    fresh_b = RelevanceRun(inp, mlp_b).run()
+    ra2 = RelevanceRun(inp, mlp_a, table=ra.table).run()      # and A again
+    torch.cuda.synchronize()
+    assert not torch.equal(act_a, rb.act)
+    for key in ("act", "prim", "w"):
+        assert torch.equal(getattr(rb, key), getattr(fresh_b, key)), key
+    assert torch.equal(ra2.act, act_a)
+
+
 # Sparse injection through the SwiGLU fusion (Eq. 10): (workload, d_ff,
 # sampled tokens or None).  Rows of unit scale (value_std 1) so that f is of
 # the order of H; ragged kept counts and widths (d_h 80, d_ff 192, n_keep
