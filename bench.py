@@ -465,8 +465,11 @@ class Bench:
             b["inject"] = None
         if self.mlp is not None:
             hid = self.mlp["hidden"]
-            # the two MLP layers (the cosines are 2 k d_e per row, negligible)
-            flops["score"] = 2 * rows * 2 * wl.d_e * hid + 2 * rows * hid * wl.prims
+            # the two MLP layers per row: the query half of the first (its
+            # scene half is a per-scene table, computed once per registered
+            # MLP, not per step) and the second; the cosines are 2 k d_e per
+            # row, negligible
+            flops["score"] = 2 * rows * wl.d_e * hid + 2 * rows * hid * wl.prims
             b["score"] = None
         return b, flops, nonempty
 
