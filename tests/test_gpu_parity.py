@@ -372,13 +372,14 @@ def test_layers_batched_equal_sequential():
 # tokens or None for all).  Ragged rows and primitive counts (200, 37, 300)
 # leave partial 64 x 64 tiles in both layers; the image and multi-scale
 # cases have the benchmarks' shapes.  Hidden rows of 512 or 1024 bytes take
-# the fused second layer + top-k (bf16 with k <= 16: the 32 x 32 tile form,
-# else 16 x 16): the "fused" cases cover both widths in both dtypes and both
-# forms, a ragged last block of W2 rows (P 37, 300, 1000; at P 300 the last
-# 32-key block's second image lies wholly past P), W2 split into ranges
-# merged afterwards (P 300 over 2, P 1000 over 4 with a short last range, the
-# image shape over 8), a unit with rows for one wave only (130 rows) and one
-# range of 4096 rows (Zipf).
+# the fused second layer + top-k (bf16 batches of >= 4096 rows with k <= 16:
+# the 32 x 32 tile form, else 16 x 16): the "fused" and "rel32" cases cover
+# both widths in both dtypes and both forms, ragged last blocks of W2 rows
+# (P 37, 300, 1000; at P 300 the last 32-key block's second image lies
+# wholly past P), W2 split into ranges merged afterwards (P 300 over 2,
+# P 1000 over 4 with a short last range, the image shape over 8), units with
+# rows for one wave only (130 rows, 4200 rows) and one range of 4096 rows
+# (Zipf).
 RELEVANCE = {
     "bf16_rel_fused_h256": (Workload("bf16_rel_fused_h256", "bf16", 130, 1, 128, 64, 7, 300, 32,
                                      32, 32, 30, usage="uniform"), 256, None),
@@ -389,6 +390,16 @@ RELEVANCE = {
     "f32_rel_fused_h256": (Workload("f32_rel_fused_h256", "f32", 200, 1, 96, 64, 6, 1000, 40, 40,
                                     8, 40, usage="uniform"), 256, None),
     "bf16_rel_zipf": (WORKLOADS[4], 512, 40),
+    # batches of >= 4096 rows take the 32 x 32 form: 512-byte hidden rows with
+    # ragged P (300: the last 32-key block's second image wholly past P; two
+    # ranges) and a ragged last unit (4200 rows), 1024-byte rows with P 1000
+    # and k 16, and k 4
+    "bf16_rel32_h256_p300": (Workload("bf16_rel32_h256_p300", "bf16", 4200, 1, 128, 64, 7, 300,
+                                      32, 32, 8, 30, usage="uniform"), 256, 48),
+    "bf16_rel32_h512_p1000_k16": (Workload("bf16_rel32_h512_p1000_k16", "bf16", 4100, 1, 128, 64,
+                                           5, 1000, 32, 32, 16, 30, usage="uniform"), 512, 48),
+    "bf16_rel32_k4": (Workload("bf16_rel32_k4", "bf16", 4096, 1, 128, 64, 3, 200, 32, 32, 4, 30,
+                               usage="iid"), 256, 48),
     # query rows of 512 and 1024 bytes with k < 32 take the weights on the
     # matrix cores: both widths, both dtypes, k < 16 (one tile with the
     # query), k = 16 (the query broadcast) and k = 20 (two tiles); k = 32
