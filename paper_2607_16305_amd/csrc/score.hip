@@ -737,6 +737,22 @@ static int route_unit_rows(int64_t rows, int shared_rows) {
 
 static int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
+// Key ranges per row block of the tile kernel (at least `least`, so that a
+// unit's bias table fits its LDS).  The kernel runs one workgroup a CU (its
+// LDS): when the row blocks alone fill whole rounds of the 256 CUs to 90%,
+// no split (each unit walks every key tile, no partial lists to merge;
+// Zipf batch 176 -> 164 us against two splits); else about 512 workgroups
+// (measured better than rounds filled with one-tile units, whose pipeline
+// start and merge cost more than a partial round's idle CUs: multi-scale
+// batch 51 us with 2 splits, 55 with 4).
+static int route_splits(int64_t blocks, int tiles, int least) {
+  const double fill = (double)blocks / (double)(cdiv(blocks, 256) * 256);
+  if (least <= 1 && fill >= 0.9) return 1;
+  int sp = blocks < 512 ? cdiv(512, blocks) : 1;
+  sp = sp < tiles ? sp : tiles;
+  return sp > least ? sp : least;
+}
+
 RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes, bool cos) {
   RoutePlan p{ROUTE_SHARED, 1, S, 0};
   if (rows <= 0 || S <= 0) return p;
@@ -749,10 +765,8 @@ RoutePlan route_plan(int64_t rows, int S, int64_t row_bytes, bool cos) {
     // 512 workgroups run (and at most ROUTE_DTL_MAX_TPS tiles stay with one
     // workgroup, whose bias table lives in LDS)
     const int tiles = cdiv(S, ROUTE_DTL_KEYS);
-    int sp = blocks < 512 ? cdiv(512, blocks) : 1;
-    sp = sp < tiles ? sp : tiles;
     const int least = cdiv(tiles, ROUTE_DTL_MAX_TPS);
-    sp = sp > least ? sp : least;
+    int sp = route_splits(blocks, tiles, least);
     const int tps = cdiv(tiles, sp);
     sp = cdiv(tiles, tps);
     if (sp == 1 || blocks <= ROUTE_COUNTERS) {
