@@ -218,7 +218,9 @@ lookme_status_t lookme_inject_noalloc(lookme_t h, int32_t layers, int64_t n, int
  * -- the set that lookme_inject selects.  It reads no routing or lookup
  * result and its part of the workspace is disjoint from theirs, so it may run
  * on another stream, concurrently with lookme_route / lookme_lookup of the
- * same batch; lookme_inject_kept then adds the rows.  Requires
+ * same batch; lookme_inject_kept then adds the rows.  Made for that: its
+ * norms run on one workgroup a CU (they leave most of every CU to the
+ * kernels beside them, and take longer alone than lookme_inject's).  Requires
  * 0 <= n_keep <= n, d_c * elem_size a multiple of 16 bytes, kept_out non-NULL
  * when n_keep > 0 (n_keep = 0 does nothing).  Needs the workspace of
  * lookme_workspace_size.

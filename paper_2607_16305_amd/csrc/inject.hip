@@ -22,6 +22,7 @@
 namespace lookme {
 
 constexpr int NORM_WAVES = 4;
+constexpr int64_t NORM_BACKGROUND_WGS = 256;
 constexpr int INJ_THREADS = 256;
 
 template <int DT>
@@ -29,10 +30,11 @@ __global__ __launch_bounds__(NORM_WAVES * WAVE) void crit_norm_kernel(
     const char* __restrict__ crit, int64_t rows, int64_t row_bytes,
     uint32_t* __restrict__ key) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * NORM_WAVES + (threadIdx.x >> 6);
-  if (r >= rows) return;
-  const float acc = row_sumsq<DT>(crit + r * row_bytes, (int)(row_bytes / 16), lane);
-  if (lane == 0) key[r] = as_u32(acc);
+  for (int64_t r = (int64_t)blockIdx.x * NORM_WAVES + (threadIdx.x >> 6); r < rows;
+       r += (int64_t)gridDim.x * NORM_WAVES) {
+    const float acc = row_sumsq<DT>(crit + r * row_bytes, (int)(row_bytes / 16), lane);
+    if (lane == 0) key[r] = as_u32(acc);
+  }
 }
 
 template <int CN>
@@ -167,10 +169,16 @@ static void launch_inject_k(int kk, dim3 grid, hipStream_t st, int64_t n, int64_
 }
 
 hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uint32_t* key,
-                            hipStream_t st) {
+                            hipStream_t st, bool background) {
   if (rows == 0) return hipSuccess;
   const int es = dt == DT_BF16 ? 2 : 4;
-  const dim3 grid((unsigned)((rows + NORM_WAVES - 1) / NORM_WAVES));
+  // a wave a row; in the background form 256 workgroups walk the rows, one
+  // per CU, so that the norms leave the projection and routing running
+  // beside them most of every CU (Zipf batch: those two 312 -> 289 us, the
+  // step 2.248 -> 2.216 ms median, while the norms stretch from 107 to
+  // ~185 us behind them)
+  const int64_t g0 = (rows + NORM_WAVES - 1) / NORM_WAVES;
+  const dim3 grid((unsigned)(background && g0 > NORM_BACKGROUND_WGS ? NORM_BACKGROUND_WGS : g0));
   if (dt == DT_BF16)
     hipLaunchKernelGGL(crit_norm_kernel<DT_BF16>, grid, dim3(NORM_WAVES * WAVE), 0, st,
                        static_cast<const char*>(crit), rows, (int64_t)d_c * es, key);

@@ -203,8 +203,11 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
                          const hipEvent_t* stamp = nullptr);
 
 // ---- criticality, select and injection ------------------------------------
+// background: a grid of one workgroup a CU walking the rows, for norms that
+// run on a second stream beside the projection and routing (slower alone,
+// but they take less of each CU from the kernels beside them)
 hipError_t launch_crit_norm(int dt, int64_t rows, const void* crit, int d_c, uint32_t* key,
-                            hipStream_t st);
+                            hipStream_t st, bool background = false);
 hipError_t launch_crit_select(int layers, int64_t n, int64_t n_keep, const uint32_t* key,
                               int32_t* kept, hipStream_t st);
 // The injections' count of rows with an index out of range (see

@@ -266,12 +266,12 @@ class Stamped {
 // criticality norms and, when n_keep > 0, the top-n_keep select (Eq. 9)
 lookme_status_t run_select(lookme_t h, const Layout& L, int32_t layers, int64_t n,
                            int64_t n_keep, const void* crit, int32_t d_c, int32_t* kept,
-                           hipStream_t st) {
+                           hipStream_t st, bool background = false) {
   uint32_t* key = reinterpret_cast<uint32_t*>(static_cast<char*>(h->ws) + L.crit_key);
   {
     Timed tm(h, LOOKME_GROUP_NORM, st);
     LOOKME_TRY(hip_status(lookme::launch_crit_norm(h->d.dtype, (int64_t)layers * n, crit, d_c,
-                                                   key, st),
+                                                   key, st, background),
                           "criticality launch"));
   }
   if (n_keep == 0) return LOOKME_OK;
@@ -686,7 +686,10 @@ lookme_status_t lookme_select(lookme_t h, int32_t layers, int64_t n, int64_t n_k
   LOOKME_TRY(check_ptr(kept_out, "kept_out"));
   Layout L;
   LOOKME_TRY(check_workspace(h, layers, n, &L));
-  return run_select(h, L, layers, n, n_keep, crit, d_c, kept_out, static_cast<hipStream_t>(stream));
+  // the norms in their background form: lookme_select is the call that runs
+  // beside lookme_route / lookme_lookup on a second stream
+  return run_select(h, L, layers, n, n_keep, crit, d_c, kept_out, static_cast<hipStream_t>(stream),
+                    true);
 }
 
 lookme_status_t lookme_inject_kept(lookme_t h, int32_t layers, int64_t n, int64_t n_keep,
