@@ -81,8 +81,10 @@ def parse():
                     help="select the kept set on a second stream even where the lookup's "
                          "bucketing launch can carry it (batches of at most 1024 rows)")
     ap.add_argument("--select-on-main", action="store_true",
-                    help="run the select on the launch stream before routing instead of on a "
-                         "second stream beside it (times its kernels without the overlap)")
+                    help="run the select on the launch stream instead of on a second stream "
+                         "beside projection and routing (times its kernels without the overlap: "
+                         "the plain path through lookme_inject after the lookup, the others "
+                         "through lookme_select before routing)")
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="first run a plain 256 MiB read+write kernel (counter calibration)")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -337,7 +339,8 @@ class Bench:
         # kept buffer it overwrites) and runs beside the projection and
         # routing; measured faster than beside the Level-2 lookup, whose
         # workgroups it would slow
-        if self.select_on_main and not self.gate:
+        plain = not self.gate and self.fus is None and not self.scales
+        if self.select_on_main and not self.gate and not plain:
             lk.lookme_select(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.kept,
                              self.stream)
         self.ev_start.record(self.main)
@@ -379,6 +382,11 @@ class Bench:
             else:
                 lk.lookme_inject_fused_gated(h, L, n, self.kept, self.count, self.scene,
                                              self.prim, self.w, self.hidden, wl.d_h, self.stream)
+        elif plain and self.select_on_main:
+            # norms, select and the adds in one call on the launch stream, each
+            # kernel alone on the chip (the norms in their full-grid form)
+            lk.lookme_inject(h, L, n, wl.n_keep, inp["delta"], wl.crit_dim, self.scene,
+                             self.prim, self.w, self.hidden, wl.d_h, self.kept, self.stream)
         elif self.fus is None:
             lk.lookme_inject_kept(h, L, n, wl.n_keep, self.kept, self.scene, self.prim, self.w,
                                   self.hidden, wl.d_h, self.stream)
@@ -847,7 +855,9 @@ def main():
                                "launch (one stream)" if args.gate else
                                "norms in the bucketing launch, top-n_keep in the Level-2 launch "
                                "(one stream)") if b.one_stream
-                              else "launch stream, before routing" if b.select_on_main
+                              else ("launch stream, in lookme_inject after the lookup"
+                                    if not (args.fusion or args.scales) else
+                                    "launch stream, before routing") if b.select_on_main
                               else "second stream beside projection and routing"),
                    "kept_set": ("learned gate, " + "+".join(str(c) for c in b.count.tolist())
                                 + " open" if args.gate else f"top {wl.n_keep} by criticality")},
