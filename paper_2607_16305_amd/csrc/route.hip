@@ -7,7 +7,8 @@
 // 2 x 4 grid each compute a 64 x 64 block of every tile.  The queries and the
 // keys of a tile stream through LDS in 128-byte K stages by direct global-to-
 // LDS loads (dtl.h), one stream of stages across all of the workgroup's key
-// tiles, the next stage in flight while one is multiplied.  After a tile's
+// tiles, the next stages in flight while one is multiplied; the operand
+// fragments are read from LDS half a stage ahead of their products.  After a tile's
 // last stage every lane folds its scores (plus the bias, staged in LDS) into
 // a running best per row; at the end the 16 lanes and then the 4 waves that
 // share a row are merged in key order.  When a batch has few row blocks the
@@ -51,6 +52,7 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
   constexpr int MI = RT_MI, NJ = RT_NJ, KB = RT_KB, KSL = KB / 64, NS = rt_stages(BIAS);
   constexpr int THREADS = 64 * RT_WM * RT_WN;
   static_assert(NS >= 2, "a stage in flight while one is multiplied");
+  static_assert(KSL == 2, "a stage is two 64-byte halves");
   // All of the kernel's LDS is one object.  With several __shared__ objects
   // the compiler tags their accesses with alias scopes and then, finding the
   // stage buffers' direct-to-LDS loads and fragment reads in one scope, puts
@@ -163,43 +165,64 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
     }
   }
 
+  // Fragments are read one half-stage (a 64-byte K slice) ahead of the
+  // products that use them: f0 holds the first half of a stage, f1 the
+  // second.  The second half's reads are issued before the first half's
+  // products, the next stage's first half after the barrier that makes it
+  // visible, so the products of each half run while the next half's reads
+  // are in flight.
+  u32x4_t f0a[MI], f0b[NJ], f1a[MI], f1b[NJ];
+  auto read_half = [&](const char* buf, int ks, u32x4_t (&fa)[MI], u32x4_t (&fb)[NJ]) {
 #pragma unroll
-  for (int i = 0; i < NS - 1; ++i) issue();
+    for (int i = 0; i < MI; ++i) fa[i] = read_frag<KB>(buf, wm + 16 * i, ks, n16, g);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
+  };
+  auto products = [&](const u32x4_t (&fa)[MI], const u32x4_t (&fb)[NJ]) {
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_chunk<DT>(fa[i], fb[j], acc[i][j]);
+  };
+  // matrix-core instructions per fragment pair, fragment reads per half-stage
+  constexpr int MPC = DT == DT_BF16 ? 1 : 4, READS = MI + NJ;
+
+  // every buffer of the ring filled: stages 0 .. NS - 1 in flight
+#pragma unroll
+  for (int i = 0; i < NS; ++i) issue();
+  // stage 0 has landed (the NS - 1 younger stages may be outstanding) and
+  // the barrier makes every wave's part visible (and the bias table)
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 1) * S::PER_WAVE) : "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  read_half(lds[0], 0, f0a, f0b);
   // the consumer's position: tile within the unit, K stage, buffer
   int c_tile = 0, c_stage = 0, c_buf = 0;
   for (int sigma = 0; sigma < total; ++sigma) {
-    // this wave's loads of stage sigma have landed once at most those of the
-    // NS - 2 younger stages are outstanding; the barrier makes every wave's
-    // visible (and the bias table, the first time) and ends every read of
-    // stage sigma - 1, whose buffer the next loads fill (a plain s_barrier:
-    // the fence of __syncthreads would wait for every load in flight; the
-    // empty asm statements keep LDS accesses on their side)
+    const char* buf = lds[c_buf];
+    const char* nbuf = lds[c_buf == NS - 1 ? 0 : c_buf + 1];
+    // the first product waits for f0 (read during the previous half-stage's
+    // products); the second half's reads go out behind it, so that at most
+    // one half-stage of reads is outstanding (the LDS counter holds 15)
+    read_half(buf, 1, f1a, f1b);
+    products(f0a, f0b);
+    __builtin_amdgcn_sched_group_barrier(0x008, MPC, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, MPC * (MI * NJ - 1), 0);
+    // stage sigma + 1 has landed once at most the loads of the NS - 2
+    // younger stages are outstanding; after the barrier it is visible and
+    // no wave reads this stage's buffer any more, so the loads of stage
+    // sigma + NS refill it (a plain s_barrier: the fence of __syncthreads
+    // would wait for every load in flight; the scheduling barriers keep the
+    // products on their side of it)
+    __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NS - 2) * S::PER_WAVE) : "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
     issue();
-    const char* buf = lds[c_buf];
-    // the first stage of a tile starts its accumulators from zero (the MFMA
-    // takes a zero operand; no register is cleared)
-    auto stage = [&](auto first) {
-#pragma unroll
-      for (int ks = 0; ks < KSL; ++ks) {
-        u32x4_t fa[MI], fb[NJ];
-#pragma unroll
-        for (int i = 0; i < MI; ++i) fa[i] = read_frag<KB>(buf, wm + 16 * i, ks, n16, g);
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) fb[j] = read_frag<KB>(buf, S::BM + wn + 16 * j, ks, n16, g);
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-          for (int j = 0; j < NJ; ++j)
-            acc[i][j] = mfma_chunk<DT>(fa[i], fb[j],
-                                       (decltype(first)::value && ks == 0)
-                                           ? f32x4_t{0.f, 0.f, 0.f, 0.f} : acc[i][j]);
-      }
-    };
-    if (c_stage == 0) stage(std::true_type{});
-    else stage(std::false_type{});
+    read_half(nbuf, 0, f0a, f0b);
+    products(f1a, f1b);
     c_buf = c_buf == NS - 1 ? 0 : c_buf + 1;
     if (c_stage == nst - 1) {
       // the tile is complete: the lane holds rows wm + 16 i + 4 g + r and
@@ -232,6 +255,10 @@ __global__ __launch_bounds__(64 * RT_WM * RT_WN) void route_dtl_kernel(RouteDtlP
             bi[i][r] = v > bs[i][r] ? kj[j] : bi[i][r];
             bs[i][r] = fmaxf(bs[i][r], v);
           }
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       c_stage = 0;
       ++c_tile;
     } else {
