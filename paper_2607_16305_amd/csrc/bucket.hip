@@ -34,30 +34,53 @@ __device__ __forceinline__ int stream_units(int size) {
 }
 
 // List position of shared unit i and of streaming unit j (nb shared and ns
-// streaming units in all): the two kinds alternate while both last, shared
-// first, then the rest of the longer kind.  A CU then tends to hold one
-// shared unit (matrix-core and vector work on keys mostly found in L2) and
-// one streaming unit (HBM-bound) at a time; with the shared units first, the
-// Zipf workload's 487 of them filled every slot for the first ~300 us while
-// the key stream from HBM ran at about half its rate.
-__device__ __forceinline__ int shared_pos(int i, int ns) { return i < ns ? 2 * i : ns + i; }
-__device__ __forceinline__ int stream_pos(int j, int nb) { return j < nb ? 2 * j + 1 : nb + j; }
+// streaming units in all): while both last, groups of one shared unit and
+// ORDER_STREAM streaming units (c groups), then the rest of the shared units,
+// then the rest of the streaming ones.  About a quarter of the resident
+// units are then shared ones (matrix-core and vector work on keys mostly
+// found in L2) and the rest stream keys from HBM.  With every shared unit
+// first, the Zipf workload's 487 of them filled every slot for the first
+// ~300 us while the key stream from HBM ran at about half its rate; with
+// the kinds alternating one to one, the first ~550 us still had half of the
+// slots on shared units and the stream at ~6.3 TB/s; one to three: 7.1-7.3
+// TB/s there (Zipf Level-2 1836 -> 1829 us, multi-scale 186 -> 183 us).
+constexpr int ORDER_STREAM = 3;
+__device__ __forceinline__ int order_groups(int nb, int ns) { return min(nb, ns / ORDER_STREAM); }
+__device__ __forceinline__ int shared_pos(int i, int nb, int ns) {
+  const int c = order_groups(nb, ns);
+  return i < c ? i * (ORDER_STREAM + 1) : c * (ORDER_STREAM + 1) + (i - c);
+}
+__device__ __forceinline__ int stream_pos(int j, int nb, int ns) {
+  const int c = order_groups(nb, ns);
+  return j < c * ORDER_STREAM ? (j / ORDER_STREAM) * (ORDER_STREAM + 1) + 1 + j % ORDER_STREAM
+                              : nb + j;
+}
 
 // Writes the units of scene s: shared ones as shared units sh.., a streaming
-// one as streaming unit st (list positions from shared_pos / stream_pos).
+// one as streaming unit st (list positions from shared_pos / stream_pos).  Of
+// the last nsplit streaming units (all past the groups: ns - nsplit >=
+// ORDER_STREAM c) each becomes two entries, its halves, from position
+// nb + ns - nsplit on.
 __device__ __forceinline__ void write_units(int s, int offset, int size, int sh, int st, int nb,
-                                            int ns, int shared_rows, int32_t* unit_scene,
-                                            int32_t* unit_begin) {
+                                            int ns, int nsplit, int shared_rows,
+                                            int32_t* unit_scene, int32_t* unit_begin) {
   if (size == 0) return;
   if (size <= UNIT_STREAM_ROWS) {
-    const int p = stream_pos(st, nb);
+    const int first = ns - nsplit;
+    if (st >= first) {
+      const int p = nb + first + 2 * (st - first);
+      unit_scene[p] = unit_scene[p + 1] = s;
+      unit_begin[p] = unit_begin[p + 1] = offset;
+      return;
+    }
+    const int p = stream_pos(st, nb, ns);
     unit_scene[p] = s;
     unit_begin[p] = offset;
     return;
   }
   const int units = shared_units(size, shared_rows);
   for (int u = 0; u < units; ++u) {
-    const int p = shared_pos(sh + u, ns);
+    const int p = shared_pos(sh + u, nb, ns);
     unit_scene[p] = s | UNIT_SHARED;
     unit_begin[p] = offset + u * shared_rows;
   }
@@ -66,7 +89,8 @@ __device__ __forceinline__ void write_units(int s, int offset, int size, int sh,
 int64_t bucket_chunks(int64_t rows) { return (rows + BK_THREADS - 1) / BK_THREADS; }
 
 int64_t bucket_max_units(int64_t rows, int S) {
-  return std::min<int64_t>(S, rows) + (rows + TILE_ROWS - 1) / TILE_ROWS;
+  // the halves of a cut last round add at most SPLIT_UNITS entries
+  return std::min<int64_t>(S, rows) + (rows + TILE_ROWS - 1) / TILE_ROWS + SPLIT_UNITS;
 }
 
 __device__ __forceinline__ int clamp_scene(int s, int S) { return s < 0 ? 0 : (s >= S ? S - 1 : s); }
@@ -143,12 +167,15 @@ __device__ __forceinline__ void block_excl_scan3(int (&v)[3], int (&tot)[3]) {
 }
 
 // Offsets of the buckets [s0, s1) given their sizes in size_of(s), and the
-// work list: returns the unit count through *unit_count (thread 0).
+// work list: the entry count, the first half's position and a zero fetch
+// count into unit_count[0..2] (thread 0).  split_max: the number of last
+// streaming units to cut in halves, when the streaming units outnumber the
+// shared ones by that many and fill at least two rounds with them (else 0).
 template <typename SizeOf, typename SetOffset>
 __device__ __forceinline__ void offsets_and_units(int S, int shared_rows, SizeOf size_of,
                                                   SetOffset set_offset, int32_t* offsets,
                                                   int32_t* unit_scene, int32_t* unit_begin,
-                                                  int32_t* unit_count) {
+                                                  int32_t* unit_count, int split_max = 0) {
   const int ipt = (S + BK_THREADS - 1) / BK_THREADS;
   const int s0 = min(S, (int)threadIdx.x * ipt), s1 = min(S, s0 + ipt);
   int v[3] = {0, 0, 0};   // rows, shared units, streaming units
@@ -160,18 +187,25 @@ __device__ __forceinline__ void offsets_and_units(int S, int shared_rows, SizeOf
   }
   int tot[3];
   block_excl_scan3(v, tot);
+  const int nb = tot[1], ns = tot[2];
+  const int nsplit = (split_max > 0 && ns - split_max >= ORDER_STREAM * order_groups(nb, ns) &&
+                      ns - nb >= split_max && nb + ns >= 2 * split_max)
+                         ? split_max
+                         : 0;
   int row = v[0], sh = v[1], st = v[2];
   for (int s = s0; s < s1; ++s) {
     const int size = size_of(s);
     set_offset(s, row);
-    write_units(s, row, size, sh, st, tot[1], tot[2], shared_rows, unit_scene, unit_begin);
+    write_units(s, row, size, sh, st, nb, ns, nsplit, shared_rows, unit_scene, unit_begin);
     row += size;
     sh += shared_units(size, shared_rows);
     st += stream_units(size);
   }
   if (threadIdx.x == 0) {
     offsets[S] = tot[0];
-    *unit_count = tot[1] + tot[2];
+    unit_count[0] = nb + ns + nsplit;
+    unit_count[1] = nb + ns - nsplit;
+    unit_count[2] = 0;
   }
 }
 
@@ -209,7 +243,7 @@ template <bool COLS>
 __global__ __launch_bounds__(BK_THREADS) void bucket_scan_kernel(
     int32_t* __restrict__ chunk_hist, int64_t chunks, int S, int shared_rows,
     int32_t* __restrict__ offsets, int32_t* __restrict__ unit_scene,
-    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count) {
+    int32_t* __restrict__ unit_begin, int32_t* __restrict__ unit_count, int split_max) {
   if constexpr (!COLS) {
     for (int s = threadIdx.x; s < S; s += BK_THREADS) {
       int run = 0;
@@ -230,7 +264,8 @@ __global__ __launch_bounds__(BK_THREADS) void bucket_scan_kernel(
   // exclusive scan of the bucket sizes over scenes: offsets and the work list
   offsets_and_units(
       S, shared_rows, [&](int s) { return offsets[s]; },
-      [&](int s, int off) { offsets[s] = off; }, offsets, unit_scene, unit_begin, unit_count);
+      [&](int s, int off) { offsets[s] = off; }, offsets, unit_scene, unit_begin, unit_count,
+      split_max);
 }
 
 __global__ __launch_bounds__(BK_THREADS) void bucket_scatter_kernel(
@@ -377,11 +412,11 @@ hipError_t launch_bucket(const int32_t* scene, int64_t rows, int S, int shared_r
                        st, ws.chunk_hist, chunks, S, ws.offsets);
     hipLaunchKernelGGL(bucket_scan_kernel<true>, dim3(1), dim3(BK_THREADS), 0, st, ws.chunk_hist,
                        chunks, S, shared_rows, ws.offsets, ws.unit_scene, ws.unit_begin,
-                       ws.unit_count);
+                       ws.unit_count, ws.split_max);
   } else {
     hipLaunchKernelGGL(bucket_scan_kernel<false>, dim3(1), dim3(BK_THREADS), 0, st, ws.chunk_hist,
                        chunks, S, shared_rows, ws.offsets, ws.unit_scene, ws.unit_begin,
-                       ws.unit_count);
+                       ws.unit_count, ws.split_max);
   }
   hipLaunchKernelGGL(bucket_scatter_kernel, dim3((unsigned)chunks), dim3(BK_THREADS), 0, st,
                      scene, rows, S, ws.chunk_hist, ws.local_rank, ws.offsets, ws.perm);

@@ -73,13 +73,15 @@ constexpr int32_t MAX_SCENES = 16384;   // bucketing keeps one histogram per chu
 // Workspace layout for `layers` x `n` rows.
 struct Layout {
   size_t chunk_hist, local_rank, offsets, perm, unit_scene, unit_begin, unit_count, route_count,
-      route_part, crit_key, kept, rel_tab, rel_logits, fus_r, fus_u, ms_r, ms_q, total;
+      route_part, split_row, split_part, crit_key, kept, rel_tab, rel_logits, fus_r, fus_u, ms_r,
+      ms_q, total;
 };
 
 // The leading bytes of the workspace hold counters that start at zero; they
 // are zero-filled once when the workspace is attached and every call leaves
 // them at zero.
-constexpr size_t ZEROED_BYTES = 256 + lookme::ROUTE_COUNTERS * 4;
+constexpr size_t ZEROED_BYTES =
+    256 + lookme::ROUTE_COUNTERS * 4 + (size_t)lookme::SPLIT_UNITS * lookme::UNIT_STREAM_ROWS * 4;
 
 Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, int32_t relevance,
               int32_t fusion_dff, int32_t scales) {
@@ -95,6 +97,7 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, int32_t relevan
   };
   L.unit_count = take(256);   // counters first: the region zeroed at set-up
   L.route_count = take((size_t)lookme::ROUTE_COUNTERS * 4);
+  L.split_row = take((size_t)lookme::SPLIT_UNITS * lookme::UNIT_STREAM_ROWS * 4);
   // the relevance MLP's per-scene table [S, hidden] float32, kept across
   // calls: at an offset that does not depend on the batch
   L.rel_tab = take(relevance ? (size_t)d.num_scenes * relevance * 4 : 0);
@@ -108,6 +111,9 @@ Layout layout(const lookme_desc_t& d, int32_t layers, int64_t n, int32_t relevan
   L.perm = take((size_t)rows * 4);
   L.unit_scene = take((size_t)units * 4);
   L.unit_begin = take((size_t)units * 4);
+  // the partial lists of a Level-2 launch's cut last round (batches of at
+  // least two rounds of units)
+  L.split_part = take(rows >= 2 * lookme::SPLIT_UNITS ? lookme::SPLIT_PART_BYTES : 0);
   L.crit_key = take((size_t)rows * 4);
   L.kept = take((size_t)rows * 4);
   // relevance logits [rows, P] float32, when an MLP is registered (the
@@ -337,6 +343,21 @@ lookme_status_t run_lookup(lookme_t h, const Layout& L, int32_t layers, int64_t 
   const bool select = sel != nullptr && (sel->n_keep > 0 || gate);
   // the Level-2 kernels that carry a select score dot products only
   const bool cos = d.score == LOOKME_SCORE_COS;
+  // the last round of streaming units may be cut in halves (kernels.h) where
+  // the streaming units keep their key blocks in LDS, each half holds at
+  // least k keys, no select rides in the Level-2 launch (one-chunk batches
+  // with a select, below), and the batch averages at most one streaming
+  // unit's rows a scene (with more, few buckets are streaming units; the
+  // merge's launch, ~4 us, would then be spent on nothing: multi-scale and
+  // 4-layer workloads)
+  const int64_t key_bytes = (int64_t)d.key_dim * elem_size(d.dtype);
+  const bool cut = rows >= 2 * lookme::SPLIT_UNITS &&
+                   rows <= (int64_t)lookme::UNIT_STREAM_ROWS * d.num_scenes &&
+                   lookme::score_ks(key_bytes) <= 16 && d.prims_per_scene >= 512 &&
+                   d.top_k <= lookme::SPLIT_KMAX && !(select && !cos && b.chunks == 1);
+  b.split_max = cut ? lookme::SPLIT_UNITS : 0;
+  b.split_part = reinterpret_cast<uint64_t*>(ws + L.split_part);
+  b.split_row = reinterpret_cast<int32_t*>(ws + L.split_row);
   bool normed = false;
   {
     Timed tm(h, LOOKME_GROUP_BUCKET, st);

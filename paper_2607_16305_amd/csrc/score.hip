@@ -51,7 +51,9 @@ struct ScoreParams {
   const int32_t* offsets;   // lookup: bucket offsets [S+1]
   const int32_t* unit_scene;
   const int32_t* unit_begin;
-  const int32_t* unit_count;
+  int32_t* unit_count;      // lookup: [3] (kernels.h); [2] counts the halves taken
+  uint64_t* split_part;     // lookup: the halves' partial lists (SPLIT_PART_BYTES)
+  int32_t* split_row;       // lookup: [SPLIT_UNITS, 16] output row + 1 of a cut unit's rows, else 0
   int64_t rows;             // routing: number of query rows
   int64_t row_bytes;        // d_e * elem size
   int ks;                   // chunk steps per row = row_bytes / 64
@@ -112,6 +114,60 @@ template <bool LOOKUP>
 __device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, int slot) {
   if constexpr (LOOKUP) return a.perm[begin + slot];
   else return begin + slot;
+}
+
+// The partial list slot of row t of half h of cut unit `pair`: SPLIT_KMAX
+// entries (index << 32 | score bits), sorted as the outputs.
+__device__ __forceinline__ uint64_t* split_slot(const ScoreParams& a, int pair, int h, int t) {
+  return a.split_part + ((int64_t)(pair * 2 + h) * UNIT_STREAM_ROWS + t) * SPLIT_KMAX;
+}
+
+// The top k of a row's two partial lists by the order of the outputs (score
+// descending, then index ascending; the first half's keys are the lower
+// ones).  The two lists, the second reversed, form a bitonic sequence of
+// 2 KL entries (padded with -inf); one half-cleaner keeps the larger of each
+// pair at distance KL, which leaves the top KL as a bitonic sequence that
+// log2(KL) more half-cleaner rounds sort (static register indices only).
+template <int KL>
+__device__ __forceinline__ void merge_halves(const uint64_t* A, const uint64_t* B, int k,
+                                             float (&top_s)[KL], int (&top_i)[KL]) {
+  float cs[2 * KL];
+  int ci[2 * KL];
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    const bool in = e < k;
+    const uint64_t x = A[e], y = B[e];   // a whole slot (entries from k on: padding)
+    cs[e] = in ? __uint_as_float((uint32_t)x) : -__builtin_inff();
+    ci[e] = in ? (int)(x >> 32) : 0x7fffffff;
+    cs[2 * KL - 1 - e] = in ? __uint_as_float((uint32_t)y) : -__builtin_inff();
+    ci[2 * KL - 1 - e] = in ? (int)(y >> 32) : 0x7fffffff;
+  }
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    const bool w = beats(cs[e + KL], ci[e + KL], cs[e], ci[e]);
+    cs[e] = w ? cs[e + KL] : cs[e];
+    ci[e] = w ? ci[e + KL] : ci[e];
+  }
+#pragma unroll
+  for (int d = KL / 2; d >= 1; d >>= 1) {
+#pragma unroll
+    for (int e = 0; e < KL; ++e) {
+      if ((e & d) == 0) {
+        const bool w = beats(cs[e + d], ci[e + d], cs[e], ci[e]);
+        const float ts = cs[e];
+        const int ti = ci[e];
+        cs[e] = w ? cs[e + d] : cs[e];
+        ci[e] = w ? ci[e + d] : ci[e];
+        cs[e + d] = w ? ts : cs[e + d];
+        ci[e + d] = w ? ti : ci[e + d];
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < KL; ++e) {
+    top_s[e] = cs[e];
+    top_i[e] = ci[e];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -285,9 +341,17 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
 // block's loads are issued into the image, so they fly while the block is
 // multiplied and folded.  The waves never wait for each other until the
 // merge.  LDS: 4 waves x KS KiB, so that two workgroups fit a CU.
+// half (0 or 1, -1 for a whole unit): a half of a cut unit (kernels.h) takes
+// the first ceil(nblk / 2) key blocks or the rest and keeps the exact top k
+// of its keys for each row in the partial list slot of `pair`, which
+// split_merge_kernel merges after the launch.  (Merging in the second half
+// to finish, after an agent-scope acquire-release arrival, cost more than
+// the extra launch: each release writes back the XCD's L2 and each acquire
+// invalidates it, 1861.7 against 1833 + 8 us on the Zipf workload.)
 template <int DT, int KS, bool MASKED, int KL, bool COS>
 __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem, int64_t begin,
-                                                int nr, const char* keys) {
+                                                int nr, const char* keys, int half = -1,
+                                                int pair = 0) {
   constexpr int NL = SC_WAVES * 4;   // candidate lists per query row
   constexpr int BLOCK = KS * 1024;
   static_assert(KS <= 16, "fragments of a block held in registers");
@@ -305,9 +369,11 @@ __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem
                              g, a.ks);
 
   const int nblk = (nkeys + 15) >> 4;
-  const int bpw = (nblk + SC_WAVES - 1) / SC_WAVES;
-  const int kb0 = wv * bpw;
-  const int kb1 = min(nblk, kb0 + bpw);
+  const int hb = (nblk + 1) >> 1;
+  const int rb0 = half == 1 ? hb : 0, rb1 = half == 0 ? hb : nblk;   // the unit's blocks
+  const int bpw = (rb1 - rb0 + SC_WAVES - 1) / SC_WAVES;
+  const int kb0 = rb0 + wv * bpw;
+  const int kb1 = min(rb1, kb0 + bpw);
   const int kend = min(nkeys, kb1 * 16);
 
   uint32_t off[KS];
@@ -385,7 +451,36 @@ __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem
   float top_s[KL];
   int top_i[KL];
   merge_lists<KL, 4>(ms, mi, a.k, 1, top_s, top_i);
-  if (L == 0 && t < nr) write_row<true, KL>(a, row_id<true>(a, begin, t), top_s, top_i);
+  if (half < 0) {
+    if (L == 0 && t < nr) write_row<true, KL>(a, row_id<true>(a, begin, t), top_s, top_i);
+    return;
+  }
+  if (L == 0 && t < nr) {
+    uint64_t* o = split_slot(a, pair, half, t);
+#pragma unroll
+    for (int e = 0; e < KL; ++e)
+      if (e < a.k) o[e] = ((uint64_t)(uint32_t)top_i[e] << 32) | __float_as_uint(top_s[e]);
+    // the first half names the row's output row for the merge (plus one:
+    // zero marks a slot row with nothing to merge)
+    if (half == 0) a.split_row[pair * UNIT_STREAM_ROWS + t] = (int32_t)row_id<true>(a, begin, t) + 1;
+  }
+}
+
+// The merge of the cut units' halves, after the Level-2 launch on the same
+// stream: thread (pair, t) merges row t's two partial lists when the first
+// half named an output row for it, writes the outputs as the whole unit would
+// have, and clears the name for the next launch.
+template <int KL>
+__global__ __launch_bounds__(256) void split_merge_kernel(ScoreParams a) {
+  const int pair = blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int t = threadIdx.x & 15;
+  const int named = a.split_row[pair * UNIT_STREAM_ROWS + t];
+  if (named == 0) return;
+  float top_s[KL];
+  int top_i[KL];
+  merge_halves<KL>(split_slot(a, pair, 0, t), split_slot(a, pair, 1, t), a.k, top_s, top_i);
+  write_row<true, KL>(a, named - 1, top_s, top_i);
+  a.split_row[pair * UNIT_STREAM_ROWS + t] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -643,15 +738,34 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   bool shared;
   const char* keys;
   int key0 = 0, nk = a.nkeys, split = 0;
+  int half = -1, pair = 0;   // lookup: a half of a cut unit (kernels.h)
   bool multi = false;
   if constexpr (LOOKUP) {
-    // units in list order (shared and streaming alternating), dealt to the
-    // XCDs in fours: two consecutive shared units of a bucket cut into
-    // several (list positions 4q and 4q + 2) read their keys into one XCD's
-    // L2, while a scene with many units is still spread over all
+    // units in list order (groups of one shared and three streaming units
+    // while both kinds last), dealt to the XCDs in fours: each XCD takes a
+    // whole group at a time, the same mix of the two kinds
     const int b = blockIdx.x, slot = b >> 3;
-    const int u = (slot >> 2) * 32 + (b & 7) * 4 + (slot & 3);
-    if (u >= *a.unit_count) return;
+    int u = (slot >> 2) * 32 + (b & 7) * 4 + (slot & 3);
+    const int total = a.unit_count[0], first_half = a.unit_count[1];
+    if (u >= first_half) {
+      // past the statically dealt units: the halves of the cut last round go
+      // to whichever workgroups start first (those of the XCDs that are
+      // through with their units), one fetch a workgroup; the slot past the
+      // LDS's other uses carries the result to every wave
+      if (KS > 16 || first_half == total) return;   // halves only with KS <= 16
+      int* s_u = reinterpret_cast<int*>(smem + SMEM);
+      if (threadIdx.x == 0) {
+        int v = total;
+        if (__hip_atomic_load(&a.unit_count[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
+            total - first_half)
+          v = first_half + __hip_atomic_fetch_add(&a.unit_count[2], 1, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+        *s_u = v;
+      }
+      __syncthreads();
+      u = *s_u;
+      if (u >= total) return;
+    }
     const int tag = a.unit_scene[u];
     const int s = tag & ~UNIT_SHARED;
     shared = (tag & UNIT_SHARED) != 0;
@@ -659,6 +773,10 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     nr = min(shared ? a.shared_rows : UNIT_STREAM_ROWS, a.offsets[s + 1] - (int)begin);
     multi = a.offsets[s + 1] - a.offsets[s] > a.shared_rows;
     keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
+    if (u >= first_half) {
+      half = (u - first_half) & 1;
+      pair = (u - first_half) >> 1;
+    }
   } else {
     const int R = a.route_rows;
     const int splits = R > 16 ? 1 : a.route_splits;
@@ -674,9 +792,10 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     keys = a.keys + (int64_t)key0 * a.row_bytes;
   }
   if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, multi);
-  else if constexpr (LOOKUP && KS <= 16) stream_unit_lds<DT, KS, MASKED, KL, COS>(a, smem, begin, nr, keys);
+  else if constexpr (LOOKUP && KS <= 16) stream_unit_lds<DT, KS, MASKED, KL, COS>(a, smem, begin, nr, keys, half, pair);
   else stream_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, key0, nk, split);
 }
+
 
 // ---------------------------------------------------------------------------
 // Launchers
@@ -824,6 +943,22 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
   return launch_dt<false, 1>(dt, p.ks, (int)round8(units), p, st);
 }
 
+// The Level-2 launch and, when the bucketing may cut the last round, the
+// merge of the halves right after it on the same stream (its threads return
+// at once where nothing was cut).  With stamps, the pair of events brackets
+// both launches.
+template <int KL>
+static hipError_t launch_lookup_kl(int dt, int grid, const ScoreParams& p, bool split,
+                                   hipStream_t st, const hipEvent_t* stamp) {
+  if (!split) return launch_dt<true, KL>(dt, p.ks, grid, p, st, stamp);
+  const hipEvent_t first[2] = {stamp != nullptr ? stamp[0] : nullptr, nullptr};
+  const hipError_t e = launch_dt<true, KL>(dt, p.ks, grid, p, st, stamp != nullptr ? first : nullptr);
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL((split_merge_kernel<KL>), dim3(SPLIT_UNITS / 16), dim3(256), 0, st,
+                        nullptr, stamp != nullptr ? stamp[1] : nullptr, 0, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const BucketWs& ws,
                          int d_e, int P, int k, int32_t* prim, float* w, hipStream_t st,
                          const SideSelect* side, bool cos, const hipEvent_t* stamp) {
@@ -843,6 +978,8 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
   p.k = k;
   p.out_idx = prim;
   p.out_w = w;
+  p.split_part = ws.split_part;
+  p.split_row = ws.split_row;
   int grid = (int)((ws.max_units + 31) / 32 * 32);   // whole fours on every XCD
   if (side != nullptr && (side->n_keep > 0 || side->count != nullptr) && side->n > 0) {
     p.side0 = grid;
@@ -853,10 +990,10 @@ hipError_t launch_lookup(int dt, const void* q, const void* prim_keys, const Buc
     p.gate_count = side->count;
     grid += side->layers;
   }
-  if (k <= 4) return launch_dt<true, 4>(dt, p.ks, grid, p, st, stamp);
-  if (k <= 8) return launch_dt<true, 8>(dt, p.ks, grid, p, st, stamp);
-  if (k <= 16) return launch_dt<true, 16>(dt, p.ks, grid, p, st, stamp);
-  return launch_dt<true, 32>(dt, p.ks, grid, p, st, stamp);
+  if (k <= 4) return launch_lookup_kl<4>(dt, grid, p, ws.split_max > 0, st, stamp);
+  if (k <= 8) return launch_lookup_kl<8>(dt, grid, p, ws.split_max > 0, st, stamp);
+  if (k <= 16) return launch_lookup_kl<16>(dt, grid, p, ws.split_max > 0, st, stamp);
+  return launch_lookup_kl<32>(dt, grid, p, ws.split_max > 0, st, stamp);
 }
 
 }  // namespace lookme

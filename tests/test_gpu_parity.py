@@ -102,6 +102,50 @@ def test_small_workloads_every_token(name):
         assert np.mean(got == lab) > 0.99
 
 
+# Batches whose last round of Level-2 units is cut in halves (more than two
+# rounds of single-bucket streaming units, P >= 512): masked bf16 keys with
+# k = 16, fp32 with k = 32 (the widest partial list) and a ragged last key
+# block (P = 520) over two layers, the cosine scores, and Zipf buckets (shared
+# units in groups with streaming ones ahead of the halves); and one batch the
+# host allows to cut but whose buckets are too few (no halves, the merge
+# launch finds nothing).
+CUT = {
+    "bf16_cut_k16": (Workload("bf16_cut_k16", "bf16", 2048, 1, 64, 64, 2048, 512, 16, 16, 16,
+                              20, usage="uniform"), "dot", True),
+    "f32_cut_k32_p520": (Workload("f32_cut_k32_p520", "f32", 1500, 2, 64, 64, 3000, 520, 16, 16,
+                                  32, 20, usage="uniform"), "dot", True),
+    "bf16_cut_cos": (Workload("bf16_cut_cos", "bf16", 2048, 1, 64, 64, 2048, 512, 16, 16, 8, 20,
+                              usage="uniform"), "cos", True),
+    "bf16_cut_zipf": (Workload("bf16_cut_zipf", "bf16", 8000, 1, 64, 64, 2048, 512, 16, 16, 16,
+                               20, usage="zipf"), "dot", True),
+    "bf16_cut_declined": (Workload("bf16_cut_declined", "bf16", 1100, 1, 64, 64, 100, 512, 16,
+                                   16, 8, 20, usage="uniform"), "dot", False),
+}
+
+
+@pytest.mark.parametrize("name", list(CUT))
+def test_cut_last_round_every_token(name):
+    """The Level-2 launch whose last 512 streaming units run as two halves
+    each (partial top-k lists merged after the launch) against the oracle on
+    every token; the work list's counters show the halves were made and
+    taken."""
+    wl, score, cut = CUT[name]
+    _announce(f"{name}: {wl} score={score}")
+    r, _ = _run_check(make_inputs(wl, seed=5, device=DEV), score=score)
+    torch.cuda.synchronize()
+    entries, first_half, taken = r.table.ws[:12].view(torch.int32).cpu().tolist()
+    assert entries - first_half == (2 * 512 if cut else 0), (entries, first_half)
+    assert taken >= (2 * 512 if cut else 0)
+    # the merge's row names (after the routing counters at the start of the
+    # workspace) are back at zero, and a second lookup gives the same bits
+    named = r.table.ws[256 + 4096 * 4:256 + 4096 * 4 + 512 * 16 * 4].view(torch.int32)
+    assert int(named.abs().sum()) == 0
+    prim2, w2 = torch.full_like(r.prim, -7), torch.full_like(r.w, -7.0)
+    r.table.lookup(r.q, r.scene, prim2, w2, layers=r.L)
+    torch.cuda.synchronize()
+    assert torch.equal(prim2, r.prim) and torch.equal(w2, r.w)
+
+
 def test_tiny_f32_workload_every_token():
     from tests.harness import check_end_to_end_run
     wl = WORKLOADS[0]
