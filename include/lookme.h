@@ -96,7 +96,7 @@ lookme_status_t lookme_create(const lookme_desc_t* desc, const void* scene_keys,
 lookme_status_t lookme_workspace_size(lookme_t h, int32_t layers, int64_t n_tokens,
                                       size_t* bytes);
 
-/* Attach caller-owned device workspace (256-byte aligned, at least 16640
+/* Attach caller-owned device workspace (256-byte aligned, at least 49408
  * bytes; lookme_workspace_size gives what a call needs).  The library
  * zero-fills a small counter region of it once here (hipMemset on the current
  * device); every call leaves those counters at zero again.  The workspace
@@ -128,7 +128,10 @@ lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in
  *   prim_out [layers, n, k] int32   the k primitives p in [0, N_p) of largest
  *                                   <q, prim_keys[scene, p]>, score-descending
  *   w_out    [layers, n, k] float32 softmax of those k scores (temperature 1)
- * Needs a workspace of at least lookme_workspace_size(layers, n).
+ * Needs a workspace of at least lookme_workspace_size(layers, n).  Launches
+ * the bucketing, the Level-2 scoring and, for batches of at least 1024 rows
+ * averaging at most 16 rows a scene, a small launch after it that merges the
+ * halves of work units cut in two (the outputs are the same bits either way).
  */
 lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void* q,
                               const int32_t* scene, int32_t* prim_out, float* w_out,
