@@ -812,7 +812,8 @@ def main():
     score_ms = prof.get("score")
     if b.mlp is None:
         achieved = bytes_["score"] / (score_ms * 1e-3) / 1e9 if score_ms else None
-        roofline = {"bound": "hbm", "kernel": "score_kernel (Level-2 scoring + top-k + softmax)",
+        roofline = {"bound": "hbm", "kernel": "score_kernel (Level-2 scoring + top-k + softmax; "
+                    "with split_merge_kernel where the last round is cut)",
                     "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS,
                     "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
