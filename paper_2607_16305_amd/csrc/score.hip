@@ -394,7 +394,10 @@ __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem
     load_key_block<KS, MASKED, KS>(im, a, keys, blk * 16, kend, off, 0, 1, img, lane);
   };
 
-  // the query fragments land before the key stream starts
+  // the first key block goes out with the query fragments (one memory round
+  // trip at the unit's start instead of two); both land before the loop, so
+  // that no load is outstanding at its head
+  if (kb0 < kb1) issue(kb0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   float qinv = 0.f;
   if constexpr (COS) {
@@ -404,7 +407,6 @@ __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem
       if (!MASKED || j < a.ks) qsq = chunk_sumsq<DT>(qb[j], qsq);
     qinv = inv_norm(sum_lane_groups(qsq));
   }
-  if (kb0 < kb1) issue(kb0);
   for (int blk = kb0; blk < kb1; ++blk) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // block blk is in the image
     u32x4_t kf[KS];
@@ -601,10 +603,13 @@ __device__ __forceinline__ void shared_unit(const ScoreParams& a, char* smem, in
         load_key_block<KS, MASKED, PW>(im, a, keys, blk * 16, nkeys, off, wv, SC_WAVES,
                                        smem + (blk % NBUF) * BLOCK_BYTES, lane, nt);
     };
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // query fragments first
-    qnorms();
+    // the ring's first blocks go out with the query fragments (one memory
+    // round trip at the unit's start instead of two); all land before the
+    // loop, so that no load is outstanding at its head
 #pragma unroll
     for (int b = 0; b < NBUF - 1; ++b) issue(b);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    qnorms();
     for (int blk = 0; blk < nblk; ++blk) {
       // this wave's loads of block blk have landed once at most those of the
       // NBUF - 2 younger blocks are outstanding (near the end, or with masked
