@@ -457,7 +457,18 @@ class Bench:
         if self.gate:
             gl = self.w_g.shape[0]
             b["norm"] = gl * n * wl.crit_dim * es + gl * wl.crit_dim * es + gl * n * 4
-        b["inject"] = keep * (k * wl.d_v * es + 2 * wl.d_v * es + k * 8 + 8)
+        # the injection reads each distinct value row of the kept tokens'
+        # picks once (the caches serve its repeats), H read and written, the
+        # picks and weights read
+        fetched = keep * k
+        self.inject_rows = {"fetched": fetched, "distinct": fetched}
+        if not (self.gate or self.scales or self.fus is not None):
+            kept = self.kept[:, :wl.n_keep].long()
+            sc = torch.gather(self.scene.long(), 1, kept)
+            pr = torch.gather(self.prim.long(), 1, kept.unsqueeze(-1).expand(-1, -1, k))
+            self.inject_rows["distinct"] = int(torch.unique(sc.unsqueeze(-1) * wl.prims + pr).numel())
+        b["inject"] = (self.inject_rows["distinct"] * wl.d_v * es
+                       + keep * (2 * wl.d_v * es + k * 8 + 8))
         flops = {"project": 2 * n * wl.d_in * L * wl.d_e, "route": 2 * rows * wl.d_e * scenes,
                  "score": 2 * rows * wl.d_e * wl.prims}
         if self.scales:
@@ -808,6 +819,8 @@ def main():
             e["hbm_frac"] = round(gbs / HBM_PEAK_GBS, 4)
         if name in flops:
             e["tflops"] = round(flops[name] / (ms * 1e-3) / 1e12, 2)
+        if name == "inject" and bytes_.get(name):
+            e["value_rows"] = b.inject_rows
         kern[name] = e
     score_ms = prof.get("score")
     if b.mlp is None:
