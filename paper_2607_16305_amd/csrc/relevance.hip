@@ -771,7 +771,7 @@ __global__ __launch_bounds__(256) void relevance_weights_mma_kernel(
   // products: G[T] = tile T x tile T^T, and with two tiles C = tile 0 x
   // tile 1^T (keys 0..15 against keys 16.. and the query); lane (g, n) holds
   // [row 4g + r][row n]
-  const int kt = k >> 4, kr = k & 15;   // the query's tile and row
+  const int kr = k & 15;   // the query's row in its tile (tile k >> 4)
   f32x4_t G[NTT], C = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int T = 0; T < NTT; ++T) {
@@ -790,7 +790,7 @@ __global__ __launch_bounds__(256) void relevance_weights_mma_kernel(
     const float v = __shfl(G[NTT - 1][r], 16 * (kr >> 2) + kr, 64);
     qq = (kr & 3) == r ? v : qq;
   }
-  // lanes n == kr hold key (4g + r) . q of each tile: tile kt in its own
+  // lanes n == kr hold key (4g + r) . q of each tile: tile k >> 4 in its own
   // product, tile 0 (when the query is in tile 1) in C
   float z[NTT][4];
 #pragma unroll
