@@ -131,7 +131,7 @@ lookme_status_t lookme_route(lookme_t h, int32_t layers, int64_t n, int32_t d_in
  * Needs a workspace of at least lookme_workspace_size(layers, n).  Launches
  * the bucketing, the Level-2 scoring and, for batches of at least 1024 rows
  * averaging at most 16 rows a scene, a small launch after it that merges the
- * halves of work units cut in two (the outputs are the same bits either way).
+ * parts of work units cut in two (the outputs are the same bits either way).
  */
 lookme_status_t lookme_lookup(lookme_t h, int32_t layers, int64_t n, const void* q,
                               const int32_t* scene, int32_t* prim_out, float* w_out,

@@ -59,7 +59,7 @@ __device__ __forceinline__ int stream_pos(int j, int nb, int ns) {
 // Writes the units of scene s: shared ones as shared units sh.., a streaming
 // one as streaming unit st (list positions from shared_pos / stream_pos).  Of
 // the last nsplit streaming units (all past the groups: ns - nsplit >=
-// ORDER_STREAM c) each becomes two entries, its halves, from position
+// ORDER_STREAM c) each becomes SPLIT_PARTS entries, its parts, from position
 // nb + ns - nsplit on.
 __device__ __forceinline__ void write_units(int s, int offset, int size, int sh, int st, int nb,
                                             int ns, int nsplit, int shared_rows,
@@ -68,9 +68,11 @@ __device__ __forceinline__ void write_units(int s, int offset, int size, int sh,
   if (size <= UNIT_STREAM_ROWS) {
     const int first = ns - nsplit;
     if (st >= first) {
-      const int p = nb + first + 2 * (st - first);
-      unit_scene[p] = unit_scene[p + 1] = s;
-      unit_begin[p] = unit_begin[p + 1] = offset;
+      const int p = nb + first + SPLIT_PARTS * (st - first);
+      for (int q = 0; q < SPLIT_PARTS; ++q) {
+        unit_scene[p + q] = s;
+        unit_begin[p + q] = offset;
+      }
       return;
     }
     const int p = stream_pos(st, nb, ns);
@@ -89,8 +91,10 @@ __device__ __forceinline__ void write_units(int s, int offset, int size, int sh,
 int64_t bucket_chunks(int64_t rows) { return (rows + BK_THREADS - 1) / BK_THREADS; }
 
 int64_t bucket_max_units(int64_t rows, int S) {
-  // the halves of a cut last round add at most SPLIT_UNITS entries
-  return std::min<int64_t>(S, rows) + (rows + TILE_ROWS - 1) / TILE_ROWS + SPLIT_UNITS;
+  // the parts of a cut last round add at most (SPLIT_PARTS - 1) SPLIT_UNITS
+  // entries
+  return std::min<int64_t>(S, rows) + (rows + TILE_ROWS - 1) / TILE_ROWS +
+         (int64_t)(SPLIT_PARTS - 1) * SPLIT_UNITS;
 }
 
 __device__ __forceinline__ int clamp_scene(int s, int S) { return s < 0 ? 0 : (s >= S ? S - 1 : s); }
@@ -167,9 +171,9 @@ __device__ __forceinline__ void block_excl_scan3(int (&v)[3], int (&tot)[3]) {
 }
 
 // Offsets of the buckets [s0, s1) given their sizes in size_of(s), and the
-// work list: the entry count, the first half's position and a zero fetch
+// work list: the entry count, the first part's position and a zero fetch
 // count into unit_count[0..2] (thread 0).  split_max: the number of last
-// streaming units to cut in halves, when the streaming units outnumber the
+// streaming units to cut in parts, when the streaming units outnumber the
 // shared ones by that many and fill at least two rounds with them (else 0).
 template <typename SizeOf, typename SetOffset>
 __device__ __forceinline__ void offsets_and_units(int S, int shared_rows, SizeOf size_of,
@@ -203,7 +207,7 @@ __device__ __forceinline__ void offsets_and_units(int S, int shared_rows, SizeOf
   }
   if (threadIdx.x == 0) {
     offsets[S] = tot[0];
-    unit_count[0] = nb + ns + nsplit;
+    unit_count[0] = nb + ns + (SPLIT_PARTS - 1) * nsplit;
     unit_count[1] = nb + ns - nsplit;
     unit_count[2] = 0;
   }

@@ -71,21 +71,23 @@ hipError_t launch_route_dtl(int dt, const void* q, const void* scene_keys, const
 //
 // The launch's last round: when the streaming units outnumber the shared ones
 // by at least SPLIT_UNITS (and the caller allows it), the last SPLIT_UNITS
-// streaming units of the list are each cut into two halves of the scene's
-// key blocks, listed as consecutive entries at the end.  Each half keeps the
-// exact top k of its keys as a partial list; a small launch after the
-// Level-2 launch merges the two (the results are those of the whole unit,
-// bit for bit).  unit_count holds [0] the number of list entries, [1] the
-// position of the first half (= [0] without halves), [2] the count of halves
-// taken so far by the Level-2 launch's workgroups past the statically dealt
-// units (zeroed by the bucketing).
+// streaming units of the list are each cut into SPLIT_PARTS parts, equal
+// ranges of the scene's key blocks, listed as consecutive entries at the end.
+// Each part keeps the exact top k of its keys as a partial list; a small
+// launch after the Level-2 launch merges a unit's lists (the results are
+// those of the whole unit, bit for bit).  unit_count holds [0] the number of
+// list entries, [1] the position of the first part (= [0] without parts),
+// [2] the count of parts taken so far by the Level-2 launch's workgroups past
+// the statically dealt units (zeroed by the bucketing).
 constexpr int UNIT_STREAM_ROWS = 16;
 constexpr int32_t UNIT_SHARED = 1 << 30;
 constexpr int SPLIT_UNITS = 512;
+constexpr int SPLIT_PARTS = 2;
 constexpr int SPLIT_KMAX = 32;   // entries of a partial list slot (k <= 32)
-// partial lists: [SPLIT_UNITS pairs][2 halves][16 rows][SPLIT_KMAX] of
-// (index << 32 | score bits)
-constexpr size_t SPLIT_PART_BYTES = (size_t)SPLIT_UNITS * 2 * UNIT_STREAM_ROWS * SPLIT_KMAX * 8;
+// partial lists: [SPLIT_UNITS units][SPLIT_PARTS parts][16 rows][SPLIT_KMAX]
+// of (index << 32 | score bits)
+constexpr size_t SPLIT_PART_BYTES =
+    (size_t)SPLIT_UNITS * SPLIT_PARTS * UNIT_STREAM_ROWS * SPLIT_KMAX * 8;
 // Chunk steps (64 bytes of a key row each) the scoring kernel is compiled
 // for, given the row width: 4, 8, 16 or 32 exactly; narrower rows run the
 // 4-step kernel and other widths the 32-step kernel, with the steps past the
@@ -112,11 +114,11 @@ struct BucketWs {
   int32_t* perm;         // [rows]
   int32_t* unit_scene;   // [max_units]
   int32_t* unit_begin;   // [max_units]
-  int32_t* unit_count;   // [3]: entries, first half, halves taken
+  int32_t* unit_count;   // [3]: entries, first part, parts taken
   int64_t chunks;
   int64_t max_units;
   int split_max;         // SPLIT_UNITS or 0: whether the last round may be cut
-  uint64_t* split_part;  // [SPLIT_PART_BYTES] partial lists of the halves
+  uint64_t* split_part;  // [SPLIT_PART_BYTES] partial lists of the parts
   int32_t* split_row;    // [SPLIT_UNITS, 16] output row + 1 of a cut unit's rows, zero between launches
 };
 int64_t bucket_chunks(int64_t rows);

@@ -51,8 +51,8 @@ struct ScoreParams {
   const int32_t* offsets;   // lookup: bucket offsets [S+1]
   const int32_t* unit_scene;
   const int32_t* unit_begin;
-  int32_t* unit_count;      // lookup: [3] (kernels.h); [2] counts the halves taken
-  uint64_t* split_part;     // lookup: the halves' partial lists (SPLIT_PART_BYTES)
+  int32_t* unit_count;      // lookup: [3] (kernels.h); [2] counts the parts taken
+  uint64_t* split_part;     // lookup: the cut units' partial lists (SPLIT_PART_BYTES)
   int32_t* split_row;       // lookup: [SPLIT_UNITS, 16] output row + 1 of a cut unit's rows, else 0
   int64_t rows;             // routing: number of query rows
   int64_t row_bytes;        // d_e * elem size
@@ -116,59 +116,12 @@ __device__ __forceinline__ int64_t row_id(const ScoreParams& a, int64_t begin, i
   else return begin + slot;
 }
 
-// The partial list slot of row t of half h of cut unit `pair`: SPLIT_KMAX
+// The partial list slot of row t of part `part` of cut unit `cut`: SPLIT_KMAX
 // entries (index << 32 | score bits), sorted as the outputs.
-__device__ __forceinline__ uint64_t* split_slot(const ScoreParams& a, int pair, int h, int t) {
-  return a.split_part + ((int64_t)(pair * 2 + h) * UNIT_STREAM_ROWS + t) * SPLIT_KMAX;
+__device__ __forceinline__ uint64_t* split_slot(const ScoreParams& a, int cut, int part, int t) {
+  return a.split_part + ((int64_t)(cut * SPLIT_PARTS + part) * UNIT_STREAM_ROWS + t) * SPLIT_KMAX;
 }
 
-// The top k of a row's two partial lists by the order of the outputs (score
-// descending, then index ascending; the first half's keys are the lower
-// ones).  The two lists, the second reversed, form a bitonic sequence of
-// 2 KL entries (padded with -inf); one half-cleaner keeps the larger of each
-// pair at distance KL, which leaves the top KL as a bitonic sequence that
-// log2(KL) more half-cleaner rounds sort (static register indices only).
-template <int KL>
-__device__ __forceinline__ void merge_halves(const uint64_t* A, const uint64_t* B, int k,
-                                             float (&top_s)[KL], int (&top_i)[KL]) {
-  float cs[2 * KL];
-  int ci[2 * KL];
-#pragma unroll
-  for (int e = 0; e < KL; ++e) {
-    const bool in = e < k;
-    const uint64_t x = A[e], y = B[e];   // a whole slot (entries from k on: padding)
-    cs[e] = in ? __uint_as_float((uint32_t)x) : -__builtin_inff();
-    ci[e] = in ? (int)(x >> 32) : 0x7fffffff;
-    cs[2 * KL - 1 - e] = in ? __uint_as_float((uint32_t)y) : -__builtin_inff();
-    ci[2 * KL - 1 - e] = in ? (int)(y >> 32) : 0x7fffffff;
-  }
-#pragma unroll
-  for (int e = 0; e < KL; ++e) {
-    const bool w = beats(cs[e + KL], ci[e + KL], cs[e], ci[e]);
-    cs[e] = w ? cs[e + KL] : cs[e];
-    ci[e] = w ? ci[e + KL] : ci[e];
-  }
-#pragma unroll
-  for (int d = KL / 2; d >= 1; d >>= 1) {
-#pragma unroll
-    for (int e = 0; e < KL; ++e) {
-      if ((e & d) == 0) {
-        const bool w = beats(cs[e + d], ci[e + d], cs[e], ci[e]);
-        const float ts = cs[e];
-        const int ti = ci[e];
-        cs[e] = w ? cs[e + d] : cs[e];
-        ci[e] = w ? ci[e + d] : ci[e];
-        cs[e + d] = w ? ts : cs[e + d];
-        ci[e + d] = w ? ti : ci[e + d];
-      }
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < KL; ++e) {
-    top_s[e] = cs[e];
-    top_i[e] = ci[e];
-  }
-}
 
 // ---------------------------------------------------------------------------
 // Level-2 key blocks in LDS (the image layout: KeyImage, topk.h)
@@ -341,17 +294,19 @@ __device__ __forceinline__ void stream_unit(const ScoreParams& a, char* smem, in
 // block's loads are issued into the image, so they fly while the block is
 // multiplied and folded.  The waves never wait for each other until the
 // merge.  LDS: 4 waves x KS KiB, so that two workgroups fit a CU.
-// half (0 or 1, -1 for a whole unit): a half of a cut unit (kernels.h) takes
-// the first ceil(nblk / 2) key blocks or the rest and keeps the exact top k
-// of its keys for each row in the partial list slot of `pair`, which
-// split_merge_kernel merges after the launch.  (Merging in the second half
-// to finish, after an agent-scope acquire-release arrival, cost more than
-// the extra launch: each release writes back the XCD's L2 and each acquire
-// invalidates it, 1861.7 against 1833 + 8 us on the Zipf workload.)
+// part (0 .. SPLIT_PARTS - 1, -1 for a whole unit): a part of a cut unit
+// (kernels.h) takes blocks [part nblk / SPLIT_PARTS, (part + 1) nblk /
+// SPLIT_PARTS) of the scene's keys and keeps the exact top k of its keys for
+// each row in the partial list slot of cut unit `cut`, which
+// split_merge_kernel merges after the launch.  (Merging in the last part to
+// finish, after an agent-scope acquire-release arrival, cost more than the
+// extra launch: each release writes back the XCD's L2 and each acquire
+// invalidates it, 1861.7 against 1833 + 8 us on the Zipf workload with two
+// parts.)
 template <int DT, int KS, bool MASKED, int KL, bool COS>
 __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem, int64_t begin,
-                                                int nr, const char* keys, int half = -1,
-                                                int pair = 0) {
+                                                int nr, const char* keys, int part = -1,
+                                                int cut = 0) {
   constexpr int NL = SC_WAVES * 4;   // candidate lists per query row
   constexpr int BLOCK = KS * 1024;
   static_assert(KS <= 16, "fragments of a block held in registers");
@@ -369,8 +324,9 @@ __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem
                              g, a.ks);
 
   const int nblk = (nkeys + 15) >> 4;
-  const int hb = (nblk + 1) >> 1;
-  const int rb0 = half == 1 ? hb : 0, rb1 = half == 0 ? hb : nblk;   // the unit's blocks
+  // the unit's blocks
+  const int rb0 = part < 0 ? 0 : part * nblk / SPLIT_PARTS;
+  const int rb1 = part < 0 ? nblk : (part + 1) * nblk / SPLIT_PARTS;
   const int bpw = (rb1 - rb0 + SC_WAVES - 1) / SC_WAVES;
   const int kb0 = rb0 + wv * bpw;
   const int kb1 = min(rb1, kb0 + bpw);
@@ -453,36 +409,86 @@ __device__ __forceinline__ void stream_unit_lds(const ScoreParams& a, char* smem
   float top_s[KL];
   int top_i[KL];
   merge_lists<KL, 4>(ms, mi, a.k, 1, top_s, top_i);
-  if (half < 0) {
+  if (part < 0) {
     if (L == 0 && t < nr) write_row<true, KL>(a, row_id<true>(a, begin, t), top_s, top_i);
     return;
   }
   if (L == 0 && t < nr) {
-    uint64_t* o = split_slot(a, pair, half, t);
+    uint64_t* o = split_slot(a, cut, part, t);
 #pragma unroll
     for (int e = 0; e < KL; ++e)
       if (e < a.k) o[e] = ((uint64_t)(uint32_t)top_i[e] << 32) | __float_as_uint(top_s[e]);
-    // the first half names the row's output row for the merge (plus one:
+    // the first part names the row's output row for the merge (plus one:
     // zero marks a slot row with nothing to merge)
-    if (half == 0) a.split_row[pair * UNIT_STREAM_ROWS + t] = (int32_t)row_id<true>(a, begin, t) + 1;
+    if (part == 0) a.split_row[cut * UNIT_STREAM_ROWS + t] = (int32_t)row_id<true>(a, begin, t) + 1;
   }
 }
 
-// The merge of the cut units' halves, after the Level-2 launch on the same
-// stream: thread (pair, t) merges row t's two partial lists when the first
-// half named an output row for it, writes the outputs as the whole unit would
-// have, and clears the name for the next launch.
+// The merge of the cut units' parts, after the Level-2 launch on the same
+// stream: 2 KL lanes a row slot (cut unit, t).  Where the first part named an
+// output row for it, lane e < KL holds the e-th entry of the merged lists so
+// far and lane KL + e entry KL - 1 - e of the next part's list (a bitonic
+// sequence, padded with -inf); the xor-partner compare-exchanges of a bitonic
+// merge sort it by the order of the outputs (score descending, then index
+// ascending), one part after another.  The row's outputs are then written as
+// write_row writes them (the softmax sum in entry order, in every lane) and
+// the name is cleared for the next launch.
 template <int KL>
 __global__ __launch_bounds__(256) void split_merge_kernel(ScoreParams a) {
-  const int pair = blockIdx.x * 16 + (threadIdx.x >> 4);
-  const int t = threadIdx.x & 15;
-  const int named = a.split_row[pair * UNIT_STREAM_ROWS + t];
+  constexpr int LPR = 2 * KL;                    // lanes a row slot
+  constexpr int RPW = WAVE / LPR;                // row slots a wave
+  static_assert(RPW >= 1 && (SPLIT_UNITS * UNIT_STREAM_ROWS) % (4 * RPW) == 0, "whole waves");
+  const int lane = threadIdx.x & 63;
+  const int slot = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW + lane / LPR;
+  const int e = lane % LPR, base = lane - e;
+  const int named = a.split_row[slot];
+  if (!__any(named != 0)) return;                // nothing cut here (wave-uniform)
+  const int cut = slot / UNIT_STREAM_ROWS, t = slot % UNIT_STREAM_ROWS;
+  const int k = a.k;
+  float s = -__builtin_inff();
+  int i = 0x7fffffff;
+  if (e < KL && e < k && named != 0) {
+    const uint64_t v = split_slot(a, cut, 0, t)[e];
+    s = __uint_as_float((uint32_t)v);
+    i = (int)(v >> 32);
+  }
+#pragma unroll
+  for (int q = 1; q < SPLIT_PARTS; ++q) {
+    if (e >= KL) {
+      const int r = LPR - 1 - e;
+      s = -__builtin_inff();
+      i = 0x7fffffff;
+      if (r < k && named != 0) {
+        const uint64_t v = split_slot(a, cut, q, t)[r];
+        s = __uint_as_float((uint32_t)v);
+        i = (int)(v >> 32);
+      }
+    }
+#pragma unroll
+    for (int d = KL; d >= 1; d >>= 1) {
+      const float os = __shfl_xor(s, d, WAVE);
+      const int oi = __shfl_xor(i, d, WAVE);
+      // the lower lane of the pair keeps the winner, the upper the other
+      const bool take = (e & d) == 0 ? beats(os, oi, s, i) : beats(s, i, os, oi);
+      s = take ? os : s;
+      i = take ? oi : i;
+    }
+  }
   if (named == 0) return;
-  float top_s[KL];
-  int top_i[KL];
-  merge_halves<KL>(split_slot(a, pair, 0, t), split_slot(a, pair, 1, t), a.k, top_s, top_i);
-  write_row<true, KL>(a, named - 1, top_s, top_i);
-  a.split_row[pair * UNIT_STREAM_ROWS + t] = 0;
+  const float s0 = __shfl(s, base, WAVE);
+  float sum = 0.f;
+#pragma unroll
+  for (int x = 0; x < KL; ++x) {
+    const float sx = __shfl(s, base + x, WAVE);
+    if (x < k) sum += expf(sx - s0);
+  }
+  const float inv = 1.0f / sum;
+  if (e < k) {
+    const int64_t row = named - 1;
+    a.out_idx[row * k + e] = i;
+    a.out_w[row * k + e] = expf(s - s0) * inv;
+  }
+  if (e == 0) a.split_row[slot] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -743,7 +749,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
   bool shared;
   const char* keys;
   int key0 = 0, nk = a.nkeys, split = 0;
-  int half = -1, pair = 0;   // lookup: a half of a cut unit (kernels.h)
+  int part = -1, cut = 0;   // lookup: a part of a cut unit (kernels.h)
   bool multi = false;
   if constexpr (LOOKUP) {
     // units in list order (groups of one shared and three streaming units
@@ -751,19 +757,19 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     // whole group at a time, the same mix of the two kinds
     const int b = blockIdx.x, slot = b >> 3;
     int u = (slot >> 2) * 32 + (b & 7) * 4 + (slot & 3);
-    const int total = a.unit_count[0], first_half = a.unit_count[1];
-    if (u >= first_half) {
-      // past the statically dealt units: the halves of the cut last round go
+    const int total = a.unit_count[0], first_part = a.unit_count[1];
+    if (u >= first_part) {
+      // past the statically dealt units: the parts of the cut last round go
       // to whichever workgroups start first (those of the XCDs that are
       // through with their units), one fetch a workgroup; the slot past the
       // LDS's other uses carries the result to every wave
-      if (KS > 16 || first_half == total) return;   // halves only with KS <= 16
+      if (KS > 16 || first_part == total) return;   // parts only with KS <= 16
       int* s_u = reinterpret_cast<int*>(smem + SMEM);
       if (threadIdx.x == 0) {
         int v = total;
         if (__hip_atomic_load(&a.unit_count[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
-            total - first_half)
-          v = first_half + __hip_atomic_fetch_add(&a.unit_count[2], 1, __ATOMIC_RELAXED,
+            total - first_part)
+          v = first_part + __hip_atomic_fetch_add(&a.unit_count[2], 1, __ATOMIC_RELAXED,
                                                   __HIP_MEMORY_SCOPE_AGENT);
         *s_u = v;
       }
@@ -778,9 +784,9 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     nr = min(shared ? a.shared_rows : UNIT_STREAM_ROWS, a.offsets[s + 1] - (int)begin);
     multi = a.offsets[s + 1] - a.offsets[s] > a.shared_rows;
     keys = a.keys + (int64_t)s * a.nkeys * a.row_bytes;
-    if (u >= first_half) {
-      half = (u - first_half) & 1;
-      pair = (u - first_half) >> 1;
+    if (u >= first_part) {
+      part = (u - first_part) % SPLIT_PARTS;
+      cut = (u - first_part) / SPLIT_PARTS;
     }
   } else {
     const int R = a.route_rows;
@@ -797,7 +803,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreParams a) {
     keys = a.keys + (int64_t)key0 * a.row_bytes;
   }
   if (shared) shared_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, multi);
-  else if constexpr (LOOKUP && KS <= 16) stream_unit_lds<DT, KS, MASKED, KL, COS>(a, smem, begin, nr, keys, half, pair);
+  else if constexpr (LOOKUP && KS <= 16) stream_unit_lds<DT, KS, MASKED, KL, COS>(a, smem, begin, nr, keys, part, cut);
   else stream_unit<DT, KS, MASKED, LOOKUP, KL, COS>(a, smem, begin, nr, keys, key0, nk, split);
 }
 
@@ -949,7 +955,7 @@ hipError_t launch_route(int dt, const void* q, const void* scene_keys, const flo
 }
 
 // The Level-2 launch and, when the bucketing may cut the last round, the
-// merge of the halves right after it on the same stream (its threads return
+// merge of the parts right after it on the same stream (its threads return
 // at once where nothing was cut).  With stamps, the pair of events brackets
 // both launches.
 template <int KL>
@@ -959,8 +965,10 @@ static hipError_t launch_lookup_kl(int dt, int grid, const ScoreParams& p, bool 
   const hipEvent_t first[2] = {stamp != nullptr ? stamp[0] : nullptr, nullptr};
   const hipError_t e = launch_dt<true, KL>(dt, p.ks, grid, p, st, stamp != nullptr ? first : nullptr);
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL((split_merge_kernel<KL>), dim3(SPLIT_UNITS / 16), dim3(256), 0, st,
-                        nullptr, stamp != nullptr ? stamp[1] : nullptr, 0, p);
+  // 2 KL lanes a row slot, four waves a workgroup
+  const unsigned blocks = (unsigned)(SPLIT_UNITS * UNIT_STREAM_ROWS * 2 * KL / (4 * WAVE));
+  hipExtLaunchKernelGGL((split_merge_kernel<KL>), dim3(blocks), dim3(256), 0, st, nullptr,
+                        stamp != nullptr ? stamp[1] : nullptr, 0, p);
   return hipGetLastError();
 }
 

@@ -102,12 +102,12 @@ def test_small_workloads_every_token(name):
         assert np.mean(got == lab) > 0.99
 
 
-# Batches whose last round of Level-2 units is cut in halves (more than two
+# Batches whose last round of Level-2 units is cut in two parts (more than two
 # rounds of single-bucket streaming units, P >= 512): masked bf16 keys with
 # k = 16, fp32 with k = 32 (the widest partial list) and a ragged last key
 # block (P = 520) over two layers, the cosine scores, and Zipf buckets (shared
-# units in groups with streaming ones ahead of the halves); and one batch the
-# host allows to cut but whose buckets are too few (no halves, the merge
+# units in groups with streaming ones ahead of the parts); and one batch the
+# host allows to cut but whose buckets are too few (no parts, the merge
 # launch finds nothing).
 CUT = {
     "bf16_cut_k16": (Workload("bf16_cut_k16", "bf16", 2048, 1, 64, 64, 2048, 512, 16, 16, 16,
@@ -125,16 +125,16 @@ CUT = {
 
 @pytest.mark.parametrize("name", list(CUT))
 def test_cut_last_round_every_token(name):
-    """The Level-2 launch whose last 512 streaming units run as two halves
+    """The Level-2 launch whose last 512 streaming units run as two parts
     each (partial top-k lists merged after the launch) against the oracle on
-    every token; the work list's counters show the halves were made and
+    every token; the work list's counters show the parts were made and
     taken."""
     wl, score, cut = CUT[name]
     _announce(f"{name}: {wl} score={score}")
     r, _ = _run_check(make_inputs(wl, seed=5, device=DEV), score=score)
     torch.cuda.synchronize()
-    entries, first_half, taken = r.table.ws[:12].view(torch.int32).cpu().tolist()
-    assert entries - first_half == (2 * 512 if cut else 0), (entries, first_half)
+    entries, first_part, taken = r.table.ws[:12].view(torch.int32).cpu().tolist()
+    assert entries - first_part == (2 * 512 if cut else 0), (entries, first_part)
     assert taken >= (2 * 512 if cut else 0)
     # the merge's row names (after the routing counters at the start of the
     # workspace) are back at zero, and a second lookup gives the same bits
