@@ -120,6 +120,9 @@ CUT = {
                                20, usage="zipf"), "dot", True),
     "bf16_cut_declined": (Workload("bf16_cut_declined", "bf16", 1100, 1, 64, 64, 100, 512, 16,
                                    16, 8, 20, usage="uniform"), "dot", False),
+    # the narrowest lists (k = 2, eight merge lanes a row) on 512-byte keys
+    "f32_cut_k2_ks8": (Workload("f32_cut_k2_ks8", "f32", 2600, 1, 64, 128, 1300, 512, 16, 16, 2,
+                                20, usage="uniform"), "dot", True),
 }
 
 
