@@ -34,7 +34,12 @@
 
 namespace lookme {
 
-using TgShape = DtlShape<2, 2, 2, 2, 128>;
+// BIG: 128 x 128 output tiles (each wave 4 x 4 MFMA tiles), for products with
+// enough rows to fill the chip with them (the relevance MLP's first layer of
+// large batches): a quarter of the tiles, half the operand bytes into LDS.
+template <bool BIG>
+using TgShapeT = DtlShape<2, 2, BIG ? 4 : 2, BIG ? 4 : 2, 128>;
+using TgShape = TgShapeT<false>;
 constexpr int TG_KB = 128;
 
 enum : int {
@@ -71,30 +76,34 @@ struct TileGemmParams {
 // when col_major (so they land on one XCD and share its L2 copy of the B
 // rows, which the larger operand then crosses HBM once), else the column
 // tiles of one row block.
+template <bool BIG = false>
 __device__ __forceinline__ void tile_origin(const TileGemmParams& a, int tile, int tcols,
                                             int64_t* m0, int* n0) {
+  constexpr int BM = TgShapeT<BIG>::BM;
   if (a.col_major) {
-    const int tiles_m = (int)((a.rows + TgShape::BM - 1) / TgShape::BM);
-    *m0 = (int64_t)(tile % tiles_m) * TgShape::BM;
+    const int tiles_m = (int)((a.rows + BM - 1) / BM);
+    *m0 = (int64_t)(tile % tiles_m) * BM;
     *n0 = (tile / tiles_m) * tcols;
   } else {
     const int tiles_n = (a.cols + tcols - 1) / tcols;
-    *m0 = (int64_t)(tile / tiles_n) * TgShape::BM;
+    *m0 = (int64_t)(tile / tiles_n) * BM;
     *n0 = (tile % tiles_n) * tcols;
   }
 }
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
 
-// Epilogue of a 64 x 64 tile (tile index `tile` of batch z) from the
-// accumulators of thread tid: the lane holds rows m0 + wm + 16 i + 4 g + r and
-// tile columns wn + 16 j + n16.  xch: 4096 floats of LDS (EPI_SWIGLU only).
-template <int DT, int EPI>
-__device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (&acc)[2][2],
+// Epilogue of a tile (tile index `tile` of batch z) from the accumulators of
+// thread tid: the lane holds rows m0 + wm + 16 i + 4 g + r and tile columns
+// wn + 16 j + n16.  xch: 4096 floats of LDS (EPI_SWIGLU only, small tiles).
+template <int DT, int EPI, bool BIG = false>
+__device__ __forceinline__ void tile_epilogue(const TileGemmParams& a,
+                                              f32x4_t (&acc)[BIG ? 4 : 2][BIG ? 4 : 2],
                                               int64_t z, int tile, int tid, float* xch,
                                               int64_t rows) {
-  using S = TgShape;
-  constexpr int MI = 2, NJ = 2, WN = 2;
+  using S = TgShapeT<BIG>;
+  constexpr int MI = BIG ? 4 : 2, NJ = BIG ? 4 : 2, WN = 2;
+  static_assert(!BIG || EPI != EPI_SWIGLU, "the SwiGLU exchange is laid out for small tiles");
   constexpr int ES = DT == DT_BF16 ? 2 : 4;
   constexpr int TCOLS = EPI == EPI_SWIGLU ? S::BN / 2 : S::BN;
   const int lane = tid & 63, wv = tid >> 6;
@@ -102,7 +111,50 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
   const int wm = (wv / WN) * 16 * MI, wn = (wv % WN) * 16 * NJ;
   int64_t m0;
   int n0;
-  tile_origin(a, tile, TCOLS, &m0, &n0);
+  tile_origin<BIG>(a, tile, TCOLS, &m0, &n0);
+  if constexpr (BIG && EPI == EPI_ACT_TAB) {
+    // 32-bit row and table indices (rows of a product and scenes stay far
+    // below 2^31) keep the big tile's epilogue within the registers of two
+    // waves a SIMD; every table load still precedes the first store
+    int orow[MI][4], trow[MI][4];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = m0 + wm + 16 * i + 4 * g + r;
+        orow[i][r] = (int)(row < rows ? row : rows - 1);
+        const int sc = a.sel[orow[i][r]];
+        trow[i][r] = sc < 0 ? 0 : (sc >= a.sel_rows ? a.sel_rows - 1 : sc);
+      }
+    int col[NJ];
+    float old[NJ][MI][4];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      col[j] = n0 + wn + 16 * j + n16;
+      const int cc = col[j] < a.cols ? col[j] : a.cols - 1;
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) old[j][i][r] = a.tab[(int64_t)trow[i][r] * a.cols + cc];
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      if (col[j] >= a.cols) continue;
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (m0 + wm + 16 * i + 4 * g + r >= rows) continue;
+          const float v = fmaxf(acc[i][j][r] + old[j][i][r], 0.f);
+          char* dst = a.out + ((int64_t)orow[i][r] * a.cols + col[j]) * ES;
+          if constexpr (DT == DT_BF16)
+            *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16_rne(v);
+          else
+            *reinterpret_cast<float*>(dst) = v;
+        }
+    }
+    return;
+  }
   if constexpr (EPI == EPI_SWIGLU) {
     // the up half (waves with wn = 32) passes its tile through LDS to the
     // gate half (wn = 0) of the same rows
@@ -231,10 +283,10 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a, f32x4_t (
   }
 }
 
-template <int DT, int EPI, int NS>
-__global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
-  using S = TgShape;
-  constexpr int MI = 2, NJ = 2, KB = TG_KB, KSL = KB / 64, WN = 2;
+template <int DT, int EPI, int NS, bool BIG = false>
+__global__ __launch_bounds__(256, BIG ? 2 : 1) void tile_gemm_kernel(TileGemmParams a) {
+  using S = TgShapeT<BIG>;
+  constexpr int MI = BIG ? 4 : 2, NJ = BIG ? 4 : 2, KB = TG_KB, KSL = KB / 64, WN = 2;
   constexpr int TCOLS = EPI == EPI_SWIGLU ? S::BN / 2 : S::BN;   // output columns a tile
   static_assert(NS >= 2, "a stage in flight while one is multiplied");
   __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
@@ -249,7 +301,7 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
   if (tile < 0) return;
   int64_t m0;
   int n0;
-  tile_origin(a, tile, TCOLS, &m0, &n0);
+  tile_origin<BIG>(a, tile, TCOLS, &m0, &n0);
   int64_t rows = a.rows;   // live rows of this batch
   if (a.count != nullptr) {
     const int64_t c = a.count[z * a.count_step];
@@ -355,7 +407,7 @@ __global__ __launch_bounds__(256) void tile_gemm_kernel(TileGemmParams a) {
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no load into LDS outlives the wave
 
-  tile_epilogue<DT, EPI>(a, acc, z, tile, tid, reinterpret_cast<float*>(&lds[0][0]), rows);
+  tile_epilogue<DT, EPI, BIG>(a, acc, z, tile, tid, reinterpret_cast<float*>(&lds[0][0]), rows);
 }
 
 // Launches the product over `batches` batches (blockIdx.y), tiles in the
@@ -367,6 +419,24 @@ template <int EPI>
 hipError_t launch_tile_gemm(int dt, TileGemmParams p, int batches, hipStream_t st) {
   // column-major tile order when B has at least as many rows as A
   p.col_major = (int64_t)p.cols * (EPI == EPI_SWIGLU ? 2 : 1) >= p.rows;
+  if constexpr (EPI == EPI_ACT_TAB) {
+    // 128 x 128 tiles once they alone fill two whole rounds of the CUs at
+    // two a CU (relevance first layer, Zipf batch: 1024 tiles, 51.0 -> 44.5
+    // us; the multi-scale batch's 720 took 37.4 against 35.4 us on 64 x 64)
+    constexpr int BB = TgShapeT<true>::BM;
+    const int64_t big = ((p.rows + BB - 1) / BB) * ((p.cols + BB - 1) / BB);
+    if (big * batches >= 1024) {
+      p.tiles = (int)big;
+      const unsigned gx = (unsigned)((p.tiles + 7) / 8 * 8);
+      const dim3 grid(gx, (unsigned)batches);
+      // two 32 KiB stages: two workgroups a CU
+      if (dt == DT_BF16)
+        hipLaunchKernelGGL((tile_gemm_kernel<DT_BF16, EPI, 2, true>), grid, dim3(256), 0, st, p);
+      else
+        hipLaunchKernelGGL((tile_gemm_kernel<DT_F32, EPI, 2, true>), grid, dim3(256), 0, st, p);
+      return hipGetLastError();
+    }
+  }
   const unsigned gx = (unsigned)((p.tiles + 7) / 8 * 8);
   const dim3 grid(gx, (unsigned)batches);
   const int64_t wgs = (int64_t)gx * batches;
