@@ -113,6 +113,61 @@ __device__ __forceinline__ void tile_epilogue(const TileGemmParams& a,
   int n0;
   tile_origin<BIG>(a, tile, TCOLS, &m0, &n0);
   if constexpr (BIG && EPI == EPI_ACT_TAB) {
+    if (a.cols % 8 == 0 &&
+        ((reinterpret_cast<uintptr_t>(a.out) | reinterpret_cast<uintptr_t>(a.tab)) & 15) == 0) {
+      // through LDS, 64 rows at a time (xch: the stage ring, free once every
+      // wave is past its last loads): the waves of those rows write their
+      // sums, then every thread takes 8-column pieces of a row, whose table
+      // part and output are 16-byte loads and stores (the lane layout of the
+      // accumulators gave 2-byte stores and 4-byte table loads, ~25 us of
+      // the Zipf batch's ~57)
+      constexpr int LD = S::BN + 4;   // padded row: the four row groups of a write on distinct banks
+#pragma unroll 1
+      for (int half = 0; half < 2; ++half) {
+        __syncthreads();
+        if (wv / WN == half) {
+#pragma unroll
+          for (int i = 0; i < MI; ++i)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                xch[(16 * i + 4 * g + r) * LD + wn + 16 * j + n16] = acc[i][j][r];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < 64 * S::BN / 8 / 256; ++c) {
+          const int id = tid + 256 * c;
+          const int lr = id / (S::BN / 8), cc = (id % (S::BN / 8)) * 8;
+          const int64_t row = m0 + 64 * half + lr;
+          const int col = n0 + cc;
+          if (row >= rows || col >= a.cols) continue;
+          int sc = a.sel[row];
+          sc = sc < 0 ? 0 : (sc >= a.sel_rows ? a.sel_rows - 1 : sc);
+          const f32x4_t* tp = reinterpret_cast<const f32x4_t*>(a.tab + (int64_t)sc * a.cols + col);
+          const f32x4_t t0 = tp[0], t1 = tp[1];
+          const f32x4_t* xp = reinterpret_cast<const f32x4_t*>(xch + lr * LD + cc);
+          const f32x4_t x0 = xp[0], x1 = xp[1];
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = fmaxf(x0[e] + t0[e], 0.f);
+            v[4 + e] = fmaxf(x1[e] + t1[e], 0.f);
+          }
+          char* dst = a.out + (row * a.cols + col) * ES;
+          if constexpr (DT == DT_BF16) {
+            u32x4_t o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+            *reinterpret_cast<u32x4_t*>(dst) = o;
+          } else {
+            *reinterpret_cast<f32x4_t*>(dst) = f32x4_t{v[0], v[1], v[2], v[3]};
+            *reinterpret_cast<f32x4_t*>(dst + 16) = f32x4_t{v[4], v[5], v[6], v[7]};
+          }
+        }
+      }
+      return;
+    }
     // 32-bit row and table indices (rows of a product and scenes stay far
     // below 2^31) keep the big tile's epilogue within the registers of two
     // waves a SIMD; every table load still precedes the first store
@@ -289,6 +344,7 @@ __global__ __launch_bounds__(256, BIG ? 2 : 1) void tile_gemm_kernel(TileGemmPar
   constexpr int MI = BIG ? 4 : 2, NJ = BIG ? 4 : 2, KB = TG_KB, KSL = KB / 64, WN = 2;
   constexpr int TCOLS = EPI == EPI_SWIGLU ? S::BN / 2 : S::BN;   // output columns a tile
   static_assert(NS >= 2, "a stage in flight while one is multiplied");
+  static_assert(!BIG || NS * S::STAGE >= 64 * (S::BN + 4) * 4, "room for the epilogue's 64 rows");
   __shared__ __attribute__((aligned(1024))) char lds[NS][S::STAGE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;

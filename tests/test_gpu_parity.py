@@ -437,6 +437,10 @@ RELEVANCE = {
     "f32_rel_fused_h256": (Workload("f32_rel_fused_h256", "f32", 200, 1, 96, 64, 6, 1000, 40, 40,
                                     8, 40, usage="uniform"), 256, None),
     "bf16_rel_zipf": (WORKLOADS[4], 512, 40),
+    # 1032 tiles of 128 x 128 in the first layer, a ragged last row block and
+    # K of two 64-byte stages (fewer than the ring holds)
+    "bf16_rel_big_ragged": (Workload("bf16_rel_big_ragged", "bf16", 33001, 1, 128, 64, 9, 300,
+                                     32, 32, 8, 30, usage="uniform"), 512, 48),
     # batches of >= 4096 rows take the 32 x 32 form: 512-byte hidden rows with
     # ragged P (300: the last 32-key block's second image wholly past P; two
     # ranges) and a ragged last unit (4200 rows), 1024-byte rows with P 1000
@@ -483,7 +487,10 @@ def test_relevance_lookup(name):
     r = RelevanceRun(inp, mlp).run()
     toks = None
     if sample:
-        toks = np.random.default_rng(5).choice(wl.n_tokens, sample, replace=False)
+        # random rows plus the first and the last ones (the ragged edge)
+        toks = np.unique(np.concatenate([
+            np.random.default_rng(5).choice(wl.n_tokens, sample, replace=False),
+            [0, wl.n_tokens - 2, wl.n_tokens - 1]]))
     rep = check_relevance_run(r, tokens=toks)
     assert rep.ok, str(rep)
     assert min(rep.decisions.get(kind, 0) for kind in ("act", "prim", "w", "hidden_row")) > 0
