@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--reps", type=int, default=5,
                     help="K-step blocks timed in all (the first gives value; all give the "
                          "median and spread)")
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", type=int, default=4,
                     help="index into synth.WORKLOADS (default: the 32 GiB Zipf table, the "
                          "largest single-GPU workload)")
