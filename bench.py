@@ -766,7 +766,7 @@ def cpu_baseline(b: "Bench", m: int, min_seconds: float = 10.0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
     from synth import WORKLOADS
     wl = WORKLOADS[args.workload]

@@ -47,7 +47,7 @@ typedef struct lookme_s* lookme_t;           /* opaque; borrows the table */
 typedef enum {
   LOOKME_OK = 0,
   LOOKME_ERR_INVALID = 1,       /* bad argument (null, size, alignment, range) */
-  LOOKME_ERR_UNSUPPORTED = 2,   /* valid but outside what this build implements */
+  LOOKME_ERR_UNSUPPORTED = 2,   /* valid but outside what the library implements */
   LOOKME_ERR_WORKSPACE = 3,     /* no workspace set, or too small for the call */
   LOOKME_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed */
 } lookme_status_t;
